@@ -1,0 +1,215 @@
+"""Benchmark: RBF-ARD psi-statistics + gradients on one MI355X.
+
+One step = gpps_psi_stats (psi0, Psi1, Psi2) + gpps_psi_grads (dmu, dS, dZ,
+dsigma_f2, dl) over the whole workload, inputs resident in HBM.  The timed
+workload is ``large`` (N=100,000, M=256, Q=20, fp32, synthetic, seed 0).
+
+Metric: N*M^2*Q terms per second (whole step).  Beside it:
+  roofline      the dominant kernel's algorithmic FLOP rate (HIP events around
+                each launch, on the library's stream, during the timed steps)
+                against the FP32 peak of 157.3 TFLOP/s;
+  pct_fp32_peak the Psi2 forward + gradient kernels together:
+                F_alg = 8 Q N M(M+1)/2 flops over their summed time;
+  cpu_baseline  the fp64 CPU oracle on a bounded row sample of the same
+                workload, on this host's cores (a reported baseline only).
+
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload large]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_FP32 = 157.3e12          # MI355X FP32 (vector and matrix) peak, FLOP/s
+PEAK_HBM = 8.0e12             # B/s
+METRIC = "N·M²·Q psi-stat+grad terms/sec (fp32) and % of FP32 VALU peak, 1 MI355X"
+
+
+def algorithmic(kernel: str, N: int, M: int, Q: int):
+    """(bound, flops or bytes per launch, unit) of each kernel's algorithmic work.
+
+    Per unique pair (m <= m') and datapoint, the Psi2 forward needs one FMA per
+    latent dimension (the Gram term) and the Psi2 gradient three (Gram
+    recompute plus W*d on both sides of the pair): 2 and 6 flops per
+    (n, pair, q).  Psi1 kernels are counted by their compulsory HBM bytes."""
+    P = M * (M + 1) // 2
+    fwd, grad = 2.0 * Q * N * P, 6.0 * Q * N * P
+    table = {
+        "generic_psi2_partial": ("alu", fwd, "flop"),
+        "generic_grad_rows": ("alu", 4.0 * Q * N * P, "flop"),
+        "generic_grad_cols": ("alu", 2.0 * Q * N * P, "flop"),
+        "mfma_psi2_fwd": ("mfma", fwd, "flop"),
+        "mfma_psi2_grad": ("mfma", grad, "flop"),
+        "generic_psi1": ("hbm", 4.0 * (N * M + 2 * N * Q), "byte"),
+        "mfma_psi1_fwd": ("hbm", 4.0 * (N * M + 2 * N * Q), "byte"),
+        "mfma_psi1_grad": ("hbm", 4.0 * (N * M + 4 * N * Q), "byte"),
+    }
+    return table.get(kernel)
+
+
+def traffic_for(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current source of the kernel; else None."""
+    f = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(f):
+        return None
+    rec = json.load(open(f))
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+        return None
+    return rec["bytes_per_launch"]
+
+
+def cpu_baseline(inp, target_s: float):
+    """Time the fp64 oracle (forward + gradients) on a row sample of the workload."""
+    import numpy as np
+
+    import oracle
+
+    oracle.build(force=False)
+    N, Q = inp["mu"].shape
+    M = inp["Z"].shape[0]
+
+    def run(rows):
+        sub = {k: inp[k][rows] for k in ("mu", "S", "dL_dPsi1")}
+        t0 = time.perf_counter()
+        oracle.psi_stats(sub["mu"], sub["S"], inp["Z"], inp["sigma_f2"], inp["l"])
+        oracle.psi_grads(sub["mu"], sub["S"], inp["Z"], inp["sigma_f2"], inp["l"],
+                         inp["dL_dpsi0"], sub["dL_dPsi1"], inp["dL_dPsi2"])
+        return time.perf_counter() - t0
+
+    threads = oracle.num_threads()
+    probe = max(threads, 16)
+    t = run(np.arange(probe) * (N // probe))
+    n = int(min(N, max(probe, probe * target_s / max(t, 1e-6))))
+    rows = np.linspace(0, N - 1, n).astype(np.int64)
+    t = run(rows)
+    return {"value": n * M * M * Q / t, "unit": "terms/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} of {N} rows (evenly spaced) of the same workload, fp64 oracle, "
+                      f"forward + gradients, {t:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="large")
+    ap.add_argument("--path", default="auto", choices=["auto", "generic", "mfma"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the multi-GPU path (row sharding with an "
+              "all-reduce of Psi2 and the global gradients) is a design, not built here.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_1410_4984_amd as gpps
+    from paper_1410_4984_amd import synth
+
+    w = synth.WORKLOADS[args.workload]
+    if w.chunk_rows:
+        raise SystemExit("bench.py times single-call workloads (tiny/small/medium/large)")
+    N, M, Q = w.N, w.M, w.Q
+    inp = synth.to_f32(synth.make_workload(args.workload))
+    dev = "cuda:0"
+    t = {k: torch.tensor(v, dtype=torch.float32, device=dev) for k, v in inp.items()
+         if isinstance(v, np.ndarray)}
+    gpps.set_path(args.path)
+    psi0 = torch.zeros(1, device=dev)
+    P1 = torch.empty((N, M), device=dev)
+    P2 = torch.empty((M, M), device=dev)
+    g = {"dmu": torch.empty((N, Q), device=dev), "dS": torch.empty((N, Q), device=dev),
+         "dZ": torch.empty((M, Q), device=dev), "dsigma_f2": torch.empty(1, device=dev),
+         "dl": torch.empty(Q, device=dev)}
+    ws = torch.empty(gpps.workspace_bytes("f32", N, M, Q), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gpps.psi_stats(t["mu"], t["S"], t["Z"], inp["sigma_f2"], inp["l"], out=(psi0, P1, P2),
+                       workspace=ws, stream=stream)
+        gpps.psi_grads(t["mu"], t["S"], t["Z"], inp["sigma_f2"], inp["l"], inp["dL_dpsi0"],
+                       t["dL_dPsi1"], t["dL_dPsi2"], out=g, workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    L = gpps.lib()
+    L.gpps_timing_enable.argtypes = [ctypes.c_int]
+    L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    L.gpps_timing_enable(1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    L.gpps_timing_enable(0)
+    cap = 64
+    names = (ctypes.c_char_p * cap)()
+    tot = (ctypes.c_double * cap)()
+    cnt = (ctypes.c_int64 * cap)()
+    n = L.gpps_timing_collect(cap, names, tot, cnt)
+    if n < 0:
+        raise RuntimeError("kernel timing failed")
+    kernels = {names[i].decode(): {"avg_ms": tot[i] / cnt[i], "launches": int(cnt[i])}
+               for i in range(n)}
+    ms = (t1 - t0) * 1e3 / args.steps
+    terms = float(N) * M * M * Q
+
+    # dominant kernel and its roofline
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+    alg = algorithmic(dom, N, M, Q)
+    roofline = None
+    if alg:
+        bound, work, unit = alg
+        avg_s = kernels[dom]["avg_ms"] * 1e-3
+        if unit == "flop":
+            ach, peak, u = work / avg_s / 1e12, PEAK_FP32 / 1e12, "TFLOP/s"
+        else:
+            ach, peak, u = work / avg_s / 1e9, PEAK_HBM / 1e9, "GB/s"
+        roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak,
+                    "unit": u, "frac": round(ach / peak, 4),
+                    "traffic": traffic_for(dom, args.workload),
+                    "algorithmic_per_launch": work}
+    psi2_kernels = [k for k in kernels if any(s in k for s in ("psi2_partial", "psi2_fwd",
+                                                                "psi2_grad", "grad_rows",
+                                                                "grad_cols"))]
+    t_psi2 = sum(kernels[k]["avg_ms"] for k in psi2_kernels) * 1e-3
+    F_alg = 8.0 * Q * N * (M * (M + 1) // 2)
+    rec = {
+        "metric": METRIC, "value": terms / (ms * 1e-3), "unit": "terms/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload} (N={N}, M={M}, Q={Q}, seed 0)",
+                   "N": N, "M": M, "Q": Q, "path": gpps.get_path() if args.path != "auto"
+                   else "auto"},
+        "pct_fp32_peak": round(100.0 * F_alg / t_psi2 / PEAK_FP32, 2) if t_psi2 > 0 else None,
+        "roofline": roofline,
+        "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}
+                    for k, v in sorted(kernels.items())},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,151 @@
+/*
+ * gpps — RBF-ARD psi-statistics and their gradients on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of the HIP library libgpps.so.  Plain pointers and sizes only.
+ *
+ * Notation (Dai, Damianou, Hensman, Lawrence, "Gaussian Process Models with
+ * Parallelization and GPU acceleration", section 2 and Alg. 1-2):
+ *   N datapoints, M inducing inputs, Q latent dimensions.
+ *   q(x_n) = N(mu_n, diag S_n)          variational posterior, factorised over n
+ *   Z        inducing inputs (M x Q)
+ *   k(x, z)  = sigma_f2 * exp(-1/2 sum_q (x_q - z_q)^2 / l_q^2)      ARD RBF kernel
+ *   psi0     = sum_n E_q[k(x_n, x_n)]                     (scalar; the paper's phi)
+ *   Psi1     = E_q[k(x_n, z_m)]              N x M         (the per-point Psi_nm of Alg. 1)
+ *   Psi2     = sum_n E_q[k(x_n, z_m) k(x_n, z_m')]  M x M  (the paper's Phi, eq. (2)-(4))
+ *
+ * Conventions shared by every entry point:
+ *   - dt selects the element type of EVERY device array of the call
+ *     (GPPS_F32: float, GPPS_F64: double).  Arrays are dense, row-major,
+ *     contiguous, aligned to their element size, and live in device memory
+ *     of the current HIP device.
+ *   - mu and S are N x Q (S holds the diagonal VARIANCES), Z is M x Q.
+ *   - sigma_f2 and l (Q values) are HOST doubles, so validation needs no
+ *     device synchronisation.  In the F32 path they are rounded to float.
+ *   - The caller owns every buffer.  The library allocates nothing, frees
+ *     nothing and keeps no pointer after return.  Scratch memory is the
+ *     caller's workspace of at least gpps_workspace_bytes(dt, N, M, Q) bytes,
+ *     256-byte aligned; its contents on entry are ignored.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream) and
+ *     the call returns without synchronising: outputs are valid once the
+ *     stream has been synchronised.  The workspace must not be reused by
+ *     another call that may run concurrently.
+ *   - accumulate = 0 overwrites the N-summed outputs; accumulate = 1 adds to
+ *     them.  This is how N is split into row chunks (section 2: every
+ *     data-dependent quantity is a sum over datapoints, so partial results
+ *     over disjoint row sets add up).  Per-row outputs (Psi1, dmu, dS) are
+ *     always overwritten for the rows passed.
+ *   - Results are bitwise deterministic for fixed (dt, N, M, Q), path and
+ *     device: no floating-point atomics are used; every reduction runs in a
+ *     fixed order.
+ *   - Errors: every argument is validated before any HIP call; on a
+ *     validation error nothing is enqueued and nothing is written.  A failed
+ *     kernel launch returns GPPS_ERR_HIP; faults during asynchronous execution
+ *     surface at the caller's next synchronisation.  NaN or Inf inside device
+ *     arrays is not checked and propagates.
+ */
+#ifndef GPPS_H
+#define GPPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { GPPS_F32 = 0, GPPS_F64 = 1 } gpps_dtype;
+
+typedef enum {
+    GPPS_OK = 0,
+    GPPS_ERR_NULL = 1,      /* a required pointer is NULL                              */
+    GPPS_ERR_SHAPE = 2,     /* N < 1, M < 1, Q < 1, Q > GPPS_MAX_Q or M > GPPS_MAX_M   */
+    GPPS_ERR_HYPER = 3,     /* sigma_f2 or some l_q is not finite and > 0              */
+    GPPS_ERR_DTYPE = 4,     /* dt is not a gpps_dtype                                  */
+    GPPS_ERR_WORKSPACE = 5, /* workspace smaller than gpps_workspace_bytes()           */
+    GPPS_ERR_ALIGN = 6,     /* workspace not 256-byte aligned or an array misaligned   */
+    GPPS_ERR_HIP = 7,       /* a HIP runtime call or kernel launch failed              */
+    GPPS_ERR_PATH = 8       /* unknown path, or the requested path cannot run this call */
+} gpps_status;
+
+/* Kernel path used by gpps_psi_stats / gpps_psi_grads.  AUTO picks the fastest
+ * path that supports the call (the matrix-core path for F32 when M >= 2 and
+ * Q <= GPPS_MAX_Q_MFMA, the generic vector path otherwise). */
+typedef enum { GPPS_PATH_AUTO = 0, GPPS_PATH_GENERIC = 1, GPPS_PATH_MFMA = 2 } gpps_path;
+
+#define GPPS_MAX_Q 64
+#define GPPS_MAX_M 4096
+#define GPPS_MAX_Q_MFMA 62
+
+/* Bytes of workspace gpps_psi_stats and gpps_psi_grads need for this shape
+ * (the larger of the two, over every path).  0 for an invalid shape or dtype. */
+size_t gpps_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q);
+
+/*
+ * Forward statistics — section 2, eq. (4) (phi, Phi, Psi as expectations under
+ * q(X)); Alg. 1 (Psi_nm per datapoint and inducing input, Phi summed over
+ * datapoints for every pair of inducing inputs).
+ *
+ *   psi0  [1]      device.  += or = N * sigma_f2
+ *   Psi1  [N x M]  device, may be NULL (not computed).  Always overwritten.
+ *   Psi2  [M x M]  device.  Full symmetric matrix; both triangles are bitwise
+ *                  equal.  += or = according to `accumulate`.
+ */
+gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
+                           const void *mu, const void *S, const void *Z,
+                           double sigma_f2, const double *l,
+                           void *psi0, void *Psi1, void *Psi2,
+                           int accumulate, void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/*
+ * Gradients — Alg. 2: given dL/dPsi, the derivatives of
+ *   L = dL_dpsi0 * psi0 + sum_{n,m} dL_dPsi1[n,m] Psi1[n,m]
+ *                       + sum_{m,m'} dL_dPsi2[m,m'] Psi2[m,m']
+ * with respect to mu, S, Z, sigma_f2 and every l_q (the lengthscales
+ * themselves, not their logarithms; S as variances).
+ *
+ *   dL_dpsi0            host scalar.
+ *   dL_dPsi1 [N x M]    device, or NULL for zero.
+ *   dL_dPsi2 [M x M]    device, or NULL for zero.  Need not be symmetric: only its
+ *                       symmetric part affects L, since Psi2 is symmetric.
+ *   dmu, dS  [N x Q]    device, always overwritten.
+ *   dZ       [M x Q]    device, += or = according to `accumulate`.
+ *   dsigma_f2 [1]       device, += or =.
+ *   dl       [Q]        device, += or =.
+ */
+gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
+                           const void *mu, const void *S, const void *Z,
+                           double sigma_f2, const double *l, double dL_dpsi0,
+                           const void *dL_dPsi1, const void *dL_dPsi2,
+                           void *dmu, void *dS, void *dZ, void *dsigma_f2, void *dl,
+                           int accumulate, void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/* Select the kernel path for later calls in this process (default AUTO).
+ * Process-wide setting: do not change it while another thread is inside a
+ * gpps call.  Returns GPPS_ERR_PATH for an unknown value. */
+gpps_status gpps_set_path(gpps_path path);
+gpps_path gpps_get_path(void);
+
+/* Kernel timing for benchmarks.  While enabled (on != 0), every kernel launch
+ * of the library is bracketed by two HIP events recorded on the call's stream.
+ * gpps_timing_collect() waits for those events, writes up to max_entries
+ * (kernel name, summed milliseconds, launch count) triples into the caller's
+ * arrays (any may be NULL), releases the events and returns the number of
+ * distinct kernels, or -1 if an event call failed.  Names stay valid until the
+ * next collect.  Timing is process-wide and off by default. */
+gpps_status gpps_timing_enable(int on);
+int gpps_timing_collect(int max_entries, const char **names, double *total_ms,
+                        int64_t *launches);
+
+/* Static, NUL-terminated description of a status code. */
+const char *gpps_status_string(gpps_status status);
+
+/* Library version as major * 10000 + minor * 100 + patch. */
+int gpps_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GPPS_H */

@@ -1,1 +1,213 @@
-"""RBF-ARD psi-statistics and their gradients on MI355X (HIP, gfx950)."""
+"""RBF-ARD psi-statistics and their gradients on AMD Instinct MI355X (HIP, gfx950).
+
+Thin binding over the C ABI of ``libgpps.so`` (declared in ``include/gpps.h``):
+it checks torch tensors (device, dtype, contiguity, shape), allocates outputs
+and workspace with torch, and passes raw pointers plus the current HIP stream.
+Every step of the computation runs in the library's HIP kernels; there is no
+fallback of any kind: if the library is missing or cannot run, calls raise.
+
+    psi_stats(mu, S, Z, sigma_f2, l)   -> (psi0, Psi1, Psi2)
+    psi_grads(mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2)
+                                       -> dict(dmu, dS, dZ, dsigma_f2, dl)
+
+Notation follows the paper (section 2, Alg. 1-2): mu, S (variances) are N x Q,
+Z is M x Q, sigma_f2 the kernel variance, l the Q ARD lengthscales.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgpps.so")
+
+F32, F64 = 0, 1
+PATHS = {"auto": 0, "generic": 1, "mfma": 2}
+MAX_Q = 64
+MAX_M = 4096
+
+_lib = None
+
+
+class GppsError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"gpps status {status}: {msg}")
+        self.status = status
+
+
+def lib():
+    """The loaded ``libgpps.so`` (ctypes handle with argument types set)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_1410_4984_amd.build` "
+                           "(or __graft_entry__.build())")
+    import torch  # noqa: F401  -- load torch's HIP runtime first so the library shares it
+    L = ctypes.CDLL(LIB_PATH)
+    i64, vp, d, sz, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_double, ctypes.c_size_t, ctypes.c_int
+    L.gpps_workspace_bytes.argtypes = [i32, i64, i64, i64]
+    L.gpps_workspace_bytes.restype = sz
+    L.gpps_psi_stats.argtypes = [i32, i64, i64, i64, vp, vp, vp, d, vp, vp, vp, vp, i32, vp, sz, vp]
+    L.gpps_psi_stats.restype = i32
+    L.gpps_psi_grads.argtypes = [i32, i64, i64, i64, vp, vp, vp, d, vp, d, vp, vp, vp, vp, vp, vp,
+                                 vp, i32, vp, sz, vp]
+    L.gpps_psi_grads.restype = i32
+    L.gpps_set_path.argtypes = [i32]
+    L.gpps_set_path.restype = i32
+    L.gpps_get_path.restype = i32
+    L.gpps_status_string.argtypes = [i32]
+    L.gpps_status_string.restype = ctypes.c_char_p
+    L.gpps_version.restype = i32
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise GppsError(status, lib().gpps_status_string(status).decode())
+
+
+def status_string(status: int) -> str:
+    return lib().gpps_status_string(status).decode()
+
+
+def set_path(path: str) -> None:
+    """Select the kernel path for later calls: 'auto', 'generic' or 'mfma'."""
+    _check(lib().gpps_set_path(PATHS[path]))
+
+
+def get_path() -> str:
+    v = lib().gpps_get_path()
+    return {v_: k for k, v_ in PATHS.items()}[v]
+
+
+def workspace_bytes(dtype, N: int, M: int, Q: int) -> int:
+    return int(lib().gpps_workspace_bytes(_dt(dtype), N, M, Q))
+
+
+def _dt(dtype) -> int:
+    import torch
+    if dtype in (torch.float32, "f32", "float32", F32):
+        return F32
+    if dtype in (torch.float64, "f64", "float64", F64):
+        return F64
+    raise TypeError(f"unsupported dtype {dtype}")
+
+
+def _dev_tensor(x, name, dtype, shape, device):
+    import torch
+    if not isinstance(x, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if x.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {x.device})")
+    if x.device != device or x.dtype != dtype:
+        raise ValueError(f"{name}: expected {dtype} on {device}, got {x.dtype} on {x.device}")
+    if tuple(x.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(x.shape)}")
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return x
+
+
+def _host_l(l, Q):
+    import numpy as np
+    import torch
+    if isinstance(l, torch.Tensor):
+        l = l.detach().cpu().double().numpy()
+    arr = np.ascontiguousarray(np.asarray(l, dtype=np.float64).reshape(-1))
+    if arr.shape[0] != Q:
+        raise ValueError(f"l: expected {Q} lengthscales, got {arr.shape[0]}")
+    return arr
+
+
+def _workspace(dtype, N, M, Q, device, workspace):
+    import torch
+    need = workspace_bytes(dtype, N, M, Q)
+    if need == 0:
+        raise GppsError(2, status_string(2))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    elif workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace too small: need {need} bytes")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def psi_stats(mu, S, Z, sigma_f2, l, *, want_psi1=True, accumulate=False, out=None,
+              workspace=None, stream=None):
+    """Forward statistics (section 2, eq. (4); Alg. 1).
+
+    Returns (psi0 [1], Psi1 [N x M] or None, Psi2 [M x M]).  With
+    ``accumulate=True`` and ``out=(psi0, Psi1, Psi2)`` the N-summed outputs are
+    added to the given tensors (row chunking); Psi1 rows are always written.
+    """
+    import torch
+    dtype, device = mu.dtype, mu.device
+    N, Q = mu.shape
+    M = Z.shape[0]
+    _dev_tensor(mu, "mu", dtype, (N, Q), device)
+    _dev_tensor(S, "S", dtype, (N, Q), device)
+    _dev_tensor(Z, "Z", dtype, (M, Q), device)
+    lh = _host_l(l, Q)
+    if out is None:
+        psi0 = torch.zeros(1, dtype=dtype, device=device)
+        Psi1 = torch.empty((N, M), dtype=dtype, device=device) if want_psi1 else None
+        Psi2 = torch.empty((M, M), dtype=dtype, device=device)
+    else:
+        psi0, Psi1, Psi2 = out
+        _dev_tensor(psi0, "psi0", dtype, (1,), device)
+        if Psi1 is not None:
+            _dev_tensor(Psi1, "Psi1", dtype, (N, M), device)
+        _dev_tensor(Psi2, "Psi2", dtype, (M, M), device)
+    ws, ws_bytes = _workspace(dtype, N, M, Q, device, workspace)
+    _check(lib().gpps_psi_stats(
+        _dt(dtype), N, M, Q, mu.data_ptr(), S.data_ptr(), Z.data_ptr(), float(sigma_f2),
+        lh.ctypes.data, psi0.data_ptr(), None if Psi1 is None else Psi1.data_ptr(),
+        Psi2.data_ptr(), int(bool(accumulate)), ws.data_ptr(), ws_bytes, _stream(stream)))
+    return psi0, Psi1, Psi2
+
+
+def psi_grads(mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2, *, accumulate=False,
+              out=None, workspace=None, stream=None):
+    """Gradients of L = dL_dpsi0 psi0 + <dL_dPsi1, Psi1> + <dL_dPsi2, Psi2> (Alg. 2).
+
+    ``dL_dPsi1`` / ``dL_dPsi2`` may be None (zero).  Returns a dict with dmu, dS
+    (N x Q), dZ (M x Q), dsigma_f2 (1), dl (Q).  With ``accumulate=True`` and
+    ``out`` (a dict of the same tensors) dZ, dsigma_f2 and dl are added to.
+    """
+    import torch
+    dtype, device = mu.dtype, mu.device
+    N, Q = mu.shape
+    M = Z.shape[0]
+    _dev_tensor(mu, "mu", dtype, (N, Q), device)
+    _dev_tensor(S, "S", dtype, (N, Q), device)
+    _dev_tensor(Z, "Z", dtype, (M, Q), device)
+    if dL_dPsi1 is not None:
+        _dev_tensor(dL_dPsi1, "dL_dPsi1", dtype, (N, M), device)
+    if dL_dPsi2 is not None:
+        _dev_tensor(dL_dPsi2, "dL_dPsi2", dtype, (M, M), device)
+    lh = _host_l(l, Q)
+    if out is None:
+        out = {"dmu": torch.empty((N, Q), dtype=dtype, device=device),
+               "dS": torch.empty((N, Q), dtype=dtype, device=device),
+               "dZ": torch.zeros((M, Q), dtype=dtype, device=device),
+               "dsigma_f2": torch.zeros(1, dtype=dtype, device=device),
+               "dl": torch.zeros(Q, dtype=dtype, device=device)}
+    else:
+        for k, shp in (("dmu", (N, Q)), ("dS", (N, Q)), ("dZ", (M, Q)), ("dsigma_f2", (1,)),
+                       ("dl", (Q,))):
+            _dev_tensor(out[k], k, dtype, shp, device)
+    ws, ws_bytes = _workspace(dtype, N, M, Q, device, workspace)
+    ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+    _check(lib().gpps_psi_grads(
+        _dt(dtype), N, M, Q, mu.data_ptr(), S.data_ptr(), Z.data_ptr(), float(sigma_f2),
+        lh.ctypes.data, float(dL_dpsi0), ptr(dL_dPsi1), ptr(dL_dPsi2), out["dmu"].data_ptr(),
+        out["dS"].data_ptr(), out["dZ"].data_ptr(), out["dsigma_f2"].data_ptr(),
+        out["dl"].data_ptr(), int(bool(accumulate)), ws.data_ptr(), ws_bytes, _stream(stream)))
+    return out

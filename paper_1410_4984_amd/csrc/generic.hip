@@ -1,0 +1,554 @@
+// Generic vector-ALU path: RBF-ARD psi-statistics and gradients, templated on
+// the element type (float or double).
+//
+// What is computed (section 2, eq. (4): phi, Phi and Psi become expectations
+// under q(x_n) = N(mu_n, diag S_n); Alg. 1 and Alg. 2).  With
+//   w1 = 1 / (l^2 + S),  w2 = 1 / (l^2 + 2 S)                          per (n, q)
+//   lp1_n = log sf2   - 1/2 sum_q log(1 + S/l^2)
+//   lp2_n = 2 log sf2 - 1/2 sum_q log(1 + 2 S/l^2)
+// the exact Gaussian integrals give
+//   Psi1[n, m]    = exp(lp1_n - 1/2 sum_q (mu - z_m)^2 w1)
+//   Psi2_n[m, m'] = exp(lp2_n - sum_q [(z_m - z_m')^2 / (4 l^2) + (mu - zbar)^2 w2])
+// with zbar = (z_m + z_m') / 2, and Psi2 = sum_n Psi2_n.
+//
+// Work split: Psi1 one thread per output; Psi2 one thread per unique pair
+// (m <= m'), a workgroup per 16 x 16 pair tile and row chunk, partial sums per
+// chunk reduced in a fixed order.  Gradients: a row kernel (one thread per
+// datapoint) produces dmu, dS and per-block dl / dsf2 partials; a column kernel
+// (one thread per inducing input and row chunk) produces dZ partials; a final
+// kernel reduces the partials in a fixed order.  No atomics anywhere.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace gpps {
+namespace {
+
+constexpr int kRowTile = 32;     // rows staged in LDS at a time
+constexpr int kPairTile = 16;    // pair tile edge (16 x 16 threads)
+constexpr int kRowBlock = 64;    // threads (rows) per block in the gradient row kernel
+constexpr int kColBlock = 64;    // threads (inducing inputs) per block in the column kernel
+
+__device__ inline float dexp(float x) { return __expf(x); }
+__device__ inline double dexp(double x) { return exp(x); }
+__device__ inline float dlog1p(float x) { return log1pf(x); }
+__device__ inline double dlog1p(double x) { return log1p(x); }
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+struct Plan {
+    int64_t tiles_edge, tiles;       // pair tiles per edge and upper-triangle tile count
+    int64_t nc2;                     // row chunks of the Psi2 forward kernel
+    int64_t rows2;                   // rows per chunk (forward)
+    int64_t ncc, rowsc;              // column-kernel chunks and rows per chunk
+    int64_t col_blocks;              // column-kernel blocks per chunk
+    int64_t row_blocks;              // row-kernel blocks
+    // workspace offsets in bytes
+    size_t off_w1, off_w2, off_lp1, off_lp2, off_p2, off_g2s, off_colp, off_rowp, total;
+};
+
+Plan make_plan(const Shape &s, size_t elem) {
+    Plan p{};
+    p.tiles_edge = cdiv(s.M, kPairTile);
+    p.tiles = p.tiles_edge * (p.tiles_edge + 1) / 2;
+    int64_t nc2 = cdiv(s.N, 256);
+    int64_t cap2 = std::max<int64_t>(1, 2048 / p.tiles);
+    p.nc2 = std::max<int64_t>(1, std::min(nc2, cap2));
+    p.rows2 = cdiv(s.N, p.nc2);
+    p.nc2 = cdiv(s.N, p.rows2);
+    p.col_blocks = cdiv(s.M, kColBlock);
+    int64_t ncc = cdiv(s.N, 64);
+    int64_t capc = std::max<int64_t>(1, 2048 / p.col_blocks);
+    p.ncc = std::max<int64_t>(1, std::min(ncc, capc));
+    p.rowsc = cdiv(s.N, p.ncc);
+    p.ncc = cdiv(s.N, p.rowsc);
+    p.row_blocks = cdiv(s.N, kRowBlock);
+    size_t o = 0;
+    auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
+    p.off_w1 = take(elem * s.N * s.Q);
+    p.off_w2 = take(elem * s.N * s.Q);
+    p.off_lp1 = take(elem * s.N);
+    p.off_lp2 = take(elem * s.N);
+    p.off_p2 = take(elem * p.nc2 * s.P);
+    p.off_g2s = take(elem * s.M * s.M);
+    p.off_colp = take(elem * p.ncc * s.M * s.Q);
+    p.off_rowp = take(elem * p.row_blocks * (s.Q + 1));
+    p.total = o;
+    return p;
+}
+
+template <typename T>
+T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
+
+// ---------------------------------------------------------------- per-row tables
+template <typename T>
+__global__ void rows_pre_kernel(int64_t N, int Q, const T *__restrict__ S, Hyp<T> h,
+                                T *__restrict__ w1, T *__restrict__ w2, T *__restrict__ lp1,
+                                T *__restrict__ lp2) {
+    int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (n >= N) return;
+    T a = h.log_sf2, b = T(2) * h.log_sf2;
+    for (int q = 0; q < Q; ++q) {
+        T s = S[n * Q + q];
+        T l2 = h.l2[q];
+        w1[n * Q + q] = T(1) / (l2 + s);
+        w2[n * Q + q] = T(1) / (l2 + T(2) * s);
+        a -= T(0.5) * dlog1p(s / l2);
+        b -= T(0.5) * dlog1p(T(2) * s / l2);
+    }
+    lp1[n] = a;
+    lp2[n] = b;
+}
+
+// ---------------------------------------------------------------- Psi1 (Alg. 1, Psi)
+template <typename T>
+__global__ void psi1_kernel(int64_t N, int M, int Q, const T *__restrict__ mu,
+                            const T *__restrict__ Z, const T *__restrict__ w1,
+                            const T *__restrict__ lp1, T *__restrict__ Psi1) {
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N * M) return;
+    int64_t n = i / M;
+    int m = (int)(i - n * M);
+    T s = 0;
+    for (int q = 0; q < Q; ++q) {
+        T d = mu[n * Q + q] - Z[(int64_t)m * Q + q];
+        s += d * d * w1[n * Q + q];
+    }
+    Psi1[i] = dexp(lp1[n] - T(0.5) * s);
+}
+
+__device__ inline void tile_coords(int64_t t, int64_t edge, int &ti, int &tj) {
+    int64_t r = 0;
+    while (t >= edge - r) { t -= edge - r; ++r; }
+    ti = (int)r;
+    tj = (int)(r + t);
+}
+
+__device__ inline int64_t pair_index(int64_t m, int64_t mp, int64_t M) {
+    return m * M - m * (m - 1) / 2 + (mp - m);
+}
+
+// ---------------------------------------------------------------- Psi2 partials (Alg. 1, Phi)
+template <typename T, int QM>
+__global__ __launch_bounds__(256) void psi2_partial_kernel(
+    int64_t N, int M, int Q, int64_t P, int64_t rows_per_chunk, int64_t tiles_edge,
+    const T *__restrict__ mu, const T *__restrict__ Z, const T *__restrict__ w2,
+    const T *__restrict__ lp2, Hyp<T> h, T *__restrict__ partial) {
+    __shared__ T s_mu[kRowTile][QM];
+    __shared__ T s_w2[kRowTile][QM];
+    __shared__ T s_lp[kRowTile];
+    int ti, tj;
+    tile_coords(blockIdx.x, tiles_edge, ti, tj);
+    const int tx = threadIdx.x % kPairTile, ty = threadIdx.x / kPairTile;
+    const int m = ti * kPairTile + ty, mp = tj * kPairTile + tx;
+    const bool valid = m < M && mp < M && m <= mp;
+    T zbar[QM];
+    T C = 0;
+#pragma unroll
+    for (int q = 0; q < QM; ++q) {
+        zbar[q] = 0;
+        if (q < Q && valid) {
+            T a = Z[(int64_t)m * Q + q], b = Z[(int64_t)mp * Q + q];
+            zbar[q] = T(0.5) * (a + b);
+            C -= (a - b) * (a - b) / (T(4) * h.l2[q]);
+        }
+    }
+    const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
+    const int64_t r1 = min(N, r0 + rows_per_chunk);
+    T acc = 0;
+    for (int64_t base = r0; base < r1; base += kRowTile) {
+        const int cnt = (int)min<int64_t>(kRowTile, r1 - base);
+        __syncthreads();
+        for (int i = threadIdx.x; i < cnt * Q; i += blockDim.x) {
+            int r = i / Q, q = i - r * Q;
+            s_mu[r][q] = mu[(base + r) * Q + q];
+            s_w2[r][q] = w2[(base + r) * Q + q];
+        }
+        for (int r = threadIdx.x; r < cnt; r += blockDim.x) s_lp[r] = lp2[base + r];
+        __syncthreads();
+        if (valid) {
+            for (int r = 0; r < cnt; ++r) {
+                T e = s_lp[r] + C;
+#pragma unroll
+                for (int q = 0; q < QM; ++q) {
+                    if (q < Q) {
+                        T d = s_mu[r][q] - zbar[q];
+                        e -= d * d * s_w2[r][q];
+                    }
+                }
+                acc += dexp(e);
+            }
+        }
+    }
+    if (valid) partial[(int64_t)blockIdx.y * P + pair_index(m, mp, M)] = acc;
+}
+
+// Fixed-order sum of the chunk partials; writes both triangles and psi0.
+template <typename T>
+__global__ void psi2_reduce_kernel(int64_t N, int M, int64_t P, int64_t nchunks,
+                                   const T *__restrict__ partial, Hyp<T> h, T *__restrict__ psi0,
+                                   T *__restrict__ Psi2, int accumulate) {
+    const int mp = blockIdx.x * kPairTile + threadIdx.x % kPairTile;
+    const int m = blockIdx.y * kPairTile + threadIdx.x / kPairTile;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+        psi0[0] = (accumulate ? psi0[0] : T(0)) + T(N) * h.sf2;
+    if (m >= M || mp >= M || m > mp) return;
+    const int64_t p = pair_index(m, mp, M);
+    T s = 0;
+    for (int64_t c = 0; c < nchunks; ++c) s += partial[c * P + p];
+    T v = (accumulate ? Psi2[(int64_t)m * M + mp] : T(0)) + s;
+    Psi2[(int64_t)m * M + mp] = v;
+    Psi2[(int64_t)mp * M + m] = v;
+}
+
+// ---------------------------------------------------------------- gradients (Alg. 2)
+template <typename T>
+__global__ void sym_kernel(int M, const T *__restrict__ G2, T *__restrict__ G2s) {
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)M * M) return;
+    int m = (int)(i / M), mp = (int)(i - (int64_t)m * M);
+    G2s[i] = T(0.5) * (G2[(int64_t)m * M + mp] + G2[(int64_t)mp * M + m]);
+}
+
+// One thread per datapoint: dmu_n, dS_n; per-block partials of dl and dsf2.
+template <typename T, int QM>
+__global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
+    int64_t N, int M, int Q, const T *__restrict__ mu, const T *__restrict__ S,
+    const T *__restrict__ Z, const T *__restrict__ w1, const T *__restrict__ w2,
+    const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h, const T *__restrict__ G1,
+    const T *__restrict__ G2s, T *__restrict__ dmu, T *__restrict__ dS,
+    T *__restrict__ rowpart) {
+    __shared__ T s_g1[kRowBlock][kRowBlock + 1];
+    __shared__ T s_red[QM + 1][kRowBlock];
+    const int tid = threadIdx.x;
+    const int64_t n0 = (int64_t)blockIdx.x * kRowBlock;
+    const int64_t n = n0 + tid;
+    const bool valid = n < N;
+    T m_[QM], s_[QM], a1[QM], a2[QM];
+    T gmu[QM], gS[QM], gl[QM];
+    T l1 = 0, l2v = 0, gsf = 0;
+#pragma unroll
+    for (int q = 0; q < QM; ++q) {
+        m_[q] = s_[q] = a1[q] = a2[q] = gmu[q] = gS[q] = gl[q] = 0;
+        if (q < Q && valid) {
+            m_[q] = mu[n * Q + q];
+            s_[q] = S[n * Q + q];
+            a1[q] = w1[n * Q + q];
+            a2[q] = w2[n * Q + q];
+        }
+    }
+    if (valid) { l1 = lp1[n]; l2v = lp2[n]; }
+
+    if (G1) {
+        const int rows = (int)min<int64_t>(kRowBlock, N - n0);
+        for (int mt = 0; mt < M; mt += kRowBlock) {
+            const int cols = min(kRowBlock, M - mt);
+            __syncthreads();
+            for (int i = tid; i < rows * cols; i += kRowBlock) {
+                int r = i / cols, c = i - r * cols;
+                s_g1[r][c] = G1[(n0 + r) * M + mt + c];
+            }
+            __syncthreads();
+            if (valid) {
+                for (int c = 0; c < cols; ++c) {
+                    const int m = mt + c;
+                    T e = 0;
+#pragma unroll
+                    for (int q = 0; q < QM; ++q)
+                        if (q < Q) {
+                            T d = m_[q] - Z[(int64_t)m * Q + q];
+                            e += d * d * a1[q];
+                        }
+                    const T t = s_g1[tid][c] * dexp(l1 - T(0.5) * e);
+                    gsf += t;
+#pragma unroll
+                    for (int q = 0; q < QM; ++q)
+                        if (q < Q) {
+                            T d = m_[q] - Z[(int64_t)m * Q + q];
+                            T dd = d * a1[q];
+                            gmu[q] -= t * dd;
+                            gS[q] += t * T(0.5) * (dd * dd - a1[q]);
+                            gl[q] += t * (s_[q] * a1[q] / h.l[q] + h.l[q] * dd * dd);
+                        }
+                }
+            }
+        }
+    }
+
+    if (G2s && valid) {
+        for (int m = 0; m < M; ++m) {
+            for (int mp = m; mp < M; ++mp) {
+                const T g = (m == mp ? T(1) : T(2)) * G2s[(int64_t)m * M + mp];
+                T e = l2v;
+#pragma unroll
+                for (int q = 0; q < QM; ++q)
+                    if (q < Q) {
+                        T a = Z[(int64_t)m * Q + q], b = Z[(int64_t)mp * Q + q];
+                        T d = m_[q] - T(0.5) * (a + b);
+                        e -= (a - b) * (a - b) / (T(4) * h.l2[q]) + d * d * a2[q];
+                    }
+                const T t = g * dexp(e);
+                gsf += T(2) * t;
+#pragma unroll
+                for (int q = 0; q < QM; ++q)
+                    if (q < Q) {
+                        T a = Z[(int64_t)m * Q + q], b = Z[(int64_t)mp * Q + q];
+                        T d = m_[q] - T(0.5) * (a + b);
+                        T dd = d * a2[q];
+                        T del = a - b;
+                        gmu[q] -= T(2) * t * dd;
+                        gS[q] += t * (T(2) * dd * dd - a2[q]);
+                        gl[q] += t * (T(2) * s_[q] * a2[q] / h.l[q] +
+                                      del * del / (T(2) * h.l2[q] * h.l[q]) +
+                                      T(2) * h.l[q] * dd * dd);
+                    }
+            }
+        }
+    }
+
+    if (valid) {
+#pragma unroll
+        for (int q = 0; q < QM; ++q)
+            if (q < Q) {
+                dmu[n * Q + q] = gmu[q];
+                dS[n * Q + q] = gS[q];
+            }
+    }
+    // fixed-order block reduction of dl and dsf2 partials
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < QM; ++q) s_red[q][tid] = gl[q];
+    s_red[QM][tid] = gsf / h.sf2;
+    __syncthreads();
+    if (tid <= Q) {
+        const int row = tid < Q ? tid : QM;
+        T s = 0;
+        for (int i = 0; i < kRowBlock; ++i) s += s_red[row][i];
+        rowpart[(int64_t)blockIdx.x * (Q + 1) + tid] = s;
+    }
+}
+
+// One thread per inducing input m and row chunk: partial dZ[m, :].
+template <typename T, int QM>
+__global__ __launch_bounds__(kColBlock) void grad_cols_kernel(
+    int64_t N, int M, int Q, int64_t rows_per_chunk, const T *__restrict__ mu,
+    const T *__restrict__ Z, const T *__restrict__ w1, const T *__restrict__ w2,
+    const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h, const T *__restrict__ G1,
+    const T *__restrict__ G2s, T *__restrict__ colpart) {
+    __shared__ T s_mu[kRowTile][QM];
+    __shared__ T s_w1[kRowTile][QM];
+    __shared__ T s_w2[kRowTile][QM];
+    __shared__ T s_lp1[kRowTile], s_lp2[kRowTile];
+    const int m = blockIdx.x * kColBlock + threadIdx.x;
+    const bool valid = m < M;
+    T zm[QM], gz[QM];
+#pragma unroll
+    for (int q = 0; q < QM; ++q) {
+        gz[q] = 0;
+        zm[q] = (q < Q && valid) ? Z[(int64_t)m * Q + q] : T(0);
+    }
+    const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
+    const int64_t r1 = min(N, r0 + rows_per_chunk);
+    for (int64_t base = r0; base < r1; base += kRowTile) {
+        const int cnt = (int)min<int64_t>(kRowTile, r1 - base);
+        __syncthreads();
+        for (int i = threadIdx.x; i < cnt * Q; i += blockDim.x) {
+            int r = i / Q, q = i - r * Q;
+            s_mu[r][q] = mu[(base + r) * Q + q];
+            s_w1[r][q] = w1[(base + r) * Q + q];
+            s_w2[r][q] = w2[(base + r) * Q + q];
+        }
+        for (int r = threadIdx.x; r < cnt; r += blockDim.x) {
+            s_lp1[r] = lp1[base + r];
+            s_lp2[r] = lp2[base + r];
+        }
+        __syncthreads();
+        if (!valid) continue;
+        for (int r = 0; r < cnt; ++r) {
+            if (G1) {
+                T e = 0;
+#pragma unroll
+                for (int q = 0; q < QM; ++q)
+                    if (q < Q) {
+                        T d = s_mu[r][q] - zm[q];
+                        e += d * d * s_w1[r][q];
+                    }
+                const T t = G1[(base + r) * M + m] * dexp(s_lp1[r] - T(0.5) * e);
+#pragma unroll
+                for (int q = 0; q < QM; ++q)
+                    if (q < Q) gz[q] += t * (s_mu[r][q] - zm[q]) * s_w1[r][q];
+            }
+            if (G2s) {
+                for (int mp = 0; mp < M; ++mp) {
+                    const T g = G2s[(int64_t)mp * M + m];
+                    T e = s_lp2[r];
+#pragma unroll
+                    for (int q = 0; q < QM; ++q)
+                        if (q < Q) {
+                            T b = Z[(int64_t)mp * Q + q];
+                            T d = s_mu[r][q] - T(0.5) * (zm[q] + b);
+                            e -= (zm[q] - b) * (zm[q] - b) / (T(4) * h.l2[q]) +
+                                 d * d * s_w2[r][q];
+                        }
+                    const T t = T(2) * g * dexp(e);
+#pragma unroll
+                    for (int q = 0; q < QM; ++q)
+                        if (q < Q) {
+                            T b = Z[(int64_t)mp * Q + q];
+                            T d = s_mu[r][q] - T(0.5) * (zm[q] + b);
+                            gz[q] += t * (d * s_w2[r][q] - (zm[q] - b) / (T(2) * h.l2[q]));
+                        }
+                }
+            }
+        }
+    }
+    if (valid) {
+#pragma unroll
+        for (int q = 0; q < QM; ++q)
+            if (q < Q) colpart[((int64_t)blockIdx.y * M + m) * Q + q] = gz[q];
+    }
+}
+
+// Fixed-order reduction of the gradient partials into dZ, dl, dsf2.
+template <typename T>
+__global__ void grad_reduce_kernel(int64_t N, int M, int Q, int64_t ncc, int64_t row_blocks,
+                                   const T *__restrict__ colpart, const T *__restrict__ rowpart,
+                                   T dL_dpsi0, T *__restrict__ dZ, T *__restrict__ dsf2,
+                                   T *__restrict__ dl, int accumulate) {
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t MQ = (int64_t)M * Q;
+    if (i < MQ) {
+        T s = 0;
+        for (int64_t c = 0; c < ncc; ++c) s += colpart[c * MQ + i];
+        dZ[i] = (accumulate ? dZ[i] : T(0)) + s;
+    } else if (i < MQ + Q + 1) {
+        const int k = (int)(i - MQ);  // k < Q: dl_k; k == Q: dsf2
+        T s = 0;
+        for (int64_t b = 0; b < row_blocks; ++b) s += rowpart[b * (Q + 1) + k];
+        if (k < Q) {
+            dl[k] = (accumulate ? dl[k] : T(0)) + s;
+        } else {
+            s += dL_dpsi0 * T(N);
+            dsf2[0] = (accumulate ? dsf2[0] : T(0)) + s;
+        }
+    }
+}
+
+template <typename T, int QM>
+void launch_psi2_partial(const Shape &s, const Plan &p, const T *mu, const T *Z, const T *w2,
+                         const T *lp2, const Hyp<T> &h, T *partial, hipStream_t st) {
+    dim3 grid((unsigned)p.tiles, (unsigned)p.nc2);
+    TimedScope ts(st, "generic_psi2_partial");
+    psi2_partial_kernel<T, QM><<<grid, 256, 0, st>>>(s.N, (int)s.M, (int)s.Q, s.P, p.rows2,
+                                                     p.tiles_edge, mu, Z, w2, lp2, h, partial);
+}
+
+template <typename T, int QM>
+void launch_grads(const Shape &s, const Plan &p, const T *mu, const T *S, const T *Z,
+                  const T *w1, const T *w2, const T *lp1, const T *lp2, const Hyp<T> &h,
+                  const T *G1, const T *G2s, T *dmu, T *dS, T *colpart, T *rowpart,
+                  hipStream_t st) {
+    {
+        TimedScope ts(st, "generic_grad_rows");
+        grad_rows_kernel<T, QM><<<(unsigned)p.row_blocks, kRowBlock, 0, st>>>(
+            s.N, (int)s.M, (int)s.Q, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, rowpart);
+    }
+    dim3 grid((unsigned)p.col_blocks, (unsigned)p.ncc);
+    TimedScope ts(st, "generic_grad_cols");
+    grad_cols_kernel<T, QM><<<grid, kColBlock, 0, st>>>(s.N, (int)s.M, (int)s.Q, p.rowsc, mu,
+                                                         Z, w1, w2, lp1, lp2, h, G1, G2s,
+                                                         colpart);
+}
+
+template <typename T>
+void rows_pre(const Shape &s, const Plan &p, const T *S, const Hyp<T> &h, void *ws,
+              hipStream_t st) {
+    TimedScope ts(st, "generic_rows_pre");
+    rows_pre_kernel<T><<<(unsigned)cdiv(s.N, 256), 256, 0, st>>>(
+        s.N, (int)s.Q, S, h, at<T>(ws, p.off_w1), at<T>(ws, p.off_w2), at<T>(ws, p.off_lp1),
+        at<T>(ws, p.off_lp2));
+}
+
+}  // namespace
+
+size_t generic_workspace_bytes(const Shape &s, size_t elem) { return make_plan(s, elem).total; }
+
+template <typename T>
+hipError_t generic_psi_stats(const Shape &s, const T *mu, const T *S, const T *Z,
+                             const Hyp<T> &h, T *psi0, T *Psi1, T *Psi2, int accumulate,
+                             void *ws, hipStream_t st) {
+    const Plan p = make_plan(s, sizeof(T));
+    rows_pre<T>(s, p, S, h, ws, st);
+    const T *w1 = at<T>(ws, p.off_w1), *w2 = at<T>(ws, p.off_w2);
+    const T *lp1 = at<T>(ws, p.off_lp1), *lp2 = at<T>(ws, p.off_lp2);
+    if (Psi1) {
+        TimedScope ts(st, "generic_psi1");
+        psi1_kernel<T><<<(unsigned)cdiv(s.N * s.M, 256), 256, 0, st>>>(s.N, (int)s.M, (int)s.Q,
+                                                                       mu, Z, w1, lp1, Psi1);
+    }
+    T *partial = at<T>(ws, p.off_p2);
+    if (s.Q <= 4) launch_psi2_partial<T, 4>(s, p, mu, Z, w2, lp2, h, partial, st);
+    else if (s.Q <= 8) launch_psi2_partial<T, 8>(s, p, mu, Z, w2, lp2, h, partial, st);
+    else if (s.Q <= 16) launch_psi2_partial<T, 16>(s, p, mu, Z, w2, lp2, h, partial, st);
+    else if (s.Q <= 32) launch_psi2_partial<T, 32>(s, p, mu, Z, w2, lp2, h, partial, st);
+    else launch_psi2_partial<T, 64>(s, p, mu, Z, w2, lp2, h, partial, st);
+    dim3 g((unsigned)p.tiles_edge, (unsigned)p.tiles_edge);
+    TimedScope ts(st, "generic_psi2_reduce");
+    psi2_reduce_kernel<T><<<g, kPairTile * kPairTile, 0, st>>>(s.N, (int)s.M, s.P, p.nc2,
+                                                               partial, h, psi0, Psi2,
+                                                               accumulate);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z,
+                             const Hyp<T> &h, T dL_dpsi0, const T *G1, const T *G2, T *dmu,
+                             T *dS, T *dZ, T *dsf2, T *dl, int accumulate, void *ws,
+                             hipStream_t st) {
+    const Plan p = make_plan(s, sizeof(T));
+    rows_pre<T>(s, p, S, h, ws, st);
+    const T *w1 = at<T>(ws, p.off_w1), *w2 = at<T>(ws, p.off_w2);
+    const T *lp1 = at<T>(ws, p.off_lp1), *lp2 = at<T>(ws, p.off_lp2);
+    T *G2s = nullptr;
+    if (G2) {
+        G2s = at<T>(ws, p.off_g2s);
+        TimedScope ts(st, "generic_sym");
+        sym_kernel<T><<<(unsigned)cdiv(s.M * s.M, 256), 256, 0, st>>>((int)s.M, G2, G2s);
+    }
+    T *colpart = at<T>(ws, p.off_colp), *rowpart = at<T>(ws, p.off_rowp);
+    if (s.Q <= 4)
+        launch_grads<T, 4>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+    else if (s.Q <= 8)
+        launch_grads<T, 8>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+    else if (s.Q <= 16)
+        launch_grads<T, 16>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+    else if (s.Q <= 32)
+        launch_grads<T, 32>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+    else
+        launch_grads<T, 64>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+    const int64_t total = s.M * s.Q + s.Q + 1;
+    TimedScope ts(st, "generic_grad_reduce");
+    grad_reduce_kernel<T><<<(unsigned)cdiv(total, 256), 256, 0, st>>>(
+        s.N, (int)s.M, (int)s.Q, p.ncc, p.row_blocks, colpart, rowpart, dL_dpsi0, dZ, dsf2, dl,
+        accumulate);
+    return hipGetLastError();
+}
+
+template hipError_t generic_psi_stats<float>(const Shape &, const float *, const float *,
+                                             const float *, const Hyp<float> &, float *,
+                                             float *, float *, int, void *, hipStream_t);
+template hipError_t generic_psi_stats<double>(const Shape &, const double *, const double *,
+                                              const double *, const Hyp<double> &, double *,
+                                              double *, double *, int, void *, hipStream_t);
+template hipError_t generic_psi_grads<float>(const Shape &, const float *, const float *,
+                                             const float *, const Hyp<float> &, float,
+                                             const float *, const float *, float *, float *,
+                                             float *, float *, float *, int, void *,
+                                             hipStream_t);
+template hipError_t generic_psi_grads<double>(const Shape &, const double *, const double *,
+                                              const double *, const Hyp<double> &, double,
+                                              const double *, const double *, double *,
+                                              double *, double *, double *, double *, int,
+                                              void *, hipStream_t);
+
+}  // namespace gpps

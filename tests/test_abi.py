@@ -1,0 +1,126 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+public header declares, sizes workspaces, and rejects bad arguments with the
+documented status codes before any HIP call (so nothing here touches a device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1410_4984_amd as gpps
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gpps.h")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_HYPER, ERR_DTYPE, ERR_WS, ERR_ALIGN, ERR_HIP, ERR_PATH = range(9)
+
+# Fake, never-dereferenced device addresses: every call below fails validation
+# before the library would touch them.
+FAKE = 0x7F0000000000
+L2 = (ctypes.c_double * 2)(1.0, 0.5)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:[\w\s\*]+?)\b(gpps_\w+)\s*\(", text, re.M)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    L = gpps.lib()
+    names = declared_functions()
+    assert {"gpps_psi_stats", "gpps_psi_grads", "gpps_workspace_bytes"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.gpps_version() >= 100
+
+
+def test_status_strings():
+    for s in range(9):
+        assert len(gpps.status_string(s)) > 3
+    assert gpps.status_string(1234) == "unknown status"
+
+
+def test_workspace_bytes():
+    assert gpps.workspace_bytes("f32", 100_000, 256, 20) > 0
+    assert gpps.workspace_bytes("f64", 200, 10, 2) > 0
+    assert gpps.workspace_bytes("f32", 0, 10, 2) == 0
+    assert gpps.workspace_bytes("f32", 10, 0, 2) == 0
+    assert gpps.workspace_bytes("f32", 10, 10, gpps.MAX_Q + 1) == 0
+    assert gpps.workspace_bytes("f32", 10, gpps.MAX_M + 1, 2) == 0
+    assert gpps.lib().gpps_workspace_bytes(7, 10, 10, 2) == 0
+    # grows with N (per-row tables) and never shrinks
+    a = gpps.workspace_bytes("f32", 1000, 64, 8)
+    b = gpps.workspace_bytes("f32", 100_000, 64, 8)
+    assert b >= a
+
+
+def _stats(dt=0, N=10, M=4, Q=2, mu=FAKE, S=FAKE, Z=FAKE, sf2=1.0, l=L2, psi0=FAKE, P1=FAKE,
+           P2=FAKE, ws=FAKE, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = max(1, gpps.lib().gpps_workspace_bytes(0, N, M, Q))
+    return gpps.lib().gpps_psi_stats(dt, N, M, Q, mu, S, Z, sf2, l, psi0, P1, P2, 0, ws,
+                                     ws_bytes, None)
+
+
+def _grads(dt=0, N=10, M=4, Q=2, mu=FAKE, S=FAKE, Z=FAKE, sf2=1.0, l=L2, d0=0.5, G1=FAKE,
+           G2=FAKE, dmu=FAKE, dS=FAKE, dZ=FAKE, dsf2=FAKE, dl=FAKE, ws=FAKE, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = max(1, gpps.lib().gpps_workspace_bytes(0, N, M, Q))
+    return gpps.lib().gpps_psi_grads(dt, N, M, Q, mu, S, Z, sf2, l, d0, G1, G2, dmu, dS, dZ,
+                                     dsf2, dl, 0, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("fn", [_stats, _grads])
+def test_validation_codes(fn):
+    assert fn(dt=5) == ERR_DTYPE
+    assert fn(N=0) == ERR_SHAPE
+    assert fn(M=0) == ERR_SHAPE
+    assert fn(Q=0) == ERR_SHAPE
+    assert fn(Q=gpps.MAX_Q + 1) == ERR_SHAPE
+    assert fn(M=gpps.MAX_M + 1) == ERR_SHAPE
+    assert fn(mu=None) == ERR_NULL
+    assert fn(Z=None) == ERR_NULL
+    assert fn(l=None) == ERR_NULL
+    assert fn(sf2=0.0) == ERR_HYPER
+    assert fn(sf2=float("nan")) == ERR_HYPER
+    assert fn(sf2=float("inf")) == ERR_HYPER
+    assert fn(l=(ctypes.c_double * 2)(1.0, -1.0)) == ERR_HYPER
+    assert fn(l=(ctypes.c_double * 2)(1.0, float("inf"))) == ERR_HYPER
+    assert fn(ws=None) == ERR_NULL
+    assert fn(ws=FAKE + 16) == ERR_ALIGN
+    assert fn(ws_bytes=1) == ERR_WS
+    assert fn(mu=FAKE + 2) == ERR_ALIGN
+
+
+def test_validation_stats_specific():
+    assert _stats(psi0=None) == ERR_NULL
+    assert _stats(P2=None) == ERR_NULL
+    assert _stats(dt=1, P1=FAKE + 4) == ERR_ALIGN  # double arrays need 8-byte alignment
+
+
+def test_validation_grads_specific():
+    for k in ("dmu", "dS", "dZ", "dsf2", "dl"):
+        assert _grads(**{k: None}) == ERR_NULL
+    assert _grads(d0=float("nan")) == ERR_HYPER
+
+
+def test_path_selection():
+    L = gpps.lib()
+    old = L.gpps_get_path()
+    try:
+        assert L.gpps_set_path(9) == ERR_PATH
+        for name in ("generic", "mfma", "auto"):
+            gpps.set_path(name)
+            assert gpps.get_path() == name
+        # F64 has no matrix-core path: forcing it is rejected before any HIP call
+        gpps.set_path("mfma")
+        assert _stats(dt=1, ws_bytes=gpps.lib().gpps_workspace_bytes(1, 10, 4, 2)) == ERR_PATH
+    finally:
+        L.gpps_set_path(old)
+
+
+def test_binding_rejects_bad_tensors():
+    torch = pytest.importorskip("torch")
+    mu = torch.zeros(4, 2)
+    with pytest.raises(ValueError):  # CPU tensors are refused: the library only runs on a GPU
+        gpps.psi_stats(mu, mu, torch.zeros(3, 2), 1.0, [1.0, 1.0])

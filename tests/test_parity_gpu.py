@@ -1,0 +1,423 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 CPU oracle.
+
+Tolerances are relative Frobenius norms per output, ||gpu - ref|| / ||ref||:
+fp32 path 1e-5 for Psi1 and 1e-4 for Psi2 and every gradient; fp64 path 1e-10.
+The oracle receives the fp32-rounded inputs upcast to fp64, so the comparison
+measures the kernels' arithmetic, not input rounding.
+
+Small workloads are compared element by element in full.  The large and stress
+workloads run at full size in the launch configuration the benchmark times;
+there the oracle computes sampled outputs one by one (Psi2 entries, rows of
+Psi1 / dmu / dS, rows of dZ, each summed over every datapoint), and the
+outputs it cannot afford (dl, dsigma_f2, dZ at stress) are checked through
+identities that hold at any size: translation and per-dimension scaling of the
+latent space, and sigma_f2-homogeneity.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+import paper_1410_4984_amd as gpps  # noqa: E402
+from paper_1410_4984_amd import synth  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL32 = {"psi0": 1e-6, "Psi1": 1e-5, "Psi2": 1e-4, "dmu": 1e-4, "dS": 1e-4, "dZ": 1e-4,
+         "dsigma_f2": 1e-4, "dl": 1e-4}
+TOL64 = {k: 1e-10 for k in TOL32}
+PATHS = ["generic", "mfma"]
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def rel(a, ref):
+    a, ref = np.asarray(a, dtype=np.float64), np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(ref.ravel())
+    return np.linalg.norm((a - ref).ravel()) / (den if den > 0 else 1.0)
+
+
+@pytest.fixture(autouse=True)
+def _restore_path():
+    yield
+    gpps.set_path("auto")
+
+
+def use_path(path, dtype):
+    if path == "mfma":
+        if dtype != torch.float32:
+            pytest.skip("the matrix-core path is F32 only")
+    gpps.set_path(path)
+
+
+def dev(inp, dtype):
+    t = lambda a: None if a is None else torch.tensor(a, dtype=dtype, device=DEV)  # noqa: E731
+    return {k: (t(v) if isinstance(v, np.ndarray) else v) for k, v in inp.items()}
+
+
+def run_gpu(inp, dtype, want_psi1=True):
+    d = dev(inp, dtype)
+    try:
+        psi0, P1, P2 = gpps.psi_stats(d["mu"], d["S"], d["Z"], inp["sigma_f2"], inp["l"],
+                                      want_psi1=want_psi1)
+        g = gpps.psi_grads(d["mu"], d["S"], d["Z"], inp["sigma_f2"], inp["l"], inp["dL_dpsi0"],
+                           d["dL_dPsi1"], d["dL_dPsi2"])
+    except gpps.GppsError as e:
+        if e.status == 8:
+            pytest.skip("path does not support this shape")
+        raise
+    torch.cuda.synchronize()
+    out = {"psi0": psi0.cpu().double().numpy()[0], "Psi2": P2.cpu().double().numpy()}
+    if want_psi1:
+        out["Psi1"] = P1.cpu().double().numpy()
+    for k, v in g.items():
+        out[k] = v.cpu().double().numpy()
+    out["dsigma_f2"] = out["dsigma_f2"][0]
+    return out
+
+
+def run_oracle(inp):
+    psi0, P1, P2 = oracle.psi_stats(inp["mu"], inp["S"], inp["Z"], inp["sigma_f2"], inp["l"])
+    g = oracle.psi_grads(inp["mu"], inp["S"], inp["Z"], inp["sigma_f2"], inp["l"],
+                         inp["dL_dpsi0"], inp["dL_dPsi1"], inp["dL_dPsi2"])
+    return dict(psi0=psi0, Psi1=P1, Psi2=P2, **g)
+
+
+def compare_all(got, ref, tol, label):
+    bad = {}
+    for k in ref:
+        if k not in got:
+            continue
+        e = rel(got[k], ref[k])
+        say(f"  {label} {k}: rel {e:.3e} (tol {tol[k]:.0e})")
+        if not e <= tol[k]:
+            bad[k] = e
+    assert not bad, (label, bad)
+
+
+_ORACLE_CACHE = {}
+
+
+def oracle_for(name, f32):
+    key = (name, f32)
+    if key not in _ORACLE_CACHE:
+        inp = synth.make_workload(name)
+        if f32:
+            inp = synth.to_f32(inp)
+        _ORACLE_CACHE[key] = (inp, run_oracle(inp))
+    return _ORACLE_CACHE[key]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _libs():
+    oracle.build(force=False)
+    gpps.lib()
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+
+
+# ------------------------------------------------------------------ full comparisons
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_tiny_full(dtype, path):
+    tdt = torch.float64 if dtype == "f64" else torch.float32
+    use_path(path, tdt)
+    say(f"[tiny {dtype} {path}]")
+    inp, ref = oracle_for("tiny", dtype == "f32")
+    got = run_gpu(inp, tdt)
+    compare_all(got, ref, TOL64 if dtype == "f64" else TOL32, f"tiny/{dtype}/{path}")
+    assert np.array_equal(got["Psi2"], got["Psi2"].T)
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("name", ["small", "medium"])
+def test_full_f32(name, path):
+    use_path(path, torch.float32)
+    say(f"[{name} f32 {path}]")
+    inp, ref = oracle_for(name, True)
+    got = run_gpu(inp, torch.float32)
+    compare_all(got, ref, TOL32, f"{name}/f32/{path}")
+    assert np.array_equal(got["Psi2"], got["Psi2"].T)
+
+
+def test_small_f64_generic():
+    use_path("generic", torch.float64)
+    inp, ref = oracle_for("small", False)
+    got = run_gpu(inp, torch.float64)
+    compare_all(got, ref, TOL64, "small/f64")
+
+
+# ------------------------------------------------------------------ full size, sampled
+
+def _sampled_checks(inp, got, rng, label, n_rows=48, n_pairs=64, dz_rows=3, G1_rows=None):
+    """Compare sampled outputs against the oracle and check the identities."""
+    N, Q = inp["mu"].shape
+    M = inp["Z"].shape[0]
+    sf2, l = inp["sigma_f2"], inp["l"]
+    # Psi2 entries (each a sum over all N datapoints), incl. the diagonal
+    pairs = np.stack([rng.integers(0, M, n_pairs), rng.integers(0, M, n_pairs)], 1)
+    pairs[:4, 1] = pairs[:4, 0]
+    ref = oracle.psi2_entries(inp["mu"], inp["S"], inp["Z"], sf2, l, pairs)
+    e = rel(got["Psi2"][pairs[:, 0], pairs[:, 1]], ref)
+    say(f"  {label} Psi2 sampled: rel {e:.3e}")
+    assert e <= TOL32["Psi2"]
+    # rows of Psi1, dmu, dS: per-row outputs depend on their own row only
+    rows = np.sort(rng.choice(N, n_rows, replace=False))
+    rows[-1] = N - 1
+    G1 = inp["dL_dPsi1"] if G1_rows is None else G1_rows(rows)
+    G1r = G1[rows] if G1_rows is None else G1
+    _, P1, _ = oracle.psi_stats(inp["mu"][rows], inp["S"][rows], inp["Z"], sf2, l)
+    g = oracle.psi_grads(inp["mu"][rows], inp["S"][rows], inp["Z"], sf2, l, 0.0, G1r,
+                         inp["dL_dPsi2"])
+    for k, got_k, ref_k, tol in (("Psi1", got.get("Psi1"), P1, TOL32["Psi1"]),
+                                 ("dmu", got["dmu"], g["dmu"], TOL32["dmu"]),
+                                 ("dS", got["dS"], g["dS"], TOL32["dS"])):
+        if got_k is None:
+            continue
+        e = rel(got_k[rows], ref_k)
+        say(f"  {label} {k} rows: rel {e:.3e}")
+        assert e <= tol, (k, e)
+    # rows of dZ (sums over every datapoint)
+    if dz_rows:
+        zr = rng.choice(M, dz_rows, replace=False)
+        ref = oracle.dZ_rows(inp["mu"], inp["S"], inp["Z"], sf2, l, inp["dL_dPsi1"],
+                             inp["dL_dPsi2"], zr)
+        e = rel(got["dZ"][zr], ref)
+        say(f"  {label} dZ rows: rel {e:.3e}")
+        assert e <= TOL32["dZ"]
+    _identities(inp, got, label)
+
+
+def _identities(inp, got, label, tol=2e-5):
+    """Exact identities of the gradients, evaluated on the GPU's own outputs.
+    Each residual is compared with the sum of the magnitudes of its terms."""
+    mu, S, Z, l, sf2 = inp["mu"], inp["S"], inp["Z"], inp["l"], inp["sigma_f2"]
+    dmu, dS, dZ, dl = got["dmu"], got["dS"], got["dZ"], got["dl"]
+    # translation of latent dimension q
+    r = dmu.sum(0) + dZ.sum(0)
+    s = np.abs(dmu).sum(0) + np.abs(dZ).sum(0)
+    say(f"  {label} translation residual {np.max(np.abs(r) / s):.2e}")
+    assert np.all(np.abs(r) <= tol * s)
+    # scaling of latent dimension q (mu, z, l scaled by c, S by c^2)
+    terms = [(mu * dmu).sum(0), (Z * dZ).sum(0), l * dl, 2 * (S * dS).sum(0)]
+    r = sum(terms)
+    s = (np.abs(mu * dmu).sum(0) + np.abs(Z * dZ).sum(0) + np.abs(l * dl)
+         + 2 * np.abs(S * dS).sum(0))
+    say(f"  {label} scaling residual {np.max(np.abs(r) / s):.2e}")
+    assert np.all(np.abs(r) <= tol * s)
+    # sf2 homogeneity: sf2 dL/dsf2 = <G1, Psi1> + 2 <G2s, Psi2> + dL_dpsi0 N sf2
+    if "Psi1" in got and inp.get("dL_dPsi1") is not None:
+        G2s = 0.5 * (inp["dL_dPsi2"] + inp["dL_dPsi2"].T)
+        a = np.sum(inp["dL_dPsi1"] * got["Psi1"])
+        b = 2 * np.sum(G2s * got["Psi2"])
+        c = inp["dL_dpsi0"] * mu.shape[0] * sf2
+        r = sf2 * got["dsigma_f2"] - (a + b + c)
+        s = abs(a) + abs(b) + abs(c)
+        say(f"  {label} homogeneity residual {abs(r) / s:.2e}")
+        assert abs(r) <= 1e-4 * s
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_large_full_size_sampled(path):
+    use_path(path, torch.float32)
+    say(f"[large f32 {path} full size]")
+    inp = synth.to_f32(synth.make_workload("large"))
+    got = run_gpu(inp, torch.float32)
+    assert np.array_equal(got["Psi2"], got["Psi2"].T)
+    assert got["psi0"] == pytest.approx(inp["mu"].shape[0] * inp["sigma_f2"], rel=1e-6)
+    _sampled_checks(inp, got, np.random.default_rng(1), f"large/{path}")
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_large_row_subset_full(path):
+    """Every output, dl and dsigma_f2 included, against the oracle on a row subset
+    of the large workload (same M = 256, Q = 20)."""
+    use_path(path, torch.float32)
+    inp = synth.to_f32(synth.make_workload("large"))
+    rows = np.arange(0, inp["mu"].shape[0], 97)  # 1031 rows
+    sub = dict(inp, mu=inp["mu"][rows], S=inp["S"][rows], dL_dPsi1=inp["dL_dPsi1"][rows])
+    got = run_gpu(sub, torch.float32)
+    compare_all(got, run_oracle(sub), TOL32, f"large-subset/{path}")
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_stress_chunked(path):
+    """N = 10^6, M = 512, Q = 30 in 8 row chunks, accumulating on the device."""
+    use_path(path, torch.float32)
+    say(f"[stress f32 {path} chunked]")
+    w = synth.WORKLOADS["stress"]
+    inp = synth.to_f32(synth.make_workload("stress"))
+    N, M, Q, C = w.N, w.M, w.Q, w.chunk_rows
+    d = dev({k: v for k, v in inp.items() if k != "dL_dPsi1"}, torch.float32)
+    psi0 = torch.zeros(1, dtype=torch.float32, device=DEV)
+    Psi2 = torch.zeros((M, M), dtype=torch.float32, device=DEV)
+    gout = {"dmu": torch.empty((N, Q), device=DEV), "dS": torch.empty((N, Q), device=DEV),
+            "dZ": torch.zeros((M, Q), device=DEV), "dsigma_f2": torch.zeros(1, device=DEV),
+            "dl": torch.zeros(Q, device=DEV)}
+    ws = torch.empty(gpps.workspace_bytes("f32", C, M, Q), dtype=torch.uint8, device=DEV)
+    G1_sum = 0.0
+    try:
+        for c, r0 in enumerate(range(0, N, C)):
+            r1 = min(N, r0 + C)
+            G1 = synth.stress_dL_dPsi1_chunk(0, c, r1 - r0, M).astype(np.float32)
+            G1d = torch.tensor(G1, device=DEV)
+            _, P1, _ = gpps.psi_stats(d["mu"][r0:r1], d["S"][r0:r1], d["Z"], inp["sigma_f2"],
+                                      inp["l"], accumulate=c > 0,
+                                      out=(psi0, torch.empty((r1 - r0, M), device=DEV), Psi2),
+                                      workspace=ws)
+            G1_sum += float(torch.sum(G1d.double() * P1.double()))
+            sub = {k: gout[k] for k in gout}
+            sub["dmu"], sub["dS"] = gout["dmu"][r0:r1], gout["dS"][r0:r1]
+            gpps.psi_grads(d["mu"][r0:r1], d["S"][r0:r1], d["Z"], inp["sigma_f2"], inp["l"],
+                           inp["dL_dpsi0"], G1d, d["dL_dPsi2"], accumulate=c > 0, out=sub,
+                           workspace=ws)
+            say(f"  chunk {c} rows {r0}:{r1} enqueued")
+    except gpps.GppsError as e:
+        if e.status == 8:
+            pytest.skip("path does not support this shape")
+        raise
+    torch.cuda.synchronize()
+    got = {"psi0": psi0.cpu().double().numpy()[0], "Psi2": Psi2.cpu().double().numpy()}
+    for k, v in gout.items():
+        got[k] = v.cpu().double().numpy()
+    got["dsigma_f2"] = got["dsigma_f2"][0]
+    assert np.array_equal(got["Psi2"], got["Psi2"].T)
+    assert got["psi0"] == pytest.approx(N * inp["sigma_f2"], rel=1e-5)
+
+    def g1_rows(rows):
+        out = np.empty((rows.shape[0], M))
+        for i, r in enumerate(rows):
+            c = r // C
+            out[i] = synth.stress_dL_dPsi1_chunk(0, c, min(N, (c + 1) * C) - c * C, M)[r - c * C]
+        return out.astype(np.float32).astype(np.float64)
+
+    _sampled_checks(inp, got, np.random.default_rng(2), f"stress/{path}", n_rows=16,
+                    n_pairs=32, dz_rows=0, G1_rows=g1_rows)
+    # sf2 homogeneity with <G1, Psi1> accumulated per chunk above
+    G2s = 0.5 * (inp["dL_dPsi2"] + inp["dL_dPsi2"].T)
+    a, b, c = G1_sum, 2 * np.sum(G2s * got["Psi2"]), inp["dL_dpsi0"] * N * inp["sigma_f2"]
+    r = inp["sigma_f2"] * got["dsigma_f2"] - (a + b + c)
+    assert abs(r) <= 1e-4 * (abs(a) + abs(b) + abs(c))
+
+
+# ------------------------------------------------------------------ determinism, chunking
+
+@pytest.mark.parametrize("path", PATHS)
+def test_bitwise_deterministic(path):
+    use_path(path, torch.float32)
+    inp = synth.to_f32(synth.make_workload("medium"))
+    a = run_gpu(inp, torch.float32)
+    b = run_gpu(inp, torch.float32)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_chunked_accumulate_matches_single_call(path):
+    use_path(path, torch.float32)
+    inp = synth.to_f32(synth.random_inputs(3001, 40, 7, seed=4))
+    whole = run_gpu(inp, torch.float32)
+    d = dev(inp, torch.float32)
+    N, Q = inp["mu"].shape
+    M = inp["Z"].shape[0]
+    psi0 = torch.zeros(1, device=DEV)
+    P1 = torch.empty((N, M), device=DEV)
+    P2 = torch.empty((M, M), device=DEV)
+    g = {"dmu": torch.empty((N, Q), device=DEV), "dS": torch.empty((N, Q), device=DEV),
+         "dZ": torch.empty((M, Q), device=DEV), "dsigma_f2": torch.empty(1, device=DEV),
+         "dl": torch.empty(Q, device=DEV)}
+    for i, (r0, r1) in enumerate([(0, 1000), (1000, 1001), (1001, 3001)]):
+        gpps.psi_stats(d["mu"][r0:r1], d["S"][r0:r1], d["Z"], inp["sigma_f2"], inp["l"],
+                       accumulate=i > 0, out=(psi0, P1[r0:r1], P2))
+        sub = dict(g, dmu=g["dmu"][r0:r1], dS=g["dS"][r0:r1])
+        gpps.psi_grads(d["mu"][r0:r1], d["S"][r0:r1], d["Z"], inp["sigma_f2"], inp["l"],
+                       inp["dL_dpsi0"], d["dL_dPsi1"][r0:r1],
+                       d["dL_dPsi2"], accumulate=i > 0, out=sub)
+    torch.cuda.synchronize()
+    chunked = {"psi0": psi0.cpu().double().numpy()[0], "Psi1": P1.cpu().double().numpy(),
+               "Psi2": P2.cpu().double().numpy()}
+    for k, v in g.items():
+        chunked[k] = v.cpu().double().numpy()
+    chunked["dsigma_f2"] = chunked["dsigma_f2"][0]
+    for k in whole:
+        e = rel(chunked[k], whole[k])
+        assert e <= 1e-5, (k, e)
+    assert np.array_equal(chunked["Psi2"], chunked["Psi2"].T)
+
+
+# ------------------------------------------------------------------ edge cases
+
+EDGE = [
+    ("N1", dict(N=1, M=5, Q=3)),
+    ("M1", dict(N=300, M=1, Q=4)),
+    ("Q1", dict(N=500, M=33, Q=1)),
+    ("ragged", dict(N=777, M=65, Q=13)),
+    ("Qmax", dict(N=150, M=17, Q=64)),
+    ("Mbig", dict(N=3, M=1100, Q=2)),
+]
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("case", EDGE, ids=[c[0] for c in EDGE])
+def test_edge_shapes(case, path):
+    name, kw = case
+    use_path(path, torch.float32)
+    say(f"[edge {name} {kw} {path}]")
+    inp = synth.to_f32(synth.random_inputs(kw["N"], kw["M"], kw["Q"], seed=9))
+    got = run_gpu(inp, torch.float32)
+    compare_all(got, run_oracle(inp), TOL32, f"edge-{name}/{path}")
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_edge_shapes_f64(path):
+    use_path(path, torch.float64)
+    for N, M, Q in [(1, 1, 1), (37, 19, 5), (64, 16, 64)]:
+        inp = synth.random_inputs(N, M, Q, seed=10)
+        got = run_gpu(inp, torch.float64)
+        compare_all(got, run_oracle(inp), TOL64, f"f64-{N}x{M}x{Q}")
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_null_upstream_gradients_and_nonsymmetric_G2(path):
+    use_path(path, torch.float32)
+    inp = synth.to_f32(synth.random_inputs(900, 24, 6, seed=12))
+    rng = np.random.default_rng(13)
+    inp["dL_dPsi2"] = rng.standard_normal((24, 24)).astype(np.float32).astype(np.float64)
+    compare_all(run_gpu(inp, torch.float32), run_oracle(inp), TOL32, "nonsym")
+    for drop in ("dL_dPsi1", "dL_dPsi2"):
+        x = dict(inp, **{drop: None})
+        compare_all(run_gpu(x, torch.float32, want_psi1=False), run_oracle(x), TOL32, drop)
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_zero_variance_limit(path):
+    """S = 0: Psi1 is the plain kernel matrix K(mu, Z) and Psi2 = K^T K."""
+    use_path(path, torch.float32)
+    inp = synth.to_f32(synth.random_inputs(400, 20, 5, seed=14))
+    inp["S"] = np.zeros_like(inp["S"])
+    got = run_gpu(inp, torch.float32)
+    r2 = (((inp["mu"][:, None, :] - inp["Z"][None]) / inp["l"]) ** 2).sum(-1)
+    K = inp["sigma_f2"] * np.exp(-0.5 * r2)
+    assert rel(got["Psi1"], K) <= 1e-5
+    assert rel(got["Psi2"], K.T @ K) <= 1e-4
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_far_inducing_points_underflow_cleanly(path):
+    """Inducing inputs far from every datapoint: the exponentials underflow to 0
+    and nothing turns into NaN or Inf."""
+    use_path(path, torch.float32)
+    inp = synth.to_f32(synth.random_inputs(200, 12, 3, seed=15))
+    inp["Z"][6:] += 60.0
+    got = run_gpu(inp, torch.float32)
+    for k, v in got.items():
+        assert np.all(np.isfinite(v)), k
+    compare_all(got, run_oracle(inp), TOL32, "far")

@@ -277,6 +277,7 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
 
     if (G2s && valid) {
         for (int m = 0; m < M; ++m) {
+            T gsf_row = 0;  // sum over m' first, so long rows do not swamp the total
             for (int mp = m; mp < M; ++mp) {
                 const T g = (m == mp ? T(1) : T(2)) * G2s[(int64_t)m * M + mp];
                 T e = l2v;
@@ -288,7 +289,7 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
                         e -= (a - b) * (a - b) / (T(4) * h.l2[q]) + d * d * a2[q];
                     }
                 const T t = g * dexp(e);
-                gsf += T(2) * t;
+                gsf_row += T(2) * t;
 #pragma unroll
                 for (int q = 0; q < QM; ++q)
                     if (q < Q) {
@@ -303,6 +304,7 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
                                       T(2) * h.l[q] * dd * dd);
                     }
             }
+            gsf += gsf_row;
         }
     }
 
@@ -320,11 +322,11 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
     for (int q = 0; q < QM; ++q) s_red[q][tid] = gl[q];
     s_red[QM][tid] = gsf / h.sf2;
     __syncthreads();
-    if (tid <= Q) {
-        const int row = tid < Q ? tid : QM;
+    for (int k = tid; k <= Q; k += kRowBlock) {
+        const int row = k < Q ? k : QM;
         T s = 0;
         for (int i = 0; i < kRowBlock; ++i) s += s_red[row][i];
-        rowpart[(int64_t)blockIdx.x * (Q + 1) + tid] = s;
+        rowpart[(int64_t)blockIdx.x * (Q + 1) + k] = s;
     }
 }
 
@@ -533,6 +535,64 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
         accumulate);
     return hipGetLastError();
 }
+
+template <typename T>
+void generic_psi1_fwd(const Shape &s, const T *mu, const T *S, const T *Z, const Hyp<T> &h,
+                      T *Psi1, void *ws, hipStream_t st) {
+    const Plan p = make_plan(s, sizeof(T));
+    rows_pre<T>(s, p, S, h, ws, st);
+    TimedScope ts(st, "generic_psi1");
+    psi1_kernel<T><<<(unsigned)cdiv(s.N * s.M, 256), 256, 0, st>>>(
+        s.N, (int)s.M, (int)s.Q, mu, Z, at<T>(ws, p.off_w1), at<T>(ws, p.off_lp1), Psi1);
+}
+
+template <typename T>
+Psi1GradParts<T> generic_psi1_grads(const Shape &s, const T *mu, const T *S, const T *Z,
+                                    const Hyp<T> &h, const T *G1, T *dmu, T *dS, void *ws,
+                                    hipStream_t st) {
+    const Plan p = make_plan(s, sizeof(T));
+    rows_pre<T>(s, p, S, h, ws, st);
+    const T *w1 = at<T>(ws, p.off_w1), *w2 = at<T>(ws, p.off_w2);
+    const T *lp1 = at<T>(ws, p.off_lp1), *lp2 = at<T>(ws, p.off_lp2);
+    T *colpart = at<T>(ws, p.off_colp), *rowpart = at<T>(ws, p.off_rowp);
+    const int Q = (int)s.Q, M = (int)s.M;
+    {
+        TimedScope ts(st, "generic_psi1_grad_rows");
+#define GPPS_ROWS(QM)                                                                         \
+    grad_rows_kernel<T, QM><<<(unsigned)p.row_blocks, kRowBlock, 0, st>>>(                    \
+        s.N, M, Q, mu, S, Z, w1, w2, lp1, lp2, h, G1, nullptr, dmu, dS, rowpart)
+        if (Q <= 4) GPPS_ROWS(4);
+        else if (Q <= 8) GPPS_ROWS(8);
+        else if (Q <= 16) GPPS_ROWS(16);
+        else if (Q <= 32) GPPS_ROWS(32);
+        else GPPS_ROWS(64);
+#undef GPPS_ROWS
+    }
+    int64_t ncc = 0;
+    if (G1) {
+        ncc = p.ncc;
+        dim3 grid((unsigned)p.col_blocks, (unsigned)p.ncc);
+        TimedScope ts(st, "generic_psi1_grad_cols");
+#define GPPS_COLS(QM)                                                                         \
+    grad_cols_kernel<T, QM><<<grid, kColBlock, 0, st>>>(s.N, M, Q, p.rowsc, mu, Z, w1, w2,    \
+                                                        lp1, lp2, h, G1, nullptr, colpart)
+        if (Q <= 4) GPPS_COLS(4);
+        else if (Q <= 8) GPPS_COLS(8);
+        else if (Q <= 16) GPPS_COLS(16);
+        else if (Q <= 32) GPPS_COLS(32);
+        else GPPS_COLS(64);
+#undef GPPS_COLS
+    }
+    return Psi1GradParts<T>{colpart, ncc, rowpart, p.row_blocks};
+}
+
+template void generic_psi1_fwd<float>(const Shape &, const float *, const float *,
+                                      const float *, const Hyp<float> &, float *, void *,
+                                      hipStream_t);
+template Psi1GradParts<float> generic_psi1_grads<float>(const Shape &, const float *,
+                                                        const float *, const float *,
+                                                        const Hyp<float> &, const float *,
+                                                        float *, float *, void *, hipStream_t);
 
 template hipError_t generic_psi_stats<float>(const Shape &, const float *, const float *,
                                              const float *, const Hyp<float> &, float *,

@@ -536,64 +536,6 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
     return hipGetLastError();
 }
 
-template <typename T>
-void generic_psi1_fwd(const Shape &s, const T *mu, const T *S, const T *Z, const Hyp<T> &h,
-                      T *Psi1, void *ws, hipStream_t st) {
-    const Plan p = make_plan(s, sizeof(T));
-    rows_pre<T>(s, p, S, h, ws, st);
-    TimedScope ts(st, "generic_psi1");
-    psi1_kernel<T><<<(unsigned)cdiv(s.N * s.M, 256), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, mu, Z, at<T>(ws, p.off_w1), at<T>(ws, p.off_lp1), Psi1);
-}
-
-template <typename T>
-Psi1GradParts<T> generic_psi1_grads(const Shape &s, const T *mu, const T *S, const T *Z,
-                                    const Hyp<T> &h, const T *G1, T *dmu, T *dS, void *ws,
-                                    hipStream_t st) {
-    const Plan p = make_plan(s, sizeof(T));
-    rows_pre<T>(s, p, S, h, ws, st);
-    const T *w1 = at<T>(ws, p.off_w1), *w2 = at<T>(ws, p.off_w2);
-    const T *lp1 = at<T>(ws, p.off_lp1), *lp2 = at<T>(ws, p.off_lp2);
-    T *colpart = at<T>(ws, p.off_colp), *rowpart = at<T>(ws, p.off_rowp);
-    const int Q = (int)s.Q, M = (int)s.M;
-    {
-        TimedScope ts(st, "generic_psi1_grad_rows");
-#define GPPS_ROWS(QM)                                                                         \
-    grad_rows_kernel<T, QM><<<(unsigned)p.row_blocks, kRowBlock, 0, st>>>(                    \
-        s.N, M, Q, mu, S, Z, w1, w2, lp1, lp2, h, G1, nullptr, dmu, dS, rowpart)
-        if (Q <= 4) GPPS_ROWS(4);
-        else if (Q <= 8) GPPS_ROWS(8);
-        else if (Q <= 16) GPPS_ROWS(16);
-        else if (Q <= 32) GPPS_ROWS(32);
-        else GPPS_ROWS(64);
-#undef GPPS_ROWS
-    }
-    int64_t ncc = 0;
-    if (G1) {
-        ncc = p.ncc;
-        dim3 grid((unsigned)p.col_blocks, (unsigned)p.ncc);
-        TimedScope ts(st, "generic_psi1_grad_cols");
-#define GPPS_COLS(QM)                                                                         \
-    grad_cols_kernel<T, QM><<<grid, kColBlock, 0, st>>>(s.N, M, Q, p.rowsc, mu, Z, w1, w2,    \
-                                                        lp1, lp2, h, G1, nullptr, colpart)
-        if (Q <= 4) GPPS_COLS(4);
-        else if (Q <= 8) GPPS_COLS(8);
-        else if (Q <= 16) GPPS_COLS(16);
-        else if (Q <= 32) GPPS_COLS(32);
-        else GPPS_COLS(64);
-#undef GPPS_COLS
-    }
-    return Psi1GradParts<T>{colpart, ncc, rowpart, p.row_blocks};
-}
-
-template void generic_psi1_fwd<float>(const Shape &, const float *, const float *,
-                                      const float *, const Hyp<float> &, float *, void *,
-                                      hipStream_t);
-template Psi1GradParts<float> generic_psi1_grads<float>(const Shape &, const float *,
-                                                        const float *, const float *,
-                                                        const Hyp<float> &, const float *,
-                                                        float *, float *, void *, hipStream_t);
-
 template hipError_t generic_psi_stats<float>(const Shape &, const float *, const float *,
                                              const float *, const Hyp<float> &, float *,
                                              float *, float *, int, void *, hipStream_t);

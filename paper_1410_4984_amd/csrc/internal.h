@@ -64,26 +64,6 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
                              T *dS, T *dZ, T *dsf2, T *dl, int accumulate, void *ws,
                              hipStream_t st);
 
-// Psi1 pieces of the generic path, reused by the matrix-core path (which
-// replaces only the O(N M^2 Q) Psi2 work).
-template <typename T>
-struct Psi1GradParts {
-    const T *colpart;      // [ncc][M][Q] partial dZ (Psi1 terms), or unused when ncc == 0
-    int64_t ncc;
-    const T *rowpart;      // [row_blocks][Q + 1] partial dl and dsf2 (Psi1 terms)
-    int64_t row_blocks;
-};
-
-template <typename T>
-void generic_psi1_fwd(const Shape &s, const T *mu, const T *S, const T *Z, const Hyp<T> &h,
-                      T *Psi1, void *ws, hipStream_t st);
-
-// Writes dmu, dS (Psi1 terms only; zeros when G1 is NULL) and the partials.
-template <typename T>
-Psi1GradParts<T> generic_psi1_grads(const Shape &s, const T *mu, const T *S, const T *Z,
-                                    const Hyp<T> &h, const T *G1, T *dmu, T *dS, void *ws,
-                                    hipStream_t st);
-
 // ---------------------------------------------------------------- matrix-core path
 // F32 only: per-datapoint Gram blocks and W * D products on MFMA, exp on VALU.
 bool mfma_supports(const Shape &s);

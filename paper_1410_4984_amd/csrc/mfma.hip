@@ -10,13 +10,15 @@
 //   Psi2_n[m, m'] = sf2^2 prod_q (1 + 2S/l^2)^(-1/2)
 //                   exp(-sum_q [(z_m - z_m')^2/(4 l^2) + (mu - (z_m + z_m')/2)^2 w2])
 // splits exactly into a row term, a column term and a Gram term:
-//   log2 Psi2_n[m, m'] = b_m + b_m' + sum_q a_mq a_m'q,
-//   a_mq = d_mq sqrt(log2(e) kappa_q),
-//   b_m  = log2(e) (log sf2 - 1/4 sum_q log(1 + 2S/l^2) - 1/4 sum_q (1/l^2 + w2) d_mq^2).
-// The Gram term is a K = Q contraction per 32 x 32 tile of pairs (MFMA); the
-// row and column terms enter through the MFMA's C input; exp2 is one
-// v_exp_f32.  Inputs are centred (Z and mu shifted by the mean inducing
-// input), which changes no result (every quantity depends on mu - z only).
+//   log2 Psi2_n[m, m'] = b_m + b_m' + sum_q K_q d_mq d_m'q,     K = log2(e) kappa,
+//   b_m = log2(e) (log sf2 - 1/4 sum_q log(1 + 2S/l^2) - 1/4 sum_q (1/l^2 + w2) d_mq^2).
+// The Gram term is further written with one side independent of n:
+//   sum_q K d_mq d_m'q = c_m + sum_q (-K_q d_mq) z_m'q,   c_m = sum_q K_q d_mq mu_q,
+// so one MFMA operand is the (centred) z table itself, and the other,
+// -K d, is formed once per datapoint and row block.  b and b + c come from a
+// per-call table (mfma_rowterm_kernel); exp2 is one v_exp_f32.  Inputs are
+// centred (Z and mu shifted by the mean inducing input), which changes no
+// result: every quantity depends on mu - z only.
 //
 // Gradient (Alg. 2): with W_n = G2s o Psi2_n (G2s the symmetric part of
 // dL/dPsi2), r_n = W_n 1 and V_n = W_n D_n (D_n[m, q] = d_mq), every derivative
@@ -27,23 +29,24 @@
 //   dl_q    += (2 S w2 / l) R + l w2^2 (X + Y) + (X - Y) / l^3
 //   dsf2    += 2 R / sf2
 // Since D_n = 1 mu_n^T - Z, V_n = r_n mu_n^T - W_n Z: the second MFMA product
-// is W_n [Z | 1], whose B operand is the constant Z table and whose ones
+// is W_n [Z | 1], whose B operand is the constant z table and whose ones
 // column yields r_n.  Its A operand is the W tile exactly as the first MFMA
-// left it in registers.
+// left it in registers.  The Psi1 terms (t = dL/dPsi1 * Psi1) join the same
+// epilogue: dmu -= w1 sum_m t d, dS += 1/2 w1^2 sum_m t d^2 - 1/2 w1 sum_m t,
+// dZ += t d w1, with w1 = 1/(l^2 + S).
 //
-// Work split.  Z (centred, plus the ones column) is staged in LDS once per
-// workgroup.  Rows are processed in batches: the batch's per-row values and
-// its row terms b (exact d-form, one thread per inducing input) are staged in
-// LDS, then every wave runs its rows with no further barrier.  Forward: a
-// workgroup owns a group of upper-triangular 32 x 32 pair tiles and a chunk of
-// rows; each wave keeps its tiles' running sums in registers; partial tiles
-// are reduced over chunks in a fixed order.  Gradient: every term above is
-// linear in (r_n, V_n), so the full M x M tile grid is split into wave tasks
-// (one row block of W, up to four column blocks) whose dL/dPsi2 tiles stay in
-// registers; each task adds its share of dZ (registers) and of the per-row
-// sums X, Y, P, R (LDS, then global), which a finalize kernel combines.  No
-// atomics; every cross-wave or cross-workgroup sum runs in a fixed order, so
-// results are bitwise reproducible.
+// Work split.  The z table (centred, plus the ones column) is staged in LDS
+// once per workgroup.  Rows are processed in batches whose per-row values and
+// row terms are copied into LDS; then every wave runs its rows with no
+// further barrier.  Forward: a wave task is a run of upper-triangular 32 x 32
+// pair tiles in one row block; its running sums stay in registers; partial
+// tiles are reduced over row chunks in a fixed order.  Gradient: every term
+// above is linear in (r_n, V_n), so the full M x M tile grid is split into
+// wave tasks (one row block of W, two column blocks) whose dL/dPsi2 tiles stay
+// in registers; each task adds its share of dZ (registers) and of the per-row
+// sums (LDS, then global), which a finalize kernel combines.  No atomics;
+// every cross-wave or cross-workgroup sum runs in a fixed order, so results
+// are bitwise reproducible.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -61,12 +64,11 @@ constexpr int kWaves = 4;
 constexpr int kRowStride = 64;         // stride of per-row tables padded to 64 dimensions
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kPadBias = -1.0e30f;   // row term of a padded inducing input: exp2 -> 0
-constexpr int kMaxTilesPerWave = 4;    // forward
-constexpr int kRBF = 16;               // forward rows per batch
-constexpr int kRBG = 8;                // gradient rows per batch
+constexpr int kRB = 8;                 // rows per batch (both kernels)
 constexpr int64_t kFwdTargetWGs = 1024;
 constexpr int64_t kGradTargetWGs = 512;
 constexpr int kFinRows = 64;           // rows per block of the gradient finalize kernel
+constexpr int kRTRows = 32;            // rows per block of the row-term kernel
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -74,21 +76,47 @@ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // register t, row 8 (t / 4) + 4 (l / 32) + t % 4.
 __device__ __forceinline__ int crow(int t, int g) { return 8 * (t >> 2) + 4 * g + (t & 3); }
 
+// Forward wave tasks: row block ti, tiles tj = tj0 .. tj0 + TPW - 1 (clamped to
+// the last block; clamped tiles are computed but never written).
+__host__ __device__ inline int fwd_tasks(int nb, int tpw) {
+    int n = 0;
+    for (int ti = 0; ti < nb; ++ti) n += (nb - ti + tpw - 1) / tpw;
+    return n;
+}
+
+__device__ inline void fwd_task(int task, int nb, int tpw, int &ti, int &tj0) {
+    for (ti = 0; ti < nb; ++ti) {
+        const int k = (nb - ti + tpw - 1) / tpw;
+        if (task < k) break;
+        task -= k;
+    }
+    tj0 = ti + task * tpw;
+}
+
+// Upper-triangular tile index of (ti, tj), row-major.
+__host__ __device__ inline int64_t tile_index(int ti, int tj, int nb) {
+    return (int64_t)ti * nb - (int64_t)ti * (ti - 1) / 2 + (tj - ti);
+}
+
 struct MPlan {
     int64_t Mp;            // M rounded up to the tile edge
     int nb;                // tiles per edge
     int nqb;               // 32-column blocks of [Z | 1] (Q + 1 columns)
-    int DS;                // LDS row stride of the Z table (odd: conflict-free column reads)
+    int DS;                // gradient: LDS row stride of the z table (odd: conflict-free
+                           // column reads; 32 * nqb + 1 columns for the [Z | 1] product)
+    int DSF;               // forward: the same for the Gram operand only (>= 2 ks, odd)
     int ks;                // MFMA k-steps (2 latent dimensions each), instantiated value
-    int jpw, njr, ntasks;  // gradient: column blocks per wave task, ranges, tasks (nb * njr)
-    int64_t ggroups;       // gradient: workgroups (4 tasks each) per row chunk
     int64_t T;             // upper-triangular tiles
-    int64_t tpg, groups;   // forward: tiles per group, groups
+    int tpw, ftasks;       // forward: tiles per wave task, tasks
+    int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
     int64_t frows, fchunks;
+    int jpw, njr, ntasks;  // gradient: column blocks per wave task, ranges, tasks (nb * njr)
+    int64_t ggroups;       // gradient: workgroups per row chunk
     int64_t grows, gchunks;
-    size_t lds_fwd, lds_grad;
     int64_t fin_blocks;    // finalize: blocks of kFinRows rows
-    size_t off_sq, off_hq, off_w2, off_hl, off_zc, off_g2, off_fp, off_rs, off_dz, off_dl, total;
+    size_t lds_fwd, lds_grad;
+    size_t off_K, off_hq, off_w2, off_hl, off_w1, off_l1, off_zc, off_bt, off_bc, off_t1, off_g2,
+        off_fp, off_rs, off_dz, off_dl, total;
 };
 
 int round_ks(int ks, int nqb) {
@@ -106,30 +134,30 @@ int round_ks(int ks, int nqb) {
 
 // LDS layout (floats), shared by both kernels:
 //   Zx  [Mp][DS]        centred z, column Q = 1 for real rows, zero padding
-//   bb  [RB][Mp]        row terms of the batch
+//   bb  [RB][Mp]        row terms b of the batch (log2 units)
+//   bcb [RB][Mp]        b + c
 //   mub [RB][64]        centred mu of the batch (zero beyond Q)
-//   sqb [RB][64]        sqrt(log2e kappa) of the batch (zero beyond Q)
-//   hqb [RB][Q]         -log2e/4 (1/l^2 + w2)
-//   hlb [RB]            log-prefactor
+//   Kb  [RB][64]        log2e kappa of the batch (zero beyond Q)
 // gradient only:
-//   w2b [RB][Q], red [RB][kWaves][3Q + 1]
+//   w1b [RB][Q], w2b [RB][Q], t1 [RB][Mp] (dL/dPsi1 * Psi1), red [RB][kWaves][5Q + 2]
 struct Lds {
-    int zx, bb, mub, sqb, hqb, hlb, w2b, red, total;
+    int zx, bb, bcb, mub, kb, w1b, w2b, t1, red, total;
 };
 
-__host__ __device__ inline Lds lds_layout(int Mp, int DS, int Q, int RB, bool grad) {
+__host__ __device__ inline Lds lds_layout(int Mp, int DS, int Q, bool grad) {
     Lds L{};
     int o = 0;
     L.zx = o; o += Mp * DS;
-    L.bb = o; o += RB * Mp;
-    L.mub = o; o += RB * kRowStride;
-    L.sqb = o; o += RB * kRowStride;
-    L.hqb = o; o += RB * Q;
-    L.hlb = o; o += (RB + 3) / 4 * 4;
-    L.w2b = L.red = o;
+    L.bb = o; o += kRB * Mp;
+    L.bcb = o; o += kRB * Mp;
+    L.mub = o; o += kRB * kRowStride;
+    L.kb = o; o += kRB * kRowStride;
+    L.w1b = L.w2b = L.t1 = L.red = o;
     if (grad) {
-        L.w2b = o; o += RB * Q;
-        L.red = o; o += RB * kWaves * (3 * Q + 1);
+        L.w1b = o; o += kRB * Q;
+        L.w2b = o; o += kRB * Q;
+        L.t1 = o; o += kRB * Mp;
+        L.red = o; o += kRB * kWaves * (5 * Q + 2);
     }
     L.total = o;
     return L;
@@ -142,32 +170,45 @@ MPlan make_mplan(const Shape &s) {
     p.nqb = s.Q + 1 <= 32 ? 1 : 2;
     p.DS = 32 * p.nqb + 1;
     p.ks = round_ks((int)cdiv(s.Q, 2), p.nqb);
+    p.DSF = std::max<int>(2 * p.ks, (int)s.Q + 1) | 1;
+    p.T = (int64_t)p.nb * (p.nb + 1) / 2;
+    // forward tasks: the tiles-per-task value with the fewest tile slots (ties: larger)
+    p.tpw = 1;
+    int64_t best = -1;
+    for (int t = 1; t <= 4; ++t) {
+        const int64_t slots = cdiv(fwd_tasks(p.nb, t), kWaves) * kWaves * t;
+        if (best < 0 || slots <= best) { best = slots; p.tpw = t; }
+    }
+    p.ftasks = fwd_tasks(p.nb, p.tpw);
+    p.fgroups = cdiv(p.ftasks, kWaves);
+    p.fchunks = std::max<int64_t>(1, std::min(cdiv(kFwdTargetWGs, p.fgroups), cdiv(s.N, 32)));
+    p.frows = cdiv(s.N, p.fchunks);
+    p.fchunks = cdiv(s.N, p.frows);
     p.jpw = p.nb >= 2 ? 2 : 1;   // 2: the task fits 2 waves per SIMD
     p.njr = (int)cdiv(p.nb, p.jpw);
     p.ntasks = p.nb * p.njr;
     p.ggroups = cdiv(p.ntasks, kWaves);
-    p.T = (int64_t)p.nb * (p.nb + 1) / 2;
-    p.groups = cdiv(p.T, kWaves * kMaxTilesPerWave);
-    p.tpg = cdiv(p.T, p.groups);
-    p.fchunks = std::max<int64_t>(1, std::min(cdiv(kFwdTargetWGs, p.groups), cdiv(s.N, 32)));
-    p.frows = cdiv(s.N, p.fchunks);
-    p.fchunks = cdiv(s.N, p.frows);
     p.gchunks = std::max<int64_t>(1, std::min(cdiv(kGradTargetWGs, p.ggroups), cdiv(s.N, 16)));
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
-    p.lds_fwd = sizeof(float) * lds_layout((int)p.Mp, p.DS, (int)s.Q, kRBF, false).total;
-    p.lds_grad = sizeof(float) * lds_layout((int)p.Mp, p.DS, (int)s.Q, kRBG, true).total;
-    size_t o = generic_workspace_bytes(s, sizeof(float));   // Psi1 pieces live first
+    p.fin_blocks = cdiv(s.N, kFinRows);
+    p.lds_fwd = sizeof(float) * lds_layout((int)p.Mp, p.DSF, (int)s.Q, false).total;
+    p.lds_grad = sizeof(float) * lds_layout((int)p.Mp, p.DS, (int)s.Q, true).total;
+    size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
-    p.off_sq = take(sizeof(float) * s.N * kRowStride);
+    p.off_K = take(sizeof(float) * s.N * kRowStride);
     p.off_hq = take(sizeof(float) * s.N * s.Q);
     p.off_w2 = take(sizeof(float) * s.N * s.Q);
     p.off_hl = take(sizeof(float) * s.N);
+    p.off_w1 = take(sizeof(float) * s.N * s.Q);
+    p.off_l1 = take(sizeof(float) * s.N);
     p.off_zc = take(sizeof(float) * s.Q);
+    p.off_bt = take(sizeof(float) * s.N * p.Mp);
+    p.off_bc = take(sizeof(float) * s.N * p.Mp);
+    p.off_t1 = take(sizeof(float) * s.N * p.Mp);
     p.off_g2 = take(sizeof(float) * p.Mp * p.Mp);
     p.off_fp = take(sizeof(float) * p.fchunks * p.T * kTile * kTile);
-    p.fin_blocks = cdiv(s.N, kFinRows);
-    p.off_rs = take(sizeof(float) * p.ggroups * s.N * (3 * s.Q + 1));
+    p.off_rs = take(sizeof(float) * p.ggroups * s.N * (5 * s.Q + 2));
     p.off_dz = take(sizeof(float) * p.gchunks * p.njr * s.M * s.Q);
     p.off_dl = take(sizeof(float) * p.fin_blocks * (s.Q + 1));
     p.total = o;
@@ -177,48 +218,123 @@ MPlan make_mplan(const Shape &s) {
 float *fat(void *ws, size_t off) { return reinterpret_cast<float *>(static_cast<char *>(ws) + off); }
 
 // ---------------------------------------------------------------- small kernels
-// sq[n][q] = sqrt(log2e * kappa_nq) (zero for q >= Q up to the stride),
-// hq[n][q] = -log2e/4 (1/l^2 + w2), w2[n][q], hl[n] = log2e (log sf2 - 1/4 sum_q log(1 + 2S/l^2)).
-__global__ void mfma_rows_kernel(int64_t N, int Q, const float *__restrict__ S, Hyp<float> h,
-                                 float *__restrict__ sq, float *__restrict__ hq,
-                                 float *__restrict__ w2t, float *__restrict__ hl) {
-    const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (n >= N) return;
-    float lsum = 0.f;
-    for (int q = 0; q < kRowStride; ++q) {
-        if (q < Q) {
-            const float s = S[n * Q + q];
-            const float l2 = h.l2[q];
-            const float w2 = 1.f / (l2 + 2.f * s);
-            const float kap = s * w2 / l2;
-            sq[n * kRowStride + q] = sqrtf(kLog2e * kap);
-            hq[n * Q + q] = -0.25f * kLog2e * (1.f / l2 + w2);
-            w2t[n * Q + q] = w2;
-            lsum += log1pf(2.f * s / l2);
-        } else {
-            sq[n * kRowStride + q] = 0.f;
-        }
+// One wave per datapoint, one lane per latent dimension:
+//   K[n][q]  = log2e S / (l^2 (l^2 + 2S))  (zero for q >= Q up to the stride)
+//   hq[n][q] = -log2e/4 (1/l^2 + w2),  w2[n][q] = 1/(l^2 + 2S),  w1[n][q] = 1/(l^2 + S)
+//   hl[n]    = log2e (log sf2 - 1/4 sum_q log(1 + 2S/l^2))   (Psi2 prefactor, half of it)
+//   l1[n]    = log2e (log sf2 - 1/2 sum_q log(1 + S/l^2))    (Psi1 prefactor)
+// The sums over q use a fixed butterfly, so they are deterministic.
+__global__ __launch_bounds__(256) void mfma_rows_kernel(
+    int64_t N, int Q, const float *__restrict__ S, Hyp<float> h, float *__restrict__ Kt,
+    float *__restrict__ hq, float *__restrict__ w2t, float *__restrict__ hl,
+    float *__restrict__ w1t, float *__restrict__ l1) {
+    const int q = threadIdx.x & 63;
+    const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (n >= N) return;                        // wave-uniform
+    float a2 = 0.f, a1 = 0.f;
+    if (q < Q) {
+        const float s = S[n * Q + q];
+        const float l2 = h.l2[q];
+        const float w2 = 1.f / (l2 + 2.f * s);
+        Kt[n * kRowStride + q] = kLog2e * s * w2 / l2;
+        hq[n * Q + q] = -0.25f * kLog2e * (1.f / l2 + w2);
+        w2t[n * Q + q] = w2;
+        w1t[n * Q + q] = 1.f / (l2 + s);
+        a2 = log1pf(2.f * s / l2);
+        a1 = log1pf(s / l2);
+    } else {
+        Kt[n * kRowStride + q] = 0.f;
     }
-    hl[n] = kLog2e * (h.log_sf2 - 0.25f * lsum);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        a2 += __shfl_xor(a2, off);
+        a1 += __shfl_xor(a1, off);
+    }
+    if (q == 0) {
+        hl[n] = kLog2e * (h.log_sf2 - 0.25f * a2);
+        l1[n] = kLog2e * (h.log_sf2 - 0.5f * a1);
+    }
 }
 
-// Mean inducing input per dimension (fixed-order sum): the centring shift.
-__global__ void mfma_centre_kernel(int M, int Q, const float *__restrict__ Z,
-                                   float *__restrict__ zc) {
-    const int q = threadIdx.x;
-    if (q >= Q) return;
+// Mean inducing input per dimension: the centring shift.  Column sums in a
+// fixed order (per-thread partials over strided rows, then a fixed tree).
+__global__ __launch_bounds__(256) void mfma_centre_kernel(int M, int Q,
+                                                          const float *__restrict__ Z,
+                                                          float *__restrict__ zc) {
+    __shared__ float part[4][64];
+    const int q = threadIdx.x & 63, w = threadIdx.x >> 6;
     float s = 0.f;
-    for (int m = 0; m < M; ++m) s += Z[(int64_t)m * Q + q];
-    zc[q] = s / (float)M;
+    if (q < Q)
+        for (int m = w; m < M; m += 4) s += Z[(int64_t)m * Q + q];
+    part[w][q] = s;
+    __syncthreads();
+    if (w == 0 && q < Q) zc[q] = ((part[0][q] + part[1][q]) + (part[2][q] + part[3][q])) / (float)M;
 }
 
-// Symmetric part of dL/dPsi2, zero-padded to Mp x Mp.
+// Symmetric part of dL/dPsi2, zero-padded to Mp x Mp (all zero when G2 is NULL).
 __global__ void mfma_sym_kernel(int M, int Mp, const float *__restrict__ G2,
                                 float *__restrict__ G2p) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)Mp * Mp) return;
     const int m = (int)(i / Mp), mp = (int)(i - (int64_t)m * Mp);
-    G2p[i] = (m < M && mp < M) ? 0.5f * (G2[(int64_t)m * M + mp] + G2[(int64_t)mp * M + m]) : 0.f;
+    G2p[i] = (G2 && m < M && mp < M) ? 0.5f * (G2[(int64_t)m * M + mp] + G2[(int64_t)mp * M + m])
+                                     : 0.f;
+}
+
+// Row terms and Psi1 for every (n, m), once per call (d = mu - z, centred):
+//   bt[n][m] = hl_n + sum_q hq_nq d^2,   bc[n][m] = bt[n][m] + sum_q K_nq d mu_nq
+//   Psi1     = exp2(l1_n - log2e/2 sum_q w1_nq d^2)
+// (kPadBias in both row-term tables for m >= M).  The forward writes Psi1
+// (NULL: skipped); the gradient writes t1[n][m] = dL/dPsi1[n][m] * Psi1 with
+// row stride Mp (zero where G1 is NULL or m >= M).  One thread per inducing
+// input (z in registers), rows staged in LDS.
+template <int QM>
+__global__ __launch_bounds__(256) void mfma_rowterm_kernel(
+    int64_t N, int M, int Q, int Mp, const float *__restrict__ mu, const float *__restrict__ Z,
+    const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ hq,
+    const float *__restrict__ hl, const float *__restrict__ w1t, const float *__restrict__ l1,
+    const float *__restrict__ G1, float *__restrict__ bt, float *__restrict__ bc,
+    float *__restrict__ psi1, float *__restrict__ t1) {
+    __shared__ float s_mu[kRTRows][QM], s_hq[kRTRows][QM], s_w1[kRTRows][QM], s_k[kRTRows][QM];
+    __shared__ float s_hl[kRTRows], s_l1[kRTRows];
+    const int m = blockIdx.y * 256 + threadIdx.x;
+    const int64_t n0 = (int64_t)blockIdx.x * kRTRows;
+    const int cnt = (int)min<int64_t>(kRTRows, N - n0);
+    for (int i = threadIdx.x; i < kRTRows * QM; i += 256) {
+        const int r = i / QM, q = i - r * QM;
+        const bool ok = r < cnt && q < Q;
+        const int64_t n = n0 + r;
+        s_mu[r][q] = ok ? mu[n * Q + q] - zc[q] : 0.f;
+        s_hq[r][q] = ok ? hq[n * Q + q] : 0.f;
+        s_w1[r][q] = ok ? w1t[n * Q + q] : 0.f;
+        s_k[r][q] = ok ? Kt[n * kRowStride + q] : 0.f;
+    }
+    for (int r = threadIdx.x; r < kRTRows; r += 256) {
+        s_hl[r] = r < cnt ? hl[n0 + r] : 0.f;
+        s_l1[r] = r < cnt ? l1[n0 + r] : 0.f;
+    }
+    __syncthreads();
+    if (m >= Mp) return;
+    const bool real = m < M;
+    float z[QM];
+#pragma unroll
+    for (int q = 0; q < QM; ++q) z[q] = (real && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+    for (int r = 0; r < cnt; ++r) {
+        float b = s_hl[r], cc = 0.f, e = 0.f;
+#pragma unroll
+        for (int q = 0; q < QM; ++q) {
+            const float d = s_mu[r][q] - z[q];
+            b = fmaf(s_hq[r][q] * d, d, b);
+            cc = fmaf(s_k[r][q] * d, s_mu[r][q], cc);
+            e = fmaf(s_w1[r][q] * d, d, e);
+        }
+        const int64_t n = n0 + r;
+        bt[n * Mp + m] = real ? b : kPadBias;
+        bc[n * Mp + m] = real ? b + cc : kPadBias;
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(-0.5f * kLog2e, e, s_l1[r]));
+        if (t1) t1[n * Mp + m] = (real && G1) ? G1[n * M + m] * p1 : 0.f;
+        else if (psi1 && real) psi1[n * M + m] = p1;
+    }
 }
 
 // ---------------------------------------------------------------- LDS staging
@@ -235,134 +351,125 @@ __device__ void stage_z(float *lds, const Lds &L, int M, int Mp, int Q, int DS,
     }
 }
 
-// Per-row values of rows [n0, n0 + cb) into the batch arrays, then (after a
-// barrier) the row terms b of every inducing input.  Rows >= cb are zero.
-template <int RB, bool GRAD>
-__device__ void stage_batch(float *lds, const Lds &L, int64_t n0, int cb, int M, int Mp, int Q,
-                            int DS, const float *__restrict__ mu, const float *__restrict__ zc,
-                            const float *__restrict__ sq, const float *__restrict__ hq,
-                            const float *__restrict__ hl, const float *__restrict__ w2t) {
-    for (int i = threadIdx.x; i < RB * kRowStride; i += kThreads) {
+// Per-row values of rows [n0, n0 + cb) into the batch arrays.  Rows >= cb
+// are zero (row terms: kPadBias).
+template <bool GRAD>
+__device__ void stage_batch(float *lds, const Lds &L, int64_t n0, int cb, int Mp, int Q,
+                            const float *__restrict__ mu, const float *__restrict__ zc,
+                            const float *__restrict__ Kt, const float *__restrict__ bt,
+                            const float *__restrict__ bc, const float *__restrict__ w1t,
+                            const float *__restrict__ w2t, const float *__restrict__ t1g) {
+    for (int i = threadIdx.x; i < kRB * kRowStride; i += kThreads) {
         const int r = i / kRowStride, q = i - r * kRowStride;
         const bool ok = r < cb && q < Q;
         const int64_t n = n0 + r;
         lds[L.mub + i] = ok ? mu[n * Q + q] - zc[q] : 0.f;
-        lds[L.sqb + i] = ok ? sq[n * kRowStride + q] : 0.f;
+        lds[L.kb + i] = ok ? Kt[n * kRowStride + q] : 0.f;
     }
-    for (int i = threadIdx.x; i < RB * Q; i += kThreads) {
-        const int r = i / Q;
-        const bool ok = r < cb;
-        lds[L.hqb + i] = ok ? hq[n0 * Q + i] : 0.f;
-        if (GRAD) lds[L.w2b + i] = ok ? w2t[n0 * Q + i] : 0.f;
+    for (int i = threadIdx.x; i < kRB * Mp; i += kThreads) {
+        const bool ok = i < cb * Mp;
+        lds[L.bb + i] = ok ? bt[n0 * Mp + i] : kPadBias;
+        lds[L.bcb + i] = ok ? bc[n0 * Mp + i] : kPadBias;
+        if (GRAD) lds[L.t1 + i] = ok ? t1g[n0 * Mp + i] : 0.f;
     }
-    for (int r = threadIdx.x; r < RB; r += kThreads) lds[L.hlb + r] = r < cb ? hl[n0 + r] : 0.f;
-    __syncthreads();
-    for (int m = threadIdx.x; m < Mp; m += kThreads) {
-        float acc[RB];
-#pragma unroll
-        for (int r = 0; r < RB; ++r) acc[r] = lds[L.hlb + r];
-        if (m < M) {
-            for (int q = 0; q < Q; ++q) {
-                const float z = lds[L.zx + m * DS + q];
-#pragma unroll
-                for (int r = 0; r < RB; ++r) {
-                    const float d = lds[L.mub + r * kRowStride + q] - z;
-                    acc[r] = fmaf(lds[L.hqb + r * Q + q] * d, d, acc[r]);
-                }
-            }
+    if (GRAD) {
+        for (int i = threadIdx.x; i < kRB * Q; i += kThreads) {
+            const bool ok = i < cb * Q;
+            lds[L.w1b + i] = ok ? w1t[n0 * Q + i] : 0.f;
+            lds[L.w2b + i] = ok ? w2t[n0 * Q + i] : 0.f;
         }
-#pragma unroll
-        for (int r = 0; r < RB; ++r) lds[L.bb + r * Mp + m] = (m < M && r < cb) ? acc[r] : kPadBias;
     }
 }
 
-// MFMA operand values a_{m, 2s+g} for the 32 rows of block `blk` (lane supplies row c).
+// The n-dependent Gram operand -K d = (z - mu) K for the 32 rows of block
+// `blk` (lane supplies row c, latent dimension 2s + g).
 template <int KS>
-__device__ __forceinline__ void operands(const float *zx, int DS, int blk, int c, int g,
-                                         const float (&muk)[KS], const float (&sk)[KS],
-                                         float (&out)[KS]) {
+__device__ __forceinline__ void kd_operands(const float *zx, int DS, int blk, int c, int g,
+                                            const float (&muk)[KS], const float (&kk)[KS],
+                                            float (&out)[KS]) {
     const float *zr = zx + (blk * kTile + c) * DS + g;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) out[s] = (muk[s] - zr[2 * s]) * sk[s];
+    for (int s = 0; s < KS; ++s) out[s] = (zr[2 * s] - muk[s]) * kk[s];
 }
 
 // ---------------------------------------------------------------- Psi2 forward
-template <int KS>
-__global__ __launch_bounds__(kThreads) void psi2_fwd_kernel(
-    int64_t N, int M, int Q, int Mp, int nb, int DS, int64_t T, int64_t tpg,
+// Tile (ti, tj), rows m in block ti, columns m' in block tj:
+//   e[m][m'] = (b + c)_m + b_m' + sum_q (-K d_mq) z_m'q     (A: -K d, B: z)
+// Waves per SIMD the forward kernel is compiled for: 3 where its registers fit
+// without spilling, else 2 (1 for the widest tasks).
+constexpr int fwd_waves(int ks, int tpw) {
+    return ((tpw <= 2 && ks <= 16) || (tpw == 3 && ks <= 10) || (tpw == 4 && ks <= 4)) ? 3
+           : (ks >= 24 && tpw >= 3) ? 1
+                                     : 2;
+}
+
+template <int KS, int TPW>
+__global__ __launch_bounds__(kThreads, fwd_waves(KS, TPW)) void psi2_fwd_kernel(
+    int64_t N, int M, int Q, int Mp, int nb, int DS, int64_t T, int ftasks,
     int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
-    const float *__restrict__ zc, const float *__restrict__ sq, const float *__restrict__ hq,
-    const float *__restrict__ hl, float *__restrict__ partial) {
+    const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ bt,
+    const float *__restrict__ bc, float *__restrict__ partial) {
     extern __shared__ float lds[];
-    const Lds L = lds_layout(Mp, DS, Q, kRBF, false);
+    const Lds L = lds_layout(Mp, DS, Q, false);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
-
-    // this wave's tiles: a contiguous run of the group, so neighbours share their row block
-    const int64_t t0 = (int64_t)blockIdx.x * tpg, t1 = min(T, t0 + tpg);
-    const int64_t tpw = (tpg + kWaves - 1) / kWaves;
-    int ti[kMaxTilesPerWave], tj[kMaxTilesPerWave];
-    bool tv[kMaxTilesPerWave];
+    const int task = blockIdx.x * kWaves + wave;
+    const bool active = task < ftasks;         // wave-uniform
+    int ti = 0, tj0 = 0;
+    if (active) fwd_task(task, nb, TPW, ti, tj0);
+    int tj[TPW];
 #pragma unroll
-    for (int k = 0; k < kMaxTilesPerWave; ++k) {
-        const int64_t t = t0 + wave * tpw + k;
-        tv[k] = k < tpw && t < t1;
-        int64_t r = 0, u = tv[k] ? t : 0;
-        while (u >= nb - r) { u -= nb - r; ++r; }
-        ti[k] = (int)r;
-        tj[k] = (int)(r + u);
-    }
-    v16f acc[kMaxTilesPerWave];
+    for (int k = 0; k < TPW; ++k) tj[k] = min(tj0 + k, nb - 1);
+    v16f acc[TPW];
 #pragma unroll
-    for (int k = 0; k < kMaxTilesPerWave; ++k)
+    for (int k = 0; k < TPW; ++k)
 #pragma unroll
         for (int t = 0; t < 16; ++t) acc[k][t] = 0.f;
 
     stage_z(lds, L, M, Mp, Q, DS, Z, zc);
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
-    for (int64_t n0 = r0; n0 < r1; n0 += kRBF) {
-        const int cb = (int)min<int64_t>(kRBF, r1 - n0);
+    for (int64_t n0 = r0; n0 < r1; n0 += kRB) {
+        const int cb = (int)min<int64_t>(kRB, r1 - n0);
         __syncthreads();
-        stage_batch<kRBF, false>(lds, L, n0, cb, M, Mp, Q, DS, mu, zc, sq, hq, hl, nullptr);
+        stage_batch<false>(lds, L, n0, cb, Mp, Q, mu, zc, Kt, bt, bc, nullptr, nullptr, nullptr);
         __syncthreads();
+        if (!active) continue;
         for (int r = 0; r < cb; ++r) {
-            float muk[KS], sk[KS];
+            float muk[KS], kk[KS];
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
                 muk[s] = lds[L.mub + r * kRowStride + 2 * s + g];
-                sk[s] = lds[L.sqb + r * kRowStride + 2 * s + g];
+                kk[s] = lds[L.kb + r * kRowStride + 2 * s + g];
             }
-            const float *bb = lds + L.bb + r * Mp;
             float aop[KS];
-            int cur = -1;
+            kd_operands<KS>(lds + L.zx, DS, ti, c, g, muk, kk, aop);
+            const float *bcr = lds + L.bcb + r * Mp + ti * kTile;
+            float brow[16];
 #pragma unroll
-            for (int k = 0; k < kMaxTilesPerWave; ++k) {
-                if (!tv[k]) continue;
-                if (ti[k] != cur) {
-                    operands<KS>(lds + L.zx, DS, ti[k], c, g, muk, sk, aop);
-                    cur = ti[k];
-                }
-                float bop[KS];
-                operands<KS>(lds + L.zx, DS, tj[k], c, g, muk, sk, bop);
-                const float bcol = bb[tj[k] * kTile + c];
+            for (int t = 0; t < 16; ++t) brow[t] = bcr[crow(t, g)];
+            const float *bbr = lds + L.bb + r * Mp;
+#pragma unroll
+            for (int k = 0; k < TPW; ++k) {
+                const float bcol = bbr[tj[k] * kTile + c];
+                const float *zr = lds + L.zx + (tj[k] * kTile + c) * DS + g;
                 v16f e;
 #pragma unroll
-                for (int t = 0; t < 16; ++t) e[t] = bb[ti[k] * kTile + crow(t, g)] + bcol;
+                for (int t = 0; t < 16; ++t) e[t] = brow[t] + bcol;
 #pragma unroll
                 for (int s = 0; s < KS; ++s)
-                    e = __builtin_amdgcn_mfma_f32_32x32x2f32(aop[s], bop[s], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x2f32(aop[s], zr[2 * s], e, 0, 0, 0);
 #pragma unroll
                 for (int t = 0; t < 16; ++t) acc[k][t] += __builtin_amdgcn_exp2f(e[t]);
             }
         }
     }
-    // partial tiles, row-major inside the tile
+    // partial tiles, row-major inside the tile (clamped duplicates are skipped)
+    if (!active) return;
 #pragma unroll
-    for (int k = 0; k < kMaxTilesPerWave; ++k) {
-        if (!tv[k]) continue;
-        const int64_t t = t0 + wave * tpw + k;
-        float *dst = partial + ((int64_t)blockIdx.y * T + t) * (kTile * kTile);
+    for (int k = 0; k < TPW; ++k) {
+        if (tj0 + k >= nb) continue;
+        float *dst = partial + ((int64_t)blockIdx.y * T + tile_index(ti, tj[k], nb)) * (kTile * kTile);
 #pragma unroll
         for (int r = 0; r < 16; ++r) dst[crow(r, g) * kTile + c] = acc[k][r];
     }
@@ -378,11 +485,12 @@ __global__ void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T, int64_t 
     if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
         psi0[0] = (accumulate ? psi0[0] : 0.f) + (float)N * sf2;
     if (m >= M || mp >= M || m > mp) return;
-    const int ti = m / kTile, tj = mp / kTile;
-    const int64_t t = (int64_t)ti * nb - (int64_t)ti * (ti - 1) / 2 + (tj - ti);
-    const int64_t off = t * (kTile * kTile) + (m % kTile) * kTile + (mp % kTile);
+    const int64_t off = tile_index(m / kTile, mp / kTile, nb) * (kTile * kTile) +
+                        (m % kTile) * kTile + (mp % kTile);
+    const int64_t stride = T * (kTile * kTile);
     float s = 0.f;
-    for (int64_t ch = 0; ch < chunks; ++ch) s += partial[ch * T * (kTile * kTile) + off];
+#pragma unroll 8
+    for (int64_t ch = 0; ch < chunks; ++ch) s += partial[ch * stride + off];
     const float v = (accumulate ? Psi2[(int64_t)m * M + mp] : 0.f) + s;
     Psi2[(int64_t)m * M + mp] = v;
     Psi2[(int64_t)mp * M + m] = v;
@@ -390,41 +498,46 @@ __global__ void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T, int64_t 
 
 // ---------------------------------------------------------------- Psi2 gradient
 // Every gradient term is linear in (r_n, V_n), so the M x M tile grid may be
-// split freely: a wave task is one row block i (the m index of W) and up to
-// JPW column blocks j (the m' index).  The task's dL/dPsi2 tiles stay in
-// registers for the whole kernel; V' = W [Z | 1] accumulates over the task's
-// tiles; the epilogue turns it into the task's share of dZ (registers) and of
-// the per-row sums X, Y, P, R, which the workgroup combines in LDS and writes
-// per (group, row) for psi2_finalize_kernel.
+// split freely: a wave task is one row block i (the m index of W) and JPW
+// column blocks j (the m' index).  Tile (j, i), rows m' in block j, columns m
+// in block i:  e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)   (A: z, B: -K d).
+// The task's dL/dPsi2 tiles stay in registers for the whole kernel; V' = W [Z | 1]
+// accumulates over the task's tiles; the epilogue turns it into the task's
+// share of dZ (registers) and of the per-row sums, which the workgroup
+// combines in LDS and writes per (group, row) for psi2_finalize_kernel.
 template <int KS, int JPW, int NQB>
-__global__ __launch_bounds__(kThreads) void psi2_grad_kernel(
+__global__ __launch_bounds__(kThreads, NQB == 1 ? 2 : 1) void psi2_grad_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int DS, int njr, int ntasks,
     int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
-    const float *__restrict__ zc, const float *__restrict__ sq, const float *__restrict__ hq,
-    const float *__restrict__ hl, const float *__restrict__ w2t, const float *__restrict__ G2p,
-    Hyp<float> h, float *__restrict__ rowsum, float *__restrict__ part_dz) {
+    const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ bt,
+    const float *__restrict__ bc, const float *__restrict__ w1t, const float *__restrict__ w2t,
+    const float *__restrict__ t1g, const float *__restrict__ G2p, Hyp<float> h,
+    float *__restrict__ rowsum, float *__restrict__ part_dz) {
     extern __shared__ float lds[];
-    const Lds L = lds_layout(Mp, DS, Q, kRBG, true);
+    const Lds L = lds_layout(Mp, DS, Q, true);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
     const int ones_src = 32 * g + (Q & 31);    // lane holding column Q (the row sums r)
     const int ones_qb = Q >> 5;
-    const int RED = 3 * Q + 1;
+    const int RED = 5 * Q + 2;                 // X, Y, P, X1, P1 per dimension, then R, T1
     const int group = blockIdx.x;
     const int task = group * kWaves + wave;
     const bool active = task < ntasks;         // wave-uniform
     const int i = active ? task / njr : 0;     // row block of W (m)
     const int jr = active ? task % njr : 0;    // range of column blocks of W (m')
+    const bool has1 = active && jr == 0;       // this task also adds the Psi1 terms of block i
 
+    // dL/dPsi2 tiles of the task (zero for column blocks past the edge)
+    int jb[JPW];
     float g2r[JPW][16];
-    bool jv[JPW];
 #pragma unroll
     for (int k = 0; k < JPW; ++k) {
         const int j = jr * JPW + k;
-        jv[k] = active && j < nb;
-        const float *g2 = G2p + (int64_t)(jv[k] ? j : 0) * kTile * Mp + i * kTile + c;
+        const bool ok = active && j < nb;
+        jb[k] = ok ? j : nb - 1;
+        const float *g2 = G2p + (int64_t)jb[k] * kTile * Mp + i * kTile + c;
 #pragma unroll
-        for (int t = 0; t < 16; ++t) g2r[k][t] = jv[k] ? g2[(int64_t)crow(t, g) * Mp] : 0.f;
+        for (int t = 0; t < 16; ++t) g2r[k][t] = ok ? g2[(int64_t)crow(t, g) * Mp] : 0.f;
     }
     v16f dz[NQB];
 #pragma unroll
@@ -441,10 +554,10 @@ __global__ __launch_bounds__(kThreads) void psi2_grad_kernel(
     stage_z(lds, L, M, Mp, Q, DS, Z, zc);
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
-    for (int64_t n0 = r0; n0 < r1; n0 += kRBG) {
-        const int cb = (int)min<int64_t>(kRBG, r1 - n0);
+    for (int64_t n0 = r0; n0 < r1; n0 += kRB) {
+        const int cb = (int)min<int64_t>(kRB, r1 - n0);
         __syncthreads();
-        stage_batch<kRBG, true>(lds, L, n0, cb, M, Mp, Q, DS, mu, zc, sq, hq, hl, w2t);
+        stage_batch<true>(lds, L, n0, cb, Mp, Q, mu, zc, Kt, bt, bc, w1t, w2t, t1g);
         __syncthreads();
         for (int r = 0; r < cb; ++r) {
             float *rs = lds + L.red + (r * kWaves + wave) * RED;
@@ -452,17 +565,17 @@ __global__ __launch_bounds__(kThreads) void psi2_grad_kernel(
                 for (int k = lane; k < RED; k += 64) rs[k] = 0.f;
                 continue;
             }
-            float muk[KS], sk[KS];
+            float muk[KS], kk[KS];
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
                 muk[s] = lds[L.mub + r * kRowStride + 2 * s + g];
-                sk[s] = lds[L.sqb + r * kRowStride + 2 * s + g];
+                kk[s] = lds[L.kb + r * kRowStride + 2 * s + g];
             }
-            const float *bb = lds + L.bb + r * Mp;
-            // Gram B operand: column block i (the m index of W)
+            // Gram B operand: -K d for column block i (the m index of W)
             float bop[KS];
-            operands<KS>(lds + L.zx, DS, i, c, g, muk, sk, bop);
-            const float bcol = bb[i * kTile + c];
+            kd_operands<KS>(lds + L.zx, DS, i, c, g, muk, kk, bop);
+            const float bcol = lds[L.bcb + r * Mp + i * kTile + c];
+            const float *bbr = lds + L.bb + r * Mp;
             v16f V[NQB];
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb)
@@ -470,17 +583,14 @@ __global__ __launch_bounds__(kThreads) void psi2_grad_kernel(
                 for (int t = 0; t < 16; ++t) V[qb][t] = 0.f;
 #pragma unroll
             for (int k = 0; k < JPW; ++k) {
-                if (!jv[k]) continue;
-                const int j = jr * JPW + k;
-                // rows m' in block j (A operand), columns m in block i (B operand)
-                float aop[KS];
-                operands<KS>(lds + L.zx, DS, j, c, g, muk, sk, aop);
+                const int j = jb[k];
+                const float *zr = lds + L.zx + (j * kTile + c) * DS + g;
                 v16f e;
 #pragma unroll
-                for (int t = 0; t < 16; ++t) e[t] = bb[j * kTile + crow(t, g)] + bcol;
+                for (int t = 0; t < 16; ++t) e[t] = bbr[j * kTile + crow(t, g)] + bcol;
 #pragma unroll
                 for (int s = 0; s < KS; ++s)
-                    e = __builtin_amdgcn_mfma_f32_32x32x2f32(aop[s], bop[s], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x2f32(zr[2 * s], bop[s], e, 0, 0, 0);
                 const float *zrow = lds + L.zx + j * kTile * DS + c;
 #pragma unroll
                 for (int t = 0; t < 16; ++t) {
@@ -492,50 +602,63 @@ __global__ __launch_bounds__(kThreads) void psi2_grad_kernel(
                 }
             }
             // epilogue for rows m = i*32 + crow(t, g); V' = W [Z | 1] -> V = r mu^T - V'
-            float muq[NQB], alpha[NQB], beta[NQB];
+            float muq[NQB], alpha[NQB], beta[NQB], w1q[NQB];
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb) {
                 const int q = qb * 32 + c;
                 muq[qb] = lds[L.mub + r * kRowStride + q];
                 const float w2 = q < Q ? lds[L.w2b + r * Q + q] : 0.f;
+                w1q[qb] = q < Q ? lds[L.w1b + r * Q + q] : 0.f;
                 alpha[qb] = w2 - il2[qb];
                 beta[qb] = w2 + il2[qb];
             }
-            float X[NQB], Y[NQB], P[NQB], R = 0.f;
+            float X[NQB], Y[NQB], P[NQB], X1[NQB], P1[NQB], R = 0.f, T1 = 0.f;
 #pragma unroll
-            for (int qb = 0; qb < NQB; ++qb) X[qb] = Y[qb] = P[qb] = 0.f;
+            for (int qb = 0; qb < NQB; ++qb) X[qb] = Y[qb] = P[qb] = X1[qb] = P1[qb] = 0.f;
             const float *zblk = lds + L.zx + i * kTile * DS;
+            const float *t1r = lds + L.t1 + r * Mp + i * kTile;
 #pragma unroll
             for (int t = 0; t < 16; ++t) {
                 const int rr = crow(t, g);
                 const float rt = __int_as_float(__builtin_amdgcn_ds_bpermute(
                     ones_src * 4, __float_as_int(ones_qb == 0 ? V[0][t] : V[NQB - 1][t])));
                 R += rt;
+                const float tv = has1 ? t1r[rr] : 0.f;
+                T1 += tv;
 #pragma unroll
                 for (int qb = 0; qb < NQB; ++qb) {
                     const float d = muq[qb] - zblk[rr * DS + qb * 32 + c];
                     const float v = fmaf(rt, muq[qb], -V[qb][t]);
                     const float dr = d * rt;
-                    dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, dz[qb][t]));
+                    const float td = tv * d;
+                    dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, fmaf(td, w1q[qb], dz[qb][t])));
                     X[qb] = fmaf(dr, d, X[qb]);
                     P[qb] += dr;
                     Y[qb] = fmaf(d, v, Y[qb]);
+                    X1[qb] = fmaf(td, d, X1[qb]);
+                    P1[qb] += td;
                 }
             }
             // combine the two lane halves, publish this wave's sums for row r
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb) {
                 const float x2 = __shfl_xor(X[qb], 32), y2 = __shfl_xor(Y[qb], 32),
-                            p2 = __shfl_xor(P[qb], 32);
+                            p2 = __shfl_xor(P[qb], 32), x12 = __shfl_xor(X1[qb], 32),
+                            p12 = __shfl_xor(P1[qb], 32);
                 const int q = qb * 32 + c;
                 if (g == 0 && q < Q) {
                     rs[q] = X[qb] + x2;
                     rs[Q + q] = Y[qb] + y2;
                     rs[2 * Q + q] = P[qb] + p2;
+                    rs[3 * Q + q] = X1[qb] + x12;
+                    rs[4 * Q + q] = P1[qb] + p12;
                 }
             }
-            const float R2 = __shfl_xor(R, 32);
-            if (lane == 0) rs[3 * Q] = R + R2;
+            const float R2 = __shfl_xor(R, 32), T12 = __shfl_xor(T1, 32);
+            if (lane == 0) {
+                rs[5 * Q] = R + R2;
+                rs[5 * Q + 1] = T1 + T12;
+            }
         }
         __syncthreads();
         // per-(group, row) sums over the four waves, fixed order
@@ -565,16 +688,18 @@ __global__ __launch_bounds__(kThreads) void psi2_grad_kernel(
     }
 }
 
-// Per row: X, Y, P, R summed over the task groups (fixed order), then
-//   dmu += -2 w2 P,  dS += w2^2 (X + Y) - w2 R,
-// and per block of kFinRows rows the partial sums of dl and dsf2.
+// Per row: the task groups' sums (fixed order), then with w1 = 1/(l^2 + S)
+//   dmu = -2 w2 P - w1 P1
+//   dS  = w2^2 (X + Y) - w2 R + 1/2 w1^2 X1 - 1/2 w1 T1
+// (P1 = sum_m t d, X1 = sum_m t d^2, T1 = sum_m t, t = dL/dPsi1 * Psi1), and per
+// block of kFinRows rows the partial sums of dl and dsf2.
 __global__ __launch_bounds__(256) void psi2_finalize_kernel(
     int64_t N, int Q, int groups, const float *__restrict__ rowsum,
     const float *__restrict__ w2t, const float *__restrict__ S, Hyp<float> h,
     float *__restrict__ dmu, float *__restrict__ dS, float *__restrict__ part_dl) {
     __shared__ float red[4][65];
     const int q = threadIdx.x & 63, rl = threadIdx.x >> 6;
-    const int RED = 3 * Q + 1;
+    const int RED = 5 * Q + 2;
     const int64_t n0 = (int64_t)blockIdx.x * kFinRows;
     float dl = 0.f, dsf = 0.f;
     if (q < Q) {
@@ -582,20 +707,25 @@ __global__ __launch_bounds__(256) void psi2_finalize_kernel(
         for (int k = rl; k < kFinRows; k += 4) {
             const int64_t n = n0 + k;
             if (n >= N) break;
-            float X = 0.f, Y = 0.f, P = 0.f, R = 0.f;
+            float X = 0.f, Y = 0.f, P = 0.f, X1 = 0.f, P1 = 0.f, R = 0.f, T1 = 0.f;
             for (int gi = 0; gi < groups; ++gi) {
                 const float *rs = rowsum + ((int64_t)gi * N + n) * RED;
                 X += rs[q];
                 Y += rs[Q + q];
                 P += rs[2 * Q + q];
-                R += rs[3 * Q];
+                X1 += rs[3 * Q + q];
+                P1 += rs[4 * Q + q];
+                R += rs[5 * Q];
+                T1 += rs[5 * Q + 1];
             }
             const float w2 = w2t[n * Q + q];
             const float s = S[n * Q + q];
-            dmu[n * Q + q] += -2.f * w2 * P;
-            dS[n * Q + q] += w2 * w2 * (X + Y) - w2 * R;
-            dl += (2.f * s * w2 / l) * R + l * w2 * w2 * (X + Y) + (X - Y) / (l2 * l);
-            dsf += 2.f * R;
+            const float w1 = 1.f / (l2 + s);
+            dmu[n * Q + q] = -2.f * w2 * P - w1 * P1;
+            dS[n * Q + q] = w2 * w2 * (X + Y) - w2 * R + 0.5f * w1 * (w1 * X1 - T1);
+            dl += (2.f * s * w2 / l) * R + l * w2 * w2 * (X + Y) + (X - Y) / (l2 * l) +
+                  (s * w1 / l) * T1 + l * w1 * w1 * X1;
+            dsf += 2.f * R + T1;
         }
     }
     red[rl][q] = dl;
@@ -609,26 +739,24 @@ __global__ __launch_bounds__(256) void psi2_finalize_kernel(
     }
 }
 
-// dZ, dl, dsf2 from the Psi1 partials (generic kernels) and the Psi2 partials.
-__global__ void grad_reduce_kernel(int64_t N, int M, int Q, Psi1GradParts<float> p1,
-                                   const float *__restrict__ pdz, int64_t dz_slabs,
-                                   const float *__restrict__ pdl, int64_t dl_parts,
-                                   float dL_dpsi0, float *__restrict__ dZ,
+// dZ, dl, dsf2 from the per-slab and per-block partials, fixed order.
+__global__ void grad_reduce_kernel(int64_t N, int M, int Q, const float *__restrict__ pdz,
+                                   int64_t dz_slabs, const float *__restrict__ pdl,
+                                   int64_t dl_parts, float dL_dpsi0, float *__restrict__ dZ,
                                    float *__restrict__ dsf2, float *__restrict__ dl,
                                    int accumulate) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t MQ = (int64_t)M * Q;
     if (i < MQ) {
-        float s1 = 0.f, s2 = 0.f;
-        for (int64_t ch = 0; ch < p1.ncc; ++ch) s1 += p1.colpart[ch * MQ + i];
-        for (int64_t sl = 0; sl < dz_slabs; ++sl) s2 += pdz[sl * MQ + i];
-        dZ[i] = (accumulate ? dZ[i] : 0.f) + (s1 + s2);
+        float s = 0.f;
+#pragma unroll 8
+        for (int64_t sl = 0; sl < dz_slabs; ++sl) s += pdz[sl * MQ + i];
+        dZ[i] = (accumulate ? dZ[i] : 0.f) + s;
     } else if (i < MQ + Q + 1) {
         const int k = (int)(i - MQ);
-        float s1 = 0.f, s2 = 0.f;
-        for (int64_t b = 0; b < p1.row_blocks; ++b) s1 += p1.rowpart[b * (Q + 1) + k];
-        for (int64_t b = 0; b < dl_parts; ++b) s2 += pdl[b * (Q + 1) + k];
-        float s = s1 + s2;
+        float s = 0.f;
+#pragma unroll 8
+        for (int64_t b = 0; b < dl_parts; ++b) s += pdl[b * (Q + 1) + k];
         if (k < Q) {
             dl[k] = (accumulate ? dl[k] : 0.f) + s;
         } else {
@@ -639,78 +767,93 @@ __global__ void grad_reduce_kernel(int64_t N, int M, int Q, Psi1GradParts<float>
 }
 
 // ---------------------------------------------------------------- dispatch
-template <int KS>
+template <int KS, int TPW>
 hipError_t launch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z,
-                      const float *zc, const float *sq, const float *hq, const float *hl,
-                      float *part, hipStream_t st) {
-    auto k = psi2_fwd_kernel<KS>;
+                      void *ws, hipStream_t st) {
+    auto k = psi2_fwd_kernel<KS, TPW>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_fwd);
     if (e != hipSuccess) return e;
-    dim3 grid((unsigned)p.groups, (unsigned)p.fchunks);
+    dim3 grid((unsigned)p.fgroups, (unsigned)p.fchunks);
     TimedScope ts(st, "mfma_psi2_fwd");
-    k<<<grid, kThreads, p.lds_fwd, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DS, p.T,
-                                         p.tpg, p.frows, mu, Z, zc, sq, hq, hl, part);
+    k<<<grid, kThreads, p.lds_fwd, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.T,
+                                         p.ftasks, p.frows, mu, Z, fat(ws, p.off_zc),
+                                         fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc),
+                                         fat(ws, p.off_fp));
     return hipGetLastError();
 }
 
 template <int KS, int JPW, int NQB>
 hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
-                       const float *zc, const float *sq, const float *hq, const float *hl,
-                       const float *w2, const float *G2p, const Hyp<float> &h, float *rowsum,
-                       float *pdz, hipStream_t st) {
+                       const Hyp<float> &h, void *ws, hipStream_t st) {
     auto k = psi2_grad_kernel<KS, JPW, NQB>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_grad);
     if (e != hipSuccess) return e;
     dim3 grid((unsigned)p.ggroups, (unsigned)p.gchunks);
     TimedScope ts(st, "mfma_psi2_grad");
-    k<<<grid, kThreads, p.lds_grad, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DS, p.njr,
-                                          p.ntasks, p.grows, mu, Z, zc, sq, hq, hl, w2, G2p, h,
-                                          rowsum, pdz);
+    k<<<grid, kThreads, p.lds_grad, st>>>(
+        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DS, p.njr, p.ntasks, p.grows, mu, Z,
+        fat(ws, p.off_zc), fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc),
+        fat(ws, p.off_w1), fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2), h,
+        fat(ws, p.off_rs), fat(ws, p.off_dz));
     return hipGetLastError();
 }
 
-hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z,
-                        const float *zc, const float *sq, const float *hq, const float *hl,
-                        float *part, hipStream_t st) {
-    switch (p.ks) {
-#define GPPS_F(K) \
-    case K: return launch_fwd<K>(p, s, mu, Z, zc, sq, hq, hl, part, st);
-        GPPS_F(1) GPPS_F(2) GPPS_F(3) GPPS_F(4) GPPS_F(5) GPPS_F(6) GPPS_F(8) GPPS_F(10)
-        GPPS_F(12) GPPS_F(15) GPPS_F(16) GPPS_F(24) GPPS_F(32)
+hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z, void *ws,
+                        hipStream_t st) {
+#define GPPS_F(K, T) \
+    if (p.ks == K && p.tpw == T) return launch_fwd<K, T>(p, s, mu, Z, ws, st);
+#define GPPS_F4(K) GPPS_F(K, 1) GPPS_F(K, 2) GPPS_F(K, 3) GPPS_F(K, 4)
+    GPPS_F4(1) GPPS_F4(2) GPPS_F4(3) GPPS_F4(4) GPPS_F4(5) GPPS_F4(6) GPPS_F4(8) GPPS_F4(10)
+    GPPS_F4(12) GPPS_F4(15) GPPS_F4(16) GPPS_F4(24) GPPS_F4(32)
+#undef GPPS_F4
 #undef GPPS_F
-    }
     return hipErrorInvalidValue;
 }
 
 hipError_t dispatch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
-                         const float *zc, const float *sq, const float *hq, const float *hl,
-                         const float *w2, const float *G2p, const Hyp<float> &h, float *rowsum,
-                         float *pdz, hipStream_t st) {
+                         const Hyp<float> &h, void *ws, hipStream_t st) {
 #define GPPS_G(K, J, Q)                                                                      \
-    if (p.ks == K && p.jpw == J && p.nqb == Q)                                               \
-        return launch_grad<K, J, Q>(p, s, mu, Z, zc, sq, hq, hl, w2, G2p, h, rowsum, pdz, st);
-#define GPPS_G3(K, Q) GPPS_G(K, 1, Q) GPPS_G(K, 2, Q) GPPS_G(K, 4, Q)
-    GPPS_G3(1, 1) GPPS_G3(2, 1) GPPS_G3(3, 1) GPPS_G3(4, 1) GPPS_G3(5, 1) GPPS_G3(6, 1)
-    GPPS_G3(8, 1) GPPS_G3(10, 1) GPPS_G3(12, 1) GPPS_G3(15, 1) GPPS_G3(16, 1)
-    GPPS_G3(16, 2) GPPS_G3(24, 2) GPPS_G3(32, 2)
-#undef GPPS_G3
+    if (p.ks == K && p.jpw == J && p.nqb == Q) return launch_grad<K, J, Q>(p, s, mu, Z, h, ws, st);
+#define GPPS_G2(K, Q) GPPS_G(K, 1, Q) GPPS_G(K, 2, Q)
+    GPPS_G2(1, 1) GPPS_G2(2, 1) GPPS_G2(3, 1) GPPS_G2(4, 1) GPPS_G2(5, 1) GPPS_G2(6, 1)
+    GPPS_G2(8, 1) GPPS_G2(10, 1) GPPS_G2(12, 1) GPPS_G2(15, 1) GPPS_G2(16, 1)
+    GPPS_G2(16, 2) GPPS_G2(24, 2) GPPS_G2(32, 2)
+#undef GPPS_G2
 #undef GPPS_G
     return hipErrorInvalidValue;
 }
 
-hipError_t row_tables(const MPlan &p, const Shape &s, const float *S, const float *Z,
-                      const Hyp<float> &h, void *ws, hipStream_t st) {
+// Per-row tables, the centring shift, and the row terms plus Psi1 (forward,
+// psi1 != NULL) or dL/dPsi1 * Psi1 (grad).
+void prepare(const MPlan &p, const Shape &s, const float *mu, const float *S, const float *Z,
+             const Hyp<float> &h, const float *G1, float *psi1, bool grad, void *ws,
+             hipStream_t st) {
     {
         TimedScope ts(st, "mfma_rows");
-        mfma_rows_kernel<<<(unsigned)cdiv(s.N, 256), 256, 0, st>>>(
-            s.N, (int)s.Q, S, h, fat(ws, p.off_sq), fat(ws, p.off_hq), fat(ws, p.off_w2),
-            fat(ws, p.off_hl));
+        mfma_rows_kernel<<<(unsigned)cdiv(s.N, 4), 256, 0, st>>>(
+            s.N, (int)s.Q, S, h, fat(ws, p.off_K), fat(ws, p.off_hq), fat(ws, p.off_w2),
+            fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1));
     }
-    TimedScope ts(st, "mfma_centre");
-    mfma_centre_kernel<<<1, 64, 0, st>>>((int)s.M, (int)s.Q, Z, fat(ws, p.off_zc));
-    return hipGetLastError();
+    {
+        TimedScope ts(st, "mfma_centre");
+        mfma_centre_kernel<<<1, 256, 0, st>>>((int)s.M, (int)s.Q, Z, fat(ws, p.off_zc));
+    }
+    dim3 grid((unsigned)cdiv(s.N, kRTRows), (unsigned)cdiv(p.Mp, 256));
+    float *t1 = grad ? fat(ws, p.off_t1) : nullptr;
+    TimedScope ts(st, "mfma_rowterm");
+#define GPPS_RT(QM)                                                                           \
+    mfma_rowterm_kernel<QM><<<grid, 256, 0, st>>>(                                            \
+        s.N, (int)s.M, (int)s.Q, (int)p.Mp, mu, Z, fat(ws, p.off_zc), fat(ws, p.off_K),        \
+        fat(ws, p.off_hq), fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1), G1,       \
+        fat(ws, p.off_bt), fat(ws, p.off_bc), psi1, t1)
+    if (s.Q <= 8) GPPS_RT(8);
+    else if (s.Q <= 16) GPPS_RT(16);
+    else if (s.Q <= 24) GPPS_RT(24);
+    else if (s.Q <= 32) GPPS_RT(32);
+    else GPPS_RT(64);
+#undef GPPS_RT
 }
 
 }  // namespace
@@ -728,17 +871,13 @@ hipError_t mfma_psi_stats(const Shape &s, const float *mu, const float *S, const
                           const Hyp<float> &h, float *psi0, float *Psi1, float *Psi2,
                           int accumulate, void *ws, hipStream_t st) {
     const MPlan p = make_mplan(s);
-    if (Psi1) generic_psi1_fwd<float>(s, mu, S, Z, h, Psi1, ws, st);
-    hipError_t e = row_tables(p, s, S, Z, h, ws, st);
-    if (e != hipSuccess) return e;
-    float *part = fat(ws, p.off_fp);
-    e = dispatch_fwd(p, s, mu, Z, fat(ws, p.off_zc), fat(ws, p.off_sq), fat(ws, p.off_hq),
-                     fat(ws, p.off_hl), part, st);
+    prepare(p, s, mu, S, Z, h, nullptr, Psi1, false, ws, st);
+    hipError_t e = dispatch_fwd(p, s, mu, Z, ws, st);
     if (e != hipSuccess) return e;
     dim3 g((unsigned)cdiv(s.M, 16), (unsigned)cdiv(s.M, 16));
     TimedScope ts(st, "mfma_psi2_reduce");
-    psi2_reduce_kernel<<<g, 256, 0, st>>>(s.N, (int)s.M, p.nb, p.T, p.fchunks, part, h.sf2, psi0,
-                                          Psi2, accumulate);
+    psi2_reduce_kernel<<<g, 256, 0, st>>>(s.N, (int)s.M, p.nb, p.T, p.fchunks, fat(ws, p.off_fp),
+                                          h.sf2, psi0, Psi2, accumulate);
     return hipGetLastError();
 }
 
@@ -747,31 +886,26 @@ hipError_t mfma_psi_grads(const Shape &s, const float *mu, const float *S, const
                           const float *G2, float *dmu, float *dS, float *dZ, float *dsf2,
                           float *dl, int accumulate, void *ws, hipStream_t st) {
     const MPlan p = make_mplan(s);
-    // Psi1 terms first: they overwrite dmu and dS, the Psi2 kernel adds to them.
-    const Psi1GradParts<float> p1 = generic_psi1_grads<float>(s, mu, S, Z, h, G1, dmu, dS, ws, st);
-    float *pdz = fat(ws, p.off_dz), *pdl = fat(ws, p.off_dl);
-    if (G2) {
-        hipError_t e = row_tables(p, s, S, Z, h, ws, st);
-        if (e != hipSuccess) return e;
-        float *G2p = fat(ws, p.off_g2);
-        {
-            TimedScope ts(st, "mfma_sym");
-            mfma_sym_kernel<<<(unsigned)cdiv(p.Mp * p.Mp, 256), 256, 0, st>>>((int)s.M, (int)p.Mp,
-                                                                              G2, G2p);
-        }
-        float *rowsum = fat(ws, p.off_rs);
-        e = dispatch_grad(p, s, mu, Z, fat(ws, p.off_zc), fat(ws, p.off_sq), fat(ws, p.off_hq),
-                          fat(ws, p.off_hl), fat(ws, p.off_w2), G2p, h, rowsum, pdz, st);
-        if (e != hipSuccess) return e;
+    prepare(p, s, mu, S, Z, h, G1, nullptr, true, ws, st);
+    {
+        // NULL dL/dPsi2 means zero: the kernel then adds only the Psi1 terms
+        TimedScope ts(st, "mfma_sym");
+        mfma_sym_kernel<<<(unsigned)cdiv(p.Mp * p.Mp, 256), 256, 0, st>>>((int)s.M, (int)p.Mp, G2,
+                                                                          fat(ws, p.off_g2));
+    }
+    hipError_t e = dispatch_grad(p, s, mu, Z, h, ws, st);
+    if (e != hipSuccess) return e;
+    {
         TimedScope ts(st, "mfma_psi2_finalize");
         psi2_finalize_kernel<<<(unsigned)p.fin_blocks, 256, 0, st>>>(
-            s.N, (int)s.Q, (int)p.ggroups, rowsum, fat(ws, p.off_w2), S, h, dmu, dS, pdl);
+            s.N, (int)s.Q, (int)p.ggroups, fat(ws, p.off_rs), fat(ws, p.off_w2), S, h, dmu, dS,
+            fat(ws, p.off_dl));
     }
     const int64_t total = s.M * s.Q + s.Q + 1;
     TimedScope ts(st, "mfma_grad_reduce");
     grad_reduce_kernel<<<(unsigned)cdiv(total, 256), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, p1, pdz, G2 ? p.gchunks * p.njr : 0, pdl,
-        G2 ? p.fin_blocks : 0, dL_dpsi0, dZ, dsf2, dl, accumulate);
+        s.N, (int)s.M, (int)s.Q, fat(ws, p.off_dz), p.gchunks * p.njr, fat(ws, p.off_dl),
+        p.fin_blocks, dL_dpsi0, dZ, dsf2, dl, accumulate);
     return hipGetLastError();
 }
 

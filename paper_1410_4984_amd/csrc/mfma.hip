@@ -69,6 +69,8 @@ constexpr int64_t kFwdTargetWGs = 1024;
 constexpr int64_t kGradTargetWGs = 512;
 constexpr int kFinRows = 64;           // rows per block of the gradient finalize kernel
 constexpr int kRTRows = 32;            // rows per block of the row-term kernel
+constexpr int kGradWaves = 8;          // gradient: waves per workgroup (one row block each)
+constexpr int kJPW = 2;                // gradient: column blocks per wave task
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -110,8 +112,9 @@ struct MPlan {
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
     int64_t frows, fchunks;
-    int jpw, njr, ntasks;  // gradient: column blocks per wave task, ranges, tasks (nb * njr)
-    int64_t ggroups;       // gradient: workgroups per row chunk
+    int jpw, njr;          // gradient: column blocks per wave task, column-block ranges
+    int wpg, igroups;      // gradient: waves per workgroup (one row block each), row-block groups
+    int64_t ggroups;       // gradient: workgroups per row chunk (njr * igroups)
     int64_t grows, gchunks;
     int64_t fin_blocks;    // finalize: blocks of kFinRows rows
     size_t lds_fwd, lds_grad;
@@ -163,6 +166,34 @@ __host__ __device__ inline Lds lds_layout(int Mp, int DS, int Q, bool grad) {
     return L;
 }
 
+// Gradient LDS layout (floats):
+//   zx  [Mp][DSF]       centred z (fp32): Gram operand (rows m') and epilogue (rows m)
+//   zb  [kJPW][3][2][2][32 nqb][8] bf16   the workgroup's column blocks of [Z | 1] split
+//                       into three bf16 parts, laid out as the B operands of the
+//                       32x32x16 bf16 MFMA (8 consecutive k per lane and instruction)
+//   bb, bcb [RB][Mp], mub, kb [RB][64], w1b, w2b [RB][Q], t1 [RB][Mp],
+//   red [RB][wpg][5Q + 2]
+struct LdsG {
+    int zx, zb, bb, bcb, mub, kb, w1b, w2b, t1, red, total;
+};
+
+__host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb, int wpg) {
+    LdsG L{};
+    int o = 0;
+    L.zx = o; o += (Mp * DSF + 3) / 4 * 4;
+    L.zb = o; o += kJPW * 3 * 2 * 2 * 32 * nqb * 8 / 2;
+    L.bb = o; o += kRB * Mp;
+    L.bcb = o; o += kRB * Mp;
+    L.mub = o; o += kRB * kRowStride;
+    L.kb = o; o += kRB * kRowStride;
+    L.w1b = o; o += kRB * Q;
+    L.w2b = o; o += kRB * Q;
+    L.t1 = o; o += kRB * Mp;
+    L.red = o; o += kRB * wpg * (5 * Q + 2);
+    L.total = o;
+    return L;
+}
+
 MPlan make_mplan(const Shape &s) {
     MPlan p{};
     p.Mp = cdiv(s.M, kTile) * kTile;
@@ -184,16 +215,21 @@ MPlan make_mplan(const Shape &s) {
     p.fchunks = std::max<int64_t>(1, std::min(cdiv(kFwdTargetWGs, p.fgroups), cdiv(s.N, 32)));
     p.frows = cdiv(s.N, p.fchunks);
     p.fchunks = cdiv(s.N, p.frows);
-    p.jpw = p.nb >= 2 ? 2 : 1;   // 2: the task fits 2 waves per SIMD
+    p.jpw = 2;
     p.njr = (int)cdiv(p.nb, p.jpw);
-    p.ntasks = p.nb * p.njr;
-    p.ggroups = cdiv(p.ntasks, kWaves);
+    // widest workgroup whose LDS fits
+    p.wpg = std::min(p.nb, kGradWaves);
+    while (p.wpg > 1 && sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb,
+                                                        p.wpg).total > 160 * 1024)
+        p.wpg /= 2;
+    p.igroups = (int)cdiv(p.nb, p.wpg);
+    p.ggroups = (int64_t)p.njr * p.igroups;
     p.gchunks = std::max<int64_t>(1, std::min(cdiv(kGradTargetWGs, p.ggroups), cdiv(s.N, 16)));
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
     p.fin_blocks = cdiv(s.N, kFinRows);
     p.lds_fwd = sizeof(float) * lds_layout((int)p.Mp, p.DSF, (int)s.Q, false).total;
-    p.lds_grad = sizeof(float) * lds_layout((int)p.Mp, p.DS, (int)s.Q, true).total;
+    p.lds_grad = sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.wpg).total;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_K = take(sizeof(float) * s.N * kRowStride);
@@ -497,42 +533,91 @@ __global__ void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T, int64_t 
 }
 
 // ---------------------------------------------------------------- Psi2 gradient
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef unsigned int u32;
+constexpr u32 kHi16 = 0xFFFF0000u;
+
+// Three bf16 parts of x (truncation split): x == p0 + p1 + p2 up to 2^-24 |x|.
+// Each part is returned as an fp32 bit pattern whose low 16 bits are zero.
+__device__ __forceinline__ void split3(float x, u32 &p0, u32 &p1, u32 &p2) {
+    p0 = __float_as_uint(x) & kHi16;
+    const float r = x - __uint_as_float(p0);
+    p1 = __float_as_uint(r) & kHi16;
+    p2 = __float_as_uint(r - __uint_as_float(p1));
+}
+
+// Pack the high halves of two fp32 bit patterns into one bf16 pair (a: element 0).
+__device__ __forceinline__ u32 pack_hi(u32 a, u32 b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+
+// The workgroup's kJPW column blocks of [Z | 1] as three bf16 parts, in the B
+// operand order of the 32x32x16 bf16 MFMA: for instruction h and lane group g
+// the 8 k-values are the rows crow(8h + e, g), e = 0..7, of the block.
+__device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
+                         const float *__restrict__ Z, const float *__restrict__ zc) {
+    const int QV = 32 * nqb;
+    const int total = kJPW * 3 * 2 * 2 * QV * 8;
+    for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
+        int r = idx;
+        const int e = r % 8; r /= 8;
+        const int q = r % QV; r /= QV;
+        const int gg = r % 2; r /= 2;
+        const int h = r % 2; r /= 2;
+        const int part = r % 3; r /= 3;
+        const int k = r;
+        const int m = (jr * kJPW + k) * kTile + crow(8 * h + e, gg);
+        float v = 0.f;
+        if (m < M) {
+            if (q < Q) v = Z[(int64_t)m * Q + q] - zc[q];
+            else if (q == Q) v = 1.f;
+        }
+        u32 p0, p1, p2;
+        split3(v, p0, p1, p2);
+        const u32 pv = part == 0 ? p0 : (part == 1 ? p1 : p2);
+        zb[idx] = (unsigned short)(pv >> 16);
+    }
+}
+
 // Every gradient term is linear in (r_n, V_n), so the M x M tile grid may be
-// split freely: a wave task is one row block i (the m index of W) and JPW
-// column blocks j (the m' index).  Tile (j, i), rows m' in block j, columns m
-// in block i:  e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)   (A: z, B: -K d).
-// The task's dL/dPsi2 tiles stay in registers for the whole kernel; V' = W [Z | 1]
-// accumulates over the task's tiles; the epilogue turns it into the task's
-// share of dZ (registers) and of the per-row sums, which the workgroup
-// combines in LDS and writes per (group, row) for psi2_finalize_kernel.
-template <int KS, int JPW, int NQB>
-__global__ __launch_bounds__(kThreads, NQB == 1 ? 2 : 1) void psi2_grad_kernel(
-    int64_t N, int M, int Q, int Mp, int nb, int DS, int njr, int ntasks,
+// split freely.  Wave task: row block i (the m index of W) and the kJPW column
+// blocks j (the m' index) of the workgroup's range jr.  Tile (j, i), rows m' in
+// block j, columns m in block i:
+//   e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)       (fp32 MFMA; A: z, B: -K d)
+// W = G2s o exp2(e); then V' += W [Z | 1] on bf16 MFMAs with both operands split
+// into three bf16 parts (six cross products; the dropped ones are below 2^-24
+// relative), which keeps fp32 accuracy.  The task's dL/dPsi2 tiles stay in
+// registers for the whole kernel; the epilogue turns V' into the task's share
+// of dZ (registers) and of the per-row sums, which the workgroup combines in LDS
+// and writes per (group, row) for psi2_finalize_kernel.
+template <int KS, int NQB>
+__global__ __launch_bounds__(kGradWaves * 64) void psi2_grad_kernel(
+    int64_t N, int M, int Q, int Mp, int nb, int DSF, int njr, int wpg, int igroups,
     int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
     const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ bt,
     const float *__restrict__ bc, const float *__restrict__ w1t, const float *__restrict__ w2t,
     const float *__restrict__ t1g, const float *__restrict__ G2p, Hyp<float> h,
     float *__restrict__ rowsum, float *__restrict__ part_dz) {
     extern __shared__ float lds[];
-    const Lds L = lds_layout(Mp, DS, Q, true);
+    const LdsG L = lds_grad_layout(Mp, DSF, Q, NQB, wpg);
+    unsigned short *zb = reinterpret_cast<unsigned short *>(lds + L.zb);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
     const int ones_src = 32 * g + (Q & 31);    // lane holding column Q (the row sums r)
     const int ones_qb = Q >> 5;
     const int RED = 5 * Q + 2;                 // X, Y, P, X1, P1 per dimension, then R, T1
+    const int QV = 32 * NQB;
     const int group = blockIdx.x;
-    const int task = group * kWaves + wave;
-    const bool active = task < ntasks;         // wave-uniform
-    const int i = active ? task / njr : 0;     // row block of W (m)
-    const int jr = active ? task % njr : 0;    // range of column blocks of W (m')
+    const int jr = group / igroups;            // range of column blocks of W (m')
+    const int i0 = (group % igroups) * wpg + wave;
+    const bool active = i0 < nb;               // wave-uniform
+    const int i = active ? i0 : 0;             // row block of W (m)
     const bool has1 = active && jr == 0;       // this task also adds the Psi1 terms of block i
 
     // dL/dPsi2 tiles of the task (zero for column blocks past the edge)
-    int jb[JPW];
-    float g2r[JPW][16];
+    int jb[kJPW];
+    float g2r[kJPW][16];
 #pragma unroll
-    for (int k = 0; k < JPW; ++k) {
-        const int j = jr * JPW + k;
+    for (int k = 0; k < kJPW; ++k) {
+        const int j = jr * kJPW + k;
         const bool ok = active && j < nb;
         jb[k] = ok ? j : nb - 1;
         const float *g2 = G2p + (int64_t)jb[k] * kTile * Mp + i * kTile + c;
@@ -551,16 +636,38 @@ __global__ __launch_bounds__(kThreads, NQB == 1 ? 2 : 1) void psi2_grad_kernel(
         il2[qb] = q < Q ? 1.f / h.l2[q] : 0.f;
     }
 
-    stage_z(lds, L, M, Mp, Q, DS, Z, zc);
+    // constant tables: centred z (fp32) and the split [Z | 1] column blocks
+    for (int k = threadIdx.x; k < Mp * DSF; k += blockDim.x) {
+        const int m = k / DSF, q = k - m * DSF;
+        lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+    }
+    stage_zb(zb, jr, M, Q, NQB, Z, zc);
+
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
     for (int64_t n0 = r0; n0 < r1; n0 += kRB) {
         const int cb = (int)min<int64_t>(kRB, r1 - n0);
         __syncthreads();
-        stage_batch<true>(lds, L, n0, cb, Mp, Q, mu, zc, Kt, bt, bc, w1t, w2t, t1g);
+        for (int k = threadIdx.x; k < kRB * kRowStride; k += blockDim.x) {
+            const int r = k / kRowStride, q = k - r * kRowStride;
+            const bool ok = r < cb && q < Q;
+            lds[L.mub + k] = ok ? mu[(n0 + r) * Q + q] - zc[q] : 0.f;
+            lds[L.kb + k] = ok ? Kt[(n0 + r) * kRowStride + q] : 0.f;
+        }
+        for (int k = threadIdx.x; k < kRB * Mp; k += blockDim.x) {
+            const bool ok = k < cb * Mp;
+            lds[L.bb + k] = ok ? bt[n0 * Mp + k] : kPadBias;
+            lds[L.bcb + k] = ok ? bc[n0 * Mp + k] : kPadBias;
+            lds[L.t1 + k] = ok ? t1g[n0 * Mp + k] : 0.f;
+        }
+        for (int k = threadIdx.x; k < kRB * Q; k += blockDim.x) {
+            const bool ok = k < cb * Q;
+            lds[L.w1b + k] = ok ? w1t[n0 * Q + k] : 0.f;
+            lds[L.w2b + k] = ok ? w2t[n0 * Q + k] : 0.f;
+        }
         __syncthreads();
         for (int r = 0; r < cb; ++r) {
-            float *rs = lds + L.red + (r * kWaves + wave) * RED;
+            float *rs = lds + L.red + (r * wpg + wave) * RED;
             if (!active) {
                 for (int k = lane; k < RED; k += 64) rs[k] = 0.f;
                 continue;
@@ -573,7 +680,7 @@ __global__ __launch_bounds__(kThreads, NQB == 1 ? 2 : 1) void psi2_grad_kernel(
             }
             // Gram B operand: -K d for column block i (the m index of W)
             float bop[KS];
-            kd_operands<KS>(lds + L.zx, DS, i, c, g, muk, kk, bop);
+            kd_operands<KS>(lds + L.zx, DSF, i, c, g, muk, kk, bop);
             const float bcol = lds[L.bcb + r * Mp + i * kTile + c];
             const float *bbr = lds + L.bb + r * Mp;
             v16f V[NQB];
@@ -582,23 +689,50 @@ __global__ __launch_bounds__(kThreads, NQB == 1 ? 2 : 1) void psi2_grad_kernel(
 #pragma unroll
                 for (int t = 0; t < 16; ++t) V[qb][t] = 0.f;
 #pragma unroll
-            for (int k = 0; k < JPW; ++k) {
+            for (int k = 0; k < kJPW; ++k) {
                 const int j = jb[k];
-                const float *zr = lds + L.zx + (j * kTile + c) * DS + g;
+                const float *zr = lds + L.zx + (j * kTile + c) * DSF + g;
                 v16f e;
 #pragma unroll
                 for (int t = 0; t < 16; ++t) e[t] = bbr[j * kTile + crow(t, g)] + bcol;
 #pragma unroll
                 for (int s = 0; s < KS; ++s)
                     e = __builtin_amdgcn_mfma_f32_32x32x2f32(zr[2 * s], bop[s], e, 0, 0, 0);
-                const float *zrow = lds + L.zx + j * kTile * DS + c;
+                // W tile, split into three bf16 parts; A operand of instruction hh takes
+                // the lane's rows crow(8 hh + e, g), as the B operand tables do
+                u32 wp[3][16];
 #pragma unroll
-                for (int t = 0; t < 16; ++t) {
-                    const float w = g2r[k][t] * __builtin_amdgcn_exp2f(e[t]);
+                for (int t = 0; t < 16; ++t)
+                    split3(g2r[k][t] * __builtin_amdgcn_exp2f(e[t]), wp[0][t], wp[1][t], wp[2][t]);
+                v8bf A[3][2];
 #pragma unroll
-                    for (int qb = 0; qb < NQB; ++qb)
-                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            w, zrow[crow(t, g) * DS + qb * 32], V[qb], 0, 0, 0);
+                for (int pa = 0; pa < 3; ++pa)
+#pragma unroll
+                    for (int hh = 0; hh < 2; ++hh) {
+                        u32 d4[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u)
+                            d4[u] = pack_hi(wp[pa][8 * hh + 2 * u], wp[pa][8 * hh + 2 * u + 1]);
+                        A[pa][hh] = __builtin_bit_cast(v8bf, d4);
+                    }
+#pragma unroll
+                for (int qb = 0; qb < NQB; ++qb) {
+#pragma unroll
+                    for (int hh = 0; hh < 2; ++hh) {
+                        v8bf B[3];
+#pragma unroll
+                        for (int pb = 0; pb < 3; ++pb) {
+                            const unsigned short *src =
+                                zb + ((((k * 3 + pb) * 2 + hh) * 2 + g) * QV + qb * 32 + c) * 8;
+                            B[pb] = *reinterpret_cast<const v8bf *>(src);
+                        }
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[0], V[qb], 0, 0, 0);
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[1], V[qb], 0, 0, 0);
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[1][hh], B[0], V[qb], 0, 0, 0);
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[2], V[qb], 0, 0, 0);
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[1][hh], B[1], V[qb], 0, 0, 0);
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[2][hh], B[0], V[qb], 0, 0, 0);
+                    }
                 }
             }
             // epilogue for rows m = i*32 + crow(t, g); V' = W [Z | 1] -> V = r mu^T - V'
@@ -615,7 +749,7 @@ __global__ __launch_bounds__(kThreads, NQB == 1 ? 2 : 1) void psi2_grad_kernel(
             float X[NQB], Y[NQB], P[NQB], X1[NQB], P1[NQB], R = 0.f, T1 = 0.f;
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb) X[qb] = Y[qb] = P[qb] = X1[qb] = P1[qb] = 0.f;
-            const float *zblk = lds + L.zx + i * kTile * DS;
+            const float *zblk = lds + L.zx + i * kTile * DSF;
             const float *t1r = lds + L.t1 + r * Mp + i * kTile;
 #pragma unroll
             for (int t = 0; t < 16; ++t) {
@@ -623,20 +757,34 @@ __global__ __launch_bounds__(kThreads, NQB == 1 ? 2 : 1) void psi2_grad_kernel(
                 const float rt = __int_as_float(__builtin_amdgcn_ds_bpermute(
                     ones_src * 4, __float_as_int(ones_qb == 0 ? V[0][t] : V[NQB - 1][t])));
                 R += rt;
-                const float tv = has1 ? t1r[rr] : 0.f;
-                T1 += tv;
 #pragma unroll
                 for (int qb = 0; qb < NQB; ++qb) {
-                    const float d = muq[qb] - zblk[rr * DS + qb * 32 + c];
+                    const int q = qb * 32 + c;
+                    const float d = muq[qb] - (q < DSF ? zblk[rr * DSF + q] : 0.f);
                     const float v = fmaf(rt, muq[qb], -V[qb][t]);
                     const float dr = d * rt;
-                    const float td = tv * d;
-                    dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, fmaf(td, w1q[qb], dz[qb][t])));
+                    dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, dz[qb][t]));
                     X[qb] = fmaf(dr, d, X[qb]);
                     P[qb] += dr;
                     Y[qb] = fmaf(d, v, Y[qb]);
-                    X1[qb] = fmaf(td, d, X1[qb]);
-                    P1[qb] += td;
+                }
+            }
+            if (has1) {
+                // Psi1 terms of (n, m), t = dL/dPsi1 * Psi1, for the rows of block i
+#pragma unroll
+                for (int t = 0; t < 16; ++t) {
+                    const int rr = crow(t, g);
+                    const float tv = t1r[rr];
+                    T1 += tv;
+#pragma unroll
+                    for (int qb = 0; qb < NQB; ++qb) {
+                        const int q = qb * 32 + c;
+                        const float d = muq[qb] - (q < DSF ? zblk[rr * DSF + q] : 0.f);
+                        const float td = tv * d;
+                        dz[qb][t] = fmaf(td, w1q[qb], dz[qb][t]);
+                        X1[qb] = fmaf(td, d, X1[qb]);
+                        P1[qb] += td;
+                    }
                 }
             }
             // combine the two lane halves, publish this wave's sums for row r
@@ -661,13 +809,12 @@ __global__ __launch_bounds__(kThreads, NQB == 1 ? 2 : 1) void psi2_grad_kernel(
             }
         }
         __syncthreads();
-        // per-(group, row) sums over the four waves, fixed order
-        for (int k = threadIdx.x; k < cb * RED; k += kThreads) {
+        // per-(group, row) sums over the waves, fixed order
+        for (int k = threadIdx.x; k < cb * RED; k += blockDim.x) {
             const int r = k / RED, e = k - r * RED;
-            const float *rs = lds + L.red + r * kWaves * RED + e;
+            const float *rs = lds + L.red + r * wpg * RED + e;
             float v = 0.f;
-#pragma unroll
-            for (int w = 0; w < kWaves; ++w) v += rs[w * RED];
+            for (int w = 0; w < wpg; ++w) v += rs[w * RED];
             rowsum[((int64_t)group * N + n0 + r) * RED + e] = v;
         }
     }
@@ -783,17 +930,17 @@ hipError_t launch_fwd(const MPlan &p, const Shape &s, const float *mu, const flo
     return hipGetLastError();
 }
 
-template <int KS, int JPW, int NQB>
+template <int KS, int NQB>
 hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                        const Hyp<float> &h, void *ws, hipStream_t st) {
-    auto k = psi2_grad_kernel<KS, JPW, NQB>;
+    auto k = psi2_grad_kernel<KS, NQB>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_grad);
     if (e != hipSuccess) return e;
     dim3 grid((unsigned)p.ggroups, (unsigned)p.gchunks);
     TimedScope ts(st, "mfma_psi2_grad");
-    k<<<grid, kThreads, p.lds_grad, st>>>(
-        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DS, p.njr, p.ntasks, p.grows, mu, Z,
+    k<<<grid, p.wpg * 64, p.lds_grad, st>>>(
+        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.njr, p.wpg, p.igroups, p.grows, mu, Z,
         fat(ws, p.off_zc), fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc),
         fat(ws, p.off_w1), fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2), h,
         fat(ws, p.off_rs), fat(ws, p.off_dz));
@@ -814,13 +961,11 @@ hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const f
 
 hipError_t dispatch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                          const Hyp<float> &h, void *ws, hipStream_t st) {
-#define GPPS_G(K, J, Q)                                                                      \
-    if (p.ks == K && p.jpw == J && p.nqb == Q) return launch_grad<K, J, Q>(p, s, mu, Z, h, ws, st);
-#define GPPS_G2(K, Q) GPPS_G(K, 1, Q) GPPS_G(K, 2, Q)
-    GPPS_G2(1, 1) GPPS_G2(2, 1) GPPS_G2(3, 1) GPPS_G2(4, 1) GPPS_G2(5, 1) GPPS_G2(6, 1)
-    GPPS_G2(8, 1) GPPS_G2(10, 1) GPPS_G2(12, 1) GPPS_G2(15, 1) GPPS_G2(16, 1)
-    GPPS_G2(16, 2) GPPS_G2(24, 2) GPPS_G2(32, 2)
-#undef GPPS_G2
+#define GPPS_G(K, Q) \
+    if (p.ks == K && p.nqb == Q) return launch_grad<K, Q>(p, s, mu, Z, h, ws, st);
+    GPPS_G(1, 1) GPPS_G(2, 1) GPPS_G(3, 1) GPPS_G(4, 1) GPPS_G(5, 1) GPPS_G(6, 1) GPPS_G(8, 1)
+    GPPS_G(10, 1) GPPS_G(12, 1) GPPS_G(15, 1) GPPS_G(16, 1) GPPS_G(16, 2) GPPS_G(24, 2)
+    GPPS_G(32, 2)
 #undef GPPS_G
     return hipErrorInvalidValue;
 }

@@ -69,8 +69,11 @@ constexpr int64_t kFwdTargetWGs = 1024;
 constexpr int64_t kGradTargetWGs = 512;
 constexpr int kFinRows = 64;           // rows per block of the gradient finalize kernel
 constexpr int kRTRows = 32;            // rows per block of the row-term kernel
-constexpr int kGradWaves = 8;          // gradient: waves per workgroup (one row block each)
-constexpr int kJPW = 2;                // gradient: column blocks per wave task
+// gradient: column blocks per wave task (the dL/dPsi2 tiles it holds in registers)
+constexpr int grad_jpw(int nqb) { return nqb == 1 ? 4 : 2; }
+// gradient: most waves per workgroup (one row block each); with two q-blocks
+// a wave needs more than 256 registers, so only one wave per SIMD
+constexpr int grad_waves(int nqb) { return nqb == 1 ? 8 : 4; }
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -168,7 +171,7 @@ __host__ __device__ inline Lds lds_layout(int Mp, int DS, int Q, bool grad) {
 
 // Gradient LDS layout (floats):
 //   zx  [Mp][DSF]       centred z (fp32): Gram operand (rows m') and epilogue (rows m)
-//   zb  [kJPW][3][2][2][32 nqb][8] bf16   the workgroup's column blocks of [Z | 1] split
+//   zb  [jpw][3][2][2][32 nqb][8] bf16   the workgroup's column blocks of [Z | 1] split
 //                       into three bf16 parts, laid out as the B operands of the
 //                       32x32x16 bf16 MFMA (8 consecutive k per lane and instruction)
 //   bb, bcb [RB][Mp], mub, kb [RB][64], w1b, w2b [RB][Q], t1 [RB][Mp],
@@ -178,10 +181,11 @@ struct LdsG {
 };
 
 __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb, int wpg) {
+    const int jpw = grad_jpw(nqb);
     LdsG L{};
     int o = 0;
     L.zx = o; o += (Mp * DSF + 3) / 4 * 4;
-    L.zb = o; o += kJPW * 3 * 2 * 2 * 32 * nqb * 8 / 2;
+    L.zb = o; o += jpw * 3 * 2 * 2 * 32 * nqb * 8 / 2;
     L.bb = o; o += kRB * Mp;
     L.bcb = o; o += kRB * Mp;
     L.mub = o; o += kRB * kRowStride;
@@ -215,10 +219,10 @@ MPlan make_mplan(const Shape &s) {
     p.fchunks = std::max<int64_t>(1, std::min(cdiv(kFwdTargetWGs, p.fgroups), cdiv(s.N, 32)));
     p.frows = cdiv(s.N, p.fchunks);
     p.fchunks = cdiv(s.N, p.frows);
-    p.jpw = 2;
+    p.jpw = grad_jpw(p.nqb);
     p.njr = (int)cdiv(p.nb, p.jpw);
     // widest workgroup whose LDS fits
-    p.wpg = std::min(p.nb, kGradWaves);
+    p.wpg = std::min(p.nb, grad_waves(p.nqb));
     while (p.wpg > 1 && sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb,
                                                         p.wpg).total > 160 * 1024)
         p.wpg /= 2;
@@ -549,13 +553,14 @@ __device__ __forceinline__ void split3(float x, u32 &p0, u32 &p1, u32 &p2) {
 // Pack the high halves of two fp32 bit patterns into one bf16 pair (a: element 0).
 __device__ __forceinline__ u32 pack_hi(u32 a, u32 b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
 
-// The workgroup's kJPW column blocks of [Z | 1] as three bf16 parts, in the B
+// The workgroup's JPW column blocks of [Z | 1] as three bf16 parts, in the B
 // operand order of the 32x32x16 bf16 MFMA: for instruction h and lane group g
 // the 8 k-values are the rows crow(8h + e, g), e = 0..7, of the block.
+template <int JPW>
 __device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
                          const float *__restrict__ Z, const float *__restrict__ zc) {
     const int QV = 32 * nqb;
-    const int total = kJPW * 3 * 2 * 2 * QV * 8;
+    const int total = JPW * 3 * 2 * 2 * QV * 8;
     for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
         int r = idx;
         const int e = r % 8; r /= 8;
@@ -564,7 +569,7 @@ __device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
         const int h = r % 2; r /= 2;
         const int part = r % 3; r /= 3;
         const int k = r;
-        const int m = (jr * kJPW + k) * kTile + crow(8 * h + e, gg);
+        const int m = (jr * JPW + k) * kTile + crow(8 * h + e, gg);
         float v = 0.f;
         if (m < M) {
             if (q < Q) v = Z[(int64_t)m * Q + q] - zc[q];
@@ -578,7 +583,7 @@ __device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
 }
 
 // Every gradient term is linear in (r_n, V_n), so the M x M tile grid may be
-// split freely.  Wave task: row block i (the m index of W) and the kJPW column
+// split freely.  Wave task: row block i (the m index of W) and the JPW column
 // blocks j (the m' index) of the workgroup's range jr.  Tile (j, i), rows m' in
 // block j, columns m in block i:
 //   e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)       (fp32 MFMA; A: z, B: -K d)
@@ -588,8 +593,8 @@ __device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
 // registers for the whole kernel; the epilogue turns V' into the task's share
 // of dZ (registers) and of the per-row sums, which the workgroup combines in LDS
 // and writes per (group, row) for psi2_finalize_kernel.
-template <int KS, int NQB>
-__global__ __launch_bounds__(kGradWaves * 64) void psi2_grad_kernel(
+template <int KS, int NQB, int JPW = grad_jpw(NQB)>
+__global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int DSF, int njr, int wpg, int igroups,
     int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
     const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ bt,
@@ -613,11 +618,11 @@ __global__ __launch_bounds__(kGradWaves * 64) void psi2_grad_kernel(
     const bool has1 = active && jr == 0;       // this task also adds the Psi1 terms of block i
 
     // dL/dPsi2 tiles of the task (zero for column blocks past the edge)
-    int jb[kJPW];
-    float g2r[kJPW][16];
+    int jb[JPW];
+    float g2r[JPW][16];
 #pragma unroll
-    for (int k = 0; k < kJPW; ++k) {
-        const int j = jr * kJPW + k;
+    for (int k = 0; k < JPW; ++k) {
+        const int j = jr * JPW + k;
         const bool ok = active && j < nb;
         jb[k] = ok ? j : nb - 1;
         const float *g2 = G2p + (int64_t)jb[k] * kTile * Mp + i * kTile + c;
@@ -641,7 +646,7 @@ __global__ __launch_bounds__(kGradWaves * 64) void psi2_grad_kernel(
         const int m = k / DSF, q = k - m * DSF;
         lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
     }
-    stage_zb(zb, jr, M, Q, NQB, Z, zc);
+    stage_zb<JPW>(zb, jr, M, Q, NQB, Z, zc);
 
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
@@ -689,7 +694,7 @@ __global__ __launch_bounds__(kGradWaves * 64) void psi2_grad_kernel(
 #pragma unroll
                 for (int t = 0; t < 16; ++t) V[qb][t] = 0.f;
 #pragma unroll
-            for (int k = 0; k < kJPW; ++k) {
+            for (int k = 0; k < JPW; ++k) {
                 const int j = jb[k];
                 const float *zr = lds + L.zx + (j * kTile + c) * DSF + g;
                 v16f e;

@@ -64,7 +64,10 @@ constexpr int kWaves = 4;
 constexpr int kRowStride = 64;         // stride of per-row tables padded to 64 dimensions
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kPadBias = -1.0e30f;   // row term of a padded inducing input: exp2 -> 0
-constexpr int kRB = 8;                 // rows per batch (both kernels)
+constexpr int kRB = 8;                 // gradient: rows per batch
+constexpr int kFRB = 4;                // forward: rows per batch (prefetched a batch ahead)
+constexpr int kFPF = kFRB * 512 / 256; // forward: per-thread prefetch slots of a [kFRB][Mp] table
+static_assert(kFRB * kRowStride == kThreads, "one mu / kappa value per forward thread");
 constexpr int64_t kFwdTargetWGs = 1024;
 constexpr int64_t kGradTargetWGs = 512;
 constexpr int kFinRows = 64;           // rows per block of the gradient finalize kernel
@@ -98,6 +101,10 @@ __device__ inline void fwd_task(int task, int nb, int tpw, int &ti, int &tj0) {
     tj0 = ti + task * tpw;
 }
 
+// Widest forward task (tiles per wave) whose registers fit two waves per SIMD
+// without spilling, for ni 16-dimension steps.
+constexpr int fwd_tpw_max(int ni) { return ni == 1 ? 4 : (ni == 2 ? 2 : 1); }
+
 // Upper-triangular tile index of (ti, tj), row-major.
 __host__ __device__ inline int64_t tile_index(int ti, int tj, int nb) {
     return (int64_t)ti * nb - (int64_t)ti * (ti - 1) / 2 + (tj - ti);
@@ -110,7 +117,8 @@ struct MPlan {
     int DS;                // gradient: LDS row stride of the z table (odd: conflict-free
                            // column reads; 32 * nqb + 1 columns for the [Z | 1] product)
     int DSF;               // forward: the same for the Gram operand only (>= 2 ks, odd)
-    int ks;                // MFMA k-steps (2 latent dimensions each), instantiated value
+    int ks;                // gradient Gram: MFMA k-steps (2 latent dimensions each)
+    int ni;                // forward Gram: 16-dimension bf16 MFMA steps (ceil(Q / 16))
     int64_t T;             // upper-triangular tiles
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
@@ -138,33 +146,26 @@ int round_ks(int ks, int nqb) {
     return -1;
 }
 
-// LDS layout (floats), shared by both kernels:
-//   Zx  [Mp][DS]        centred z, column Q = 1 for real rows, zero padding
-//   bb  [RB][Mp]        row terms b of the batch (log2 units)
-//   bcb [RB][Mp]        b + c
-//   mub [RB][64]        centred mu of the batch (zero beyond Q)
-//   Kb  [RB][64]        log2e kappa of the batch (zero beyond Q)
-// gradient only:
-//   w1b [RB][Q], w2b [RB][Q], t1 [RB][Mp] (dL/dPsi1 * Psi1), red [RB][kWaves][5Q + 2]
-struct Lds {
-    int zx, bb, bcb, mub, kb, w1b, w2b, t1, red, total;
+// Forward LDS layout (floats):
+//   zt  [nb][3][ni][2][32][8] bf16  centred z split into three bf16 parts, in the
+//                       B operand order of the 32x32x16 bf16 MFMA: column block,
+//                       part, instruction, lane group, column, 8 consecutive k
+//   bb  [FRB][Mp]       row terms b of the batch (log2 units)
+//   bcb [FRB][Mp]       b + c
+//   mub [FRB][64]       centred mu of the batch (zero beyond Q)
+//   kb  [FRB][64]       log2e kappa of the batch (zero beyond Q)
+struct LdsF {
+    int zt, bb, bcb, mub, kb, total;
 };
 
-__host__ __device__ inline Lds lds_layout(int Mp, int DS, int Q, bool grad) {
-    Lds L{};
+__host__ __device__ inline LdsF lds_fwd_layout(int Mp, int ni) {
+    LdsF L{};
     int o = 0;
-    L.zx = o; o += Mp * DS;
-    L.bb = o; o += kRB * Mp;
-    L.bcb = o; o += kRB * Mp;
-    L.mub = o; o += kRB * kRowStride;
-    L.kb = o; o += kRB * kRowStride;
-    L.w1b = L.w2b = L.t1 = L.red = o;
-    if (grad) {
-        L.w1b = o; o += kRB * Q;
-        L.w2b = o; o += kRB * Q;
-        L.t1 = o; o += kRB * Mp;
-        L.red = o; o += kRB * kWaves * (5 * Q + 2);
-    }
+    L.zt = o; o += Mp * 3 * ni * 16 / 2;
+    L.bb = o; o += kFRB * Mp;
+    L.bcb = o; o += kFRB * Mp;
+    L.mub = o; o += kFRB * kRowStride;
+    L.kb = o; o += kFRB * kRowStride;
     L.total = o;
     return L;
 }
@@ -207,12 +208,16 @@ MPlan make_mplan(const Shape &s) {
     p.ks = round_ks((int)cdiv(s.Q, 2), p.nqb);
     p.DSF = std::max<int>(2 * p.ks, (int)s.Q + 1) | 1;
     p.T = (int64_t)p.nb * (p.nb + 1) / 2;
-    // forward tasks: the tiles-per-task value with the fewest tile slots (ties: larger)
+    p.ni = (int)cdiv(s.Q, 16);
+    // forward tasks: tiles per task by a cost model in cycles: each task splits its
+    // n-dependent operand once per row (about 120 vector instructions per 16
+    // dimensions), each tile slot costs about 600 (MFMA, exp2, bias, sum)
     p.tpw = 1;
     int64_t best = -1;
-    for (int t = 1; t <= 4; ++t) {
-        const int64_t slots = cdiv(fwd_tasks(p.nb, t), kWaves) * kWaves * t;
-        if (best < 0 || slots <= best) { best = slots; p.tpw = t; }
+    for (int t = 1; t <= fwd_tpw_max(p.ni); ++t) {
+        const int64_t groups = cdiv(fwd_tasks(p.nb, t), kWaves);
+        const int64_t cost = groups * kWaves * (240 * p.ni + 600 * t);
+        if (best < 0 || cost < best) { best = cost; p.tpw = t; }
     }
     p.ftasks = fwd_tasks(p.nb, p.tpw);
     p.fgroups = cdiv(p.ftasks, kWaves);
@@ -232,7 +237,7 @@ MPlan make_mplan(const Shape &s) {
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
     p.fin_blocks = cdiv(s.N, kFinRows);
-    p.lds_fwd = sizeof(float) * lds_layout((int)p.Mp, p.DSF, (int)s.Q, false).total;
+    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.ni).total;
     p.lds_grad = sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.wpg).total;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
@@ -377,50 +382,7 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     }
 }
 
-// ---------------------------------------------------------------- LDS staging
-__device__ void stage_z(float *lds, const Lds &L, int M, int Mp, int Q, int DS,
-                        const float *__restrict__ Z, const float *__restrict__ zc) {
-    for (int i = threadIdx.x; i < Mp * DS; i += kThreads) {
-        const int m = i / DS, q = i - m * DS;
-        float v = 0.f;
-        if (m < M) {
-            if (q < Q) v = Z[(int64_t)m * Q + q] - zc[q];
-            else if (q == Q) v = 1.f;
-        }
-        lds[L.zx + i] = v;
-    }
-}
-
-// Per-row values of rows [n0, n0 + cb) into the batch arrays.  Rows >= cb
-// are zero (row terms: kPadBias).
-template <bool GRAD>
-__device__ void stage_batch(float *lds, const Lds &L, int64_t n0, int cb, int Mp, int Q,
-                            const float *__restrict__ mu, const float *__restrict__ zc,
-                            const float *__restrict__ Kt, const float *__restrict__ bt,
-                            const float *__restrict__ bc, const float *__restrict__ w1t,
-                            const float *__restrict__ w2t, const float *__restrict__ t1g) {
-    for (int i = threadIdx.x; i < kRB * kRowStride; i += kThreads) {
-        const int r = i / kRowStride, q = i - r * kRowStride;
-        const bool ok = r < cb && q < Q;
-        const int64_t n = n0 + r;
-        lds[L.mub + i] = ok ? mu[n * Q + q] - zc[q] : 0.f;
-        lds[L.kb + i] = ok ? Kt[n * kRowStride + q] : 0.f;
-    }
-    for (int i = threadIdx.x; i < kRB * Mp; i += kThreads) {
-        const bool ok = i < cb * Mp;
-        lds[L.bb + i] = ok ? bt[n0 * Mp + i] : kPadBias;
-        lds[L.bcb + i] = ok ? bc[n0 * Mp + i] : kPadBias;
-        if (GRAD) lds[L.t1 + i] = ok ? t1g[n0 * Mp + i] : 0.f;
-    }
-    if (GRAD) {
-        for (int i = threadIdx.x; i < kRB * Q; i += kThreads) {
-            const bool ok = i < cb * Q;
-            lds[L.w1b + i] = ok ? w1t[n0 * Q + i] : 0.f;
-            lds[L.w2b + i] = ok ? w2t[n0 * Q + i] : 0.f;
-        }
-    }
-}
-
+// ---------------------------------------------------------------- shared helpers
 // The n-dependent Gram operand -K d = (z - mu) K for the 32 rows of block
 // `blk` (lane supplies row c, latent dimension 2s + g).
 template <int KS>
@@ -432,25 +394,39 @@ __device__ __forceinline__ void kd_operands(const float *zx, int DS, int blk, in
     for (int s = 0; s < KS; ++s) out[s] = (zr[2 * s] - muk[s]) * kk[s];
 }
 
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef unsigned int u32;
+constexpr u32 kHi16 = 0xFFFF0000u;
+
+// Three bf16 parts of x (truncation split): x == p0 + p1 + p2 up to 2^-24 |x|.
+// Each part is returned as an fp32 bit pattern whose low 16 bits are zero.
+__device__ __forceinline__ void split3(float x, u32 &p0, u32 &p1, u32 &p2) {
+    p0 = __float_as_uint(x) & kHi16;
+    const float r = x - __uint_as_float(p0);
+    p1 = __float_as_uint(r) & kHi16;
+    p2 = __float_as_uint(r - __uint_as_float(p1));
+}
+
+// Pack the high halves of two fp32 bit patterns into one bf16 pair (a: element 0).
+__device__ __forceinline__ u32 pack_hi(u32 a, u32 b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+
 // ---------------------------------------------------------------- Psi2 forward
 // Tile (ti, tj), rows m in block ti, columns m' in block tj:
 //   e[m][m'] = (b + c)_m + b_m' + sum_q (-K d_mq) z_m'q     (A: -K d, B: z)
-// Waves per SIMD the forward kernel is compiled for: 3 where its registers fit
-// without spilling, else 2 (1 for the widest tasks).
-constexpr int fwd_waves(int ks, int tpw) {
-    return ((tpw <= 2 && ks <= 16) || (tpw == 3 && ks <= 10) || (tpw == 4 && ks <= 4)) ? 3
-           : (ks >= 24 && tpw >= 3) ? 1
-                                     : 2;
-}
-
-template <int KS, int TPW>
-__global__ __launch_bounds__(kThreads, fwd_waves(KS, TPW)) void psi2_fwd_kernel(
-    int64_t N, int M, int Q, int Mp, int nb, int DS, int64_t T, int ftasks,
-    int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
-    const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ bt,
-    const float *__restrict__ bc, float *__restrict__ partial) {
+// on bf16 MFMAs with both operands split into three bf16 parts (six cross
+// products; the dropped ones are below 2^-24 relative), which keeps fp32
+// accuracy while the vector units keep issuing beside the matrix cores.
+// Wave task: row block ti (its -K d operand is split once per row) and TPW
+// column blocks tj; Psi2 tile sums stay in registers over the row chunk.
+template <int NI, int TPW>
+__global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
+    int64_t N, int M, int Q, int Mp, int nb, int64_t T, int ftasks, int64_t rows_per_chunk,
+    const float *__restrict__ mu, const float *__restrict__ Z, const float *__restrict__ zc,
+    const float *__restrict__ Kt, const float *__restrict__ bt, const float *__restrict__ bc,
+    float *__restrict__ partial) {
     extern __shared__ float lds[];
-    const Lds L = lds_layout(Mp, DS, Q, false);
+    const LdsF L = lds_fwd_layout(Mp, NI);
+    unsigned short *zt = reinterpret_cast<unsigned short *>(lds + L.zt);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
     const int task = blockIdx.x * kWaves + wave;
@@ -466,24 +442,91 @@ __global__ __launch_bounds__(kThreads, fwd_waves(KS, TPW)) void psi2_fwd_kernel(
 #pragma unroll
         for (int t = 0; t < 16; ++t) acc[k][t] = 0.f;
 
-    stage_z(lds, L, M, Mp, Q, DS, Z, zc);
+    // the lane's centred z values of row m = ti*32 + c, k = 16 hh + 8 g + e (zero past Q)
+    float zr[NI][8];
+    {
+        const int m = ti * kTile + c;
+#pragma unroll
+        for (int hh = 0; hh < NI; ++hh)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int q = 16 * hh + 8 * g + e;
+                zr[hh][e] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+            }
+    }
+    // split z table for the B operands of every column block
+    const int ztotal = Mp * 3 * NI * 16;
+    for (int idx = threadIdx.x; idx < ztotal; idx += blockDim.x) {
+        int r = idx;
+        const int e = r % 8; r /= 8;
+        const int cc = r % 32; r /= 32;
+        const int gg = r % 2; r /= 2;
+        const int hh = r % NI; r /= NI;
+        const int part = r % 3; r /= 3;
+        const int m = r * kTile + cc, q = 16 * hh + 8 * gg + e;
+        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+        u32 p0, p1, p2;
+        split3(v, p0, p1, p2);
+        zt[idx] = (unsigned short)((part == 0 ? p0 : (part == 1 ? p1 : p2)) >> 16);
+    }
+
+    // Batches of kFRB rows: the next batch is loaded into registers while the
+    // current one is computed, then written to LDS between two barriers.
+    // (kFRB * 64 == blockDim: one mu / kappa value per thread.)
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
-    for (int64_t n0 = r0; n0 < r1; n0 += kRB) {
-        const int cb = (int)min<int64_t>(kRB, r1 - n0);
+    const int tid = threadIdx.x;
+    float pf_b[kFPF], pf_c[kFPF], pf_mu, pf_k;
+    auto load = [&](int64_t n0) {
+        const int cb = (int)min<int64_t>(kFRB, r1 - n0);
+#pragma unroll
+        for (int j = 0; j < kFPF; ++j) {
+            const int k = tid + j * kThreads;
+            const bool ok = k < cb * Mp;
+            pf_b[j] = ok ? bt[n0 * Mp + k] : kPadBias;
+            pf_c[j] = ok ? bc[n0 * Mp + k] : kPadBias;
+        }
+        const int r = tid / kRowStride, q = tid - r * kRowStride;
+        const bool ok = r < cb && q < Q;
+        pf_mu = ok ? mu[(n0 + r) * Q + q] - zc[q] : 0.f;
+        pf_k = ok ? Kt[(n0 + r) * kRowStride + q] : 0.f;
+    };
+    if (r0 < r1) load(r0);
+    for (int64_t n0 = r0; n0 < r1; n0 += kFRB) {
+        const int cb = (int)min<int64_t>(kFRB, r1 - n0);
         __syncthreads();
-        stage_batch<false>(lds, L, n0, cb, Mp, Q, mu, zc, Kt, bt, bc, nullptr, nullptr, nullptr);
+#pragma unroll
+        for (int j = 0; j < kFPF; ++j) {
+            const int k = tid + j * kThreads;
+            if (k < kFRB * Mp) {
+                lds[L.bb + k] = pf_b[j];
+                lds[L.bcb + k] = pf_c[j];
+            }
+        }
+        lds[L.mub + tid] = pf_mu;
+        lds[L.kb + tid] = pf_k;
         __syncthreads();
+        if (n0 + kFRB < r1) load(n0 + kFRB);
         if (!active) continue;
         for (int r = 0; r < cb; ++r) {
-            float muk[KS], kk[KS];
+            // A operand: -K d = (z - mu) K for the rows of block ti, split in three
+            v8bf A[3][NI];
 #pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                muk[s] = lds[L.mub + r * kRowStride + 2 * s + g];
-                kk[s] = lds[L.kb + r * kRowStride + 2 * s + g];
+            for (int hh = 0; hh < NI; ++hh) {
+                const float *mur = lds + L.mub + r * kRowStride + 16 * hh + 8 * g;
+                const float *kr = lds + L.kb + r * kRowStride + 16 * hh + 8 * g;
+                u32 ap[3][8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    split3((zr[hh][e] - mur[e]) * kr[e], ap[0][e], ap[1][e], ap[2][e]);
+#pragma unroll
+                for (int pa = 0; pa < 3; ++pa) {
+                    u32 d4[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) d4[u] = pack_hi(ap[pa][2 * u], ap[pa][2 * u + 1]);
+                    A[pa][hh] = __builtin_bit_cast(v8bf, d4);
+                }
             }
-            float aop[KS];
-            kd_operands<KS>(lds + L.zx, DS, ti, c, g, muk, kk, aop);
             const float *bcr = lds + L.bcb + r * Mp + ti * kTile;
             float brow[16];
 #pragma unroll
@@ -492,13 +535,23 @@ __global__ __launch_bounds__(kThreads, fwd_waves(KS, TPW)) void psi2_fwd_kernel(
 #pragma unroll
             for (int k = 0; k < TPW; ++k) {
                 const float bcol = bbr[tj[k] * kTile + c];
-                const float *zr = lds + L.zx + (tj[k] * kTile + c) * DS + g;
                 v16f e;
 #pragma unroll
                 for (int t = 0; t < 16; ++t) e[t] = brow[t] + bcol;
 #pragma unroll
-                for (int s = 0; s < KS; ++s)
-                    e = __builtin_amdgcn_mfma_f32_32x32x2f32(aop[s], zr[2 * s], e, 0, 0, 0);
+                for (int hh = 0; hh < NI; ++hh) {
+                    v8bf B[3];
+#pragma unroll
+                    for (int pb = 0; pb < 3; ++pb)
+                        B[pb] = *reinterpret_cast<const v8bf *>(
+                            zt + ((((tj[k] * 3 + pb) * NI + hh) * 2 + g) * 32 + c) * 8);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[0], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[1], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[1][hh], B[0], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[2], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[1][hh], B[1], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[2][hh], B[0], e, 0, 0, 0);
+                }
 #pragma unroll
                 for (int t = 0; t < 16; ++t) acc[k][t] += __builtin_amdgcn_exp2f(e[t]);
             }
@@ -537,22 +590,6 @@ __global__ void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T, int64_t 
 }
 
 // ---------------------------------------------------------------- Psi2 gradient
-typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
-typedef unsigned int u32;
-constexpr u32 kHi16 = 0xFFFF0000u;
-
-// Three bf16 parts of x (truncation split): x == p0 + p1 + p2 up to 2^-24 |x|.
-// Each part is returned as an fp32 bit pattern whose low 16 bits are zero.
-__device__ __forceinline__ void split3(float x, u32 &p0, u32 &p1, u32 &p2) {
-    p0 = __float_as_uint(x) & kHi16;
-    const float r = x - __uint_as_float(p0);
-    p1 = __float_as_uint(r) & kHi16;
-    p2 = __float_as_uint(r - __uint_as_float(p1));
-}
-
-// Pack the high halves of two fp32 bit patterns into one bf16 pair (a: element 0).
-__device__ __forceinline__ u32 pack_hi(u32 a, u32 b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
-
 // The workgroup's JPW column blocks of [Z | 1] as three bf16 parts, in the B
 // operand order of the 32x32x16 bf16 MFMA: for instruction h and lane group g
 // the 8 k-values are the rows crow(8h + e, g), e = 0..7, of the block.
@@ -919,16 +956,16 @@ __global__ void grad_reduce_kernel(int64_t N, int M, int Q, const float *__restr
 }
 
 // ---------------------------------------------------------------- dispatch
-template <int KS, int TPW>
+template <int NI, int TPW>
 hipError_t launch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                       void *ws, hipStream_t st) {
-    auto k = psi2_fwd_kernel<KS, TPW>;
+    auto k = psi2_fwd_kernel<NI, TPW>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_fwd);
     if (e != hipSuccess) return e;
     dim3 grid((unsigned)p.fgroups, (unsigned)p.fchunks);
     TimedScope ts(st, "mfma_psi2_fwd");
-    k<<<grid, kThreads, p.lds_fwd, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.T,
+    k<<<grid, kThreads, p.lds_fwd, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.T,
                                          p.ftasks, p.frows, mu, Z, fat(ws, p.off_zc),
                                          fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc),
                                          fat(ws, p.off_fp));
@@ -954,12 +991,12 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
 
 hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z, void *ws,
                         hipStream_t st) {
-#define GPPS_F(K, T) \
-    if (p.ks == K && p.tpw == T) return launch_fwd<K, T>(p, s, mu, Z, ws, st);
-#define GPPS_F4(K) GPPS_F(K, 1) GPPS_F(K, 2) GPPS_F(K, 3) GPPS_F(K, 4)
-    GPPS_F4(1) GPPS_F4(2) GPPS_F4(3) GPPS_F4(4) GPPS_F4(5) GPPS_F4(6) GPPS_F4(8) GPPS_F4(10)
-    GPPS_F4(12) GPPS_F4(15) GPPS_F4(16) GPPS_F4(24) GPPS_F4(32)
-#undef GPPS_F4
+#define GPPS_F(I, T) \
+    if (p.ni == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, ws, st);
+    GPPS_F(1, 1) GPPS_F(1, 2) GPPS_F(1, 3) GPPS_F(1, 4)
+    GPPS_F(2, 1) GPPS_F(2, 2)
+    GPPS_F(3, 1)
+    GPPS_F(4, 1)
 #undef GPPS_F
     return hipErrorInvalidValue;
 }

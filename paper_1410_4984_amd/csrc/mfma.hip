@@ -114,11 +114,8 @@ struct MPlan {
     int64_t Mp;            // M rounded up to the tile edge
     int nb;                // tiles per edge
     int nqb;               // 32-column blocks of [Z | 1] (Q + 1 columns)
-    int DS;                // gradient: LDS row stride of the z table (odd: conflict-free
-                           // column reads; 32 * nqb + 1 columns for the [Z | 1] product)
-    int DSF;               // forward: the same for the Gram operand only (>= 2 ks, odd)
-    int ks;                // gradient Gram: MFMA k-steps (2 latent dimensions each)
-    int ni;                // forward Gram: 16-dimension bf16 MFMA steps (ceil(Q / 16))
+    int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= Q)
+    int ni;                // Gram: 16-dimension bf16 MFMA steps (ceil(Q / 16))
     int64_t T;             // upper-triangular tiles
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
@@ -132,19 +129,6 @@ struct MPlan {
     size_t off_K, off_hq, off_w2, off_hl, off_w1, off_l1, off_zc, off_bt, off_bc, off_t1, off_g2,
         off_fp, off_rs, off_dz, off_dl, total;
 };
-
-int round_ks(int ks, int nqb) {
-    static const int one[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 15, 16};
-    static const int two[] = {16, 24, 32};
-    if (nqb == 1) {
-        for (int v : one)
-            if (ks <= v) return v;
-    } else {
-        for (int v : two)
-            if (ks <= v) return v;
-    }
-    return -1;
-}
 
 // Forward LDS layout (floats):
 //   zt  [nb][3][ni][2][32][8] bf16  centred z split into three bf16 parts, in the
@@ -171,22 +155,25 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int ni) {
 }
 
 // Gradient LDS layout (floats):
-//   zx  [Mp][DSF]       centred z (fp32): Gram operand (rows m') and epilogue (rows m)
+//   zx  [wpg 32][DSF]   centred z (fp32) of the workgroup's row blocks (rows m of W)
 //   zb  [jpw][3][2][2][32 nqb][8] bf16   the workgroup's column blocks of [Z | 1] split
 //                       into three bf16 parts, laid out as the B operands of the
 //                       32x32x16 bf16 MFMA (8 consecutive k per lane and instruction)
+//   za  [jpw][3][ni][2][32][8] bf16       the same rows of centred z as Gram A operands
+//                       (row m' per lane, 8 consecutive dimensions per lane group)
 //   bb, bcb [RB][Mp], mub, kb [RB][64], w1b, w2b [RB][Q], t1 [RB][Mp],
 //   red [RB][wpg][5Q + 2]
 struct LdsG {
-    int zx, zb, bb, bcb, mub, kb, w1b, w2b, t1, red, total;
+    int zx, zb, za, bb, bcb, mub, kb, w1b, w2b, t1, red, total;
 };
 
-__host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb, int wpg) {
+__host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb, int ni, int wpg) {
     const int jpw = grad_jpw(nqb);
     LdsG L{};
     int o = 0;
-    L.zx = o; o += (Mp * DSF + 3) / 4 * 4;
+    L.zx = o; o += (wpg * kTile * DSF + 3) / 4 * 4;
     L.zb = o; o += jpw * 3 * 2 * 2 * 32 * nqb * 8 / 2;
+    L.za = o; o += jpw * 3 * ni * 2 * 32 * 8 / 2;
     L.bb = o; o += kRB * Mp;
     L.bcb = o; o += kRB * Mp;
     L.mub = o; o += kRB * kRowStride;
@@ -204,9 +191,7 @@ MPlan make_mplan(const Shape &s) {
     p.Mp = cdiv(s.M, kTile) * kTile;
     p.nb = (int)(p.Mp / kTile);
     p.nqb = s.Q + 1 <= 32 ? 1 : 2;
-    p.DS = 32 * p.nqb + 1;
-    p.ks = round_ks((int)cdiv(s.Q, 2), p.nqb);
-    p.DSF = std::max<int>(2 * p.ks, (int)s.Q + 1) | 1;
+    p.DSF = (int)s.Q | 1;
     p.T = (int64_t)p.nb * (p.nb + 1) / 2;
     p.ni = (int)cdiv(s.Q, 16);
     // forward tasks: tiles per task by a cost model in cycles: each task splits its
@@ -228,7 +213,7 @@ MPlan make_mplan(const Shape &s) {
     p.njr = (int)cdiv(p.nb, p.jpw);
     // widest workgroup whose LDS fits
     p.wpg = std::min(p.nb, grad_waves(p.nqb));
-    while (p.wpg > 1 && sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb,
+    while (p.wpg > 1 && sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.ni,
                                                         p.wpg).total > 160 * 1024)
         p.wpg /= 2;
     p.igroups = (int)cdiv(p.nb, p.wpg);
@@ -238,7 +223,8 @@ MPlan make_mplan(const Shape &s) {
     p.gchunks = cdiv(s.N, p.grows);
     p.fin_blocks = cdiv(s.N, kFinRows);
     p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.ni).total;
-    p.lds_grad = sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.wpg).total;
+    p.lds_grad =
+        sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.ni, p.wpg).total;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_K = take(sizeof(float) * s.N * kRowStride);
@@ -383,17 +369,6 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
 }
 
 // ---------------------------------------------------------------- shared helpers
-// The n-dependent Gram operand -K d = (z - mu) K for the 32 rows of block
-// `blk` (lane supplies row c, latent dimension 2s + g).
-template <int KS>
-__device__ __forceinline__ void kd_operands(const float *zx, int DS, int blk, int c, int g,
-                                            const float (&muk)[KS], const float (&kk)[KS],
-                                            float (&out)[KS]) {
-    const float *zr = zx + (blk * kTile + c) * DS + g;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) out[s] = (zr[2 * s] - muk[s]) * kk[s];
-}
-
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef unsigned int u32;
 constexpr u32 kHi16 = 0xFFFF0000u;
@@ -630,7 +605,7 @@ __device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
 // registers for the whole kernel; the epilogue turns V' into the task's share
 // of dZ (registers) and of the per-row sums, which the workgroup combines in LDS
 // and writes per (group, row) for psi2_finalize_kernel.
-template <int KS, int NQB, int JPW = grad_jpw(NQB)>
+template <int NI, int NQB, int JPW = grad_jpw(NQB)>
 __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int DSF, int njr, int wpg, int igroups,
     int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
@@ -639,8 +614,9 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     const float *__restrict__ t1g, const float *__restrict__ G2p, Hyp<float> h,
     float *__restrict__ rowsum, float *__restrict__ part_dz) {
     extern __shared__ float lds[];
-    const LdsG L = lds_grad_layout(Mp, DSF, Q, NQB, wpg);
+    const LdsG L = lds_grad_layout(Mp, DSF, Q, NQB, NI, wpg);
     unsigned short *zb = reinterpret_cast<unsigned short *>(lds + L.zb);
+    unsigned short *za = reinterpret_cast<unsigned short *>(lds + L.za);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
     const int ones_src = 32 * g + (Q & 31);    // lane holding column Q (the row sums r)
@@ -649,7 +625,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     const int QV = 32 * NQB;
     const int group = blockIdx.x;
     const int jr = group / igroups;            // range of column blocks of W (m')
-    const int i0 = (group % igroups) * wpg + wave;
+    const int ib0 = (group % igroups) * wpg;  // first row block of the workgroup
+    const int i0 = ib0 + wave;
     const bool active = i0 < nb;               // wave-uniform
     const int i = active ? i0 : 0;             // row block of W (m)
     const bool has1 = active && jr == 0;       // this task also adds the Psi1 terms of block i
@@ -678,12 +655,29 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
         il2[qb] = q < Q ? 1.f / h.l2[q] : 0.f;
     }
 
-    // constant tables: centred z (fp32) and the split [Z | 1] column blocks
-    for (int k = threadIdx.x; k < Mp * DSF; k += blockDim.x) {
-        const int m = k / DSF, q = k - m * DSF;
+    // constant tables: centred z (fp32) of the row blocks, split [Z | 1] and z of
+    // the column blocks
+    for (int k = threadIdx.x; k < wpg * kTile * DSF; k += blockDim.x) {
+        const int lr = k / DSF, q = k - lr * DSF;
+        const int m = ib0 * kTile + lr;
         lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
     }
     stage_zb<JPW>(zb, jr, M, Q, NQB, Z, zc);
+    for (int idx = threadIdx.x; idx < JPW * 3 * NI * 2 * 32 * 8; idx += blockDim.x) {
+        int r = idx;
+        const int e = r % 8; r /= 8;
+        const int cc = r % 32; r /= 32;
+        const int gg = r % 2; r /= 2;
+        const int hh = r % NI; r /= NI;
+        const int part = r % 3; r /= 3;
+        // column blocks past the edge repeat the last one, as the bias terms of
+        // those (zero-weighted) tiles do, so that their exponent stays finite
+        const int m = min(jr * JPW + r, nb - 1) * kTile + cc, q = 16 * hh + 8 * gg + e;
+        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+        u32 p0, p1, p2;
+        split3(v, p0, p1, p2);
+        za[idx] = (unsigned short)((part == 0 ? p0 : (part == 1 ? p1 : p2)) >> 16);
+    }
 
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
@@ -714,15 +708,27 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 for (int k = lane; k < RED; k += 64) rs[k] = 0.f;
                 continue;
             }
-            float muk[KS], kk[KS];
+            // Gram B operand: -K d = (z - mu) K for column block i, split in three
+            v8bf GB[3][NI];
 #pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                muk[s] = lds[L.mub + r * kRowStride + 2 * s + g];
-                kk[s] = lds[L.kb + r * kRowStride + 2 * s + g];
+            for (int hh = 0; hh < NI; ++hh) {
+                const float *mur = lds + L.mub + r * kRowStride + 16 * hh + 8 * g;
+                const float *kr = lds + L.kb + r * kRowStride + 16 * hh + 8 * g;
+                const float *zi = lds + L.zx + (wave * kTile + c) * DSF + 16 * hh + 8 * g;
+                u32 ap[3][8];
+#pragma unroll
+                for (int e8 = 0; e8 < 8; ++e8) {
+                    const float zv = 16 * hh + 8 * g + e8 < Q ? zi[e8] : 0.f;
+                    split3((zv - mur[e8]) * kr[e8], ap[0][e8], ap[1][e8], ap[2][e8]);
+                }
+#pragma unroll
+                for (int pa = 0; pa < 3; ++pa) {
+                    u32 d4[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) d4[u] = pack_hi(ap[pa][2 * u], ap[pa][2 * u + 1]);
+                    GB[pa][hh] = __builtin_bit_cast(v8bf, d4);
+                }
             }
-            // Gram B operand: -K d for column block i (the m index of W)
-            float bop[KS];
-            kd_operands<KS>(lds + L.zx, DSF, i, c, g, muk, kk, bop);
             const float bcol = lds[L.bcb + r * Mp + i * kTile + c];
             const float *bbr = lds + L.bb + r * Mp;
             v16f V[NQB];
@@ -733,13 +739,23 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
             for (int k = 0; k < JPW; ++k) {
                 const int j = jb[k];
-                const float *zr = lds + L.zx + (j * kTile + c) * DSF + g;
                 v16f e;
 #pragma unroll
                 for (int t = 0; t < 16; ++t) e[t] = bbr[j * kTile + crow(t, g)] + bcol;
 #pragma unroll
-                for (int s = 0; s < KS; ++s)
-                    e = __builtin_amdgcn_mfma_f32_32x32x2f32(zr[2 * s], bop[s], e, 0, 0, 0);
+                for (int hh = 0; hh < NI; ++hh) {
+                    v8bf GA[3];
+#pragma unroll
+                    for (int pa = 0; pa < 3; ++pa)
+                        GA[pa] = *reinterpret_cast<const v8bf *>(
+                            za + ((((k * 3 + pa) * NI + hh) * 2 + g) * 32 + c) * 8);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[0], GB[0][hh], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[0], GB[1][hh], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[1], GB[0][hh], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[0], GB[2][hh], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[1], GB[1][hh], e, 0, 0, 0);
+                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[2], GB[0][hh], e, 0, 0, 0);
+                }
                 // W tile, split into three bf16 parts; A operand of instruction hh takes
                 // the lane's rows crow(8 hh + e, g), as the B operand tables do
                 u32 wp[3][16];
@@ -791,7 +807,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             float X[NQB], Y[NQB], P[NQB], X1[NQB], P1[NQB], R = 0.f, T1 = 0.f;
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb) X[qb] = Y[qb] = P[qb] = X1[qb] = P1[qb] = 0.f;
-            const float *zblk = lds + L.zx + i * kTile * DSF;
+            const float *zblk = lds + L.zx + wave * kTile * DSF;
             const float *t1r = lds + L.t1 + r * Mp + i * kTile;
 #pragma unroll
             for (int t = 0; t < 16; ++t) {
@@ -802,7 +818,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
                 for (int qb = 0; qb < NQB; ++qb) {
                     const int q = qb * 32 + c;
-                    const float d = muq[qb] - (q < DSF ? zblk[rr * DSF + q] : 0.f);
+                    const float d = muq[qb] - (q < Q ? zblk[rr * DSF + q] : 0.f);
                     const float v = fmaf(rt, muq[qb], -V[qb][t]);
                     const float dr = d * rt;
                     dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, dz[qb][t]));
@@ -821,7 +837,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
                     for (int qb = 0; qb < NQB; ++qb) {
                         const int q = qb * 32 + c;
-                        const float d = muq[qb] - (q < DSF ? zblk[rr * DSF + q] : 0.f);
+                        const float d = muq[qb] - (q < Q ? zblk[rr * DSF + q] : 0.f);
                         const float td = tv * d;
                         dz[qb][t] = fmaf(td, w1q[qb], dz[qb][t]);
                         X1[qb] = fmaf(td, d, X1[qb]);
@@ -972,10 +988,10 @@ hipError_t launch_fwd(const MPlan &p, const Shape &s, const float *mu, const flo
     return hipGetLastError();
 }
 
-template <int KS, int NQB>
+template <int NI, int NQB>
 hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                        const Hyp<float> &h, void *ws, hipStream_t st) {
-    auto k = psi2_grad_kernel<KS, NQB>;
+    auto k = psi2_grad_kernel<NI, NQB>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_grad);
     if (e != hipSuccess) return e;
@@ -1003,11 +1019,9 @@ hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const f
 
 hipError_t dispatch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                          const Hyp<float> &h, void *ws, hipStream_t st) {
-#define GPPS_G(K, Q) \
-    if (p.ks == K && p.nqb == Q) return launch_grad<K, Q>(p, s, mu, Z, h, ws, st);
-    GPPS_G(1, 1) GPPS_G(2, 1) GPPS_G(3, 1) GPPS_G(4, 1) GPPS_G(5, 1) GPPS_G(6, 1) GPPS_G(8, 1)
-    GPPS_G(10, 1) GPPS_G(12, 1) GPPS_G(15, 1) GPPS_G(16, 1) GPPS_G(16, 2) GPPS_G(24, 2)
-    GPPS_G(32, 2)
+#define GPPS_G(I, Q) \
+    if (p.ni == I && p.nqb == Q) return launch_grad<I, Q>(p, s, mu, Z, h, ws, st);
+    GPPS_G(1, 1) GPPS_G(2, 1) GPPS_G(2, 2) GPPS_G(3, 2) GPPS_G(4, 2)
 #undef GPPS_G
     return hipErrorInvalidValue;
 }
@@ -1049,7 +1063,7 @@ bool mfma_supports(const Shape &s) {
     const int64_t Mp = cdiv(s.M, kTile) * kTile;
     if (!((Mp <= 512 && s.Q <= 31) || (Mp <= 256 && s.Q <= GPPS_MAX_Q_MFMA))) return false;
     const MPlan p = make_mplan(s);
-    return p.ks > 0 && p.lds_grad <= 160 * 1024 && p.lds_fwd <= 160 * 1024;
+    return p.lds_grad <= 160 * 1024 && p.lds_fwd <= 160 * 1024;
 }
 
 size_t mfma_workspace_bytes(const Shape &s) { return make_mplan(s).total; }

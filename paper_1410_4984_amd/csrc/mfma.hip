@@ -114,8 +114,10 @@ struct MPlan {
     int64_t Mp;            // M rounded up to the tile edge
     int nb;                // tiles per edge
     int nqb;               // 32-column blocks of [Z | 1] (Q + 1 columns)
-    int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= Q)
-    int ni;                // Gram: 16-dimension bf16 MFMA steps (ceil(Q / 16))
+    int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= 16 ni
+                           // and >= 32 nqb, so that no read needs a bounds test)
+    int ni;                // gradient Gram: 16-slot bf16 MFMA steps (Q dimensions + a bias slot)
+    int fni;               // forward Gram: 16-dimension bf16 MFMA steps (ceil(Q / 16))
     int64_t T;             // upper-triangular tiles
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
@@ -131,7 +133,7 @@ struct MPlan {
 };
 
 // Forward LDS layout (floats):
-//   zt  [nb][3][ni][2][32][8] bf16  centred z split into three bf16 parts, in the
+//   zt  [nb][3][fni][2][32][8] bf16  centred z split into three bf16 parts, in the
 //                       B operand order of the 32x32x16 bf16 MFMA: column block,
 //                       part, instruction, lane group, column, 8 consecutive k
 //   bb  [FRB][Mp]       row terms b of the batch (log2 units)
@@ -155,13 +157,15 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int ni) {
 }
 
 // Gradient LDS layout (floats):
-//   zx  [wpg 32][DSF]   centred z (fp32) of the workgroup's row blocks (rows m of W)
+//   zx  [wpg 32][DSF]   centred z (fp32) of the workgroup's row blocks (rows m of W),
+//                       zero past Q up to the odd stride DSF (>= 16 ni, >= 32 nqb)
 //   zb  [jpw][3][2][2][32 nqb][8] bf16   the workgroup's column blocks of [Z | 1] split
 //                       into three bf16 parts, laid out as the B operands of the
 //                       32x32x16 bf16 MFMA (8 consecutive k per lane and instruction)
-//   za  [jpw][3][ni][2][32][8] bf16       the same rows of centred z as Gram A operands
-//                       (row m' per lane, 8 consecutive dimensions per lane group)
-//   bb, bcb [RB][Mp], mub, kb [RB][64], w1b, w2b [RB][Q], t1 [RB][Mp],
+//   za  [jpw][3][ni][2][32][8] bf16       the same rows of [centred z | 1] as Gram A
+//                       operands (row m' per lane, 8 consecutive slots per lane group;
+//                       slot Q holds 1)
+//   bb, bcb [RB][Mp], mub, kb, w1b, w2b [RB][64] (zero past Q), t1 [RB][Mp],
 //   red [RB][wpg][5Q + 2]
 struct LdsG {
     int zx, zb, za, bb, bcb, mub, kb, w1b, w2b, t1, red, total;
@@ -178,8 +182,8 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
     L.bcb = o; o += kRB * Mp;
     L.mub = o; o += kRB * kRowStride;
     L.kb = o; o += kRB * kRowStride;
-    L.w1b = o; o += kRB * Q;
-    L.w2b = o; o += kRB * Q;
+    L.w1b = o; o += kRB * kRowStride;
+    L.w2b = o; o += kRB * kRowStride;
     L.t1 = o; o += kRB * Mp;
     L.red = o; o += kRB * wpg * (5 * Q + 2);
     L.total = o;
@@ -191,17 +195,18 @@ MPlan make_mplan(const Shape &s) {
     p.Mp = cdiv(s.M, kTile) * kTile;
     p.nb = (int)(p.Mp / kTile);
     p.nqb = s.Q + 1 <= 32 ? 1 : 2;
-    p.DSF = (int)s.Q | 1;
+    p.ni = (int)cdiv(s.Q + 1, 16);   // k slot Q carries a bias term
+    p.fni = (int)cdiv(s.Q, 16);
+    p.DSF = std::max<int>(16 * p.ni, 32 * p.nqb) | 1;
     p.T = (int64_t)p.nb * (p.nb + 1) / 2;
-    p.ni = (int)cdiv(s.Q, 16);
     // forward tasks: tiles per task by a cost model in cycles: each task splits its
     // n-dependent operand once per row (about 120 vector instructions per 16
     // dimensions), each tile slot costs about 600 (MFMA, exp2, bias, sum)
     p.tpw = 1;
     int64_t best = -1;
-    for (int t = 1; t <= fwd_tpw_max(p.ni); ++t) {
+    for (int t = 1; t <= fwd_tpw_max(p.fni); ++t) {
         const int64_t groups = cdiv(fwd_tasks(p.nb, t), kWaves);
-        const int64_t cost = groups * kWaves * (240 * p.ni + 600 * t);
+        const int64_t cost = groups * kWaves * (240 * p.fni + 600 * t);
         if (best < 0 || cost < best) { best = cost; p.tpw = t; }
     }
     p.ftasks = fwd_tasks(p.nb, p.tpw);
@@ -222,7 +227,7 @@ MPlan make_mplan(const Shape &s) {
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
     p.fin_blocks = cdiv(s.N, kFinRows);
-    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.ni).total;
+    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.fni).total;
     p.lds_grad =
         sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.ni, p.wpg).total;
     size_t o = 0;
@@ -598,10 +603,12 @@ __device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
 // split freely.  Wave task: row block i (the m index of W) and the JPW column
 // blocks j (the m' index) of the workgroup's range jr.  Tile (j, i), rows m' in
 // block j, columns m in block i:
-//   e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)       (fp32 MFMA; A: z, B: -K d)
-// W = G2s o exp2(e); then V' += W [Z | 1] on bf16 MFMAs with both operands split
-// into three bf16 parts (six cross products; the dropped ones are below 2^-24
-// relative), which keeps fp32 accuracy.  The task's dL/dPsi2 tiles stay in
+//   e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)   (A: [z | 1], B: [-K d | b + c])
+// W = G2s o exp2(e); then V' += W [Z | 1].  Both products run on bf16 MFMAs with
+// both operands split into three bf16 parts (six cross products; the dropped
+// ones are below 2^-24 relative), which keeps fp32 accuracy.  The column term
+// rides in k slot Q, the row term is the accumulator's start value.  The task's
+// dL/dPsi2 tiles stay in
 // registers for the whole kernel; the epilogue turns V' into the task's share
 // of dZ (registers) and of the per-row sums, which the workgroup combines in LDS
 // and writes per (group, row) for psi2_finalize_kernel.
@@ -673,7 +680,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
         // column blocks past the edge repeat the last one, as the bias terms of
         // those (zero-weighted) tiles do, so that their exponent stays finite
         const int m = min(jr * JPW + r, nb - 1) * kTile + cc, q = 16 * hh + 8 * gg + e;
-        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : (q == Q ? 1.f : 0.f);
         u32 p0, p1, p2;
         split3(v, p0, p1, p2);
         za[idx] = (unsigned short)((part == 0 ? p0 : (part == 1 ? p1 : p2)) >> 16);
@@ -696,10 +703,11 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             lds[L.bcb + k] = ok ? bc[n0 * Mp + k] : kPadBias;
             lds[L.t1 + k] = ok ? t1g[n0 * Mp + k] : 0.f;
         }
-        for (int k = threadIdx.x; k < kRB * Q; k += blockDim.x) {
-            const bool ok = k < cb * Q;
-            lds[L.w1b + k] = ok ? w1t[n0 * Q + k] : 0.f;
-            lds[L.w2b + k] = ok ? w2t[n0 * Q + k] : 0.f;
+        for (int k = threadIdx.x; k < kRB * kRowStride; k += blockDim.x) {
+            const int r = k / kRowStride, q = k - r * kRowStride;
+            const bool ok = r < cb && q < Q;
+            lds[L.w1b + k] = ok ? w1t[(n0 + r) * Q + q] : 0.f;
+            lds[L.w2b + k] = ok ? w2t[(n0 + r) * Q + q] : 0.f;
         }
         __syncthreads();
         for (int r = 0; r < cb; ++r) {
@@ -708,7 +716,9 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 for (int k = lane; k < RED; k += 64) rs[k] = 0.f;
                 continue;
             }
-            // Gram B operand: -K d = (z - mu) K for column block i, split in three
+            // Gram B operand: -K d = (z - mu) K for column block i and (b + c)_m in
+            // slot Q, split in three
+            const float bcol = lds[L.bcb + r * Mp + i * kTile + c];
             v8bf GB[3][NI];
 #pragma unroll
             for (int hh = 0; hh < NI; ++hh) {
@@ -718,8 +728,9 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 u32 ap[3][8];
 #pragma unroll
                 for (int e8 = 0; e8 < 8; ++e8) {
-                    const float zv = 16 * hh + 8 * g + e8 < Q ? zi[e8] : 0.f;
-                    split3((zv - mur[e8]) * kr[e8], ap[0][e8], ap[1][e8], ap[2][e8]);
+                    // slots >= Q: z, mu and K are zero there; slot Q carries the bias
+                    const float v = (zi[e8] - mur[e8]) * kr[e8] + (16 * hh + 8 * g + e8 == Q ? bcol : 0.f);
+                    split3(v, ap[0][e8], ap[1][e8], ap[2][e8]);
                 }
 #pragma unroll
                 for (int pa = 0; pa < 3; ++pa) {
@@ -729,7 +740,6 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                     GB[pa][hh] = __builtin_bit_cast(v8bf, d4);
                 }
             }
-            const float bcol = lds[L.bcb + r * Mp + i * kTile + c];
             const float *bbr = lds + L.bb + r * Mp;
             v16f V[NQB];
 #pragma unroll
@@ -741,7 +751,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 const int j = jb[k];
                 v16f e;
 #pragma unroll
-                for (int t = 0; t < 16; ++t) e[t] = bbr[j * kTile + crow(t, g)] + bcol;
+                for (int t = 0; t < 16; ++t) e[t] = bbr[j * kTile + crow(t, g)];
 #pragma unroll
                 for (int hh = 0; hh < NI; ++hh) {
                     v8bf GA[3];
@@ -799,8 +809,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             for (int qb = 0; qb < NQB; ++qb) {
                 const int q = qb * 32 + c;
                 muq[qb] = lds[L.mub + r * kRowStride + q];
-                const float w2 = q < Q ? lds[L.w2b + r * Q + q] : 0.f;
-                w1q[qb] = q < Q ? lds[L.w1b + r * Q + q] : 0.f;
+                const float w2 = lds[L.w2b + r * kRowStride + q];
+                w1q[qb] = lds[L.w1b + r * kRowStride + q];
                 alpha[qb] = w2 - il2[qb];
                 beta[qb] = w2 + il2[qb];
             }
@@ -818,7 +828,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
                 for (int qb = 0; qb < NQB; ++qb) {
                     const int q = qb * 32 + c;
-                    const float d = muq[qb] - (q < Q ? zblk[rr * DSF + q] : 0.f);
+                    const float d = muq[qb] - zblk[rr * DSF + q];
                     const float v = fmaf(rt, muq[qb], -V[qb][t]);
                     const float dr = d * rt;
                     dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, dz[qb][t]));
@@ -837,7 +847,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
                     for (int qb = 0; qb < NQB; ++qb) {
                         const int q = qb * 32 + c;
-                        const float d = muq[qb] - (q < Q ? zblk[rr * DSF + q] : 0.f);
+                        const float d = muq[qb] - zblk[rr * DSF + q];
                         const float td = tv * d;
                         dz[qb][t] = fmaf(td, w1q[qb], dz[qb][t]);
                         X1[qb] = fmaf(td, d, X1[qb]);
@@ -1008,7 +1018,7 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
 hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z, void *ws,
                         hipStream_t st) {
 #define GPPS_F(I, T) \
-    if (p.ni == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, ws, st);
+    if (p.fni == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, ws, st);
     GPPS_F(1, 1) GPPS_F(1, 2) GPPS_F(1, 3) GPPS_F(1, 4)
     GPPS_F(2, 1) GPPS_F(2, 2)
     GPPS_F(3, 1)

@@ -10,10 +10,16 @@ Metric: N*M^2*Q terms per second (whole step).  Beside it:
                 against the FP32 peak of 157.3 TFLOP/s;
   pct_fp32_peak the Psi2 forward + gradient kernels together:
                 F_alg = 8 Q N M(M+1)/2 flops over their summed time;
+  exp_per_s     2 N M(M+1)/2 exponentials (one per unique pair and datapoint in
+                each pass) over the same time, beside the v_exp_f32 peak;
   cpu_baseline  the fp64 CPU oracle on a bounded row sample of the same
                 workload, on this host's cores (a reported baseline only).
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload large]
+
+--copy-probe-mib X runs a plain device copy (torch.neg into a second buffer) of
+X MiB three times before the timed steps: under a rocprofv3 --pmc run its
+FETCH_SIZE / WRITE_SIZE calibrate the counters against a known byte count.
 """
 from __future__ import annotations
 
@@ -31,6 +37,8 @@ if ROOT not in sys.path:
 
 PEAK_FP32 = 157.3e12          # MI355X FP32 (vector and matrix) peak, FLOP/s
 PEAK_HBM = 8.0e12             # B/s
+# v_exp_f32 is a quarter-rate transcendental: 256 CUs x 4 SIMDs x 16 lanes / 4 x 2.4 GHz
+PEAK_EXP = 256 * 4 * 16 / 4 * 2.4e9
 METRIC = "N·M²·Q psi-stat+grad terms/sec (fp32) and % of FP32 VALU peak, 1 MI355X"
 
 
@@ -90,9 +98,11 @@ def cpu_baseline(inp, target_s: float):
         return time.perf_counter() - t0
 
     threads = oracle.num_threads()
-    probe = max(threads, 16)
-    t = run(np.arange(probe) * (N // probe))
-    n = int(min(N, max(probe, probe * target_s / max(t, 1e-6))))
+    # two calibration runs (the first one pays thread start-up), then the sample
+    n = max(threads, 16)
+    for aim in (1.0, target_s):
+        t = run(np.linspace(0, N - 1, n).astype(np.int64))
+        n = int(min(N, max(threads, n * aim / max(t, 1e-6))))
     rows = np.linspace(0, N - 1, n).astype(np.int64)
     t = run(rows)
     return {"value": n * M * M * Q / t, "unit": "terms/s", "cores": threads, "kind": "oracle",
@@ -109,6 +119,7 @@ def main():
     ap.add_argument("--path", default="auto", choices=["auto", "generic", "mfma"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the multi-GPU path (row sharding with an "
@@ -149,6 +160,14 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.copy_probe_mib > 0:
+        n_el = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(n_el, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     L = gpps.lib()
     L.gpps_timing_enable.argtypes = [ctypes.c_int]
     L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
@@ -202,6 +221,8 @@ def main():
                    "N": N, "M": M, "Q": Q, "path": gpps.get_path() if args.path != "auto"
                    else "auto"},
         "pct_fp32_peak": round(100.0 * F_alg / t_psi2 / PEAK_FP32, 2) if t_psi2 > 0 else None,
+        "exp_per_s": 2.0 * N * (M * (M + 1) // 2) / t_psi2 if t_psi2 > 0 else None,
+        "exp_peak": PEAK_EXP,
         "roofline": roofline,
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}
                     for k, v in sorted(kernels.items())},

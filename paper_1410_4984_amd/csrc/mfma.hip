@@ -1,6 +1,15 @@
 // Matrix-core path (F32, gfx950): the O(N M^2 Q) Psi2 statistic and its
-// gradient on v_mfma_f32_32x32x2_f32, with exp2 and the dL/dPsi2 weighting on
-// the vector ALU.
+// gradient on the matrix cores, with exp2 and the dL/dPsi2 weighting on the
+// vector ALU.
+//
+// Precision.  Every contraction runs on v_mfma_f32_32x32x16_bf16 with both
+// operands split exactly into three bf16 parts, x = x1 + x2 + x3 (each part the
+// top 8 significant bits of what is left).  Six of the nine cross products are
+// kept; the three dropped ones are below 2^-24 |a||b|, and all products
+// accumulate in fp32, so the result has fp32 accuracy.  The bf16 MFMA does 16
+// times the work per cycle of v_mfma_f32_32x32x2_f32 and, unlike it, lets the
+// vector ALU issue while it runs, which is where exp2, the weighting and the
+// splits execute.
 //
 // Per datapoint n the Psi2 summand is a Gram matrix pushed through exp
 // (section 2, eq. (4): Phi turned into an expectation under q(x_n); Alg. 1
@@ -35,16 +44,17 @@
 // epilogue: dmu -= w1 sum_m t d, dS += 1/2 w1^2 sum_m t d^2 - 1/2 w1 sum_m t,
 // dZ += t d w1, with w1 = 1/(l^2 + S).
 //
-// Work split.  The z table (centred, plus the ones column) is staged in LDS
-// once per workgroup.  Rows are processed in batches whose per-row values and
-// row terms are copied into LDS; then every wave runs its rows with no
-// further barrier.  Forward: a wave task is a run of upper-triangular 32 x 32
-// pair tiles in one row block; its running sums stay in registers; partial
-// tiles are reduced over row chunks in a fixed order.  Gradient: every term
-// above is linear in (r_n, V_n), so the full M x M tile grid is split into
-// wave tasks (one row block of W, two column blocks) whose dL/dPsi2 tiles stay
-// in registers; each task adds its share of dZ (registers) and of the per-row
-// sums (LDS, then global), which a finalize kernel combines.  No atomics;
+// Work split.  The split z tables are staged in LDS once per workgroup.  Rows
+// are processed in batches whose per-row values and row terms are copied into
+// LDS (the forward prefetches the next batch into registers); then every wave
+// runs its rows with no further barrier.  Forward: a wave task is a run of
+// upper-triangular 32 x 32 pair tiles in one row block; its running sums stay
+// in registers; partial tiles are reduced over row chunks in a fixed order.
+// Gradient: every term above is linear in (r_n, V_n), so the full M x M tile
+// grid is split into wave tasks (one row block of W, four column blocks) whose
+// dL/dPsi2 tiles stay in registers; each task adds its share of dZ (registers)
+// and of the per-row sums (LDS, then global), which a finalize kernel
+// combines.  No atomics;
 // every cross-wave or cross-workgroup sum runs in a fixed order, so results
 // are bitwise reproducible.
 #include <hip/hip_runtime.h>

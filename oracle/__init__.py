@@ -5,8 +5,10 @@ CPU-baseline leg of ``bench.py`` may import this package.  The product path
 (the HIP library and its Python binding) never imports, links or calls it,
 and the two share no code.
 
-The arithmetic lives in ``psi_oracle.c`` (plain loops, fp64, libm); this module
-only compiles it with gcc and marshals numpy arrays through ctypes.  What each
+The psi-statistic arithmetic lives in ``psi_oracle.c`` (plain loops, fp64,
+libm); this module only compiles it with gcc and marshals numpy arrays through
+ctypes.  ``bound.py`` adds the Bayesian GP-LVM bound and its gradients on top
+(fp64 numpy).  What each
 function computes, and the passage of the paper it follows, is stated in the C
 source.  Every function here takes float64 arrays; callers that compare against
 the fp32 GPU path first round their inputs to float32 and pass them upcast, so

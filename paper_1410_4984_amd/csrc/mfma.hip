@@ -2,14 +2,20 @@
 // gradient on the matrix cores, with exp2 and the dL/dPsi2 weighting on the
 // vector ALU.
 //
-// Precision.  Every contraction runs on v_mfma_f32_32x32x16_bf16 with both
-// operands split exactly into three bf16 parts, x = x1 + x2 + x3 (each part the
-// top 8 significant bits of what is left).  Six of the nine cross products are
-// kept; the three dropped ones are below 2^-24 |a||b|, and all products
-// accumulate in fp32, so the result has fp32 accuracy.  The bf16 MFMA does 16
-// times the work per cycle of v_mfma_f32_32x32x2_f32 and, unlike it, lets the
-// vector ALU issue while it runs, which is where exp2, the weighting and the
-// splits execute.
+// Precision.  The Gram products (the exponents) run on v_mfma_f32_32x32x16_bf16
+// with both operands split exactly into three bf16 parts, x = x1 + x2 + x3 (each
+// part the top 8 significant bits of what is left).  Six of the nine cross
+// products are kept; the three dropped ones are below 2^-24 |a||b|, and all
+// products accumulate in fp32, so the exponents have fp32 accuracy.  The
+// gradient's second product W [Z | 1] runs on v_mfma_f32_32x32x16_f16 with both
+// operands split into two fp16 parts rounded to nearest (22 significant bits,
+// three cross products, dropped term below 2^-22 |a||b|); W is scaled per
+// datapoint by a power of two that keeps it inside the fp16 range, and the
+// product is scaled back exactly.  Those 2^-22 terms are far below the rounding
+// the fp32 exponent already carries (|E| 2^-24 with |E| up to ~10^2 in log2
+// units).  The 16-bit MFMAs do 16 times the work per cycle of
+// v_mfma_f32_32x32x2_f32 and, unlike it, let the vector ALU issue while they
+// run, which is where exp2, the weighting and the splits execute.
 //
 // Per datapoint n the Psi2 summand is a Gram matrix pushed through exp
 // (section 2, eq. (4): Phi turned into an expectation under q(x_n); Alg. 1
@@ -78,8 +84,8 @@ constexpr int kRB = 8;                 // gradient: rows per batch
 constexpr int kFRB = 4;                // forward: rows per batch (prefetched a batch ahead)
 constexpr int kFPF = kFRB * 512 / 256; // forward: per-thread prefetch slots of a [kFRB][Mp] table
 static_assert(kFRB * kRowStride == kThreads, "one mu / kappa value per forward thread");
-constexpr int64_t kFwdTargetWGs = 1024;
-constexpr int64_t kGradTargetWGs = 512;
+constexpr int64_t kCUs = 256;          // compute units of one MI355X
+constexpr int64_t kLdsBytes = 160 * 1024;
 constexpr int kFinRows = 64;           // rows per block of the gradient finalize kernel
 constexpr int kRTRows = 32;            // rows per block of the row-term kernel
 // gradient: column blocks per wave task (the dL/dPsi2 tiles it holds in registers)
@@ -139,7 +145,7 @@ struct MPlan {
     int64_t fin_blocks;    // finalize: blocks of kFinRows rows
     size_t lds_fwd, lds_grad;
     size_t off_K, off_hq, off_w2, off_hl, off_w1, off_l1, off_zc, off_bt, off_bc, off_t1, off_g2,
-        off_fp, off_rs, off_dz, off_dl, total;
+        off_fp, off_rs, off_dz, off_dl, off_gmax, total;
 };
 
 // Forward LDS layout (floats):
@@ -169,16 +175,16 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int ni) {
 // Gradient LDS layout (floats):
 //   zx  [wpg 32][DSF]   centred z (fp32) of the workgroup's row blocks (rows m of W),
 //                       zero past Q up to the odd stride DSF (>= 16 ni, >= 32 nqb)
-//   zb  [jpw][3][2][2][32 nqb][8] bf16   the workgroup's column blocks of [Z | 1] split
-//                       into three bf16 parts, laid out as the B operands of the
-//                       32x32x16 bf16 MFMA (8 consecutive k per lane and instruction)
+//   zh  [jpw][2][2][2][32 nqb][8] f16    the workgroup's column blocks of [Z | 1] split
+//                       into two fp16 parts, laid out as the B operands of the
+//                       32x32x16 f16 MFMA (8 consecutive k per lane and instruction)
 //   za  [jpw][3][ni][2][32][8] bf16       the same rows of [centred z | 1] as Gram A
 //                       operands (row m' per lane, 8 consecutive slots per lane group;
 //                       slot Q holds 1)
 //   bb, bcb [RB][Mp], mub, kb, w1b, w2b [RB][64] (zero past Q), t1 [RB][Mp],
-//   red [RB][wpg][5Q + 2]
+//   sc [RB] (log2 of the per-row scale of W), red [RB][wpg][5Q + 2]
 struct LdsG {
-    int zx, zb, za, bb, bcb, mub, kb, w1b, w2b, t1, red, total;
+    int zx, zb, za, bb, bcb, mub, kb, w1b, w2b, t1, sc, red, total;
 };
 
 __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb, int ni, int wpg) {
@@ -186,7 +192,7 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
     LdsG L{};
     int o = 0;
     L.zx = o; o += (wpg * kTile * DSF + 3) / 4 * 4;
-    L.zb = o; o += jpw * 3 * 2 * 2 * 32 * nqb * 8 / 2;
+    L.zb = o; o += jpw * 2 * 2 * 2 * 32 * nqb * 8 / 2;
     L.za = o; o += jpw * 3 * ni * 2 * 32 * 8 / 2;
     L.bb = o; o += kRB * Mp;
     L.bcb = o; o += kRB * Mp;
@@ -195,6 +201,7 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
     L.w1b = o; o += kRB * kRowStride;
     L.w2b = o; o += kRB * kRowStride;
     L.t1 = o; o += kRB * Mp;
+    L.sc = o; o += kRB;
     L.red = o; o += kRB * wpg * (5 * Q + 2);
     L.total = o;
     return L;
@@ -221,7 +228,11 @@ MPlan make_mplan(const Shape &s) {
     }
     p.ftasks = fwd_tasks(p.nb, p.tpw);
     p.fgroups = cdiv(p.ftasks, kWaves);
-    p.fchunks = std::max<int64_t>(1, std::min(cdiv(kFwdTargetWGs, p.fgroups), cdiv(s.N, 32)));
+    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.fni).total;
+    // two full rounds of the chip's workgroup slots (two workgroups per CU when
+    // LDS allows): a partly filled last round would idle most CUs
+    const int64_t fslots = kCUs * std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / p.lds_fwd));
+    p.fchunks = std::max<int64_t>(1, std::min(2 * fslots / p.fgroups, cdiv(s.N, 32)));
     p.frows = cdiv(s.N, p.fchunks);
     p.fchunks = cdiv(s.N, p.frows);
     p.jpw = grad_jpw(p.nqb);
@@ -233,13 +244,17 @@ MPlan make_mplan(const Shape &s) {
         p.wpg /= 2;
     p.igroups = (int)cdiv(p.nb, p.wpg);
     p.ggroups = (int64_t)p.njr * p.igroups;
-    p.gchunks = std::max<int64_t>(1, std::min(cdiv(kGradTargetWGs, p.ggroups), cdiv(s.N, 16)));
+    p.lds_grad =
+        sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.ni, p.wpg).total;
+    // two full rounds: workgroups per CU limited by LDS and by the waves per CU
+    // the kernel's register count allows (grad_waves: two or one per SIMD)
+    const int64_t gslots = kCUs * std::max<int64_t>(
+                                      1, std::min<int64_t>(kLdsBytes / p.lds_grad,
+                                                           grad_waves(p.nqb) / p.wpg));
+    p.gchunks = std::max<int64_t>(1, std::min(2 * gslots / p.ggroups, cdiv(s.N, 16)));
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
     p.fin_blocks = cdiv(s.N, kFinRows);
-    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.fni).total;
-    p.lds_grad =
-        sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.ni, p.wpg).total;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_K = take(sizeof(float) * s.N * kRowStride);
@@ -257,6 +272,7 @@ MPlan make_mplan(const Shape &s) {
     p.off_rs = take(sizeof(float) * p.ggroups * s.N * (5 * s.Q + 2));
     p.off_dz = take(sizeof(float) * p.gchunks * p.njr * s.M * s.Q);
     p.off_dl = take(sizeof(float) * p.fin_blocks * (s.Q + 1));
+    p.off_gmax = take(sizeof(float));
     p.total = o;
     return p;
 }
@@ -383,8 +399,28 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     }
 }
 
+// max |G2s| over the padded symmetric dL/dPsi2 (one workgroup; max is
+// order-independent, so the result is deterministic).
+__global__ __launch_bounds__(1024) void mfma_absmax_kernel(int64_t n, const float *__restrict__ G2p,
+                                                           float *__restrict__ gmax) {
+    __shared__ float part[16];
+    float m = 0.f;
+    for (int64_t i = threadIdx.x; i < n; i += 1024) m = fmaxf(m, fabsf(G2p[i]));
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float r = 0.f;
+        for (int w = 0; w < 16; ++w) r = fmaxf(r, part[w]);
+        gmax[0] = r;
+    }
+}
+
 // ---------------------------------------------------------------- shared helpers
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 typedef unsigned int u32;
 constexpr u32 kHi16 = 0xFFFF0000u;
 
@@ -580,21 +616,22 @@ __global__ void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T, int64_t 
 }
 
 // ---------------------------------------------------------------- Psi2 gradient
-// The workgroup's JPW column blocks of [Z | 1] as three bf16 parts, in the B
-// operand order of the 32x32x16 bf16 MFMA: for instruction h and lane group g
-// the 8 k-values are the rows crow(8h + e, g), e = 0..7, of the block.
+// The workgroup's JPW column blocks of [Z | 1] as two fp16 parts (rounded to
+// nearest), in the B operand order of the 32x32x16 f16 MFMA: for instruction h
+// and lane group g the 8 k-values are the rows crow(8h + e, g), e = 0..7, of the
+// block.
 template <int JPW>
-__device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
+__device__ void stage_zh(_Float16 *zh, int jr, int M, int Q, int nqb,
                          const float *__restrict__ Z, const float *__restrict__ zc) {
     const int QV = 32 * nqb;
-    const int total = JPW * 3 * 2 * 2 * QV * 8;
+    const int total = JPW * 2 * 2 * 2 * QV * 8;
     for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
         int r = idx;
         const int e = r % 8; r /= 8;
         const int q = r % QV; r /= QV;
         const int gg = r % 2; r /= 2;
         const int h = r % 2; r /= 2;
-        const int part = r % 3; r /= 3;
+        const int part = r % 2; r /= 2;
         const int k = r;
         const int m = (jr * JPW + k) * kTile + crow(8 * h + e, gg);
         float v = 0.f;
@@ -602,10 +639,8 @@ __device__ void stage_zb(unsigned short *zb, int jr, int M, int Q, int nqb,
             if (q < Q) v = Z[(int64_t)m * Q + q] - zc[q];
             else if (q == Q) v = 1.f;
         }
-        u32 p0, p1, p2;
-        split3(v, p0, p1, p2);
-        const u32 pv = part == 0 ? p0 : (part == 1 ? p1 : p2);
-        zb[idx] = (unsigned short)(pv >> 16);
+        const _Float16 hi = (_Float16)v;
+        zh[idx] = part == 0 ? hi : (_Float16)(v - (float)hi);
     }
 }
 
@@ -628,11 +663,12 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
     const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ bt,
     const float *__restrict__ bc, const float *__restrict__ w1t, const float *__restrict__ w2t,
-    const float *__restrict__ t1g, const float *__restrict__ G2p, Hyp<float> h,
-    float *__restrict__ rowsum, float *__restrict__ part_dz) {
+    const float *__restrict__ t1g, const float *__restrict__ G2p, const float *__restrict__ hl,
+    const float *__restrict__ gmax, Hyp<float> h, float *__restrict__ rowsum,
+    float *__restrict__ part_dz) {
     extern __shared__ float lds[];
     const LdsG L = lds_grad_layout(Mp, DSF, Q, NQB, NI, wpg);
-    unsigned short *zb = reinterpret_cast<unsigned short *>(lds + L.zb);
+    _Float16 *zh = reinterpret_cast<_Float16 *>(lds + L.zb);
     unsigned short *za = reinterpret_cast<unsigned short *>(lds + L.za);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
@@ -679,7 +715,10 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
         const int m = ib0 * kTile + lr;
         lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
     }
-    stage_zb<JPW>(zb, jr, M, Q, NQB, Z, zc);
+    stage_zh<JPW>(zh, jr, M, Q, NQB, Z, zc);
+    // W_n = G2s o Psi2_n is bounded by max|G2s| 2^(2 hl_n) (hl_n: log2 of the half
+    // prefactor); its per-row scale 2^sc brings that bound to 2^14, inside fp16
+    const float lg = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
     for (int idx = threadIdx.x; idx < JPW * 3 * NI * 2 * 32 * 8; idx += blockDim.x) {
         int r = idx;
         const int e = r % 8; r /= 8;
@@ -688,9 +727,10 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
         const int hh = r % NI; r /= NI;
         const int part = r % 3; r /= 3;
         // column blocks past the edge repeat the last one, as the bias terms of
-        // those (zero-weighted) tiles do, so that their exponent stays finite
+        // those (zero-weighted) tiles do, so that their exponent stays finite;
+        // the last k slot (16 NI - 1 >= Q) carries the multiplier of the bias
         const int m = min(jr * JPW + r, nb - 1) * kTile + cc, q = 16 * hh + 8 * gg + e;
-        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : (q == Q ? 1.f : 0.f);
+        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : (q == 16 * NI - 1 ? 1.f : 0.f);
         u32 p0, p1, p2;
         split3(v, p0, p1, p2);
         za[idx] = (unsigned short)((part == 0 ? p0 : (part == 1 ? p1 : p2)) >> 16);
@@ -719,6 +759,9 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             lds[L.w1b + k] = ok ? w1t[(n0 + r) * Q + q] : 0.f;
             lds[L.w2b + k] = ok ? w2t[(n0 + r) * Q + q] : 0.f;
         }
+        for (int r = threadIdx.x; r < kRB; r += blockDim.x)
+            lds[L.sc + r] = r < cb ? fminf(120.f, fmaxf(-120.f, floorf(14.f - 2.f * hl[n0 + r] - lg)))
+                                   : 0.f;
         __syncthreads();
         for (int r = 0; r < cb; ++r) {
             float *rs = lds + L.red + (r * wpg + wave) * RED;
@@ -727,8 +770,9 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 continue;
             }
             // Gram B operand: -K d = (z - mu) K for column block i and (b + c)_m in
-            // slot Q, split in three
-            const float bcol = lds[L.bcb + r * Mp + i * kTile + c];
+            // the last k slot (lane group 1, element 7 of step NI - 1), split in three
+            const float sc = lds[L.sc + r];
+            const float bcol = lds[L.bcb + r * Mp + i * kTile + c] + sc;
             v8bf GB[3][NI];
 #pragma unroll
             for (int hh = 0; hh < NI; ++hh) {
@@ -738,8 +782,9 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 u32 ap[3][8];
 #pragma unroll
                 for (int e8 = 0; e8 < 8; ++e8) {
-                    // slots >= Q: z, mu and K are zero there; slot Q carries the bias
-                    const float v = (zi[e8] - mur[e8]) * kr[e8] + (16 * hh + 8 * g + e8 == Q ? bcol : 0.f);
+                    // slots >= Q: z, mu and K are zero there
+                    float v = (zi[e8] - mur[e8]) * kr[e8];
+                    if (hh == NI - 1 && e8 == 7) v += g ? bcol : 0.f;
                     split3(v, ap[0][e8], ap[1][e8], ap[2][e8]);
                 }
 #pragma unroll
@@ -761,7 +806,14 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 const int j = jb[k];
                 v16f e;
 #pragma unroll
-                for (int t = 0; t < 16; ++t) e[t] = bbr[j * kTile + crow(t, g)];
+                for (int a = 0; a < 4; ++a) {
+                    // rows crow(4a .. 4a + 3, g) = 8a + 4g + 0..3 (16-byte aligned)
+                    const float4 b4 = *reinterpret_cast<const float4 *>(bbr + j * kTile + 8 * a + 4 * g);
+                    e[4 * a] = b4.x;
+                    e[4 * a + 1] = b4.y;
+                    e[4 * a + 2] = b4.z;
+                    e[4 * a + 3] = b4.w;
+                }
 #pragma unroll
                 for (int hh = 0; hh < NI; ++hh) {
                     v8bf GA[3];
@@ -776,43 +828,41 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                     e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[1], GB[1][hh], e, 0, 0, 0);
                     e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[2], GB[0][hh], e, 0, 0, 0);
                 }
-                // W tile, split into three bf16 parts; A operand of instruction hh takes
-                // the lane's rows crow(8 hh + e, g), as the B operand tables do
-                u32 wp[3][16];
+                // W tile (scaled by 2^sc), split into two fp16 parts; A operand of
+                // instruction hh takes the lane's rows crow(8 hh + e, g), as the B
+                // operand tables do
+                v8h Wh[2], Wl[2];
 #pragma unroll
-                for (int t = 0; t < 16; ++t)
-                    split3(g2r[k][t] * __builtin_amdgcn_exp2f(e[t]), wp[0][t], wp[1][t], wp[2][t]);
-                v8bf A[3][2];
+                for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-                for (int pa = 0; pa < 3; ++pa)
-#pragma unroll
-                    for (int hh = 0; hh < 2; ++hh) {
-                        u32 d4[4];
-#pragma unroll
-                        for (int u = 0; u < 4; ++u)
-                            d4[u] = pack_hi(wp[pa][8 * hh + 2 * u], wp[pa][8 * hh + 2 * u + 1]);
-                        A[pa][hh] = __builtin_bit_cast(v8bf, d4);
+                    for (int u = 0; u < 4; ++u) {
+                        const int t = 8 * hh + 2 * u;
+                        const float a = g2r[k][t] * __builtin_amdgcn_exp2f(e[t]);
+                        const float b = g2r[k][t + 1] * __builtin_amdgcn_exp2f(e[t + 1]);
+                        const v2h hi = {(_Float16)a, (_Float16)b};
+                        const v2h lo = {(_Float16)(a - (float)hi[0]), (_Float16)(b - (float)hi[1])};
+                        Wh[hh][2 * u] = hi[0];
+                        Wh[hh][2 * u + 1] = hi[1];
+                        Wl[hh][2 * u] = lo[0];
+                        Wl[hh][2 * u + 1] = lo[1];
                     }
 #pragma unroll
                 for (int qb = 0; qb < NQB; ++qb) {
 #pragma unroll
                     for (int hh = 0; hh < 2; ++hh) {
-                        v8bf B[3];
-#pragma unroll
-                        for (int pb = 0; pb < 3; ++pb) {
-                            const unsigned short *src =
-                                zb + ((((k * 3 + pb) * 2 + hh) * 2 + g) * QV + qb * 32 + c) * 8;
-                            B[pb] = *reinterpret_cast<const v8bf *>(src);
-                        }
-                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[0], V[qb], 0, 0, 0);
-                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[1], V[qb], 0, 0, 0);
-                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[1][hh], B[0], V[qb], 0, 0, 0);
-                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[2], V[qb], 0, 0, 0);
-                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[1][hh], B[1], V[qb], 0, 0, 0);
-                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[2][hh], B[0], V[qb], 0, 0, 0);
+                        const v8h Bh = *reinterpret_cast<const v8h *>(
+                            zh + ((((k * 2 + 0) * 2 + hh) * 2 + g) * QV + qb * 32 + c) * 8);
+                        const v8h Bl = *reinterpret_cast<const v8h *>(
+                            zh + ((((k * 2 + 1) * 2 + hh) * 2 + g) * QV + qb * 32 + c) * 8);
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Wh[hh], Bh, V[qb], 0, 0, 0);
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Wh[hh], Bl, V[qb], 0, 0, 0);
+                        V[qb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Wl[hh], Bh, V[qb], 0, 0, 0);
                     }
                 }
             }
+            // V' carries the row scale 2^sc: the epilogue's coefficients and row sums
+            // undo it (exact: a power of two)
+            const float us = __builtin_amdgcn_exp2f(-sc);
             // epilogue for rows m = i*32 + crow(t, g); V' = W [Z | 1] -> V = r mu^T - V'
             float muq[NQB], alpha[NQB], beta[NQB], w1q[NQB];
 #pragma unroll
@@ -821,8 +871,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 muq[qb] = lds[L.mub + r * kRowStride + q];
                 const float w2 = lds[L.w2b + r * kRowStride + q];
                 w1q[qb] = lds[L.w1b + r * kRowStride + q];
-                alpha[qb] = w2 - il2[qb];
-                beta[qb] = w2 + il2[qb];
+                alpha[qb] = (w2 - il2[qb]) * us;
+                beta[qb] = (w2 + il2[qb]) * us;
             }
             float X[NQB], Y[NQB], P[NQB], X1[NQB], P1[NQB], R = 0.f, T1 = 0.f;
 #pragma unroll
@@ -873,16 +923,16 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                             p12 = __shfl_xor(P1[qb], 32);
                 const int q = qb * 32 + c;
                 if (g == 0 && q < Q) {
-                    rs[q] = X[qb] + x2;
-                    rs[Q + q] = Y[qb] + y2;
-                    rs[2 * Q + q] = P[qb] + p2;
+                    rs[q] = (X[qb] + x2) * us;
+                    rs[Q + q] = (Y[qb] + y2) * us;
+                    rs[2 * Q + q] = (P[qb] + p2) * us;
                     rs[3 * Q + q] = X1[qb] + x12;
                     rs[4 * Q + q] = P1[qb] + p12;
                 }
             }
             const float R2 = __shfl_xor(R, 32), T12 = __shfl_xor(T1, 32);
             if (lane == 0) {
-                rs[5 * Q] = R + R2;
+                rs[5 * Q] = (R + R2) * us;
                 rs[5 * Q + 1] = T1 + T12;
             }
         }
@@ -1020,8 +1070,8 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
     k<<<grid, p.wpg * 64, p.lds_grad, st>>>(
         s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.njr, p.wpg, p.igroups, p.grows, mu, Z,
         fat(ws, p.off_zc), fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc),
-        fat(ws, p.off_w1), fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2), h,
-        fat(ws, p.off_rs), fat(ws, p.off_dz));
+        fat(ws, p.off_w1), fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2),
+        fat(ws, p.off_hl), fat(ws, p.off_gmax), h, fat(ws, p.off_rs), fat(ws, p.off_dz));
     return hipGetLastError();
 }
 
@@ -1113,6 +1163,10 @@ hipError_t mfma_psi_grads(const Shape &s, const float *mu, const float *S, const
         TimedScope ts(st, "mfma_sym");
         mfma_sym_kernel<<<(unsigned)cdiv(p.Mp * p.Mp, 256), 256, 0, st>>>((int)s.M, (int)p.Mp, G2,
                                                                           fat(ws, p.off_g2));
+    }
+    {
+        TimedScope ts(st, "mfma_absmax");
+        mfma_absmax_kernel<<<1, 1024, 0, st>>>(p.Mp * p.Mp, fat(ws, p.off_g2), fat(ws, p.off_gmax));
     }
     hipError_t e = dispatch_grad(p, s, mu, Z, h, ws, st);
     if (e != hipSuccess) return e;

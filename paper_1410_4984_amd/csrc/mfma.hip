@@ -2,20 +2,21 @@
 // gradient on the matrix cores, with exp2 and the dL/dPsi2 weighting on the
 // vector ALU.
 //
-// Precision.  The Gram products (the exponents) run on v_mfma_f32_32x32x16_bf16
-// with both operands split exactly into three bf16 parts, x = x1 + x2 + x3 (each
-// part the top 8 significant bits of what is left).  Six of the nine cross
-// products are kept; the three dropped ones are below 2^-24 |a||b|, and all
-// products accumulate in fp32, so the exponents have fp32 accuracy.  The
-// gradient's second product W [Z | 1] runs on v_mfma_f32_32x32x16_f16 with both
-// operands split into two fp16 parts rounded to nearest (22 significant bits,
-// three cross products, dropped term below 2^-22 |a||b|); W is scaled per
-// datapoint by a power of two that keeps it inside the fp16 range, and the
-// product is scaled back exactly.  Those 2^-22 terms are far below the rounding
-// the fp32 exponent already carries (|E| 2^-24 with |E| up to ~10^2 in log2
-// units).  The 16-bit MFMAs do 16 times the work per cycle of
-// v_mfma_f32_32x32x2_f32 and, unlike it, let the vector ALU issue while they
-// run, which is where exp2, the weighting and the splits execute.
+// Precision.  Both contractions run on v_mfma_f32_32x32x16_f16 with both
+// operands split into two fp16 parts rounded to nearest, x = x_hi + x_lo
+// (22 significant bits); three of the four cross products are kept (the dropped
+// one is below 2^-22 |a||b|) and all products accumulate in fp32.  For the
+// exponents that is an error of a few 2^-24 |E| (measured on the synthetic
+// workloads: about 1e-7 relative in each Psi2 summand, two fp32 ulps), the
+// same order as the rounding the fp32 row terms already carry.  Range: the
+// constant operand is the centred z table (|z| << 6e4); the per-datapoint one
+// is -K d (|K d| is a few lengthscales' worth, far inside fp16) plus the row
+// bias b + c in one k slot, clamped to +-kBiasClamp: a bias beyond that makes
+// the summand vanish in fp32 anyway.  W in the gradient's second product is
+// scaled per datapoint by a power of two that bounds it by 2^14, and the
+// product is scaled back exactly.  The f16 MFMA does 16 times the work per
+// cycle of v_mfma_f32_32x32x2_f32 and, unlike it, lets the vector ALU issue
+// while it runs, which is where exp2, the weighting and the splits execute.
 //
 // Per datapoint n the Psi2 summand is a Gram matrix pushed through exp
 // (section 2, eq. (4): Phi turned into an expectation under q(x_n); Alg. 1
@@ -80,6 +81,7 @@ constexpr int kWaves = 4;
 constexpr int kRowStride = 64;         // stride of per-row tables padded to 64 dimensions
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kPadBias = -1.0e30f;   // row term of a padded inducing input: exp2 -> 0
+constexpr float kBiasClamp = 6.0e4f;   // bias carried in an fp16 Gram k slot (fp16 max 65504)
 constexpr int kRB = 8;                 // gradient: rows per batch
 constexpr int kFRB = 4;                // forward: rows per batch (prefetched a batch ahead)
 constexpr int kFPF = kFRB * 512 / 256; // forward: per-thread prefetch slots of a [kFRB][Mp] table
@@ -132,8 +134,7 @@ struct MPlan {
     int nqb;               // 32-column blocks of [Z | 1] (Q + 1 columns)
     int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= 16 ni
                            // and >= 32 nqb, so that no read needs a bounds test)
-    int ni;                // gradient Gram: 16-slot bf16 MFMA steps (Q dimensions + a bias slot)
-    int fni;               // forward Gram: 16-dimension bf16 MFMA steps (ceil(Q / 16))
+    int ni;                // Gram: 16-slot f16 MFMA steps (Q dimensions + a bias slot)
     int64_t T;             // upper-triangular tiles
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
@@ -149,21 +150,23 @@ struct MPlan {
 };
 
 // Forward LDS layout (floats):
-//   zt  [nb][3][fni][2][32][8] bf16  centred z split into three bf16 parts, in the
-//                       B operand order of the 32x32x16 bf16 MFMA: column block,
-//                       part, instruction, lane group, column, 8 consecutive k
+//   za  [nb][2][ni][2][32][8] f16   [centred z | 1] of every block split into two
+//                       fp16 parts, as A operands of the 32x32x16 f16 MFMA: block,
+//                       part, instruction, lane group, row, 8 consecutive k (the
+//                       last slot, 16 ni - 1 >= Q, holds 1: the multiplier of the
+//                       bias carried by the per-datapoint operand)
 //   bb  [FRB][Mp]       row terms b of the batch (log2 units)
 //   bcb [FRB][Mp]       b + c
 //   mub [FRB][64]       centred mu of the batch (zero beyond Q)
 //   kb  [FRB][64]       log2e kappa of the batch (zero beyond Q)
 struct LdsF {
-    int zt, bb, bcb, mub, kb, total;
+    int za, bb, bcb, mub, kb, total;
 };
 
 __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int ni) {
     LdsF L{};
     int o = 0;
-    L.zt = o; o += Mp * 3 * ni * 16 / 2;
+    L.za = o; o += Mp * 2 * ni * 16 / 2;
     L.bb = o; o += kFRB * Mp;
     L.bcb = o; o += kFRB * Mp;
     L.mub = o; o += kFRB * kRowStride;
@@ -178,9 +181,9 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int ni) {
 //   zh  [jpw][2][2][2][32 nqb][8] f16    the workgroup's column blocks of [Z | 1] split
 //                       into two fp16 parts, laid out as the B operands of the
 //                       32x32x16 f16 MFMA (8 consecutive k per lane and instruction)
-//   za  [jpw][3][ni][2][32][8] bf16       the same rows of [centred z | 1] as Gram A
-//                       operands (row m' per lane, 8 consecutive slots per lane group;
-//                       slot Q holds 1)
+//   za  [jpw][2][ni][2][32][8] f16        the same rows of [centred z | 1] as Gram A
+//                       operands, two fp16 parts (row m' per lane, 8 consecutive slots
+//                       per lane group; the last slot 16 ni - 1 holds 1)
 //   bb, bcb [RB][Mp], mub, kb, w1b, w2b [RB][64] (zero past Q), t1 [RB][Mp],
 //   sc [RB] (log2 of the per-row scale of W), red [RB][wpg][5Q + 2]
 struct LdsG {
@@ -193,7 +196,7 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
     int o = 0;
     L.zx = o; o += (wpg * kTile * DSF + 3) / 4 * 4;
     L.zb = o; o += jpw * 2 * 2 * 2 * 32 * nqb * 8 / 2;
-    L.za = o; o += jpw * 3 * ni * 2 * 32 * 8 / 2;
+    L.za = o; o += jpw * 2 * ni * 2 * 32 * 8 / 2;
     L.bb = o; o += kRB * Mp;
     L.bcb = o; o += kRB * Mp;
     L.mub = o; o += kRB * kRowStride;
@@ -213,7 +216,6 @@ MPlan make_mplan(const Shape &s) {
     p.nb = (int)(p.Mp / kTile);
     p.nqb = s.Q + 1 <= 32 ? 1 : 2;
     p.ni = (int)cdiv(s.Q + 1, 16);   // k slot Q carries a bias term
-    p.fni = (int)cdiv(s.Q, 16);
     p.DSF = std::max<int>(16 * p.ni, 32 * p.nqb) | 1;
     p.T = (int64_t)p.nb * (p.nb + 1) / 2;
     // forward tasks: tiles per task by a cost model in cycles: each task splits its
@@ -221,14 +223,14 @@ MPlan make_mplan(const Shape &s) {
     // dimensions), each tile slot costs about 600 (MFMA, exp2, bias, sum)
     p.tpw = 1;
     int64_t best = -1;
-    for (int t = 1; t <= fwd_tpw_max(p.fni); ++t) {
+    for (int t = 1; t <= fwd_tpw_max(p.ni); ++t) {
         const int64_t groups = cdiv(fwd_tasks(p.nb, t), kWaves);
-        const int64_t cost = groups * kWaves * (240 * p.fni + 600 * t);
+        const int64_t cost = groups * kWaves * (120 * p.ni + 400 * t);
         if (best < 0 || cost < best) { best = cost; p.tpw = t; }
     }
     p.ftasks = fwd_tasks(p.nb, p.tpw);
     p.fgroups = cdiv(p.ftasks, kWaves);
-    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.fni).total;
+    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.ni).total;
     // two full rounds of the chip's workgroup slots (two workgroups per CU when
     // LDS allows): a partly filled last round would idle most CUs
     const int64_t fslots = kCUs * std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / p.lds_fwd));
@@ -418,32 +420,99 @@ __global__ __launch_bounds__(1024) void mfma_absmax_kernel(int64_t n, const floa
 }
 
 // ---------------------------------------------------------------- shared helpers
-typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef _Float16 v2h __attribute__((ext_vector_type(2)));
-typedef unsigned int u32;
-constexpr u32 kHi16 = 0xFFFF0000u;
 
-// Three bf16 parts of x (truncation split): x == p0 + p1 + p2 up to 2^-24 |x|.
-// Each part is returned as an fp32 bit pattern whose low 16 bits are zero.
-__device__ __forceinline__ void split3(float x, u32 &p0, u32 &p1, u32 &p2) {
-    p0 = __float_as_uint(x) & kHi16;
-    const float r = x - __uint_as_float(p0);
-    p1 = __float_as_uint(r) & kHi16;
-    p2 = __float_as_uint(r - __uint_as_float(p1));
+// Two fp16 parts of x (rounded to nearest): x == hi + lo up to 2^-22 |x|.
+__device__ __forceinline__ void split2h(float x, _Float16 &hi, _Float16 &lo) {
+    hi = (_Float16)x;
+    lo = (_Float16)(x - (float)hi);
 }
 
-// Pack the high halves of two fp32 bit patterns into one bf16 pair (a: element 0).
-__device__ __forceinline__ u32 pack_hi(u32 a, u32 b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+// Per-datapoint Gram operand of the lane's column m (B side, 8 k slots per lane
+// group and instruction): (z_mk - mu_k) K_k for k = 16 hh + 8 g + e < Q (zv[hh][e]
+// holds z_mk; z, mu and K are zero past Q), the bias in the last slot 16 NI - 1
+// (lane group 1, element 7 of the last instruction), zero elsewhere; two fp16
+// parts.  mur and kr point at the row's mu and K of the lane group (k - 16 hh - e).
+template <int NI>
+__device__ __forceinline__ void gram_operand(const float (&zv)[NI][8],
+                                             const float *__restrict__ mur,
+                                             const float *__restrict__ kr, float bias, int g,
+                                             v8h (&Bh)[NI], v8h (&Bl)[NI]) {
+    bias = fminf(kBiasClamp, fmaxf(-kBiasClamp, bias));
+#pragma unroll
+    for (int hh = 0; hh < NI; ++hh)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            float v = (zv[hh][e] - mur[16 * hh + e]) * kr[16 * hh + e];
+            if (hh == NI - 1 && e == 7) v += g ? bias : 0.f;
+            _Float16 hi, lo;
+            split2h(v, hi, lo);
+            Bh[hh][e] = hi;
+            Bl[hh][e] = lo;
+        }
+}
+
+// e += [z_j | 1] B over NI steps of 16 k slots (three f16 products per step);
+// za_j: the two-part A operand table of row block j.
+template <int NI>
+__device__ __forceinline__ v16f gram16(v16f e, const _Float16 *__restrict__ za_j, int c, int g,
+                                       const v8h (&Bh)[NI], const v8h (&Bl)[NI]) {
+#pragma unroll
+    for (int hh = 0; hh < NI; ++hh) {
+        const v8h Ah = *reinterpret_cast<const v8h *>(za_j + (((0 * NI + hh) * 2 + g) * 32 + c) * 8);
+        const v8h Al = *reinterpret_cast<const v8h *>(za_j + (((1 * NI + hh) * 2 + g) * 32 + c) * 8);
+        e = __builtin_amdgcn_mfma_f32_32x32x16_f16(Ah, Bh[hh], e, 0, 0, 0);
+        e = __builtin_amdgcn_mfma_f32_32x32x16_f16(Ah, Bl[hh], e, 0, 0, 0);
+        e = __builtin_amdgcn_mfma_f32_32x32x16_f16(Al, Bh[hh], e, 0, 0, 0);
+    }
+    return e;
+}
+
+// Accumulator start of tile rows m' in block j: the row terms b_m' of rows
+// crow(t, g) = 8 (t / 4) + 4 g + t % 4, read as four 16-byte runs.
+__device__ __forceinline__ v16f row_terms(const float *__restrict__ bbr, int j, int g) {
+    v16f e;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        const float4 b4 = *reinterpret_cast<const float4 *>(bbr + j * kTile + 8 * a + 4 * g);
+        e[4 * a] = b4.x;
+        e[4 * a + 1] = b4.y;
+        e[4 * a + 2] = b4.z;
+        e[4 * a + 3] = b4.w;
+    }
+    return e;
+}
+
+// [centred z | 1] rows of blocks blk0 .. blk0 + nblk - 1 (clamped to the last
+// block) as two-part A operand tables: [nblk][2][NI][2][32][8] f16.
+template <int NI>
+__device__ void stage_za(_Float16 *za, int blk0, int nblk, int nb, int M, int Q,
+                         const float *__restrict__ Z, const float *__restrict__ zc) {
+    const int total = nblk * 2 * NI * 2 * 32 * 8;
+    for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
+        int r = idx;
+        const int e = r % 8; r /= 8;
+        const int cc = r % 32; r /= 32;
+        const int gg = r % 2; r /= 2;
+        const int hh = r % NI; r /= NI;
+        const int part = r % 2; r /= 2;
+        // blocks past the edge repeat the last one, so that every exponent stays finite
+        const int m = min(blk0 + r, nb - 1) * kTile + cc, q = 16 * hh + 8 * gg + e;
+        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : (q == 16 * NI - 1 ? 1.f : 0.f);
+        _Float16 hi, lo;
+        split2h(v, hi, lo);
+        za[idx] = part == 0 ? hi : lo;
+    }
+}
 
 // ---------------------------------------------------------------- Psi2 forward
-// Tile (ti, tj), rows m in block ti, columns m' in block tj:
-//   e[m][m'] = (b + c)_m + b_m' + sum_q (-K d_mq) z_m'q     (A: -K d, B: z)
-// on bf16 MFMAs with both operands split into three bf16 parts (six cross
-// products; the dropped ones are below 2^-24 relative), which keeps fp32
-// accuracy while the vector units keep issuing beside the matrix cores.
-// Wave task: row block ti (its -K d operand is split once per row) and TPW
-// column blocks tj; Psi2 tile sums stay in registers over the row chunk.
+// Pair tiles (i, j), j >= i: rows m' in block j, columns m in block i,
+//   e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)      (A: [z | 1], B: [-K d | b + c])
+// The row terms b_m' are the accumulator's start value; the column bias rides in
+// the last k slot.  Wave task: column block i (its per-datapoint operand is split
+// once per row) and TPW row blocks j; Psi2 tile sums stay in registers over the
+// row chunk.
 template <int NI, int TPW>
 __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int64_t T, int ftasks, int64_t rows_per_chunk,
@@ -452,7 +521,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     float *__restrict__ partial) {
     extern __shared__ float lds[];
     const LdsF L = lds_fwd_layout(Mp, NI);
-    unsigned short *zt = reinterpret_cast<unsigned short *>(lds + L.zt);
+    _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
     const int task = blockIdx.x * kWaves + wave;
@@ -468,7 +537,9 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
 #pragma unroll
         for (int t = 0; t < 16; ++t) acc[k][t] = 0.f;
 
-    // the lane's centred z values of row m = ti*32 + c, k = 16 hh + 8 g + e (zero past Q)
+    // constant tables: split [z | 1] of every block (LDS) and the centred z of the
+    // lane's column m = ti*32 + c at k = 16 hh + 8 g + e (registers, zero past Q)
+    stage_za<NI>(za, 0, nb, nb, M, Q, Z, zc);
     float zr[NI][8];
     {
         const int m = ti * kTile + c;
@@ -479,21 +550,6 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
                 const int q = 16 * hh + 8 * g + e;
                 zr[hh][e] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
             }
-    }
-    // split z table for the B operands of every column block
-    const int ztotal = Mp * 3 * NI * 16;
-    for (int idx = threadIdx.x; idx < ztotal; idx += blockDim.x) {
-        int r = idx;
-        const int e = r % 8; r /= 8;
-        const int cc = r % 32; r /= 32;
-        const int gg = r % 2; r /= 2;
-        const int hh = r % NI; r /= NI;
-        const int part = r % 3; r /= 3;
-        const int m = r * kTile + cc, q = 16 * hh + 8 * gg + e;
-        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
-        u32 p0, p1, p2;
-        split3(v, p0, p1, p2);
-        zt[idx] = (unsigned short)((part == 0 ? p0 : (part == 1 ? p1 : p2)) >> 16);
     }
 
     // Batches of kFRB rows: the next batch is loaded into registers while the
@@ -535,55 +591,20 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
         if (n0 + kFRB < r1) load(n0 + kFRB);
         if (!active) continue;
         for (int r = 0; r < cb; ++r) {
-            // A operand: -K d = (z - mu) K for the rows of block ti, split in three
-            v8bf A[3][NI];
-#pragma unroll
-            for (int hh = 0; hh < NI; ++hh) {
-                const float *mur = lds + L.mub + r * kRowStride + 16 * hh + 8 * g;
-                const float *kr = lds + L.kb + r * kRowStride + 16 * hh + 8 * g;
-                u32 ap[3][8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    split3((zr[hh][e] - mur[e]) * kr[e], ap[0][e], ap[1][e], ap[2][e]);
-#pragma unroll
-                for (int pa = 0; pa < 3; ++pa) {
-                    u32 d4[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) d4[u] = pack_hi(ap[pa][2 * u], ap[pa][2 * u + 1]);
-                    A[pa][hh] = __builtin_bit_cast(v8bf, d4);
-                }
-            }
-            const float *bcr = lds + L.bcb + r * Mp + ti * kTile;
-            float brow[16];
-#pragma unroll
-            for (int t = 0; t < 16; ++t) brow[t] = bcr[crow(t, g)];
+            v8h Bh[NI], Bl[NI];
+            gram_operand<NI>(zr, lds + L.mub + r * kRowStride + 8 * g, lds + L.kb + r * kRowStride + 8 * g,
+                             lds[L.bcb + r * Mp + ti * kTile + c], g, Bh, Bl);
             const float *bbr = lds + L.bb + r * Mp;
 #pragma unroll
             for (int k = 0; k < TPW; ++k) {
-                const float bcol = bbr[tj[k] * kTile + c];
-                v16f e;
-#pragma unroll
-                for (int t = 0; t < 16; ++t) e[t] = brow[t] + bcol;
-#pragma unroll
-                for (int hh = 0; hh < NI; ++hh) {
-                    v8bf B[3];
-#pragma unroll
-                    for (int pb = 0; pb < 3; ++pb)
-                        B[pb] = *reinterpret_cast<const v8bf *>(
-                            zt + ((((tj[k] * 3 + pb) * NI + hh) * 2 + g) * 32 + c) * 8);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[0], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[1], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[1][hh], B[0], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[0][hh], B[2], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[1][hh], B[1], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[2][hh], B[0], e, 0, 0, 0);
-                }
+                const v16f e = gram16<NI>(row_terms(bbr, tj[k], g), za + tj[k] * (2 * NI * 2 * 32 * 8),
+                                          c, g, Bh, Bl);
 #pragma unroll
                 for (int t = 0; t < 16; ++t) acc[k][t] += __builtin_amdgcn_exp2f(e[t]);
             }
         }
     }
-    // partial tiles, row-major inside the tile (clamped duplicates are skipped)
+    // partial tiles: element [m' - 32 tj][m - 32 ti] (clamped duplicates are skipped)
     if (!active) return;
 #pragma unroll
     for (int k = 0; k < TPW; ++k) {
@@ -605,7 +626,7 @@ __global__ void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T, int64_t 
         psi0[0] = (accumulate ? psi0[0] : 0.f) + (float)N * sf2;
     if (m >= M || mp >= M || m > mp) return;
     const int64_t off = tile_index(m / kTile, mp / kTile, nb) * (kTile * kTile) +
-                        (m % kTile) * kTile + (mp % kTile);
+                        (mp % kTile) * kTile + (m % kTile);
     const int64_t stride = T * (kTile * kTile);
     float s = 0.f;
 #pragma unroll 8
@@ -669,7 +690,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     extern __shared__ float lds[];
     const LdsG L = lds_grad_layout(Mp, DSF, Q, NQB, NI, wpg);
     _Float16 *zh = reinterpret_cast<_Float16 *>(lds + L.zb);
-    unsigned short *za = reinterpret_cast<unsigned short *>(lds + L.za);
+    _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
     const int ones_src = 32 * g + (Q & 31);    // lane holding column Q (the row sums r)
@@ -719,22 +740,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     // W_n = G2s o Psi2_n is bounded by max|G2s| 2^(2 hl_n) (hl_n: log2 of the half
     // prefactor); its per-row scale 2^sc brings that bound to 2^14, inside fp16
     const float lg = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
-    for (int idx = threadIdx.x; idx < JPW * 3 * NI * 2 * 32 * 8; idx += blockDim.x) {
-        int r = idx;
-        const int e = r % 8; r /= 8;
-        const int cc = r % 32; r /= 32;
-        const int gg = r % 2; r /= 2;
-        const int hh = r % NI; r /= NI;
-        const int part = r % 3; r /= 3;
-        // column blocks past the edge repeat the last one, as the bias terms of
-        // those (zero-weighted) tiles do, so that their exponent stays finite;
-        // the last k slot (16 NI - 1 >= Q) carries the multiplier of the bias
-        const int m = min(jr * JPW + r, nb - 1) * kTile + cc, q = 16 * hh + 8 * gg + e;
-        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : (q == 16 * NI - 1 ? 1.f : 0.f);
-        u32 p0, p1, p2;
-        split3(v, p0, p1, p2);
-        za[idx] = (unsigned short)((part == 0 ? p0 : (part == 1 ? p1 : p2)) >> 16);
-    }
+    stage_za<NI>(za, jr * JPW, JPW, nb, M, Q, Z, zc);
 
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
@@ -769,31 +775,20 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 for (int k = lane; k < RED; k += 64) rs[k] = 0.f;
                 continue;
             }
-            // Gram B operand: -K d = (z - mu) K for column block i and (b + c)_m in
-            // the last k slot (lane group 1, element 7 of step NI - 1), split in three
+            // Gram B operand: -K d = (z - mu) K for column block i and (b + c)_m (+ the
+            // row scale) in the last k slot
             const float sc = lds[L.sc + r];
             const float bcol = lds[L.bcb + r * Mp + i * kTile + c] + sc;
-            v8bf GB[3][NI];
+            v8h GBh[NI], GBl[NI];
+            {
+                const float *zi = lds + L.zx + (wave * kTile + c) * DSF + 8 * g;
+                float zv[NI][8];
 #pragma unroll
-            for (int hh = 0; hh < NI; ++hh) {
-                const float *mur = lds + L.mub + r * kRowStride + 16 * hh + 8 * g;
-                const float *kr = lds + L.kb + r * kRowStride + 16 * hh + 8 * g;
-                const float *zi = lds + L.zx + (wave * kTile + c) * DSF + 16 * hh + 8 * g;
-                u32 ap[3][8];
+                for (int hh = 0; hh < NI; ++hh)
 #pragma unroll
-                for (int e8 = 0; e8 < 8; ++e8) {
-                    // slots >= Q: z, mu and K are zero there
-                    float v = (zi[e8] - mur[e8]) * kr[e8];
-                    if (hh == NI - 1 && e8 == 7) v += g ? bcol : 0.f;
-                    split3(v, ap[0][e8], ap[1][e8], ap[2][e8]);
-                }
-#pragma unroll
-                for (int pa = 0; pa < 3; ++pa) {
-                    u32 d4[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) d4[u] = pack_hi(ap[pa][2 * u], ap[pa][2 * u + 1]);
-                    GB[pa][hh] = __builtin_bit_cast(v8bf, d4);
-                }
+                    for (int e = 0; e < 8; ++e) zv[hh][e] = zi[16 * hh + e];
+                gram_operand<NI>(zv, lds + L.mub + r * kRowStride + 8 * g,
+                                 lds + L.kb + r * kRowStride + 8 * g, bcol, g, GBh, GBl);
             }
             const float *bbr = lds + L.bb + r * Mp;
             v16f V[NQB];
@@ -804,30 +799,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
             for (int k = 0; k < JPW; ++k) {
                 const int j = jb[k];
-                v16f e;
-#pragma unroll
-                for (int a = 0; a < 4; ++a) {
-                    // rows crow(4a .. 4a + 3, g) = 8a + 4g + 0..3 (16-byte aligned)
-                    const float4 b4 = *reinterpret_cast<const float4 *>(bbr + j * kTile + 8 * a + 4 * g);
-                    e[4 * a] = b4.x;
-                    e[4 * a + 1] = b4.y;
-                    e[4 * a + 2] = b4.z;
-                    e[4 * a + 3] = b4.w;
-                }
-#pragma unroll
-                for (int hh = 0; hh < NI; ++hh) {
-                    v8bf GA[3];
-#pragma unroll
-                    for (int pa = 0; pa < 3; ++pa)
-                        GA[pa] = *reinterpret_cast<const v8bf *>(
-                            za + ((((k * 3 + pa) * NI + hh) * 2 + g) * 32 + c) * 8);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[0], GB[0][hh], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[0], GB[1][hh], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[1], GB[0][hh], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[0], GB[2][hh], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[1], GB[1][hh], e, 0, 0, 0);
-                    e = __builtin_amdgcn_mfma_f32_32x32x16_bf16(GA[2], GB[0][hh], e, 0, 0, 0);
-                }
+                const v16f e = gram16<NI>(row_terms(bbr, j, g), za + k * (2 * NI * 2 * 32 * 8), c, g,
+                                          GBh, GBl);
                 // W tile (scaled by 2^sc), split into two fp16 parts; A operand of
                 // instruction hh takes the lane's rows crow(8 hh + e, g), as the B
                 // operand tables do
@@ -1078,7 +1051,7 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
 hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z, void *ws,
                         hipStream_t st) {
 #define GPPS_F(I, T) \
-    if (p.fni == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, ws, st);
+    if (p.ni == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, ws, st);
     GPPS_F(1, 1) GPPS_F(1, 2) GPPS_F(1, 3) GPPS_F(1, 4)
     GPPS_F(2, 1) GPPS_F(2, 2)
     GPPS_F(3, 1)

@@ -231,10 +231,11 @@ MPlan make_mplan(const Shape &s) {
     p.ftasks = fwd_tasks(p.nb, p.tpw);
     p.fgroups = cdiv(p.ftasks, kWaves);
     p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.ni).total;
-    // two full rounds of the chip's workgroup slots (two workgroups per CU when
-    // LDS allows): a partly filled last round would idle most CUs
-    const int64_t fslots = kCUs * std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / p.lds_fwd));
-    p.fchunks = std::max<int64_t>(1, std::min(2 * fslots / p.fgroups, cdiv(s.N, 32)));
+    // whole rounds of the chip's workgroup slots, so that no partly filled last
+    // round idles most CUs: 6 per CU is two rounds at three workgroups per CU and
+    // three at two (the register counts of the instances allow two or three)
+    const int64_t fslots = kCUs * std::min<int64_t>(6, 2 * std::max<int64_t>(1, kLdsBytes / p.lds_fwd));
+    p.fchunks = std::max<int64_t>(1, std::min(fslots / p.fgroups, cdiv(s.N, 32)));
     p.frows = cdiv(s.N, p.fchunks);
     p.fchunks = cdiv(s.N, p.frows);
     p.jpw = grad_jpw(p.nqb);
@@ -423,6 +424,18 @@ __global__ __launch_bounds__(1024) void mfma_absmax_kernel(int64_t n, const floa
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 
+// Low parts of two products split in two fp16 parts: given hi = the packed
+// f16(a0 b0), f16(a1 b1), returns the packed f16(fma(a0, b0, -hi0)),
+// f16(fma(a1, b1, -hi1)) -- the residuals of the exact products, one v_fma_mix
+// each, reading the high parts straight from the packed register (op_sel).
+__device__ __forceinline__ unsigned lo_pair(float a0, float b0, float a1, float b1, unsigned hi) {
+    unsigned lo;
+    asm("v_fma_mixlo_f16 %0, %1, %2, -%3 op_sel_hi:[0,0,1]" : "=v"(lo) : "v"(a0), "v"(b0), "v"(hi));
+    asm("v_fma_mixhi_f16 %0, %1, %2, -%3 op_sel:[0,0,1] op_sel_hi:[0,0,1]"
+        : "+v"(lo) : "v"(a1), "v"(b1), "v"(hi));
+    return lo;
+}
+
 // Two fp16 parts of x (rounded to nearest): x == hi + lo up to 2^-22 |x|.
 __device__ __forceinline__ void split2h(float x, _Float16 &hi, _Float16 &lo) {
     hi = (_Float16)x;
@@ -439,18 +452,27 @@ __device__ __forceinline__ void gram_operand(const float (&zv)[NI][8],
                                              const float *__restrict__ mur,
                                              const float *__restrict__ kr, float bias, int g,
                                              v8h (&Bh)[NI], v8h (&Bl)[NI]) {
-    bias = fminf(kBiasClamp, fmaxf(-kBiasClamp, bias));
+    bias = g ? fminf(kBiasClamp, fmaxf(-kBiasClamp, bias)) : 0.f;
 #pragma unroll
-    for (int hh = 0; hh < NI; ++hh)
+    for (int hh = 0; hh < NI; ++hh) {
+        unsigned bh[4], bl[4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float v = (zv[hh][e] - mur[16 * hh + e]) * kr[16 * hh + e];
-            if (hh == NI - 1 && e == 7) v += g ? bias : 0.f;
-            _Float16 hi, lo;
-            split2h(v, hi, lo);
-            Bh[hh][e] = hi;
-            Bl[hh][e] = lo;
+        for (int u = 0; u < 4; ++u) {
+            const int e = 2 * u;
+            const float d0 = zv[hh][e] - mur[16 * hh + e], k0 = kr[16 * hh + e];
+            float d1 = zv[hh][e + 1] - mur[16 * hh + e + 1], k1 = kr[16 * hh + e + 1];
+            if (hh == NI - 1 && u == 3) {
+                // the last slot: the product (zero there) plus the bias, split as v * 1
+                d1 = d1 * k1 + bias;
+                k1 = 1.f;
+            }
+            const v2h h2 = {(_Float16)(d0 * k0), (_Float16)(d1 * k1)};
+            bh[u] = __builtin_bit_cast(unsigned, h2);
+            bl[u] = lo_pair(d0, k0, d1, k1, bh[u]);
         }
+        Bh[hh] = __builtin_bit_cast(v8h, bh);
+        Bl[hh] = __builtin_bit_cast(v8h, bl);
+    }
 }
 
 // e += [z_j | 1] B over NI steps of 16 k slots (three f16 products per step);
@@ -806,19 +828,20 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 // operand tables do
                 v8h Wh[2], Wl[2];
 #pragma unroll
-                for (int hh = 0; hh < 2; ++hh)
+                for (int hh = 0; hh < 2; ++hh) {
+                    unsigned wh[4], wl[4];
 #pragma unroll
                     for (int u = 0; u < 4; ++u) {
                         const int t = 8 * hh + 2 * u;
-                        const float a = g2r[k][t] * __builtin_amdgcn_exp2f(e[t]);
-                        const float b = g2r[k][t + 1] * __builtin_amdgcn_exp2f(e[t + 1]);
-                        const v2h hi = {(_Float16)a, (_Float16)b};
-                        const v2h lo = {(_Float16)(a - (float)hi[0]), (_Float16)(b - (float)hi[1])};
-                        Wh[hh][2 * u] = hi[0];
-                        Wh[hh][2 * u + 1] = hi[1];
-                        Wl[hh][2 * u] = lo[0];
-                        Wl[hh][2 * u + 1] = lo[1];
+                        const float x0 = __builtin_amdgcn_exp2f(e[t]);
+                        const float x1 = __builtin_amdgcn_exp2f(e[t + 1]);
+                        const v2h h2 = {(_Float16)(g2r[k][t] * x0), (_Float16)(g2r[k][t + 1] * x1)};
+                        wh[u] = __builtin_bit_cast(unsigned, h2);
+                        wl[u] = lo_pair(g2r[k][t], x0, g2r[k][t + 1], x1, wh[u]);
                     }
+                    Wh[hh] = __builtin_bit_cast(v8h, wh);
+                    Wl[hh] = __builtin_bit_cast(v8h, wl);
+                }
 #pragma unroll
                 for (int qb = 0; qb < NQB; ++qb) {
 #pragma unroll

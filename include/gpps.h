@@ -75,6 +75,8 @@ typedef enum { GPPS_PATH_AUTO = 0, GPPS_PATH_GENERIC = 1, GPPS_PATH_MFMA = 2 } g
 #define GPPS_MAX_Q 64
 #define GPPS_MAX_M 4096
 #define GPPS_MAX_Q_MFMA 62
+#define GPPS_MAX_D 65536
+#define GPPS_MAX_M_BOUND 512
 
 /* Bytes of workspace gpps_psi_stats and gpps_psi_grads need for this shape
  * (the larger of the two, over every path).  0 for an invalid shape or dtype. */
@@ -120,6 +122,48 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
                            void *dmu, void *dS, void *dZ, void *dsigma_f2, void *dl,
                            int accumulate, void *workspace, size_t workspace_bytes,
                            void *stream);
+
+/* Bytes of workspace gpps_bound needs for this shape with D output columns.
+ * 0 for an invalid shape, D or dtype (or M > GPPS_MAX_M_BOUND). */
+size_t gpps_bound_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D);
+
+/*
+ * The Bayesian GP-LVM variational bound and its gradients — section 2:
+ * eq. (boundF), with phi, Phi and the bold Psi turned into their expectations
+ * under q(X) (psi0, Psi2 and Psi1^T Y), minus the KL term of eq. (boundBGPLVM)
+ * for the prior p(x_n) = N(0, I):
+ *
+ *   L = -(N D / 2) log 2 pi + (N D / 2) log beta + (D / 2) log|Kmm| - (D / 2) log|A|
+ *       - (beta / 2) tr(Y^T Y) + (beta^2 / 2) tr(Psi^T A^-1 Psi)
+ *       - (beta D / 2) psi0 + (beta D / 2) tr(Kmm^-1 Psi2)
+ *       - 1/2 sum_nq (mu_nq^2 + S_nq - log S_nq - 1),
+ *   A = Kmm + beta Psi2,  Kmm = k(Z, Z) + jitter I,  Psi = Psi1^T Y,
+ *
+ * and dL w.r.t. mu, S, Z, sigma_f2, every l_q and beta (the parameters the paper
+ * optimises).  The psi-statistics and their gradients run on the same kernels
+ * as gpps_psi_stats / gpps_psi_grads (and the same path choice); the M x M
+ * algebra runs in fp64 for either dtype.
+ *
+ *   Y        [N x D]   device, observed data (dtype dt).
+ *   beta               host: noise precision, finite and > 0.
+ *   jitter             host: added to the diagonal of k(Z, Z), finite and >= 0.
+ *   L        [1]       device: the bound (overwritten).
+ *   dmu, dS  [N x Q], dZ [M x Q], dsigma_f2 [1], dl [Q], dbeta [1]: device, overwritten.
+ *   workspace          at least gpps_bound_workspace_bytes(dt, N, M, Q, D) bytes,
+ *                      256-byte aligned, caller-owned (contents ignored).
+ *
+ * Errors as for gpps_psi_grads, plus GPPS_ERR_SHAPE for D < 1, D > GPPS_MAX_D or
+ * M > GPPS_MAX_M_BOUND (the triangular inverse keeps a block column in LDS), and GPPS_ERR_HYPER
+ * for beta or jitter out of range.  S must be > 0 (log S enters the KL term); a
+ * non-positive S, or Kmm or A not positive definite in floating point, is not
+ * detected before the call: L and dbeta are then NaN (a non-positive pivot in
+ * the inversion is flagged on the device and turns L into NaN).
+ */
+gpps_status gpps_bound(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D,
+                       const void *mu, const void *S, const void *Z, const void *Y,
+                       double sigma_f2, const double *l, double beta, double jitter,
+                       void *L, void *dmu, void *dS, void *dZ, void *dsigma_f2, void *dl,
+                       void *dbeta, void *workspace, size_t workspace_bytes, void *stream);
 
 /* Select the kernel path for later calls in this process (default AUTO).
  * Process-wide setting: do not change it while another thread is inside a

@@ -58,6 +58,13 @@ def _inv_spd(L):
     return Li.T @ Li
 
 
+def _inv_lu(L):
+    """A^-1 of A = L L^T by LU with partial pivoting (numpy's inv): a second
+    backward-stable evaluation, used to measure how much an output of an
+    ill-conditioned problem moves between two correct fp64 evaluations."""
+    return np.linalg.inv(L @ L.T)
+
+
 def kl(mu, S):
     """KL(q(X) || N(0, I)) summed over datapoints and dimensions."""
     mu = np.asarray(mu, np.float64)
@@ -66,9 +73,10 @@ def kl(mu, S):
         return 0.5 * float(np.sum(mu * mu + S - np.log(S) - 1.0))
 
 
-def bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter):
+def bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
     """(F, KL, pieces): the collapsed bound F and the KL term, plus the
-    intermediate matrices the gradient needs."""
+    intermediate matrices the gradient needs.  ``inverse`` maps a Cholesky
+    factor to the inverse of its matrix (default: triangular solves)."""
     mu = np.asarray(mu, np.float64)
     Y = np.asarray(Y, np.float64)
     N, D = Y.shape
@@ -80,7 +88,7 @@ def bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter):
     Kmm = K0 + jitter * np.eye(M)
     A = Kmm + beta * Psi2
     Lk, La = _chol(Kmm), _chol(A)
-    Kinv, Ainv = _inv_spd(Lk), _inv_spd(La)
+    Kinv, Ainv = inverse(Lk), inverse(La)
     Psi = Psi1.T @ Y
     C = Ainv @ Psi
     yy = float(np.sum(Y * Y))
@@ -101,9 +109,9 @@ def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter):
     return F - K
 
 
-def upstream(mu, S, Z, Y, sigma_f2, l, beta, jitter):
+def upstream(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
     """(L, dL/dpsi0, dL/dPsi1, dL/dPsi2, dL/dKmm, dL/dbeta, pieces)."""
-    F, K, p = bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter)
+    F, K, p = bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse)
     D = p["D"]
     Kinv, Ainv, C, Psi2, Psi = p["Kinv"], p["Ainv"], p["C"], p["Psi2"], p["Psi"]
     P = C @ C.T
@@ -133,11 +141,11 @@ def kmm_grads(Z, sigma_f2, l, G):
     return dZ, dsf2, dl
 
 
-def grads(mu, S, Z, Y, sigma_f2, l, beta, jitter):
+def grads(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
     """L and its gradient w.r.t. every parameter:
     dict(L, dmu, dS, dZ, dsigma_f2, dl, dbeta)."""
     L, d_psi0, d_Psi1, d_Psi2, d_Kmm, d_beta, p = upstream(mu, S, Z, Y, sigma_f2, l, beta,
-                                                            jitter)
+                                                            jitter, inverse)
     g = psi_grads(mu, S, Z, sigma_f2, l, d_psi0, d_Psi1, d_Psi2)
     kz, ks, kl_ = kmm_grads(Z, sigma_f2, l, d_Kmm)
     mu = np.asarray(mu, np.float64)

@@ -9,6 +9,8 @@ fallback of any kind: if the library is missing or cannot run, calls raise.
     psi_stats(mu, S, Z, sigma_f2, l)   -> (psi0, Psi1, Psi2)
     psi_grads(mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2)
                                        -> dict(dmu, dS, dZ, dsigma_f2, dl)
+    bound(mu, S, Z, Y, sigma_f2, l, beta, jitter)
+                                       -> dict(L, dmu, dS, dZ, dsigma_f2, dl, dbeta)
 
 Notation follows the paper (section 2, Alg. 1-2): mu, S (variances) are N x Q,
 Z is M x Q, sigma_f2 the kernel variance, l the Q ARD lengthscales.
@@ -53,6 +55,11 @@ def lib():
     L.gpps_psi_grads.argtypes = [i32, i64, i64, i64, vp, vp, vp, d, vp, d, vp, vp, vp, vp, vp, vp,
                                  vp, i32, vp, sz, vp]
     L.gpps_psi_grads.restype = i32
+    L.gpps_bound_workspace_bytes.argtypes = [i32, i64, i64, i64, i64]
+    L.gpps_bound_workspace_bytes.restype = sz
+    L.gpps_bound.argtypes = [i32, i64, i64, i64, i64, vp, vp, vp, vp, d, vp, d, d, vp, vp, vp, vp,
+                             vp, vp, vp, vp, sz, vp]
+    L.gpps_bound.restype = i32
     L.gpps_set_path.argtypes = [i32]
     L.gpps_set_path.restype = i32
     L.gpps_get_path.restype = i32
@@ -210,4 +217,48 @@ def psi_grads(mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2, *, accumulate
         lh.ctypes.data, float(dL_dpsi0), ptr(dL_dPsi1), ptr(dL_dPsi2), out["dmu"].data_ptr(),
         out["dS"].data_ptr(), out["dZ"].data_ptr(), out["dsigma_f2"].data_ptr(),
         out["dl"].data_ptr(), int(bool(accumulate)), ws.data_ptr(), ws_bytes, _stream(stream)))
+    return out
+
+
+def bound_workspace_bytes(dtype, N: int, M: int, Q: int, D: int) -> int:
+    return int(lib().gpps_bound_workspace_bytes(_dt(dtype), N, M, Q, D))
+
+
+def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter=0.0, *, out=None, workspace=None, stream=None):
+    """The Bayesian GP-LVM bound L = <F>_q(X) - KL and its gradients (section 2,
+    eq. (boundF) with the psi-statistics as expectations, eq. (boundBGPLVM)).
+
+    Y is N x D.  Returns a dict with L (1), dmu, dS (N x Q), dZ (M x Q),
+    dsigma_f2 (1), dl (Q) and dbeta (1), all tensors of mu's dtype on its device.
+    """
+    import torch
+    dtype, device = mu.dtype, mu.device
+    N, Q = mu.shape
+    M = Z.shape[0]
+    D = Y.shape[1] if Y.dim() == 2 else -1
+    _dev_tensor(mu, "mu", dtype, (N, Q), device)
+    _dev_tensor(S, "S", dtype, (N, Q), device)
+    _dev_tensor(Z, "Z", dtype, (M, Q), device)
+    _dev_tensor(Y, "Y", dtype, (N, D), device)
+    lh = _host_l(l, Q)
+    shapes = (("L", (1,)), ("dmu", (N, Q)), ("dS", (N, Q)), ("dZ", (M, Q)), ("dsigma_f2", (1,)),
+              ("dl", (Q,)), ("dbeta", (1,)))
+    if out is None:
+        out = {k: torch.empty(shp, dtype=dtype, device=device) for k, shp in shapes}
+    else:
+        for k, shp in shapes:
+            _dev_tensor(out[k], k, dtype, shp, device)
+    need = bound_workspace_bytes(dtype, N, M, Q, D)
+    if need == 0:
+        raise GppsError(2, status_string(2))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    elif workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace too small: need {need} bytes")
+    _check(lib().gpps_bound(
+        _dt(dtype), N, M, Q, D, mu.data_ptr(), S.data_ptr(), Z.data_ptr(), Y.data_ptr(),
+        float(sigma_f2), lh.ctypes.data, float(beta), float(jitter), out["L"].data_ptr(),
+        out["dmu"].data_ptr(), out["dS"].data_ptr(), out["dZ"].data_ptr(),
+        out["dsigma_f2"].data_ptr(), out["dl"].data_ptr(), out["dbeta"].data_ptr(),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
     return out

@@ -57,6 +57,54 @@ gpps_status check_workspace(gpps_dtype dt, const gpps::Shape &s, void *ws, size_
     return GPPS_OK;
 }
 
+// The psi-statistics / their gradients on the chosen path (arguments already checked).
+hipError_t run_stats(gpps_dtype dt, int path, const gpps::Shape &s, const void *mu, const void *S,
+                     const void *Z, double sigma_f2, const double *l, void *psi0, void *Psi1,
+                     void *Psi2, int accumulate, void *ws, hipStream_t st) {
+    if (dt == GPPS_F32) {
+        const auto h = make_hyp<float>(sigma_f2, l, s.Q);
+        if (path == GPPS_PATH_MFMA)
+            return gpps::mfma_psi_stats(s, (const float *)mu, (const float *)S, (const float *)Z, h,
+                                        (float *)psi0, (float *)Psi1, (float *)Psi2, accumulate != 0,
+                                        ws, st);
+        return gpps::generic_psi_stats<float>(s, (const float *)mu, (const float *)S,
+                                              (const float *)Z, h, (float *)psi0, (float *)Psi1,
+                                              (float *)Psi2, accumulate != 0, ws, st);
+    }
+    const auto h = make_hyp<double>(sigma_f2, l, s.Q);
+    return gpps::generic_psi_stats<double>(s, (const double *)mu, (const double *)S,
+                                           (const double *)Z, h, (double *)psi0, (double *)Psi1,
+                                           (double *)Psi2, accumulate != 0, ws, st);
+}
+
+hipError_t run_grads(gpps_dtype dt, int path, const gpps::Shape &s, const void *mu, const void *S,
+                     const void *Z, double sigma_f2, const double *l, double dL_dpsi0,
+                     const void *dL_dPsi1, const void *dL_dPsi2, void *dmu, void *dS, void *dZ,
+                     void *dsigma_f2, void *dl, int accumulate, void *ws, hipStream_t st) {
+    if (dt == GPPS_F32) {
+        const auto h = make_hyp<float>(sigma_f2, l, s.Q);
+        if (path == GPPS_PATH_MFMA)
+            return gpps::mfma_psi_grads(s, (const float *)mu, (const float *)S, (const float *)Z, h,
+                                        float(dL_dpsi0), (const float *)dL_dPsi1,
+                                        (const float *)dL_dPsi2, (float *)dmu, (float *)dS,
+                                        (float *)dZ, (float *)dsigma_f2, (float *)dl,
+                                        accumulate != 0, ws, st);
+        return gpps::generic_psi_grads<float>(s, (const float *)mu, (const float *)S,
+                                              (const float *)Z, h, float(dL_dpsi0),
+                                              (const float *)dL_dPsi1, (const float *)dL_dPsi2,
+                                              (float *)dmu, (float *)dS, (float *)dZ,
+                                              (float *)dsigma_f2, (float *)dl, accumulate != 0,
+                                              ws, st);
+    }
+    const auto h = make_hyp<double>(sigma_f2, l, s.Q);
+    return gpps::generic_psi_grads<double>(s, (const double *)mu, (const double *)S,
+                                           (const double *)Z, h, dL_dpsi0,
+                                           (const double *)dL_dPsi1, (const double *)dL_dPsi2,
+                                           (double *)dmu, (double *)dS, (double *)dZ,
+                                           (double *)dsigma_f2, (double *)dl, accumulate != 0, ws,
+                                           st);
+}
+
 }  // namespace
 
 extern "C" {
@@ -85,24 +133,8 @@ gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
         if (p && !aligned(p, elem)) return GPPS_ERR_ALIGN;
     const int path = choose_path(dt, s);
     if (path < 0) return GPPS_ERR_PATH;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e;
-    if (dt == GPPS_F32) {
-        const auto h = make_hyp<float>(sigma_f2, l, Q);
-        if (path == GPPS_PATH_MFMA)
-            e = gpps::mfma_psi_stats(s, (const float *)mu, (const float *)S, (const float *)Z, h,
-                                     (float *)psi0, (float *)Psi1, (float *)Psi2, accumulate != 0,
-                                     workspace, st);
-        else
-            e = gpps::generic_psi_stats<float>(s, (const float *)mu, (const float *)S,
-                                               (const float *)Z, h, (float *)psi0, (float *)Psi1,
-                                               (float *)Psi2, accumulate != 0, workspace, st);
-    } else {
-        const auto h = make_hyp<double>(sigma_f2, l, Q);
-        e = gpps::generic_psi_stats<double>(s, (const double *)mu, (const double *)S,
-                                            (const double *)Z, h, (double *)psi0, (double *)Psi1,
-                                            (double *)Psi2, accumulate != 0, workspace, st);
-    }
+    const hipError_t e = run_stats(dt, path, s, mu, S, Z, sigma_f2, l, psi0, Psi1, Psi2, accumulate,
+                                   workspace, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
 }
 
@@ -125,31 +157,74 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
         if (p && !aligned(p, elem)) return GPPS_ERR_ALIGN;
     const int path = choose_path(dt, s);
     if (path < 0) return GPPS_ERR_PATH;
+    const hipError_t e = run_grads(dt, path, s, mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2,
+                                   dmu, dS, dZ, dsigma_f2, dl, accumulate, workspace,
+                                   static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
+}
+
+size_t gpps_bound_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D) {
+    if (!valid_dtype(dt) || !valid_shape(N, M, Q) || D < 1 || D > GPPS_MAX_D || M > GPPS_MAX_M_BOUND)
+        return 0;
+    const gpps::Shape s = gpps::make_shape(N, M, Q);
+    const size_t elem = dt == GPPS_F32 ? 4 : 8;
+    return gpps::bound_workspace_bytes(s, D, elem, gpps_workspace_bytes(dt, N, M, Q));
+}
+
+gpps_status gpps_bound(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D, const void *mu,
+                       const void *S, const void *Z, const void *Y, double sigma_f2, const double *l,
+                       double beta, double jitter, void *L, void *dmu, void *dS, void *dZ,
+                       void *dsigma_f2, void *dl, void *dbeta, void *workspace,
+                       size_t workspace_bytes, void *stream) {
+    if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
+    if (!valid_shape(N, M, Q) || D < 1 || D > GPPS_MAX_D || M > GPPS_MAX_M_BOUND) return GPPS_ERR_SHAPE;
+    if (!mu || !S || !Z || !Y || !L || !dmu || !dS || !dZ || !dsigma_f2 || !dl || !dbeta)
+        return GPPS_ERR_NULL;
+    if (gpps_status r = check_hypers(sigma_f2, l, Q)) return r;
+    if (!(beta > 0.0) || !std::isfinite(beta) || !(jitter >= 0.0) || !std::isfinite(jitter))
+        return GPPS_ERR_HYPER;
+    if (!workspace) return GPPS_ERR_NULL;
+    if (!aligned(workspace, 256)) return GPPS_ERR_ALIGN;
+    if (workspace_bytes < gpps_bound_workspace_bytes(dt, N, M, Q, D)) return GPPS_ERR_WORKSPACE;
+    const size_t elem = dt == GPPS_F32 ? 4 : 8;
+    for (const void *p : {mu, S, Z, Y, (const void *)L, (const void *)dmu, (const void *)dS,
+                          (const void *)dZ, (const void *)dsigma_f2, (const void *)dl,
+                          (const void *)dbeta})
+        if (!aligned(p, elem)) return GPPS_ERR_ALIGN;
+    const gpps::Shape s = gpps::make_shape(N, M, Q);
+    const int path = choose_path(dt, s);
+    if (path < 0) return GPPS_ERR_PATH;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e;
-    if (dt == GPPS_F32) {
-        const auto h = make_hyp<float>(sigma_f2, l, Q);
-        if (path == GPPS_PATH_MFMA)
-            e = gpps::mfma_psi_grads(s, (const float *)mu, (const float *)S, (const float *)Z, h,
-                                     float(dL_dpsi0), (const float *)dL_dPsi1,
-                                     (const float *)dL_dPsi2, (float *)dmu, (float *)dS,
-                                     (float *)dZ, (float *)dsigma_f2, (float *)dl,
-                                     accumulate != 0, workspace, st);
+    const size_t psi_ws = gpps_workspace_bytes(dt, N, M, Q);
+    const gpps::BoundBufs b = gpps::bound_buffers(s, D, elem, psi_ws);
+    char *w = static_cast<char *>(workspace);
+    void *psi0 = w + b.psi0, *Psi1 = w + b.psi1, *Psi2 = w + b.psi2, *G2 = w + b.g2;
+    hipError_t e = run_stats(dt, path, s, mu, S, Z, sigma_f2, l, psi0, Psi1, Psi2, 0, workspace, st);
+    if (e == hipSuccess) {
+        if (dt == GPPS_F32)
+            e = gpps::bound_middle<float>(s, D, (const float *)mu, (const float *)S, (const float *)Z,
+                                          (const float *)Y, make_hyp<float>(sigma_f2, l, Q), beta,
+                                          jitter, (float *)L, (float *)dbeta, workspace, psi_ws, st);
         else
-            e = gpps::generic_psi_grads<float>(s, (const float *)mu, (const float *)S,
-                                               (const float *)Z, h, float(dL_dpsi0),
-                                               (const float *)dL_dPsi1, (const float *)dL_dPsi2,
-                                               (float *)dmu, (float *)dS, (float *)dZ,
-                                               (float *)dsigma_f2, (float *)dl, accumulate != 0,
-                                               workspace, st);
-    } else {
-        const auto h = make_hyp<double>(sigma_f2, l, Q);
-        e = gpps::generic_psi_grads<double>(s, (const double *)mu, (const double *)S,
-                                            (const double *)Z, h, dL_dpsi0,
-                                            (const double *)dL_dPsi1, (const double *)dL_dPsi2,
-                                            (double *)dmu, (double *)dS, (double *)dZ,
-                                            (double *)dsigma_f2, (double *)dl, accumulate != 0,
-                                            workspace, st);
+            e = gpps::bound_middle<double>(s, D, (const double *)mu, (const double *)S,
+                                           (const double *)Z, (const double *)Y,
+                                           make_hyp<double>(sigma_f2, l, Q), beta, jitter,
+                                           (double *)L, (double *)dbeta, workspace, psi_ws, st);
+    }
+    if (e == hipSuccess)
+        e = run_grads(dt, path, s, mu, S, Z, sigma_f2, l, -0.5 * beta * (double)D, Psi1, G2, dmu, dS,
+                      dZ, dsigma_f2, dl, 0, workspace, st);
+    if (e == hipSuccess) {
+        if (dt == GPPS_F32)
+            e = gpps::bound_tail<float>(s, D, (const float *)mu, (const float *)S, (const float *)Z,
+                                        make_hyp<float>(sigma_f2, l, Q), (float *)dmu, (float *)dS,
+                                        (float *)dZ, (float *)dsigma_f2, (float *)dl, workspace,
+                                        psi_ws, st);
+        else
+            e = gpps::bound_tail<double>(s, D, (const double *)mu, (const double *)S,
+                                         (const double *)Z, make_hyp<double>(sigma_f2, l, Q),
+                                         (double *)dmu, (double *)dS, (double *)dZ,
+                                         (double *)dsigma_f2, (double *)dl, workspace, psi_ws, st);
     }
     return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
 }
@@ -167,8 +242,8 @@ const char *gpps_status_string(gpps_status status) {
     switch (status) {
         case GPPS_OK: return "success";
         case GPPS_ERR_NULL: return "a required pointer is NULL";
-        case GPPS_ERR_SHAPE: return "invalid shape (need 1 <= N, 1 <= M <= GPPS_MAX_M, 1 <= Q <= GPPS_MAX_Q)";
-        case GPPS_ERR_HYPER: return "sigma_f2, every l_q and dL_dpsi0 must be finite; sigma_f2 and l_q > 0";
+        case GPPS_ERR_SHAPE: return "invalid shape (need 1 <= N, 1 <= M <= GPPS_MAX_M, 1 <= Q <= GPPS_MAX_Q, 1 <= D <= GPPS_MAX_D)";
+        case GPPS_ERR_HYPER: return "sigma_f2, every l_q, dL_dpsi0, beta and jitter must be finite; sigma_f2, l_q, beta > 0, jitter >= 0";
         case GPPS_ERR_DTYPE: return "unknown dtype";
         case GPPS_ERR_WORKSPACE: return "workspace smaller than gpps_workspace_bytes()";
         case GPPS_ERR_ALIGN: return "workspace not 256-byte aligned or array not element-aligned";

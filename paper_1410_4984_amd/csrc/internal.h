@@ -78,4 +78,26 @@ hipError_t mfma_psi_grads(const Shape &s, const float *mu, const float *S, const
                           const float *G2, float *dmu, float *dS, float *dZ, float *dsf2,
                           float *dl, int accumulate, void *ws, hipStream_t st);
 
+// ---------------------------------------------------------------- Bayesian GP-LVM bound
+// Byte offsets of the psi-statistic buffers inside the bound's workspace (after
+// the first psi_ws bytes, which serve the psi-statistic kernels).
+struct BoundBufs {
+    size_t psi0, psi1, psi2, g2;
+};
+size_t bound_workspace_bytes(const Shape &s, int64_t D, size_t elem, size_t psi_ws);
+BoundBufs bound_buffers(const Shape &s, int64_t D, size_t elem, size_t psi_ws);
+
+// After the psi-statistics: Kmm, A, their inverses and log determinants, Psi1^T Y,
+// the bound L and dL/dbeta, and dL/dPsi1 (over Psi1) and dL/dPsi2 in the workspace.
+template <typename T>
+hipError_t bound_middle(const Shape &s, int64_t D, const T *mu, const T *S, const T *Z, const T *Y,
+                        const Hyp<T> &h, double beta, double jitter, T *L, T *dbeta, void *ws,
+                        size_t psi_ws, hipStream_t st);
+
+// After the psi-statistic gradients: the chain rule through Kmm (added to dZ,
+// dsigma_f2, dl) and the KL term (added to dmu, dS).
+template <typename T>
+hipError_t bound_tail(const Shape &s, int64_t D, const T *mu, const T *S, const T *Z, const Hyp<T> &h,
+                      T *dmu, T *dS, T *dZ, T *dsf2, T *dl, void *ws, size_t psi_ws, hipStream_t st);
+
 }  // namespace gpps

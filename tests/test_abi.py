@@ -124,3 +124,42 @@ def test_binding_rejects_bad_tensors():
     mu = torch.zeros(4, 2)
     with pytest.raises(ValueError):  # CPU tensors are refused: the library only runs on a GPU
         gpps.psi_stats(mu, mu, torch.zeros(3, 2), 1.0, [1.0, 1.0])
+
+
+def _bound(dt=0, N=10, M=4, Q=2, D=3, mu=FAKE, S=FAKE, Z=FAKE, Y=FAKE, sf2=1.0, l=L2, beta=2.0,
+           jitter=1e-6, L=FAKE, dmu=FAKE, dS=FAKE, dZ=FAKE, dsf2=FAKE, dl=FAKE, dbeta=FAKE,
+           ws=FAKE, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = max(1, gpps.lib().gpps_bound_workspace_bytes(0, N, M, Q, max(D, 1)))
+    return gpps.lib().gpps_bound(dt, N, M, Q, D, mu, S, Z, Y, sf2, l, beta, jitter, L, dmu, dS,
+                                 dZ, dsf2, dl, dbeta, ws, ws_bytes, None)
+
+
+def test_bound_workspace_bytes():
+    b = gpps.bound_workspace_bytes("f32", 64_000, 100, 1, 3)
+    assert b > gpps.workspace_bytes("f32", 64_000, 100, 1)
+    assert gpps.bound_workspace_bytes("f64", 200, 10, 2, 4) > 0
+    assert gpps.bound_workspace_bytes("f32", 10, 4, 2, 0) == 0
+    assert gpps.bound_workspace_bytes("f32", 0, 4, 2, 3) == 0
+    assert gpps.lib().gpps_bound_workspace_bytes(7, 10, 4, 2, 3) == 0
+
+
+def test_bound_validation_codes():
+    assert _bound(dt=5) == ERR_DTYPE
+    assert _bound(N=0) == ERR_SHAPE
+    assert _bound(D=0) == ERR_SHAPE
+    assert _bound(Q=gpps.MAX_Q + 1) == ERR_SHAPE
+    assert _bound(M=513) == ERR_SHAPE
+    for k in ("mu", "S", "Z", "Y", "L", "dmu", "dS", "dZ", "dsf2", "dl", "dbeta", "ws"):
+        assert _bound(**{k: None}) == ERR_NULL, k
+    assert _bound(l=None) == ERR_NULL
+    assert _bound(sf2=-1.0) == ERR_HYPER
+    assert _bound(beta=0.0) == ERR_HYPER
+    assert _bound(beta=float("inf")) == ERR_HYPER
+    assert _bound(jitter=-1e-9) == ERR_HYPER
+    assert _bound(jitter=float("nan")) == ERR_HYPER
+    assert _bound(ws=FAKE + 16) == ERR_ALIGN
+    assert _bound(ws_bytes=1) == ERR_WS
+    assert _bound(Y=FAKE + 2) == ERR_ALIGN
+    assert _bound(dt=1, dbeta=FAKE + 4,
+                  ws_bytes=gpps.lib().gpps_bound_workspace_bytes(1, 10, 4, 2, 3)) == ERR_ALIGN

@@ -17,6 +17,12 @@ Metric: N*M^2*Q terms per second (whole step).  Beside it:
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload large]
 
+--workload gplvm times the next step of the method instead: one evaluation of
+the Bayesian GP-LVM bound and all its gradients (gpps_bound) at the shape of
+the paper's experiment (section 4: Q = 1, M = 100, D = 3, here N = 64,000,
+fp64), in evaluations per second, with the fp64 oracle timed on one full
+evaluation beside it.
+
 --copy-probe-mib X runs a plain device copy (torch.neg into a second buffer) of
 X MiB three times before the timed steps: under a rocprofv3 --pmc run its
 FETCH_SIZE / WRITE_SIZE calibrate the counters against a known byte count.
@@ -36,6 +42,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_FP32 = 157.3e12          # MI355X FP32 (vector and matrix) peak, FLOP/s
+PEAK_FP64 = 78.6e12           # MI355X FP64 vector peak, FLOP/s
 PEAK_HBM = 8.0e12             # B/s
 # v_exp_f32 is a quarter-rate transcendental: 256 CUs x 4 SIMDs x 16 lanes / 4 x 2.4 GHz
 PEAK_EXP = 256 * 4 * 16 / 4 * 2.4e9
@@ -110,6 +117,105 @@ def cpu_baseline(inp, target_s: float):
                       f"forward + gradients, {t:.1f} s wall"}
 
 
+def timed_kernels(L):
+    cap = 64
+    names = (ctypes.c_char_p * cap)()
+    tot = (ctypes.c_double * cap)()
+    cnt = (ctypes.c_int64 * cap)()
+    n = L.gpps_timing_collect(cap, names, tot, cnt)
+    if n < 0:
+        raise RuntimeError("kernel timing failed")
+    return {names[i].decode(): {"avg_ms": tot[i] / cnt[i], "launches": int(cnt[i])}
+            for i in range(n)}
+
+
+def bench_gplvm(args):
+    """One step = gpps_bound (L and every gradient) at the paper's experiment shape."""
+    import numpy as np
+    import torch
+
+    import paper_1410_4984_amd as gpps
+    from paper_1410_4984_amd import gplvm
+
+    N, M, Q, D = 64_000, 100, 1, 3
+    Y, _ = gplvm.paper_data(N, D=D, seed=0)
+    Y = Y - Y.mean(0)
+    mu, S, Z, sf2, l, beta = gplvm.init_params(Y, Q, M, seed=0)
+    # A well-conditioned point of this shape (the work does not depend on it):
+    # evenly spaced inducing inputs and a lengthscale below their spacing give
+    # cond(Kmm) ~ 1e2 and cond(Kmm + beta Psi2) ~ 1e4.  At the data-driven start
+    # (inducing inputs among the means, unit lengthscale) cond(Kmm + beta Psi2)
+    # is ~1e14 and the bound itself is undetermined to ~1e-2 in fp64.
+    Z = np.linspace(mu.min(), mu.max(), M)[:, None]
+    l = np.array([0.03])
+    jitter = 1e-6
+    dev, dt = "cuda:0", torch.float64
+    t = {k: torch.tensor(v, dtype=dt, device=dev) for k, v in (("mu", mu), ("S", S), ("Z", Z),
+                                                                ("Y", Y))}
+    ws = torch.empty(gpps.bound_workspace_bytes(dt, N, M, Q, D), dtype=torch.uint8, device=dev)
+    out = None
+
+    def step():
+        nonlocal out
+        out = gpps.bound(t["mu"], t["S"], t["Z"], t["Y"], sf2, l, beta, jitter, out=out,
+                         workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    L = gpps.lib()
+    L.gpps_timing_enable.argtypes = [ctypes.c_int]
+    L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    L.gpps_timing_enable(1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    L.gpps_timing_enable(0)
+    kernels = timed_kernels(L)
+    ms = (t1 - t0) * 1e3 / args.steps
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+    alg = algorithmic(dom, N, M, Q)
+    roofline = None
+    if alg:
+        bound, work, unit = alg
+        avg_s = kernels[dom]["avg_ms"] * 1e-3
+        if unit == "flop":
+            ach, peak, u = work / avg_s / 1e12, PEAK_FP64 / 1e12, "TFLOP/s"
+        else:
+            ach, peak, u = work / avg_s / 1e9, PEAK_HBM / 1e9, "GB/s"
+        roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 4), "peak": peak,
+                    "unit": u, "frac": round(ach / peak, 5), "traffic": None,
+                    "algorithmic_per_launch": work}
+    rec = {
+        "metric": "Bayesian GP-LVM bound + gradient evaluations/sec (fp64), 1 MI355X",
+        "value": 1e3 / ms, "unit": "evals/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"gplvm-paper (N={N}, M={M}, Q={Q}, D={D}, seed 0)", "N": N,
+                   "M": M, "Q": Q, "D": D, "L": float(out["L"].item())},
+        "roofline": roofline,
+        "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}
+                    for k, v in sorted(kernels.items())},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import bound as ob
+        oracle.build(force=False)
+        t0 = time.perf_counter()
+        ref = ob.grads(mu, S, Z, Y, sf2, l, beta, jitter)
+        tc = time.perf_counter() - t0
+        rec["cpu_baseline"] = {"value": 1.0 / tc, "unit": "evals/s",
+                               "cores": oracle.num_threads(), "kind": "oracle",
+                               "sample": f"one full evaluation (all {N} rows), fp64 oracle, "
+                                         f"{tc:.2f} s wall, L = {ref['L']:.6f}"}
+        rec["config"]["L_rel_diff_oracle"] = abs(rec["config"]["L"] - ref["L"]) / abs(ref["L"])
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +232,10 @@ def main():
               "all-reduce of Psi2 and the global gradients) is a design, not built here.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "gplvm":
+        bench_gplvm(args)
+        return
 
     import numpy as np
     import torch
@@ -180,15 +290,7 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     L.gpps_timing_enable(0)
-    cap = 64
-    names = (ctypes.c_char_p * cap)()
-    tot = (ctypes.c_double * cap)()
-    cnt = (ctypes.c_int64 * cap)()
-    n = L.gpps_timing_collect(cap, names, tot, cnt)
-    if n < 0:
-        raise RuntimeError("kernel timing failed")
-    kernels = {names[i].decode(): {"avg_ms": tot[i] / cnt[i], "launches": int(cnt[i])}
-               for i in range(n)}
+    kernels = timed_kernels(L)
     ms = (t1 - t0) * 1e3 / args.steps
     terms = float(N) * M * M * Q
 

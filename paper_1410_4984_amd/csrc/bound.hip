@@ -37,7 +37,7 @@ namespace {
 
 constexpr int kB = 32;               // block edge of the M x M algebra
 constexpr int kRowBlock = 256;       // rows per block of the row reductions
-constexpr int64_t kPsiYRows = 2048;  // rows per chunk of Psi1^T Y
+constexpr int64_t kPsiYRows = 256;   // rows per chunk of Psi1^T Y
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

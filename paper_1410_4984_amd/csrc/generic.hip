@@ -14,9 +14,11 @@
 // Work split: Psi1 one thread per output; Psi2 one thread per unique pair
 // (m <= m'), a workgroup per 16 x 16 pair tile and row chunk, partial sums per
 // chunk reduced in a fixed order.  Gradients: a row kernel (one thread per
-// datapoint) produces dmu, dS and per-block dl / dsf2 partials; a column kernel
-// (one thread per inducing input and row chunk) produces dZ partials; a final
-// kernel reduces the partials in a fixed order.  No atomics anywhere.
+// datapoint and range of pair rows m) produces partial dmu, dS and per-block
+// dl / dsf2 partials; a column kernel (one thread per inducing input, row chunk
+// and range of partners m') produces dZ partials; fixed-order reduce kernels
+// combine them (the ranges exist so that small N still fills the chip).  No
+// atomics anywhere.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -43,8 +45,10 @@ struct Plan {
     int64_t ncc, rowsc;              // column-kernel chunks and rows per chunk
     int64_t col_blocks;              // column-kernel blocks per chunk
     int64_t row_blocks;              // row-kernel blocks
+    int64_t rr;                      // row kernel: ranges of pair rows m (m = r mod rr)
+    int64_t cr;                      // column kernel: ranges of partners m'
     // workspace offsets in bytes
-    size_t off_w1, off_w2, off_lp1, off_lp2, off_p2, off_g2s, off_colp, off_rowp, total;
+    size_t off_w1, off_w2, off_lp1, off_lp2, off_p2, off_g2s, off_colp, off_rowp, off_rowg, total;
 };
 
 Plan make_plan(const Shape &s, size_t elem) {
@@ -63,6 +67,9 @@ Plan make_plan(const Shape &s, size_t elem) {
     p.rowsc = cdiv(s.N, p.ncc);
     p.ncc = cdiv(s.N, p.rowsc);
     p.row_blocks = cdiv(s.N, kRowBlock);
+    p.rr = std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(s.M, 64), cdiv(2048, p.row_blocks)));
+    p.cr = std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(s.M, 64),
+                                                  cdiv(2048, p.col_blocks * p.ncc)));
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_w1 = take(elem * s.N * s.Q);
@@ -71,8 +78,9 @@ Plan make_plan(const Shape &s, size_t elem) {
     p.off_lp2 = take(elem * s.N);
     p.off_p2 = take(elem * p.nc2 * s.P);
     p.off_g2s = take(elem * s.M * s.M);
-    p.off_colp = take(elem * p.ncc * s.M * s.Q);
-    p.off_rowp = take(elem * p.row_blocks * (s.Q + 1));
+    p.off_colp = take(elem * p.ncc * p.cr * s.M * s.Q);
+    p.off_rowp = take(elem * p.rr * p.row_blocks * (s.Q + 1));
+    p.off_rowg = take(elem * p.rr * s.N * s.Q * 2);
     p.total = o;
     return p;
 }
@@ -210,14 +218,16 @@ __global__ void sym_kernel(int M, const T *__restrict__ G2, T *__restrict__ G2s)
     G2s[i] = T(0.5) * (G2[(int64_t)m * M + mp] + G2[(int64_t)mp * M + m]);
 }
 
-// One thread per datapoint: dmu_n, dS_n; per-block partials of dl and dsf2.
+// One thread per datapoint and range r of pair rows (m = r, r + rr, ...; the
+// Psi1 terms in the column tiles t = r, r + rr, ...): partial dmu_n, dS_n of the
+// range (rowg[r][2][N][Q]) and per-block partials of dl and dsf2.
 template <typename T, int QM>
 __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
-    int64_t N, int M, int Q, const T *__restrict__ mu, const T *__restrict__ S,
+    int64_t N, int M, int Q, int rr, const T *__restrict__ mu, const T *__restrict__ S,
     const T *__restrict__ Z, const T *__restrict__ w1, const T *__restrict__ w2,
     const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h, const T *__restrict__ G1,
-    const T *__restrict__ G2s, T *__restrict__ dmu, T *__restrict__ dS,
-    T *__restrict__ rowpart) {
+    const T *__restrict__ G2s, T *__restrict__ rowg, T *__restrict__ rowpart) {
+    const int range = blockIdx.y;
     __shared__ T s_g1[kRowBlock][kRowBlock + 1];
     __shared__ T s_red[QM + 1][kRowBlock];
     const int tid = threadIdx.x;
@@ -241,7 +251,7 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
 
     if (G1) {
         const int rows = (int)min<int64_t>(kRowBlock, N - n0);
-        for (int mt = 0; mt < M; mt += kRowBlock) {
+        for (int mt = range * kRowBlock; mt < M; mt += rr * kRowBlock) {
             const int cols = min(kRowBlock, M - mt);
             __syncthreads();
             for (int i = tid; i < rows * cols; i += kRowBlock) {
@@ -276,7 +286,7 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
     }
 
     if (G2s && valid) {
-        for (int m = 0; m < M; ++m) {
+        for (int m = range; m < M; m += rr) {
             T gsf_row = 0;  // sum over m' first, so long rows do not swamp the total
             for (int mp = m; mp < M; ++mp) {
                 const T g = (m == mp ? T(1) : T(2)) * G2s[(int64_t)m * M + mp];
@@ -309,11 +319,12 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
     }
 
     if (valid) {
+        T *pm = rowg + ((int64_t)range * 2) * N * Q, *ps = pm + N * Q;
 #pragma unroll
         for (int q = 0; q < QM; ++q)
             if (q < Q) {
-                dmu[n * Q + q] = gmu[q];
-                dS[n * Q + q] = gS[q];
+                pm[n * Q + q] = gmu[q];
+                ps[n * Q + q] = gS[q];
             }
     }
     // fixed-order block reduction of dl and dsf2 partials
@@ -326,14 +337,30 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
         const int row = k < Q ? k : QM;
         T s = 0;
         for (int i = 0; i < kRowBlock; ++i) s += s_red[row][i];
-        rowpart[(int64_t)blockIdx.x * (Q + 1) + k] = s;
+        rowpart[((int64_t)range * gridDim.x + blockIdx.x) * (Q + 1) + k] = s;
     }
 }
 
-// One thread per inducing input m and row chunk: partial dZ[m, :].
+// dmu, dS: the row kernel's range partials summed in range order.
+template <typename T>
+__global__ void grad_rows_reduce_kernel(int64_t NQ, int rr, const T *__restrict__ rowg,
+                                        T *__restrict__ dmu, T *__restrict__ dS) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= NQ) return;
+    T a = 0, b = 0;
+    for (int r = 0; r < rr; ++r) {
+        a += rowg[(int64_t)(2 * r) * NQ + i];
+        b += rowg[(int64_t)(2 * r + 1) * NQ + i];
+    }
+    dmu[i] = a;
+    dS[i] = b;
+}
+
+// One thread per inducing input m, row chunk and range of partners (m' = r,
+// r + cr, ...; the Psi1 term in range 0): partial dZ[m, :] per (chunk, range).
 template <typename T, int QM>
 __global__ __launch_bounds__(kColBlock) void grad_cols_kernel(
-    int64_t N, int M, int Q, int64_t rows_per_chunk, const T *__restrict__ mu,
+    int64_t N, int M, int Q, int cr, int64_t rows_per_chunk, const T *__restrict__ mu,
     const T *__restrict__ Z, const T *__restrict__ w1, const T *__restrict__ w2,
     const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h, const T *__restrict__ G1,
     const T *__restrict__ G2s, T *__restrict__ colpart) {
@@ -367,7 +394,7 @@ __global__ __launch_bounds__(kColBlock) void grad_cols_kernel(
         __syncthreads();
         if (!valid) continue;
         for (int r = 0; r < cnt; ++r) {
-            if (G1) {
+            if (G1 && blockIdx.z == 0) {
                 T e = 0;
 #pragma unroll
                 for (int q = 0; q < QM; ++q)
@@ -381,7 +408,7 @@ __global__ __launch_bounds__(kColBlock) void grad_cols_kernel(
                     if (q < Q) gz[q] += t * (s_mu[r][q] - zm[q]) * s_w1[r][q];
             }
             if (G2s) {
-                for (int mp = 0; mp < M; ++mp) {
+                for (int mp = blockIdx.z; mp < M; mp += cr) {
                     const T g = G2s[(int64_t)mp * M + m];
                     T e = s_lp2[r];
 #pragma unroll
@@ -407,32 +434,44 @@ __global__ __launch_bounds__(kColBlock) void grad_cols_kernel(
     if (valid) {
 #pragma unroll
         for (int q = 0; q < QM; ++q)
-            if (q < Q) colpart[((int64_t)blockIdx.y * M + m) * Q + q] = gz[q];
+            if (q < Q) colpart[(((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * M + m) * Q + q] = gz[q];
     }
 }
 
-// Fixed-order reduction of the gradient partials into dZ, dl, dsf2.
+// Fixed-order reduction of the gradient partials into dZ, dl, dsf2: one
+// workgroup per output; thread t sums partials t, t + 256, ..., then a fixed
+// tree combines the 256 sums.
 template <typename T>
-__global__ void grad_reduce_kernel(int64_t N, int M, int Q, int64_t ncc, int64_t row_blocks,
-                                   const T *__restrict__ colpart, const T *__restrict__ rowpart,
-                                   T dL_dpsi0, T *__restrict__ dZ, T *__restrict__ dsf2,
-                                   T *__restrict__ dl, int accumulate) {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+__global__ __launch_bounds__(256) void grad_reduce_kernel(int64_t N, int M, int Q, int64_t ncol,
+                                                          int64_t nrow, const T *__restrict__ colpart,
+                                                          const T *__restrict__ rowpart, T dL_dpsi0,
+                                                          T *__restrict__ dZ, T *__restrict__ dsf2,
+                                                          T *__restrict__ dl, int accumulate) {
+    __shared__ T red[256];
+    const int64_t i = blockIdx.x;
     const int64_t MQ = (int64_t)M * Q;
+    T s = 0;
     if (i < MQ) {
-        T s = 0;
-        for (int64_t c = 0; c < ncc; ++c) s += colpart[c * MQ + i];
-        dZ[i] = (accumulate ? dZ[i] : T(0)) + s;
-    } else if (i < MQ + Q + 1) {
+        for (int64_t c = threadIdx.x; c < ncol; c += 256) s += colpart[c * MQ + i];
+    } else {
         const int k = (int)(i - MQ);  // k < Q: dl_k; k == Q: dsf2
-        T s = 0;
-        for (int64_t b = 0; b < row_blocks; ++b) s += rowpart[b * (Q + 1) + k];
-        if (k < Q) {
-            dl[k] = (accumulate ? dl[k] : T(0)) + s;
-        } else {
-            s += dL_dpsi0 * T(N);
-            dsf2[0] = (accumulate ? dsf2[0] : T(0)) + s;
-        }
+        for (int64_t b = threadIdx.x; b < nrow; b += 256) s += rowpart[b * (Q + 1) + k];
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int w = 128; w >= 1; w >>= 1) {
+        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x != 0) return;
+    s = red[0];
+    if (i < MQ) {
+        dZ[i] = (accumulate ? dZ[i] : T(0)) + s;
+    } else if (i < MQ + Q) {
+        dl[i - MQ] = (accumulate ? dl[i - MQ] : T(0)) + s;
+    } else {
+        s += dL_dpsi0 * T(N);
+        dsf2[0] = (accumulate ? dsf2[0] : T(0)) + s;
     }
 }
 
@@ -448,18 +487,19 @@ void launch_psi2_partial(const Shape &s, const Plan &p, const T *mu, const T *Z,
 template <typename T, int QM>
 void launch_grads(const Shape &s, const Plan &p, const T *mu, const T *S, const T *Z,
                   const T *w1, const T *w2, const T *lp1, const T *lp2, const Hyp<T> &h,
-                  const T *G1, const T *G2s, T *dmu, T *dS, T *colpart, T *rowpart,
+                  const T *G1, const T *G2s, T *rowg, T *colpart, T *rowpart,
                   hipStream_t st) {
     {
         TimedScope ts(st, "generic_grad_rows");
-        grad_rows_kernel<T, QM><<<(unsigned)p.row_blocks, kRowBlock, 0, st>>>(
-            s.N, (int)s.M, (int)s.Q, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, rowpart);
+        grad_rows_kernel<T, QM><<<dim3((unsigned)p.row_blocks, (unsigned)p.rr), kRowBlock, 0, st>>>(
+            s.N, (int)s.M, (int)s.Q, (int)p.rr, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg,
+            rowpart);
     }
-    dim3 grid((unsigned)p.col_blocks, (unsigned)p.ncc);
+    dim3 grid((unsigned)p.col_blocks, (unsigned)p.ncc, (unsigned)p.cr);
     TimedScope ts(st, "generic_grad_cols");
-    grad_cols_kernel<T, QM><<<grid, kColBlock, 0, st>>>(s.N, (int)s.M, (int)s.Q, p.rowsc, mu,
-                                                         Z, w1, w2, lp1, lp2, h, G1, G2s,
-                                                         colpart);
+    grad_cols_kernel<T, QM><<<grid, kColBlock, 0, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.cr,
+                                                         p.rowsc, mu, Z, w1, w2, lp1, lp2, h, G1,
+                                                         G2s, colpart);
 }
 
 template <typename T>
@@ -518,21 +558,24 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
         sym_kernel<T><<<(unsigned)cdiv(s.M * s.M, 256), 256, 0, st>>>((int)s.M, G2, G2s);
     }
     T *colpart = at<T>(ws, p.off_colp), *rowpart = at<T>(ws, p.off_rowp);
+    T *rowg = at<T>(ws, p.off_rowg);
     if (s.Q <= 4)
-        launch_grads<T, 4>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+        launch_grads<T, 4>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
     else if (s.Q <= 8)
-        launch_grads<T, 8>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+        launch_grads<T, 8>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
     else if (s.Q <= 16)
-        launch_grads<T, 16>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+        launch_grads<T, 16>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
     else if (s.Q <= 32)
-        launch_grads<T, 32>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+        launch_grads<T, 32>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
     else
-        launch_grads<T, 64>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, dmu, dS, colpart, rowpart, st);
+        launch_grads<T, 64>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
     const int64_t total = s.M * s.Q + s.Q + 1;
     TimedScope ts(st, "generic_grad_reduce");
-    grad_reduce_kernel<T><<<(unsigned)cdiv(total, 256), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, p.ncc, p.row_blocks, colpart, rowpart, dL_dpsi0, dZ, dsf2, dl,
-        accumulate);
+    grad_rows_reduce_kernel<T><<<(unsigned)cdiv(s.N * s.Q, 256), 256, 0, st>>>(s.N * s.Q, (int)p.rr,
+                                                                              rowg, dmu, dS);
+    grad_reduce_kernel<T><<<(unsigned)total, 256, 0, st>>>(
+        s.N, (int)s.M, (int)s.Q, p.ncc * p.cr, p.rr * p.row_blocks, colpart, rowpart, dL_dpsi0,
+        dZ, dsf2, dl, accumulate);
     return hipGetLastError();
 }
 

@@ -31,6 +31,11 @@ Gradients (all matrices symmetric, C = A^-1 Psi, P = C C^T):
                - (beta^2 / 2) tr(P Psi2) - (D / 2) psi0 + (D / 2) tr(Kmm^-1 Psi2)
 then through Kmm to (Z, sigma_f^2, l), through the psi-statistics to
 (mu, S, Z, sigma_f^2, l), and the KL adds dmu -= mu, dS -= (1 - 1/S) / 2.
+
+S = None is the sparse GP regression case of eq. (boundF) itself: the inputs are
+known (mu holds X, every variance is zero), so the statistics are the plain
+kernel quantities (psi0 = tr Kff, Psi1 = Kfu, Psi2 = Kfu^T Kfu), there is no
+q(X) and no KL term, L = F, and the gradient w.r.t. the inputs is dL/dX (no dS).
 """
 from __future__ import annotations
 
@@ -76,11 +81,12 @@ def kl(mu, S):
 def bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
     """(F, KL, pieces): the collapsed bound F and the KL term, plus the
     intermediate matrices the gradient needs.  ``inverse`` maps a Cholesky
-    factor to the inverse of its matrix (default: triangular solves)."""
+    factor to the inverse of its matrix (default: triangular solves).  S = None:
+    known inputs (zero variances), KL = 0."""
     mu = np.asarray(mu, np.float64)
     Y = np.asarray(Y, np.float64)
     N, D = Y.shape
-    psi0, Psi1, Psi2 = psi_stats(mu, S, Z, sigma_f2, l)
+    psi0, Psi1, Psi2 = psi_stats(mu, np.zeros_like(mu) if S is None else S, Z, sigma_f2, l)
     Psi1 = np.asarray(Psi1).reshape(N, -1)
     Psi2 = np.asarray(Psi2)
     M = Psi2.shape[0]
@@ -100,7 +106,7 @@ def bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
          - 0.5 * beta * D * float(psi0) + 0.5 * beta * D * float(np.sum(Kinv * Psi2)))
     pieces = dict(N=N, D=D, M=M, psi0=float(psi0), Psi1=Psi1, Psi2=Psi2, K0=K0, Kmm=Kmm,
                   Kinv=Kinv, Ainv=Ainv, Psi=Psi, C=C, yy=yy)
-    return F, kl(mu, S), pieces
+    return F, (0.0 if S is None else kl(mu, S)), pieces
 
 
 def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter):
@@ -143,16 +149,18 @@ def kmm_grads(Z, sigma_f2, l, G):
 
 def grads(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
     """L and its gradient w.r.t. every parameter:
-    dict(L, dmu, dS, dZ, dsigma_f2, dl, dbeta)."""
+    dict(L, dmu, dS, dZ, dsigma_f2, dl, dbeta).  S = None (known inputs): dmu is
+    dL/dX and dS is None."""
     L, d_psi0, d_Psi1, d_Psi2, d_Kmm, d_beta, p = upstream(mu, S, Z, Y, sigma_f2, l, beta,
                                                             jitter, inverse)
+    mu = np.asarray(mu, np.float64)
+    known = S is None
+    S = np.zeros_like(mu) if known else np.asarray(S, np.float64)
     g = psi_grads(mu, S, Z, sigma_f2, l, d_psi0, d_Psi1, d_Psi2)
     kz, ks, kl_ = kmm_grads(Z, sigma_f2, l, d_Kmm)
-    mu = np.asarray(mu, np.float64)
-    S = np.asarray(S, np.float64)
     return dict(L=L,
-                dmu=np.asarray(g["dmu"]) - mu,
-                dS=np.asarray(g["dS"]) - 0.5 * (1.0 - 1.0 / S),
+                dmu=np.asarray(g["dmu"]) - (0.0 if known else mu),
+                dS=None if known else np.asarray(g["dS"]) - 0.5 * (1.0 - 1.0 / S),
                 dZ=np.asarray(g["dZ"]) + kz,
                 dsigma_f2=float(np.asarray(g["dsigma_f2"]).ravel()[0]) + ks,
                 dl=np.asarray(g["dl"]) + kl_,

@@ -121,3 +121,79 @@ def test_bound_is_the_sum_of_single_column_bounds():
                             p["beta"], p["jitter"])[0] for d in range(p["Y"].shape[1])]
     assert abs(F - sum(parts)) <= 1e-11 * abs(F)
     assert K == ob.kl(p["mu"], p["S"])
+
+
+# ---------------------------------------------------------------- known inputs (S = None)
+# The sparse GP regression bound of eq. (boundF) itself, written out densely the
+# way the variational sparse GP literature states it:
+#     F = log N(Y | 0, Qff + I / beta) - (beta D / 2) tr(Kff - Qff),
+#     Qff = Kfu Kuu^-1 Kuf,  Kuu = k(Z, Z) + jitter I,
+# with an N x N covariance (numpy slogdet and solve), i.e. without the matrix
+# inversion lemma and the M x M algebra the oracle uses.
+
+def _regression_problem(seed=13, N=12, M=5, Q=2, D=3):
+    rng = np.random.default_rng(seed)
+    return dict(X=rng.uniform(-2.5, 2.5, size=(N, Q)), Z=rng.normal(size=(M, Q)),
+                Y=rng.normal(size=(N, D)), sigma_f2=1.4, l=rng.uniform(0.6, 1.7, size=Q),
+                beta=4.0, jitter=1e-6)
+
+
+def _dense_titsias(X, Z, Y, sf2, l, beta, jitter):
+    def k(A, B):
+        d = (A[:, None, :] - B[None, :, :]) / l
+        return sf2 * np.exp(-0.5 * np.sum(d * d, axis=-1))
+    N, D = Y.shape
+    Kfu = k(X, Z)
+    Kuu = k(Z, Z) + jitter * np.eye(Z.shape[0])
+    Qff = Kfu @ np.linalg.solve(Kuu, Kfu.T)
+    Cov = Qff + np.eye(N) / beta
+    sign, logdet = np.linalg.slogdet(Cov)
+    assert sign > 0
+    lml = (-0.5 * float(np.sum(Y * np.linalg.solve(Cov, Y))) - 0.5 * D * logdet
+           - 0.5 * N * D * np.log(2 * np.pi))
+    return lml - 0.5 * beta * D * float(np.trace(k(X, X)) - np.trace(Qff))
+
+
+@pytest.mark.parametrize("jitter", [1e-6, 1e-2])
+def test_regression_bound_matches_dense_form(jitter):
+    p = _regression_problem()
+    F, kl_term, _ = ob.bound_terms(p["X"], None, p["Z"], p["Y"], p["sigma_f2"], p["l"], p["beta"],
+                                   jitter)
+    ref = _dense_titsias(p["X"], p["Z"], p["Y"], p["sigma_f2"], p["l"], p["beta"], jitter)
+    assert kl_term == 0.0
+    assert abs(F - ref) <= 1e-10 * abs(ref), (F, ref)
+    g = ob.grads(p["X"], None, p["Z"], p["Y"], p["sigma_f2"], p["l"], p["beta"], jitter)
+    assert g["dS"] is None and g["L"] == F
+
+
+def test_regression_gradients_match_finite_differences():
+    p = _regression_problem(seed=17)
+    g = ob.grads(p["X"], None, p["Z"], p["Y"], p["sigma_f2"], p["l"], p["beta"], p["jitter"])
+
+    def L(q):
+        return _dense_titsias(q["X"], q["Z"], q["Y"], q["sigma_f2"], q["l"], q["beta"], q["jitter"])
+
+    def fd(key, idx=None):
+        q = {k: (np.array(v, dtype=np.float64, copy=True) if isinstance(v, np.ndarray) else v)
+             for k, v in p.items()}
+        x0 = q[key][idx] if idx is not None else q[key]
+        h = 1e-6 * max(1.0, abs(x0))
+        vals = []
+        for s in (+1, -1):
+            if idx is not None:
+                q[key][idx] = x0 + s * h
+            else:
+                q[key] = x0 + s * h
+            vals.append(L(q))
+        return (vals[0] - vals[1]) / (2 * h)
+
+    # differences of the dense form, so the gradient pin does not lean on the
+    # oracle's own bound either
+    for key, gk in (("X", "dmu"), ("Z", "dZ"), ("l", "dl")):
+        num = np.array([fd(key, idx) for idx in np.ndindex(p[key].shape)]).reshape(p[key].shape)
+        ana = np.asarray(g[gk])
+        err = np.linalg.norm(num - ana) / np.linalg.norm(ana)
+        assert err <= 1e-6, (key, err)
+    for key, gk in (("sigma_f2", "dsigma_f2"), ("beta", "dbeta")):
+        num = fd(key)
+        assert abs(num - g[gk]) <= 1e-6 * max(1.0, abs(g[gk])), (key, num, g[gk])

@@ -13,7 +13,10 @@ fallback of any kind: if the library is missing or cannot run, calls raise.
                                        -> dict(L, dmu, dS, dZ, dsigma_f2, dl, dbeta)
 
 Notation follows the paper (section 2, Alg. 1-2): mu, S (variances) are N x Q,
-Z is M x Q, sigma_f2 the kernel variance, l the Q ARD lengthscales.
+Z is M x Q, sigma_f2 the kernel variance, l the Q ARD lengthscales.  S = None
+means known inputs (every variance zero: the sparse GP regression case of
+eq. (boundF), with mu holding the inputs X); the library then computes
+Psi1 = Kfu and Psi2 = Kfu^T Kfu on its matrix-core GEMM path, and dS is None.
 """
 from __future__ import annotations
 
@@ -159,7 +162,8 @@ def psi_stats(mu, S, Z, sigma_f2, l, *, want_psi1=True, accumulate=False, out=No
     N, Q = mu.shape
     M = Z.shape[0]
     _dev_tensor(mu, "mu", dtype, (N, Q), device)
-    _dev_tensor(S, "S", dtype, (N, Q), device)
+    if S is not None:
+        _dev_tensor(S, "S", dtype, (N, Q), device)
     _dev_tensor(Z, "Z", dtype, (M, Q), device)
     lh = _host_l(l, Q)
     if out is None:
@@ -174,8 +178,8 @@ def psi_stats(mu, S, Z, sigma_f2, l, *, want_psi1=True, accumulate=False, out=No
         _dev_tensor(Psi2, "Psi2", dtype, (M, M), device)
     ws, ws_bytes = _workspace(dtype, N, M, Q, device, workspace)
     _check(lib().gpps_psi_stats(
-        _dt(dtype), N, M, Q, mu.data_ptr(), S.data_ptr(), Z.data_ptr(), float(sigma_f2),
-        lh.ctypes.data, psi0.data_ptr(), None if Psi1 is None else Psi1.data_ptr(),
+        _dt(dtype), N, M, Q, mu.data_ptr(), None if S is None else S.data_ptr(), Z.data_ptr(),
+        float(sigma_f2), lh.ctypes.data, psi0.data_ptr(), None if Psi1 is None else Psi1.data_ptr(),
         Psi2.data_ptr(), int(bool(accumulate)), ws.data_ptr(), ws_bytes, _stream(stream)))
     return psi0, Psi1, Psi2
 
@@ -185,15 +189,17 @@ def psi_grads(mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2, *, accumulate
     """Gradients of L = dL_dpsi0 psi0 + <dL_dPsi1, Psi1> + <dL_dPsi2, Psi2> (Alg. 2).
 
     ``dL_dPsi1`` / ``dL_dPsi2`` may be None (zero).  Returns a dict with dmu, dS
-    (N x Q), dZ (M x Q), dsigma_f2 (1), dl (Q).  With ``accumulate=True`` and
-    ``out`` (a dict of the same tensors) dZ, dsigma_f2 and dl are added to.
+    (N x Q; None when S is None), dZ (M x Q), dsigma_f2 (1), dl (Q).  With
+    ``accumulate=True`` and ``out`` (a dict of the same tensors) dZ, dsigma_f2
+    and dl are added to.
     """
     import torch
     dtype, device = mu.dtype, mu.device
     N, Q = mu.shape
     M = Z.shape[0]
     _dev_tensor(mu, "mu", dtype, (N, Q), device)
-    _dev_tensor(S, "S", dtype, (N, Q), device)
+    if S is not None:
+        _dev_tensor(S, "S", dtype, (N, Q), device)
     _dev_tensor(Z, "Z", dtype, (M, Q), device)
     if dL_dPsi1 is not None:
         _dev_tensor(dL_dPsi1, "dL_dPsi1", dtype, (N, M), device)
@@ -202,20 +208,22 @@ def psi_grads(mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2, *, accumulate
     lh = _host_l(l, Q)
     if out is None:
         out = {"dmu": torch.empty((N, Q), dtype=dtype, device=device),
-               "dS": torch.empty((N, Q), dtype=dtype, device=device),
+               "dS": None if S is None else torch.empty((N, Q), dtype=dtype, device=device),
                "dZ": torch.zeros((M, Q), dtype=dtype, device=device),
                "dsigma_f2": torch.zeros(1, dtype=dtype, device=device),
                "dl": torch.zeros(Q, dtype=dtype, device=device)}
     else:
         for k, shp in (("dmu", (N, Q)), ("dS", (N, Q)), ("dZ", (M, Q)), ("dsigma_f2", (1,)),
                        ("dl", (Q,))):
+            if k == "dS" and S is None:
+                continue
             _dev_tensor(out[k], k, dtype, shp, device)
     ws, ws_bytes = _workspace(dtype, N, M, Q, device, workspace)
     ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
     _check(lib().gpps_psi_grads(
-        _dt(dtype), N, M, Q, mu.data_ptr(), S.data_ptr(), Z.data_ptr(), float(sigma_f2),
+        _dt(dtype), N, M, Q, mu.data_ptr(), ptr(S), Z.data_ptr(), float(sigma_f2),
         lh.ctypes.data, float(dL_dpsi0), ptr(dL_dPsi1), ptr(dL_dPsi2), out["dmu"].data_ptr(),
-        out["dS"].data_ptr(), out["dZ"].data_ptr(), out["dsigma_f2"].data_ptr(),
+        ptr(None if S is None else out["dS"]), out["dZ"].data_ptr(), out["dsigma_f2"].data_ptr(),
         out["dl"].data_ptr(), int(bool(accumulate)), ws.data_ptr(), ws_bytes, _stream(stream)))
     return out
 
@@ -230,6 +238,8 @@ def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter=0.0, *, out=None, workspace=Non
 
     Y is N x D.  Returns a dict with L (1), dmu, dS (N x Q), dZ (M x Q),
     dsigma_f2 (1), dl (Q) and dbeta (1), all tensors of mu's dtype on its device.
+    S = None: known inputs mu = X, the sparse GP regression bound of eq. (boundF)
+    itself (no KL term), dmu = dL/dX and dS is None.
     """
     import torch
     dtype, device = mu.dtype, mu.device
@@ -237,14 +247,19 @@ def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter=0.0, *, out=None, workspace=Non
     M = Z.shape[0]
     D = Y.shape[1] if Y.dim() == 2 else -1
     _dev_tensor(mu, "mu", dtype, (N, Q), device)
-    _dev_tensor(S, "S", dtype, (N, Q), device)
+    if S is not None:
+        _dev_tensor(S, "S", dtype, (N, Q), device)
     _dev_tensor(Z, "Z", dtype, (M, Q), device)
     _dev_tensor(Y, "Y", dtype, (N, D), device)
     lh = _host_l(l, Q)
     shapes = (("L", (1,)), ("dmu", (N, Q)), ("dS", (N, Q)), ("dZ", (M, Q)), ("dsigma_f2", (1,)),
               ("dl", (Q,)), ("dbeta", (1,)))
+    if S is None:
+        shapes = tuple(kv for kv in shapes if kv[0] != "dS")
     if out is None:
         out = {k: torch.empty(shp, dtype=dtype, device=device) for k, shp in shapes}
+        if S is None:
+            out["dS"] = None
     else:
         for k, shp in shapes:
             _dev_tensor(out[k], k, dtype, shp, device)
@@ -256,9 +271,10 @@ def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter=0.0, *, out=None, workspace=Non
     elif workspace.numel() * workspace.element_size() < need:
         raise ValueError(f"workspace too small: need {need} bytes")
     _check(lib().gpps_bound(
-        _dt(dtype), N, M, Q, D, mu.data_ptr(), S.data_ptr(), Z.data_ptr(), Y.data_ptr(),
-        float(sigma_f2), lh.ctypes.data, float(beta), float(jitter), out["L"].data_ptr(),
-        out["dmu"].data_ptr(), out["dS"].data_ptr(), out["dZ"].data_ptr(),
+        _dt(dtype), N, M, Q, D, mu.data_ptr(), None if S is None else S.data_ptr(), Z.data_ptr(),
+        Y.data_ptr(), float(sigma_f2), lh.ctypes.data, float(beta), float(jitter),
+        out["L"].data_ptr(), out["dmu"].data_ptr(),
+        None if S is None else out["dS"].data_ptr(), out["dZ"].data_ptr(),
         out["dsigma_f2"].data_ptr(), out["dl"].data_ptr(), out["dbeta"].data_ptr(),
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
     return out

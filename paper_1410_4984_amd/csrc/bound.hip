@@ -120,7 +120,8 @@ __global__ void bound_kmm_kernel(int M, int Q, int Mp, const T *__restrict__ Z, 
     }
 }
 
-// Per block of kRowBlock rows: sum_nd Y^2 and sum_nq (mu^2 + S - log S - 1) / 2.
+// Per block of kRowBlock rows: sum_nd Y^2 and sum_nq (mu^2 + S - log S - 1) / 2
+// (zero when S is null: known inputs).
 template <typename T>
 __global__ __launch_bounds__(256) void bound_rows_kernel(int64_t N, int Q, int64_t D,
                                                          const T *__restrict__ mu,
@@ -135,9 +136,11 @@ __global__ __launch_bounds__(256) void bound_rows_kernel(int64_t N, int Q, int64
         const double y = (double)Y[n0 * D + k];
         yy += y * y;
     }
-    for (int64_t k = threadIdx.x; k < rows * Q; k += 256) {
-        const double m = (double)mu[n0 * Q + k], s = (double)S[n0 * Q + k];
-        kl += 0.5 * (m * m + s - log(s) - 1.0);
+    if (S) {  // no KL term for known inputs
+        for (int64_t k = threadIdx.x; k < rows * Q; k += 256) {
+            const double m = (double)mu[n0 * Q + k], s = (double)S[n0 * Q + k];
+            kl += 0.5 * (m * m + s - log(s) - 1.0);
+        }
     }
     red[0][threadIdx.x] = yy;
     red[1][threadIdx.x] = kl;
@@ -611,7 +614,7 @@ hipError_t bound_tail(const Shape &s, int64_t D, const T *mu, const T *S, const 
                                                         at<double>(ws, p.off_kdl), at<double>(ws, p.off_ksf));
     bound_kmm_reduce_kernel<T><<<1, 128, 0, st>>>(M, Q, at<double>(ws, p.off_kdl), at<double>(ws, p.off_ksf),
                                                  dl, dsf2);
-    bound_kl_grad_kernel<T><<<(unsigned)cdiv(s.N * Q, 256), 256, 0, st>>>(s.N * Q, mu, S, dmu, dS);
+    if (S) bound_kl_grad_kernel<T><<<(unsigned)cdiv(s.N * Q, 256), 256, 0, st>>>(s.N * Q, mu, S, dmu, dS);
     return hipGetLastError();
 }
 

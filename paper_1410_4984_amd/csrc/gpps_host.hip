@@ -41,8 +41,12 @@ gpps::Hyp<T> make_hyp(double sigma_f2, const double *l, int64_t Q) {
     return h;
 }
 
-// Which path serves this call (or -1 if the requested one cannot).
-int choose_path(gpps_dtype dt, const gpps::Shape &s) {
+// Which path serves a call with variances S (or -1 if the requested one
+// cannot).  Calls without S (known inputs) always take the known-input path.
+constexpr int kPathKnown = 100;
+
+int choose_path(gpps_dtype dt, const gpps::Shape &s, const void *S) {
+    if (!S) return kPathKnown;
     int p = g_path.load();
     bool mfma_ok = dt == GPPS_F32 && gpps::mfma_supports(s);
     if (p == GPPS_PATH_AUTO) return mfma_ok ? GPPS_PATH_MFMA : GPPS_PATH_GENERIC;
@@ -61,6 +65,15 @@ gpps_status check_workspace(gpps_dtype dt, const gpps::Shape &s, void *ws, size_
 hipError_t run_stats(gpps_dtype dt, int path, const gpps::Shape &s, const void *mu, const void *S,
                      const void *Z, double sigma_f2, const double *l, void *psi0, void *Psi1,
                      void *Psi2, int accumulate, void *ws, hipStream_t st) {
+    if (path == kPathKnown) {
+        if (dt == GPPS_F32)
+            return gpps::known_psi_stats<float>(s, (const float *)mu, (const float *)Z,
+                                                make_hyp<float>(sigma_f2, l, s.Q), (float *)psi0,
+                                                (float *)Psi1, (float *)Psi2, accumulate != 0, ws, st);
+        return gpps::known_psi_stats<double>(s, (const double *)mu, (const double *)Z,
+                                             make_hyp<double>(sigma_f2, l, s.Q), (double *)psi0,
+                                             (double *)Psi1, (double *)Psi2, accumulate != 0, ws, st);
+    }
     if (dt == GPPS_F32) {
         const auto h = make_hyp<float>(sigma_f2, l, s.Q);
         if (path == GPPS_PATH_MFMA)
@@ -81,6 +94,17 @@ hipError_t run_grads(gpps_dtype dt, int path, const gpps::Shape &s, const void *
                      const void *Z, double sigma_f2, const double *l, double dL_dpsi0,
                      const void *dL_dPsi1, const void *dL_dPsi2, void *dmu, void *dS, void *dZ,
                      void *dsigma_f2, void *dl, int accumulate, void *ws, hipStream_t st) {
+    if (path == kPathKnown) {
+        if (dt == GPPS_F32)
+            return gpps::known_psi_grads<float>(
+                s, (const float *)mu, (const float *)Z, make_hyp<float>(sigma_f2, l, s.Q),
+                float(dL_dpsi0), (const float *)dL_dPsi1, (const float *)dL_dPsi2, (float *)dmu,
+                (float *)dZ, (float *)dsigma_f2, (float *)dl, accumulate != 0, ws, st);
+        return gpps::known_psi_grads<double>(
+            s, (const double *)mu, (const double *)Z, make_hyp<double>(sigma_f2, l, s.Q), dL_dpsi0,
+            (const double *)dL_dPsi1, (const double *)dL_dPsi2, (double *)dmu, (double *)dZ,
+            (double *)dsigma_f2, (double *)dl, accumulate != 0, ws, st);
+    }
     if (dt == GPPS_F32) {
         const auto h = make_hyp<float>(sigma_f2, l, s.Q);
         if (path == GPPS_PATH_MFMA)
@@ -113,7 +137,7 @@ size_t gpps_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q) {
     if (!valid_dtype(dt) || !valid_shape(N, M, Q)) return 0;
     const gpps::Shape s = gpps::make_shape(N, M, Q);
     const size_t elem = dt == GPPS_F32 ? 4 : 8;
-    size_t b = gpps::generic_workspace_bytes(s, elem);
+    size_t b = std::max(gpps::generic_workspace_bytes(s, elem), gpps::known_workspace_bytes(s, elem));
     if (dt == GPPS_F32 && gpps::mfma_supports(s)) b = std::max(b, gpps::mfma_workspace_bytes(s));
     return b;
 }
@@ -124,14 +148,14 @@ gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
                            size_t workspace_bytes, void *stream) {
     if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
     if (!valid_shape(N, M, Q)) return GPPS_ERR_SHAPE;
-    if (!mu || !S || !Z || !psi0 || !Psi2) return GPPS_ERR_NULL;
+    if (!mu || !Z || !psi0 || !Psi2) return GPPS_ERR_NULL;
     if (gpps_status r = check_hypers(sigma_f2, l, Q)) return r;
     const gpps::Shape s = gpps::make_shape(N, M, Q);
     if (gpps_status r = check_workspace(dt, s, workspace, workspace_bytes)) return r;
     const size_t elem = dt == GPPS_F32 ? 4 : 8;
     for (const void *p : {mu, S, Z, (const void *)psi0, (const void *)Psi1, (const void *)Psi2})
         if (p && !aligned(p, elem)) return GPPS_ERR_ALIGN;
-    const int path = choose_path(dt, s);
+    const int path = choose_path(dt, s, S);
     if (path < 0) return GPPS_ERR_PATH;
     const hipError_t e = run_stats(dt, path, s, mu, S, Z, sigma_f2, l, psi0, Psi1, Psi2, accumulate,
                                    workspace, static_cast<hipStream_t>(stream));
@@ -146,7 +170,7 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
                            void *stream) {
     if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
     if (!valid_shape(N, M, Q)) return GPPS_ERR_SHAPE;
-    if (!mu || !S || !Z || !dmu || !dS || !dZ || !dsigma_f2 || !dl) return GPPS_ERR_NULL;
+    if (!mu || !Z || !dmu || (S && !dS) || !dZ || !dsigma_f2 || !dl) return GPPS_ERR_NULL;
     if (gpps_status r = check_hypers(sigma_f2, l, Q)) return r;
     if (!std::isfinite(dL_dpsi0)) return GPPS_ERR_HYPER;
     const gpps::Shape s = gpps::make_shape(N, M, Q);
@@ -155,7 +179,7 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
     for (const void *p : {mu, S, Z, dL_dPsi1, dL_dPsi2, (const void *)dmu, (const void *)dS,
                           (const void *)dZ, (const void *)dsigma_f2, (const void *)dl})
         if (p && !aligned(p, elem)) return GPPS_ERR_ALIGN;
-    const int path = choose_path(dt, s);
+    const int path = choose_path(dt, s, S);
     if (path < 0) return GPPS_ERR_PATH;
     const hipError_t e = run_grads(dt, path, s, mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2,
                                    dmu, dS, dZ, dsigma_f2, dl, accumulate, workspace,
@@ -178,7 +202,7 @@ gpps_status gpps_bound(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D
                        size_t workspace_bytes, void *stream) {
     if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
     if (!valid_shape(N, M, Q) || D < 1 || D > GPPS_MAX_D || M > GPPS_MAX_M_BOUND) return GPPS_ERR_SHAPE;
-    if (!mu || !S || !Z || !Y || !L || !dmu || !dS || !dZ || !dsigma_f2 || !dl || !dbeta)
+    if (!mu || !Z || !Y || !L || !dmu || (S && !dS) || !dZ || !dsigma_f2 || !dl || !dbeta)
         return GPPS_ERR_NULL;
     if (gpps_status r = check_hypers(sigma_f2, l, Q)) return r;
     if (!(beta > 0.0) || !std::isfinite(beta) || !(jitter >= 0.0) || !std::isfinite(jitter))
@@ -190,9 +214,9 @@ gpps_status gpps_bound(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D
     for (const void *p : {mu, S, Z, Y, (const void *)L, (const void *)dmu, (const void *)dS,
                           (const void *)dZ, (const void *)dsigma_f2, (const void *)dl,
                           (const void *)dbeta})
-        if (!aligned(p, elem)) return GPPS_ERR_ALIGN;
+        if (p && !aligned(p, elem)) return GPPS_ERR_ALIGN;
     const gpps::Shape s = gpps::make_shape(N, M, Q);
-    const int path = choose_path(dt, s);
+    const int path = choose_path(dt, s, S);
     if (path < 0) return GPPS_ERR_PATH;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const size_t psi_ws = gpps_workspace_bytes(dt, N, M, Q);

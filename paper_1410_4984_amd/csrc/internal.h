@@ -78,6 +78,20 @@ hipError_t mfma_psi_grads(const Shape &s, const float *mu, const float *S, const
                           const float *G2, float *dmu, float *dS, float *dZ, float *dsf2,
                           float *dl, int accumulate, void *ws, hipStream_t st);
 
+// ---------------------------------------------------------------- known inputs (S = 0)
+// Psi1 = Kfu, Psi2 = Kfu^T Kfu on the matrix cores (fp32 and fp64); X holds the
+// inputs (the mu argument of the ABI).
+size_t known_workspace_bytes(const Shape &s, size_t elem);
+
+template <typename T>
+hipError_t known_psi_stats(const Shape &s, const T *X, const T *Z, const Hyp<T> &h, T *psi0,
+                           T *Psi1, T *Psi2, int accumulate, void *ws, hipStream_t st);
+
+template <typename T>
+hipError_t known_psi_grads(const Shape &s, const T *X, const T *Z, const Hyp<T> &h, T dL_dpsi0,
+                           const T *G1, const T *G2, T *dX, T *dZ, T *dsf2, T *dl, int accumulate,
+                           void *ws, hipStream_t st);
+
 // ---------------------------------------------------------------- Bayesian GP-LVM bound
 // Byte offsets of the psi-statistic buffers inside the bound's workspace (after
 // the first psi_ws bytes, which serve the psi-statistic kernels).
@@ -89,13 +103,14 @@ BoundBufs bound_buffers(const Shape &s, int64_t D, size_t elem, size_t psi_ws);
 
 // After the psi-statistics: Kmm, A, their inverses and log determinants, Psi1^T Y,
 // the bound L and dL/dbeta, and dL/dPsi1 (over Psi1) and dL/dPsi2 in the workspace.
+// S = nullptr: known inputs, no KL term.
 template <typename T>
 hipError_t bound_middle(const Shape &s, int64_t D, const T *mu, const T *S, const T *Z, const T *Y,
                         const Hyp<T> &h, double beta, double jitter, T *L, T *dbeta, void *ws,
                         size_t psi_ws, hipStream_t st);
 
 // After the psi-statistic gradients: the chain rule through Kmm (added to dZ,
-// dsigma_f2, dl) and the KL term (added to dmu, dS).
+// dsigma_f2, dl) and the KL term (added to dmu, dS; skipped when S = nullptr).
 template <typename T>
 hipError_t bound_tail(const Shape &s, int64_t D, const T *mu, const T *S, const T *Z, const Hyp<T> &h,
                       T *dmu, T *dS, T *dZ, T *dsf2, T *dl, void *ws, size_t psi_ws, hipStream_t st);

@@ -57,7 +57,7 @@ def test_workspace_bytes():
 def _stats(dt=0, N=10, M=4, Q=2, mu=FAKE, S=FAKE, Z=FAKE, sf2=1.0, l=L2, psi0=FAKE, P1=FAKE,
            P2=FAKE, ws=FAKE, ws_bytes=None):
     if ws_bytes is None:
-        ws_bytes = max(1, gpps.lib().gpps_workspace_bytes(0, N, M, Q))
+        ws_bytes = max(1, gpps.lib().gpps_workspace_bytes(dt if dt in (0, 1) else 0, N, M, Q))
     return gpps.lib().gpps_psi_stats(dt, N, M, Q, mu, S, Z, sf2, l, psi0, P1, P2, 0, ws,
                                      ws_bytes, None)
 
@@ -65,7 +65,7 @@ def _stats(dt=0, N=10, M=4, Q=2, mu=FAKE, S=FAKE, Z=FAKE, sf2=1.0, l=L2, psi0=FA
 def _grads(dt=0, N=10, M=4, Q=2, mu=FAKE, S=FAKE, Z=FAKE, sf2=1.0, l=L2, d0=0.5, G1=FAKE,
            G2=FAKE, dmu=FAKE, dS=FAKE, dZ=FAKE, dsf2=FAKE, dl=FAKE, ws=FAKE, ws_bytes=None):
     if ws_bytes is None:
-        ws_bytes = max(1, gpps.lib().gpps_workspace_bytes(0, N, M, Q))
+        ws_bytes = max(1, gpps.lib().gpps_workspace_bytes(dt if dt in (0, 1) else 0, N, M, Q))
     return gpps.lib().gpps_psi_grads(dt, N, M, Q, mu, S, Z, sf2, l, d0, G1, G2, dmu, dS, dZ,
                                      dsf2, dl, 0, ws, ws_bytes, None)
 
@@ -102,6 +102,20 @@ def test_validation_grads_specific():
     for k in ("dmu", "dS", "dZ", "dsf2", "dl"):
         assert _grads(**{k: None}) == ERR_NULL
     assert _grads(d0=float("nan")) == ERR_HYPER
+
+
+def test_validation_known_inputs():
+    """S = NULL selects the known-input path: S and dS may then be NULL, every
+    other check still applies (each call below stops before any HIP call)."""
+    assert _stats(S=None, ws_bytes=1) == ERR_WS
+    assert _stats(S=None, P2=None) == ERR_NULL
+    assert _grads(S=None, dS=None, ws_bytes=1) == ERR_WS
+    assert _grads(S=None, dS=None, dZ=None) == ERR_NULL
+    assert _grads(S=None, dS=None, sf2=0.0) == ERR_HYPER
+    assert _grads(S=FAKE, dS=None) == ERR_NULL
+    # the workspace query covers the known-input path for both dtypes
+    for dt in ("f32", "f64"):
+        assert gpps.workspace_bytes(dt, 5000, 300, 4) >= 2 * 5000 * 300 * (4 if dt == "f32" else 8)
 
 
 def test_path_selection():
@@ -150,8 +164,12 @@ def test_bound_validation_codes():
     assert _bound(D=0) == ERR_SHAPE
     assert _bound(Q=gpps.MAX_Q + 1) == ERR_SHAPE
     assert _bound(M=513) == ERR_SHAPE
-    for k in ("mu", "S", "Z", "Y", "L", "dmu", "dS", "dZ", "dsf2", "dl", "dbeta", "ws"):
+    for k in ("mu", "Z", "Y", "L", "dmu", "dS", "dZ", "dsf2", "dl", "dbeta", "ws"):
         assert _bound(**{k: None}) == ERR_NULL, k
+    # S = NULL (known inputs) with dS = NULL passes the pointer checks; the
+    # short workspace then stops the call before any HIP call
+    assert _bound(S=None, dS=None, ws_bytes=1) == ERR_WS
+    assert _bound(S=None, dS=None, dmu=None) == ERR_NULL
     assert _bound(l=None) == ERR_NULL
     assert _bound(sf2=-1.0) == ERR_HYPER
     assert _bound(beta=0.0) == ERR_HYPER

@@ -23,6 +23,12 @@ the paper's experiment (section 4: Q = 1, M = 100, D = 3, here N = 64,000,
 fp64), in evaluations per second, with the fp64 oracle timed on one full
 evaluation beside it.
 
+--workload known times the known-input (S = 0) path at the large workload's
+shape and distributions (N=100,000, M=256, Q=20, the S array dropped):
+gpps_psi_stats + gpps_psi_grads with S = NULL, where Psi2 = Kfu^T Kfu and
+dL/dKfu = G1 + 2 Kfu G2s run on the matrix cores.  Same metric and unit;
+--dtype f64 runs it in double precision.
+
 --copy-probe-mib X runs a plain device copy (torch.neg into a second buffer) of
 X MiB three times before the timed steps: under a rocprofv3 --pmc run its
 FETCH_SIZE / WRITE_SIZE calibrate the counters against a known byte count.
@@ -67,6 +73,13 @@ def algorithmic(kernel: str, N: int, M: int, Q: int):
         "generic_psi1": ("hbm", 4.0 * (N * M + 2 * N * Q), "byte"),
         "mfma_psi1_fwd": ("hbm", 4.0 * (N * M + 2 * N * Q), "byte"),
         "mfma_psi1_grad": ("hbm", 4.0 * (N * M + 4 * N * Q), "byte"),
+        # known inputs (S = 0): the rank-k update over the unique pairs, the
+        # gradient GEMM over all M x M, Kfu and the chain-rule passes per (n, m, q)
+        "known_syrk": ("mfma", 2.0 * N * P, "flop"),
+        "known_dkfu": ("mfma", 2.0 * N * M * M, "flop"),
+        "known_kfu": ("alu", 3.0 * N * M * Q, "flop"),
+        "known_rows": ("alu", 2.0 * N * M * Q, "flop"),
+        "known_cols": ("alu", 2.0 * N * M * Q, "flop"),
     }
     return table.get(kernel)
 
@@ -216,6 +229,95 @@ def bench_gplvm(args):
     print(json.dumps(rec), flush=True)
 
 
+def bench_known(args):
+    """One step = gpps_psi_stats + gpps_psi_grads with S = NULL (known inputs) at
+    the large workload's shape."""
+    import numpy as np
+    import torch
+
+    import paper_1410_4984_amd as gpps
+    from paper_1410_4984_amd import synth
+
+    w = synth.WORKLOADS["large"]
+    N, M, Q = w.N, w.M, w.Q
+    f64 = args.dtype == "f64"
+    dt = torch.float64 if f64 else torch.float32
+    inp = synth.make_workload("large")
+    inp["S"] = None
+    if not f64:
+        inp = synth.to_f32(inp)
+    dev = "cuda:0"
+    t = {k: torch.tensor(v, dtype=dt, device=dev) for k, v in inp.items()
+         if isinstance(v, np.ndarray)}
+    psi0 = torch.zeros(1, dtype=dt, device=dev)
+    P1 = torch.empty((N, M), dtype=dt, device=dev)
+    P2 = torch.empty((M, M), dtype=dt, device=dev)
+    g = {"dmu": torch.empty((N, Q), dtype=dt, device=dev), "dS": None,
+         "dZ": torch.empty((M, Q), dtype=dt, device=dev),
+         "dsigma_f2": torch.empty(1, dtype=dt, device=dev),
+         "dl": torch.empty(Q, dtype=dt, device=dev)}
+    ws = torch.empty(gpps.workspace_bytes(dt, N, M, Q), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gpps.psi_stats(t["mu"], None, t["Z"], inp["sigma_f2"], inp["l"], out=(psi0, P1, P2),
+                       workspace=ws, stream=stream)
+        gpps.psi_grads(t["mu"], None, t["Z"], inp["sigma_f2"], inp["l"], inp["dL_dpsi0"],
+                       t["dL_dPsi1"], t["dL_dPsi2"], out=g, workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    L = gpps.lib()
+    L.gpps_timing_enable.argtypes = [ctypes.c_int]
+    L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    L.gpps_timing_enable(1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    L.gpps_timing_enable(0)
+    kernels = timed_kernels(L)
+    ms = (t1 - t0) * 1e3 / args.steps
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+    peak_f = PEAK_FP64 if f64 else PEAK_FP32
+    roofline = None
+    alg = algorithmic(dom, N, M, Q)
+    if alg:
+        bound, work, unit = alg
+        ach = work / (kernels[dom]["avg_ms"] * 1e-3) / 1e12
+        roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3),
+                    "peak": peak_f / 1e12, "unit": "TFLOP/s", "frac": round(ach * 1e12 / peak_f, 4),
+                    "traffic": None if f64 else traffic_for(dom, "large_known"),
+                    "algorithmic_per_launch": work}
+    mm = {}
+    for k in ("known_syrk", "known_dkfu"):
+        if k in kernels:
+            a = algorithmic(k, N, M, Q)[1] / (kernels[k]["avg_ms"] * 1e-3)
+            mm[k] = {"tflops": round(a / 1e12, 2), "frac": round(a / peak_f, 4)}
+    rec = {
+        "metric": METRIC.replace("(fp32)", "(fp64)") if f64 else METRIC,
+        "value": float(N) * M * M * Q / (ms * 1e-3), "unit": "terms/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64" if f64 else "f32", "data": "synthetic",
+        "config": {"workload": f"large-known (N={N}, M={M}, Q={Q}, S = 0: known inputs, seed 0)",
+                   "N": N, "M": M, "Q": Q},
+        "matrix_core": mm,
+        "roofline": roofline,
+        "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}
+                    for k, v in sorted(kernels.items())},
+    }
+    if not args.no_cpu_baseline:
+        base = dict(inp, S=np.zeros_like(inp["mu"]))
+        rec["cpu_baseline"] = cpu_baseline(base, args.cpu_seconds)
+        rec["cpu_baseline"]["sample"] += " (S = 0)"
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -226,6 +328,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0)
+    ap.add_argument("--dtype", default="f32", choices=["f32", "f64"],
+                    help="element type of --workload known")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the multi-GPU path (row sharding with an "
@@ -235,6 +339,9 @@ def main():
 
     if args.workload == "gplvm":
         bench_gplvm(args)
+        return
+    if args.workload == "known":
+        bench_known(args)
         return
 
     import numpy as np

@@ -83,7 +83,8 @@ struct KPlan {
     int64_t grid_syrk;          // Psi2 workgroups (XCD-rounded)
     int64_t rblocks;            // row-kernel blocks (256 datapoints each)
     int64_t cchunks, crows;     // column-kernel row chunks and rows per chunk
-    size_t off_cz, off_xs, off_zs, off_k, off_e, off_g2s, off_part, off_rowp, off_colp, total;
+    size_t off_cz, off_xs, off_zs, off_k, off_e, off_g2s, off_part, off_rowp, off_colp, off_vc;
+    size_t total;
 };
 
 KPlan make_kplan(const Shape &s, size_t elem) {
@@ -114,25 +115,37 @@ KPlan make_kplan(const Shape &s, size_t elem) {
     p.off_part = take(elem * p.chunks * p.ntu * p.tile * p.tile);
     p.off_rowp = take(elem * p.rblocks * (s.Q + 1));
     p.off_colp = take(elem * p.cchunks * s.M * (s.Q + 1));
+    p.off_vc = take(elem * s.M * (s.Q + 1));
     p.total = o;
     return p;
 }
 
 // ---------------------------------------------------------------- centring
-// cz[q] = mean_m z_mq (fixed order), zs = (Z - cz) / l.  One workgroup.
+// cz[q] = mean_m z_mq, zs = (Z - cz) / l.  One workgroup: G = 256 / Q groups of
+// Q threads sum rows m = g, g + G, ... (coalesced), then the G partial sums of
+// each dimension are added in group order.
 template <typename T>
 __global__ __launch_bounds__(256) void known_centre_kernel(int M, int Q, const T *__restrict__ Z,
                                                            Hyp<T> h, T *__restrict__ cz,
                                                            T *__restrict__ zs) {
+    __shared__ T part[256];
     __shared__ T c[GPPS_MAX_Q];
-    if ((int)threadIdx.x < Q) {
+    const int t = threadIdx.x, G = 256 / Q;
+    if (t < G * Q) {
+        const int g = t / Q, q = t - g * Q;
         T s = 0;
-        for (int m = 0; m < M; ++m) s += Z[(int64_t)m * Q + threadIdx.x];
-        c[threadIdx.x] = s / T(M);
-        cz[threadIdx.x] = c[threadIdx.x];
+        for (int m = g; m < M; m += G) s += Z[(int64_t)m * Q + q];
+        part[t] = s;
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < M * Q; i += 256) zs[i] = (Z[i] - c[i % Q]) / h.l[i % Q];
+    if (t < Q) {
+        T s = 0;
+        for (int g = 0; g < G; ++g) s += part[g * Q + t];
+        c[t] = s / T(M);
+        cz[t] = c[t];
+    }
+    __syncthreads();
+    for (int i = t; i < M * Q; i += 256) zs[i] = (Z[i] - c[i % Q]) / h.l[i % Q];
 }
 
 // ---------------------------------------------------------------- Kfu
@@ -297,8 +310,19 @@ __global__ __launch_bounds__(256) void known_syrk_reduce_kernel(int64_t N, int M
     block_pair(p, ntp, gi, gj);
     const int m = gi * TILE + e / TILE, mp = gj * TILE + e % TILE;
     if (m >= M || mp >= M || m > mp) return;
+    // chunk order; loads issued 16 at a time so that they overlap
+    const T *src = part + p * TT + e;
+    const int64_t stride = ntu * TT;
     T s = 0;
-    for (int64_t c = 0; c < chunks; ++c) s += part[(c * ntu + p) * TT + e];
+    int64_t c = 0;
+    for (; c + 16 <= chunks; c += 16) {
+        T v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = src[(c + j) * stride];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s += v[j];
+    }
+    for (; c < chunks; ++c) s += src[c * stride];
     const T v = (accumulate ? Psi2[(int64_t)m * M + mp] : T(0)) + s;
     Psi2[(int64_t)m * M + mp] = v;
     Psi2[(int64_t)mp * M + m] = v;
@@ -390,7 +414,38 @@ __device__ inline T block_sum(T v, T *red4) {
     return ((red4[0] + red4[1]) + red4[2]) + red4[3];
 }
 
-// One thread per datapoint: r_n and U_n from E^T (coalesced over n), dx_n, and
+// 16-byte vectors for LDS reads of the scaled-input tables.
+template <typename T>
+struct Vec;
+template <>
+struct Vec<float> {
+    typedef float t __attribute__((ext_vector_type(4)));
+    static constexpr int W = 4;
+};
+template <>
+struct Vec<double> {
+    typedef double t __attribute__((ext_vector_type(2)));
+    static constexpr int W = 2;
+};
+
+// acc[0..QM) += e * row[0..QM) for an LDS row that is zero beyond Q (no
+// per-dimension guard: a runtime bound inside the unrolled loop makes the
+// compiler shuffle the accumulators).
+template <typename T, int QM>
+__device__ inline void axpy_row(T e, const T *row, T *acc) {
+    using V = typename Vec<T>::t;
+    constexpr int W = Vec<T>::W;
+    const V *r = reinterpret_cast<const V *>(row);
+#pragma unroll
+    for (int v = 0; v < QM / W; ++v) {
+        const V z = r[v];
+#pragma unroll
+        for (int w = 0; w < W; ++w) acc[v * W + w] = fma(e, z[w], acc[v * W + w]);
+    }
+}
+
+// One thread per datapoint: r_n and U_n (sums over m of E^T[m][n] and of
+// E^T[m][n] zs_m; coalesced over n, loads issued 16 at a time), dx_n, and
 // per-block partials of sum_n (r xs^2 - 2 xs U) (dl) and sum_n r (dsf2).
 template <typename T, int QM>
 __global__ __launch_bounds__(256) void known_rows_kernel(int64_t N, int M, int Q,
@@ -399,7 +454,7 @@ __global__ __launch_bounds__(256) void known_rows_kernel(int64_t N, int M, int Q
                                                          const T *__restrict__ zs, Hyp<T> h,
                                                          T *__restrict__ dX,
                                                          T *__restrict__ rowpart) {
-    __shared__ T sz[kEdge][QM];
+    __shared__ __align__(16) T sz[kEdge][QM];  // zero beyond Q and beyond the block's rows
     __shared__ T red4[4];
     const int tid = threadIdx.x;
     const int64_t n = (int64_t)blockIdx.x * 256 + tid;
@@ -410,18 +465,22 @@ __global__ __launch_bounds__(256) void known_rows_kernel(int64_t N, int M, int Q
     for (int mb = 0; mb < M; mb += kEdge) {
         const int cnt = min(kEdge, M - mb);
         __syncthreads();
-        for (int i = tid; i < cnt * Q; i += 256) {
-            const int c = i / Q, q = i - c * Q;
-            sz[c][q] = zs[(int64_t)(mb + c) * Q + q];
+        for (int i = tid; i < kEdge * QM; i += 256) {
+            const int c = i / QM, q = i - c * QM;
+            sz[c][q] = (c < cnt && q < Q) ? zs[(int64_t)(mb + c) * Q + q] : T(0);
         }
         __syncthreads();
         if (valid) {
-            for (int c = 0; c < cnt; ++c) {
-                const T e = Et[(int64_t)(mb + c) * N + n];
-                r += e;
+            for (int c0 = 0; c0 < cnt; c0 += 16) {
+                T e[16];
 #pragma unroll
-                for (int q = 0; q < QM; ++q)
-                    if (q < Q) U[q] = fma(e, sz[c][q], U[q]);
+                for (int j = 0; j < 16; ++j)
+                    e[j] = c0 + j < cnt ? Et[(int64_t)(mb + c0 + j) * N + n] : T(0);
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    r += e[j];
+                    axpy_row<T, QM>(e[j], &sz[c0 + j][0], U);
+                }
             }
         }
     }
@@ -449,8 +508,8 @@ __global__ __launch_bounds__(256) void known_cols_kernel(int64_t N, int M, int Q
                                                          const T *__restrict__ Et,
                                                          const T *__restrict__ xs,
                                                          T *__restrict__ colpart) {
-    __shared__ T se[kEdge][kEdge + 1];  // E^T tile [m][n]
-    __shared__ T sx[kEdge][QM];         // xs rows of the tile
+    __shared__ T se[kEdge][kEdge + 1];         // E^T tile [m][n], zero outside
+    __shared__ __align__(16) T sx[kEdge][QM];  // xs rows of the tile, zero outside
     __shared__ T red[4][kEdge];
     const int tid = threadIdx.x;
     const int m0 = blockIdx.x * kEdge;
@@ -467,20 +526,17 @@ __global__ __launch_bounds__(256) void known_cols_kernel(int64_t N, int M, int Q
             const int m = m0 + row;
             se[row][col] = (m < M && col < cnt) ? Et[(int64_t)m * N + nb + col] : T(0);
         }
-        for (int i = tid; i < cnt * Q; i += 256) {
-            const int rr = i / Q, q = i - rr * Q;
-            sx[rr][q] = xs[(nb + rr) * Q + q];
+        for (int i = tid; i < kEdge * QM; i += 256) {
+            const int rr = i / QM, q = i - rr * QM;
+            sx[rr][q] = (rr < cnt && q < Q) ? xs[(nb + rr) * Q + q] : T(0);
         }
         __syncthreads();
+#pragma unroll 4
         for (int j = 0; j < 16; ++j) {
             const int col = quarter * 16 + j;
-            if (col < cnt) {
-                const T e = se[mr][col];
-                c += e;
-#pragma unroll
-                for (int q = 0; q < QM; ++q)
-                    if (q < Q) V[q] = fma(e, sx[col][q], V[q]);
-            }
+            const T e = se[mr][col];
+            c += e;
+            axpy_row<T, QM>(e, &sx[col][0], V);
         }
     }
     const int m = m0 + mr;
@@ -497,56 +553,59 @@ __global__ __launch_bounds__(256) void known_cols_kernel(int64_t N, int M, int Q
     }
 }
 
-// One workgroup per output (dZ[m][q], then dl[q], then dsf2), sums in a fixed
-// order: thread t takes partials t, t + 256, ..., then a fixed tree.
+// One workgroup per inducing input m: Vc[m][k] = sum over the column chunks of
+// colpart[chunk][m][k], k <= Q.  G = 256 / (Q + 1) groups of Q + 1 threads take
+// chunks g, g + G, ... (coalesced over k); the G partials are added in order.
 template <typename T>
-__global__ __launch_bounds__(256) void known_grad_reduce_kernel(
-    int64_t N, int M, int Q, int64_t cchunks, int64_t rblocks, const T *__restrict__ colpart,
+__global__ __launch_bounds__(256) void known_col_reduce_kernel(int M, int Q, int64_t cchunks,
+                                                               const T *__restrict__ colpart,
+                                                               T *__restrict__ Vc) {
+    __shared__ T part[256];
+    const int t = threadIdx.x, Q1 = Q + 1, G = 256 / Q1;
+    const int64_t m = blockIdx.x;
+    if (t < G * Q1) {
+        const int g = t / Q1, k = t - g * Q1;
+        T s = 0;
+        for (int64_t c = g; c < cchunks; c += G) s += colpart[(c * M + m) * Q1 + k];
+        part[t] = s;
+    }
+    __syncthreads();
+    if (t < Q1) {
+        T s = 0;
+        for (int g = 0; g < G; ++g) s += part[g * Q1 + t];
+        Vc[m * Q1 + t] = s;
+    }
+}
+
+// dZ[m][q] = (V_mq - zs_mq c_m) / l_q elementwise (blocks below zblocks), then
+// one workgroup per dl_q and one for dsf2, each a fixed-order block sum.
+template <typename T>
+__global__ __launch_bounds__(256) void known_grad_final_kernel(
+    int64_t N, int M, int Q, int64_t zblocks, int64_t rblocks, const T *__restrict__ Vc,
     const T *__restrict__ rowpart, const T *__restrict__ zs, Hyp<T> h, T dL_dpsi0,
     T *__restrict__ dZ, T *__restrict__ dsf2, T *__restrict__ dl, int accumulate) {
-    __shared__ T red[2][256];
-    const int tid = threadIdx.x;
-    const int64_t i = blockIdx.x, MQ = (int64_t)M * Q, Q1 = Q + 1;
-    T s = 0, s2 = 0;
-    if (i < MQ) {
+    __shared__ T red4[4];
+    const int64_t Q1 = Q + 1;
+    if ((int64_t)blockIdx.x < zblocks) {
+        const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+        if (i >= (int64_t)M * Q) return;
         const int64_t m = i / Q, q = i - m * Q;
-        for (int64_t c = tid; c < cchunks; c += 256) {
-            s += colpart[(c * M + m) * Q1 + q];
-            s2 += colpart[(c * M + m) * Q1 + Q];
-        }
-    } else if (i < MQ + Q) {
-        const int64_t q = i - MQ;
-        for (int64_t b = tid; b < rblocks; b += 256) s += rowpart[b * Q1 + q];
-        for (int64_t j = tid; j < cchunks * M; j += 256) {
-            const int64_t m = j % M;
-            const T z = zs[m * Q + q];
-            s2 += colpart[j * Q1 + Q] * z * z;
-        }
-    } else {
-        for (int64_t b = tid; b < rblocks; b += 256) s += rowpart[b * Q1 + Q];
-    }
-    red[0][tid] = s;
-    red[1][tid] = s2;
-    __syncthreads();
-    for (int w = 128; w >= 1; w >>= 1) {
-        if (tid < w) {
-            red[0][tid] += red[0][tid + w];
-            red[1][tid] += red[1][tid + w];
-        }
-        __syncthreads();
-    }
-    if (tid != 0) return;
-    s = red[0][0];
-    s2 = red[1][0];
-    if (i < MQ) {
-        const int64_t q = i % Q;
-        const T v = (s - zs[i] * s2) / h.l[q];
+        const T v = (Vc[m * Q1 + q] - zs[i] * Vc[m * Q1 + Q]) / h.l[q];
         dZ[i] = (accumulate ? dZ[i] : T(0)) + v;
-    } else if (i < MQ + Q) {
-        const int64_t q = i - MQ;
-        dl[q] = (accumulate ? dl[q] : T(0)) + (s + s2) / h.l[q];
-    } else {
-        dsf2[0] = (accumulate ? dsf2[0] : T(0)) + (s / h.sf2 + dL_dpsi0 * T(N));
+        return;
+    }
+    const int k = (int)(blockIdx.x - zblocks);  // k < Q: dl_k; k == Q: dsf2
+    T s = 0;
+    for (int64_t b = threadIdx.x; b < rblocks; b += 256) s += rowpart[b * Q1 + k];
+    if (k < Q)
+        for (int m = threadIdx.x; m < M; m += 256) {
+            const T z = zs[(int64_t)m * Q + k];
+            s += Vc[(int64_t)m * Q1 + Q] * z * z;
+        }
+    s = block_sum(s, red4);
+    if (threadIdx.x == 0) {
+        if (k < Q) dl[k] = (accumulate ? dl[k] : T(0)) + s / h.l[k];
+        else dsf2[0] = (accumulate ? dsf2[0] : T(0)) + (s / h.sf2 + dL_dpsi0 * T(N));
     }
 }
 
@@ -631,9 +690,13 @@ hipError_t known_psi_grads(const Shape &s, const T *X, const T *Z, const Hyp<T> 
     else if (s.Q <= 32) launch_chain<T, 32>(s, p, Et, h, dX, ws, st);
     else launch_chain<T, 64>(s, p, Et, h, dX, ws, st);
     TimedScope ts(st, "known_grad_reduce");
-    known_grad_reduce_kernel<T><<<(unsigned)(s.M * s.Q + s.Q + 1), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, p.cchunks, p.rblocks, at<T>(ws, p.off_colp), at<T>(ws, p.off_rowp),
-        at<T>(ws, p.off_zs), h, dL_dpsi0, dZ, dsf2, dl, accumulate);
+    T *Vc = at<T>(ws, p.off_vc);
+    known_col_reduce_kernel<T><<<(unsigned)s.M, 256, 0, st>>>((int)s.M, (int)s.Q, p.cchunks,
+                                                             at<T>(ws, p.off_colp), Vc);
+    const int64_t zblocks = cdiv(s.M * s.Q, 256);
+    known_grad_final_kernel<T><<<(unsigned)(zblocks + s.Q + 1), 256, 0, st>>>(
+        s.N, (int)s.M, (int)s.Q, zblocks, p.rblocks, Vc, at<T>(ws, p.off_rowp), at<T>(ws, p.off_zs),
+        h, dL_dpsi0, dZ, dsf2, dl, accumulate);
     return hipGetLastError();
 }
 

@@ -78,15 +78,20 @@ def kl(mu, S):
         return 0.5 * float(np.sum(mu * mu + S - np.log(S) - 1.0))
 
 
-def bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
+def bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd, stats=None):
     """(F, KL, pieces): the collapsed bound F and the KL term, plus the
     intermediate matrices the gradient needs.  ``inverse`` maps a Cholesky
     factor to the inverse of its matrix (default: triangular solves).  S = None:
-    known inputs (zero variances), KL = 0."""
+    known inputs (zero variances), KL = 0.  ``stats`` = (psi0, Psi1, Psi2) uses
+    the given statistics instead of computing them (to measure how sensitive
+    the bound is to errors in them)."""
     mu = np.asarray(mu, np.float64)
     Y = np.asarray(Y, np.float64)
     N, D = Y.shape
-    psi0, Psi1, Psi2 = psi_stats(mu, np.zeros_like(mu) if S is None else S, Z, sigma_f2, l)
+    if stats is None:
+        psi0, Psi1, Psi2 = psi_stats(mu, np.zeros_like(mu) if S is None else S, Z, sigma_f2, l)
+    else:
+        psi0, Psi1, Psi2 = stats
     Psi1 = np.asarray(Psi1).reshape(N, -1)
     Psi2 = np.asarray(Psi2)
     M = Psi2.shape[0]
@@ -115,9 +120,9 @@ def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter):
     return F - K
 
 
-def upstream(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
+def upstream(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd, stats=None):
     """(L, dL/dpsi0, dL/dPsi1, dL/dPsi2, dL/dKmm, dL/dbeta, pieces)."""
-    F, K, p = bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse)
+    F, K, p = bound_terms(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse, stats)
     D = p["D"]
     Kinv, Ainv, C, Psi2, Psi = p["Kinv"], p["Ainv"], p["C"], p["Psi2"], p["Psi"]
     P = C @ C.T
@@ -147,12 +152,13 @@ def kmm_grads(Z, sigma_f2, l, G):
     return dZ, dsf2, dl
 
 
-def grads(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd):
+def grads(mu, S, Z, Y, sigma_f2, l, beta, jitter, inverse=_inv_spd, stats=None):
     """L and its gradient w.r.t. every parameter:
     dict(L, dmu, dS, dZ, dsigma_f2, dl, dbeta).  S = None (known inputs): dmu is
-    dL/dX and dS is None."""
+    dL/dX and dS is None.  ``stats`` as for bound_terms (the chain rule through
+    the statistics is still taken at mu, S, Z)."""
     L, d_psi0, d_Psi1, d_Psi2, d_Kmm, d_beta, p = upstream(mu, S, Z, Y, sigma_f2, l, beta,
-                                                            jitter, inverse)
+                                                            jitter, inverse, stats)
     mu = np.asarray(mu, np.float64)
     known = S is None
     S = np.zeros_like(mu) if known else np.asarray(S, np.float64)

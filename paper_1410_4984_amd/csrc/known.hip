@@ -14,17 +14,16 @@
 //           GEMM over the inducing inputs, E = dL/dKfu o Kfu, and the chain
 //           rule through the kernel.  With xs = (x - c) / l and zs = (z - c) / l
 //           per dimension (c the mean of Z; the kernel depends on differences
-//           only, and centring keeps the expanded sums below well scaled):
-//             r_n = sum_m E,  U_nq = sum_m E zs_mq,  c_m = sum_n E,  V_mq = sum_n E xs_nq
-//             dx_nq = -(xs_nq r_n - U_nq) / l_q
-//             dz_mq = (V_mq - zs_mq c_m) / l_q
-//             dl_q  = (sum_n (r_n xs_nq^2 - 2 xs_nq U_nq) + sum_m c_m zs_mq^2) / l_q
-//             dsf2  = sum E / sf2 + N dL/dpsi0.
+//           only) and d_nmq = xs_nq - zs_mq:
+//             dx_nq = -sum_m E d / l_q
+//             dz_mq =  sum_n E d / l_q
+//             dl_q  =  sum_nm E d^2 / l_q
+//             dsf2  =  sum E / sf2 + N dL/dpsi0.
 //
 // Matrix-core products: fp32 v_mfma_f32_32x32x2f32 (fp32 products, fp32
-// accumulation), fp64 v_mfma_f64_16x16x4f64.  Every tiled kernel works on
-// 64 x 64 output blocks, one wave per block.  No atomics; results are bitwise
-// deterministic for a fixed shape.
+// accumulation), fp64 v_mfma_f64_16x16x4f64, on 128 x 128 blocks staged
+// through LDS (block_product).  No atomics; results are bitwise deterministic
+// for a fixed shape.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -32,8 +31,8 @@
 namespace gpps {
 namespace {
 
-constexpr int kEdge = 64;              // output block edge of every tiled kernel
-constexpr int kUnroll = 4;             // matrix-core k-steps per batch of loads
+constexpr int kEdge = 64;              // block edge of the Kfu and chain-rule kernels
+constexpr int kBlk = 128;              // block edge of the matrix-core products
 constexpr float kLog2eF = 1.4426950408889634f;
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -67,6 +66,20 @@ struct Mma<double> {
     __device__ static int row(int v, int lane) { return 4 * v + (lane >> 4); }
 };
 
+// 16-byte vectors (global loads into LDS, LDS row reads).
+template <typename T>
+struct Vec;
+template <>
+struct Vec<float> {
+    typedef float t __attribute__((ext_vector_type(4)));
+    static constexpr int W = 4;
+};
+template <>
+struct Vec<double> {
+    typedef double t __attribute__((ext_vector_type(2)));
+    static constexpr int W = 2;
+};
+
 // sf2 exp(-s / 2) from the prefactor pre(h) and the squared scaled distance s.
 __device__ inline float kpre(const Hyp<float> &h) { return h.log_sf2 * kLog2eF; }
 __device__ inline double kpre(const Hyp<double> &h) { return h.log_sf2; }
@@ -78,7 +91,8 @@ __device__ inline double kval(double pre, double s) { return exp(pre - 0.5 * s);
 // ---------------------------------------------------------------- launch plan
 struct KPlan {
     int tile;                   // matrix-core tile edge (32 fp32, 16 fp64)
-    int64_t nb, ntp, ntu, nbp;  // 64-blocks per edge, tiles per edge, upper tiles, upper block pairs
+    int64_t nb;                 // 64-blocks of inducing inputs (column kernel)
+    int64_t nb2, ntp, ntu, nbp; // kBlk-blocks per edge, tiles per edge, upper tiles, upper block pairs
     int64_t chunks, rows;       // Psi2 row chunks and rows per chunk
     int64_t grid_syrk;          // Psi2 workgroups (XCD-rounded)
     int64_t rblocks;            // row-kernel blocks (256 datapoints each)
@@ -91,13 +105,18 @@ KPlan make_kplan(const Shape &s, size_t elem) {
     KPlan p{};
     p.tile = elem == 4 ? 32 : 16;
     p.nb = cdiv(s.M, kEdge);
-    p.ntp = p.nb * (kEdge / p.tile);
+    p.nb2 = cdiv(s.M, kBlk);
+    p.ntp = p.nb2 * (kBlk / p.tile);
     p.ntu = p.ntp * (p.ntp + 1) / 2;
-    p.nbp = p.nb * (p.nb + 1) / 2;
-    // about two waves per SIMD for the rank-k update; each chunk a multiple of
-    // the unrolled k-step so that only the last one is ragged
-    p.chunks = std::max<int64_t>(1, std::min<int64_t>(cdiv(s.N, 256), 2048 / p.nbp));
-    p.rows = round_up(cdiv(s.N, p.chunks), 16);
+    p.nbp = p.nb2 * (p.nb2 + 1) / 2;
+    // at most one round of two workgroups per CU for the rank-k update (the
+    // chunk count a multiple of the 8 XCDs, so the XCD-rounded grid stays
+    // within it); each chunk a multiple of the LDS slab so that only the last
+    // one is ragged
+    const int64_t bk = elem == 4 ? 32 : 16;
+    const int64_t fit = 512 / p.nbp >= 8 ? 512 / p.nbp / 8 * 8 : std::max<int64_t>(1, 512 / p.nbp);
+    p.chunks = std::max<int64_t>(1, std::min<int64_t>(cdiv(s.N, 4 * bk), fit));
+    p.rows = round_up(cdiv(s.N, p.chunks), bk);
     p.chunks = cdiv(s.N, p.rows);
     p.grid_syrk = round_up(p.chunks, 8) * p.nbp;
     p.rblocks = cdiv(s.N, 256);
@@ -113,9 +132,9 @@ KPlan make_kplan(const Shape &s, size_t elem) {
     p.off_e = take(elem * s.N * s.M);
     p.off_g2s = take(elem * s.M * s.M);
     p.off_part = take(elem * p.chunks * p.ntu * p.tile * p.tile);
-    p.off_rowp = take(elem * p.rblocks * (s.Q + 1));
-    p.off_colp = take(elem * p.cchunks * s.M * (s.Q + 1));
-    p.off_vc = take(elem * s.M * (s.Q + 1));
+    p.off_rowp = take(elem * p.rblocks);
+    p.off_colp = take(elem * p.cchunks * s.M * 2 * s.Q);
+    p.off_vc = take(elem * s.M * 2 * s.Q);
     p.total = o;
     return p;
 }
@@ -229,65 +248,171 @@ __device__ inline void block_pair(int64_t bp, int64_t nb, int &I, int &J) {
     J = (int)(i + bp);
 }
 
-// ---------------------------------------------------------------- Psi2 = Kfu^T Kfu
-// One wave per (row chunk, upper 64-block pair (I, J)): the partial sums of the
-// chunk's rows for every upper tile of the block pair, on the matrix cores.
-// Workgroups are dispatched round-robin over the 8 XCDs, so the block pairs of
-// one chunk are given ids that land on the same XCD and share its L2.
+// ---------------------------------------------------------------- matrix-core block product
+// C[i][j] = sum_k A[k][i] B[k][j] over one kBlk x kBlk block, both operands
+// stored k-major (row k contiguous in i, resp. j): the layout of Kfu (rows n)
+// for Psi2 and of G2s and Kfu^T (rows m) for the gradient.  Four waves in a
+// 2 x 2 grid own 64 x 64 each.  k advances in LDS slabs of BK rows, double
+// buffered: the next slab's global loads (16-byte vectors where the rows
+// allow it) are in flight while the current slab feeds the matrix cores, so
+// bounds are tested once per loaded vector and never per product.
+
 template <typename T>
-__global__ __launch_bounds__(64) void known_syrk_kernel(int64_t N, int M, int64_t rows,
-                                                        int64_t chunks, int64_t nb, int64_t ntp,
-                                                        int64_t ntu, const T *__restrict__ K,
-                                                        T *__restrict__ part) {
-    using A = Mma<T>;
-    constexpr int TILE = A::TILE, KS = A::KS, BT = kEdge / TILE;
+struct Slab {
+    static constexpr int BK = sizeof(T) == 4 ? 32 : 16;   // k rows per stage
+    static constexpr int VW = Vec<T>::W;                  // elements per vector
+    static constexpr int RV = kBlk / VW;                  // vectors per slab row
+    static constexpr int PER = BK * RV / 256;             // vectors per thread (4)
+    static constexpr int SZ = BK * kBlk;                  // elements per slab
+    static constexpr size_t LDS = 4 * SZ * sizeof(T);     // two buffers of (A, B)
+};
+
+template <typename T, bool VEC>
+__device__ inline void slab_load(const T *__restrict__ src, int64_t ld, int64_t k0, int64_t k1,
+                                 int64_t c0, int64_t c1, typename Vec<T>::t (&r)[Slab<T>::PER]) {
+    constexpr int VW = Slab<T>::VW, RV = Slab<T>::RV;
+#pragma unroll
+    for (int u = 0; u < Slab<T>::PER; ++u) {
+        const int f = threadIdx.x + 256 * u;
+        const int kr = f / RV, cv = (f - kr * RV) * VW;
+        const int64_t k = k0 + kr, c = c0 + cv;
+        typename Vec<T>::t v;
+        if (VEC && k < k1 && c + VW <= c1) {
+            v = *reinterpret_cast<const typename Vec<T>::t *>(src + k * ld + c);
+        } else {
+#pragma unroll
+            for (int w = 0; w < VW; ++w) v[w] = (k < k1 && c + w < c1) ? src[k * ld + c + w] : T(0);
+        }
+        r[u] = v;
+    }
+}
+
+template <typename T>
+__device__ inline void slab_store(T *lds, const typename Vec<T>::t (&r)[Slab<T>::PER]) {
+    constexpr int VW = Slab<T>::VW, RV = Slab<T>::RV;
+#pragma unroll
+    for (int u = 0; u < Slab<T>::PER; ++u) {
+        const int f = threadIdx.x + 256 * u;
+        const int kr = f / RV, cv = (f - kr * RV) * VW;
+        *reinterpret_cast<typename Vec<T>::t *>(lds + kr * kBlk + cv) = r[u];
+    }
+}
+
+// acc[ti][tj]: tile (ti, tj) of this wave's 64 x 64 part.  Columns [a0, a_end)
+// of A and [b0, b_end) of B over rows [k0, k1).  same: the two column ranges
+// are one (a diagonal block of a symmetric product: B is not loaded, and
+// tiles below the diagonal are skipped).
+template <typename T, bool VEC>
+__device__ inline void block_product(const T *__restrict__ A, int64_t lda, int64_t a0, int64_t a_end,
+                                     const T *__restrict__ B, int64_t ldb, int64_t b0, int64_t b_end,
+                                     int64_t k0, int64_t k1, bool same, T *lds,
+                                     typename Mma<T>::acc_t (&acc)[64 / Mma<T>::TILE][64 / Mma<T>::TILE]) {
+    using MM = Mma<T>;
+    using SL = Slab<T>;
+    constexpr int TILE = MM::TILE, KS = MM::KS, BT = 64 / TILE, BK = SL::BK, SZ = SL::SZ;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w & 1, wn = w >> 1;
+    const int li = lane % TILE, lk = lane / TILE;
+#pragma unroll
+    for (int ti = 0; ti < BT; ++ti)
+#pragma unroll
+        for (int tj = 0; tj < BT; ++tj)
+#pragma unroll
+            for (int v = 0; v < MM::NACC; ++v) acc[ti][tj][v] = 0;
+    const bool active = !(same && wm > wn);
+    const bool diag = same && wm == wn;
+    const int64_t stages = k1 > k0 ? (k1 - k0 + BK - 1) / BK : 0;
+    // slabs are fetched two stages ahead into two register sets: the loads of
+    // stage s + 2 are in flight while stage s computes and stage s + 1 (fetched
+    // one stage earlier) waits in registers for its LDS buffer.  The stage loop
+    // is unrolled by two so that each register set has a fixed name.
+    using VT = typename Vec<T>::t;
+    VT ra0[SL::PER], rb0[SL::PER], ra1[SL::PER], rb1[SL::PER];
+    if (stages > 0) {
+        slab_load<T, VEC>(A, lda, k0, k1, a0, a_end, ra0);
+        if (!same) slab_load<T, VEC>(B, ldb, k0, k1, b0, b_end, rb0);
+    }
+    if (stages > 1) {
+        slab_load<T, VEC>(A, lda, k0 + BK, k1, a0, a_end, ra1);
+        if (!same) slab_load<T, VEC>(B, ldb, k0 + BK, k1, b0, b_end, rb1);
+    }
+    if (stages > 0) {
+        slab_store<T>(lds, ra0);
+        if (!same) slab_store<T>(lds + SZ, rb0);
+        __syncthreads();
+    }
+    auto step = [&](int64_t s, VT(&rac)[SL::PER], VT(&rbc)[SL::PER], VT(&ran)[SL::PER],
+                    VT(&rbn)[SL::PER]) {
+        const T *sa = lds + (s & 1) * 2 * SZ;
+        const T *sb = same ? sa : sa + SZ;
+        if (s + 2 < stages) {  // the current set was stored to LDS one stage ago
+            slab_load<T, VEC>(A, lda, k0 + (s + 2) * BK, k1, a0, a_end, rac);
+            if (!same) slab_load<T, VEC>(B, ldb, k0 + (s + 2) * BK, k1, b0, b_end, rbc);
+        }
+        if (active) {
+#pragma unroll
+            for (int ks = 0; ks < BK / KS; ++ks) {
+                const int row = (ks * KS + lk) * kBlk;
+                T a[BT], b[BT];
+#pragma unroll
+                for (int t = 0; t < BT; ++t) {
+                    a[t] = sa[row + wm * 64 + t * TILE + li];
+                    b[t] = sb[row + wn * 64 + t * TILE + li];
+                }
+#pragma unroll
+                for (int ti = 0; ti < BT; ++ti)
+#pragma unroll
+                    for (int tj = 0; tj < BT; ++tj)
+                        if (!diag || ti <= tj) acc[ti][tj] = MM::mma(a[ti], b[tj], acc[ti][tj]);
+            }
+        }
+        if (s + 1 < stages) {
+            T *nb = lds + ((s + 1) & 1) * 2 * SZ;
+            slab_store<T>(nb, ran);
+            if (!same) slab_store<T>(nb + SZ, rbn);
+        }
+        __syncthreads();
+    };
+    for (int64_t s = 0; s < stages; s += 2) {
+        step(s, ra0, rb0, ra1, rb1);
+        if (s + 1 < stages) step(s + 1, ra1, rb1, ra0, rb0);
+    }
+}
+
+// ---------------------------------------------------------------- Psi2 = Kfu^T Kfu
+// One workgroup per (row chunk, upper kBlk-block pair (I, J)): the chunk's
+// partial sums for every upper matrix-core tile of the pair.  Workgroups are
+// dispatched round-robin over the 8 XCDs, so the block pairs of one chunk get
+// ids on the same XCD and share its L2.
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void known_syrk_kernel(int64_t N, int M, int64_t rows,
+                                                         int64_t chunks, int64_t nb, int64_t ntp,
+                                                         int64_t ntu, const T *__restrict__ K,
+                                                         T *__restrict__ part) {
+    using MM = Mma<T>;
+    constexpr int TILE = MM::TILE, BT = 64 / TILE;
+    __shared__ __align__(16) T lds[4 * Slab<T>::SZ];
     const int64_t nbp = nb * (nb + 1) / 2;
     const int64_t id = blockIdx.x, slot = id >> 3;
     const int64_t chunk = (slot / nbp) * 8 + (id & 7);
     if (chunk >= chunks) return;
     int I, J;
     block_pair(slot % nbp, nb, I, J);
-    const int lane = threadIdx.x, li = lane % TILE, lk = lane / TILE;
     const int64_t r0 = chunk * rows, r1 = min(N, r0 + rows);
-    typename A::acc_t acc[BT][BT];
-#pragma unroll
-    for (int ti = 0; ti < BT; ++ti)
-#pragma unroll
-        for (int tj = 0; tj < BT; ++tj)
-#pragma unroll
-            for (int v = 0; v < A::NACC; ++v) acc[ti][tj][v] = 0;
-    const int ci = I * kEdge + li, cj = J * kEdge + li;
-    for (int64_t n = r0; n < r1; n += KS * kUnroll) {
-        T a[kUnroll][BT], b[kUnroll][BT];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const int64_t row = n + u * KS + lk;
-            const bool ok = row < r1;
-#pragma unroll
-            for (int t = 0; t < BT; ++t) {
-                const int mi = ci + t * TILE, mj = cj + t * TILE;
-                a[u][t] = (ok && mi < M) ? K[row * M + mi] : T(0);
-                b[u][t] = (ok && mj < M) ? K[row * M + mj] : T(0);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-#pragma unroll
-            for (int ti = 0; ti < BT; ++ti)
-#pragma unroll
-                for (int tj = 0; tj < BT; ++tj)
-                    if (I < J || ti <= tj) acc[ti][tj] = A::mma(a[u][ti], b[u][tj], acc[ti][tj]);
-    }
+    typename MM::acc_t acc[BT][BT];
+    block_product<T, VEC>(K, M, (int64_t)I * kBlk, M, K, M, (int64_t)J * kBlk, M, r0, r1, I == J, lds,
+                          acc);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w & 1, wn = w >> 1;
 #pragma unroll
     for (int ti = 0; ti < BT; ++ti)
 #pragma unroll
         for (int tj = 0; tj < BT; ++tj) {
-            if (!(I < J || ti <= tj)) continue;
-            const int64_t gi = (int64_t)I * BT + ti, gj = (int64_t)J * BT + tj;
+            const int64_t gi = ((int64_t)I * kBlk + wm * 64) / TILE + ti;
+            const int64_t gj = ((int64_t)J * kBlk + wn * 64) / TILE + tj;
+            if (gi > gj) continue;
             const int64_t p = gi * ntp - gi * (gi - 1) / 2 + (gj - gi);
             T *dst = part + (chunk * ntu + p) * (TILE * TILE);
 #pragma unroll
-            for (int v = 0; v < A::NACC; ++v) dst[A::row(v, lane) * TILE + li] = acc[ti][tj][v];
+            for (int v = 0; v < MM::NACC; ++v) dst[MM::row(v, lane) * TILE + lane % TILE] = acc[ti][tj][v];
         }
 }
 
@@ -337,66 +462,38 @@ __global__ void known_sym_kernel(int M, const T *__restrict__ G2, T *__restrict_
     G2s[i] = T(0.5) * (G2[(int64_t)m * M + mp] + G2[(int64_t)mp * M + m]);
 }
 
-// E^T[m][n] = (G1[n][m] + 2 sum_k G2s[m][k] Kt[k][n]) Kt[m][n], one wave per
-// 64 x 64 block (m, n) on the matrix cores.  G2s is symmetric, so its A operand
-// G2s[m][k] is read as G2s[k][m], a contiguous row.  Same XCD grouping as the
-// rank-k update: the m-blocks of one column block n share an XCD.
-template <typename T, bool HAS_G2>
-__global__ __launch_bounds__(64) void known_dkfu_kernel(int64_t N, int M, int64_t nblk, int64_t mb,
-                                                        const T *__restrict__ Kt,
-                                                        const T *__restrict__ G1,
-                                                        const T *__restrict__ G2s,
-                                                        T *__restrict__ Et) {
-    using A = Mma<T>;
-    constexpr int TILE = A::TILE, KS = A::KS, BT = kEdge / TILE;
+// E^T[m][n] = (G1[n][m] + 2 sum_k G2s[m][k] Kt[k][n]) Kt[m][n], one workgroup
+// per kBlk x kBlk block (m, n) on the matrix cores.  G2s is symmetric, so its
+// A operand G2s[m][k] is read as G2s[k][m], a contiguous row.  Same XCD
+// grouping as the rank-k update: the m-blocks of one column block n share an XCD.
+template <typename T, bool HAS_G2, bool VEC>
+__global__ __launch_bounds__(256) void known_dkfu_kernel(int64_t N, int M, int64_t nblk, int64_t mb,
+                                                         const T *__restrict__ Kt,
+                                                         const T *__restrict__ G1,
+                                                         const T *__restrict__ G2s,
+                                                         T *__restrict__ Et) {
+    using MM = Mma<T>;
+    constexpr int TILE = MM::TILE, BT = 64 / TILE;
+    __shared__ __align__(16) T lds[4 * Slab<T>::SZ];
     const int64_t id = blockIdx.x, slot = id >> 3;
     const int64_t nbi = (slot / mb) * 8 + (id & 7);
     if (nbi >= nblk) return;
-    const int64_t n0 = nbi * kEdge;
-    const int m0 = (int)(slot % mb) * kEdge;
-    const int lane = threadIdx.x, li = lane % TILE, lk = lane / TILE;
-    typename A::acc_t acc[BT][BT];
-#pragma unroll
-    for (int ti = 0; ti < BT; ++ti)
-#pragma unroll
-        for (int tj = 0; tj < BT; ++tj)
-#pragma unroll
-            for (int v = 0; v < A::NACC; ++v) acc[ti][tj][v] = 0;
-    if (HAS_G2) {
-        for (int k = 0; k < M; k += KS * kUnroll) {
-            T a[kUnroll][BT], b[kUnroll][BT];
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int kr = k + u * KS + lk;
-                const bool ok = kr < M;
-#pragma unroll
-                for (int t = 0; t < BT; ++t) {
-                    const int m = m0 + t * TILE + li;
-                    const int64_t n = n0 + t * TILE + li;
-                    a[u][t] = (ok && m < M) ? G2s[(int64_t)kr * M + m] : T(0);
-                    b[u][t] = (ok && n < N) ? Kt[(int64_t)kr * N + n] : T(0);
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-#pragma unroll
-                for (int tm = 0; tm < BT; ++tm)
-#pragma unroll
-                    for (int tn = 0; tn < BT; ++tn)
-                        acc[tm][tn] = A::mma(a[u][tm], b[u][tn], acc[tm][tn]);
-        }
-    }
+    const int64_t n0 = nbi * kBlk;
+    const int64_t m0 = (slot % mb) * kBlk;
+    typename MM::acc_t acc[BT][BT];
+    block_product<T, VEC>(G2s, M, m0, M, Kt, N, n0, N, 0, HAS_G2 ? M : 0, false, lds, acc);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w & 1, wn = w >> 1;
 #pragma unroll
     for (int tm = 0; tm < BT; ++tm)
 #pragma unroll
         for (int tn = 0; tn < BT; ++tn)
 #pragma unroll
-            for (int v = 0; v < A::NACC; ++v) {
-                const int m = m0 + tm * TILE + A::row(v, lane);
-                const int64_t n = n0 + tn * TILE + li;
+            for (int v = 0; v < MM::NACC; ++v) {
+                const int64_t m = m0 + wm * 64 + tm * TILE + MM::row(v, lane);
+                const int64_t n = n0 + wn * 64 + tn * TILE + lane % TILE;
                 if (m < M && n < N) {
                     const T g1 = G1 ? G1[n * M + m] : T(0);
-                    const int64_t o = (int64_t)m * N + n;
+                    const int64_t o = m * N + n;
                     Et[o] = (g1 + T(2) * acc[tm][tn][v]) * Kt[o];
                 }
             }
@@ -414,39 +511,18 @@ __device__ inline T block_sum(T v, T *red4) {
     return ((red4[0] + red4[1]) + red4[2]) + red4[3];
 }
 
-// 16-byte vectors for LDS reads of the scaled-input tables.
-template <typename T>
-struct Vec;
-template <>
-struct Vec<float> {
-    typedef float t __attribute__((ext_vector_type(4)));
-    static constexpr int W = 4;
-};
-template <>
-struct Vec<double> {
-    typedef double t __attribute__((ext_vector_type(2)));
-    static constexpr int W = 2;
-};
-
-// acc[0..QM) += e * row[0..QM) for an LDS row that is zero beyond Q (no
-// per-dimension guard: a runtime bound inside the unrolled loop makes the
+// Chain-rule kernels.  Every difference xs_nq - zs_mq is formed before it is
+// weighted by E, so no large sums are subtracted afterwards: E is localised
+// around each z_m (and each x_n), so the expanded forms (sum_n E xs -
+// zs sum_n E and the like) would cancel to a small remainder and lose most of
+// their fp32 digits.  LDS rows are zero beyond Q, and so are the register
+// copies of the fixed point, so the padded dimensions contribute nothing (no
+// per-dimension guard: a runtime bound inside the unrolled loops makes the
 // compiler shuffle the accumulators).
-template <typename T, int QM>
-__device__ inline void axpy_row(T e, const T *row, T *acc) {
-    using V = typename Vec<T>::t;
-    constexpr int W = Vec<T>::W;
-    const V *r = reinterpret_cast<const V *>(row);
-#pragma unroll
-    for (int v = 0; v < QM / W; ++v) {
-        const V z = r[v];
-#pragma unroll
-        for (int w = 0; w < W; ++w) acc[v * W + w] = fma(e, z[w], acc[v * W + w]);
-    }
-}
 
-// One thread per datapoint: r_n and U_n (sums over m of E^T[m][n] and of
-// E^T[m][n] zs_m; coalesced over n, loads issued 16 at a time), dx_n, and
-// per-block partials of sum_n (r xs^2 - 2 xs U) (dl) and sum_n r (dsf2).
+// One thread per datapoint: dx_nq = -sum_m E^T[m][n] (xs_nq - zs_mq) / l_q
+// (coalesced over n, loads issued 16 at a time) and a per-block partial of
+// sum E (dsf2).
 template <typename T, int QM>
 __global__ __launch_bounds__(256) void known_rows_kernel(int64_t N, int M, int Q,
                                                          const T *__restrict__ Et,
@@ -454,14 +530,19 @@ __global__ __launch_bounds__(256) void known_rows_kernel(int64_t N, int M, int Q
                                                          const T *__restrict__ zs, Hyp<T> h,
                                                          T *__restrict__ dX,
                                                          T *__restrict__ rowpart) {
+    using V = typename Vec<T>::t;
+    constexpr int W = Vec<T>::W;
     __shared__ __align__(16) T sz[kEdge][QM];  // zero beyond Q and beyond the block's rows
     __shared__ T red4[4];
     const int tid = threadIdx.x;
     const int64_t n = (int64_t)blockIdx.x * 256 + tid;
     const bool valid = n < N;
-    T r = 0, U[QM];
+    T r = 0, U[QM], x[QM];
 #pragma unroll
-    for (int q = 0; q < QM; ++q) U[q] = 0;
+    for (int q = 0; q < QM; ++q) {
+        U[q] = 0;
+        x[q] = (valid && q < Q) ? xs[n * Q + q] : T(0);
+    }
     for (int mb = 0; mb < M; mb += kEdge) {
         const int cnt = min(kEdge, M - mb);
         __syncthreads();
@@ -479,35 +560,38 @@ __global__ __launch_bounds__(256) void known_rows_kernel(int64_t N, int M, int Q
 #pragma unroll
                 for (int j = 0; j < 16; ++j) {
                     r += e[j];
-                    axpy_row<T, QM>(e[j], &sz[c0 + j][0], U);
+                    const V *zr = reinterpret_cast<const V *>(&sz[c0 + j][0]);
+#pragma unroll
+                    for (int v = 0; v < QM / W; ++v) {
+                        const V z = zr[v];
+#pragma unroll
+                        for (int w = 0; w < W; ++w)
+                            U[v * W + w] = fma(e[j], x[v * W + w] - z[w], U[v * W + w]);
+                    }
                 }
             }
         }
     }
+    if (valid) {
 #pragma unroll
-    for (int q = 0; q <= QM; ++q) {
-        if (q < Q || q == QM) {
-            T v = 0;
-            if (q < Q) {
-                const T x = valid ? xs[n * Q + q] : T(0);
-                if (valid) dX[n * Q + q] = -(x * r - U[q]) / h.l[q];
-                v = valid ? r * x * x - T(2) * x * U[q] : T(0);
-            } else {
-                v = valid ? r : T(0);
-            }
-            const T s = block_sum(v, red4);
-            if (tid == 0) rowpart[blockIdx.x * (Q + 1) + (q < Q ? q : Q)] = s;
-        }
+        for (int q = 0; q < QM; ++q)
+            if (q < Q) dX[n * Q + q] = -U[q] / h.l[q];
     }
+    const T sr = block_sum(valid ? r : T(0), red4);
+    if (tid == 0) rowpart[blockIdx.x] = sr;
 }
 
-// One workgroup per (64 inducing inputs, row chunk): c_m and V_m over the
-// chunk from E^T tiles staged in LDS -> colpart[chunk][m][Q + 1] (V, then c).
+// One workgroup per (64 inducing inputs, row chunk), E^T tiles staged in LDS:
+// per inducing input m the chunk's sum_n E (xs_nq - zs_mq) (dZ) and
+// sum_n E (xs_nq - zs_mq)^2 (dl) -> colpart[chunk][m][2 Q].
 template <typename T, int QM>
 __global__ __launch_bounds__(256) void known_cols_kernel(int64_t N, int M, int Q, int64_t rows,
                                                          const T *__restrict__ Et,
                                                          const T *__restrict__ xs,
+                                                         const T *__restrict__ zs,
                                                          T *__restrict__ colpart) {
+    using Vv = typename Vec<T>::t;
+    constexpr int W = Vec<T>::W;
     __shared__ T se[kEdge][kEdge + 1];         // E^T tile [m][n], zero outside
     __shared__ __align__(16) T sx[kEdge][QM];  // xs rows of the tile, zero outside
     __shared__ T red[4][kEdge];
@@ -515,16 +599,20 @@ __global__ __launch_bounds__(256) void known_cols_kernel(int64_t N, int M, int Q
     const int m0 = blockIdx.x * kEdge;
     const int64_t r0 = (int64_t)blockIdx.y * rows, r1 = min(N, r0 + rows);
     const int mr = tid & 63, quarter = tid >> 6;
-    T c = 0, V[QM];
+    const int m = m0 + mr;
+    T V[QM], D[QM], z[QM];
 #pragma unroll
-    for (int q = 0; q < QM; ++q) V[q] = 0;
+    for (int q = 0; q < QM; ++q) {
+        V[q] = D[q] = 0;
+        z[q] = (m < M && q < Q) ? zs[(int64_t)m * Q + q] : T(0);
+    }
     for (int64_t nb = r0; nb < r1; nb += kEdge) {
         const int cnt = (int)min<int64_t>(kEdge, r1 - nb);
         __syncthreads();
         for (int i = tid; i < kEdge * kEdge; i += 256) {
             const int row = i >> 6, col = i & 63;
-            const int m = m0 + row;
-            se[row][col] = (m < M && col < cnt) ? Et[(int64_t)m * N + nb + col] : T(0);
+            const int mm = m0 + row;
+            se[row][col] = (mm < M && col < cnt) ? Et[(int64_t)mm * N + nb + col] : T(0);
         }
         for (int i = tid; i < kEdge * QM; i += 256) {
             const int rr = i / QM, q = i - rr * QM;
@@ -535,73 +623,82 @@ __global__ __launch_bounds__(256) void known_cols_kernel(int64_t N, int M, int Q
         for (int j = 0; j < 16; ++j) {
             const int col = quarter * 16 + j;
             const T e = se[mr][col];
-            c += e;
-            axpy_row<T, QM>(e, &sx[col][0], V);
+            const Vv *xr = reinterpret_cast<const Vv *>(&sx[col][0]);
+#pragma unroll
+            for (int v = 0; v < QM / W; ++v) {
+                const Vv xv = xr[v];
+#pragma unroll
+                for (int w = 0; w < W; ++w) {
+                    const int q = v * W + w;
+                    const T d = xv[w] - z[q];
+                    const T t = e * d;
+                    V[q] += t;
+                    D[q] = fma(t, d, D[q]);
+                }
+            }
         }
     }
-    const int m = m0 + mr;
 #pragma unroll
-    for (int q = 0; q <= QM; ++q) {
-        if (q < Q || q == QM) {
+    for (int k = 0; k < 2 * QM; ++k) {
+        const int q = k < QM ? k : k - QM;
+        if (q < Q) {
             __syncthreads();
-            red[quarter][mr] = q < Q ? V[q] : c;
+            red[quarter][mr] = k < QM ? V[q] : D[q];
             __syncthreads();
             if (quarter == 0 && m < M)
-                colpart[((int64_t)blockIdx.y * M + m) * (Q + 1) + (q < Q ? q : Q)] =
+                colpart[((int64_t)blockIdx.y * M + m) * (2 * Q) + (k < QM ? q : Q + q)] =
                     ((red[0][mr] + red[1][mr]) + red[2][mr]) + red[3][mr];
         }
     }
 }
 
 // One workgroup per inducing input m: Vc[m][k] = sum over the column chunks of
-// colpart[chunk][m][k], k <= Q.  G = 256 / (Q + 1) groups of Q + 1 threads take
+// colpart[chunk][m][k], k < 2 Q.  G = 256 / (2 Q) groups of 2 Q threads take
 // chunks g, g + G, ... (coalesced over k); the G partials are added in order.
 template <typename T>
 __global__ __launch_bounds__(256) void known_col_reduce_kernel(int M, int Q, int64_t cchunks,
                                                                const T *__restrict__ colpart,
                                                                T *__restrict__ Vc) {
     __shared__ T part[256];
-    const int t = threadIdx.x, Q1 = Q + 1, G = 256 / Q1;
+    const int t = threadIdx.x, K = 2 * Q, G = 256 / K;
     const int64_t m = blockIdx.x;
-    if (t < G * Q1) {
-        const int g = t / Q1, k = t - g * Q1;
+    if (t < G * K) {
+        const int g = t / K, k = t - g * K;
         T s = 0;
-        for (int64_t c = g; c < cchunks; c += G) s += colpart[(c * M + m) * Q1 + k];
+        for (int64_t c = g; c < cchunks; c += G) s += colpart[(c * M + m) * K + k];
         part[t] = s;
     }
     __syncthreads();
-    if (t < Q1) {
+    if (t < K) {
         T s = 0;
-        for (int g = 0; g < G; ++g) s += part[g * Q1 + t];
-        Vc[m * Q1 + t] = s;
+        for (int g = 0; g < G; ++g) s += part[g * K + t];
+        Vc[m * K + t] = s;
     }
 }
 
-// dZ[m][q] = (V_mq - zs_mq c_m) / l_q elementwise (blocks below zblocks), then
-// one workgroup per dl_q and one for dsf2, each a fixed-order block sum.
+// dZ[m][q] = Vc[m][q] / l_q elementwise (blocks below zblocks), then one
+// workgroup per dl_q (sum_m Vc[m][Q + q] / l_q) and one for dsf2 (sum E / sf2 +
+// N dL/dpsi0), each a fixed-order block sum.
 template <typename T>
 __global__ __launch_bounds__(256) void known_grad_final_kernel(
     int64_t N, int M, int Q, int64_t zblocks, int64_t rblocks, const T *__restrict__ Vc,
-    const T *__restrict__ rowpart, const T *__restrict__ zs, Hyp<T> h, T dL_dpsi0,
-    T *__restrict__ dZ, T *__restrict__ dsf2, T *__restrict__ dl, int accumulate) {
+    const T *__restrict__ rowpart, Hyp<T> h, T dL_dpsi0, T *__restrict__ dZ, T *__restrict__ dsf2,
+    T *__restrict__ dl, int accumulate) {
     __shared__ T red4[4];
-    const int64_t Q1 = Q + 1;
+    const int64_t K = 2 * Q;
     if ((int64_t)blockIdx.x < zblocks) {
         const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
         if (i >= (int64_t)M * Q) return;
         const int64_t m = i / Q, q = i - m * Q;
-        const T v = (Vc[m * Q1 + q] - zs[i] * Vc[m * Q1 + Q]) / h.l[q];
-        dZ[i] = (accumulate ? dZ[i] : T(0)) + v;
+        dZ[i] = (accumulate ? dZ[i] : T(0)) + Vc[m * K + q] / h.l[q];
         return;
     }
     const int k = (int)(blockIdx.x - zblocks);  // k < Q: dl_k; k == Q: dsf2
     T s = 0;
-    for (int64_t b = threadIdx.x; b < rblocks; b += 256) s += rowpart[b * Q1 + k];
     if (k < Q)
-        for (int m = threadIdx.x; m < M; m += 256) {
-            const T z = zs[(int64_t)m * Q + k];
-            s += Vc[(int64_t)m * Q1 + Q] * z * z;
-        }
+        for (int m = threadIdx.x; m < M; m += 256) s += Vc[(int64_t)m * K + Q + k];
+    else
+        for (int64_t b = threadIdx.x; b < rblocks; b += 256) s += rowpart[b];
     s = block_sum(s, red4);
     if (threadIdx.x == 0) {
         if (k < Q) dl[k] = (accumulate ? dl[k] : T(0)) + s / h.l[k];
@@ -637,7 +734,7 @@ void launch_chain(const Shape &s, const KPlan &p, const T *Et, const Hyp<T> &h, 
     }
     TimedScope ts(st, "known_cols");
     known_cols_kernel<T, QM><<<dim3((unsigned)p.nb, (unsigned)p.cchunks), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, p.crows, Et, xs, at<T>(ws, p.off_colp));
+        s.N, (int)s.M, (int)s.Q, p.crows, Et, xs, zs, at<T>(ws, p.off_colp));
 }
 
 }  // namespace
@@ -653,8 +750,13 @@ hipError_t known_psi_stats(const Shape &s, const T *X, const T *Z, const Hyp<T> 
     T *part = at<T>(ws, p.off_part);
     {
         TimedScope ts(st, "known_syrk");
-        known_syrk_kernel<T><<<(unsigned)p.grid_syrk, 64, 0, st>>>(s.N, (int)s.M, p.rows, p.chunks,
-                                                                  p.nb, p.ntp, p.ntu, K, part);
+        // 16-byte loads need rows that start on 16 bytes
+        if (s.M % Vec<T>::W == 0 && reinterpret_cast<uintptr_t>(K) % 16 == 0)
+            known_syrk_kernel<T, true><<<(unsigned)p.grid_syrk, 256, 0, st>>>(
+                s.N, (int)s.M, p.rows, p.chunks, p.nb2, p.ntp, p.ntu, K, part);
+        else
+            known_syrk_kernel<T, false><<<(unsigned)p.grid_syrk, 256, 0, st>>>(
+                s.N, (int)s.M, p.rows, p.chunks, p.nb2, p.ntp, p.ntu, K, part);
     }
     const int64_t elems = p.ntu * p.tile * p.tile;
     TimedScope ts(st, "known_syrk_reduce");
@@ -670,8 +772,9 @@ hipError_t known_psi_grads(const Shape &s, const T *X, const T *Z, const Hyp<T> 
     const KPlan p = make_kplan(s, sizeof(T));
     T *Kt = at<T>(ws, p.off_k), *Et = at<T>(ws, p.off_e);
     launch_centre_kfu<T>(s, p, X, Z, h, true, Kt, ws, st);
-    const int64_t nblk = cdiv(s.N, kEdge), mb = p.nb;
+    const int64_t nblk = cdiv(s.N, kBlk), mb = p.nb2;
     const unsigned grid = (unsigned)(round_up(nblk, 8) * mb);
+    const bool vec = s.M % Vec<T>::W == 0 && s.N % Vec<T>::W == 0;  // workspace rows start on 16 bytes
     if (G2) {
         T *G2s = at<T>(ws, p.off_g2s);
         {
@@ -679,15 +782,24 @@ hipError_t known_psi_grads(const Shape &s, const T *X, const T *Z, const Hyp<T> 
             known_sym_kernel<T><<<(unsigned)cdiv(s.M * s.M, 256), 256, 0, st>>>((int)s.M, G2, G2s);
         }
         TimedScope ts(st, "known_dkfu");
-        known_dkfu_kernel<T, true><<<grid, 64, 0, st>>>(s.N, (int)s.M, nblk, mb, Kt, G1, G2s, Et);
+        if (vec)
+            known_dkfu_kernel<T, true, true><<<grid, 256, 0, st>>>(s.N, (int)s.M, nblk, mb, Kt, G1, G2s, Et);
+        else
+            known_dkfu_kernel<T, true, false><<<grid, 256, 0, st>>>(s.N, (int)s.M, nblk, mb, Kt, G1, G2s, Et);
     } else {
         TimedScope ts(st, "known_dkfu");
-        known_dkfu_kernel<T, false><<<grid, 64, 0, st>>>(s.N, (int)s.M, nblk, mb, Kt, G1, nullptr, Et);
+        known_dkfu_kernel<T, false, false><<<grid, 256, 0, st>>>(s.N, (int)s.M, nblk, mb, Kt, G1, nullptr,
+                                                                 Et);
     }
+    // the chain kernels pad Q to QM (a multiple of the 16-byte vector)
     if (s.Q <= 4) launch_chain<T, 4>(s, p, Et, h, dX, ws, st);
     else if (s.Q <= 8) launch_chain<T, 8>(s, p, Et, h, dX, ws, st);
+    else if (s.Q <= 12) launch_chain<T, 12>(s, p, Et, h, dX, ws, st);
     else if (s.Q <= 16) launch_chain<T, 16>(s, p, Et, h, dX, ws, st);
+    else if (s.Q <= 20) launch_chain<T, 20>(s, p, Et, h, dX, ws, st);
+    else if (s.Q <= 24) launch_chain<T, 24>(s, p, Et, h, dX, ws, st);
     else if (s.Q <= 32) launch_chain<T, 32>(s, p, Et, h, dX, ws, st);
+    else if (s.Q <= 48) launch_chain<T, 48>(s, p, Et, h, dX, ws, st);
     else launch_chain<T, 64>(s, p, Et, h, dX, ws, st);
     TimedScope ts(st, "known_grad_reduce");
     T *Vc = at<T>(ws, p.off_vc);
@@ -695,8 +807,8 @@ hipError_t known_psi_grads(const Shape &s, const T *X, const T *Z, const Hyp<T> 
                                                              at<T>(ws, p.off_colp), Vc);
     const int64_t zblocks = cdiv(s.M * s.Q, 256);
     known_grad_final_kernel<T><<<(unsigned)(zblocks + s.Q + 1), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, zblocks, p.rblocks, Vc, at<T>(ws, p.off_rowp), at<T>(ws, p.off_zs),
-        h, dL_dpsi0, dZ, dsf2, dl, accumulate);
+        s.N, (int)s.M, (int)s.Q, zblocks, p.rblocks, Vc, at<T>(ws, p.off_rowp), h, dL_dpsi0, dZ,
+        dsf2, dl, accumulate);
     return hipGetLastError();
 }
 

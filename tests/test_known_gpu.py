@@ -306,12 +306,39 @@ def _grid_problem():
                 jitter=1e-3)
 
 
+def fp32_stats_spread(p, trials=3):
+    """Per output, the largest relative change of the oracle's result when Psi1
+    and Psi2 carry independent relative errors of a few fp32 units (uniform in
+    +-2^-24 and +-2^-22): how much an output moves for errors an fp32 path
+    cannot avoid in its stored statistics."""
+    q = {k: (np.asarray(v, np.float32).astype(np.float64) if isinstance(v, np.ndarray) else v)
+         for k, v in p.items()}
+    args = (q["X"], None, q["Z"], q["Y"], q["sigma_f2"], q["l"], q["beta"], q["jitter"])
+    X = q["X"]
+    psi0, P1, P2 = oracle.psi_stats(X, np.zeros_like(X), q["Z"], q["sigma_f2"], q["l"])
+    P1 = np.asarray(P1).reshape(X.shape[0], -1)
+    ref = ob.grads(*args, stats=(psi0, P1, P2))
+    rng = np.random.default_rng(0)
+    spread = {k: 0.0 for k in ("L",) + BKEYS}
+    for _ in range(trials):
+        E2 = rng.uniform(-1, 1, P2.shape) * 2.0 ** -22
+        alt = ob.grads(*args, stats=(psi0, P1 * (1 + rng.uniform(-1, 1, P1.shape) * 2.0 ** -24),
+                                     P2 * (1 + (E2 + E2.T) / 2)))
+        for k in spread:
+            a, r = np.asarray(alt[k], np.float64), np.asarray(ref[k], np.float64)
+            spread[k] = max(spread[k], rel(a, r))
+    return spread
+
+
 @pytest.mark.parametrize("case", ["random16", "grid25"])
 def test_regression_bound_f32_matches_oracle(case):
-    """fp32 rounding of Psi2 and of the GEMM operands is amplified in the bound by
-    the conditioning of A = Kmm + beta Psi2 (dL/dPsi2 holds Kmm^-1 and A^-1,
-    whose entries grow with it, and dL/dKfu = G1 + 2 Kfu G2s cancels them), so
-    the fp32 cases keep cond(A) <= 1e4 (checked)."""
+    """The fp32 path stores Psi1 and Psi2 in fp32; the bound's M x M algebra
+    (fp64) amplifies their rounding by the conditioning of A = Kmm + beta Psi2,
+    and dZ (a difference of its contributions through Kfu and through Kmm) most
+    of all.  Tolerance per output: max(1e-4, 10 x the oracle's own spread under
+    errors of a few fp32 units in Psi1 and Psi2).  The cases keep cond(A) <=
+    1e4 (checked): random16 is the harder one (dZ spread ~1e-4), grid25 a
+    well-spread design (every spread below 1e-5)."""
     p = regression_problem(5000, 16, 2, 3, seed=7, jitter=1e-3) if case == "random16" \
         else _grid_problem()
     _, _, pc = ob.bound_terms(p["X"], None, p["Z"], p["Y"], p["sigma_f2"], p["l"], p["beta"],
@@ -319,12 +346,17 @@ def test_regression_bound_f32_matches_oracle(case):
     cond = np.linalg.cond(pc["Kmm"] + p["beta"] * pc["Psi2"])
     say(f"  regression f32 {case}: cond(A) {cond:.1e}")
     assert cond <= 1e4
+    spread = fp32_stats_spread(p)
     got, ref = run_bound(p, torch.float32), oracle_bound(p, True)
     e = abs(got["L"][0] - ref["L"]) / abs(ref["L"])
-    say(f"  regression f32 {case} L: rel {e:.2e}")
-    assert e <= 1e-4
+    tol = max(1e-4, 10 * spread["L"])
+    say(f"  regression f32 {case} L: rel {e:.2e} (tol {tol:.1e})")
+    assert e <= tol
     for k in BKEYS:
         r = np.asarray(ref[k])
         e = rel(got[k].reshape(r.shape), r)
-        say(f"  regression f32 {case} {k}: rel {e:.2e}")
-        assert e <= 1e-4, k
+        tol = max(1e-4, 10 * spread[k])
+        say(f"  regression f32 {case} {k}: rel {e:.2e} (tol {tol:.1e})")
+        assert e <= tol, k
+    if case == "grid25":
+        assert max(spread.values()) <= 1e-5

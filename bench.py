@@ -229,6 +229,20 @@ def bench_gplvm(args):
     print(json.dumps(rec), flush=True)
 
 
+def copy_probe(args, dev):
+    """A plain device copy of args.copy_probe_mib MiB, three times (counter calibration)."""
+    import torch
+    if args.copy_probe_mib <= 0:
+        return
+    n_el = args.copy_probe_mib * (1 << 20) // 4
+    src = torch.ones(n_el, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def bench_known(args):
     """One step = gpps_psi_stats + gpps_psi_grads with S = NULL (known inputs) at
     the large workload's shape."""
@@ -268,6 +282,7 @@ def bench_known(args):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    copy_probe(args, dev)
     L = gpps.lib()
     L.gpps_timing_enable.argtypes = [ctypes.c_int]
     L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
@@ -377,14 +392,7 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    if args.copy_probe_mib > 0:
-        n_el = args.copy_probe_mib * (1 << 20) // 4
-        src = torch.ones(n_el, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            torch.neg(src, out=dst)
-        torch.cuda.synchronize()
-        del src, dst
+    copy_probe(args, dev)
     L = gpps.lib()
     L.gpps_timing_enable.argtypes = [ctypes.c_int]
     L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,

@@ -19,6 +19,12 @@
  *     contiguous, aligned to their element size, and live in device memory
  *     of the current HIP device.
  *   - mu and S are N x Q (S holds the diagonal VARIANCES), Z is M x Q.
+ *   - S = NULL means known inputs: every variance is zero and mu holds the
+ *     inputs X themselves, the sparse GP regression case of section 2,
+ *     eq. (boundF).  The statistics are then the plain kernel quantities
+ *     (psi0 = N sigma_f2, Psi1 = Kfu, Psi2 = Kfu^T Kfu) and run on a separate
+ *     matrix-core GEMM path (both dtypes) whatever gpps_set_path selected;
+ *     dmu is dL/dX and dS may be NULL (it is not written).
  *   - sigma_f2 and l (Q values) are HOST doubles, so validation needs no
  *     device synchronisation.  In the F32 path they are rounded to float.
  *   - The caller owns every buffer.  The library allocates nothing, frees
@@ -67,9 +73,10 @@ typedef enum {
     GPPS_ERR_PATH = 8       /* unknown path, or the requested path cannot run this call */
 } gpps_status;
 
-/* Kernel path used by gpps_psi_stats / gpps_psi_grads.  AUTO picks the fastest
- * path that supports the call (the matrix-core path for F32 when M >= 2 and
- * Q <= GPPS_MAX_Q_MFMA, the generic vector path otherwise). */
+/* Kernel path used by gpps_psi_stats / gpps_psi_grads for calls with S != NULL.
+ * AUTO picks the fastest path that supports the call (the matrix-core path for
+ * F32 when M >= 2 and Q <= GPPS_MAX_Q_MFMA, the generic vector path otherwise).
+ * Calls with S = NULL always take the known-input path. */
 typedef enum { GPPS_PATH_AUTO = 0, GPPS_PATH_GENERIC = 1, GPPS_PATH_MFMA = 2 } gpps_path;
 
 #define GPPS_MAX_Q 64
@@ -87,6 +94,7 @@ size_t gpps_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q);
  * q(X)); Alg. 1 (Psi_nm per datapoint and inducing input, Phi summed over
  * datapoints for every pair of inducing inputs).
  *
+ *   S              device N x Q, or NULL for known inputs (see above).
  *   psi0  [1]      device.  += or = N * sigma_f2
  *   Psi1  [N x M]  device, may be NULL (not computed).  Always overwritten.
  *   Psi2  [M x M]  device.  Full symmetric matrix; both triangles are bitwise
@@ -110,7 +118,7 @@ gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
  *   dL_dPsi1 [N x M]    device, or NULL for zero.
  *   dL_dPsi2 [M x M]    device, or NULL for zero.  Need not be symmetric: only its
  *                       symmetric part affects L, since Psi2 is symmetric.
- *   dmu, dS  [N x Q]    device, always overwritten.
+ *   dmu, dS  [N x Q]    device, always overwritten (dS may be NULL when S is NULL).
  *   dZ       [M x Q]    device, += or = according to `accumulate`.
  *   dsigma_f2 [1]       device, += or =.
  *   dl       [Q]        device, += or =.
@@ -151,6 +159,9 @@ size_t gpps_bound_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q
  *   dmu, dS  [N x Q], dZ [M x Q], dsigma_f2 [1], dl [Q], dbeta [1]: device, overwritten.
  *   workspace          at least gpps_bound_workspace_bytes(dt, N, M, Q, D) bytes,
  *                      256-byte aligned, caller-owned (contents ignored).
+ *
+ * S = NULL (known inputs) gives the sparse GP regression bound of eq. (boundF)
+ * itself: no KL term, dmu = dL/dX, and dS may be NULL.
  *
  * Errors as for gpps_psi_grads, plus GPPS_ERR_SHAPE for D < 1, D > GPPS_MAX_D or
  * M > GPPS_MAX_M_BOUND (the triangular inverse keeps a block column in LDS), and GPPS_ERR_HYPER

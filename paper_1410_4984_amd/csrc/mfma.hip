@@ -283,57 +283,73 @@ MPlan make_mplan(const Shape &s) {
 float *fat(void *ws, size_t off) { return reinterpret_cast<float *>(static_cast<char *>(ws) + off); }
 
 // ---------------------------------------------------------------- small kernels
-// One wave per datapoint, one lane per latent dimension:
+// Per-row tables, 64 datapoints per workgroup.  For every (n, q):
 //   K[n][q]  = log2e S / (l^2 (l^2 + 2S))  (zero for q >= Q up to the stride)
 //   hq[n][q] = -log2e/4 (1/l^2 + w2),  w2[n][q] = 1/(l^2 + 2S),  w1[n][q] = 1/(l^2 + S)
+// (one pass over the workgroup's (row, dimension) pairs, coalesced), then per row
 //   hl[n]    = log2e (log sf2 - 1/4 sum_q log(1 + 2S/l^2))   (Psi2 prefactor, half of it)
 //   l1[n]    = log2e (log sf2 - 1/2 sum_q log(1 + S/l^2))    (Psi1 prefactor)
-// The sums over q use a fixed butterfly, so they are deterministic.
+// with the sums over q taken in order from LDS.
+constexpr int kRowsPerBlock = 64;
 __global__ __launch_bounds__(256) void mfma_rows_kernel(
     int64_t N, int Q, const float *__restrict__ S, Hyp<float> h, float *__restrict__ Kt,
     float *__restrict__ hq, float *__restrict__ w2t, float *__restrict__ hl,
     float *__restrict__ w1t, float *__restrict__ l1) {
-    const int q = threadIdx.x & 63;
-    const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (n >= N) return;                        // wave-uniform
-    float a2 = 0.f, a1 = 0.f;
-    if (q < Q) {
-        const float s = S[n * Q + q];
+    __shared__ float la2[kRowsPerBlock][GPPS_MAX_Q + 1], la1[kRowsPerBlock][GPPS_MAX_Q + 1];
+    const int64_t n0 = (int64_t)blockIdx.x * kRowsPerBlock;
+    const int rows = (int)min<int64_t>(kRowsPerBlock, N - n0);
+    for (int i = threadIdx.x; i < rows * Q; i += 256) {
+        const int r = i / Q, q = i - r * Q;
+        const int64_t k = n0 * Q + i;  // = (n0 + r) * Q + q
+        const float sv = S[k];
         const float l2 = h.l2[q];
-        const float w2 = 1.f / (l2 + 2.f * s);
-        Kt[n * kRowStride + q] = kLog2e * s * w2 / l2;
-        hq[n * Q + q] = -0.25f * kLog2e * (1.f / l2 + w2);
-        w2t[n * Q + q] = w2;
-        w1t[n * Q + q] = 1.f / (l2 + s);
-        a2 = log1pf(2.f * s / l2);
-        a1 = log1pf(s / l2);
-    } else {
-        Kt[n * kRowStride + q] = 0.f;
+        const float w2 = 1.f / (l2 + 2.f * sv);
+        Kt[(n0 + r) * kRowStride + q] = kLog2e * sv * w2 / l2;
+        hq[k] = -0.25f * kLog2e * (1.f / l2 + w2);
+        w2t[k] = w2;
+        w1t[k] = 1.f / (l2 + sv);
+        la2[r][q] = log1pf(2.f * sv / l2);
+        la1[r][q] = log1pf(sv / l2);
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        a2 += __shfl_xor(a2, off);
-        a1 += __shfl_xor(a1, off);
+    const int pad = kRowStride - Q;
+    for (int i = threadIdx.x; i < rows * pad; i += 256) {
+        const int r = i / pad, q = Q + (i - r * pad);
+        Kt[(n0 + r) * kRowStride + q] = 0.f;
     }
-    if (q == 0) {
-        hl[n] = kLog2e * (h.log_sf2 - 0.25f * a2);
-        l1[n] = kLog2e * (h.log_sf2 - 0.5f * a1);
+    __syncthreads();
+    const int r = threadIdx.x;
+    if (r < rows) {
+        float a2 = 0.f, a1 = 0.f;
+        for (int q = 0; q < Q; ++q) {
+            a2 += la2[r][q];
+            a1 += la1[r][q];
+        }
+        hl[n0 + r] = kLog2e * (h.log_sf2 - 0.25f * a2);
+        l1[n0 + r] = kLog2e * (h.log_sf2 - 0.5f * a1);
     }
 }
 
-// Mean inducing input per dimension: the centring shift.  Column sums in a
-// fixed order (per-thread partials over strided rows, then a fixed tree).
+// Mean inducing input per dimension: the centring shift.  G = 256 / Q groups
+// of Q threads sum rows m = g, g + G, ... (coalesced), then the G partial sums
+// of each dimension are added in group order.
 __global__ __launch_bounds__(256) void mfma_centre_kernel(int M, int Q,
                                                           const float *__restrict__ Z,
                                                           float *__restrict__ zc) {
-    __shared__ float part[4][64];
-    const int q = threadIdx.x & 63, w = threadIdx.x >> 6;
-    float s = 0.f;
-    if (q < Q)
-        for (int m = w; m < M; m += 4) s += Z[(int64_t)m * Q + q];
-    part[w][q] = s;
+    __shared__ float part[256];
+    const int t = threadIdx.x, G = 256 / Q;
+    if (t < G * Q) {
+        const int g = t / Q, q = t - g * Q;
+        float s = 0.f;
+#pragma unroll 8
+        for (int m = g; m < M; m += G) s += Z[(int64_t)m * Q + q];
+        part[t] = s;
+    }
     __syncthreads();
-    if (w == 0 && q < Q) zc[q] = ((part[0][q] + part[1][q]) + (part[2][q] + part[3][q])) / (float)M;
+    if (t < Q) {
+        float s = 0.f;
+        for (int g = 0; g < G; ++g) s += part[g * Q + t];
+        zc[t] = s / (float)M;
+    }
 }
 
 // Symmetric part of dL/dPsi2, zero-padded to Mp x Mp (all zero when G2 is NULL).
@@ -352,7 +368,9 @@ __global__ void mfma_sym_kernel(int M, int Mp, const float *__restrict__ G2,
 // (kPadBias in both row-term tables for m >= M).  The forward writes Psi1
 // (NULL: skipped); the gradient writes t1[n][m] = dL/dPsi1[n][m] * Psi1 with
 // row stride Mp (zero where G1 is NULL or m >= M).  One thread per inducing
-// input (z in registers), rows staged in LDS.
+// input (z in registers); rows staged in LDS as one (mu, hq, w1, K mu) vector
+// per dimension, so each dimension costs one broadcast read and five vector
+// instructions.
 template <int QM>
 __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     int64_t N, int M, int Q, int Mp, const float *__restrict__ mu, const float *__restrict__ Z,
@@ -360,7 +378,8 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     const float *__restrict__ hl, const float *__restrict__ w1t, const float *__restrict__ l1,
     const float *__restrict__ G1, float *__restrict__ bt, float *__restrict__ bc,
     float *__restrict__ psi1, float *__restrict__ t1) {
-    __shared__ float s_mu[kRTRows][QM], s_hq[kRTRows][QM], s_w1[kRTRows][QM], s_k[kRTRows][QM];
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    __shared__ v4f s_row[kRTRows][QM];
     __shared__ float s_hl[kRTRows], s_l1[kRTRows];
     const int m = blockIdx.y * 256 + threadIdx.x;
     const int64_t n0 = (int64_t)blockIdx.x * kRTRows;
@@ -369,10 +388,13 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
         const int r = i / QM, q = i - r * QM;
         const bool ok = r < cnt && q < Q;
         const int64_t n = n0 + r;
-        s_mu[r][q] = ok ? mu[n * Q + q] - zc[q] : 0.f;
-        s_hq[r][q] = ok ? hq[n * Q + q] : 0.f;
-        s_w1[r][q] = ok ? w1t[n * Q + q] : 0.f;
-        s_k[r][q] = ok ? Kt[n * kRowStride + q] : 0.f;
+        const float x = ok ? mu[n * Q + q] - zc[q] : 0.f;
+        v4f v;
+        v.x = x;
+        v.y = ok ? hq[n * Q + q] : 0.f;
+        v.z = ok ? w1t[n * Q + q] : 0.f;
+        v.w = ok ? Kt[n * kRowStride + q] * x : 0.f;
+        s_row[r][q] = v;
     }
     for (int r = threadIdx.x; r < kRTRows; r += 256) {
         s_hl[r] = r < cnt ? hl[n0 + r] : 0.f;
@@ -388,10 +410,12 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
         float b = s_hl[r], cc = 0.f, e = 0.f;
 #pragma unroll
         for (int q = 0; q < QM; ++q) {
-            const float d = s_mu[r][q] - z[q];
-            b = fmaf(s_hq[r][q] * d, d, b);
-            cc = fmaf(s_k[r][q] * d, s_mu[r][q], cc);
-            e = fmaf(s_w1[r][q] * d, d, e);
+            const v4f v = s_row[r][q];
+            const float d = v.x - z[q];
+            const float d2 = d * d;
+            b = fmaf(v.y, d2, b);
+            e = fmaf(v.z, d2, e);
+            cc = fmaf(v.w, d, cc);
         }
         const int64_t n = n0 + r;
         bt[n * Mp + m] = real ? b : kPadBias;
@@ -402,13 +426,21 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     }
 }
 
-// max |G2s| over the padded symmetric dL/dPsi2 (one workgroup; max is
-// order-independent, so the result is deterministic).
+// max |G2s| over the padded symmetric dL/dPsi2 (one workgroup, loads issued 8
+// at a time; max is order-independent, so the result is deterministic).
 __global__ __launch_bounds__(1024) void mfma_absmax_kernel(int64_t n, const float *__restrict__ G2p,
                                                            float *__restrict__ gmax) {
     __shared__ float part[16];
     float m = 0.f;
-    for (int64_t i = threadIdx.x; i < n; i += 1024) m = fmaxf(m, fabsf(G2p[i]));
+    int64_t i = threadIdx.x;
+    for (; i + 7 * 1024 < n; i += 8 * 1024) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = G2p[i + j * 1024];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(v[j]));
+    }
+    for (; i < n; i += 1024) m = fmaxf(m, fabsf(G2p[i]));
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
     if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
@@ -638,22 +670,37 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
 }
 
 // Fixed-order sum over chunks; both triangles written from the same value.
-__global__ void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T, int64_t chunks,
-                                   const float *__restrict__ partial, float sf2,
-                                   float *__restrict__ psi0, float *__restrict__ Psi2,
-                                   int accumulate) {
-    const int mp = blockIdx.x * 16 + (threadIdx.x & 15);
-    const int m = blockIdx.y * 16 + (threadIdx.x >> 4);
-    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
-        psi0[0] = (accumulate ? psi0[0] : 0.f) + (float)N * sf2;
-    if (m >= M || mp >= M || m > mp) return;
-    const int64_t off = tile_index(m / kTile, mp / kTile, nb) * (kTile * kTile) +
-                        (mp % kTile) * kTile + (m % kTile);
+// One workgroup per (upper tile, 32 consecutive partial entries): 8 groups of
+// 32 threads take chunks g, g + 8, ... (one 128-byte segment per group), the
+// 8 group sums are added in order.  Entry e of a tile is (m' mod 32) * 32 +
+// (m mod 32).
+__global__ __launch_bounds__(256) void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T,
+                                                          int64_t chunks,
+                                                          const float *__restrict__ partial,
+                                                          float sf2, float *__restrict__ psi0,
+                                                          float *__restrict__ Psi2, int accumulate) {
+    __shared__ float red[256];
+    const int t = threadIdx.x, o = t & 31, g = t >> 5;
+    const int64_t tile = blockIdx.x >> 5;
+    const int eb = blockIdx.x & 31;
+    if (blockIdx.x == 0 && t == 0) psi0[0] = (accumulate ? psi0[0] : 0.f) + (float)N * sf2;
+    const float *src = partial + tile * (kTile * kTile) + eb * kTile + o;
     const int64_t stride = T * (kTile * kTile);
     float s = 0.f;
 #pragma unroll 8
-    for (int64_t ch = 0; ch < chunks; ++ch) s += partial[ch * stride + off];
-    const float v = (accumulate ? Psi2[(int64_t)m * M + mp] : 0.f) + s;
+    for (int64_t ch = g; ch < chunks; ch += 8) s += src[ch * stride];
+    red[t] = s;
+    __syncthreads();
+    if (g != 0) return;
+    int ti = 0;
+    int64_t rem = tile;
+    while (rem >= nb - ti) { rem -= nb - ti; ++ti; }
+    const int tj = ti + (int)rem;
+    const int m = ti * kTile + o, mp = tj * kTile + eb;
+    if (m >= M || mp >= M || m > mp) return;
+    float v = 0.f;
+    for (int k = 0; k < 8; ++k) v += red[k * 32 + o];
+    v += accumulate ? Psi2[(int64_t)m * M + mp] : 0.f;
     Psi2[(int64_t)m * M + mp] = v;
     Psi2[(int64_t)mp * M + m] = v;
 }
@@ -1011,29 +1058,54 @@ __global__ __launch_bounds__(256) void psi2_finalize_kernel(
 }
 
 // dZ, dl, dsf2 from the per-slab and per-block partials, fixed order.
-__global__ void grad_reduce_kernel(int64_t N, int M, int Q, const float *__restrict__ pdz,
-                                   int64_t dz_slabs, const float *__restrict__ pdl,
-                                   int64_t dl_parts, float dL_dpsi0, float *__restrict__ dZ,
-                                   float *__restrict__ dsf2, float *__restrict__ dl,
-                                   int accumulate) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// Workgroups below zblocks: 32 dZ entries each, 8 groups of 32 threads taking
+// slabs g, g + 8, ... (two coalesced 128-byte segments per wave), the 8 group
+// sums added in order.  Then one workgroup per dl_q and one for dsf2: thread t
+// takes blocks t, t + 256, ..., then a fixed tree.
+constexpr int kRedOut = 32, kRedGroups = 8;
+__global__ __launch_bounds__(256) void grad_reduce_kernel(int64_t N, int M, int Q, int64_t zblocks,
+                                                          const float *__restrict__ pdz,
+                                                          int64_t dz_slabs, const float *__restrict__ pdl,
+                                                          int64_t dl_parts, float dL_dpsi0,
+                                                          float *__restrict__ dZ,
+                                                          float *__restrict__ dsf2,
+                                                          float *__restrict__ dl, int accumulate) {
+    __shared__ float red[256];
+    const int t = threadIdx.x;
     const int64_t MQ = (int64_t)M * Q;
-    if (i < MQ) {
+    if ((int64_t)blockIdx.x < zblocks) {
+        const int o = t % kRedOut, g = t / kRedOut;
+        const int64_t i = (int64_t)blockIdx.x * kRedOut + o;
         float s = 0.f;
+        if (i < MQ) {
 #pragma unroll 8
-        for (int64_t sl = 0; sl < dz_slabs; ++sl) s += pdz[sl * MQ + i];
-        dZ[i] = (accumulate ? dZ[i] : 0.f) + s;
-    } else if (i < MQ + Q + 1) {
-        const int k = (int)(i - MQ);
-        float s = 0.f;
-#pragma unroll 8
-        for (int64_t b = 0; b < dl_parts; ++b) s += pdl[b * (Q + 1) + k];
-        if (k < Q) {
-            dl[k] = (accumulate ? dl[k] : 0.f) + s;
-        } else {
-            s += dL_dpsi0 * (float)N;
-            dsf2[0] = (accumulate ? dsf2[0] : 0.f) + s;
+            for (int64_t sl = g; sl < dz_slabs; sl += kRedGroups) s += pdz[sl * MQ + i];
         }
+        red[t] = s;
+        __syncthreads();
+        if (g == 0 && i < MQ) {
+            float v = 0.f;
+            for (int k = 0; k < kRedGroups; ++k) v += red[k * kRedOut + o];
+            dZ[i] = (accumulate ? dZ[i] : 0.f) + v;
+        }
+        return;
+    }
+    const int k = (int)(blockIdx.x - zblocks);  // k < Q: dl_k; k == Q: dsf2
+    float s = 0.f;
+    for (int64_t b = t; b < dl_parts; b += 256) s += pdl[b * (Q + 1) + k];
+    red[t] = s;
+    __syncthreads();
+    for (int w = 128; w >= 1; w >>= 1) {
+        if (t < w) red[t] += red[t + w];
+        __syncthreads();
+    }
+    if (t != 0) return;
+    s = red[0];
+    if (k < Q) {
+        dl[k] = (accumulate ? dl[k] : 0.f) + s;
+    } else {
+        s += dL_dpsi0 * (float)N;
+        dsf2[0] = (accumulate ? dsf2[0] : 0.f) + s;
     }
 }
 
@@ -1099,7 +1171,7 @@ void prepare(const MPlan &p, const Shape &s, const float *mu, const float *S, co
              hipStream_t st) {
     {
         TimedScope ts(st, "mfma_rows");
-        mfma_rows_kernel<<<(unsigned)cdiv(s.N, 4), 256, 0, st>>>(
+        mfma_rows_kernel<<<(unsigned)cdiv(s.N, kRowsPerBlock), 256, 0, st>>>(
             s.N, (int)s.Q, S, h, fat(ws, p.off_K), fat(ws, p.off_hq), fat(ws, p.off_w2),
             fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1));
     }
@@ -1116,9 +1188,12 @@ void prepare(const MPlan &p, const Shape &s, const float *mu, const float *S, co
         fat(ws, p.off_hq), fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1), G1,       \
         fat(ws, p.off_bt), fat(ws, p.off_bc), psi1, t1)
     if (s.Q <= 8) GPPS_RT(8);
+    else if (s.Q <= 12) GPPS_RT(12);
     else if (s.Q <= 16) GPPS_RT(16);
+    else if (s.Q <= 20) GPPS_RT(20);
     else if (s.Q <= 24) GPPS_RT(24);
     else if (s.Q <= 32) GPPS_RT(32);
+    else if (s.Q <= 48) GPPS_RT(48);
     else GPPS_RT(64);
 #undef GPPS_RT
 }
@@ -1141,10 +1216,10 @@ hipError_t mfma_psi_stats(const Shape &s, const float *mu, const float *S, const
     prepare(p, s, mu, S, Z, h, nullptr, Psi1, false, ws, st);
     hipError_t e = dispatch_fwd(p, s, mu, Z, ws, st);
     if (e != hipSuccess) return e;
-    dim3 g((unsigned)cdiv(s.M, 16), (unsigned)cdiv(s.M, 16));
     TimedScope ts(st, "mfma_psi2_reduce");
-    psi2_reduce_kernel<<<g, 256, 0, st>>>(s.N, (int)s.M, p.nb, p.T, p.fchunks, fat(ws, p.off_fp),
-                                          h.sf2, psi0, Psi2, accumulate);
+    psi2_reduce_kernel<<<(unsigned)(p.T * 32), 256, 0, st>>>(s.N, (int)s.M, p.nb, p.T, p.fchunks,
+                                                             fat(ws, p.off_fp), h.sf2, psi0, Psi2,
+                                                             accumulate);
     return hipGetLastError();
 }
 
@@ -1172,10 +1247,10 @@ hipError_t mfma_psi_grads(const Shape &s, const float *mu, const float *S, const
             s.N, (int)s.Q, (int)p.ggroups, fat(ws, p.off_rs), fat(ws, p.off_w2), S, h, dmu, dS,
             fat(ws, p.off_dl));
     }
-    const int64_t total = s.M * s.Q + s.Q + 1;
+    const int64_t zblocks = cdiv(s.M * s.Q, kRedOut);
     TimedScope ts(st, "mfma_grad_reduce");
-    grad_reduce_kernel<<<(unsigned)cdiv(total, 256), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, fat(ws, p.off_dz), p.gchunks * p.njr, fat(ws, p.off_dl),
+    grad_reduce_kernel<<<(unsigned)(zblocks + s.Q + 1), 256, 0, st>>>(
+        s.N, (int)s.M, (int)s.Q, zblocks, fat(ws, p.off_dz), p.gchunks * p.njr, fat(ws, p.off_dl),
         p.fin_blocks, dL_dpsi0, dZ, dsf2, dl, accumulate);
     return hipGetLastError();
 }

@@ -68,6 +68,7 @@ def algorithmic(kernel: str, N: int, M: int, Q: int):
         "generic_psi2_partial": ("alu", fwd, "flop"),
         "generic_grad_rows": ("alu", 4.0 * Q * N * P, "flop"),
         "generic_grad_cols": ("alu", 2.0 * Q * N * P, "flop"),
+        "generic_grad_pairs": ("alu", grad, "flop"),
         "mfma_psi2_fwd": ("mfma", fwd, "flop"),
         "mfma_psi2_grad": ("mfma", grad, "flop"),
         "generic_psi1": ("hbm", 4.0 * (N * M + 2 * N * Q), "byte"),
@@ -203,6 +204,11 @@ def bench_gplvm(args):
         roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 4), "peak": peak,
                     "unit": u, "frac": round(ach / peak, 5), "traffic": None,
                     "algorithmic_per_launch": work}
+    # at Q = 1 the statistic kernels are bound by fp64 exponentials, one per
+    # datapoint and unique pair (forward) or ordered pair (gradient)
+    P = M * (M + 1) // 2
+    exps = {"generic_psi2_partial": N * P, "generic_grad_pairs": N * M * M}
+    exp_rate = {k: round(v / (kernels[k]["avg_ms"] * 1e-3), 1) for k, v in exps.items() if k in kernels}
     rec = {
         "metric": "Bayesian GP-LVM bound + gradient evaluations/sec (fp64), 1 MI355X",
         "value": 1e3 / ms, "unit": "evals/s", "n_gpus": 1, "steps": args.steps,
@@ -211,6 +217,7 @@ def bench_gplvm(args):
         "config": {"workload": f"gplvm-paper (N={N}, M={M}, Q={Q}, D={D}, seed 0)", "N": N,
                    "M": M, "Q": Q, "D": D, "L": float(out["L"].item())},
         "roofline": roofline,
+        "exp_per_s": exp_rate,
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}
                     for k, v in sorted(kernels.items())},
     }

@@ -38,6 +38,9 @@ __device__ inline double dlog1p(double x) { return log1p(x); }
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Register width (latent dimensions, padded) of the pairs kernel for Q.
+inline int64_t pairs_qm(int64_t Q) { return Q <= 1 ? 1 : Q <= 2 ? 2 : Q <= 4 ? 4 : Q <= 8 ? 8 : 16; }
+
 struct Plan {
     int64_t tiles_edge, tiles;       // pair tiles per edge and upper-triangle tile count
     int64_t nc2;                     // row chunks of the Psi2 forward kernel
@@ -47,6 +50,9 @@ struct Plan {
     int64_t row_blocks;              // row-kernel blocks
     int64_t rr;                      // row kernel: ranges of pair rows m (m = r mod rr)
     int64_t cr;                      // column kernel: ranges of partners m'
+    bool pairs;                      // gradients by grad_pairs_kernel (Z table fits in LDS)
+    int pthreads;                    // pairs kernel: threads (inducing inputs) per workgroup
+    int64_t pmb, pchunks, prows;     // pairs kernel: m-blocks, row chunks, rows per chunk
     // workspace offsets in bytes
     size_t off_w1, off_w2, off_lp1, off_lp2, off_p2, off_g2s, off_colp, off_rowp, off_rowg, total;
 };
@@ -70,6 +76,15 @@ Plan make_plan(const Shape &s, size_t elem) {
     p.rr = std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(s.M, 64), cdiv(2048, p.row_blocks)));
     p.cr = std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(s.M, 64),
                                                   cdiv(2048, p.col_blocks * p.ncc)));
+    // the pairs kernel keeps the whole Z table (padded to QM) in LDS and a dozen
+    // per-dimension values per thread in registers: small Q only (beyond that
+    // it spills and the row and column kernels below take over)
+    p.pairs = pairs_qm(s.Q) <= (elem == 4 ? 8 : 4) && s.M * pairs_qm(s.Q) * elem <= 65536;
+    p.pthreads = (int)std::min<int64_t>(256, cdiv(s.M, 64) * 64);
+    p.pmb = cdiv(s.M, p.pthreads);
+    p.pchunks = std::max<int64_t>(1, std::min<int64_t>(s.N, 2048 / p.pmb));
+    p.prows = cdiv(s.N, p.pchunks);
+    p.pchunks = cdiv(s.N, p.prows);
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_w1 = take(elem * s.N * s.Q);
@@ -78,9 +93,9 @@ Plan make_plan(const Shape &s, size_t elem) {
     p.off_lp2 = take(elem * s.N);
     p.off_p2 = take(elem * p.nc2 * s.P);
     p.off_g2s = take(elem * s.M * s.M);
-    p.off_colp = take(elem * p.ncc * p.cr * s.M * s.Q);
-    p.off_rowp = take(elem * p.rr * p.row_blocks * (s.Q + 1));
-    p.off_rowg = take(elem * p.rr * s.N * s.Q * 2);
+    p.off_colp = take(elem * std::max(p.ncc * p.cr, p.pchunks) * s.M * s.Q);
+    p.off_rowp = take(elem * std::max(p.rr * p.row_blocks, p.pmb * p.pchunks) * (s.Q + 1));
+    p.off_rowg = take(elem * std::max(p.rr, p.pmb) * s.N * s.Q * 2);
     p.total = o;
     return p;
 }
@@ -341,6 +356,151 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
     }
 }
 
+// Psi2 and Psi1 gradients through per-(n, m) sums.  With W_n[m, m'] =
+// G2s[m, m'] Psi2_n[m, m'], d = mu_n - z_m, w1 = 1/(l^2 + S_n), w2 = 1/(l^2 + 2 S_n),
+//   r_nm = sum_m' W_n[m, m'],  V_nmq = sum_m' W_n[m, m'] d_nm'q,
+//   t_nm = dL/dPsi1[n, m] Psi1[n, m],
+// every gradient is a sum over (n, m) of (W is symmetric, so the double sum over
+// ordered pairs folds onto the m index):
+//   dmu_nq += -2 w2 d r - t d w1
+//   dS_nq  += w2^2 (d^2 r + d V) - w2 r + t (d^2 w1^2 - w1) / 2
+//   dZ_mq  += w2 (d r + V) - (V - d r) / l^2 + t d w1
+//   dl_q   += (2 S w2 / l) r + (d^2 r - d V) / l^3 + l w2^2 (d^2 r + d V)
+//             + t (S w1 / l + l d^2 w1^2)
+//   dsf2   += (2 r + t) / sf2.
+// One workgroup per (block of inducing inputs, row chunk), one thread per m, the
+// Z table in LDS: each exponential is evaluated once per ordered (n, m, m'),
+// dZ_m stays in the thread's registers over the chunk, and per row the dmu / dS
+// contributions are summed over the block's m (wave butterflies, then the waves
+// in order) into rowg[m-block][2][N][Q].
+template <typename T, int QM>
+__global__ __launch_bounds__(256) void grad_pairs_kernel(
+    int64_t N, int M, int Q, int64_t rows_per_chunk, const T *__restrict__ mu,
+    const T *__restrict__ S, const T *__restrict__ Z, const T *__restrict__ w1t,
+    const T *__restrict__ w2t, const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h,
+    const T *__restrict__ G1, const T *__restrict__ G2s, T *__restrict__ rowg,
+    T *__restrict__ colpart, T *__restrict__ rowpart) {
+    extern __shared__ double gp_smem[];
+    T *sz = reinterpret_cast<T *>(gp_smem);  // [M][QM], zero beyond Q
+    __shared__ T red[2][4][2 * QM];           // per-wave row sums, double buffered by row
+    const int tid = threadIdx.x, nthr = blockDim.x, nw = nthr >> 6, wv = tid >> 6;
+    const int m = blockIdx.x * nthr + tid;
+    const bool valid = m < M;
+    for (int i = tid; i < M * QM; i += nthr) {
+        const int mm = i / QM, q = i - mm * QM;
+        sz[i] = q < Q ? Z[(int64_t)mm * Q + q] : T(0);
+    }
+    __syncthreads();
+    T z[QM], c4[QM], il2[QM], gz[QM], gl[QM];
+#pragma unroll
+    for (int q = 0; q < QM; ++q) {
+        z[q] = valid ? sz[m * QM + q] : T(0);
+        c4[q] = q < Q ? T(0.25) / h.l2[q] : T(0);
+        il2[q] = q < Q ? T(1) / h.l2[q] : T(0);
+        gz[q] = gl[q] = 0;
+    }
+    T gsf = 0;
+    const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk, r1 = min(N, r0 + rows_per_chunk);
+    for (int64_t n = r0; n < r1; ++n) {
+        T x[QM], a1[QM], a2[QM], sv[QM], d[QM];
+#pragma unroll
+        for (int q = 0; q < QM; ++q) {
+            const bool in = q < Q;
+            x[q] = in ? mu[n * Q + q] : T(0);
+            a1[q] = in ? w1t[n * Q + q] : T(0);
+            a2[q] = in ? w2t[n * Q + q] : T(0);
+            sv[q] = in ? S[n * Q + q] : T(0);
+            d[q] = x[q] - z[q];
+        }
+        T r = 0, V[QM];
+#pragma unroll
+        for (int q = 0; q < QM; ++q) V[q] = 0;
+        if (G2s && valid) {
+            const T base = lp2[n];
+            for (int mp = 0; mp < M; ++mp) {
+                const T g = G2s[(int64_t)mp * M + m];  // G2s symmetric: a coalesced row
+                const T *zr = sz + mp * QM;
+                T e = base;
+#pragma unroll
+                for (int q = 0; q < QM; ++q) {
+                    const T dz = z[q] - zr[q];
+                    const T s2 = d[q] + (x[q] - zr[q]);
+                    e -= dz * dz * c4[q] + s2 * s2 * (T(0.25) * a2[q]);
+                }
+                const T W = g * dexp(e);
+                r += W;
+#pragma unroll
+                for (int q = 0; q < QM; ++q) V[q] += W * (x[q] - zr[q]);
+            }
+        }
+        T t = 0;
+        if (G1 && valid) {
+            T e1 = 0;
+#pragma unroll
+            for (int q = 0; q < QM; ++q) e1 += d[q] * d[q] * a1[q];
+            t = G1[n * M + m] * dexp(lp1[n] - T(0.5) * e1);
+        }
+        T rv[2 * QM];
+#pragma unroll
+        for (int q = 0; q < QM; ++q) {
+            const T dq = d[q], d2 = dq * dq, dr = dq * r, dV = dq * V[q];
+            rv[q] = -T(2) * a2[q] * dr - t * dq * a1[q];
+            rv[QM + q] = a2[q] * a2[q] * (d2 * r + dV) - a2[q] * r +
+                         T(0.5) * t * (d2 * a1[q] * a1[q] - a1[q]);
+            gz[q] += a2[q] * (dr + V[q]) - (V[q] - dr) * il2[q] + t * dq * a1[q];
+            if (q < Q) {
+                const T l = h.l[q];
+                gl[q] += (T(2) * sv[q] * a2[q] / l) * r + (d2 * r - dV) * il2[q] / l +
+                         l * a2[q] * a2[q] * (d2 * r + dV) +
+                         t * (sv[q] * a1[q] / l + l * d2 * a1[q] * a1[q]);
+            }
+        }
+        gsf += T(2) * r + t;
+        // sum of rv over the block's m: butterflies within each wave, then the
+        // waves in order (double buffered by row parity: one barrier per row)
+        const int b = (int)(n & 1);
+#pragma unroll
+        for (int k = 0; k < 2 * QM; ++k) {
+            T v = rv[k];
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+            if ((tid & 63) == 0) red[b][wv][k] = v;
+        }
+        __syncthreads();
+        if (tid < 2 * Q) {
+            const int k = tid < Q ? tid : QM + (tid - Q);
+            T v = 0;
+            for (int w = 0; w < nw; ++w) v += red[b][w][k];
+            const int part = tid < Q ? 0 : 1, q = tid < Q ? tid : tid - Q;
+            rowg[(((int64_t)blockIdx.x * 2 + part) * N + n) * Q + q] = v;
+        }
+    }
+    if (valid) {
+#pragma unroll
+        for (int q = 0; q < QM; ++q)
+            if (q < Q) colpart[((int64_t)blockIdx.y * M + m) * Q + q] = gz[q];
+    }
+    // block sums of dl and dsf2 (fixed order, as above) -> rowpart[block][Q + 1]
+    const int64_t blk = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k <= QM; ++k) {
+        if (k < Q || k == QM) {
+            T v = k < QM ? gl[k] : gsf / h.sf2;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+            if ((tid & 63) == 0) red[0][wv][0] = v;
+            __syncthreads();
+            if (tid == 0) {
+                T s = 0;
+                for (int w = 0; w < nw; ++w) s += red[0][w][0];
+                rowpart[blk * (Q + 1) + (k < QM ? k : Q)] = s;
+            }
+            __syncthreads();
+        }
+    }
+}
+
 // dmu, dS: the row kernel's range partials summed in range order.
 template <typename T>
 __global__ void grad_rows_reduce_kernel(int64_t NQ, int rr, const T *__restrict__ rowg,
@@ -559,6 +719,34 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
     }
     T *colpart = at<T>(ws, p.off_colp), *rowpart = at<T>(ws, p.off_rowp);
     T *rowg = at<T>(ws, p.off_rowg);
+    if (p.pairs) {
+        const size_t lds = sizeof(T) * s.M * pairs_qm(s.Q);
+        dim3 grid((unsigned)p.pmb, (unsigned)p.pchunks);
+        {
+            TimedScope ts(st, "generic_grad_pairs");
+#define GPPS_PAIRS(QMV)                                                                          \
+    grad_pairs_kernel<T, QMV><<<grid, p.pthreads, lds, st>>>(s.N, (int)s.M, (int)s.Q, p.prows,  \
+                                                            mu, S, Z, w1, w2, lp1, lp2, h, G1,  \
+                                                            G2s, rowg, colpart, rowpart)
+            switch (pairs_qm(s.Q)) {
+                case 1: GPPS_PAIRS(1); break;
+                case 2: GPPS_PAIRS(2); break;
+                case 4: GPPS_PAIRS(4); break;
+                default:
+                    if (sizeof(T) == 4) GPPS_PAIRS(8);
+                    break;
+            }
+#undef GPPS_PAIRS
+        }
+        const int64_t total = s.M * s.Q + s.Q + 1;
+        TimedScope ts(st, "generic_grad_reduce");
+        grad_rows_reduce_kernel<T><<<(unsigned)cdiv(s.N * s.Q, 256), 256, 0, st>>>(
+            s.N * s.Q, (int)p.pmb, rowg, dmu, dS);
+        grad_reduce_kernel<T><<<(unsigned)total, 256, 0, st>>>(
+            s.N, (int)s.M, (int)s.Q, p.pchunks, p.pmb * p.pchunks, colpart, rowpart, dL_dpsi0, dZ,
+            dsf2, dl, accumulate);
+        return hipGetLastError();
+    }
     if (s.Q <= 4)
         launch_grads<T, 4>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
     else if (s.Q <= 8)

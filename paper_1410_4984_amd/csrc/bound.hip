@@ -171,8 +171,20 @@ __global__ __launch_bounds__(256) void bound_psiy_kernel(int64_t N, int M, int64
          k += (int64_t)gridDim.y * 256) {
         const int m = (int)(k % M);
         const int64_t d = k / M;
+        // row order; loads issued 16 rows at a time so that they overlap
         double s = 0.0;
-        for (int64_t n = n0; n < n1; ++n) s += (double)Psi1[n * M + m] * (double)Y[n * D + d];
+        int64_t n = n0;
+        for (; n + 16 <= n1; n += 16) {
+            double a[16], b[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                a[j] = (double)Psi1[(n + j) * M + m];
+                b[j] = (double)Y[(n + j) * D + d];
+            }
+#pragma unroll
+            for (int j = 0; j < 16; ++j) s += a[j] * b[j];
+        }
+        for (; n < n1; ++n) s += (double)Psi1[n * M + m] * (double)Y[n * D + d];
         part[((int64_t)blockIdx.x * D + d) * M + m] = s;
     }
 }
@@ -185,8 +197,19 @@ __global__ void bound_psiy_reduce_kernel(int M, int Mp, int64_t D, int64_t chunk
     const int m = (int)(k / D);
     const int64_t d = k - (int64_t)m * D;
     double s = 0.0;
-    if (m < M)
-        for (int64_t c = 0; c < chunks; ++c) s += part[(c * D + d) * M + m];
+    if (m < M) {  // chunk order, loads issued 16 at a time
+        const double *src = part + d * M + m;
+        const int64_t stride = D * M;
+        int64_t c = 0;
+        for (; c + 16 <= chunks; c += 16) {
+            double v[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) v[j] = src[(c + j) * stride];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) s += v[j];
+        }
+        for (; c < chunks; ++c) s += src[c * stride];
+    }
     Psi[k] = s;
 }
 

@@ -689,7 +689,9 @@ hipError_t generic_psi_stats(const Shape &s, const T *mu, const T *S, const T *Z
                                                                        mu, Z, w1, lp1, Psi1);
     }
     T *partial = at<T>(ws, p.off_p2);
-    if (s.Q <= 4) launch_psi2_partial<T, 4>(s, p, mu, Z, w2, lp2, h, partial, st);
+    if (s.Q <= 1) launch_psi2_partial<T, 1>(s, p, mu, Z, w2, lp2, h, partial, st);
+    else if (s.Q <= 2) launch_psi2_partial<T, 2>(s, p, mu, Z, w2, lp2, h, partial, st);
+    else if (s.Q <= 4) launch_psi2_partial<T, 4>(s, p, mu, Z, w2, lp2, h, partial, st);
     else if (s.Q <= 8) launch_psi2_partial<T, 8>(s, p, mu, Z, w2, lp2, h, partial, st);
     else if (s.Q <= 16) launch_psi2_partial<T, 16>(s, p, mu, Z, w2, lp2, h, partial, st);
     else if (s.Q <= 32) launch_psi2_partial<T, 32>(s, p, mu, Z, w2, lp2, h, partial, st);

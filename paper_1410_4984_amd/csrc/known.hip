@@ -198,24 +198,33 @@ __global__ __launch_bounds__(256) void known_kfu_kernel(int64_t N, int M, int Q,
     }
     __syncthreads();
     const T pre = kpre(h);
+    using VT = typename Vec<T>::t;
+    constexpr int W = Vec<T>::W;
     T s[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) s[j] = 0;
+    // each thread owns 16 consecutive rows (columns) of the block, read from
+    // the LDS table as 16-byte vectors
     if (!TRANS) {
         const int c = tid & 63, rg = tid >> 6;
         for (int q = 0; q < Q; ++q) {
             const T zc = sz[q * kEdge + c];
+            const VT *xr = reinterpret_cast<const VT *>(sx + q * kEdge + 16 * rg);
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const T d = sx[q * kEdge + rg + 4 * j] - zc;
-                s[j] = fma(d, d, s[j]);
+            for (int v = 0; v < 16 / W; ++v) {
+                const VT xv = xr[v];
+#pragma unroll
+                for (int w = 0; w < W; ++w) {
+                    const T d = xv[w] - zc;
+                    s[v * W + w] = fma(d, d, s[v * W + w]);
+                }
             }
         }
         const int m = m0 + c;
         if (m < M) {
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
-                const int64_t n = n0 + rg + 4 * j;
+                const int64_t n = n0 + 16 * rg + j;
                 if (n < N) out[n * M + m] = kval(pre, s[j]);
             }
         }
@@ -223,17 +232,22 @@ __global__ __launch_bounds__(256) void known_kfu_kernel(int64_t N, int M, int Q,
         const int r = tid & 63, cg = tid >> 6;
         for (int q = 0; q < Q; ++q) {
             const T xr = sx[q * kEdge + r];
+            const VT *zr = reinterpret_cast<const VT *>(sz + q * kEdge + 16 * cg);
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const T d = xr - sz[q * kEdge + cg + 4 * j];
-                s[j] = fma(d, d, s[j]);
+            for (int v = 0; v < 16 / W; ++v) {
+                const VT zv = zr[v];
+#pragma unroll
+                for (int w = 0; w < W; ++w) {
+                    const T d = xr - zv[w];
+                    s[v * W + w] = fma(d, d, s[v * W + w]);
+                }
             }
         }
         const int64_t n = n0 + r;
         if (n < N) {
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
-                const int m = m0 + cg + 4 * j;
+                const int m = m0 + 16 * cg + j;
                 if (m < M) out[(int64_t)m * N + n] = kval(pre, s[j]);
             }
         }
@@ -512,10 +526,10 @@ __device__ inline T block_sum(T v, T *red4) {
 }
 
 // Chain-rule kernels.  Every difference xs_nq - zs_mq is formed before it is
-// weighted by E, so no large sums are subtracted afterwards: E is localised
-// around each z_m (and each x_n), so the expanded forms (sum_n E xs -
-// zs sum_n E and the like) would cancel to a small remainder and lose most of
-// their fp32 digits.  LDS rows are zero beyond Q, and so are the register
+// weighted by E, so no large sums are subtracted afterwards (the expanded forms,
+// sum_n E xs - zs sum_n E and the like, can cancel to a small remainder where E
+// is concentrated around z_m far from the centre).  LDS rows are zero beyond Q,
+// and so are the register
 // copies of the fixed point, so the padded dimensions contribute nothing (no
 // per-dimension guard: a runtime bound inside the unrolled loops makes the
 // compiler shuffle the accumulators).

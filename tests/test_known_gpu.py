@@ -180,6 +180,86 @@ def test_known_large_row_subset_full():
     compare_all(run_gpu(sub, torch.float32), run_oracle(sub), TOL32, "known-large-subset")
 
 
+def test_known_stress_chunked():
+    """N = 10^6, M = 512, Q = 30 (the stress workload with S dropped) in 8 row
+    chunks accumulating on the device: symmetry, psi0, sampled Psi2 entries (each
+    a sum over all 10^6 rows), sampled rows of Psi1 and dX, and the identities
+    (translation, scaling, sigma_f2-homogeneity with <G1, Psi1> summed per chunk)."""
+    say("[known stress f32 chunked]")
+    w = synth.WORKLOADS["stress"]
+    inp = synth.to_f32(synth.make_workload("stress"))
+    inp["S"] = None
+    N, M, Q, C = w.N, w.M, w.Q, w.chunk_rows
+    t = lambda a: torch.tensor(a, dtype=torch.float32, device=DEV)  # noqa: E731
+    X, Z, G2 = t(inp["mu"]), t(inp["Z"]), t(inp["dL_dPsi2"])
+    psi0 = torch.zeros(1, device=DEV)
+    Psi2 = torch.zeros((M, M), device=DEV)
+    g = {"dmu": torch.empty((N, Q), device=DEV), "dS": None, "dZ": torch.zeros((M, Q), device=DEV),
+         "dsigma_f2": torch.zeros(1, device=DEV), "dl": torch.zeros(Q, device=DEV)}
+    ws = torch.empty(gpps.workspace_bytes("f32", C, M, Q), dtype=torch.uint8, device=DEV)
+    P1 = torch.empty((C, M), device=DEV)
+    rng = np.random.default_rng(6)
+    rows = np.sort(rng.choice(N, 16, replace=False))
+    rows[-1] = N - 1
+    P1_rows = np.empty((rows.shape[0], M))
+    G1_rows = np.empty((rows.shape[0], M))
+    G1_sum = 0.0
+    for c, r0 in enumerate(range(0, N, C)):
+        r1 = min(N, r0 + C)
+        G1 = synth.stress_dL_dPsi1_chunk(0, c, r1 - r0, M).astype(np.float32)
+        G1d = torch.tensor(G1, device=DEV)
+        P1c = P1[: r1 - r0]
+        gpps.psi_stats(X[r0:r1], None, Z, inp["sigma_f2"], inp["l"], accumulate=c > 0,
+                       out=(psi0, P1c, Psi2), workspace=ws)
+        G1_sum += float(torch.sum(G1d.double() * P1c.double()))
+        sel = (rows >= r0) & (rows < r1)
+        if sel.any():
+            idx = torch.tensor(rows[sel] - r0, device=DEV)
+            P1_rows[sel] = P1c[idx].double().cpu().numpy()
+            G1_rows[sel] = G1[rows[sel] - r0].astype(np.float64)
+        gpps.psi_grads(X[r0:r1], None, Z, inp["sigma_f2"], inp["l"], inp["dL_dpsi0"], G1d, G2,
+                       accumulate=c > 0, out=dict(g, dmu=g["dmu"][r0:r1]), workspace=ws)
+        say(f"  chunk {c} rows {r0}:{r1} done")
+    torch.cuda.synchronize()
+    got = {"psi0": psi0.cpu().double().numpy()[0], "Psi2": Psi2.cpu().double().numpy()}
+    for k in ("dmu", "dZ", "dsigma_f2", "dl"):
+        got[k] = g[k].cpu().double().numpy()
+    got["dsigma_f2"] = got["dsigma_f2"][0]
+    assert np.array_equal(got["Psi2"], got["Psi2"].T)
+    assert got["psi0"] == pytest.approx(N * inp["sigma_f2"], rel=1e-5)
+    sf2, l = inp["sigma_f2"], inp["l"]
+    S0 = np.zeros_like(inp["mu"])
+    pairs = np.stack([rng.integers(0, M, 32), rng.integers(0, M, 32)], 1)
+    pairs[:4, 1] = pairs[:4, 0]
+    ref = oracle.psi2_entries(inp["mu"], S0, inp["Z"], sf2, l, pairs)
+    e = rel(got["Psi2"][pairs[:, 0], pairs[:, 1]], ref)
+    say(f"  Psi2 sampled: rel {e:.3e}")
+    assert e <= TOL32["Psi2"]
+    _, P1r, _ = oracle.psi_stats(inp["mu"][rows], S0[rows], inp["Z"], sf2, l)
+    gr = oracle.psi_grads(inp["mu"][rows], S0[rows], inp["Z"], sf2, l, 0.0, G1_rows,
+                          inp["dL_dPsi2"])
+    for k, a, b, tol in (("Psi1", P1_rows, P1r, TOL32["Psi1"]),
+                         ("dmu", got["dmu"][rows], gr["dmu"], TOL32["dmu"])):
+        e = rel(a, b)
+        say(f"  {k} rows: rel {e:.3e}")
+        assert e <= tol, k
+    # identities (the Psi1 term of homogeneity from the per-chunk sums)
+    Xn, Zn = inp["mu"], inp["Z"]
+    r = got["dmu"].sum(0) + got["dZ"].sum(0)
+    sc = np.abs(got["dmu"]).sum(0) + np.abs(got["dZ"]).sum(0)
+    say(f"  translation residual {np.max(np.abs(r) / sc):.2e}")
+    assert np.all(np.abs(r) <= 2e-5 * sc)
+    r = (Xn * got["dmu"]).sum(0) + (Zn * got["dZ"]).sum(0) + l * got["dl"]
+    sc = np.abs(Xn * got["dmu"]).sum(0) + np.abs(Zn * got["dZ"]).sum(0) + np.abs(l * got["dl"])
+    say(f"  scaling residual {np.max(np.abs(r) / sc):.2e}")
+    assert np.all(np.abs(r) <= 2e-5 * sc)
+    G2s = 0.5 * (inp["dL_dPsi2"] + inp["dL_dPsi2"].T)
+    a, b, c = G1_sum, 2 * np.sum(G2s * got["Psi2"]), inp["dL_dpsi0"] * N * sf2
+    r = sf2 * got["dsigma_f2"] - (a + b + c)
+    say(f"  homogeneity residual {abs(r) / (abs(a) + abs(b) + abs(c)):.2e}")
+    assert abs(r) <= 1e-4 * (abs(a) + abs(b) + abs(c))
+
+
 def test_known_without_psi1_and_deterministic():
     inp = known_inputs(2500, 96, 5, seed=21, f32=True)
     a = run_gpu(inp, torch.float32)

@@ -6,7 +6,10 @@ library and the oracle factorise Kmm and A by different (blocked vs. LAPACK)
 Cholesky codes, so on an ill-conditioned problem an output can differ by as much
 as two backward-stable fp64 evaluations of the same definition do.  The test
 measures that spread on the oracle itself (Cholesky-based inverses against
-LU-based ones) and allows, per output, max(1e-9, 10 x that spread).  At the
+LU-based and eigendecomposition-based ones; one pair alone under-samples it: the
+LU spread of dsigma_f2 at the paper's shape measured 1.3e-10 on one host and
+4.4e-10 on another, the eigendecomposition's 1.1e-9) and allows, per output,
+max(1e-9, 10 x the largest spread).  At the
 paper's shape (Q = 1, M = 100) cond(A) reaches ~1e7 and dZ is the difference of
 two nearly equal contributions (through the psi-statistics and through Kmm), so
 its spread is ~1e-6; every other case and output is held to 1e-9.  The parity
@@ -72,11 +75,14 @@ def run_oracle(p, f32, inverse=None):
 
 
 def spread_tol(p, ref):
-    """max(1e-9, 10 x the relative spread between Cholesky- and LU-based oracle runs)."""
-    alt = run_oracle(p, False, inverse=ob._inv_lu)
-    tol = {"L": abs(alt["L"] - ref["L"]) / abs(ref["L"])}
-    for k in KEYS:
-        tol[k] = rel(np.asarray(alt[k]), np.asarray(ref[k]))
+    """max(1e-9, 10 x the largest relative spread between the Cholesky-based oracle
+    run and the LU- and eigendecomposition-based ones)."""
+    tol = {k: 0.0 for k in ("L",) + KEYS}
+    for inv in (ob._inv_lu, ob._inv_eigh):
+        alt = run_oracle(p, False, inverse=inv)
+        tol["L"] = max(tol["L"], abs(alt["L"] - ref["L"]) / abs(ref["L"]))
+        for k in KEYS:
+            tol[k] = max(tol[k], rel(np.asarray(alt[k]), np.asarray(ref[k])))
     return {k: max(1e-9, 10.0 * v) for k, v in tol.items()}
 
 
@@ -95,7 +101,8 @@ def kmm_cond(p):
 @pytest.mark.parametrize("shape,spread,jitter", [((300, 20, 3, 4), 1.0, 1e-6),
                                                  ((777, 45, 2, 1), 3.0, 1e-6),
                                                  ((64, 33, 5, 7), 1.0, 1e-6),
-                                                 ((1000, 100, 1, 3), 2.0, 1e-2)])
+                                                 ((1000, 100, 1, 3), 2.0, 1e-2),
+                                                 ((1500, 150, 3, 3), 3.0, 1e-6)])
 def test_bound_f64_matches_oracle(shape, spread, jitter):
     N, M, Q, D = shape
     p = problem(N, M, Q, D, seed=N + M, spread=spread, jitter=jitter)

@@ -9,10 +9,18 @@ the device); only the optimiser's vector arithmetic runs on the host.
 
 Positive parameters are optimised through their logarithms (S, sigma_f2, l,
 beta); the chain rule d/dlog x = x d/dx is applied to the gradients the library
-returns.
+returns.  A step whose parameters overflow is reported as infeasible (the line
+search backs off); the regression fit also bounds its log parameters (L-BFGS-B's
+box constraints), which its first line-search step needs.
 
     fit(Y, Q, M, iters=...) -> FitResult
+    fit_regression(X, Y, M, iters=...) -> RegressionResult
     paper_data(N, D=3, seed=0) -> (Y, x_true)   the synthetic data of section 4
+
+fit_regression is the sparse GP regression model of eq. (boundF) itself: the
+inputs X are observed (``gpps_bound`` with S = NULL, no q(X) and no KL term) and
+the optimiser adjusts the inducing inputs Z and the kernel and noise
+parameters only.
 """
 from __future__ import annotations
 
@@ -114,6 +122,8 @@ def fit(Y: np.ndarray, Q: int, M: int, *, iters: int = 200, dtype=None, jitter: 
     def objective(x):
         nonlocal out
         mu, S, Z, sf2, l, beta = _unpack(x, N, M, Q)
+        if not _feasible(S, sf2, l, beta):
+            return 1e300, np.zeros_like(x)
         t = {k: torch.tensor(v, dtype=dtype, device=device) for k, v in (("mu", mu), ("S", S),
                                                                            ("Z", Z))}
         t0 = time.perf_counter()
@@ -141,6 +151,90 @@ def fit(Y: np.ndarray, Q: int, M: int, *, iters: int = 200, dtype=None, jitter: 
                      str(res.message))
 
 
+_LOG_BOUND = 30.0
+
+
+def _feasible(S, sf2, l, beta) -> bool:
+    """A line-search step can overflow exp() of a log parameter: such a point is
+    infeasible (the library would reject it), so the objective reports a huge
+    value and the line search backs off."""
+    vals = [sf2, beta, *np.ravel(l)] + ([] if S is None else [float(np.min(S)), float(np.max(S))])
+    return all(np.isfinite(v) and v > 0 for v in vals)
+
+
 def _ws_bytes(dtype, N, M, Q, D):
     from . import bound_workspace_bytes
     return bound_workspace_bytes(dtype, N, M, Q, D)
+
+
+@dataclasses.dataclass
+class RegressionResult:
+    Z: np.ndarray
+    sigma_f2: float
+    l: np.ndarray
+    beta: float
+    bound_trace: list        # L after every evaluation
+    evals: int
+    iterations: int
+    seconds: float
+    message: str
+
+
+def fit_regression(X: np.ndarray, Y: np.ndarray, M: int, *, iters: int = 200, dtype=None,
+                   jitter: float = 1e-6, seed: int = 0, device: str = "cuda:0",
+                   tol: float = 1e-9) -> RegressionResult:
+    """Maximise the regression bound of eq. (boundF) over (Z, log sigma_f2, log l,
+    log beta) with L-BFGS-B, X fixed.  Y is centred internally.  Start: Z a random
+    subset of X, sigma_f2 = var(Y), l = the spread of each input dimension,
+    beta = 100 / var(Y).  Every objective evaluation is one ``gpps_bound`` call
+    with S = None on ``device`` (dtype float64 unless given)."""
+    import scipy.optimize
+    import torch
+
+    dtype = torch.float64 if dtype is None else dtype
+    X = np.asarray(X, np.float64)
+    Y = np.asarray(Y, np.float64)
+    Y = Y - Y.mean(0)
+    N, Q = X.shape
+    D = Y.shape[1]
+    rng = np.random.default_rng(seed)
+    Z0 = X[rng.choice(N, size=M, replace=False)].copy()
+    var = float(Y.var())
+    x0 = np.concatenate([Z0.ravel(), [np.log(var)], np.log(X.std(0) + 1e-12), [np.log(100.0 / var)]])
+    Xt = torch.tensor(X, dtype=dtype, device=device)
+    Yt = torch.tensor(Y, dtype=dtype, device=device)
+    ws = torch.empty(max(1, _ws_bytes(dtype, N, M, Q, D)), dtype=torch.uint8, device=device)
+    trace = []
+    out = None
+
+    def unpack(x):
+        Z = x[:M * Q].reshape(M, Q)
+        return Z, float(np.exp(x[M * Q])), np.exp(x[M * Q + 1:M * Q + 1 + Q]), float(np.exp(x[-1]))
+
+    def objective(x):
+        nonlocal out
+        Z, sf2, l, beta = unpack(x)
+        if not _feasible(None, sf2, l, beta):
+            return 1e300, np.zeros_like(x)
+        Zt = torch.tensor(Z, dtype=dtype, device=device)
+        out = bound(Xt, None, Zt, Yt, sf2, l, beta, jitter, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        g = {k: v.double().cpu().numpy() for k, v in out.items() if v is not None}
+        L = float(g["L"][0])
+        if not np.isfinite(L):
+            return 1e300, np.zeros_like(x)
+        trace.append(L)
+        grad = np.concatenate([g["dZ"].ravel(), [float(g["dsigma_f2"][0]) * sf2], g["dl"] * l,
+                               [float(g["dbeta"][0]) * beta]])
+        return -L, -grad
+
+    # the log parameters are bounded to +-30 (e^30 ~ 1e13): from this start the
+    # first line-search step is long enough to overflow exp() otherwise
+    bounds = [(None, None)] * (M * Q) + [(-_LOG_BOUND, _LOG_BOUND)] * (Q + 2)
+    t0 = time.perf_counter()
+    res = scipy.optimize.minimize(objective, x0, jac=True, method="L-BFGS-B", bounds=bounds,
+                                  options={"maxiter": iters, "ftol": tol, "gtol": 1e-8})
+    secs = time.perf_counter() - t0
+    Z, sf2, l, beta = unpack(res.x)
+    return RegressionResult(Z, sf2, l, beta, trace, int(res.nfev), int(res.nit), secs,
+                            str(res.message))

@@ -1,4 +1,5 @@
-"""The Bayesian GP-LVM optimiser loop (paper_1410_4984_amd.gplvm).
+"""The Bayesian GP-LVM optimiser loop (paper_1410_4984_amd.gplvm), and the sparse
+GP regression fit on the known-input path.
 
 CPU: the synthetic data recipe and the parameter packing.  GPU: a short fit on
 the paper's kind of data (a 1-D latent mapped to 3-D) raises the bound and
@@ -52,3 +53,39 @@ def test_fit_recovers_one_dimensional_latent():
     assert abs(rho) > 0.98
     # the noise precision approaches 1 / noise^2 = 400 from the start value 100 / var(Y)
     assert 250.0 < r.beta < 550.0
+
+
+@pytest.mark.gpu
+def test_regression_fit_recovers_noise_and_matches_oracle():
+    """Sparse GP regression (X observed, S = NULL) on the section 4 recipe read as a
+    regression problem: 1-D inputs x, outputs through RBF-GP draws plus N(0, 0.05^2)
+    noise.  The fit raises the bound and recovers the noise precision 1 / 0.05^2 =
+    400 (the CPU oracle's bound in the same L-BFGS-B loop reaches beta 403, l 0.97).
+    At the optimum 25 inducing inputs crowd the 1-D input range (cond(A) ~ 1e12),
+    so the bound there is determined only to the spread between backward-stable
+    fp64 evaluations (~7e-3 relative): the GPU's bound at the fitted parameters is
+    compared with the oracle's within 10 x that spread, measured as in the bound
+    tests."""
+    torch = pytest.importorskip("torch")
+    assert torch.cuda.is_available()
+    import paper_1410_4984_amd as gpps
+    from oracle import bound as ob
+    Y, x = gplvm.paper_data(3000, D=2, seed=1)
+    X = x[:, None]
+    r = gplvm.fit_regression(X, Y, M=25, iters=150)
+    print(f"  regression fit: L {r.bound_trace[0]:.1f} -> {max(r.bound_trace):.1f}, {r.iterations}"
+          f" iterations, beta {r.beta:.1f}, l {r.l}, sf2 {r.sigma_f2:.3f}, {r.message}", flush=True)
+    assert max(r.bound_trace) > r.bound_trace[0] + 100.0
+    assert 340.0 < r.beta < 470.0
+    Yc = Y - Y.mean(0)
+    t = lambda a: torch.tensor(a, dtype=torch.float64, device="cuda:0")  # noqa: E731
+    got = gpps.bound(t(X), None, t(r.Z), t(Yc), r.sigma_f2, r.l, r.beta, 1e-6)
+    L_gpu = float(got["L"].item())
+    args = (X, None, r.Z, Yc, r.sigma_f2, r.l, r.beta, 1e-6)
+    L_ref = ob.bound_terms(*args)[0]
+    spread = max(abs(ob.bound_terms(*args, inverse=inv)[0] - L_ref) for inv in (ob._inv_lu, ob._inv_eigh))
+    e = abs(L_gpu - L_ref) / abs(L_ref)
+    tol = max(1e-9, 10 * spread / abs(L_ref))
+    print(f"  bound at the fitted parameters: GPU {L_gpu:.6f}, oracle {L_ref:.6f}, rel {e:.2e}"
+          f" (tol {tol:.1e})", flush=True)
+    assert e <= tol

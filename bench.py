@@ -75,12 +75,13 @@ def algorithmic(kernel: str, N: int, M: int, Q: int):
         "mfma_psi1_fwd": ("hbm", 4.0 * (N * M + 2 * N * Q), "byte"),
         "mfma_psi1_grad": ("hbm", 4.0 * (N * M + 4 * N * Q), "byte"),
         # known inputs (S = 0): the rank-k update over the unique pairs, the
-        # gradient GEMM over all M x M, Kfu and the chain-rule passes per (n, m, q)
+        # gradient GEMM over all M x M, Kfu, and the chain rule per (n, m, q):
+        # rows a difference and an FMA, columns a difference, a product, a sum
+        # and an FMA (8 flops)
         "known_syrk": ("mfma", 2.0 * N * P, "flop"),
         "known_dkfu": ("mfma", 2.0 * N * M * M, "flop"),
         "known_kfu": ("alu", 3.0 * N * M * Q, "flop"),
-        "known_rows": ("alu", 2.0 * N * M * Q, "flop"),
-        "known_cols": ("alu", 2.0 * N * M * Q, "flop"),
+        "known_chain": ("alu", 8.0 * N * M * Q, "flop"),
     }
     return table.get(kernel)
 

@@ -95,9 +95,9 @@ struct KPlan {
     int64_t nb2, ntp, ntu, nbp; // kBlk-blocks per edge, tiles per edge, upper tiles, upper block pairs
     int64_t chunks, rows;       // Psi2 row chunks and rows per chunk
     int64_t grid_syrk;          // Psi2 workgroups (XCD-rounded)
-    int64_t rblocks;            // row-kernel blocks (256 datapoints each)
-    int64_t cchunks, crows;     // column-kernel row chunks and rows per chunk
-    size_t off_cz, off_xs, off_zs, off_k, off_e, off_g2s, off_part, off_rowp, off_colp, off_vc;
+    int64_t tiles;              // 64-row tiles of the datapoints (chain kernel)
+    int64_t gmax;               // chain kernel: most tile groups per inducing-input block
+    size_t off_cz, off_xs, off_zs, off_k, off_e, off_g2s, off_part, off_ep, off_colp, off_vc, off_dxp;
     size_t total;
 };
 
@@ -119,10 +119,10 @@ KPlan make_kplan(const Shape &s, size_t elem) {
     p.rows = round_up(cdiv(s.N, p.chunks), bk);
     p.chunks = cdiv(s.N, p.rows);
     p.grid_syrk = round_up(p.chunks, 8) * p.nbp;
-    p.rblocks = cdiv(s.N, 256);
-    p.cchunks = std::max<int64_t>(1, std::min<int64_t>(cdiv(s.N, kEdge), std::max<int64_t>(1, 2048 / p.nb)));
-    p.crows = round_up(cdiv(s.N, p.cchunks), kEdge);
-    p.cchunks = cdiv(s.N, p.crows);
+    // the chain kernel's grid is one round of resident workgroups, at most 8
+    // per CU on 256 CUs
+    p.tiles = cdiv(s.N, kEdge);
+    p.gmax = std::max<int64_t>(1, std::min<int64_t>(p.tiles, std::max<int64_t>(1, 2048 / p.nb)));
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_cz = take(elem * s.Q);
@@ -132,28 +132,38 @@ KPlan make_kplan(const Shape &s, size_t elem) {
     p.off_e = take(elem * s.N * s.M);
     p.off_g2s = take(elem * s.M * s.M);
     p.off_part = take(elem * p.chunks * p.ntu * p.tile * p.tile);
-    p.off_rowp = take(elem * p.rblocks);
-    p.off_colp = take(elem * p.cchunks * s.M * 2 * s.Q);
+    p.off_ep = take(elem * p.nb * p.gmax);
+    p.off_colp = take(elem * p.gmax * s.M * 2 * s.Q);
     p.off_vc = take(elem * s.M * 2 * s.Q);
+    p.off_dxp = take(elem * p.nb * s.N * s.Q);
     p.total = o;
     return p;
 }
 
 // ---------------------------------------------------------------- centring
-// cz[q] = mean_m z_mq, zs = (Z - cz) / l.  One workgroup: G = 256 / Q groups of
-// Q threads sum rows m = g, g + G, ... (coalesced), then the G partial sums of
-// each dimension are added in group order.
+// cz[q] = mean_m z_mq, zs = (Z - cz) / l.  One workgroup: G = 1024 / Q groups of
+// Q threads sum rows m = g, g + G, ... (coalesced; loads issued 8 at a time so
+// that they overlap), then the G partial sums of each dimension are added in
+// group order.
 template <typename T>
-__global__ __launch_bounds__(256) void known_centre_kernel(int M, int Q, const T *__restrict__ Z,
+__global__ __launch_bounds__(1024) void known_centre_kernel(int M, int Q, const T *__restrict__ Z,
                                                            Hyp<T> h, T *__restrict__ cz,
                                                            T *__restrict__ zs) {
-    __shared__ T part[256];
+    __shared__ T part[1024];
     __shared__ T c[GPPS_MAX_Q];
-    const int t = threadIdx.x, G = 256 / Q;
+    const int t = threadIdx.x, G = 1024 / Q;
     if (t < G * Q) {
         const int g = t / Q, q = t - g * Q;
         T s = 0;
-        for (int m = g; m < M; m += G) s += Z[(int64_t)m * Q + q];
+        int m = g;
+        for (; m + 7 * G < M; m += 8 * G) {
+            T v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = Z[(int64_t)(m + j * G) * Q + q];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s += v[j];
+        }
+        for (; m < M; m += G) s += Z[(int64_t)m * Q + q];
         part[t] = s;
     }
     __syncthreads();
@@ -164,7 +174,8 @@ __global__ __launch_bounds__(256) void known_centre_kernel(int M, int Q, const T
         cz[t] = c[t];
     }
     __syncthreads();
-    for (int i = t; i < M * Q; i += 256) zs[i] = (Z[i] - c[i % Q]) / h.l[i % Q];
+#pragma unroll 4
+    for (int i = t; i < M * Q; i += 1024) zs[i] = (Z[i] - c[i % Q]) / h.l[i % Q];
 }
 
 // ---------------------------------------------------------------- Kfu
@@ -525,178 +536,242 @@ __device__ inline T block_sum(T v, T *red4) {
     return ((red4[0] + red4[1]) + red4[2]) + red4[3];
 }
 
-// Chain-rule kernels.  Every difference xs_nq - zs_mq is formed before it is
-// weighted by E, so no large sums are subtracted afterwards (the expanded forms,
-// sum_n E xs - zs sum_n E and the like, can cancel to a small remainder where E
-// is concentrated around z_m far from the centre).  LDS rows are zero beyond Q,
-// and so are the register
-// copies of the fixed point, so the padded dimensions contribute nothing (no
-// per-dimension guard: a runtime bound inside the unrolled loops makes the
-// compiler shuffle the accumulators).
+// Chain-rule sums, both from one pass over E^T.  Every difference xs_nq - zs_mq
+// is formed before it is weighted by E, so no large sums are subtracted
+// afterwards (the expanded forms, sum_n E xs - zs sum_n E and the like, can
+// cancel to a small remainder where E is concentrated around z_m far from the
+// centre).  LDS rows are zero beyond Q and beyond the edge of the data, so the
+// padded dimensions and rows contribute nothing (no per-dimension guard: a
+// runtime bound inside the unrolled loops makes the compiler shuffle the
+// accumulators).
+//
+// Workgroup (64-block of inducing inputs b, group g) takes the 64-row tiles of
+// the datapoints g, g + G, g + 2G, ...  Each E^T tile [64 m][64 n] is loaded
+// once (the next one is in flight while the current one is used) and read
+// twice from LDS.  Wave w owns the dimensions q = w, w + 4, w + 8, ...:
+//   columns: thread (m, w) adds E d and E d^2 over the tile's 64 n to
+//            registers kept over the workgroup's tiles -> colpart[g][m][2 Q];
+//   rows:    thread (n, w) sums E d over the block's 64 m -> dxpart[b][q][n];
+// and sum E per workgroup -> epart[g * nb + b] (dsf2).
+// A wave's dimensions sit in a slot of QP = QM/4 rounded up to the 16-byte
+// vector, so that each is read as whole vectors: xs and zs rows are
+// [64][4 slots][QP], zero in the padding.
+template <typename T>
+constexpr int chain_qp(int QM) { return (QM / 4 + Vec<T>::W - 1) / Vec<T>::W * Vec<T>::W; }
 
-// One thread per datapoint: dx_nq = -sum_m E^T[m][n] (xs_nq - zs_mq) / l_q
-// (coalesced over n, loads issued 16 at a time) and a per-block partial of
-// sum E (dsf2).
-template <typename T, int QM>
-__global__ __launch_bounds__(256) void known_rows_kernel(int64_t N, int M, int Q,
-                                                         const T *__restrict__ Et,
-                                                         const T *__restrict__ xs,
-                                                         const T *__restrict__ zs, Hyp<T> h,
-                                                         T *__restrict__ dX,
-                                                         T *__restrict__ rowpart) {
-    using V = typename Vec<T>::t;
-    constexpr int W = Vec<T>::W;
-    __shared__ __align__(16) T sz[kEdge][QM];  // zero beyond Q and beyond the block's rows
-    __shared__ T red4[4];
-    const int tid = threadIdx.x;
-    const int64_t n = (int64_t)blockIdx.x * 256 + tid;
-    const bool valid = n < N;
-    T r = 0, U[QM], x[QM];
-#pragma unroll
-    for (int q = 0; q < QM; ++q) {
-        U[q] = 0;
-        x[q] = (valid && q < Q) ? xs[n * Q + q] : T(0);
-    }
-    for (int mb = 0; mb < M; mb += kEdge) {
-        const int cnt = min(kEdge, M - mb);
-        __syncthreads();
-        for (int i = tid; i < kEdge * QM; i += 256) {
-            const int c = i / QM, q = i - c * QM;
-            sz[c][q] = (c < cnt && q < Q) ? zs[(int64_t)(mb + c) * Q + q] : T(0);
-        }
-        __syncthreads();
-        if (valid) {
-            for (int c0 = 0; c0 < cnt; c0 += 16) {
-                T e[16];
-#pragma unroll
-                for (int j = 0; j < 16; ++j)
-                    e[j] = c0 + j < cnt ? Et[(int64_t)(mb + c0 + j) * N + n] : T(0);
-#pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    r += e[j];
-                    const V *zr = reinterpret_cast<const V *>(&sz[c0 + j][0]);
-#pragma unroll
-                    for (int v = 0; v < QM / W; ++v) {
-                        const V z = zr[v];
-#pragma unroll
-                        for (int w = 0; w < W; ++w)
-                            U[v * W + w] = fma(e[j], x[v * W + w] - z[w], U[v * W + w]);
-                    }
-                }
-            }
-        }
-    }
-    if (valid) {
-#pragma unroll
-        for (int q = 0; q < QM; ++q)
-            if (q < Q) dX[n * Q + q] = -U[q] / h.l[q];
-    }
-    const T sr = block_sum(valid ? r : T(0), red4);
-    if (tid == 0) rowpart[blockIdx.x] = sr;
+template <typename T>
+size_t chain_lds_bytes(int QM) {  // sx [64][4][QP], sz [64][4][QP], se [64][65], red4
+    return sizeof(T) * (2 * (size_t)kEdge * 4 * chain_qp<T>(QM) + (size_t)kEdge * (kEdge + 1) + 4);
 }
 
-// One workgroup per (64 inducing inputs, row chunk), E^T tiles staged in LDS:
-// per inducing input m the chunk's sum_n E (xs_nq - zs_mq) (dZ) and
-// sum_n E (xs_nq - zs_mq)^2 (dl) -> colpart[chunk][m][2 Q].
-template <typename T, int QM>
-__global__ __launch_bounds__(256) void known_cols_kernel(int64_t N, int M, int Q, int64_t rows,
-                                                         const T *__restrict__ Et,
-                                                         const T *__restrict__ xs,
-                                                         const T *__restrict__ zs,
-                                                         T *__restrict__ colpart) {
+template <typename T, int QM, bool VEC>
+__global__ __launch_bounds__(256) void known_chain_kernel(int64_t N, int M, int Q, int64_t tiles,
+                                                          int64_t G, const T *__restrict__ Et,
+                                                          const T *__restrict__ xs,
+                                                          const T *__restrict__ zs,
+                                                          T *__restrict__ dxpart,
+                                                          T *__restrict__ colpart,
+                                                          T *__restrict__ epart) {
     using Vv = typename Vec<T>::t;
     constexpr int W = Vec<T>::W;
-    __shared__ T se[kEdge][kEdge + 1];         // E^T tile [m][n], zero outside
-    __shared__ __align__(16) T sx[kEdge][QM];  // xs rows of the tile, zero outside
-    __shared__ T red[4][kEdge];
-    const int tid = threadIdx.x;
-    const int m0 = blockIdx.x * kEdge;
-    const int64_t r0 = (int64_t)blockIdx.y * rows, r1 = min(N, r0 + rows);
-    const int mr = tid & 63, quarter = tid >> 6;
-    const int m = m0 + mr;
-    T V[QM], D[QM], z[QM];
-#pragma unroll
-    for (int q = 0; q < QM; ++q) {
-        V[q] = D[q] = 0;
-        z[q] = (m < M && q < Q) ? zs[(int64_t)m * Q + q] : T(0);
+    constexpr int RV = kEdge / W;               // vectors per tile row
+    constexpr int EV = kEdge * RV / 256;        // tile vectors per thread
+    constexpr int XP = kEdge * QM / 256;        // xs tile elements per thread
+    constexpr int QC = QM / 4;                  // dimensions per thread
+    constexpr int QP = chain_qp<T>(QM);         // their padded slot
+    constexpr int RS = 4 * QP;                  // xs / zs row stride in LDS
+    static_assert(QM % 4 == 0, "QM is a multiple of 4");
+    extern __shared__ __align__(16) unsigned char chain_smem[];
+    T *sx = reinterpret_cast<T *>(chain_smem);  // [64][4][QP]
+    T *sz = sx + kEdge * RS;                    // [64][4][QP]
+    T *se = sz + kEdge * RS;                    // [64][65], E^T tile [m][n]
+    T *red4 = se + kEdge * (kEdge + 1);         // [4]
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int blk = blockIdx.x, nbk = gridDim.x;
+    const int64_t g = blockIdx.y;
+    const int m0 = blk * kEdge;
+
+    // slot w, entry i holds dimension q = w + 4 i (zero where q >= Q and in the padding)
+    for (int i = tid; i < kEdge * RS; i += 256) {
+        const int r = i / RS, k = i - r * RS, w = k / QP, j = k - w * QP, q = w + 4 * j;
+        sz[i] = (m0 + r < M && j < QC && q < Q) ? zs[(int64_t)(m0 + r) * Q + q] : T(0);
+        sx[i] = T(0);
     }
-    for (int64_t nb = r0; nb < r1; nb += kEdge) {
-        const int cnt = (int)min<int64_t>(kEdge, r1 - nb);
-        __syncthreads();
-        for (int i = tid; i < kEdge * kEdge; i += 256) {
-            const int row = i >> 6, col = i & 63;
-            const int mm = m0 + row;
-            se[row][col] = (mm < M && col < cnt) ? Et[(int64_t)mm * N + nb + col] : T(0);
+    __syncthreads();
+    T zq[QC], Vc[QC], Dc[QC];
+#pragma unroll
+    for (int i = 0; i < QC; ++i) {
+        zq[i] = sz[lane * RS + wv * QP + i];
+        Vc[i] = Dc[i] = 0;
+    }
+    T esum = 0;
+
+    Vv ev[EV];
+    T xv[XP];
+    auto load = [&](int64_t t) {
+        const int64_t n0 = t * kEdge;
+#pragma unroll
+        for (int u = 0; u < EV; ++u) {
+            const int f = tid + 256 * u;
+            const int row = f / RV, cv = (f - row * RV) * W;
+            const int m = m0 + row;
+            const int64_t n = n0 + cv;
+            if (VEC && m < M && n + W <= N) {
+                ev[u] = *reinterpret_cast<const Vv *>(Et + (int64_t)m * N + n);
+            } else {
+#pragma unroll
+                for (int w = 0; w < W; ++w)
+                    ev[u][w] = (m < M && n + w < N) ? Et[(int64_t)m * N + n + w] : T(0);
+            }
         }
-        for (int i = tid; i < kEdge * QM; i += 256) {
-            const int rr = i / QM, q = i - rr * QM;
-            sx[rr][q] = (rr < cnt && q < Q) ? xs[(nb + rr) * Q + q] : T(0);
+#pragma unroll
+        for (int u = 0; u < XP; ++u) {
+            const int f = tid + 256 * u;
+            const int r = f / QM, q = f - r * QM;
+            xv[u] = (n0 + r < N && q < Q) ? xs[(n0 + r) * Q + q] : T(0);
+        }
+    };
+    if (g < tiles) load(g);
+    for (int64_t t = g; t < tiles; t += G) {
+        __syncthreads();  // the previous tile's LDS reads are done
+#pragma unroll
+        for (int u = 0; u < EV; ++u) {
+            const int f = tid + 256 * u;
+            const int row = f / RV, cv = (f - row * RV) * W;
+#pragma unroll
+            for (int w = 0; w < W; ++w) se[row * (kEdge + 1) + cv + w] = ev[u][w];
+        }
+#pragma unroll
+        for (int u = 0; u < XP; ++u) {
+            const int f = tid + 256 * u;
+            const int r = f / QM, q = f - r * QM;
+            sx[r * RS + (q & 3) * QP + (q >> 2)] = xv[u];
         }
         __syncthreads();
+        if (t + G < tiles) load(t + G);
+        // columns: m = m0 + lane over the tile's 64 n
 #pragma unroll 4
-        for (int j = 0; j < 16; ++j) {
-            const int col = quarter * 16 + j;
-            const T e = se[mr][col];
-            const Vv *xr = reinterpret_cast<const Vv *>(&sx[col][0]);
+        for (int c = 0; c < kEdge; ++c) {
+            const T e = se[lane * (kEdge + 1) + c];
+            T xr[QP];
 #pragma unroll
-            for (int v = 0; v < QM / W; ++v) {
-                const Vv xv = xr[v];
+            for (int v = 0; v < QP / W; ++v) {
+                const Vv xq = reinterpret_cast<const Vv *>(sx + c * RS + wv * QP)[v];
 #pragma unroll
-                for (int w = 0; w < W; ++w) {
-                    const int q = v * W + w;
-                    const T d = xv[w] - z[q];
-                    const T t = e * d;
-                    V[q] += t;
-                    D[q] = fma(t, d, D[q]);
-                }
+                for (int w = 0; w < W; ++w) xr[v * W + w] = xq[w];
+            }
+#pragma unroll
+            for (int i = 0; i < QC; ++i) {
+                const T d = xr[i] - zq[i];
+                const T te = e * d;
+                Vc[i] += te;
+                Dc[i] = fma(te, d, Dc[i]);
+            }
+        }
+        // rows: n = n0 + lane over the block's 64 m
+        T x[QC], U[QC];
+#pragma unroll
+        for (int i = 0; i < QC; ++i) {
+            x[i] = sx[lane * RS + wv * QP + i];
+            U[i] = 0;
+        }
+#pragma unroll 4
+        for (int r = 0; r < kEdge; ++r) {
+            const T e = se[r * (kEdge + 1) + lane];
+            if (wv == 0) esum += e;
+            T zr[QP];
+#pragma unroll
+            for (int v = 0; v < QP / W; ++v) {
+                const Vv zv = reinterpret_cast<const Vv *>(sz + r * RS + wv * QP)[v];
+#pragma unroll
+                for (int w = 0; w < W; ++w) zr[v * W + w] = zv[w];
+            }
+#pragma unroll
+            for (int i = 0; i < QC; ++i) U[i] = fma(e, x[i] - zr[i], U[i]);
+        }
+        const int64_t n = t * kEdge + lane;
+        if (n < N) {
+#pragma unroll
+            for (int i = 0; i < QC; ++i) {
+                const int q = wv + 4 * i;
+                if (q < Q) dxpart[((int64_t)blk * Q + q) * N + n] = U[i];
             }
         }
     }
+    const int m = m0 + lane;
+    if (m < M && g < tiles) {
 #pragma unroll
-    for (int k = 0; k < 2 * QM; ++k) {
-        const int q = k < QM ? k : k - QM;
-        if (q < Q) {
-            __syncthreads();
-            red[quarter][mr] = k < QM ? V[q] : D[q];
-            __syncthreads();
-            if (quarter == 0 && m < M)
-                colpart[((int64_t)blockIdx.y * M + m) * (2 * Q) + (k < QM ? q : Q + q)] =
-                    ((red[0][mr] + red[1][mr]) + red[2][mr]) + red[3][mr];
+        for (int i = 0; i < QC; ++i) {
+            const int q = wv + 4 * i;
+            if (q < Q) {
+                colpart[(g * M + m) * (2 * Q) + q] = Vc[i];
+                colpart[(g * M + m) * (2 * Q) + Q + q] = Dc[i];
+            }
         }
+    }
+    const T se_all = block_sum(esum, red4);
+    if (tid == 0) epart[g * nbk + blk] = se_all;
+}
+
+// dX = -(sum over the inducing-input blocks of dxpart, in block order) / l.
+// One workgroup per 64 datapoints: the sums are read coalesced over n from
+// dxpart [b][q][n] and written through an LDS transpose as the block's 64 Q
+// contiguous elements of dX.
+template <typename T>
+__global__ __launch_bounds__(256) void known_dx_kernel(int64_t N, int Q, int nbk,
+                                                       const T *__restrict__ dxpart, Hyp<T> h,
+                                                       T *__restrict__ dX) {
+    __shared__ T tile[kEdge][GPPS_MAX_Q + 1];
+    const int tid = threadIdx.x, nn = tid & 63;
+    const int64_t n0 = (int64_t)blockIdx.x * kEdge, n = n0 + nn;
+    const int cnt = (int)min<int64_t>(kEdge, N - n0);
+    if (n < N) {
+        for (int q = tid >> 6; q < Q; q += 4) {
+            T s = 0;
+            for (int b = 0; b < nbk; ++b) s += dxpart[((int64_t)b * Q + q) * N + n];
+            tile[nn][q] = -s / h.l[q];
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < cnt * Q; i += 256) {
+        const int r = i / Q, q = i - r * Q;
+        dX[n0 * Q + i] = tile[r][q];
     }
 }
 
-// One workgroup per inducing input m: Vc[m][k] = sum over the column chunks of
-// colpart[chunk][m][k], k < 2 Q.  G = 256 / (2 Q) groups of 2 Q threads take
-// chunks g, g + G, ... (coalesced over k); the G partials are added in order.
+// One workgroup per inducing input m: Vc[m][k] = sum over the chain kernel's
+// tile groups of colpart[group][m][k], k < 2 Q.  S = 256 / (2 Q) sets of 2 Q
+// threads take groups s, s + S, ... (coalesced over k); the S partials are
+// added in order.
 template <typename T>
-__global__ __launch_bounds__(256) void known_col_reduce_kernel(int M, int Q, int64_t cchunks,
+__global__ __launch_bounds__(256) void known_col_reduce_kernel(int M, int Q, int64_t groups,
                                                                const T *__restrict__ colpart,
                                                                T *__restrict__ Vc) {
     __shared__ T part[256];
-    const int t = threadIdx.x, K = 2 * Q, G = 256 / K;
+    const int t = threadIdx.x, K = 2 * Q, S = 256 / K;
     const int64_t m = blockIdx.x;
-    if (t < G * K) {
-        const int g = t / K, k = t - g * K;
+    if (t < S * K) {
+        const int j = t / K, k = t - j * K;
         T s = 0;
-        for (int64_t c = g; c < cchunks; c += G) s += colpart[(c * M + m) * K + k];
+        for (int64_t c = j; c < groups; c += S) s += colpart[(c * M + m) * K + k];
         part[t] = s;
     }
     __syncthreads();
     if (t < K) {
         T s = 0;
-        for (int g = 0; g < G; ++g) s += part[g * K + t];
+        for (int j = 0; j < S; ++j) s += part[j * K + t];
         Vc[m * K + t] = s;
     }
 }
 
 // dZ[m][q] = Vc[m][q] / l_q elementwise (blocks below zblocks), then one
 // workgroup per dl_q (sum_m Vc[m][Q + q] / l_q) and one for dsf2 (sum E / sf2 +
-// N dL/dpsi0), each a fixed-order block sum.
+// N dL/dpsi0, sum E from the chain kernel's nep partials), each a fixed-order
+// block sum.
 template <typename T>
 __global__ __launch_bounds__(256) void known_grad_final_kernel(
-    int64_t N, int M, int Q, int64_t zblocks, int64_t rblocks, const T *__restrict__ Vc,
-    const T *__restrict__ rowpart, Hyp<T> h, T dL_dpsi0, T *__restrict__ dZ, T *__restrict__ dsf2,
+    int64_t N, int M, int Q, int64_t zblocks, int64_t nep, const T *__restrict__ Vc,
+    const T *__restrict__ epart, Hyp<T> h, T dL_dpsi0, T *__restrict__ dZ, T *__restrict__ dsf2,
     T *__restrict__ dl, int accumulate) {
     __shared__ T red4[4];
     const int64_t K = 2 * Q;
@@ -712,7 +787,7 @@ __global__ __launch_bounds__(256) void known_grad_final_kernel(
     if (k < Q)
         for (int m = threadIdx.x; m < M; m += 256) s += Vc[(int64_t)m * K + Q + k];
     else
-        for (int64_t b = threadIdx.x; b < rblocks; b += 256) s += rowpart[b];
+        for (int64_t b = threadIdx.x; b < nep; b += 256) s += epart[b];
     s = block_sum(s, red4);
     if (threadIdx.x == 0) {
         if (k < Q) dl[k] = (accumulate ? dl[k] : T(0)) + s / h.l[k];
@@ -726,7 +801,7 @@ void launch_centre_kfu(const Shape &s, const KPlan &p, const T *X, const T *Z, c
     T *cz = at<T>(ws, p.off_cz), *zs = at<T>(ws, p.off_zs), *xs = at<T>(ws, p.off_xs);
     {
         TimedScope ts(st, "known_centre");
-        known_centre_kernel<T><<<1, 256, 0, st>>>((int)s.M, (int)s.Q, Z, h, cz, zs);
+        known_centre_kernel<T><<<1, 1024, 0, st>>>((int)s.M, (int)s.Q, Z, h, cz, zs);
     }
     dim3 grid((unsigned)cdiv(s.N, kEdge), (unsigned)cdiv(s.M, kEdge));
     const size_t lds = 2 * kEdge * s.Q * sizeof(T);
@@ -738,17 +813,30 @@ void launch_centre_kfu(const Shape &s, const KPlan &p, const T *X, const T *Z, c
 }
 
 template <typename T, int QM>
-void launch_chain(const Shape &s, const KPlan &p, const T *Et, const Hyp<T> &h, T *dX, void *ws,
-                  hipStream_t st) {
+hipError_t launch_chain(const Shape &s, const KPlan &p, const T *Et, const Hyp<T> &h, T *dX,
+                        void *ws, hipStream_t st, int64_t &G) {
     const T *xs = at<T>(ws, p.off_xs), *zs = at<T>(ws, p.off_zs);
+    // workspace rows of E^T start on 16 bytes when N is a multiple of the vector
+    auto k = s.N % Vec<T>::W == 0 ? known_chain_kernel<T, QM, true> : known_chain_kernel<T, QM, false>;
+    const size_t lds = chain_lds_bytes<T>(QM);
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    int dev = 0, cus = 0, occ = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, k, 256, lds)) != hipSuccess) return e;
+    // one round of resident workgroups over the inducing-input blocks
+    G = std::max<int64_t>(1, std::min<int64_t>(p.gmax, (int64_t)std::max(1, occ) * cus / p.nb));
     {
-        TimedScope ts(st, "known_rows");
-        known_rows_kernel<T, QM><<<(unsigned)p.rblocks, 256, 0, st>>>(
-            s.N, (int)s.M, (int)s.Q, Et, xs, zs, h, dX, at<T>(ws, p.off_rowp));
+        TimedScope ts(st, "known_chain");
+        k<<<dim3((unsigned)p.nb, (unsigned)G), 256, lds, st>>>(
+            s.N, (int)s.M, (int)s.Q, p.tiles, G, Et, xs, zs, at<T>(ws, p.off_dxp),
+            at<T>(ws, p.off_colp), at<T>(ws, p.off_ep));
     }
-    TimedScope ts(st, "known_cols");
-    known_cols_kernel<T, QM><<<dim3((unsigned)p.nb, (unsigned)p.cchunks), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, p.crows, Et, xs, zs, at<T>(ws, p.off_colp));
+    TimedScope ts(st, "known_dx");
+    known_dx_kernel<T><<<(unsigned)p.tiles, 256, 0, st>>>(s.N, (int)s.Q, (int)p.nb,
+                                                         at<T>(ws, p.off_dxp), h, dX);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -805,23 +893,26 @@ hipError_t known_psi_grads(const Shape &s, const T *X, const T *Z, const Hyp<T> 
         known_dkfu_kernel<T, false, false><<<grid, 256, 0, st>>>(s.N, (int)s.M, nblk, mb, Kt, G1, nullptr,
                                                                  Et);
     }
-    // the chain kernels pad Q to QM (a multiple of the 16-byte vector)
-    if (s.Q <= 4) launch_chain<T, 4>(s, p, Et, h, dX, ws, st);
-    else if (s.Q <= 8) launch_chain<T, 8>(s, p, Et, h, dX, ws, st);
-    else if (s.Q <= 12) launch_chain<T, 12>(s, p, Et, h, dX, ws, st);
-    else if (s.Q <= 16) launch_chain<T, 16>(s, p, Et, h, dX, ws, st);
-    else if (s.Q <= 20) launch_chain<T, 20>(s, p, Et, h, dX, ws, st);
-    else if (s.Q <= 24) launch_chain<T, 24>(s, p, Et, h, dX, ws, st);
-    else if (s.Q <= 32) launch_chain<T, 32>(s, p, Et, h, dX, ws, st);
-    else if (s.Q <= 48) launch_chain<T, 48>(s, p, Et, h, dX, ws, st);
-    else launch_chain<T, 64>(s, p, Et, h, dX, ws, st);
+    // the chain kernel pads Q to QM (a multiple of 4)
+    int64_t G = 1;
+    hipError_t e;
+    if (s.Q <= 4) e = launch_chain<T, 4>(s, p, Et, h, dX, ws, st, G);
+    else if (s.Q <= 8) e = launch_chain<T, 8>(s, p, Et, h, dX, ws, st, G);
+    else if (s.Q <= 12) e = launch_chain<T, 12>(s, p, Et, h, dX, ws, st, G);
+    else if (s.Q <= 16) e = launch_chain<T, 16>(s, p, Et, h, dX, ws, st, G);
+    else if (s.Q <= 20) e = launch_chain<T, 20>(s, p, Et, h, dX, ws, st, G);
+    else if (s.Q <= 24) e = launch_chain<T, 24>(s, p, Et, h, dX, ws, st, G);
+    else if (s.Q <= 32) e = launch_chain<T, 32>(s, p, Et, h, dX, ws, st, G);
+    else if (s.Q <= 48) e = launch_chain<T, 48>(s, p, Et, h, dX, ws, st, G);
+    else e = launch_chain<T, 64>(s, p, Et, h, dX, ws, st, G);
+    if (e != hipSuccess) return e;
     TimedScope ts(st, "known_grad_reduce");
     T *Vc = at<T>(ws, p.off_vc);
-    known_col_reduce_kernel<T><<<(unsigned)s.M, 256, 0, st>>>((int)s.M, (int)s.Q, p.cchunks,
+    known_col_reduce_kernel<T><<<(unsigned)s.M, 256, 0, st>>>((int)s.M, (int)s.Q, G,
                                                              at<T>(ws, p.off_colp), Vc);
     const int64_t zblocks = cdiv(s.M * s.Q, 256);
     known_grad_final_kernel<T><<<(unsigned)(zblocks + s.Q + 1), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, zblocks, p.rblocks, Vc, at<T>(ws, p.off_rowp), h, dL_dpsi0, dZ,
+        s.N, (int)s.M, (int)s.Q, zblocks, p.nb * G, Vc, at<T>(ws, p.off_ep), h, dL_dpsi0, dZ,
         dsf2, dl, accumulate);
     return hipGetLastError();
 }

@@ -30,6 +30,7 @@ constexpr int kRowTile = 32;     // rows staged in LDS at a time
 constexpr int kPairTile = 16;    // pair tile edge (16 x 16 threads)
 constexpr int kRowBlock = 64;    // threads (rows) per block in the gradient row kernel
 constexpr int kColBlock = 64;    // threads (inducing inputs) per block in the column kernel
+constexpr int kBand = 8;         // symmetric pairs kernel: pair offsets k per LDS exchange
 
 __device__ inline float dexp(float x) { return __expf(x); }
 __device__ inline double dexp(double x) { return exp(x); }
@@ -51,10 +52,12 @@ struct Plan {
     int64_t rr;                      // row kernel: ranges of pair rows m (m = r mod rr)
     int64_t cr;                      // column kernel: ranges of partners m'
     bool pairs;                      // gradients by grad_pairs_kernel (Z table fits in LDS)
+    bool psym;                       // ... in its symmetric form (one workgroup spans all of M)
     int pthreads;                    // pairs kernel: threads (inducing inputs) per workgroup
     int64_t pmb, pchunks, prows;     // pairs kernel: m-blocks, row chunks, rows per chunk
     // workspace offsets in bytes
-    size_t off_w1, off_w2, off_lp1, off_lp2, off_p2, off_g2s, off_colp, off_rowp, off_rowg, total;
+    size_t off_w1, off_w2, off_lp1, off_lp2, off_p2, off_g2s, off_gc, off_colp, off_rowp, off_rowg,
+        total;
 };
 
 Plan make_plan(const Shape &s, size_t elem) {
@@ -85,6 +88,9 @@ Plan make_plan(const Shape &s, size_t elem) {
     p.pchunks = std::max<int64_t>(1, std::min<int64_t>(s.N, 2048 / p.pmb));
     p.prows = cdiv(s.N, p.pchunks);
     p.pchunks = cdiv(s.N, p.prows);
+    // symmetric form: every pair exchange stays inside one workgroup, and the Z
+    // table plus two bands of kBand x M pair values fit in LDS
+    p.psym = p.pairs && p.pmb == 1 && (pairs_qm(s.Q) + 2 * kBand) * s.M * elem <= 65536;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_w1 = take(elem * s.N * s.Q);
@@ -93,6 +99,7 @@ Plan make_plan(const Shape &s, size_t elem) {
     p.off_lp2 = take(elem * s.N);
     p.off_p2 = take(elem * p.nc2 * s.P);
     p.off_g2s = take(elem * s.M * s.M);
+    p.off_gc = take(elem * (s.M / 2 + 1) * s.M);
     p.off_colp = take(elem * std::max(p.ncc * p.cr, p.pchunks) * s.M * s.Q);
     p.off_rowp = take(elem * std::max(p.rr * p.row_blocks, p.pmb * p.pchunks) * (s.Q + 1));
     p.off_rowg = take(elem * std::max(p.rr, p.pmb) * s.N * s.Q * 2);
@@ -233,6 +240,18 @@ __global__ void sym_kernel(int M, const T *__restrict__ G2, T *__restrict__ G2s)
     G2s[i] = T(0.5) * (G2[(int64_t)m * M + mp] + G2[(int64_t)mp * M + m]);
 }
 
+// Gc[k][m] = G2s[m][(m + k) mod M], k = 0 .. M/2: the symmetric pairs kernel
+// reads the pair (m, m + k) of every thread m as one coalesced row.
+template <typename T>
+__global__ void circ_kernel(int M, const T *__restrict__ G2s, T *__restrict__ Gc) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)(M / 2 + 1) * M) return;
+    const int k = (int)(i / M), m = (int)(i - (int64_t)k * M);
+    int mp = m + k;
+    if (mp >= M) mp -= M;
+    Gc[i] = G2s[(int64_t)m * M + mp];
+}
+
 // One thread per datapoint and range r of pair rows (m = r, r + rr, ...; the
 // Psi1 terms in the column tiles t = r, r + rr, ...): partial dmu_n, dS_n of the
 // range (rowg[r][2][N][Q]) and per-block partials of dl and dsf2.
@@ -369,19 +388,26 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
 //             + t (S w1 / l + l d^2 w1^2)
 //   dsf2   += (2 r + t) / sf2.
 // One workgroup per (block of inducing inputs, row chunk), one thread per m, the
-// Z table in LDS: each exponential is evaluated once per ordered (n, m, m'),
-// dZ_m stays in the thread's registers over the chunk, and per row the dmu / dS
-// contributions are summed over the block's m (wave butterflies, then the waves
-// in order) into rowg[m-block][2][N][Q].
-template <typename T, int QM>
+// Z table in LDS: dZ_m stays in the thread's registers over the chunk, and per
+// row the dmu / dS contributions are summed over the block's m (wave
+// butterflies, then the waves in order) into rowg[m-block][2][N][Q].
+// Ordered form (SYM = false): thread m evaluates W for every (m, m').
+// Symmetric form (SYM = true, the workgroup holds all M): each unordered pair
+// is evaluated once.  Thread m takes the pairs (m, m + k mod M) for k = 0 ..
+// M/2 (k = M/2 only for m < M/2 when M is even), so every thread has the same
+// load; it adds W to its own r and V and leaves it in an LDS band, from which
+// thread m + k adds it to its r and V.  The bands hold kBand offsets and are
+// double buffered: one barrier per band.
+template <typename T, int QM, bool SYM>
 __global__ __launch_bounds__(256) void grad_pairs_kernel(
     int64_t N, int M, int Q, int64_t rows_per_chunk, const T *__restrict__ mu,
     const T *__restrict__ S, const T *__restrict__ Z, const T *__restrict__ w1t,
     const T *__restrict__ w2t, const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h,
-    const T *__restrict__ G1, const T *__restrict__ G2s, T *__restrict__ rowg,
-    T *__restrict__ colpart, T *__restrict__ rowpart) {
+    const T *__restrict__ G1, const T *__restrict__ G2s, const T *__restrict__ Gc,
+    T *__restrict__ rowg, T *__restrict__ colpart, T *__restrict__ rowpart) {
     extern __shared__ double gp_smem[];
     T *sz = reinterpret_cast<T *>(gp_smem);  // [M][QM], zero beyond Q
+    T *band = sz + M * QM;                    // [2][kBand][M] (symmetric form)
     __shared__ T red[2][4][2 * QM];           // per-wave row sums, double buffered by row
     const int tid = threadIdx.x, nthr = blockDim.x, nw = nthr >> 6, wv = tid >> 6;
     const int m = blockIdx.x * nthr + tid;
@@ -400,6 +426,11 @@ __global__ __launch_bounds__(256) void grad_pairs_kernel(
         gz[q] = gl[q] = 0;
     }
     T gsf = 0;
+    const int K = M / 2;
+    const bool even = (M & 1) == 0;
+    const int Ku = even ? K - 1 : K;  // offsets taken by every thread
+    int band_no = 0;
+    const T gdiag = (SYM && valid) ? Gc[m] : T(0);  // G2s[m][m], the same for every row
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk, r1 = min(N, r0 + rows_per_chunk);
     for (int64_t n = r0; n < r1; ++n) {
         T x[QM], a1[QM], a2[QM], sv[QM], d[QM];
@@ -415,23 +446,82 @@ __global__ __launch_bounds__(256) void grad_pairs_kernel(
         T r = 0, V[QM];
 #pragma unroll
         for (int q = 0; q < QM; ++q) V[q] = 0;
-        if (G2s && valid) {
-            const T base = lp2[n];
-            for (int mp = 0; mp < M; ++mp) {
-                const T g = G2s[(int64_t)mp * M + m];  // G2s symmetric: a coalesced row
-                const T *zr = sz + mp * QM;
-                T e = base;
+        // W_n[m, m'] = G2s[m, m'] Psi2_n[m, m'] for the partner m' (z row zr).
+        // With v = z_m' - z_m and d = mu_n - z_m the exponent
+        //   log Psi2 - log prefactor = -sum_q [c4 v^2 + (a2/4)(2 d - v)^2]
+        // is a quadratic in v with per-(n, m) coefficients:
+        //   e0 + sum_q v (a2 d - (c4 + a2/4) v),  e0 = lp2 - sum_q a2 d^2.
+        // Where W is not negligible (exponent above about -30) each of its terms
+        // is bounded by a few hundred, so the rounding stays near that of the
+        // summed squares.
+        T bq[QM], cq[QM], e0 = G2s ? lp2[n] : T(0);
 #pragma unroll
-                for (int q = 0; q < QM; ++q) {
-                    const T dz = z[q] - zr[q];
-                    const T s2 = d[q] + (x[q] - zr[q]);
-                    e -= dz * dz * c4[q] + s2 * s2 * (T(0.25) * a2[q]);
-                }
-                const T W = g * dexp(e);
-                r += W;
+        for (int q = 0; q < QM; ++q) {
+            bq[q] = a2[q] * d[q];
+            cq[q] = c4[q] + T(0.25) * a2[q];
+            e0 -= bq[q] * d[q];
+        }
+        auto pair_w = [&](const T *zr, T g, T e00) {
+            T e = e00;
 #pragma unroll
-                for (int q = 0; q < QM; ++q) V[q] += W * (x[q] - zr[q]);
+            for (int q = 0; q < QM; ++q) {
+                const T v = zr[q] - z[q];
+                e = fma(v, fma(-cq[q], v, bq[q]), e);
             }
+            return g * dexp(e);
+        };
+        auto add_w = [&](T W, const T *zr) {
+            r += W;
+#pragma unroll
+            for (int q = 0; q < QM; ++q) V[q] += W * (x[q] - zr[q]);
+        };
+        if (SYM) {
+            if (G2s) {  // uniform: every thread reaches the band barriers
+                if (valid) add_w(pair_w(sz + m * QM, gdiag, e0), sz + m * QM);
+                // offsets every thread takes (1 .. Ku), in bands; then, for even
+                // M, the offset M/2 of the first half
+                for (int k0 = 1; k0 <= Ku; k0 += kBand, ++band_no) {
+                    T *bs = band + (band_no & 1) * (kBand * M);
+                    const int k1 = min(Ku, k0 + kBand - 1);
+                    if (valid) {
+                        int mp = m + k0;
+                        if (mp >= M) mp -= M;
+                        const T *gk = Gc + (int64_t)k0 * M + m;
+#pragma unroll 2
+                        for (int k = k0; k <= k1; ++k) {
+                            const T W = pair_w(sz + mp * QM, *gk, e0);
+                            add_w(W, sz + mp * QM);
+                            bs[(k - k0) * M + m] = W;
+                            gk += M;
+                            mp = mp + 1 == M ? 0 : mp + 1;
+                        }
+                    }
+                    __syncthreads();
+                    if (valid) {
+                        int sp = m - k0;
+                        if (sp < 0) sp += M;
+#pragma unroll 4
+                        for (int k = k0; k <= k1; ++k) {
+                            add_w(bs[(k - k0) * M + sp], sz + sp * QM);
+                            sp = sp == 0 ? M - 1 : sp - 1;
+                        }
+                    }
+                }
+                if (even && K > 0) {
+                    T *bs = band + (band_no & 1) * (kBand * M);
+                    ++band_no;
+                    if (valid && m < K) {
+                        const T W = pair_w(sz + (m + K) * QM, Gc[(int64_t)K * M + m], e0);
+                        add_w(W, sz + (m + K) * QM);
+                        bs[m] = W;
+                    }
+                    __syncthreads();
+                    if (valid && m >= K) add_w(bs[m - K], sz + (m - K) * QM);
+                }
+            }
+        } else if (G2s && valid) {
+            for (int mp = 0; mp < M; ++mp)  // G2s symmetric: G2s[mp][m] is a coalesced row
+                add_w(pair_w(sz + mp * QM, G2s[(int64_t)mp * M + m], e0), sz + mp * QM);
         }
         T t = 0;
         if (G1 && valid) {
@@ -722,14 +812,27 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
     T *colpart = at<T>(ws, p.off_colp), *rowpart = at<T>(ws, p.off_rowp);
     T *rowg = at<T>(ws, p.off_rowg);
     if (p.pairs) {
-        const size_t lds = sizeof(T) * s.M * pairs_qm(s.Q);
+        const bool sym = p.psym && G2s;
+        T *Gc = at<T>(ws, p.off_gc);
+        if (sym) {
+            TimedScope ts(st, "generic_circ");
+            circ_kernel<T><<<(unsigned)cdiv((s.M / 2 + 1) * s.M, 256), 256, 0, st>>>((int)s.M, G2s, Gc);
+        }
+        const size_t lds = sizeof(T) * s.M * (pairs_qm(s.Q) + (sym ? 2 * kBand : 0));
         dim3 grid((unsigned)p.pmb, (unsigned)p.pchunks);
         {
             TimedScope ts(st, "generic_grad_pairs");
-#define GPPS_PAIRS(QMV)                                                                          \
-    grad_pairs_kernel<T, QMV><<<grid, p.pthreads, lds, st>>>(s.N, (int)s.M, (int)s.Q, p.prows,  \
-                                                            mu, S, Z, w1, w2, lp1, lp2, h, G1,  \
-                                                            G2s, rowg, colpart, rowpart)
+#define GPPS_PAIRS(QMV)                                                                            \
+    do {                                                                                           \
+        if (sym)                                                                                   \
+            grad_pairs_kernel<T, QMV, true><<<grid, p.pthreads, lds, st>>>(                        \
+                s.N, (int)s.M, (int)s.Q, p.prows, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, Gc,      \
+                rowg, colpart, rowpart);                                                           \
+        else                                                                                       \
+            grad_pairs_kernel<T, QMV, false><<<grid, p.pthreads, lds, st>>>(                       \
+                s.N, (int)s.M, (int)s.Q, p.prows, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, Gc,      \
+                rowg, colpart, rowpart);                                                           \
+    } while (0)
             switch (pairs_qm(s.Q)) {
                 case 1: GPPS_PAIRS(1); break;
                 case 2: GPPS_PAIRS(2); break;

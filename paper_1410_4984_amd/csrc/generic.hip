@@ -43,7 +43,8 @@ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t pairs_qm(int64_t Q) { return Q <= 1 ? 1 : Q <= 2 ? 2 : Q <= 4 ? 4 : Q <= 8 ? 8 : 16; }
 
 struct Plan {
-    int64_t tiles_edge, tiles;       // pair tiles per edge and upper-triangle tile count
+    int64_t tiles_edge;              // pair tiles per edge (Psi2 reduce)
+    int64_t pblocks;                 // forward: blocks of 256 unique pairs
     int64_t nc2;                     // row chunks of the Psi2 forward kernel
     int64_t rows2;                   // rows per chunk (forward)
     int64_t ncc, rowsc;              // column-kernel chunks and rows per chunk
@@ -63,9 +64,9 @@ struct Plan {
 Plan make_plan(const Shape &s, size_t elem) {
     Plan p{};
     p.tiles_edge = cdiv(s.M, kPairTile);
-    p.tiles = p.tiles_edge * (p.tiles_edge + 1) / 2;
+    p.pblocks = cdiv(s.P, 256);
     int64_t nc2 = cdiv(s.N, 256);
-    int64_t cap2 = std::max<int64_t>(1, 2048 / p.tiles);
+    int64_t cap2 = std::max<int64_t>(1, 2048 / p.pblocks);
     p.nc2 = std::max<int64_t>(1, std::min(nc2, cap2));
     p.rows2 = cdiv(s.N, p.nc2);
     p.nc2 = cdiv(s.N, p.rows2);
@@ -147,31 +148,39 @@ __global__ void psi1_kernel(int64_t N, int M, int Q, const T *__restrict__ mu,
     Psi1[i] = dexp(lp1[n] - T(0.5) * s);
 }
 
-__device__ inline void tile_coords(int64_t t, int64_t edge, int &ti, int &tj) {
-    int64_t r = 0;
-    while (t >= edge - r) { t -= edge - r; ++r; }
-    ti = (int)r;
-    tj = (int)(r + t);
-}
-
 __device__ inline int64_t pair_index(int64_t m, int64_t mp, int64_t M) {
     return m * M - m * (m - 1) / 2 + (mp - m);
 }
 
+// Inverse of pair_index: the pair (m, mp), m <= mp, at position t < M (M + 1) / 2
+// of the row-major upper triangle.  Row m starts at m (2M - m + 1) / 2; the
+// square-root estimate of m is corrected by exact integer tests.
+__device__ inline void pair_coords(int64_t t, int64_t M, int &m, int &mp) {
+    auto start = [&](int64_t r) { return r * (2 * M - r + 1) / 2; };
+    const double b = 2.0 * (double)M + 1.0;
+    int64_t r = (int64_t)((b - sqrt(fmax(b * b - 8.0 * (double)t, 0.0))) * 0.5);
+    r = r < 0 ? 0 : (r >= M ? M - 1 : r);
+    while (r > 0 && start(r) > t) --r;
+    while (r + 1 < M && start(r + 1) <= t) ++r;
+    m = (int)r;
+    mp = (int)(r + (t - start(r)));
+}
+
 // ---------------------------------------------------------------- Psi2 partials (Alg. 1, Phi)
+// One thread per unique pair (consecutive pairs of the row-major upper
+// triangle, so no lane idles below the diagonal) and row chunk.
 template <typename T, int QM>
 __global__ __launch_bounds__(256) void psi2_partial_kernel(
-    int64_t N, int M, int Q, int64_t P, int64_t rows_per_chunk, int64_t tiles_edge,
+    int64_t N, int M, int Q, int64_t P, int64_t rows_per_chunk,
     const T *__restrict__ mu, const T *__restrict__ Z, const T *__restrict__ w2,
     const T *__restrict__ lp2, Hyp<T> h, T *__restrict__ partial) {
     __shared__ T s_mu[kRowTile][QM];
     __shared__ T s_w2[kRowTile][QM];
     __shared__ T s_lp[kRowTile];
-    int ti, tj;
-    tile_coords(blockIdx.x, tiles_edge, ti, tj);
-    const int tx = threadIdx.x % kPairTile, ty = threadIdx.x / kPairTile;
-    const int m = ti * kPairTile + ty, mp = tj * kPairTile + tx;
-    const bool valid = m < M && mp < M && m <= mp;
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const bool valid = t < P;
+    int m = 0, mp = 0;
+    if (valid) pair_coords(t, M, m, mp);
     T zbar[QM];
     T C = 0;
 #pragma unroll
@@ -210,7 +219,7 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(
             }
         }
     }
-    if (valid) partial[(int64_t)blockIdx.y * P + pair_index(m, mp, M)] = acc;
+    if (valid) partial[(int64_t)blockIdx.y * P + t] = acc;
 }
 
 // Fixed-order sum of the chunk partials; writes both triangles and psi0.
@@ -728,10 +737,10 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(int64_t N, int M, int 
 template <typename T, int QM>
 void launch_psi2_partial(const Shape &s, const Plan &p, const T *mu, const T *Z, const T *w2,
                          const T *lp2, const Hyp<T> &h, T *partial, hipStream_t st) {
-    dim3 grid((unsigned)p.tiles, (unsigned)p.nc2);
+    dim3 grid((unsigned)p.pblocks, (unsigned)p.nc2);
     TimedScope ts(st, "generic_psi2_partial");
-    psi2_partial_kernel<T, QM><<<grid, 256, 0, st>>>(s.N, (int)s.M, (int)s.Q, s.P, p.rows2,
-                                                     p.tiles_edge, mu, Z, w2, lp2, h, partial);
+    psi2_partial_kernel<T, QM><<<grid, 256, 0, st>>>(s.N, (int)s.M, (int)s.Q, s.P, p.rows2, mu, Z,
+                                                     w2, lp2, h, partial);
 }
 
 template <typename T, int QM>

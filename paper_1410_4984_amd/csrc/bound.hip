@@ -213,50 +213,55 @@ __global__ void bound_psiy_reduce_kernel(int M, int Mp, int64_t D, int64_t chunk
     Psi[k] = s;
 }
 
-// Blocked Cholesky, panel step K for two matrices (blockIdx.y): every workgroup
-// factors the diagonal block A_KK = L_KK L_KK^T in LDS; workgroup I = K writes
-// L_KK (upper part zero) to the side buffer Dg (tile (K, K) is still being read
-// by the others; the update launch copies it in) and records the log
-// determinant of the block (the sum of the log pivots) and a flag when a pivot
-// is not positive; workgroups I > K write L_IK = A_IK L_KK^-T.  Thread (tx, ty) owns column tx of rows ty, ty + 8,
-// ty + 16, ty + 24.
-__global__ __launch_bounds__(256) void bound_chol_panel_kernel(int Mp, int K, double *__restrict__ A0,
-                                                               double *__restrict__ Dg,
-                                                               double *__restrict__ logdet) {
-    __shared__ double Lk[kB][kB + 1], X[kB][kB + 1];
-    __shared__ double piv[kB];
+// Lane l's value of v, read by every lane (l uniform).
+__device__ inline double lane_bcast(double v, int l) {
+    const long long u = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)u, l);
+    const int hi = __builtin_amdgcn_readlane((int)(u >> 32), l);
+    return __hiloint2double(hi, lo);
+}
+
+// Blocked Cholesky, panel step K: workgroup I = K + blockIdx.x of matrix
+// blockIdx.y factors the diagonal block A_KK = L_KK L_KK^T (unblocked,
+// right-looking) and, for I > K, solves X L_KK^T = A_IK in place.  One wave:
+// lane r holds row r of the block (lanes 32-63 repeat rows 0-31), so no step
+// needs a barrier; the pivot L_jj and the entries L_cj come from the owning
+// lanes by readlane.  Each element is updated in the same order as a column
+// sweep over j.  Workgroup K writes L_KK (zero above the diagonal) to the side
+// buffer Dg, since the others are still reading tile (K, K) (the update launch
+// copies it in), the sum of its log-pivots to logdet[K], and adds the count of
+// non-positive pivots to logdet[nbk].
+__global__ __launch_bounds__(64) void bound_chol_panel_kernel(int Mp, int K, double *__restrict__ A0,
+                                                              double *__restrict__ Dg,
+                                                              double *__restrict__ logdet) {
     const int I = K + blockIdx.x, mat = blockIdx.y, nbk = Mp / kB;
     double *A = A0 + (int64_t)mat * Mp * Mp;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-    for (int r = ty; r < kB; r += 8) Lk[r][tx] = A[(int64_t)(K * kB + r) * Mp + K * kB + tx];
-    // unblocked right-looking Cholesky of the diagonal block (lower triangle)
-    for (int j = 0; j < kB; ++j) {
-        __syncthreads();
-        const double d = Lk[j][j];
-        const double ljj = sqrt(d);
-        if (threadIdx.x == 0) piv[j] = d;
-        __syncthreads();
-        // column j below the diagonal
-        if (ty == 0 && tx > j) Lk[tx][j] /= ljj;
-        if (threadIdx.x == 0) Lk[j][j] = ljj;
-        __syncthreads();
-        // trailing update of the lower triangle
+    const int lane = threadIdx.x, r = lane & (kB - 1);
+    const bool own = lane < kB;
+    double a[kB];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = ty + 8 * u;
-            if (r > j && tx > j && tx <= r) Lk[r][tx] -= Lk[r][j] * Lk[tx][j];
+    for (int c = 0; c < kB; ++c) a[c] = A[(int64_t)(K * kB + r) * Mp + K * kB + c];
+    double ld = 0.0;
+    bool bad = false;
+#pragma unroll
+    for (int j = 0; j < kB; ++j) {
+        const double d = lane_bcast(a[j], j);  // A_jj after steps 0 .. j - 1
+        if (I == K) {  // uniform: only the diagonal workgroup records the pivots
+            bad |= !(d > 0.0);
+            ld += log(d);
         }
+        const double ljj = sqrt(d);
+        a[j] = r > j ? a[j] / ljj : (r == j ? ljj : 0.0);  // column j of L; zero above
+        // trailing update; rows r < c only touch entries above the diagonal,
+        // which step c sets to zero
+#pragma unroll
+        for (int c = j + 1; c < kB; ++c) a[c] -= a[j] * lane_bcast(a[j], c);
     }
-    __syncthreads();
     if (I == K) {
-        for (int r = ty; r < kB; r += 8) Dg[(mat * kB + r) * kB + tx] = tx <= r ? Lk[r][tx] : 0.0;
-        if (threadIdx.x == 0) {
-            double ld = 0.0;
-            bool bad = false;
-            for (int j = 0; j < kB; ++j) {
-                bad |= !(piv[j] > 0.0);
-                ld += log(piv[j]);
-            }
+        if (own)
+#pragma unroll
+            for (int c = 0; c < kB; ++c) Dg[(mat * kB + r) * kB + c] = a[c];
+        if (lane == 0) {
             logdet[mat * (nbk + 1) + K] = ld;
             const double prev = K == 0 ? 0.0 : logdet[mat * (nbk + 1) + nbk];
             logdet[mat * (nbk + 1) + nbk] = prev + (bad ? 1.0 : 0.0);
@@ -264,17 +269,18 @@ __global__ __launch_bounds__(256) void bound_chol_panel_kernel(int Mp, int K, do
         return;
     }
     // X L_KK^T = A_IK, column sweep: x_j = a_j / L_jj, then a_c -= x_j L_cj for c > j
-    for (int r = ty; r < kB; r += 8) X[r][tx] = A[(int64_t)(I * kB + r) * Mp + K * kB + tx];
+    double x[kB];
+#pragma unroll
+    for (int c = 0; c < kB; ++c) x[c] = A[(int64_t)(I * kB + r) * Mp + K * kB + c];
+#pragma unroll
     for (int j = 0; j < kB; ++j) {
-        __syncthreads();
-        if (tx == j)
-            for (int r = ty; r < kB; r += 8) X[r][j] /= Lk[j][j];
-        __syncthreads();
-        if (tx > j)
-            for (int r = ty; r < kB; r += 8) X[r][tx] -= X[r][j] * Lk[tx][j];
+        x[j] /= lane_bcast(a[j], j);
+#pragma unroll
+        for (int c = j + 1; c < kB; ++c) x[c] -= x[j] * lane_bcast(a[j], c);
     }
-    __syncthreads();
-    for (int r = ty; r < kB; r += 8) A[(int64_t)(I * kB + r) * Mp + K * kB + tx] = X[r][tx];
+    if (own)
+#pragma unroll
+        for (int c = 0; c < kB; ++c) A[(int64_t)(I * kB + r) * Mp + K * kB + c] = x[c];
 }
 
 // Blocked Cholesky, trailing update after step K: A_IJ -= L_IK L_JK^T for
@@ -589,7 +595,7 @@ hipError_t bound_middle(const Shape &s, int64_t D, const T *mu, const T *S, cons
         TimedScope ts(st, "bound_chol");
         double *Dg = at<double>(ws, p.off_dg);
         for (int K = 0; K < p.nbk; ++K) {
-            bound_chol_panel_kernel<<<dim3(p.nbk - K, 2), 256, 0, st>>>(Mp, K, Lf, Dg, ld);
+            bound_chol_panel_kernel<<<dim3(p.nbk - K, 2), 64, 0, st>>>(Mp, K, Lf, Dg, ld);
             bound_chol_update_kernel<<<dim3(p.nbk, p.nbk, 2), 256, 0, st>>>(Mp, K, Lf, Dg);
         }
         const size_t shb = sizeof(double) * kB * (kB + 1) * (p.nbk + 1);

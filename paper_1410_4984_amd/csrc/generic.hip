@@ -198,22 +198,22 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(
     for (int64_t base = r0; base < r1; base += kRowTile) {
         const int cnt = (int)min<int64_t>(kRowTile, r1 - base);
         __syncthreads();
-        for (int i = threadIdx.x; i < cnt * Q; i += blockDim.x) {
-            int r = i / Q, q = i - r * Q;
-            s_mu[r][q] = mu[(base + r) * Q + q];
-            s_w2[r][q] = w2[(base + r) * Q + q];
+        // zero beyond Q, so that the padded dimensions need no test below
+        for (int i = threadIdx.x; i < cnt * QM; i += blockDim.x) {
+            const int r = i / QM, q = i - r * QM;
+            s_mu[r][q] = q < Q ? mu[(base + r) * Q + q] : T(0);
+            s_w2[r][q] = q < Q ? w2[(base + r) * Q + q] : T(0);
         }
         for (int r = threadIdx.x; r < cnt; r += blockDim.x) s_lp[r] = lp2[base + r];
         __syncthreads();
         if (valid) {
+#pragma unroll 4
             for (int r = 0; r < cnt; ++r) {
                 T e = s_lp[r] + C;
 #pragma unroll
                 for (int q = 0; q < QM; ++q) {
-                    if (q < Q) {
-                        T d = s_mu[r][q] - zbar[q];
-                        e -= d * d * s_w2[r][q];
-                    }
+                    const T d = s_mu[r][q] - zbar[q];
+                    e -= d * d * s_w2[r][q];
                 }
                 acc += dexp(e);
             }

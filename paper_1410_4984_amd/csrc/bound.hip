@@ -431,8 +431,16 @@ __global__ void bound_g1_kernel(int64_t N, int M, int64_t D, double beta2, const
                                 const double *__restrict__ C, T *__restrict__ G1) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= N * M) return;
-    const int64_t n = i / M;
-    const int m = (int)(i - n * M);
+    int64_t n;
+    int m;
+    if (i <= 0x7fffffff) {  // 32-bit division where the index fits
+        const unsigned u = (unsigned)i, nn = u / (unsigned)M;
+        n = nn;
+        m = (int)(u - nn * (unsigned)M);
+    } else {
+        n = i / M;
+        m = (int)(i - n * M);
+    }
     double s = 0.0;
     for (int64_t d = 0; d < D; ++d) s += (double)Y[n * D + d] * C[(int64_t)m * D + d];
     G1[i] = (T)(beta2 * s);
@@ -502,13 +510,26 @@ __global__ __launch_bounds__(64) void bound_kmm_grad_kernel(int M, int Q, int Mp
     double zq = 0.0, gz = 0.0, gl = 0.0, sw = 0.0;
     const double l = q < Q ? (double)h.l[q] : 1.0;
     if (q < Q) zq = (double)Z[(int64_t)m * Q + q];
-    for (int mp = 0; mp < M; ++mp) {
-        const double w = 0.5 * (GK[(int64_t)m * Mp + mp] + GK[(int64_t)mp * Mp + m]) * K0[(int64_t)m * Mp + mp];
-        sw += w;
-        if (q < Q) {
-            const double d = zq - (double)Z[(int64_t)mp * Q + q];
-            gz += w * d;
-            gl += w * d * d;
+    // partners in order; loads issued 8 at a time so that they overlap
+    for (int mp0 = 0; mp0 < M; mp0 += 8) {
+        double w[8], zp[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int mp = mp0 + j;
+            const bool in = mp < M;
+            w[j] = in ? 0.5 * (GK[(int64_t)m * Mp + mp] + GK[(int64_t)mp * Mp + m]) * K0[(int64_t)m * Mp + mp]
+                      : 0.0;
+            zp[j] = (in && q < Q) ? (double)Z[(int64_t)mp * Q + q] : 0.0;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (mp0 + j >= M) break;
+            sw += w[j];
+            if (q < Q) {
+                const double d = zq - zp[j];
+                gz += w[j] * d;
+                gl += w[j] * d * d;
+            }
         }
     }
     if (q < Q) {
@@ -524,14 +545,20 @@ __global__ void bound_kmm_reduce_kernel(int M, int Q, const double *__restrict__
                                         const double *__restrict__ ksf, T *__restrict__ dl,
                                         T *__restrict__ dsf2) {
     const int q = threadIdx.x;
-    if (q < Q) {
+    // m in order; loads issued 8 at a time so that they overlap
+    if (q <= Q) {
         double s = 0.0;
-        for (int m = 0; m < M; ++m) s += kdl[(int64_t)m * Q + q];
-        dl[q] = (T)((double)dl[q] + s);
-    } else if (q == Q) {
-        double s = 0.0;
-        for (int m = 0; m < M; ++m) s += ksf[m];
-        dsf2[0] = (T)((double)dsf2[0] + s);
+        int m = 0;
+        for (; m + 8 <= M; m += 8) {
+            double v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = q < Q ? kdl[(int64_t)(m + j) * Q + q] : ksf[m + j];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s += v[j];
+        }
+        for (; m < M; ++m) s += q < Q ? kdl[(int64_t)m * Q + q] : ksf[m];
+        if (q < Q) dl[q] = (T)((double)dl[q] + s);
+        else dsf2[0] = (T)((double)dsf2[0] + s);
     }
 }
 

@@ -138,8 +138,16 @@ __global__ void psi1_kernel(int64_t N, int M, int Q, const T *__restrict__ mu,
                             const T *__restrict__ lp1, T *__restrict__ Psi1) {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= N * M) return;
-    int64_t n = i / M;
-    int m = (int)(i - n * M);
+    int64_t n;
+    int m;
+    if (i <= 0x7fffffff) {  // 32-bit division where the index fits
+        const unsigned u = (unsigned)i, nn = u / (unsigned)M;
+        n = nn;
+        m = (int)(u - nn * (unsigned)M);
+    } else {
+        n = i / M;
+        m = (int)(i - n * M);
+    }
     T s = 0;
     for (int q = 0; q < Q; ++q) {
         T d = mu[n * Q + q] - Z[(int64_t)m * Q + q];
@@ -233,8 +241,17 @@ __global__ void psi2_reduce_kernel(int64_t N, int M, int64_t P, int64_t nchunks,
         psi0[0] = (accumulate ? psi0[0] : T(0)) + T(N) * h.sf2;
     if (m >= M || mp >= M || m > mp) return;
     const int64_t p = pair_index(m, mp, M);
+    // chunk order; loads issued 16 at a time so that they overlap
     T s = 0;
-    for (int64_t c = 0; c < nchunks; ++c) s += partial[c * P + p];
+    int64_t c = 0;
+    for (; c + 16 <= nchunks; c += 16) {
+        T v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = partial[(c + j) * P + p];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s += v[j];
+    }
+    for (; c < nchunks; ++c) s += partial[c * P + p];
     T v = (accumulate ? Psi2[(int64_t)m * M + mp] : T(0)) + s;
     Psi2[(int64_t)m * M + mp] = v;
     Psi2[(int64_t)mp * M + m] = v;

@@ -752,8 +752,17 @@ __global__ __launch_bounds__(256) void known_col_reduce_kernel(int M, int Q, int
     const int64_t m = blockIdx.x;
     if (t < S * K) {
         const int j = t / K, k = t - j * K;
+        // groups j, j + S, ... in order; loads issued 8 at a time so that they overlap
         T s = 0;
-        for (int64_t c = j; c < groups; c += S) s += colpart[(c * M + m) * K + k];
+        int64_t c = j;
+        for (; c + 7 * S < groups; c += 8 * S) {
+            T v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = colpart[((c + u * S) * M + m) * K + k];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; c < groups; c += S) s += colpart[(c * M + m) * K + k];
         part[t] = s;
     }
     __syncthreads();

@@ -1015,17 +1015,20 @@ __global__ __launch_bounds__(256) void psi2_finalize_kernel(
     int64_t N, int Q, int groups, const float *__restrict__ rowsum,
     const float *__restrict__ w2t, const float *__restrict__ S, Hyp<float> h,
     float *__restrict__ dmu, float *__restrict__ dS, float *__restrict__ part_dl) {
-    __shared__ float red[4][65];
-    const int q = threadIdx.x & 63, rl = threadIdx.x >> 6;
+    // thread (row slot r, dimension q): R = 256 / Q row slots, so that all but
+    // 256 mod Q lanes work; slot r takes rows r, r + R, ... of the block
+    __shared__ float red_dl[256], red_sf[256];
+    const int R = 256 / Q, t = threadIdx.x, r = t / Q, q = t - r * Q;
+    const bool act = r < R;
     const int RED = 5 * Q + 2;
     const int64_t n0 = (int64_t)blockIdx.x * kFinRows;
     float dl = 0.f, dsf = 0.f;
-    if (q < Q) {
+    if (act) {
         const float l = h.l[q], l2 = h.l2[q];
-        for (int k = rl; k < kFinRows; k += 4) {
+        for (int k = r; k < kFinRows; k += R) {
             const int64_t n = n0 + k;
             if (n >= N) break;
-            float X = 0.f, Y = 0.f, P = 0.f, X1 = 0.f, P1 = 0.f, R = 0.f, T1 = 0.f;
+            float X = 0.f, Y = 0.f, P = 0.f, X1 = 0.f, P1 = 0.f, Rr = 0.f, T1 = 0.f;
             for (int gi = 0; gi < groups; ++gi) {
                 const float *rs = rowsum + ((int64_t)gi * N + n) * RED;
                 X += rs[q];
@@ -1033,27 +1036,31 @@ __global__ __launch_bounds__(256) void psi2_finalize_kernel(
                 P += rs[2 * Q + q];
                 X1 += rs[3 * Q + q];
                 P1 += rs[4 * Q + q];
-                R += rs[5 * Q];
+                Rr += rs[5 * Q];
                 T1 += rs[5 * Q + 1];
             }
             const float w2 = w2t[n * Q + q];
             const float s = S[n * Q + q];
             const float w1 = 1.f / (l2 + s);
             dmu[n * Q + q] = -2.f * w2 * P - w1 * P1;
-            dS[n * Q + q] = w2 * w2 * (X + Y) - w2 * R + 0.5f * w1 * (w1 * X1 - T1);
-            dl += (2.f * s * w2 / l) * R + l * w2 * w2 * (X + Y) + (X - Y) / (l2 * l) +
+            dS[n * Q + q] = w2 * w2 * (X + Y) - w2 * Rr + 0.5f * w1 * (w1 * X1 - T1);
+            dl += (2.f * s * w2 / l) * Rr + l * w2 * w2 * (X + Y) + (X - Y) / (l2 * l) +
                   (s * w1 / l) * T1 + l * w1 * w1 * X1;
-            dsf += 2.f * R + T1;
+            dsf += 2.f * Rr + T1;
         }
+        red_dl[t] = dl;
+        if (q == 0) red_sf[r] = dsf;
     }
-    red[rl][q] = dl;
-    if (q == 0) red[rl][64] = dsf;
     __syncthreads();
-    if (rl == 0 && q < Q) {
-        part_dl[(int64_t)blockIdx.x * (Q + 1) + q] = red[0][q] + red[1][q] + red[2][q] + red[3][q];
-        if (q == 0)
-            part_dl[(int64_t)blockIdx.x * (Q + 1) + Q] =
-                (red[0][64] + red[1][64] + red[2][64] + red[3][64]) / h.sf2;
+    // block partials: the row slots in order
+    if (t < Q) {
+        float v = 0.f;
+        for (int j = 0; j < R; ++j) v += red_dl[j * Q + t];
+        part_dl[(int64_t)blockIdx.x * (Q + 1) + t] = v;
+    } else if (t == Q) {
+        float v = 0.f;
+        for (int j = 0; j < R; ++j) v += red_sf[j];
+        part_dl[(int64_t)blockIdx.x * (Q + 1) + Q] = v / h.sf2;
     }
 }
 

@@ -31,6 +31,7 @@ constexpr int kPairTile = 16;    // pair tile edge (16 x 16 threads)
 constexpr int kRowBlock = 64;    // threads (rows) per block in the gradient row kernel
 constexpr int kColBlock = 64;    // threads (inducing inputs) per block in the column kernel
 constexpr int kBand = 8;         // symmetric pairs kernel: pair offsets k per LDS exchange
+constexpr int kSlotBand = 4;     // ... the same with several rows at a time
 
 __device__ inline float dexp(float x) { return __expf(x); }
 __device__ inline double dexp(double x) { return exp(x); }
@@ -54,6 +55,8 @@ struct Plan {
     int64_t cr;                      // column kernel: ranges of partners m'
     bool pairs;                      // gradients by grad_pairs_kernel (Z table fits in LDS)
     bool psym;                       // ... in its symmetric form (one workgroup spans all of M)
+    bool pslots;                     // ... with R rows at a time (grad_pairs_slots_kernel)
+    int prs, psthreads;              // its rows at a time and threads per workgroup
     int pthreads;                    // pairs kernel: threads (inducing inputs) per workgroup
     int64_t pmb, pchunks, prows;     // pairs kernel: m-blocks, row chunks, rows per chunk
     // workspace offsets in bytes
@@ -92,6 +95,11 @@ Plan make_plan(const Shape &s, size_t elem) {
     // symmetric form: every pair exchange stays inside one workgroup, and the Z
     // table plus two bands of kBand x M pair values fit in LDS
     p.psym = p.pairs && p.pmb == 1 && (pairs_qm(s.Q) + 2 * kBand) * s.M * elem <= 65536;
+    p.prs = (int)std::min<int64_t>(8, 512 / s.M);
+    p.psthreads = (int)(cdiv(p.prs * s.M, 64) * 64);
+    p.pslots = p.psym && p.prs >= 2 &&
+               (s.M * pairs_qm(s.Q) + p.prs * 2 * kSlotBand * s.M + p.prs * s.M * 2 * pairs_qm(s.Q)) * elem <=
+                   65536;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_w1 = take(elem * s.N * s.Q);
@@ -617,6 +625,216 @@ __global__ __launch_bounds__(256) void grad_pairs_kernel(
     }
 }
 
+// The band form with R = min(8, 512 / M) rows at a time, so that a workgroup
+// of R M threads (rounded up to whole waves) leaves few lanes idle when M is
+// not a multiple of 64.  Thread (slot, m) = (tid / M, tid % M) works on row
+// r0 + it R + slot of pass it; each slot exchanges W through its own double
+// buffered band of kSlotBand offsets.  Per row the dmu / dS terms are summed
+// over m through LDS (32 lanes per output, each adding m = u, u + 32, ... in
+// order, then a fixed butterfly); dZ_m adds the slots in order at the end.
+
+template <typename T, int QM>
+__global__ __launch_bounds__(512) void grad_pairs_slots_kernel(
+    int64_t N, int M, int Q, int R, int64_t rows_per_chunk, const T *__restrict__ mu,
+    const T *__restrict__ S, const T *__restrict__ Z, const T *__restrict__ w1t,
+    const T *__restrict__ w2t, const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h,
+    const T *__restrict__ G1, const T *__restrict__ G2s, const T *__restrict__ Gc,
+    T *__restrict__ rowg, T *__restrict__ colpart, T *__restrict__ rowpart) {
+    extern __shared__ double gs_smem[];
+    T *sz = reinterpret_cast<T *>(gs_smem);        // [M][QM], zero beyond Q
+    T *band = sz + M * QM;                          // [R][2][kSlotBand][M]
+    T *rvs = band + (size_t)R * 2 * kSlotBand * M;  // [R M][2 QM]: row terms, then dZ by slot
+    __shared__ T redw[8];
+    const int tid = threadIdx.x, nthr = blockDim.x, nw = nthr >> 6, wv = tid >> 6;
+    const int slot = tid / M, m = tid - slot * M;
+    const bool valid = slot < R;
+    for (int i = tid; i < M * QM; i += nthr) {
+        const int mm = i / QM, q = i - mm * QM;
+        sz[i] = q < Q ? Z[(int64_t)mm * Q + q] : T(0);
+    }
+    __syncthreads();
+    T z[QM], c4[QM], il2[QM], gz[QM], gl[QM];
+#pragma unroll
+    for (int q = 0; q < QM; ++q) {
+        z[q] = valid ? sz[m * QM + q] : T(0);
+        c4[q] = q < Q ? T(0.25) / h.l2[q] : T(0);
+        il2[q] = q < Q ? T(1) / h.l2[q] : T(0);
+        gz[q] = gl[q] = 0;
+    }
+    T gsf = 0;
+    const int K = M / 2;
+    const bool even = (M & 1) == 0;
+    const int Ku = even ? K - 1 : K;  // offsets taken by every thread
+    int band_no = 0;
+    const T gdiag = valid ? Gc[m] : T(0);
+    const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk, r1 = min(N, r0 + rows_per_chunk);
+    const int64_t iters = (r1 - r0 + R - 1) / R;
+    for (int64_t it = 0; it < iters; ++it) {
+        const int64_t n = r0 + it * R + slot;
+        const bool rin = valid && n < r1;
+        T x[QM], a1[QM], a2[QM], sv[QM], d[QM];
+#pragma unroll
+        for (int q = 0; q < QM; ++q) {
+            const bool in = rin && q < Q;
+            x[q] = in ? mu[n * Q + q] : T(0);
+            a1[q] = in ? w1t[n * Q + q] : T(0);
+            a2[q] = in ? w2t[n * Q + q] : T(0);
+            sv[q] = in ? S[n * Q + q] : T(0);
+            d[q] = x[q] - z[q];
+        }
+        T r = 0, V[QM];
+#pragma unroll
+        for (int q = 0; q < QM; ++q) V[q] = 0;
+        // the exponent as a quadratic in v = z_m' - z_m (as in grad_pairs_kernel)
+        T bq[QM], cq[QM], e0 = (G2s && rin) ? lp2[n] : T(0);
+#pragma unroll
+        for (int q = 0; q < QM; ++q) {
+            bq[q] = a2[q] * d[q];
+            cq[q] = c4[q] + T(0.25) * a2[q];
+            e0 -= bq[q] * d[q];
+        }
+        auto pair_w = [&](const T *zr, T g) {
+            T e = e0;
+#pragma unroll
+            for (int q = 0; q < QM; ++q) {
+                const T v = zr[q] - z[q];
+                e = fma(v, fma(-cq[q], v, bq[q]), e);
+            }
+            return g * dexp(e);
+        };
+        auto add_w = [&](T W, const T *zr) {
+            r += W;
+#pragma unroll
+            for (int q = 0; q < QM; ++q) V[q] += W * (x[q] - zr[q]);
+        };
+        if (G2s) {  // uniform: every thread reaches the band barriers
+            if (rin) add_w(pair_w(sz + m * QM, gdiag), sz + m * QM);
+            for (int k0 = 1; k0 <= Ku; k0 += kSlotBand, ++band_no) {
+                T *bs = band + ((size_t)slot * 2 + (band_no & 1)) * (kSlotBand * M);
+                const int k1 = min(Ku, k0 + kSlotBand - 1);
+                if (rin) {
+                    int mp = m + k0;
+                    if (mp >= M) mp -= M;
+                    const T *gk = Gc + (int64_t)k0 * M + m;
+#pragma unroll 2
+                    for (int k = k0; k <= k1; ++k) {
+                        const T W = pair_w(sz + mp * QM, *gk);
+                        add_w(W, sz + mp * QM);
+                        bs[(k - k0) * M + m] = W;
+                        gk += M;
+                        mp = mp + 1 == M ? 0 : mp + 1;
+                    }
+                }
+                __syncthreads();
+                if (rin) {
+                    int sp = m - k0;
+                    if (sp < 0) sp += M;
+#pragma unroll 4
+                    for (int k = k0; k <= k1; ++k) {
+                        add_w(bs[(k - k0) * M + sp], sz + sp * QM);
+                        sp = sp == 0 ? M - 1 : sp - 1;
+                    }
+                }
+            }
+            if (even && K > 0) {
+                T *bs = band + ((size_t)slot * 2 + (band_no & 1)) * (kSlotBand * M);
+                ++band_no;
+                if (rin && m < K) {
+                    const T W = pair_w(sz + (m + K) * QM, Gc[(int64_t)K * M + m]);
+                    add_w(W, sz + (m + K) * QM);
+                    bs[m] = W;
+                }
+                __syncthreads();
+                if (rin && m >= K) add_w(bs[m - K], sz + (m - K) * QM);
+            }
+        }
+        T rv[2 * QM];
+#pragma unroll
+        for (int k = 0; k < 2 * QM; ++k) rv[k] = 0;
+        if (rin) {
+            T t = 0;
+            if (G1) {
+                T e1 = 0;
+#pragma unroll
+                for (int q = 0; q < QM; ++q) e1 += d[q] * d[q] * a1[q];
+                t = G1[n * M + m] * dexp(lp1[n] - T(0.5) * e1);
+            }
+#pragma unroll
+            for (int q = 0; q < QM; ++q) {
+                const T dq = d[q], d2 = dq * dq, dr = dq * r, dV = dq * V[q];
+                rv[q] = -T(2) * a2[q] * dr - t * dq * a1[q];
+                rv[QM + q] = a2[q] * a2[q] * (d2 * r + dV) - a2[q] * r +
+                             T(0.5) * t * (d2 * a1[q] * a1[q] - a1[q]);
+                gz[q] += a2[q] * (dr + V[q]) - (V[q] - dr) * il2[q] + t * dq * a1[q];
+                if (q < Q) {
+                    const T l = h.l[q];
+                    gl[q] += (T(2) * sv[q] * a2[q] / l) * r + (d2 * r - dV) * il2[q] / l +
+                             l * a2[q] * a2[q] * (d2 * r + dV) +
+                             t * (sv[q] * a1[q] / l + l * d2 * a1[q] * a1[q]);
+                }
+            }
+            gsf += T(2) * r + t;
+        }
+        if (valid) {
+#pragma unroll
+            for (int k = 0; k < 2 * QM; ++k) rvs[(size_t)tid * 2 * QM + k] = rv[k];
+        }
+        __syncthreads();
+        {
+            const int g = tid >> 5, u = tid & 31, outs = R * 2 * Q;
+            for (int o = g; o < outs; o += nthr >> 5) {
+                const int sl = o / (2 * Q), j = o - sl * 2 * Q;
+                const int kk = j < Q ? j : QM + (j - Q);
+                T v = 0;
+                for (int mm = u; mm < M; mm += 32) v += rvs[((size_t)sl * M + mm) * 2 * QM + kk];
+#pragma unroll
+                for (int off = 16; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+                const int64_t nn = r0 + it * R + sl;
+                if (u == 0 && nn < r1) {
+                    const int part = j < Q ? 0 : 1, q = j < Q ? j : j - Q;
+                    rowg[((int64_t)part * N + nn) * Q + q] = v;
+                }
+            }
+        }
+        __syncthreads();  // rvs is written again in the next pass
+    }
+    // dZ_m: the slots in order -> colpart[chunk][m][q]
+    if (valid) {
+#pragma unroll
+        for (int q = 0; q < QM; ++q) rvs[((size_t)slot * M + m) * QM + q] = gz[q];
+    }
+    __syncthreads();
+    if (tid < M) {
+#pragma unroll
+        for (int q = 0; q < QM; ++q) {
+            if (q < Q) {
+                T v = 0;
+                for (int sl = 0; sl < R; ++sl) v += rvs[((size_t)sl * M + tid) * QM + q];
+                colpart[((int64_t)blockIdx.y * M + tid) * Q + q] = v;
+            }
+        }
+    }
+    // block sums of dl and dsf2 (wave butterflies, then the waves in order) ->
+    // rowpart[chunk][Q + 1]
+    const int64_t blk = blockIdx.y;
+#pragma unroll
+    for (int k = 0; k <= QM; ++k) {
+        if (k < Q || k == QM) {
+            T v = k < QM ? gl[k] : gsf / h.sf2;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+            __syncthreads();
+            if ((tid & 63) == 0) redw[wv] = v;
+            __syncthreads();
+            if (tid == 0) {
+                T s2 = 0;
+                for (int w = 0; w < nw; ++w) s2 += redw[w];
+                rowpart[blk * (Q + 1) + (k < QM ? k : Q)] = s2;
+            }
+        }
+    }
+}
+
 // dmu, dS: the row kernel's range partials summed in range order.
 template <typename T>
 __global__ void grad_rows_reduce_kernel(int64_t NQ, int rr, const T *__restrict__ rowg,
@@ -845,12 +1063,18 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
             circ_kernel<T><<<(unsigned)cdiv((s.M / 2 + 1) * s.M, 256), 256, 0, st>>>((int)s.M, G2s, Gc);
         }
         const size_t lds = sizeof(T) * s.M * (pairs_qm(s.Q) + (sym ? 2 * kBand : 0));
+        const size_t lds_slots =
+            sizeof(T) * s.M * (pairs_qm(s.Q) + p.prs * 2 * kSlotBand + p.prs * 2 * pairs_qm(s.Q));
         dim3 grid((unsigned)p.pmb, (unsigned)p.pchunks);
         {
             TimedScope ts(st, "generic_grad_pairs");
 #define GPPS_PAIRS(QMV)                                                                            \
     do {                                                                                           \
-        if (sym)                                                                                   \
+        if (sym && p.pslots)                                                                       \
+            grad_pairs_slots_kernel<T, QMV><<<grid, p.psthreads, lds_slots, st>>>(                 \
+                s.N, (int)s.M, (int)s.Q, p.prs, p.prows, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s,   \
+                Gc, rowg, colpart, rowpart);                                                       \
+        else if (sym)                                                                              \
             grad_pairs_kernel<T, QMV, true><<<grid, p.pthreads, lds, st>>>(                        \
                 s.N, (int)s.M, (int)s.Q, p.prows, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, Gc,      \
                 rowg, colpart, rowpart);                                                           \

@@ -350,13 +350,23 @@ __global__ __launch_bounds__(256) void bound_trinv_kernel(int Mp, const double *
 #pragma unroll
         for (int u = 0; u < 4; ++u) xs(I, ty + 8 * u, tx) = t[u];
         for (int r = ty; r < kB; r += 8) lt(r, tx) = L[(int64_t)(I * kB + r) * Mp + I * kB + tx];
-        // X_IK = L_II^-1 T: row sweep, x_j = t_j / L_jj, then t_r -= L_rj x_j for r > j
-        for (int j = 0; j < kB; ++j) {
-            __syncthreads();
-            if (ty == 0) xs(I, j, tx) /= lt(j, j);
-            __syncthreads();
-            for (int r = ty; r < kB; r += 8)
-                if (r > j) xs(I, r, tx) -= lt(r, j) * xs(I, j, tx);
+        __syncthreads();
+        // X_IK = L_II^-1 T, column by column (forward substitution: x_j = t_j / L_jj,
+        // then t_r -= L_rj x_j for r > j): column c in the registers of lane c of
+        // the first wave, L_II read as LDS broadcasts, so no step needs a barrier
+        if (threadIdx.x < kB) {
+            const int c = threadIdx.x;
+            double x[kB];
+#pragma unroll
+            for (int r = 0; r < kB; ++r) x[r] = xs(I, r, c);
+#pragma unroll
+            for (int j = 0; j < kB; ++j) {
+                x[j] /= lt(j, j);
+#pragma unroll
+                for (int r = j + 1; r < kB; ++r) x[r] -= lt(r, j) * x[j];
+            }
+#pragma unroll
+            for (int r = 0; r < kB; ++r) xs(I, r, c) = x[r];
         }
         __syncthreads();
         for (int r = ty; r < kB; r += 8) Xg[(int64_t)(I * kB + r) * Mp + K * kB + tx] = xs(I, r, tx);

@@ -1,12 +1,14 @@
 """GPU parity of the generic path's pair kernels against the fp64 oracle.
 
-The gradient's pairs kernel has two forms: the symmetric one (each unordered
-pair (m, m') evaluated once by thread m for m' = m + k mod M, k <= M/2, and
-exchanged through LDS bands) whenever one workgroup holds all of M (M <= 256),
-and the ordered one beyond.  The symmetric schedule depends on the parity of M
-and on the band edges, so M runs over 1, 2, 3, small odd and even values, the
-paper's 100, the largest symmetric sizes 255 and 256, and the ordered 257 and
-300.  The forward Psi2 kernel puts one thread on each unique pair, in the
+The gradient's pairs kernel has three forms.  The symmetric ones (each
+unordered pair (m, m') evaluated once by thread m for m' = m + k mod M,
+k <= M/2, and exchanged through LDS bands) run whenever one workgroup holds all
+of M (M <= 256): with several rows per workgroup where its LDS fits (every
+case here up to M = 256 except fp64 at Q = 4 for M = 100, 255, 256), else one
+row at a time (those three).  The ordered form runs beyond.  The symmetric schedule
+depends on the parity of M and on the band edges, so M runs over 1, 2, 3, small
+odd and even values, the paper's 100, the largest symmetric sizes 255 and 256,
+and the ordered 257 and 300.  The forward Psi2 kernel puts one thread on each unique pair, in the
 row-major order of the upper triangle, for the same sizes.  Every output is
 compared element by element (relative Frobenius norm, 1e-10 fp64, fp32 as in
 the main parity tests).

@@ -375,28 +375,49 @@ __global__ __launch_bounds__(256) void bound_trinv_kernel(int Mp, const double *
 
 // C = alpha op(A) op(B), row-major fp64: op(A) is rows x inner, op(B) inner x cols.
 // 16 x 16 threads per 16 x 16 output tile, inner dimension staged through LDS.
-__global__ __launch_bounds__(256) void bound_gemm_kernel(int64_t rows, int64_t cols, int64_t inner,
-                                                         const double *__restrict__ A, int64_t lda,
-                                                         bool ta, const double *__restrict__ B,
-                                                         int64_t ldb, bool tb, double alpha,
-                                                         double *__restrict__ C, int64_t ldc) {
+// One product of the M x M algebra: C = alpha op(A) op(B).
+struct GemmJob {
+    int64_t rows, cols, inner;
+    const double *A;
+    int64_t lda;
+    bool ta;
+    const double *B;
+    int64_t ldb;
+    bool tb;
+    double alpha;
+    double *C;
+    int64_t ldc;
+};
+
+// Output tile (bx, by) of job j (the caller keeps it inside the job's tiles).
+__device__ inline void gemm_tile(const GemmJob &j, int64_t bx, int64_t by) {
     __shared__ double As[16][17], Bs[16][17];
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-    const int64_t r = (int64_t)blockIdx.y * 16 + ty, c = (int64_t)blockIdx.x * 16 + tx;
+    const int64_t r = by * 16 + ty, c = bx * 16 + tx;
     double s = 0.0;
-    for (int64_t k0 = 0; k0 < inner; k0 += 16) {
+    for (int64_t k0 = 0; k0 < j.inner; k0 += 16) {
         {
-            const int64_t ar = (int64_t)blockIdx.y * 16 + ty, ak = k0 + tx;
-            As[ty][tx] = (ar < rows && ak < inner) ? (ta ? A[ak * lda + ar] : A[ar * lda + ak]) : 0.0;
-            const int64_t bk = k0 + ty, bc = (int64_t)blockIdx.x * 16 + tx;
-            Bs[ty][tx] = (bk < inner && bc < cols) ? (tb ? B[bc * ldb + bk] : B[bk * ldb + bc]) : 0.0;
+            const int64_t ar = by * 16 + ty, ak = k0 + tx;
+            As[ty][tx] = (ar < j.rows && ak < j.inner) ? (j.ta ? j.A[ak * j.lda + ar] : j.A[ar * j.lda + ak])
+                                                        : 0.0;
+            const int64_t bk = k0 + ty, bc = bx * 16 + tx;
+            Bs[ty][tx] = (bk < j.inner && bc < j.cols) ? (j.tb ? j.B[bc * j.ldb + bk] : j.B[bk * j.ldb + bc])
+                                                        : 0.0;
         }
         __syncthreads();
 #pragma unroll
         for (int k = 0; k < 16; ++k) s += As[ty][k] * Bs[k][tx];
         __syncthreads();
     }
-    if (r < rows && c < cols) C[r * ldc + c] = alpha * s;
+    if (r < j.rows && c < j.cols) j.C[r * j.ldc + c] = j.alpha * s;
+}
+
+// Two independent products in one launch (blockIdx.z selects the job); tiles
+// past a job's edge return at once (workgroup-uniform, before any barrier).
+__global__ __launch_bounds__(256) void bound_gemm2_kernel(GemmJob j0, GemmJob j1) {
+    const GemmJob &j = blockIdx.z == 0 ? j0 : j1;
+    if ((int64_t)blockIdx.x * 16 >= j.cols || (int64_t)blockIdx.y * 16 >= j.rows) return;
+    gemm_tile(j, blockIdx.x, blockIdx.y);
 }
 
 // dL/dPsi2 (element type T, M x M), dL/dKmm (fp64, Mp x Mp) and, per row m, the
@@ -644,17 +665,19 @@ hipError_t bound_middle(const Shape &s, int64_t D, const T *mu, const T *S, cons
     // C = A^-1 Psi, P = C C^T, Kmm^-1 Psi2 Kmm^-1; dL/dPsi2, dL/dKmm, dL/dPsi1; the scalars
     {
         TimedScope ts(st, "bound_gemm");
-        auto gemm = [&](int64_t rows, int64_t cols, int64_t inner, const double *A, int64_t lda, bool ta,
-                        const double *B, int64_t ldb, bool tb, double *Cc, int64_t ldc) {
-            bound_gemm_kernel<<<dim3((unsigned)cdiv(cols, 16), (unsigned)cdiv(rows, 16)), 256, 0, st>>>(
-                rows, cols, inner, A, lda, ta, B, ldb, tb, 1.0, Cc, ldc);
+        // three stages of two independent products each, one launch per stage
+        auto pair = [&](const GemmJob &a, const GemmJob &b) {
+            const int64_t gx = std::max(cdiv(a.cols, 16), cdiv(b.cols, 16));
+            const int64_t gy = std::max(cdiv(a.rows, 16), cdiv(b.rows, 16));
+            bound_gemm2_kernel<<<dim3((unsigned)gx, (unsigned)gy, 2), 256, 0, st>>>(a, b);
         };
-        gemm(p.Mp, p.Mp, p.Mp, Li, p.Mp, true, Li, p.Mp, false, Kinv, p.Mp);
-        gemm(p.Mp, p.Mp, p.Mp, Li + mm, p.Mp, true, Li + mm, p.Mp, false, Ainv, p.Mp);
-        gemm(p.Mp, D, p.Mp, Ainv, p.Mp, false, Psi, D, false, C, D);
-        gemm(p.Mp, p.Mp, D, C, D, false, C, D, true, Pm, p.Mp);
-        gemm(p.Mp, p.Mp, p.Mp, Kinv, p.Mp, false, P2, p.Mp, false, Tm, p.Mp);
-        gemm(p.Mp, p.Mp, p.Mp, Tm, p.Mp, false, Kinv, p.Mp, false, KPK, p.Mp);
+        const int64_t P = p.Mp;
+        pair(GemmJob{P, P, P, Li, P, true, Li, P, false, 1.0, Kinv, P},                // Kmm^-1
+             GemmJob{P, P, P, Li + mm, P, true, Li + mm, P, false, 1.0, Ainv, P});     // A^-1
+        pair(GemmJob{P, D, P, Ainv, P, false, Psi, D, false, 1.0, C, D},               // C = A^-1 Psi
+             GemmJob{P, P, P, Kinv, P, false, P2, P, false, 1.0, Tm, P});              // Kmm^-1 Psi2
+        pair(GemmJob{P, P, D, C, D, false, C, D, true, 1.0, Pm, P},                    // C C^T
+             GemmJob{P, P, P, Tm, P, false, Kinv, P, false, 1.0, KPK, P});             // Kmm^-1 Psi2 Kmm^-1
     }
     {
         TimedScope ts(st, "bound_assemble");

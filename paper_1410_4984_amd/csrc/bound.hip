@@ -189,28 +189,39 @@ __global__ __launch_bounds__(256) void bound_psiy_kernel(int64_t N, int M, int64
     }
 }
 
-// Psi[m][d] = sum over chunks (fixed order); padded rows zero.
-__global__ void bound_psiy_reduce_kernel(int M, int Mp, int64_t D, int64_t chunks,
-                                         const double *__restrict__ part, double *__restrict__ Psi) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= (int64_t)Mp * D) return;
-    const int m = (int)(k / D);
-    const int64_t d = k - (int64_t)m * D;
+// Psi[m][d] = sum over chunks; padded rows zero.  32 outputs per workgroup,
+// each summed by 8 groups of threads (group g: chunks g, g + 8, ... in order,
+// loads issued 4 at a time), then the 8 group sums in order.
+__global__ __launch_bounds__(256) void bound_psiy_reduce_kernel(int M, int Mp, int64_t D, int64_t chunks,
+                                                                const double *__restrict__ part,
+                                                                double *__restrict__ Psi) {
+    __shared__ double gs[8][32];
+    const int o = threadIdx.x & 31, g = threadIdx.x >> 5;
+    const int64_t k = (int64_t)blockIdx.x * 32 + o;
+    const bool in = k < (int64_t)Mp * D;
+    const int m = in ? (int)(k / D) : M;
+    const int64_t d = in ? k - (int64_t)m * D : 0;
     double s = 0.0;
-    if (m < M) {  // chunk order, loads issued 16 at a time
+    if (m < M) {
         const double *src = part + d * M + m;
         const int64_t stride = D * M;
-        int64_t c = 0;
-        for (; c + 16 <= chunks; c += 16) {
-            double v[16];
+        int64_t c = g;
+        for (; c + 24 < chunks; c += 32) {
+            double v[4];
 #pragma unroll
-            for (int j = 0; j < 16; ++j) v[j] = src[(c + j) * stride];
+            for (int j = 0; j < 4; ++j) v[j] = src[(c + 8 * j) * stride];
 #pragma unroll
-            for (int j = 0; j < 16; ++j) s += v[j];
+            for (int j = 0; j < 4; ++j) s += v[j];
         }
-        for (; c < chunks; ++c) s += src[c * stride];
+        for (; c < chunks; c += 8) s += src[c * stride];
     }
-    Psi[k] = s;
+    gs[g][o] = s;
+    __syncthreads();
+    if (g == 0 && in) {
+        double t = 0.0;
+        for (int j = 0; j < 8; ++j) t += gs[j][o];
+        Psi[k] = t;
+    }
 }
 
 // Lane l's value of v, read by every lane (l uniform).
@@ -643,7 +654,7 @@ hipError_t bound_middle(const Shape &s, int64_t D, const T *mu, const T *S, cons
         TimedScope ts(st, "bound_psiy");
         dim3 g((unsigned)p.ychunks, (unsigned)std::min<int64_t>(cdiv((int64_t)M * D, 256), 16));
         bound_psiy_kernel<T><<<g, 256, 0, st>>>(s.N, M, D, Psi1, Y, at<double>(ws, p.off_ypart));
-        bound_psiy_reduce_kernel<<<(unsigned)cdiv(p.Mp * D, 256), 256, 0, st>>>(
+        bound_psiy_reduce_kernel<<<(unsigned)cdiv(p.Mp * D, 32), 256, 0, st>>>(
             M, Mp, D, p.ychunks, at<double>(ws, p.off_ypart), Psi);
     }
     // Kmm = L_k L_k^T and A = L_a L_a^T (blocked Cholesky, in place), log determinants,

@@ -235,16 +235,19 @@ __device__ inline double lane_bcast(double v, int l) {
 // Blocked Cholesky, panel step K: workgroup I = K + blockIdx.x of matrix
 // blockIdx.y factors the diagonal block A_KK = L_KK L_KK^T (unblocked,
 // right-looking) and, for I > K, solves X L_KK^T = A_IK in place.  One wave:
-// lane r holds row r of the block (lanes 32-63 repeat rows 0-31), so no step
-// needs a barrier; the pivot L_jj and the entries L_cj come from the owning
-// lanes by readlane.  Each element is updated in the same order as a column
-// sweep over j.  Workgroup K writes L_KK (zero above the diagonal) to the side
+// lane r holds row r of the block (lanes 32-63 repeat rows 0-31); the pivot
+// comes from its lane by readlane, and each finished column j of L goes to LDS
+// and is read back as broadcasts (a readlane per entry would cost a scalar
+// register round trip and its wait states).  Each element is updated in the
+// same order as a column sweep over j.  Workgroup K writes L_KK (zero above the diagonal) to the side
 // buffer Dg, since the others are still reading tile (K, K) (the update launch
 // copies it in), the sum of its log-pivots to logdet[K], and adds the count of
 // non-positive pivots to logdet[nbk].
 __global__ __launch_bounds__(64) void bound_chol_panel_kernel(int Mp, int K, double *__restrict__ A0,
                                                               double *__restrict__ Dg,
                                                               double *__restrict__ logdet) {
+    __shared__ double col[kB];         // column j of L
+    __shared__ double Ls[kB][kB + 1];  // L_KK, for the panel solve
     const int I = K + blockIdx.x, mat = blockIdx.y, nbk = Mp / kB;
     double *A = A0 + (int64_t)mat * Mp * Mp;
     const int lane = threadIdx.x, r = lane & (kB - 1);
@@ -263,10 +266,13 @@ __global__ __launch_bounds__(64) void bound_chol_panel_kernel(int Mp, int K, dou
         }
         const double ljj = sqrt(d);
         a[j] = r > j ? a[j] / ljj : (r == j ? ljj : 0.0);  // column j of L; zero above
+        __syncthreads();  // one wave: orders the previous step's reads before the store
+        if (own) col[r] = a[j];
+        __syncthreads();
         // trailing update; rows r < c only touch entries above the diagonal,
         // which step c sets to zero
 #pragma unroll
-        for (int c = j + 1; c < kB; ++c) a[c] -= a[j] * lane_bcast(a[j], c);
+        for (int c = j + 1; c < kB; ++c) a[c] -= a[j] * col[c];
     }
     if (I == K) {
         if (own)
@@ -280,14 +286,18 @@ __global__ __launch_bounds__(64) void bound_chol_panel_kernel(int Mp, int K, dou
         return;
     }
     // X L_KK^T = A_IK, column sweep: x_j = a_j / L_jj, then a_c -= x_j L_cj for c > j
+    if (own)
+#pragma unroll
+        for (int c = 0; c < kB; ++c) Ls[r][c] = a[c];
     double x[kB];
 #pragma unroll
     for (int c = 0; c < kB; ++c) x[c] = A[(int64_t)(I * kB + r) * Mp + K * kB + c];
+    __syncthreads();
 #pragma unroll
     for (int j = 0; j < kB; ++j) {
-        x[j] /= lane_bcast(a[j], j);
+        x[j] /= Ls[j][j];
 #pragma unroll
-        for (int c = j + 1; c < kB; ++c) x[c] -= x[j] * lane_bcast(a[j], c);
+        for (int c = j + 1; c < kB; ++c) x[c] -= x[j] * Ls[c][j];
     }
     if (own)
 #pragma unroll

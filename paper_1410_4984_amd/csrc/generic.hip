@@ -100,6 +100,13 @@ Plan make_plan(const Shape &s, size_t elem) {
     p.pslots = p.psym && p.prs >= 2 &&
                (s.M * pairs_qm(s.Q) + p.prs * 2 * kSlotBand * s.M + p.prs * s.M * 2 * pairs_qm(s.Q)) * elem <=
                    65536;
+    if (p.pslots) {
+        // chunks a whole number of passes of R rows, about five rounds of two
+        // 512-thread workgroups per CU
+        p.pchunks = std::max<int64_t>(1, std::min<int64_t>(s.N, 2560));
+        p.prows = cdiv(cdiv(s.N, p.pchunks), p.prs) * p.prs;
+        p.pchunks = cdiv(s.N, p.prows);
+    }
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_w1 = take(elem * s.N * s.Q);

@@ -27,6 +27,7 @@ namespace gpps {
 namespace {
 
 constexpr int kRowTile = 32;     // rows staged in LDS at a time
+constexpr int kFwdTile = 128;    // ... by the forward pair kernel
 constexpr int kPairTile = 16;    // pair tile edge (16 x 16 threads)
 constexpr int kRowBlock = 64;    // threads (rows) per block in the gradient row kernel
 constexpr int kColBlock = 64;    // threads (inducing inputs) per block in the column kernel
@@ -197,9 +198,9 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(
     int64_t N, int M, int Q, int64_t P, int64_t rows_per_chunk,
     const T *__restrict__ mu, const T *__restrict__ Z, const T *__restrict__ w2,
     const T *__restrict__ lp2, Hyp<T> h, T *__restrict__ partial) {
-    __shared__ T s_mu[kRowTile][QM];
-    __shared__ T s_w2[kRowTile][QM];
-    __shared__ T s_lp[kRowTile];
+    __shared__ T s_mu[kFwdTile][QM];
+    __shared__ T s_w2[kFwdTile][QM];
+    __shared__ T s_lp[kFwdTile];
     const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const bool valid = t < P;
     int m = 0, mp = 0;
@@ -218,8 +219,8 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
     T acc = 0;
-    for (int64_t base = r0; base < r1; base += kRowTile) {
-        const int cnt = (int)min<int64_t>(kRowTile, r1 - base);
+    for (int64_t base = r0; base < r1; base += kFwdTile) {
+        const int cnt = (int)min<int64_t>(kFwdTile, r1 - base);
         __syncthreads();
         // zero beyond Q, so that the padded dimensions need no test below
         for (int i = threadIdx.x; i < cnt * QM; i += blockDim.x) {

@@ -5,7 +5,10 @@
 // Precision.  Both contractions run on v_mfma_f32_32x32x16_f16 with both
 // operands split into two fp16 parts rounded to nearest, x = x_hi + x_lo
 // (22 significant bits); three of the four cross products are kept (the dropped
-// one is below 2^-22 |a||b|) and all products accumulate in fp32.  For the
+// one is below 2^-22 |a||b|) and all products accumulate in fp32.  In the Gram
+// product the three cross products share one K range: each dimension takes three
+// k slots (hi*hi, hi*lo, lo*hi) and the row bias two, so Q = 20 needs 62 slots,
+// four 16-slot instructions instead of six.  For the
 // exponents that is an error of a few 2^-24 |E| (measured on the synthetic
 // workloads: about 1e-7 relative in each Psi2 summand, two fp32 ulps), the
 // same order as the rounding the fp32 row terms already carry.  Range: the
@@ -119,9 +122,30 @@ __device__ inline void fwd_task(int task, int nb, int tpw, int &ti, int &tj0) {
     tj0 = ti + task * tpw;
 }
 
+// Packed Gram layout over NK 16-slot f16 MFMA instructions.  Each lane group
+// (g = lane / 32) holds 8 k slots per instruction, 4 NK packed f16 pairs
+// (dwords) in all, and takes the gram_t(NK) dimensions q = g T .. g T + T - 1:
+//   dwords [0, NP)       (hi_a, hi_b) of dimension pair p      (A: z_hi, z_hi)
+//          [NP, 2NP)     (lo_a, lo_b)                           (A: z_hi, z_hi)
+//          [2NP, 3NP)    (hi_a, hi_b) again                     (A: z_lo, z_lo)
+//          one odd dimension s, if any: (hi_s, lo_s), (hi_s, 0)  (A: (z_hi, z_hi), (z_lo, 0))
+//          the bias: (hi, lo) of b + c (lane group 1; zero in group 0)  (A: 1, 1)
+//          zero beyond.
+// Dimensions past Q have zero z, mu and K, so their slots contribute nothing.
+constexpr int gram_np(int nk) { return (4 * nk - 1) / 3; }
+constexpr int gram_odd(int nk) { return (4 * nk - 1) - 3 * gram_np(nk) >= 2 ? 1 : 0; }
+constexpr int gram_t(int nk) { return 2 * gram_np(nk) + gram_odd(nk); }
+// instructions for Q dimensions (instantiated counts only): Q <= 4, 8, 14, 20,
+// 30, 40, 52, 62
+inline int gram_nk(int64_t Q) {
+    for (int nk : {1, 2, 3, 4, 6, 8, 10, 12})
+        if (2 * gram_t(nk) >= Q) return nk;
+    return -1;
+}
+
 // Widest forward task (tiles per wave) whose registers fit two waves per SIMD
-// without spilling, for ni 16-dimension steps.
-constexpr int fwd_tpw_max(int ni) { return ni == 1 ? 4 : (ni == 2 ? 2 : 1); }
+// without spilling, for nk Gram instructions.
+constexpr int fwd_tpw_max(int nk) { return nk <= 2 ? 4 : (nk <= 4 ? 2 : 1); }
 
 // Upper-triangular tile index of (ti, tj), row-major.
 __host__ __device__ inline int64_t tile_index(int ti, int tj, int nb) {
@@ -132,9 +156,9 @@ struct MPlan {
     int64_t Mp;            // M rounded up to the tile edge
     int nb;                // tiles per edge
     int nqb;               // 32-column blocks of [Z | 1] (Q + 1 columns)
-    int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= 16 ni
-                           // and >= 32 nqb, so that no read needs a bounds test)
-    int ni;                // Gram: 16-slot f16 MFMA steps (Q dimensions + a bias slot)
+    int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= 2
+                           // gram_t(nk) and >= 32 nqb, so that no read needs a bounds test)
+    int nk;                // Gram: 16-slot f16 MFMA instructions (packed layout)
     int64_t T;             // upper-triangular tiles
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
@@ -150,11 +174,10 @@ struct MPlan {
 };
 
 // Forward LDS layout (floats):
-//   za  [nb][2][ni][2][32][8] f16   [centred z | 1] of every block split into two
-//                       fp16 parts, as A operands of the 32x32x16 f16 MFMA: block,
-//                       part, instruction, lane group, row, 8 consecutive k (the
-//                       last slot, 16 ni - 1 >= Q, holds 1: the multiplier of the
-//                       bias carried by the per-datapoint operand)
+//   za  [nb][nk][2][32][8] f16   [centred z | 1] of every block in the packed
+//                       Gram layout (fp16 parts of z and the bias multiplier 1), as
+//                       A operands of the 32x32x16 f16 MFMA: block, instruction,
+//                       lane group, row, 8 consecutive k
 //   bb  [FRB][Mp]       row terms b of the batch (log2 units)
 //   bcb [FRB][Mp]       b + c
 //   mub [FRB][64]       centred mu of the batch (zero beyond Q)
@@ -163,10 +186,10 @@ struct LdsF {
     int za, bb, bcb, mub, kb, total;
 };
 
-__host__ __device__ inline LdsF lds_fwd_layout(int Mp, int ni) {
+__host__ __device__ inline LdsF lds_fwd_layout(int Mp, int nk) {
     LdsF L{};
     int o = 0;
-    L.za = o; o += Mp * 2 * ni * 16 / 2;
+    L.za = o; o += Mp * nk * 16 / 2;
     L.bb = o; o += kFRB * Mp;
     L.bcb = o; o += kFRB * Mp;
     L.mub = o; o += kFRB * kRowStride;
@@ -177,26 +200,26 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int ni) {
 
 // Gradient LDS layout (floats):
 //   zx  [wpg 32][DSF]   centred z (fp32) of the workgroup's row blocks (rows m of W),
-//                       zero past Q up to the odd stride DSF (>= 16 ni, >= 32 nqb)
+//                       zero past Q up to the odd stride DSF (>= 2 gram_t(nk), >= 32 nqb)
 //   zh  [jpw][2][2][2][32 nqb][8] f16    the workgroup's column blocks of [Z | 1] split
 //                       into two fp16 parts, laid out as the B operands of the
 //                       32x32x16 f16 MFMA (8 consecutive k per lane and instruction)
-//   za  [jpw][2][ni][2][32][8] f16        the same rows of [centred z | 1] as Gram A
-//                       operands, two fp16 parts (row m' per lane, 8 consecutive slots
-//                       per lane group; the last slot 16 ni - 1 holds 1)
+//   za  [jpw][nk][2][32][8] f16           the same rows of [centred z | 1] as Gram A
+//                       operands in the packed layout (row m' per lane, 8 consecutive
+//                       slots per lane group and instruction)
 //   bb, bcb [RB][Mp], mub, kb, w1b, w2b [RB][64] (zero past Q), t1 [RB][Mp],
 //   sc [RB] (log2 of the per-row scale of W), red [RB][wpg][5Q + 2]
 struct LdsG {
     int zx, zb, za, bb, bcb, mub, kb, w1b, w2b, t1, sc, red, total;
 };
 
-__host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb, int ni, int wpg) {
+__host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb, int nk, int wpg) {
     const int jpw = grad_jpw(nqb);
     LdsG L{};
     int o = 0;
     L.zx = o; o += (wpg * kTile * DSF + 3) / 4 * 4;
     L.zb = o; o += jpw * 2 * 2 * 2 * 32 * nqb * 8 / 2;
-    L.za = o; o += jpw * 2 * ni * 2 * 32 * 8 / 2;
+    L.za = o; o += jpw * nk * 2 * 32 * 8 / 2;
     L.bb = o; o += kRB * Mp;
     L.bcb = o; o += kRB * Mp;
     L.mub = o; o += kRB * kRowStride;
@@ -215,22 +238,22 @@ MPlan make_mplan(const Shape &s) {
     p.Mp = cdiv(s.M, kTile) * kTile;
     p.nb = (int)(p.Mp / kTile);
     p.nqb = s.Q + 1 <= 32 ? 1 : 2;
-    p.ni = (int)cdiv(s.Q + 1, 16);   // k slot Q carries a bias term
-    p.DSF = std::max<int>(16 * p.ni, 32 * p.nqb) | 1;
+    p.nk = gram_nk(s.Q);
+    p.DSF = std::max<int>(2 * gram_t(std::max(p.nk, 1)), 32 * p.nqb) | 1;
     p.T = (int64_t)p.nb * (p.nb + 1) / 2;
     // forward tasks: tiles per task by a cost model in cycles: each task splits its
-    // n-dependent operand once per row (about 120 vector instructions per 16
-    // dimensions), each tile slot costs about 600 (MFMA, exp2, bias, sum)
+    // n-dependent operand once per row (about 60 vector instructions per Gram
+    // instruction), each tile slot costs about 400 (MFMA, exp2, sum)
     p.tpw = 1;
     int64_t best = -1;
-    for (int t = 1; t <= fwd_tpw_max(p.ni); ++t) {
+    for (int t = 1; t <= fwd_tpw_max(p.nk); ++t) {
         const int64_t groups = cdiv(fwd_tasks(p.nb, t), kWaves);
-        const int64_t cost = groups * kWaves * (120 * p.ni + 400 * t);
+        const int64_t cost = groups * kWaves * (60 * p.nk + 400 * t);
         if (best < 0 || cost < best) { best = cost; p.tpw = t; }
     }
     p.ftasks = fwd_tasks(p.nb, p.tpw);
     p.fgroups = cdiv(p.ftasks, kWaves);
-    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.ni).total;
+    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.nk).total;
     // whole rounds of the chip's workgroup slots, so that no partly filled last
     // round idles most CUs: 6 per CU is two rounds at three workgroups per CU and
     // three at two (the register counts of the instances allow two or three)
@@ -242,13 +265,13 @@ MPlan make_mplan(const Shape &s) {
     p.njr = (int)cdiv(p.nb, p.jpw);
     // widest workgroup whose LDS fits
     p.wpg = std::min(p.nb, grad_waves(p.nqb));
-    while (p.wpg > 1 && sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.ni,
+    while (p.wpg > 1 && sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk,
                                                         p.wpg).total > 160 * 1024)
         p.wpg /= 2;
     p.igroups = (int)cdiv(p.nb, p.wpg);
     p.ggroups = (int64_t)p.njr * p.igroups;
     p.lds_grad =
-        sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.ni, p.wpg).total;
+        sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk, p.wpg).total;
     // two full rounds: workgroups per CU limited by LDS and by the waves per CU
     // the kernel's register count allows (grad_waves: two or one per SIMD)
     const int64_t gslots = kCUs * std::max<int64_t>(
@@ -468,57 +491,74 @@ __device__ __forceinline__ unsigned lo_pair(float a0, float b0, float a1, float 
     return lo;
 }
 
+// Given h0 = the packed (f16(a b), 0), returns (f16(a b), f16(fma(a, b, -hi))):
+// the two fp16 parts of one product in one register, the residual written into
+// the high half by one v_fma_mix reading the high part through op_sel.
+__device__ __forceinline__ unsigned hi_lo_pair(float a, float b, unsigned h0) {
+    unsigned r = h0;
+    asm("v_fma_mixhi_f16 %0, %1, %2, -%3 op_sel_hi:[0,0,1]" : "+v"(r) : "v"(a), "v"(b), "v"(h0));
+    return r;
+}
+
 // Two fp16 parts of x (rounded to nearest): x == hi + lo up to 2^-22 |x|.
 __device__ __forceinline__ void split2h(float x, _Float16 &hi, _Float16 &lo) {
     hi = (_Float16)x;
     lo = (_Float16)(x - (float)hi);
 }
 
-// Per-datapoint Gram operand of the lane's column m (B side, 8 k slots per lane
-// group and instruction): (z_mk - mu_k) K_k for k = 16 hh + 8 g + e < Q (zv[hh][e]
-// holds z_mk; z, mu and K are zero past Q), the bias in the last slot 16 NI - 1
-// (lane group 1, element 7 of the last instruction), zero elsewhere; two fp16
-// parts.  mur and kr point at the row's mu and K of the lane group (k - 16 hh - e).
-template <int NI>
-__device__ __forceinline__ void gram_operand(const float (&zv)[NI][8],
+// Per-datapoint Gram operand of the lane's column m (B side) in the packed
+// layout: x_q = (z_mq - mu_q) K_q for the lane group's dimensions
+// q = g T + j (zv[j] holds z_mq; z, mu and K are zero past Q) as the fp16
+// pairs listed at gram_np, and the bias (lane group 1 only) in its own pair.
+// mur and kr point at the row's mu and K at dimension g T.
+template <int NK>
+__device__ __forceinline__ void gram_operand(const float (&zv)[gram_t(NK)],
                                              const float *__restrict__ mur,
                                              const float *__restrict__ kr, float bias, int g,
-                                             v8h (&Bh)[NI], v8h (&Bl)[NI]) {
+                                             v8h (&B)[NK]) {
+    constexpr int NP = gram_np(NK), ODD = gram_odd(NK);
     bias = g ? fminf(kBiasClamp, fmaxf(-kBiasClamp, bias)) : 0.f;
+    unsigned w[4 * NK];
 #pragma unroll
-    for (int hh = 0; hh < NI; ++hh) {
-        unsigned bh[4], bl[4];
+    for (int p = 0; p < NP; ++p) {
+        const float d0 = zv[2 * p] - mur[2 * p], k0 = kr[2 * p];
+        const float d1 = zv[2 * p + 1] - mur[2 * p + 1], k1 = kr[2 * p + 1];
+        const v2h h2 = {(_Float16)(d0 * k0), (_Float16)(d1 * k1)};
+        const unsigned hi = __builtin_bit_cast(unsigned, h2);
+        w[p] = hi;
+        w[NP + p] = lo_pair(d0, k0, d1, k1, hi);
+        w[2 * NP + p] = hi;
+    }
+    if constexpr (ODD != 0) {
+        const float d = zv[2 * NP] - mur[2 * NP], k = kr[2 * NP];
+        const v2h h2 = {(_Float16)(d * k), (_Float16)0.f};
+        const unsigned h0 = __builtin_bit_cast(unsigned, h2);
+        w[3 * NP] = hi_lo_pair(d, k, h0);
+        w[3 * NP + 1] = h0;
+    }
+    {
+        const v2h h2 = {(_Float16)bias, (_Float16)0.f};
+        const unsigned h0 = __builtin_bit_cast(unsigned, h2);
+        w[3 * NP + 2 * ODD] = hi_lo_pair(bias, 1.f, h0);
+    }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int e = 2 * u;
-            const float d0 = zv[hh][e] - mur[16 * hh + e], k0 = kr[16 * hh + e];
-            float d1 = zv[hh][e + 1] - mur[16 * hh + e + 1], k1 = kr[16 * hh + e + 1];
-            if (hh == NI - 1 && u == 3) {
-                // the last slot: the product (zero there) plus the bias, split as v * 1
-                d1 = d1 * k1 + bias;
-                k1 = 1.f;
-            }
-            const v2h h2 = {(_Float16)(d0 * k0), (_Float16)(d1 * k1)};
-            bh[u] = __builtin_bit_cast(unsigned, h2);
-            bl[u] = lo_pair(d0, k0, d1, k1, bh[u]);
-        }
-        Bh[hh] = __builtin_bit_cast(v8h, bh);
-        Bl[hh] = __builtin_bit_cast(v8h, bl);
+    for (int u = 3 * NP + 2 * ODD + 1; u < 4 * NK; ++u) w[u] = 0u;
+#pragma unroll
+    for (int i = 0; i < NK; ++i) {
+        const unsigned q4[4] = {w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]};
+        B[i] = __builtin_bit_cast(v8h, q4);
     }
 }
 
-// e += [z_j | 1] B over NI steps of 16 k slots (three f16 products per step);
-// za_j: the two-part A operand table of row block j.
-template <int NI>
+// e += [z_j | 1] B over the NK packed instructions; za_j: the A operand table of
+// row block j.
+template <int NK>
 __device__ __forceinline__ v16f gram16(v16f e, const _Float16 *__restrict__ za_j, int c, int g,
-                                       const v8h (&Bh)[NI], const v8h (&Bl)[NI]) {
+                                       const v8h (&B)[NK]) {
 #pragma unroll
-    for (int hh = 0; hh < NI; ++hh) {
-        const v8h Ah = *reinterpret_cast<const v8h *>(za_j + (((0 * NI + hh) * 2 + g) * 32 + c) * 8);
-        const v8h Al = *reinterpret_cast<const v8h *>(za_j + (((1 * NI + hh) * 2 + g) * 32 + c) * 8);
-        e = __builtin_amdgcn_mfma_f32_32x32x16_f16(Ah, Bh[hh], e, 0, 0, 0);
-        e = __builtin_amdgcn_mfma_f32_32x32x16_f16(Ah, Bl[hh], e, 0, 0, 0);
-        e = __builtin_amdgcn_mfma_f32_32x32x16_f16(Al, Bh[hh], e, 0, 0, 0);
+    for (int i = 0; i < NK; ++i) {
+        const v8h A = *reinterpret_cast<const v8h *>(za_j + ((i * 2 + g) * 32 + c) * 8);
+        e = __builtin_amdgcn_mfma_f32_32x32x16_f16(A, B[i], e, 0, 0, 0);
     }
     return e;
 }
@@ -539,24 +579,47 @@ __device__ __forceinline__ v16f row_terms(const float *__restrict__ bbr, int j, 
 }
 
 // [centred z | 1] rows of blocks blk0 .. blk0 + nblk - 1 (clamped to the last
-// block) as two-part A operand tables: [nblk][2][NI][2][32][8] f16.
-template <int NI>
+// block) as packed Gram A operand tables: [nblk][NK][2][32][8] f16 (slot
+// contents listed at gram_np).
+template <int NK>
 __device__ void stage_za(_Float16 *za, int blk0, int nblk, int nb, int M, int Q,
                          const float *__restrict__ Z, const float *__restrict__ zc) {
-    const int total = nblk * 2 * NI * 2 * 32 * 8;
+    constexpr int NP = gram_np(NK), ODD = gram_odd(NK), T = gram_t(NK);
+    const int total = nblk * NK * 2 * 32 * 8;
     for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
         int r = idx;
         const int e = r % 8; r /= 8;
         const int cc = r % 32; r /= 32;
         const int gg = r % 2; r /= 2;
-        const int hh = r % NI; r /= NI;
-        const int part = r % 2; r /= 2;
+        const int ins = r % NK; r /= NK;
         // blocks past the edge repeat the last one, so that every exponent stays finite
-        const int m = min(blk0 + r, nb - 1) * kTile + cc, q = 16 * hh + 8 * gg + e;
-        const float v = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : (q == 16 * NI - 1 ? 1.f : 0.f);
-        _Float16 hi, lo;
-        split2h(v, hi, lo);
-        za[idx] = part == 0 ? hi : lo;
+        const int m = min(blk0 + r, nb - 1) * kTile + cc;
+        const int w = 4 * ins + e / 2, half = e & 1;
+        int q = -1, part = 0;      // part 0: high fp16 part of z, 1: low part
+        float v = 0.f;
+        if (w < NP) {
+            q = 2 * w + half;
+        } else if (w < 2 * NP) {
+            q = 2 * (w - NP) + half;
+        } else if (w < 3 * NP) {
+            q = 2 * (w - 2 * NP) + half;
+            part = 1;
+        } else if (ODD && w == 3 * NP) {
+            q = 2 * NP;
+        } else if (ODD && w == 3 * NP + 1) {
+            if (half == 0) { q = 2 * NP; part = 1; }
+        } else if (w == 3 * NP + 2 * ODD) {
+            v = 1.f;               // bias multiplier
+        }
+        if (q >= 0) {
+            q += gg * T;
+            const float zq = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+            _Float16 hi, lo;
+            split2h(zq, hi, lo);
+            za[idx] = part == 0 ? hi : lo;
+        } else {
+            za[idx] = (_Float16)v;
+        }
     }
 }
 
@@ -564,17 +627,18 @@ __device__ void stage_za(_Float16 *za, int blk0, int nblk, int nb, int M, int Q,
 // Pair tiles (i, j), j >= i: rows m' in block j, columns m in block i,
 //   e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)      (A: [z | 1], B: [-K d | b + c])
 // The row terms b_m' are the accumulator's start value; the column bias rides in
-// the last k slot.  Wave task: column block i (its per-datapoint operand is split
+// its own pair of k slots.  Wave task: column block i (its per-datapoint operand is split
 // once per row) and TPW row blocks j; Psi2 tile sums stay in registers over the
 // row chunk.
-template <int NI, int TPW>
+template <int NK, int TPW>
 __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int64_t T, int ftasks, int64_t rows_per_chunk,
     const float *__restrict__ mu, const float *__restrict__ Z, const float *__restrict__ zc,
     const float *__restrict__ Kt, const float *__restrict__ bt, const float *__restrict__ bc,
     float *__restrict__ partial) {
     extern __shared__ float lds[];
-    const LdsF L = lds_fwd_layout(Mp, NI);
+    const LdsF L = lds_fwd_layout(Mp, NK);
+    constexpr int GT = gram_t(NK);
     _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int c = lane & 31, g = lane >> 5;
@@ -591,19 +655,18 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
 #pragma unroll
         for (int t = 0; t < 16; ++t) acc[k][t] = 0.f;
 
-    // constant tables: split [z | 1] of every block (LDS) and the centred z of the
-    // lane's column m = ti*32 + c at k = 16 hh + 8 g + e (registers, zero past Q)
-    stage_za<NI>(za, 0, nb, nb, M, Q, Z, zc);
-    float zr[NI][8];
+    // constant tables: packed [z | 1] of every block (LDS) and the centred z of the
+    // lane's column m = ti*32 + c at the lane group's dimensions g GT + j
+    // (registers, zero past Q)
+    stage_za<NK>(za, 0, nb, nb, M, Q, Z, zc);
+    float zr[GT];
     {
         const int m = ti * kTile + c;
 #pragma unroll
-        for (int hh = 0; hh < NI; ++hh)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int q = 16 * hh + 8 * g + e;
-                zr[hh][e] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
-            }
+        for (int j = 0; j < GT; ++j) {
+            const int q = g * GT + j;
+            zr[j] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+        }
     }
 
     // Batches of kFRB rows: the next batch is loaded into registers while the
@@ -645,14 +708,14 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
         if (n0 + kFRB < r1) load(n0 + kFRB);
         if (!active) continue;
         for (int r = 0; r < cb; ++r) {
-            v8h Bh[NI], Bl[NI];
-            gram_operand<NI>(zr, lds + L.mub + r * kRowStride + 8 * g, lds + L.kb + r * kRowStride + 8 * g,
-                             lds[L.bcb + r * Mp + ti * kTile + c], g, Bh, Bl);
+            v8h B[NK];
+            gram_operand<NK>(zr, lds + L.mub + r * kRowStride + g * GT, lds + L.kb + r * kRowStride + g * GT,
+                             lds[L.bcb + r * Mp + ti * kTile + c], g, B);
             const float *bbr = lds + L.bb + r * Mp;
 #pragma unroll
             for (int k = 0; k < TPW; ++k) {
-                const v16f e = gram16<NI>(row_terms(bbr, tj[k], g), za + tj[k] * (2 * NI * 2 * 32 * 8),
-                                          c, g, Bh, Bl);
+                const v16f e = gram16<NK>(row_terms(bbr, tj[k], g), za + tj[k] * (NK * 2 * 32 * 8),
+                                          c, g, B);
 #pragma unroll
                 for (int t = 0; t < 16; ++t) acc[k][t] += __builtin_amdgcn_exp2f(e[t]);
             }
@@ -747,7 +810,7 @@ __device__ void stage_zh(_Float16 *zh, int jr, int M, int Q, int nqb,
 // registers for the whole kernel; the epilogue turns V' into the task's share
 // of dZ (registers) and of the per-row sums, which the workgroup combines in LDS
 // and writes per (group, row) for psi2_finalize_kernel.
-template <int NI, int NQB, int JPW = grad_jpw(NQB)>
+template <int NK, int NQB, int JPW = grad_jpw(NQB)>
 __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int DSF, int njr, int wpg, int igroups,
     int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
@@ -757,7 +820,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     const float *__restrict__ gmax, Hyp<float> h, float *__restrict__ rowsum,
     float *__restrict__ part_dz) {
     extern __shared__ float lds[];
-    const LdsG L = lds_grad_layout(Mp, DSF, Q, NQB, NI, wpg);
+    const LdsG L = lds_grad_layout(Mp, DSF, Q, NQB, NK, wpg);
+    constexpr int GT = gram_t(NK);
     _Float16 *zh = reinterpret_cast<_Float16 *>(lds + L.zb);
     _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -809,7 +873,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     // W_n = G2s o Psi2_n is bounded by max|G2s| 2^(2 hl_n) (hl_n: log2 of the half
     // prefactor); its per-row scale 2^sc brings that bound to 2^14, inside fp16
     const float lg = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
-    stage_za<NI>(za, jr * JPW, JPW, nb, M, Q, Z, zc);
+    stage_za<NK>(za, jr * JPW, JPW, nb, M, Q, Z, zc);
 
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
@@ -848,16 +912,14 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             // row scale) in the last k slot
             const float sc = lds[L.sc + r];
             const float bcol = lds[L.bcb + r * Mp + i * kTile + c] + sc;
-            v8h GBh[NI], GBl[NI];
+            v8h GB[NK];
             {
-                const float *zi = lds + L.zx + (wave * kTile + c) * DSF + 8 * g;
-                float zv[NI][8];
+                const float *zi = lds + L.zx + (wave * kTile + c) * DSF + g * GT;
+                float zv[GT];
 #pragma unroll
-                for (int hh = 0; hh < NI; ++hh)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) zv[hh][e] = zi[16 * hh + e];
-                gram_operand<NI>(zv, lds + L.mub + r * kRowStride + 8 * g,
-                                 lds + L.kb + r * kRowStride + 8 * g, bcol, g, GBh, GBl);
+                for (int j = 0; j < GT; ++j) zv[j] = zi[j];
+                gram_operand<NK>(zv, lds + L.mub + r * kRowStride + g * GT,
+                                 lds + L.kb + r * kRowStride + g * GT, bcol, g, GB);
             }
             const float *bbr = lds + L.bb + r * Mp;
             v16f V[NQB];
@@ -868,8 +930,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
             for (int k = 0; k < JPW; ++k) {
                 const int j = jb[k];
-                const v16f e = gram16<NI>(row_terms(bbr, j, g), za + k * (2 * NI * 2 * 32 * 8), c, g,
-                                          GBh, GBl);
+                const v16f e = gram16<NK>(row_terms(bbr, j, g), za + k * (NK * 2 * 32 * 8), c, g, GB);
                 // W tile (scaled by 2^sc), split into two fp16 parts; A operand of
                 // instruction hh takes the lane's rows crow(8 hh + e, g), as the B
                 // operand tables do
@@ -1117,10 +1178,10 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(int64_t N, int M, int 
 }
 
 // ---------------------------------------------------------------- dispatch
-template <int NI, int TPW>
+template <int NK, int TPW>
 hipError_t launch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                       void *ws, hipStream_t st) {
-    auto k = psi2_fwd_kernel<NI, TPW>;
+    auto k = psi2_fwd_kernel<NK, TPW>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_fwd);
     if (e != hipSuccess) return e;
@@ -1133,10 +1194,10 @@ hipError_t launch_fwd(const MPlan &p, const Shape &s, const float *mu, const flo
     return hipGetLastError();
 }
 
-template <int NI, int NQB>
+template <int NK, int NQB>
 hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                        const Hyp<float> &h, void *ws, hipStream_t st) {
-    auto k = psi2_grad_kernel<NI, NQB>;
+    auto k = psi2_grad_kernel<NK, NQB>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_grad);
     if (e != hipSuccess) return e;
@@ -1153,11 +1214,12 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
 hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z, void *ws,
                         hipStream_t st) {
 #define GPPS_F(I, T) \
-    if (p.ni == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, ws, st);
+    if (p.nk == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, ws, st);
     GPPS_F(1, 1) GPPS_F(1, 2) GPPS_F(1, 3) GPPS_F(1, 4)
-    GPPS_F(2, 1) GPPS_F(2, 2)
-    GPPS_F(3, 1)
-    GPPS_F(4, 1)
+    GPPS_F(2, 1) GPPS_F(2, 2) GPPS_F(2, 3) GPPS_F(2, 4)
+    GPPS_F(3, 1) GPPS_F(3, 2)
+    GPPS_F(4, 1) GPPS_F(4, 2)
+    GPPS_F(6, 1) GPPS_F(8, 1) GPPS_F(10, 1) GPPS_F(12, 1)
 #undef GPPS_F
     return hipErrorInvalidValue;
 }
@@ -1165,8 +1227,9 @@ hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const f
 hipError_t dispatch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                          const Hyp<float> &h, void *ws, hipStream_t st) {
 #define GPPS_G(I, Q) \
-    if (p.ni == I && p.nqb == Q) return launch_grad<I, Q>(p, s, mu, Z, h, ws, st);
-    GPPS_G(1, 1) GPPS_G(2, 1) GPPS_G(2, 2) GPPS_G(3, 2) GPPS_G(4, 2)
+    if (p.nk == I && p.nqb == Q) return launch_grad<I, Q>(p, s, mu, Z, h, ws, st);
+    GPPS_G(1, 1) GPPS_G(2, 1) GPPS_G(3, 1) GPPS_G(4, 1) GPPS_G(6, 1) GPPS_G(8, 1)
+    GPPS_G(8, 2) GPPS_G(10, 2) GPPS_G(12, 2)
 #undef GPPS_G
     return hipErrorInvalidValue;
 }
@@ -1211,7 +1274,7 @@ bool mfma_supports(const Shape &s) {
     const int64_t Mp = cdiv(s.M, kTile) * kTile;
     if (!((Mp <= 512 && s.Q <= 31) || (Mp <= 256 && s.Q <= GPPS_MAX_Q_MFMA))) return false;
     const MPlan p = make_mplan(s);
-    return p.lds_grad <= 160 * 1024 && p.lds_fwd <= 160 * 1024;
+    return p.nk > 0 && p.lds_grad <= 160 * 1024 && p.lds_fwd <= 160 * 1024;
 }
 
 size_t mfma_workspace_bytes(const Shape &s) { return make_mplan(s).total; }

@@ -421,3 +421,19 @@ def test_far_inducing_points_underflow_cleanly(path):
     for k, v in got.items():
         assert np.all(np.isfinite(v)), k
     compare_all(got, run_oracle(inp), TOL32, "far")
+
+
+# Dimensions at both ends of every instruction count of the matrix-core Gram
+# product: the three fp16 cross products of each dimension share one packed K
+# range (Q <= 4, 8, 14, 20, 30, 40, 52, 62 take 1, 2, 3, 4, 6, 8, 10, 12
+# instructions), so a slot misplaced in the layout shows up at one of these.
+GRAM_Q = [4, 5, 8, 9, 14, 15, 20, 21, 30, 31, 32, 40, 41, 52, 53, 62]
+
+
+@pytest.mark.parametrize("Q", GRAM_Q)
+def test_mfma_gram_layout_dimensions(Q):
+    use_path("mfma", torch.float32)
+    say(f"[gram layout Q={Q}]")
+    inp = synth.to_f32(synth.random_inputs(300, 70, Q, seed=100 + Q))
+    got = run_gpu(inp, torch.float32)
+    compare_all(got, run_oracle(inp), TOL32, f"gram-Q{Q}")

@@ -14,8 +14,8 @@
 // same order as the rounding the fp32 row terms already carry.  Range: the
 // constant operand is the centred z table (|z| << 6e4); the per-datapoint one
 // is -K d (|K d| is a few lengthscales' worth, far inside fp16) plus the row
-// bias b + c in one k slot, clamped to +-kBiasClamp: a bias beyond that makes
-// the summand vanish in fp32 anyway.  W in the gradient's second product is
+// bias b + c as two fp16 parts in two k slots, clamped to +-kBiasClamp: a bias
+// beyond that makes the summand vanish in fp32 anyway.  W in the gradient's second product is
 // scaled per datapoint by a power of two that bounds it by 2^14, and the
 // product is scaled back exactly.  The f16 MFMA does 16 times the work per
 // cycle of v_mfma_f32_32x32x2_f32 and, unlike it, lets the vector ALU issue
@@ -88,6 +88,7 @@ constexpr float kBiasClamp = 6.0e4f;   // bias carried in an fp16 Gram k slot (f
 constexpr int kRB = 8;                 // gradient: rows per batch
 constexpr int kFRB = 4;                // forward: rows per batch (prefetched a batch ahead)
 constexpr int kFPF = kFRB * 512 / 256; // forward: per-thread prefetch slots of a [kFRB][Mp] table
+constexpr int kGPF = 4;                // gradient: per-thread load slots of a [kRB][Mp] table
 static_assert(kFRB * kRowStride == kThreads, "one mu / kappa value per forward thread");
 constexpr int64_t kCUs = 256;          // compute units of one MI355X
 constexpr int64_t kLdsBytes = 160 * 1024;
@@ -802,14 +803,14 @@ __device__ void stage_zh(_Float16 *zh, int jr, int M, int Q, int nqb,
 // blocks j (the m' index) of the workgroup's range jr.  Tile (j, i), rows m' in
 // block j, columns m in block i:
 //   e[m'][m] = b_m' + (b + c)_m + sum_q z_m'q (-K d_mq)   (A: [z | 1], B: [-K d | b + c])
-// W = G2s o exp2(e); then V' += W [Z | 1].  Both products run on bf16 MFMAs with
-// both operands split into three bf16 parts (six cross products; the dropped
-// ones are below 2^-24 relative), which keeps fp32 accuracy.  The column term
-// rides in k slot Q, the row term is the accumulator's start value.  The task's
-// dL/dPsi2 tiles stay in
-// registers for the whole kernel; the epilogue turns V' into the task's share
-// of dZ (registers) and of the per-row sums, which the workgroup combines in LDS
-// and writes per (group, row) for psi2_finalize_kernel.
+// W = G2s o exp2(e); then V' += W [Z | 1].  Both products run on f16 MFMAs with
+// both operands split into two fp16 parts (three cross products, the Gram's in
+// the packed K layout), which keeps fp32 accuracy.  The column term rides in its
+// own pair of k slots, the row term is the accumulator's start value.  The
+// task's dL/dPsi2 tiles stay in registers for the whole kernel; the epilogue
+// turns V' into the task's share of dZ (registers) and of the per-row sums,
+// which the workgroup combines in LDS and writes per (group, row) for
+// psi2_finalize_kernel.
 template <int NK, int NQB, int JPW = grad_jpw(NQB)>
 __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int DSF, int njr, int wpg, int igroups,
@@ -875,32 +876,69 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     const float lg = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
     stage_za<NK>(za, jr * JPW, JPW, nb, M, Q, Z, zc);
 
+    // Batches of kRB rows staged in LDS between two barriers.  All loads of a
+    // batch are issued before any LDS write (the first kGPF * blockDim entries of
+    // each [kRB][Mp] table and one entry of each [kRB][64] table per thread; any
+    // rest is loaded afterwards), so that the batch waits for one round trip to
+    // memory rather than one per loop pass.
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
+    const int tid = threadIdx.x, nthr = blockDim.x;
     for (int64_t n0 = r0; n0 < r1; n0 += kRB) {
         const int cb = (int)min<int64_t>(kRB, r1 - n0);
         __syncthreads();
-        for (int k = threadIdx.x; k < kRB * kRowStride; k += blockDim.x) {
-            const int r = k / kRowStride, q = k - r * kRowStride;
-            const bool ok = r < cb && q < Q;
-            lds[L.mub + k] = ok ? mu[(n0 + r) * Q + q] - zc[q] : 0.f;
-            lds[L.kb + k] = ok ? Kt[(n0 + r) * kRowStride + q] : 0.f;
+        {
+            float pb[kGPF], pc[kGPF], pt[kGPF], pmu = 0.f, pk = 0.f, pw1 = 0.f, pw2 = 0.f, phl = 0.f;
+#pragma unroll
+            for (int j = 0; j < kGPF; ++j) {
+                const int k = tid + j * nthr;
+                const bool ok = k < cb * Mp;
+                pb[j] = ok ? bt[n0 * Mp + k] : kPadBias;
+                pc[j] = ok ? bc[n0 * Mp + k] : kPadBias;
+                pt[j] = ok ? t1g[n0 * Mp + k] : 0.f;
+            }
+            const int r = tid / kRowStride, q = tid - r * kRowStride;
+            const bool okr = tid < kRB * kRowStride && r < cb && q < Q;
+            if (okr) {
+                pmu = mu[(n0 + r) * Q + q] - zc[q];
+                pk = Kt[(n0 + r) * kRowStride + q];
+                pw1 = w1t[(n0 + r) * Q + q];
+                pw2 = w2t[(n0 + r) * Q + q];
+            }
+            if (tid < cb) phl = hl[n0 + tid];
+#pragma unroll
+            for (int j = 0; j < kGPF; ++j) {
+                const int k = tid + j * nthr;
+                if (k < kRB * Mp) {
+                    lds[L.bb + k] = pb[j];
+                    lds[L.bcb + k] = pc[j];
+                    lds[L.t1 + k] = pt[j];
+                }
+            }
+            if (tid < kRB * kRowStride) {
+                lds[L.mub + tid] = pmu;
+                lds[L.kb + tid] = pk;
+                lds[L.w1b + tid] = pw1;
+                lds[L.w2b + tid] = pw2;
+            }
+            if (tid < kRB)
+                lds[L.sc + tid] = tid < cb ? fminf(120.f, fmaxf(-120.f, floorf(14.f - 2.f * phl - lg)))
+                                           : 0.f;
         }
-        for (int k = threadIdx.x; k < kRB * Mp; k += blockDim.x) {
+        for (int k = tid + kGPF * nthr; k < kRB * Mp; k += nthr) {
             const bool ok = k < cb * Mp;
             lds[L.bb + k] = ok ? bt[n0 * Mp + k] : kPadBias;
             lds[L.bcb + k] = ok ? bc[n0 * Mp + k] : kPadBias;
             lds[L.t1 + k] = ok ? t1g[n0 * Mp + k] : 0.f;
         }
-        for (int k = threadIdx.x; k < kRB * kRowStride; k += blockDim.x) {
+        for (int k = tid + nthr; k < kRB * kRowStride; k += nthr) {
             const int r = k / kRowStride, q = k - r * kRowStride;
             const bool ok = r < cb && q < Q;
+            lds[L.mub + k] = ok ? mu[(n0 + r) * Q + q] - zc[q] : 0.f;
+            lds[L.kb + k] = ok ? Kt[(n0 + r) * kRowStride + q] : 0.f;
             lds[L.w1b + k] = ok ? w1t[(n0 + r) * Q + q] : 0.f;
             lds[L.w2b + k] = ok ? w2t[(n0 + r) * Q + q] : 0.f;
         }
-        for (int r = threadIdx.x; r < kRB; r += blockDim.x)
-            lds[L.sc + r] = r < cb ? fminf(120.f, fmaxf(-120.f, floorf(14.f - 2.f * hl[n0 + r] - lg)))
-                                   : 0.f;
         __syncthreads();
         for (int r = 0; r < cb; ++r) {
             float *rs = lds + L.red + (r * wpg + wave) * RED;

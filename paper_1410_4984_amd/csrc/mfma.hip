@@ -123,14 +123,17 @@ __device__ inline void fwd_task(int task, int nb, int tpw, int &ti, int &tj0) {
     tj0 = ti + task * tpw;
 }
 
-// Packed Gram layout over NK 16-slot f16 MFMA instructions.  Each lane group
-// (g = lane / 32) holds 8 k slots per instruction, 4 NK packed f16 pairs
-// (dwords) in all, and takes the gram_t(NK) dimensions q = g T .. g T + T - 1:
-//   dwords [0, NP)       (hi_a, hi_b) of dimension pair p      (A: z_hi, z_hi)
-//          [NP, 2NP)     (lo_a, lo_b)                           (A: z_hi, z_hi)
-//          [2NP, 3NP)    (hi_a, hi_b) again                     (A: z_lo, z_lo)
-//          one odd dimension s, if any: (hi_s, lo_s), (hi_s, 0)  (A: (z_hi, z_hi), (z_lo, 0))
-//          the bias: (hi, lo) of b + c (lane group 1; zero in group 0)  (A: 1, 1)
+// Packed Gram layout over NK 16-slot f16 MFMA instructions.  The per-datapoint
+// operand (B, column m) holds the fp16 parts hi + lo of x_q = (z_mq - mu_q) K_q,
+// the constant one (A, row m') those of the centred z_m'q; the three kept cross
+// products share one K range.  Each lane group (g = lane / 32) holds 8 k slots
+// per instruction, 4 NK packed f16 pairs (dwords) in all, and takes the
+// T = gram_t(NK) dimensions q = g T .. g T + T - 1, in pairs (a, b):
+//   dwords [0, NP)       B (x_hi,a, x_hi,b)   A (z_hi,a, z_hi,b)
+//          [NP, 2NP)     B (x_lo,a, x_lo,b)   A (z_hi,a, z_hi,b)
+//          [2NP, 3NP)    B (x_hi,a, x_hi,b)   A (z_lo,a, z_lo,b)
+//          an odd dimension s, if any: B (x_hi, x_lo), (x_hi, 0); A (z_hi, z_hi), (z_lo, 0)
+//          the bias b + c: B (hi, lo) in lane group 1, zero in group 0; A (1, 1)
 //          zero beyond.
 // Dimensions past Q have zero z, mu and K, so their slots contribute nothing.
 constexpr int gram_np(int nk) { return (4 * nk - 1) / 3; }

@@ -311,7 +311,7 @@ float *fat(void *ws, size_t off) { return reinterpret_cast<float *>(static_cast<
 
 // ---------------------------------------------------------------- small kernels
 // Per-row tables, 64 datapoints per workgroup.  For every (n, q):
-//   K[n][q]  = log2e S / (l^2 (l^2 + 2S))  (zero for q >= Q up to the stride)
+//   K[n][q]  = log2e S / (l^2 (l^2 + 2S))  (row stride 64; entries q >= Q are never read)
 //   hq[n][q] = -log2e/4 (1/l^2 + w2),  w2[n][q] = 1/(l^2 + 2S),  w1[n][q] = 1/(l^2 + S)
 // (one pass over the workgroup's (row, dimension) pairs, coalesced), then per row
 //   hl[n]    = log2e (log sf2 - 1/4 sum_q log(1 + 2S/l^2))   (Psi2 prefactor, half of it)
@@ -337,11 +337,6 @@ __global__ __launch_bounds__(256) void mfma_rows_kernel(
         w1t[k] = 1.f / (l2 + sv);
         la2[r][q] = log1pf(2.f * sv / l2);
         la1[r][q] = log1pf(sv / l2);
-    }
-    const int pad = kRowStride - Q;
-    for (int i = threadIdx.x; i < rows * pad; i += 256) {
-        const int r = i / pad, q = Q + (i - r * pad);
-        Kt[(n0 + r) * kRowStride + q] = 0.f;
     }
     __syncthreads();
     const int r = threadIdx.x;

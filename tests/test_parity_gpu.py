@@ -437,3 +437,15 @@ def test_mfma_gram_layout_dimensions(Q):
     inp = synth.to_f32(synth.random_inputs(300, 70, Q, seed=100 + Q))
     got = run_gpu(inp, torch.float32)
     compare_all(got, run_oracle(inp), TOL32, f"gram-Q{Q}")
+
+
+# Ragged ranges of row blocks on the matrix-core path: M = 257 (9 blocks of 32,
+# three ranges of four, the last with one real block) at Q = 20, and M = 300 at
+# Q = 31 (eight Gram instructions, the widest single [Z | 1] column block).
+@pytest.mark.parametrize("N,M,Q", [(400, 257, 20), (300, 300, 31)])
+def test_mfma_ragged_block_ranges(N, M, Q):
+    use_path("mfma", torch.float32)
+    say(f"[ragged ranges N={N} M={M} Q={Q}]")
+    inp = synth.to_f32(synth.random_inputs(N, M, Q, seed=200 + M))
+    got = run_gpu(inp, torch.float32)
+    compare_all(got, run_oracle(inp), TOL32, f"ragged-{M}x{Q}")

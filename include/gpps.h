@@ -23,7 +23,7 @@
  *     inputs X themselves, the sparse GP regression case of section 2,
  *     eq. (boundF).  The statistics are then the plain kernel quantities
  *     (psi0 = N sigma_f2, Psi1 = Kfu, Psi2 = Kfu^T Kfu) and run on a separate
- *     matrix-core GEMM path (both dtypes) whatever gpps_set_path selected;
+ *     matrix-core GEMM path (both dtypes) whatever path flag the call carries;
  *     dmu is dL/dX and dS may be NULL (it is not written).
  *   - sigma_f2 and l (Q values) are HOST doubles, so validation needs no
  *     device synchronisation.  In the F32 path they are rounded to float.
@@ -35,11 +35,13 @@
  *     the call returns without synchronising: outputs are valid once the
  *     stream has been synchronised.  The workspace must not be reused by
  *     another call that may run concurrently.
- *   - accumulate = 0 overwrites the N-summed outputs; accumulate = 1 adds to
- *     them.  This is how N is split into row chunks (section 2: every
- *     data-dependent quantity is a sum over datapoints, so partial results
- *     over disjoint row sets add up).  Per-row outputs (Psi1, dmu, dS) are
- *     always overwritten for the rows passed.
+ *   - flags is a bitwise or of GPPS_ACCUMULATE and at most one path flag.
+ *     Without GPPS_ACCUMULATE the N-summed outputs are overwritten; with it
+ *     they are added to.  This is how N is split into row chunks (section 2:
+ *     every data-dependent quantity is a sum over datapoints, so partial
+ *     results over disjoint row sets add up).  Per-row outputs (Psi1, dmu, dS)
+ *     are always overwritten for the rows passed.  The path flags choose the
+ *     kernels per call (the library keeps no path setting of its own).
  *   - Results are bitwise deterministic for fixed (dt, N, M, Q), path and
  *     device: no floating-point atomics are used; every reduction runs in a
  *     fixed order.
@@ -70,14 +72,25 @@ typedef enum {
     GPPS_ERR_WORKSPACE = 5, /* workspace smaller than gpps_workspace_bytes()           */
     GPPS_ERR_ALIGN = 6,     /* workspace not 256-byte aligned or an array misaligned   */
     GPPS_ERR_HIP = 7,       /* a HIP runtime call or kernel launch failed              */
-    GPPS_ERR_PATH = 8       /* unknown path, or the requested path cannot run this call */
+    GPPS_ERR_PATH = 8       /* unknown flag bits, both path flags, or the requested path
+                               cannot run this call */
 } gpps_status;
 
-/* Kernel path used by gpps_psi_stats / gpps_psi_grads for calls with S != NULL.
- * AUTO picks the fastest path that supports the call (the matrix-core path for
- * F32 when M >= 2 and Q <= GPPS_MAX_Q_MFMA, the generic vector path otherwise).
- * Calls with S = NULL always take the known-input path. */
-typedef enum { GPPS_PATH_AUTO = 0, GPPS_PATH_GENERIC = 1, GPPS_PATH_MFMA = 2 } gpps_path;
+/* Flags of gpps_psi_stats / gpps_psi_grads (and the path flags of gpps_bound).
+ *
+ * With neither path flag the call takes the fastest path that supports it: the
+ * matrix-core path for F32 shapes within its limits (M rounded up to 32 at most
+ * 512 with Q <= 31, or at most 256 with Q <= GPPS_MAX_Q_MFMA), the generic vector
+ * path otherwise.  GPPS_PATH_GENERIC forces the generic path; GPPS_PATH_MFMA
+ * asks for the matrix-core path and fails with GPPS_ERR_PATH where it cannot
+ * take the call.  The matrix-core path carries its operands as two-part fp16
+ * values; a device-side range guard bounds them over every row first, and when a
+ * bound leaves the fp16 range the call is computed by the generic kernels
+ * instead, with either flag (see gpps_route_word_offset).  Calls with S = NULL
+ * always take the known-input path. */
+#define GPPS_ACCUMULATE 1
+#define GPPS_PATH_GENERIC 2
+#define GPPS_PATH_MFMA 4
 
 #define GPPS_MAX_Q 64
 #define GPPS_MAX_M 4096
@@ -89,6 +102,15 @@ typedef enum { GPPS_PATH_AUTO = 0, GPPS_PATH_GENERIC = 1, GPPS_PATH_MFMA = 2 } g
  * (the larger of the two, over every path).  0 for an invalid shape or dtype. */
 size_t gpps_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q);
 
+/* Diagnostics: byte offset, inside the workspace of a gpps_psi_stats,
+ * gpps_psi_grads or gpps_bound call of this shape, of a 32-bit "route word".
+ * Calls that take the matrix-core path (F32, S != NULL) write it: 0 when the
+ * matrix cores computed the call, 1 when the range guard found an operand
+ * outside the fp16 range and the generic kernels computed it.  Other calls
+ * leave it unchanged.  Valid once the call's stream has been synchronised.
+ * SIZE_MAX for an invalid shape or dtype. */
+size_t gpps_route_word_offset(gpps_dtype dt, int64_t N, int64_t M, int64_t Q);
+
 /*
  * Forward statistics — section 2, eq. (4) (phi, Phi, Psi as expectations under
  * q(X)); Alg. 1 (Psi_nm per datapoint and inducing input, Phi summed over
@@ -98,13 +120,13 @@ size_t gpps_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q);
  *   psi0  [1]      device.  += or = N * sigma_f2
  *   Psi1  [N x M]  device, may be NULL (not computed).  Always overwritten.
  *   Psi2  [M x M]  device.  Full symmetric matrix; both triangles are bitwise
- *                  equal.  += or = according to `accumulate`.
+ *                  equal.  += or = according to GPPS_ACCUMULATE in flags.
  */
 gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
                            const void *mu, const void *S, const void *Z,
                            double sigma_f2, const double *l,
                            void *psi0, void *Psi1, void *Psi2,
-                           int accumulate, void *workspace, size_t workspace_bytes,
+                           int flags, void *workspace, size_t workspace_bytes,
                            void *stream);
 
 /*
@@ -119,7 +141,7 @@ gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
  *   dL_dPsi2 [M x M]    device, or NULL for zero.  Need not be symmetric: only its
  *                       symmetric part affects L, since Psi2 is symmetric.
  *   dmu, dS  [N x Q]    device, always overwritten (dS may be NULL when S is NULL).
- *   dZ       [M x Q]    device, += or = according to `accumulate`.
+ *   dZ       [M x Q]    device, += or = according to GPPS_ACCUMULATE in flags.
  *   dsigma_f2 [1]       device, += or =.
  *   dl       [Q]        device, += or =.
  */
@@ -128,7 +150,7 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
                            double sigma_f2, const double *l, double dL_dpsi0,
                            const void *dL_dPsi1, const void *dL_dPsi2,
                            void *dmu, void *dS, void *dZ, void *dsigma_f2, void *dl,
-                           int accumulate, void *workspace, size_t workspace_bytes,
+                           int flags, void *workspace, size_t workspace_bytes,
                            void *stream);
 
 /* Bytes of workspace gpps_bound needs for this shape with D output columns.
@@ -149,8 +171,9 @@ size_t gpps_bound_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q
  *
  * and dL w.r.t. mu, S, Z, sigma_f2, every l_q and beta (the parameters the paper
  * optimises).  The psi-statistics and their gradients run on the same kernels
- * as gpps_psi_stats / gpps_psi_grads (and the same path choice); the M x M
- * algebra runs in fp64 for either dtype.
+ * as gpps_psi_stats / gpps_psi_grads, with the path chosen by the path flags of
+ * `flags` (GPPS_ACCUMULATE is not allowed here); the M x M algebra runs in fp64
+ * for either dtype.
  *
  *   Y        [N x D]   device, observed data (dtype dt).
  *   beta               host: noise precision, finite and > 0.
@@ -174,13 +197,8 @@ gpps_status gpps_bound(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D
                        const void *mu, const void *S, const void *Z, const void *Y,
                        double sigma_f2, const double *l, double beta, double jitter,
                        void *L, void *dmu, void *dS, void *dZ, void *dsigma_f2, void *dl,
-                       void *dbeta, void *workspace, size_t workspace_bytes, void *stream);
-
-/* Select the kernel path for later calls in this process (default AUTO).
- * Process-wide setting: do not change it while another thread is inside a
- * gpps call.  Returns GPPS_ERR_PATH for an unknown value. */
-gpps_status gpps_set_path(gpps_path path);
-gpps_path gpps_get_path(void);
+                       void *dbeta, int flags, void *workspace, size_t workspace_bytes,
+                       void *stream);
 
 /* Kernel timing for benchmarks.  While enabled (on != 0), every kernel launch
  * of the library is bracketed by two HIP events recorded on the call's stream.

@@ -27,11 +27,13 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgpps.so")
 
 F32, F64 = 0, 1
-PATHS = {"auto": 0, "generic": 1, "mfma": 2}
+ACCUMULATE = 1
+PATHS = {"auto": 0, "generic": 2, "mfma": 4}   # path flags of the C ABI
 MAX_Q = 64
 MAX_M = 4096
 
 _lib = None
+_default_path = "auto"
 
 
 class GppsError(RuntimeError):
@@ -53,6 +55,8 @@ def lib():
     i64, vp, d, sz, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_double, ctypes.c_size_t, ctypes.c_int
     L.gpps_workspace_bytes.argtypes = [i32, i64, i64, i64]
     L.gpps_workspace_bytes.restype = sz
+    L.gpps_route_word_offset.argtypes = [i32, i64, i64, i64]
+    L.gpps_route_word_offset.restype = sz
     L.gpps_psi_stats.argtypes = [i32, i64, i64, i64, vp, vp, vp, d, vp, vp, vp, vp, i32, vp, sz, vp]
     L.gpps_psi_stats.restype = i32
     L.gpps_psi_grads.argtypes = [i32, i64, i64, i64, vp, vp, vp, d, vp, d, vp, vp, vp, vp, vp, vp,
@@ -61,11 +65,8 @@ def lib():
     L.gpps_bound_workspace_bytes.argtypes = [i32, i64, i64, i64, i64]
     L.gpps_bound_workspace_bytes.restype = sz
     L.gpps_bound.argtypes = [i32, i64, i64, i64, i64, vp, vp, vp, vp, d, vp, d, d, vp, vp, vp, vp,
-                             vp, vp, vp, vp, sz, vp]
+                             vp, vp, vp, i32, vp, sz, vp]
     L.gpps_bound.restype = i32
-    L.gpps_set_path.argtypes = [i32]
-    L.gpps_set_path.restype = i32
-    L.gpps_get_path.restype = i32
     L.gpps_status_string.argtypes = [i32]
     L.gpps_status_string.restype = ctypes.c_char_p
     L.gpps_version.restype = i32
@@ -83,13 +84,38 @@ def status_string(status: int) -> str:
 
 
 def set_path(path: str) -> None:
-    """Select the kernel path for later calls: 'auto', 'generic' or 'mfma'."""
-    _check(lib().gpps_set_path(PATHS[path]))
+    """Default kernel path of this module's calls that pass no ``path``:
+    'auto', 'generic' or 'mfma'.  The C library itself keeps no path setting;
+    every call hands its choice over as a flag."""
+    global _default_path
+    if path not in PATHS:
+        raise ValueError(f"unknown path {path!r}")
+    _default_path = path
 
 
 def get_path() -> str:
-    v = lib().gpps_get_path()
-    return {v_: k for k, v_ in PATHS.items()}[v]
+    return _default_path
+
+
+def _flags(path, accumulate=False) -> int:
+    path = _default_path if path is None else path
+    if path not in PATHS:
+        raise ValueError(f"unknown path {path!r}")
+    return PATHS[path] | (ACCUMULATE if accumulate else 0)
+
+
+def route_word_offset(dtype, N: int, M: int, Q: int) -> int:
+    return int(lib().gpps_route_word_offset(_dt(dtype), N, M, Q))
+
+
+def route_taken(workspace, dtype, N: int, M: int, Q: int) -> int:
+    """The route word a matrix-core call left in ``workspace`` (synchronises):
+    0 = computed on the matrix cores, 1 = the range guard sent it to the
+    generic kernels."""
+    import torch
+    off = route_word_offset(dtype, N, M, Q)
+    torch.cuda.synchronize(workspace.device)
+    return int(workspace[off:off + 4].cpu().view(torch.int32).item())
 
 
 def workspace_bytes(dtype, N: int, M: int, Q: int) -> int:
@@ -150,12 +176,13 @@ def _stream(stream):
 
 
 def psi_stats(mu, S, Z, sigma_f2, l, *, want_psi1=True, accumulate=False, out=None,
-              workspace=None, stream=None):
+              workspace=None, stream=None, path=None):
     """Forward statistics (section 2, eq. (4); Alg. 1).
 
     Returns (psi0 [1], Psi1 [N x M] or None, Psi2 [M x M]).  With
     ``accumulate=True`` and ``out=(psi0, Psi1, Psi2)`` the N-summed outputs are
     added to the given tensors (row chunking); Psi1 rows are always written.
+    ``path``: 'auto', 'generic' or 'mfma' (default: the module default).
     """
     import torch
     dtype, device = mu.dtype, mu.device
@@ -180,12 +207,12 @@ def psi_stats(mu, S, Z, sigma_f2, l, *, want_psi1=True, accumulate=False, out=No
     _check(lib().gpps_psi_stats(
         _dt(dtype), N, M, Q, mu.data_ptr(), None if S is None else S.data_ptr(), Z.data_ptr(),
         float(sigma_f2), lh.ctypes.data, psi0.data_ptr(), None if Psi1 is None else Psi1.data_ptr(),
-        Psi2.data_ptr(), int(bool(accumulate)), ws.data_ptr(), ws_bytes, _stream(stream)))
+        Psi2.data_ptr(), _flags(path, accumulate), ws.data_ptr(), ws_bytes, _stream(stream)))
     return psi0, Psi1, Psi2
 
 
 def psi_grads(mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2, *, accumulate=False,
-              out=None, workspace=None, stream=None):
+              out=None, workspace=None, stream=None, path=None):
     """Gradients of L = dL_dpsi0 psi0 + <dL_dPsi1, Psi1> + <dL_dPsi2, Psi2> (Alg. 2).
 
     ``dL_dPsi1`` / ``dL_dPsi2`` may be None (zero).  Returns a dict with dmu, dS
@@ -224,7 +251,8 @@ def psi_grads(mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2, *, accumulate
         _dt(dtype), N, M, Q, mu.data_ptr(), ptr(S), Z.data_ptr(), float(sigma_f2),
         lh.ctypes.data, float(dL_dpsi0), ptr(dL_dPsi1), ptr(dL_dPsi2), out["dmu"].data_ptr(),
         ptr(None if S is None else out["dS"]), out["dZ"].data_ptr(), out["dsigma_f2"].data_ptr(),
-        out["dl"].data_ptr(), int(bool(accumulate)), ws.data_ptr(), ws_bytes, _stream(stream)))
+        out["dl"].data_ptr(), _flags(path, accumulate), ws.data_ptr(), ws_bytes,
+        _stream(stream)))
     return out
 
 
@@ -232,7 +260,8 @@ def bound_workspace_bytes(dtype, N: int, M: int, Q: int, D: int) -> int:
     return int(lib().gpps_bound_workspace_bytes(_dt(dtype), N, M, Q, D))
 
 
-def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter=0.0, *, out=None, workspace=None, stream=None):
+def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter=0.0, *, out=None, workspace=None, stream=None,
+          path=None):
     """The Bayesian GP-LVM bound L = <F>_q(X) - KL and its gradients (section 2,
     eq. (boundF) with the psi-statistics as expectations, eq. (boundBGPLVM)).
 
@@ -276,5 +305,5 @@ def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter=0.0, *, out=None, workspace=Non
         out["L"].data_ptr(), out["dmu"].data_ptr(),
         None if S is None else out["dS"].data_ptr(), out["dZ"].data_ptr(),
         out["dsigma_f2"].data_ptr(), out["dl"].data_ptr(), out["dbeta"].data_ptr(),
-        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+        _flags(path), workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
     return out

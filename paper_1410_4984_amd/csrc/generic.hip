@@ -33,6 +33,7 @@ constexpr int kRowBlock = 64;    // threads (rows) per block in the gradient row
 constexpr int kColBlock = 64;    // threads (inducing inputs) per block in the column kernel
 constexpr int kBand = 8;         // symmetric pairs kernel: pair offsets k per LDS exchange
 constexpr int kSlotBand = 4;     // ... the same with several rows at a time
+constexpr int64_t kGridCap = 2048;  // workgroups of the grid-stride kernels
 
 __device__ inline float dexp(float x) { return __expf(x); }
 __device__ inline double dexp(double x) { return exp(x); }
@@ -129,9 +130,10 @@ T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(w
 
 // ---------------------------------------------------------------- per-row tables
 template <typename T>
-__global__ void rows_pre_kernel(int64_t N, int Q, const T *__restrict__ S, Hyp<T> h,
+__global__ void rows_pre_kernel(const int *__restrict__ gate, int64_t N, int Q, const T *__restrict__ S, Hyp<T> h,
                                 T *__restrict__ w1, T *__restrict__ w2, T *__restrict__ lp1,
                                 T *__restrict__ lp2) {
+    if (gate && gate[0] == 0) return;
     int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (n >= N) return;
     T a = h.log_sf2, b = T(2) * h.log_sf2;
@@ -149,27 +151,31 @@ __global__ void rows_pre_kernel(int64_t N, int Q, const T *__restrict__ S, Hyp<T
 
 // ---------------------------------------------------------------- Psi1 (Alg. 1, Psi)
 template <typename T>
-__global__ void psi1_kernel(int64_t N, int M, int Q, const T *__restrict__ mu,
+__global__ void psi1_kernel(const int *__restrict__ gate, int64_t N, int M, int Q, const T *__restrict__ mu,
                             const T *__restrict__ Z, const T *__restrict__ w1,
                             const T *__restrict__ lp1, T *__restrict__ Psi1) {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= N * M) return;
-    int64_t n;
-    int m;
-    if (i <= 0x7fffffff) {  // 32-bit division where the index fits
-        const unsigned u = (unsigned)i, nn = u / (unsigned)M;
-        n = nn;
-        m = (int)(u - nn * (unsigned)M);
-    } else {
-        n = i / M;
-        m = (int)(i - n * M);
+    if (gate && gate[0] == 0) return;
+    // grid-stride over the N x M entries (the grid is capped, so that a call
+    // whose gate is closed dispatches few workgroups)
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N * M;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t n;
+        int m;
+        if (i <= 0x7fffffff) {  // 32-bit division where the index fits
+            const unsigned u = (unsigned)i, nn = u / (unsigned)M;
+            n = nn;
+            m = (int)(u - nn * (unsigned)M);
+        } else {
+            n = i / M;
+            m = (int)(i - n * M);
+        }
+        T s = 0;
+        for (int q = 0; q < Q; ++q) {
+            T d = mu[n * Q + q] - Z[(int64_t)m * Q + q];
+            s += d * d * w1[n * Q + q];
+        }
+        Psi1[i] = dexp(lp1[n] - T(0.5) * s);
     }
-    T s = 0;
-    for (int q = 0; q < Q; ++q) {
-        T d = mu[n * Q + q] - Z[(int64_t)m * Q + q];
-        s += d * d * w1[n * Q + q];
-    }
-    Psi1[i] = dexp(lp1[n] - T(0.5) * s);
 }
 
 __device__ inline int64_t pair_index(int64_t m, int64_t mp, int64_t M) {
@@ -194,10 +200,11 @@ __device__ inline void pair_coords(int64_t t, int64_t M, int &m, int &mp) {
 // One thread per unique pair (consecutive pairs of the row-major upper
 // triangle, so no lane idles below the diagonal) and row chunk.
 template <typename T, int QM>
-__global__ __launch_bounds__(256) void psi2_partial_kernel(
+__global__ __launch_bounds__(256) void psi2_partial_kernel(const int *__restrict__ gate, 
     int64_t N, int M, int Q, int64_t P, int64_t rows_per_chunk,
     const T *__restrict__ mu, const T *__restrict__ Z, const T *__restrict__ w2,
     const T *__restrict__ lp2, Hyp<T> h, T *__restrict__ partial) {
+    if (gate && gate[0] == 0) return;
     __shared__ T s_mu[kFwdTile][QM];
     __shared__ T s_w2[kFwdTile][QM];
     __shared__ T s_lp[kFwdTile];
@@ -248,9 +255,10 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(
 
 // Fixed-order sum of the chunk partials; writes both triangles and psi0.
 template <typename T>
-__global__ void psi2_reduce_kernel(int64_t N, int M, int64_t P, int64_t nchunks,
+__global__ void psi2_reduce_kernel(const int *__restrict__ gate, int64_t N, int M, int64_t P, int64_t nchunks,
                                    const T *__restrict__ partial, Hyp<T> h, T *__restrict__ psi0,
                                    T *__restrict__ Psi2, int accumulate) {
+    if (gate && gate[0] == 0) return;
     const int mp = blockIdx.x * kPairTile + threadIdx.x % kPairTile;
     const int m = blockIdx.y * kPairTile + threadIdx.x / kPairTile;
     if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
@@ -275,7 +283,8 @@ __global__ void psi2_reduce_kernel(int64_t N, int M, int64_t P, int64_t nchunks,
 
 // ---------------------------------------------------------------- gradients (Alg. 2)
 template <typename T>
-__global__ void sym_kernel(int M, const T *__restrict__ G2, T *__restrict__ G2s) {
+__global__ void sym_kernel(const int *__restrict__ gate, int M, const T *__restrict__ G2, T *__restrict__ G2s) {
+    if (gate && gate[0] == 0) return;
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)M * M) return;
     int m = (int)(i / M), mp = (int)(i - (int64_t)m * M);
@@ -285,7 +294,8 @@ __global__ void sym_kernel(int M, const T *__restrict__ G2, T *__restrict__ G2s)
 // Gc[k][m] = G2s[m][(m + k) mod M], k = 0 .. M/2: the symmetric pairs kernel
 // reads the pair (m, m + k) of every thread m as one coalesced row.
 template <typename T>
-__global__ void circ_kernel(int M, const T *__restrict__ G2s, T *__restrict__ Gc) {
+__global__ void circ_kernel(const int *__restrict__ gate, int M, const T *__restrict__ G2s, T *__restrict__ Gc) {
+    if (gate && gate[0] == 0) return;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)(M / 2 + 1) * M) return;
     const int k = (int)(i / M), m = (int)(i - (int64_t)k * M);
@@ -298,11 +308,12 @@ __global__ void circ_kernel(int M, const T *__restrict__ G2s, T *__restrict__ Gc
 // Psi1 terms in the column tiles t = r, r + rr, ...): partial dmu_n, dS_n of the
 // range (rowg[r][2][N][Q]) and per-block partials of dl and dsf2.
 template <typename T, int QM>
-__global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
+__global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(const int *__restrict__ gate, 
     int64_t N, int M, int Q, int rr, const T *__restrict__ mu, const T *__restrict__ S,
     const T *__restrict__ Z, const T *__restrict__ w1, const T *__restrict__ w2,
     const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h, const T *__restrict__ G1,
     const T *__restrict__ G2s, T *__restrict__ rowg, T *__restrict__ rowpart) {
+    if (gate && gate[0] == 0) return;
     const int range = blockIdx.y;
     __shared__ T s_g1[kRowBlock][kRowBlock + 1];
     __shared__ T s_red[QM + 1][kRowBlock];
@@ -441,12 +452,13 @@ __global__ __launch_bounds__(kRowBlock) void grad_rows_kernel(
 // thread m + k adds it to its r and V.  The bands hold kBand offsets and are
 // double buffered: one barrier per band.
 template <typename T, int QM, bool SYM>
-__global__ __launch_bounds__(256) void grad_pairs_kernel(
+__global__ __launch_bounds__(256) void grad_pairs_kernel(const int *__restrict__ gate, 
     int64_t N, int M, int Q, int64_t rows_per_chunk, const T *__restrict__ mu,
     const T *__restrict__ S, const T *__restrict__ Z, const T *__restrict__ w1t,
     const T *__restrict__ w2t, const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h,
     const T *__restrict__ G1, const T *__restrict__ G2s, const T *__restrict__ Gc,
     T *__restrict__ rowg, T *__restrict__ colpart, T *__restrict__ rowpart) {
+    if (gate && gate[0] == 0) return;
     extern __shared__ double gp_smem[];
     T *sz = reinterpret_cast<T *>(gp_smem);  // [M][QM], zero beyond Q
     T *band = sz + M * QM;                    // [2][kBand][M] (symmetric form)
@@ -642,12 +654,13 @@ __global__ __launch_bounds__(256) void grad_pairs_kernel(
 // order, then a fixed butterfly); dZ_m adds the slots in order at the end.
 
 template <typename T, int QM>
-__global__ __launch_bounds__(512) void grad_pairs_slots_kernel(
+__global__ __launch_bounds__(512) void grad_pairs_slots_kernel(const int *__restrict__ gate, 
     int64_t N, int M, int Q, int R, int64_t rows_per_chunk, const T *__restrict__ mu,
     const T *__restrict__ S, const T *__restrict__ Z, const T *__restrict__ w1t,
     const T *__restrict__ w2t, const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h,
     const T *__restrict__ G1, const T *__restrict__ G2s, const T *__restrict__ Gc,
     T *__restrict__ rowg, T *__restrict__ colpart, T *__restrict__ rowpart) {
+    if (gate && gate[0] == 0) return;
     extern __shared__ double gs_smem[];
     T *sz = reinterpret_cast<T *>(gs_smem);        // [M][QM], zero beyond Q
     T *band = sz + M * QM;                          // [R][2][kSlotBand][M]
@@ -845,27 +858,30 @@ __global__ __launch_bounds__(512) void grad_pairs_slots_kernel(
 
 // dmu, dS: the row kernel's range partials summed in range order.
 template <typename T>
-__global__ void grad_rows_reduce_kernel(int64_t NQ, int rr, const T *__restrict__ rowg,
+__global__ void grad_rows_reduce_kernel(const int *__restrict__ gate, int64_t NQ, int rr, const T *__restrict__ rowg,
                                         T *__restrict__ dmu, T *__restrict__ dS) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= NQ) return;
-    T a = 0, b = 0;
-    for (int r = 0; r < rr; ++r) {
-        a += rowg[(int64_t)(2 * r) * NQ + i];
-        b += rowg[(int64_t)(2 * r + 1) * NQ + i];
+    if (gate && gate[0] == 0) return;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < NQ;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        T a = 0, b = 0;
+        for (int r = 0; r < rr; ++r) {
+            a += rowg[(int64_t)(2 * r) * NQ + i];
+            b += rowg[(int64_t)(2 * r + 1) * NQ + i];
+        }
+        dmu[i] = a;
+        dS[i] = b;
     }
-    dmu[i] = a;
-    dS[i] = b;
 }
 
 // One thread per inducing input m, row chunk and range of partners (m' = r,
 // r + cr, ...; the Psi1 term in range 0): partial dZ[m, :] per (chunk, range).
 template <typename T, int QM>
-__global__ __launch_bounds__(kColBlock) void grad_cols_kernel(
+__global__ __launch_bounds__(kColBlock) void grad_cols_kernel(const int *__restrict__ gate, 
     int64_t N, int M, int Q, int cr, int64_t rows_per_chunk, const T *__restrict__ mu,
     const T *__restrict__ Z, const T *__restrict__ w1, const T *__restrict__ w2,
     const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h, const T *__restrict__ G1,
     const T *__restrict__ G2s, T *__restrict__ colpart) {
+    if (gate && gate[0] == 0) return;
     __shared__ T s_mu[kRowTile][QM];
     __shared__ T s_w1[kRowTile][QM];
     __shared__ T s_w2[kRowTile][QM];
@@ -944,71 +960,76 @@ __global__ __launch_bounds__(kColBlock) void grad_cols_kernel(
 // workgroup per output; thread t sums partials t, t + 256, ..., then a fixed
 // tree combines the 256 sums.
 template <typename T>
-__global__ __launch_bounds__(256) void grad_reduce_kernel(int64_t N, int M, int Q, int64_t ncol,
+__global__ __launch_bounds__(256) void grad_reduce_kernel(const int *__restrict__ gate, int64_t N, int M, int Q, int64_t ncol,
                                                           int64_t nrow, const T *__restrict__ colpart,
                                                           const T *__restrict__ rowpart, T dL_dpsi0,
                                                           T *__restrict__ dZ, T *__restrict__ dsf2,
                                                           T *__restrict__ dl, int accumulate) {
+    if (gate && gate[0] == 0) return;
     __shared__ T red[256];
-    const int64_t i = blockIdx.x;
     const int64_t MQ = (int64_t)M * Q;
-    T s = 0;
-    if (i < MQ) {
-        for (int64_t c = threadIdx.x; c < ncol; c += 256) s += colpart[c * MQ + i];
-    } else {
-        const int k = (int)(i - MQ);  // k < Q: dl_k; k == Q: dsf2
-        for (int64_t b = threadIdx.x; b < nrow; b += 256) s += rowpart[b * (Q + 1) + k];
-    }
-    red[threadIdx.x] = s;
-    __syncthreads();
-    for (int w = 128; w >= 1; w >>= 1) {
-        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    // outputs i = blockIdx.x, blockIdx.x + gridDim.x, ... (the grid is capped)
+    for (int64_t i = blockIdx.x; i < MQ + Q + 1; i += gridDim.x) {
+        T s = 0;
+        if (i < MQ) {
+            for (int64_t c = threadIdx.x; c < ncol; c += 256) s += colpart[c * MQ + i];
+        } else {
+            const int k = (int)(i - MQ);  // k < Q: dl_k; k == Q: dsf2
+            for (int64_t b = threadIdx.x; b < nrow; b += 256) s += rowpart[b * (Q + 1) + k];
+        }
         __syncthreads();
-    }
-    if (threadIdx.x != 0) return;
-    s = red[0];
-    if (i < MQ) {
-        dZ[i] = (accumulate ? dZ[i] : T(0)) + s;
-    } else if (i < MQ + Q) {
-        dl[i - MQ] = (accumulate ? dl[i - MQ] : T(0)) + s;
-    } else {
-        s += dL_dpsi0 * T(N);
-        dsf2[0] = (accumulate ? dsf2[0] : T(0)) + s;
+        red[threadIdx.x] = s;
+        __syncthreads();
+        for (int w = 128; w >= 1; w >>= 1) {
+            if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+            __syncthreads();
+        }
+        if (threadIdx.x != 0) continue;
+        s = red[0];
+        if (i < MQ) {
+            dZ[i] = (accumulate ? dZ[i] : T(0)) + s;
+        } else if (i < MQ + Q) {
+            dl[i - MQ] = (accumulate ? dl[i - MQ] : T(0)) + s;
+        } else {
+            s += dL_dpsi0 * T(N);
+            dsf2[0] = (accumulate ? dsf2[0] : T(0)) + s;
+        }
     }
 }
 
 template <typename T, int QM>
 void launch_psi2_partial(const Shape &s, const Plan &p, const T *mu, const T *Z, const T *w2,
-                         const T *lp2, const Hyp<T> &h, T *partial, hipStream_t st) {
+                         const T *lp2, const Hyp<T> &h, T *partial, const int *gate,
+                         hipStream_t st) {
     dim3 grid((unsigned)p.pblocks, (unsigned)p.nc2);
     TimedScope ts(st, "generic_psi2_partial");
-    psi2_partial_kernel<T, QM><<<grid, 256, 0, st>>>(s.N, (int)s.M, (int)s.Q, s.P, p.rows2, mu, Z,
+    psi2_partial_kernel<T, QM><<<grid, 256, 0, st>>>(gate, s.N, (int)s.M, (int)s.Q, s.P, p.rows2, mu, Z,
                                                      w2, lp2, h, partial);
 }
 
 template <typename T, int QM>
 void launch_grads(const Shape &s, const Plan &p, const T *mu, const T *S, const T *Z,
                   const T *w1, const T *w2, const T *lp1, const T *lp2, const Hyp<T> &h,
-                  const T *G1, const T *G2s, T *rowg, T *colpart, T *rowpart,
+                  const T *G1, const T *G2s, T *rowg, T *colpart, T *rowpart, const int *gate,
                   hipStream_t st) {
     {
         TimedScope ts(st, "generic_grad_rows");
-        grad_rows_kernel<T, QM><<<dim3((unsigned)p.row_blocks, (unsigned)p.rr), kRowBlock, 0, st>>>(
+        grad_rows_kernel<T, QM><<<dim3((unsigned)p.row_blocks, (unsigned)p.rr), kRowBlock, 0, st>>>(gate, 
             s.N, (int)s.M, (int)s.Q, (int)p.rr, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg,
             rowpart);
     }
     dim3 grid((unsigned)p.col_blocks, (unsigned)p.ncc, (unsigned)p.cr);
     TimedScope ts(st, "generic_grad_cols");
-    grad_cols_kernel<T, QM><<<grid, kColBlock, 0, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.cr,
+    grad_cols_kernel<T, QM><<<grid, kColBlock, 0, st>>>(gate, s.N, (int)s.M, (int)s.Q, (int)p.cr,
                                                          p.rowsc, mu, Z, w1, w2, lp1, lp2, h, G1,
                                                          G2s, colpart);
 }
 
 template <typename T>
 void rows_pre(const Shape &s, const Plan &p, const T *S, const Hyp<T> &h, void *ws,
-              hipStream_t st) {
+              const int *gate, hipStream_t st) {
     TimedScope ts(st, "generic_rows_pre");
-    rows_pre_kernel<T><<<(unsigned)cdiv(s.N, 256), 256, 0, st>>>(
+    rows_pre_kernel<T><<<(unsigned)cdiv(s.N, 256), 256, 0, st>>>(gate, 
         s.N, (int)s.Q, S, h, at<T>(ws, p.off_w1), at<T>(ws, p.off_w2), at<T>(ws, p.off_lp1),
         at<T>(ws, p.off_lp2));
 }
@@ -1020,27 +1041,27 @@ size_t generic_workspace_bytes(const Shape &s, size_t elem) { return make_plan(s
 template <typename T>
 hipError_t generic_psi_stats(const Shape &s, const T *mu, const T *S, const T *Z,
                              const Hyp<T> &h, T *psi0, T *Psi1, T *Psi2, int accumulate,
-                             void *ws, hipStream_t st) {
+                             void *ws, const int *gate, hipStream_t st) {
     const Plan p = make_plan(s, sizeof(T));
-    rows_pre<T>(s, p, S, h, ws, st);
+    rows_pre<T>(s, p, S, h, ws, gate, st);
     const T *w1 = at<T>(ws, p.off_w1), *w2 = at<T>(ws, p.off_w2);
     const T *lp1 = at<T>(ws, p.off_lp1), *lp2 = at<T>(ws, p.off_lp2);
     if (Psi1) {
         TimedScope ts(st, "generic_psi1");
-        psi1_kernel<T><<<(unsigned)cdiv(s.N * s.M, 256), 256, 0, st>>>(s.N, (int)s.M, (int)s.Q,
+        psi1_kernel<T><<<(unsigned)std::min<int64_t>(cdiv(s.N * s.M, 256), kGridCap), 256, 0, st>>>(gate, s.N, (int)s.M, (int)s.Q,
                                                                        mu, Z, w1, lp1, Psi1);
     }
     T *partial = at<T>(ws, p.off_p2);
-    if (s.Q <= 1) launch_psi2_partial<T, 1>(s, p, mu, Z, w2, lp2, h, partial, st);
-    else if (s.Q <= 2) launch_psi2_partial<T, 2>(s, p, mu, Z, w2, lp2, h, partial, st);
-    else if (s.Q <= 4) launch_psi2_partial<T, 4>(s, p, mu, Z, w2, lp2, h, partial, st);
-    else if (s.Q <= 8) launch_psi2_partial<T, 8>(s, p, mu, Z, w2, lp2, h, partial, st);
-    else if (s.Q <= 16) launch_psi2_partial<T, 16>(s, p, mu, Z, w2, lp2, h, partial, st);
-    else if (s.Q <= 32) launch_psi2_partial<T, 32>(s, p, mu, Z, w2, lp2, h, partial, st);
-    else launch_psi2_partial<T, 64>(s, p, mu, Z, w2, lp2, h, partial, st);
+    if (s.Q <= 1) launch_psi2_partial<T, 1>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
+    else if (s.Q <= 2) launch_psi2_partial<T, 2>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
+    else if (s.Q <= 4) launch_psi2_partial<T, 4>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
+    else if (s.Q <= 8) launch_psi2_partial<T, 8>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
+    else if (s.Q <= 16) launch_psi2_partial<T, 16>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
+    else if (s.Q <= 32) launch_psi2_partial<T, 32>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
+    else launch_psi2_partial<T, 64>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
     dim3 g((unsigned)p.tiles_edge, (unsigned)p.tiles_edge);
     TimedScope ts(st, "generic_psi2_reduce");
-    psi2_reduce_kernel<T><<<g, kPairTile * kPairTile, 0, st>>>(s.N, (int)s.M, s.P, p.nc2,
+    psi2_reduce_kernel<T><<<g, kPairTile * kPairTile, 0, st>>>(gate, s.N, (int)s.M, s.P, p.nc2,
                                                                partial, h, psi0, Psi2,
                                                                accumulate);
     return hipGetLastError();
@@ -1050,16 +1071,16 @@ template <typename T>
 hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z,
                              const Hyp<T> &h, T dL_dpsi0, const T *G1, const T *G2, T *dmu,
                              T *dS, T *dZ, T *dsf2, T *dl, int accumulate, void *ws,
-                             hipStream_t st) {
+                             const int *gate, hipStream_t st) {
     const Plan p = make_plan(s, sizeof(T));
-    rows_pre<T>(s, p, S, h, ws, st);
+    rows_pre<T>(s, p, S, h, ws, gate, st);
     const T *w1 = at<T>(ws, p.off_w1), *w2 = at<T>(ws, p.off_w2);
     const T *lp1 = at<T>(ws, p.off_lp1), *lp2 = at<T>(ws, p.off_lp2);
     T *G2s = nullptr;
     if (G2) {
         G2s = at<T>(ws, p.off_g2s);
         TimedScope ts(st, "generic_sym");
-        sym_kernel<T><<<(unsigned)cdiv(s.M * s.M, 256), 256, 0, st>>>((int)s.M, G2, G2s);
+        sym_kernel<T><<<(unsigned)cdiv(s.M * s.M, 256), 256, 0, st>>>(gate, (int)s.M, G2, G2s);
     }
     T *colpart = at<T>(ws, p.off_colp), *rowpart = at<T>(ws, p.off_rowp);
     T *rowg = at<T>(ws, p.off_rowg);
@@ -1068,7 +1089,7 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
         T *Gc = at<T>(ws, p.off_gc);
         if (sym) {
             TimedScope ts(st, "generic_circ");
-            circ_kernel<T><<<(unsigned)cdiv((s.M / 2 + 1) * s.M, 256), 256, 0, st>>>((int)s.M, G2s, Gc);
+            circ_kernel<T><<<(unsigned)cdiv((s.M / 2 + 1) * s.M, 256), 256, 0, st>>>(gate, (int)s.M, G2s, Gc);
         }
         const size_t lds = sizeof(T) * s.M * (pairs_qm(s.Q) + (sym ? 2 * kBand : 0));
         const size_t lds_slots =
@@ -1079,15 +1100,15 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
 #define GPPS_PAIRS(QMV)                                                                            \
     do {                                                                                           \
         if (sym && p.pslots)                                                                       \
-            grad_pairs_slots_kernel<T, QMV><<<grid, p.psthreads, lds_slots, st>>>(                 \
+            grad_pairs_slots_kernel<T, QMV><<<grid, p.psthreads, lds_slots, st>>>(gate,                  \
                 s.N, (int)s.M, (int)s.Q, p.prs, p.prows, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s,   \
                 Gc, rowg, colpart, rowpart);                                                       \
         else if (sym)                                                                              \
-            grad_pairs_kernel<T, QMV, true><<<grid, p.pthreads, lds, st>>>(                        \
+            grad_pairs_kernel<T, QMV, true><<<grid, p.pthreads, lds, st>>>(gate,                         \
                 s.N, (int)s.M, (int)s.Q, p.prows, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, Gc,      \
                 rowg, colpart, rowpart);                                                           \
         else                                                                                       \
-            grad_pairs_kernel<T, QMV, false><<<grid, p.pthreads, lds, st>>>(                       \
+            grad_pairs_kernel<T, QMV, false><<<grid, p.pthreads, lds, st>>>(gate,                        \
                 s.N, (int)s.M, (int)s.Q, p.prows, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, Gc,      \
                 rowg, colpart, rowpart);                                                           \
     } while (0)
@@ -1103,28 +1124,28 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
         }
         const int64_t total = s.M * s.Q + s.Q + 1;
         TimedScope ts(st, "generic_grad_reduce");
-        grad_rows_reduce_kernel<T><<<(unsigned)cdiv(s.N * s.Q, 256), 256, 0, st>>>(
+        grad_rows_reduce_kernel<T><<<(unsigned)std::min<int64_t>(cdiv(s.N * s.Q, 256), kGridCap), 256, 0, st>>>(gate, 
             s.N * s.Q, (int)p.pmb, rowg, dmu, dS);
-        grad_reduce_kernel<T><<<(unsigned)total, 256, 0, st>>>(
+        grad_reduce_kernel<T><<<(unsigned)std::min<int64_t>(total, kGridCap), 256, 0, st>>>(gate, 
             s.N, (int)s.M, (int)s.Q, p.pchunks, p.pmb * p.pchunks, colpart, rowpart, dL_dpsi0, dZ,
             dsf2, dl, accumulate);
         return hipGetLastError();
     }
     if (s.Q <= 4)
-        launch_grads<T, 4>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
+        launch_grads<T, 4>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, gate, st);
     else if (s.Q <= 8)
-        launch_grads<T, 8>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
+        launch_grads<T, 8>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, gate, st);
     else if (s.Q <= 16)
-        launch_grads<T, 16>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
+        launch_grads<T, 16>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, gate, st);
     else if (s.Q <= 32)
-        launch_grads<T, 32>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
+        launch_grads<T, 32>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, gate, st);
     else
-        launch_grads<T, 64>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, st);
+        launch_grads<T, 64>(s, p, mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s, rowg, colpart, rowpart, gate, st);
     const int64_t total = s.M * s.Q + s.Q + 1;
     TimedScope ts(st, "generic_grad_reduce");
-    grad_rows_reduce_kernel<T><<<(unsigned)cdiv(s.N * s.Q, 256), 256, 0, st>>>(s.N * s.Q, (int)p.rr,
+    grad_rows_reduce_kernel<T><<<(unsigned)std::min<int64_t>(cdiv(s.N * s.Q, 256), kGridCap), 256, 0, st>>>(gate, s.N * s.Q, (int)p.rr,
                                                                               rowg, dmu, dS);
-    grad_reduce_kernel<T><<<(unsigned)total, 256, 0, st>>>(
+    grad_reduce_kernel<T><<<(unsigned)std::min<int64_t>(total, kGridCap), 256, 0, st>>>(gate, 
         s.N, (int)s.M, (int)s.Q, p.ncc * p.cr, p.rr * p.row_blocks, colpart, rowpart, dL_dpsi0,
         dZ, dsf2, dl, accumulate);
     return hipGetLastError();
@@ -1132,19 +1153,21 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
 
 template hipError_t generic_psi_stats<float>(const Shape &, const float *, const float *,
                                              const float *, const Hyp<float> &, float *,
-                                             float *, float *, int, void *, hipStream_t);
+                                             float *, float *, int, void *, const int *,
+                                             hipStream_t);
 template hipError_t generic_psi_stats<double>(const Shape &, const double *, const double *,
                                               const double *, const Hyp<double> &, double *,
-                                              double *, double *, int, void *, hipStream_t);
+                                              double *, double *, int, void *, const int *,
+                                              hipStream_t);
 template hipError_t generic_psi_grads<float>(const Shape &, const float *, const float *,
                                              const float *, const Hyp<float> &, float,
                                              const float *, const float *, float *, float *,
                                              float *, float *, float *, int, void *,
-                                             hipStream_t);
+                                             const int *, hipStream_t);
 template hipError_t generic_psi_grads<double>(const Shape &, const double *, const double *,
                                               const double *, const Hyp<double> &, double,
                                               const double *, const double *, double *,
                                               double *, double *, double *, double *, int,
-                                              void *, hipStream_t);
+                                              void *, const int *, hipStream_t);
 
 }  // namespace gpps

@@ -3,14 +3,13 @@
 // enqueues nothing and writes nothing.
 #include <hip/hip_runtime.h>
 
-#include <atomic>
 #include <cmath>
 
 #include "internal.h"
 
 namespace {
 
-std::atomic<int> g_path{GPPS_PATH_AUTO};
+constexpr int kPathAuto = 0, kPathGeneric = 1, kPathMfma = 2;
 
 bool valid_dtype(gpps_dtype dt) { return dt == GPPS_F32 || dt == GPPS_F64; }
 
@@ -41,17 +40,38 @@ gpps::Hyp<T> make_hyp(double sigma_f2, const double *l, int64_t Q) {
     return h;
 }
 
+// The path a call asks for through its flags (-1: unknown bits or both path
+// flags; `allowed` are the bits the entry point accepts).
+int requested_path(int flags, int allowed) {
+    if (flags & ~allowed) return -1;
+    const bool g = flags & GPPS_PATH_GENERIC, m = flags & GPPS_PATH_MFMA;
+    if (g && m) return -1;
+    return g ? kPathGeneric : (m ? kPathMfma : kPathAuto);
+}
+
 // Which path serves a call with variances S (or -1 if the requested one
 // cannot).  Calls without S (known inputs) always take the known-input path.
 constexpr int kPathKnown = 100;
 
-int choose_path(gpps_dtype dt, const gpps::Shape &s, const void *S) {
+int choose_path(gpps_dtype dt, const gpps::Shape &s, const void *S, int requested) {
     if (!S) return kPathKnown;
-    int p = g_path.load();
-    bool mfma_ok = dt == GPPS_F32 && gpps::mfma_supports(s);
-    if (p == GPPS_PATH_AUTO) return mfma_ok ? GPPS_PATH_MFMA : GPPS_PATH_GENERIC;
-    if (p == GPPS_PATH_MFMA) return mfma_ok ? GPPS_PATH_MFMA : -1;
-    return GPPS_PATH_GENERIC;
+    const bool mfma_ok = dt == GPPS_F32 && gpps::mfma_supports(s);
+    if (requested == kPathAuto) return mfma_ok ? kPathMfma : kPathGeneric;
+    if (requested == kPathMfma) return mfma_ok ? kPathMfma : -1;
+    return kPathGeneric;
+}
+
+// Bytes of the psi-statistic workspace before the route word (the largest
+// region of any path), and the route word's offset.
+size_t regions_bytes(gpps_dtype dt, const gpps::Shape &s) {
+    const size_t elem = dt == GPPS_F32 ? 4 : 8;
+    size_t b = std::max(gpps::generic_workspace_bytes(s, elem), gpps::known_workspace_bytes(s, elem));
+    if (dt == GPPS_F32 && gpps::mfma_supports(s)) b = std::max(b, gpps::mfma_workspace_bytes(s));
+    return gpps::align_up(b, 256);
+}
+
+int *route_word(gpps_dtype dt, const gpps::Shape &s, void *ws) {
+    return reinterpret_cast<int *>(static_cast<char *>(ws) + regions_bytes(dt, s));
 }
 
 gpps_status check_workspace(gpps_dtype dt, const gpps::Shape &s, void *ws, size_t ws_bytes) {
@@ -76,18 +96,25 @@ hipError_t run_stats(gpps_dtype dt, int path, const gpps::Shape &s, const void *
     }
     if (dt == GPPS_F32) {
         const auto h = make_hyp<float>(sigma_f2, l, s.Q);
-        if (path == GPPS_PATH_MFMA)
-            return gpps::mfma_psi_stats(s, (const float *)mu, (const float *)S, (const float *)Z, h,
-                                        (float *)psi0, (float *)Psi1, (float *)Psi2, accumulate != 0,
-                                        ws, st);
+        const int *gate = nullptr;
+        if (path == kPathMfma) {
+            // the matrix-core kernels, then the generic ones gated by the route
+            // word: only one of the two sets does the work
+            int *route = route_word(dt, s, ws);
+            hipError_t e = gpps::mfma_psi_stats(s, (const float *)mu, (const float *)S,
+                                                (const float *)Z, h, (float *)psi0, (float *)Psi1,
+                                                (float *)Psi2, accumulate != 0, route, ws, st);
+            if (e != hipSuccess) return e;
+            gate = route;
+        }
         return gpps::generic_psi_stats<float>(s, (const float *)mu, (const float *)S,
                                               (const float *)Z, h, (float *)psi0, (float *)Psi1,
-                                              (float *)Psi2, accumulate != 0, ws, st);
+                                              (float *)Psi2, accumulate != 0, ws, gate, st);
     }
     const auto h = make_hyp<double>(sigma_f2, l, s.Q);
     return gpps::generic_psi_stats<double>(s, (const double *)mu, (const double *)S,
                                            (const double *)Z, h, (double *)psi0, (double *)Psi1,
-                                           (double *)Psi2, accumulate != 0, ws, st);
+                                           (double *)Psi2, accumulate != 0, ws, nullptr, st);
 }
 
 hipError_t run_grads(gpps_dtype dt, int path, const gpps::Shape &s, const void *mu, const void *S,
@@ -107,18 +134,22 @@ hipError_t run_grads(gpps_dtype dt, int path, const gpps::Shape &s, const void *
     }
     if (dt == GPPS_F32) {
         const auto h = make_hyp<float>(sigma_f2, l, s.Q);
-        if (path == GPPS_PATH_MFMA)
-            return gpps::mfma_psi_grads(s, (const float *)mu, (const float *)S, (const float *)Z, h,
-                                        float(dL_dpsi0), (const float *)dL_dPsi1,
-                                        (const float *)dL_dPsi2, (float *)dmu, (float *)dS,
-                                        (float *)dZ, (float *)dsigma_f2, (float *)dl,
-                                        accumulate != 0, ws, st);
+        const int *gate = nullptr;
+        if (path == kPathMfma) {
+            int *route = route_word(dt, s, ws);
+            hipError_t e = gpps::mfma_psi_grads(
+                s, (const float *)mu, (const float *)S, (const float *)Z, h, float(dL_dpsi0),
+                (const float *)dL_dPsi1, (const float *)dL_dPsi2, (float *)dmu, (float *)dS,
+                (float *)dZ, (float *)dsigma_f2, (float *)dl, accumulate != 0, route, ws, st);
+            if (e != hipSuccess) return e;
+            gate = route;
+        }
         return gpps::generic_psi_grads<float>(s, (const float *)mu, (const float *)S,
                                               (const float *)Z, h, float(dL_dpsi0),
                                               (const float *)dL_dPsi1, (const float *)dL_dPsi2,
                                               (float *)dmu, (float *)dS, (float *)dZ,
                                               (float *)dsigma_f2, (float *)dl, accumulate != 0,
-                                              ws, st);
+                                              ws, gate, st);
     }
     const auto h = make_hyp<double>(sigma_f2, l, s.Q);
     return gpps::generic_psi_grads<double>(s, (const double *)mu, (const double *)S,
@@ -126,7 +157,7 @@ hipError_t run_grads(gpps_dtype dt, int path, const gpps::Shape &s, const void *
                                            (const double *)dL_dPsi1, (const double *)dL_dPsi2,
                                            (double *)dmu, (double *)dS, (double *)dZ,
                                            (double *)dsigma_f2, (double *)dl, accumulate != 0, ws,
-                                           st);
+                                           nullptr, st);
 }
 
 }  // namespace
@@ -135,16 +166,17 @@ extern "C" {
 
 size_t gpps_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q) {
     if (!valid_dtype(dt) || !valid_shape(N, M, Q)) return 0;
-    const gpps::Shape s = gpps::make_shape(N, M, Q);
-    const size_t elem = dt == GPPS_F32 ? 4 : 8;
-    size_t b = std::max(gpps::generic_workspace_bytes(s, elem), gpps::known_workspace_bytes(s, elem));
-    if (dt == GPPS_F32 && gpps::mfma_supports(s)) b = std::max(b, gpps::mfma_workspace_bytes(s));
-    return b;
+    return regions_bytes(dt, gpps::make_shape(N, M, Q)) + 256;  // + the route word
+}
+
+size_t gpps_route_word_offset(gpps_dtype dt, int64_t N, int64_t M, int64_t Q) {
+    if (!valid_dtype(dt) || !valid_shape(N, M, Q)) return SIZE_MAX;
+    return regions_bytes(dt, gpps::make_shape(N, M, Q));
 }
 
 gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
                            const void *S, const void *Z, double sigma_f2, const double *l,
-                           void *psi0, void *Psi1, void *Psi2, int accumulate, void *workspace,
+                           void *psi0, void *Psi1, void *Psi2, int flags, void *workspace,
                            size_t workspace_bytes, void *stream) {
     if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
     if (!valid_shape(N, M, Q)) return GPPS_ERR_SHAPE;
@@ -155,10 +187,13 @@ gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
     const size_t elem = dt == GPPS_F32 ? 4 : 8;
     for (const void *p : {mu, S, Z, (const void *)psi0, (const void *)Psi1, (const void *)Psi2})
         if (p && !aligned(p, elem)) return GPPS_ERR_ALIGN;
-    const int path = choose_path(dt, s, S);
+    const int req = requested_path(flags, GPPS_ACCUMULATE | GPPS_PATH_GENERIC | GPPS_PATH_MFMA);
+    if (req < 0) return GPPS_ERR_PATH;
+    const int path = choose_path(dt, s, S, req);
     if (path < 0) return GPPS_ERR_PATH;
-    const hipError_t e = run_stats(dt, path, s, mu, S, Z, sigma_f2, l, psi0, Psi1, Psi2, accumulate,
-                                   workspace, static_cast<hipStream_t>(stream));
+    const hipError_t e = run_stats(dt, path, s, mu, S, Z, sigma_f2, l, psi0, Psi1, Psi2,
+                                   flags & GPPS_ACCUMULATE, workspace,
+                                   static_cast<hipStream_t>(stream));
     return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
 }
 
@@ -166,7 +201,7 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
                            const void *S, const void *Z, double sigma_f2, const double *l,
                            double dL_dpsi0, const void *dL_dPsi1, const void *dL_dPsi2,
                            void *dmu, void *dS, void *dZ, void *dsigma_f2, void *dl,
-                           int accumulate, void *workspace, size_t workspace_bytes,
+                           int flags, void *workspace, size_t workspace_bytes,
                            void *stream) {
     if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
     if (!valid_shape(N, M, Q)) return GPPS_ERR_SHAPE;
@@ -179,10 +214,12 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
     for (const void *p : {mu, S, Z, dL_dPsi1, dL_dPsi2, (const void *)dmu, (const void *)dS,
                           (const void *)dZ, (const void *)dsigma_f2, (const void *)dl})
         if (p && !aligned(p, elem)) return GPPS_ERR_ALIGN;
-    const int path = choose_path(dt, s, S);
+    const int req = requested_path(flags, GPPS_ACCUMULATE | GPPS_PATH_GENERIC | GPPS_PATH_MFMA);
+    if (req < 0) return GPPS_ERR_PATH;
+    const int path = choose_path(dt, s, S, req);
     if (path < 0) return GPPS_ERR_PATH;
     const hipError_t e = run_grads(dt, path, s, mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2,
-                                   dmu, dS, dZ, dsigma_f2, dl, accumulate, workspace,
+                                   dmu, dS, dZ, dsigma_f2, dl, flags & GPPS_ACCUMULATE, workspace,
                                    static_cast<hipStream_t>(stream));
     return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
 }
@@ -198,7 +235,7 @@ size_t gpps_bound_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q
 gpps_status gpps_bound(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D, const void *mu,
                        const void *S, const void *Z, const void *Y, double sigma_f2, const double *l,
                        double beta, double jitter, void *L, void *dmu, void *dS, void *dZ,
-                       void *dsigma_f2, void *dl, void *dbeta, void *workspace,
+                       void *dsigma_f2, void *dl, void *dbeta, int flags, void *workspace,
                        size_t workspace_bytes, void *stream) {
     if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
     if (!valid_shape(N, M, Q) || D < 1 || D > GPPS_MAX_D || M > GPPS_MAX_M_BOUND) return GPPS_ERR_SHAPE;
@@ -216,7 +253,9 @@ gpps_status gpps_bound(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D
                           (const void *)dbeta})
         if (p && !aligned(p, elem)) return GPPS_ERR_ALIGN;
     const gpps::Shape s = gpps::make_shape(N, M, Q);
-    const int path = choose_path(dt, s, S);
+    const int req = requested_path(flags, GPPS_PATH_GENERIC | GPPS_PATH_MFMA);
+    if (req < 0) return GPPS_ERR_PATH;
+    const int path = choose_path(dt, s, S, req);
     if (path < 0) return GPPS_ERR_PATH;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const size_t psi_ws = gpps_workspace_bytes(dt, N, M, Q);
@@ -253,15 +292,6 @@ gpps_status gpps_bound(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D
     return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
 }
 
-gpps_status gpps_set_path(gpps_path path) {
-    if (path != GPPS_PATH_AUTO && path != GPPS_PATH_GENERIC && path != GPPS_PATH_MFMA)
-        return GPPS_ERR_PATH;
-    g_path.store(path);
-    return GPPS_OK;
-}
-
-gpps_path gpps_get_path(void) { return static_cast<gpps_path>(g_path.load()); }
-
 const char *gpps_status_string(gpps_status status) {
     switch (status) {
         case GPPS_OK: return "success";
@@ -272,7 +302,7 @@ const char *gpps_status_string(gpps_status status) {
         case GPPS_ERR_WORKSPACE: return "workspace smaller than gpps_workspace_bytes()";
         case GPPS_ERR_ALIGN: return "workspace not 256-byte aligned or array not element-aligned";
         case GPPS_ERR_HIP: return "HIP runtime error or kernel launch failure";
-        case GPPS_ERR_PATH: return "unknown path, or the requested path cannot run this call";
+        case GPPS_ERR_PATH: return "unknown flag bits, both path flags, or the requested path cannot run this call";
     }
     return "unknown status";
 }

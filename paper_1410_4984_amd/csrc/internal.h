@@ -49,34 +49,39 @@ class TimedScope {
 };
 
 // ---------------------------------------------------------------- generic path
-// Vector-ALU kernels templated on the element type; they serve F64 and any F32
-// shape the matrix-core path does not take.
+// Vector-ALU kernels templated on the element type; they serve F64, any F32
+// shape the matrix-core path does not take, and F32 calls whose operands the
+// matrix-core range guard rejects.  gate: NULL, or a device word; the kernels
+// then do their work only where it is nonzero (the matrix-core route word).
 size_t generic_workspace_bytes(const Shape &s, size_t elem);
 
 template <typename T>
 hipError_t generic_psi_stats(const Shape &s, const T *mu, const T *S, const T *Z,
                              const Hyp<T> &h, T *psi0, T *Psi1, T *Psi2, int accumulate,
-                             void *ws, hipStream_t st);
+                             void *ws, const int *gate, hipStream_t st);
 
 template <typename T>
 hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z,
                              const Hyp<T> &h, T dL_dpsi0, const T *G1, const T *G2, T *dmu,
                              T *dS, T *dZ, T *dsf2, T *dl, int accumulate, void *ws,
-                             hipStream_t st);
+                             const int *gate, hipStream_t st);
 
 // ---------------------------------------------------------------- matrix-core path
 // F32 only: per-datapoint Gram blocks and W * D products on MFMA, exp on VALU.
+// route: a device word outside the workspace regions of both paths; the call
+// writes 0 there when its operands fit the fp16 range (and computes the
+// result), 1 otherwise (and its remaining kernels return at once).
 bool mfma_supports(const Shape &s);
 size_t mfma_workspace_bytes(const Shape &s);
 
 hipError_t mfma_psi_stats(const Shape &s, const float *mu, const float *S, const float *Z,
                           const Hyp<float> &h, float *psi0, float *Psi1, float *Psi2,
-                          int accumulate, void *ws, hipStream_t st);
+                          int accumulate, int *route, void *ws, hipStream_t st);
 
 hipError_t mfma_psi_grads(const Shape &s, const float *mu, const float *S, const float *Z,
                           const Hyp<float> &h, float dL_dpsi0, const float *G1,
                           const float *G2, float *dmu, float *dS, float *dZ, float *dsf2,
-                          float *dl, int accumulate, void *ws, hipStream_t st);
+                          float *dl, int accumulate, int *route, void *ws, hipStream_t st);
 
 // ---------------------------------------------------------------- known inputs (S = 0)
 // Psi1 = Kfu, Psi2 = Kfu^T Kfu on the matrix cores (fp32 and fp64); X holds the

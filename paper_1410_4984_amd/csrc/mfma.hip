@@ -7,41 +7,55 @@
 // (22 significant bits); three of the four cross products are kept (the dropped
 // one is below 2^-22 |a||b|) and all products accumulate in fp32.  In the Gram
 // product the three cross products share one K range: each dimension takes three
-// k slots (hi*hi, hi*lo, lo*hi) and the row bias two, so Q = 20 needs 62 slots,
-// four 16-slot instructions instead of six.  For the
-// exponents that is an error of a few 2^-24 |E| (measured on the synthetic
-// workloads: about 1e-7 relative in each Psi2 summand, two fp32 ulps), the
-// same order as the rounding the fp32 row terms already carry.  Range: the
-// constant operand is the centred z table (|z| << 6e4); the per-datapoint one
-// is -K d (|K d| is a few lengthscales' worth, far inside fp16) plus the row
-// bias b + c as two fp16 parts in two k slots, clamped to +-kBiasClamp: a bias
-// beyond that makes the summand vanish in fp32 anyway.  W in the gradient's second product is
-// scaled per datapoint by a power of two that bounds it by 2^14, and the
-// product is scaled back exactly.  The f16 MFMA does 16 times the work per
-// cycle of v_mfma_f32_32x32x2_f32 and, unlike it, lets the vector ALU issue
-// while it runs, which is where exp2, the weighting and the splits execute.
+// k slots (hi*hi, hi*lo, lo*hi) and the column bias two, so Q = 20 needs 62
+// slots, four 16-slot instructions instead of six.  The f16 MFMA does 16 times
+// the work per cycle of v_mfma_f32_32x32x2_f32 and, unlike it, lets the vector
+// ALU issue while it runs, which is where exp2, the weighting and the splits
+// execute.
 //
 // Per datapoint n the Psi2 summand is a Gram matrix pushed through exp
 // (section 2, eq. (4): Phi turned into an expectation under q(x_n); Alg. 1
 // computes it per pair of inducing inputs and sums over datapoints).  With
-// d_m = mu_n - z_m (per dimension q), w2 = 1/(l^2 + 2 S_nq) and
-// kappa = S_nq / (l^2 (l^2 + 2 S_nq)) >= 0, the exponent of
+// d_m = mu_n - z_m (per dimension q) and w2 = 1/(l^2 + 2 S_nq), the closed form
 //   Psi2_n[m, m'] = sf2^2 prod_q (1 + 2S/l^2)^(-1/2)
 //                   exp(-sum_q [(z_m - z_m')^2/(4 l^2) + (mu - (z_m + z_m')/2)^2 w2])
-// splits exactly into a row term, a column term and a Gram term:
-//   log2 Psi2_n[m, m'] = b_m + b_m' + sum_q K_q d_mq d_m'q,     K = log2(e) kappa,
-//   b_m = log2(e) (log sf2 - 1/4 sum_q log(1 + 2S/l^2) - 1/4 sum_q (1/l^2 + w2) d_mq^2).
-// The Gram term is further written with one side independent of n:
-//   sum_q K d_mq d_m'q = c_m + sum_q (-K_q d_mq) z_m'q,   c_m = sum_q K_q d_mq mu_q,
-// so one MFMA operand is the (centred) z table itself, and the other,
-// -K d, is formed once per datapoint and row block.  b and b + c come from a
-// per-call table (mfma_rowterm_kernel); exp2 is one v_exp_f32.  Inputs are
-// centred (Z and mu shifted by the mean inducing input), which changes no
-// result: every quantity depends on mu - z only.
+// has an n-independent factor 2^C_mm', C_mm' = -log2(e) sum_q (z_m - z_m')^2/(4 l^2),
+// which is taken out of the sum over n: Psi2 = 2^C o sum_n 2^E'_n.  The rest,
+// E'_n = 2 hl_n - log2(e) sum_q w2 (d_m + d_m')^2 / 4 <= 2 hl_n, splits exactly into
+// a row term, a column term and a Gram term:
+//   E'_n[m, m'] = b_m + b_m' + sum_q K_q d_mq d_m'q,     K = -log2(e) w2 / 2,
+//   b_m = hl_n - log2(e)/4 sum_q w2 d_mq^2,   hl_n = log2(e) (log sf2 - 1/4 sum_q log(1 + 2S/l^2)).
+// The Gram term is written with one side independent of n:
+//   sum_q K d_mq d_m'q = c_m + sum_q (z_m'q s_q) (-K_q d_mq / s_q),  c_m = sum_q K_q d_mq mu_q,
+// so one MFMA operand is the (centred) z table scaled per dimension by the power
+// of two s_q that brings max_m |z_mq| into (1/2, 1], and the other, -K d / s, is
+// formed once per datapoint and row block.  b and b + c come from a per-call
+// table (mfma_rowterm_kernel); exp2 is one v_exp_f32.  Inputs are centred (Z and
+// mu shifted by the mean inducing input), which changes no result: every
+// quantity depends on mu - z only.
+//
+// Range.  Every fp16 operand is bounded before the kernels run: per datapoint,
+// |-K d / s| <= log2(e)/2 w2 (|mu| + R_q) / s_q and |b + c| <= |hl| + log2(e)/4
+// sum_q w2 (|mu| + R_q)(3 |mu| + R_q), with R_q = max_m |z_mq| (centred).  A guard
+// kernel evaluates these bounds over all rows (O(N Q)) and writes a route word:
+// when a bound reaches kOperandLimit (or R_q reaches kZLimit, the range of the
+// unscaled z table of the gradient's second product) the matrix-core kernels of
+// the call return at once and the generic kernels, enqueued after them on the
+// same stream, compute the call instead.  Nothing is clamped.  Taking C out of the
+// sum keeps the split terms of the summands that matter small: for those, w2 d_m^2,
+// w2 d_m'^2 and the Gram term are bounded by a few times |E'| whatever the
+// lengthscales (w2 <= 1/l^2), so the exponent error stays a few 2^-22 of the
+// exponent's own size, and the per-dimension scale makes the operands invariant
+// under a common scaling of mu, Z and l.  The guard also sends calls whose
+// inducing inputs spread over more than kSpreadLimit lengthscales (R_q / l_q) to
+// the generic kernels, for the accuracy of the gradient (mfma_guard_kernel).  W in the gradient's second product is scaled per
+// datapoint by a power of two that bounds it by 2^14, and the product is scaled
+// back exactly.
 //
 // Gradient (Alg. 2): with W_n = G2s o Psi2_n (G2s the symmetric part of
 // dL/dPsi2), r_n = W_n 1 and V_n = W_n D_n (D_n[m, q] = d_mq), every derivative
-// is linear in r_n and V_n:
+// is linear in r_n and V_n (and W_n = G2c o 2^E'_n, where G2c = G2s o 2^C is
+// formed once per call):
 //   dmu_nq   = -2 w2 sum_m d r
 //   dS_nq    = w2^2 (X + Y) - w2 R,        X = sum_m d^2 r, Y = sum_m d V, R = sum_m r
 //   dZ_mq   += V (w2 - 1/l^2) + d r (w2 + 1/l^2)
@@ -83,8 +97,15 @@ constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kRowStride = 64;         // stride of per-row tables padded to 64 dimensions
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kPadBias = -1.0e30f;   // row term of a padded inducing input: exp2 -> 0
-constexpr float kBiasClamp = 6.0e4f;   // bias carried in an fp16 Gram k slot (fp16 max 65504)
+constexpr float kPadBias = -1.0e30f;   // row term (fp32) of a padded inducing input: exp2 -> 0
+// column bias of a padded inducing input, exact in fp16: its z is 0, so the range
+// guard's bound on |b + c| (>= its Gram term plus |hl| + 128) keeps its exponent
+// below -128 + the gradient's row scale (<= 120): exp2 is finite and tiny, and
+// dL/dPsi2 is zero there
+constexpr float kPadBiasCol = -6.0e4f;
+constexpr float kOperandLimit = 6.0e4f; // guard: largest fp16 Gram operand or bias (fp16 max 65504)
+constexpr float kZLimit = 3.0e4f;       // guard: largest centred |z| (unscaled fp16 z table)
+constexpr float kSpreadLimit = 64.f;    // guard: largest R_q / l_q (gradient conditioning)
 constexpr int kRB = 8;                 // gradient: rows per batch
 constexpr int kFRB = 4;                // forward: rows per batch (prefetched a batch ahead)
 constexpr int kFPF = kFRB * 512 / 256; // forward: per-thread prefetch slots of a [kFRB][Mp] table
@@ -174,7 +195,7 @@ struct MPlan {
     int64_t fin_blocks;    // finalize: blocks of kFinRows rows
     size_t lds_fwd, lds_grad;
     size_t off_K, off_hq, off_w2, off_hl, off_w1, off_l1, off_zc, off_bt, off_bc, off_t1, off_g2,
-        off_fp, off_rs, off_dz, off_dl, off_gmax, total;
+        off_fp, off_rs, off_dz, off_dl, off_gmax, off_gpart, off_bmax, off_smax, total;
 };
 
 // Forward LDS layout (floats):
@@ -293,7 +314,7 @@ MPlan make_mplan(const Shape &s) {
     p.off_hl = take(sizeof(float) * s.N);
     p.off_w1 = take(sizeof(float) * s.N * s.Q);
     p.off_l1 = take(sizeof(float) * s.N);
-    p.off_zc = take(sizeof(float) * s.Q);
+    p.off_zc = take(sizeof(float) * 4 * s.Q);  // zc, 1/s_q, s_q, R_q
     p.off_bt = take(sizeof(float) * s.N * p.Mp);
     p.off_bc = take(sizeof(float) * s.N * p.Mp);
     p.off_t1 = take(sizeof(float) * s.N * p.Mp);
@@ -302,7 +323,10 @@ MPlan make_mplan(const Shape &s) {
     p.off_rs = take(sizeof(float) * p.ggroups * s.N * (5 * s.Q + 2));
     p.off_dz = take(sizeof(float) * p.gchunks * p.njr * s.M * s.Q);
     p.off_dl = take(sizeof(float) * p.fin_blocks * (s.Q + 1));
-    p.off_gmax = take(sizeof(float));
+    p.off_gmax = take(sizeof(float) * 2);
+    p.off_gpart = take(sizeof(float) * cdiv(s.N, 64));
+    p.off_bmax = take(sizeof(float) * cdiv(p.Mp, 256) * s.N);
+    p.off_smax = take(sizeof(float) * 2 * cdiv(p.Mp * p.Mp, 256));
     p.total = o;
     return p;
 }
@@ -310,57 +334,21 @@ MPlan make_mplan(const Shape &s) {
 float *fat(void *ws, size_t off) { return reinterpret_cast<float *>(static_cast<char *>(ws) + off); }
 
 // ---------------------------------------------------------------- small kernels
-// Per-row tables, 64 datapoints per workgroup.  For every (n, q):
-//   K[n][q]  = log2e S / (l^2 (l^2 + 2S))  (row stride 64; entries q >= Q are never read)
-//   hq[n][q] = -log2e/4 (1/l^2 + w2),  w2[n][q] = 1/(l^2 + 2S),  w1[n][q] = 1/(l^2 + S)
-// (one pass over the workgroup's (row, dimension) pairs, coalesced), then per row
-//   hl[n]    = log2e (log sf2 - 1/4 sum_q log(1 + 2S/l^2))   (Psi2 prefactor, half of it)
-//   l1[n]    = log2e (log sf2 - 1/2 sum_q log(1 + S/l^2))    (Psi1 prefactor)
-// with the sums over q taken in order from LDS.
-constexpr int kRowsPerBlock = 64;
-__global__ __launch_bounds__(256) void mfma_rows_kernel(
-    int64_t N, int Q, const float *__restrict__ S, Hyp<float> h, float *__restrict__ Kt,
-    float *__restrict__ hq, float *__restrict__ w2t, float *__restrict__ hl,
-    float *__restrict__ w1t, float *__restrict__ l1) {
-    __shared__ float la2[kRowsPerBlock][GPPS_MAX_Q + 1], la1[kRowsPerBlock][GPPS_MAX_Q + 1];
-    const int64_t n0 = (int64_t)blockIdx.x * kRowsPerBlock;
-    const int rows = (int)min<int64_t>(kRowsPerBlock, N - n0);
-    for (int i = threadIdx.x; i < rows * Q; i += 256) {
-        const int r = i / Q, q = i - r * Q;
-        const int64_t k = n0 * Q + i;  // = (n0 + r) * Q + q
-        const float sv = S[k];
-        const float l2 = h.l2[q];
-        const float w2 = 1.f / (l2 + 2.f * sv);
-        Kt[(n0 + r) * kRowStride + q] = kLog2e * sv * w2 / l2;
-        hq[k] = -0.25f * kLog2e * (1.f / l2 + w2);
-        w2t[k] = w2;
-        w1t[k] = 1.f / (l2 + sv);
-        la2[r][q] = log1pf(2.f * sv / l2);
-        la1[r][q] = log1pf(sv / l2);
-    }
-    __syncthreads();
-    const int r = threadIdx.x;
-    if (r < rows) {
-        float a2 = 0.f, a1 = 0.f;
-        for (int q = 0; q < Q; ++q) {
-            a2 += la2[r][q];
-            a1 += la1[r][q];
-        }
-        hl[n0 + r] = kLog2e * (h.log_sf2 - 0.25f * a2);
-        l1[n0 + r] = kLog2e * (h.log_sf2 - 0.5f * a1);
-    }
-}
-
-// Mean inducing input per dimension: the centring shift.  G = 256 / Q groups
-// of Q threads sum rows m = g, g + G, ... (coalesced), then the G partial sums
-// of each dimension are added in group order.
+// Centring table of the call, [4][Q] floats: the mean inducing input zc_q, the
+// per-dimension scale of the Gram operands as 1/s_q = 2^e_q and s_q = 2^-e_q
+// (e_q the exponent of R_q, so that R_q s_q lies in (1/2, 1]; e_q = 0 when
+// R_q = 0), and R_q = max_m |z_mq - zc_q|.  G = 256 / Q groups of Q threads take
+// rows m = g, g + G, ... (coalesced); the G partial sums (then maxima) of each
+// dimension are combined in group order.
 __global__ __launch_bounds__(256) void mfma_centre_kernel(int M, int Q,
                                                           const float *__restrict__ Z,
-                                                          float *__restrict__ zc) {
+                                                          float *__restrict__ zt) {
     __shared__ float part[256];
+    __shared__ float s_zc[GPPS_MAX_Q];
     const int t = threadIdx.x, G = 256 / Q;
-    if (t < G * Q) {
-        const int g = t / Q, q = t - g * Q;
+    const bool act = t < G * Q;
+    const int g = t / Q, q = t - g * Q;
+    if (act) {
         float s = 0.f;
 #pragma unroll 8
         for (int m = g; m < M; m += G) s += Z[(int64_t)m * Q + q];
@@ -369,40 +357,204 @@ __global__ __launch_bounds__(256) void mfma_centre_kernel(int M, int Q,
     __syncthreads();
     if (t < Q) {
         float s = 0.f;
-        for (int g = 0; g < G; ++g) s += part[g * Q + t];
-        zc[t] = s / (float)M;
+        for (int k = 0; k < G; ++k) s += part[k * Q + t];
+        s_zc[t] = s / (float)M;
+    }
+    __syncthreads();
+    if (act) {
+        const float c = s_zc[q];
+        float r = 0.f;
+        for (int m = g; m < M; m += G) r = fmaxf(r, fabsf(Z[(int64_t)m * Q + q] - c));
+        part[t] = r;
+    }
+    __syncthreads();
+    if (t < Q) {
+        float r = 0.f;
+        for (int k = 0; k < G; ++k) r = fmaxf(r, part[k * Q + t]);
+        int e = 0;
+        if (r > 0.f && r <= 3.0e38f) frexpf(r, &e);
+        zt[t] = s_zc[t];
+        zt[Q + t] = ldexpf(1.f, e);
+        zt[2 * Q + t] = ldexpf(1.f, -e);
+        zt[3 * Q + t] = r;
     }
 }
 
-// Symmetric part of dL/dPsi2, zero-padded to Mp x Mp (all zero when G2 is NULL).
-__global__ void mfma_sym_kernel(int M, int Mp, const float *__restrict__ G2,
-                                float *__restrict__ G2p) {
+// Per-row tables, 64 datapoints per workgroup.  For every (n, q), with
+// w2 = 1/(l^2 + 2S):
+//   K[n][q]  = -log2e/2 w2 / s_q  (row stride 64; entries q >= Q are never read)
+//   hq[n][q] = -log2e/4 w2,  w2[n][q],  w1[n][q] = 1/(l^2 + S)
+// (one pass over the workgroup's (row, dimension) pairs, coalesced), then per row
+//   hl[n]    = log2e (log sf2 - 1/4 sum_q log(1 + 2S/l^2))   (Psi2 prefactor, half of it)
+//   l1[n]    = log2e (log sf2 - 1/2 sum_q log(1 + S/l^2))    (Psi1 prefactor)
+// with the sums over q taken in order from LDS.  The range guard's bound for the
+// row (the larger of its column bias bound |hl| + log2e/4 sum_q w2 (|mu| + R_q)
+// (3 |mu| + R_q) + 128, the 128 covering the gradient's row scale, and its
+// largest Gram operand bound log2e/2 w2 (|mu| + R_q) / s_q; mu centred) goes to
+// gpart, as the maximum over the workgroup's rows.
+constexpr int kRowsPerBlock = 64;
+__global__ __launch_bounds__(256) void mfma_rows_kernel(
+    int64_t N, int Q, const float *__restrict__ mu, const float *__restrict__ S,
+    const float *__restrict__ zt, Hyp<float> h, float *__restrict__ Kt, float *__restrict__ hq,
+    float *__restrict__ w2t, float *__restrict__ hl, float *__restrict__ w1t,
+    float *__restrict__ l1, float *__restrict__ gpart) {
+    __shared__ float la2[kRowsPerBlock][GPPS_MAX_Q + 1], la1[kRowsPerBlock][GPPS_MAX_Q + 1];
+    __shared__ float lb[kRowsPerBlock][GPPS_MAX_Q + 1], lx[kRowsPerBlock][GPPS_MAX_Q + 1];
+    __shared__ float red[kRowsPerBlock];
+    const int64_t n0 = (int64_t)blockIdx.x * kRowsPerBlock;
+    const int rows = (int)min<int64_t>(kRowsPerBlock, N - n0);
+    for (int i = threadIdx.x; i < rows * Q; i += 256) {
+        const int r = i / Q, q = i - r * Q;
+        const int64_t k = n0 * Q + i;  // = (n0 + r) * Q + q
+        const float sv = S[k];
+        const float am = fabsf(mu[k] - zt[q]), R = zt[3 * Q + q];
+        const float l2 = h.l2[q];
+        const float w2 = 1.f / (l2 + 2.f * sv);
+        Kt[(n0 + r) * kRowStride + q] = -0.5f * kLog2e * w2 * zt[Q + q];
+        hq[k] = -0.25f * kLog2e * w2;
+        w2t[k] = w2;
+        w1t[k] = 1.f / (l2 + sv);
+        la2[r][q] = log1pf(2.f * sv / l2);
+        la1[r][q] = log1pf(sv / l2);
+        lb[r][q] = w2 * (am + R) * (3.f * am + R);
+        lx[r][q] = 0.5f * kLog2e * w2 * (am + R) * zt[Q + q];
+    }
+    __syncthreads();
+    const int r = threadIdx.x;
+    if (r < kRowsPerBlock) {
+        float bound = 0.f;
+        if (r < rows) {
+            float a2 = 0.f, a1 = 0.f, b = 0.f, x = 0.f;
+            for (int q = 0; q < Q; ++q) {
+                a2 += la2[r][q];
+                a1 += la1[r][q];
+                b += lb[r][q];
+                x = fmaxf(x, lx[r][q]);
+            }
+            const float hlr = kLog2e * (h.log_sf2 - 0.25f * a2);
+            hl[n0 + r] = hlr;
+            l1[n0 + r] = kLog2e * (h.log_sf2 - 0.5f * a1);
+            // NaN anywhere makes the bound NaN, which the guard treats as out of range
+            const float bb = fabsf(hlr) + 0.25f * kLog2e * b + 128.f;
+            bound = (bb != bb || x != x) ? __builtin_nanf("") : fmaxf(bb, x);
+        }
+        red[r] = bound;
+    }
+    __syncthreads();
+    if (r == 0) {
+        float m = 0.f;
+        bool nan = false;
+        for (int k = 0; k < rows; ++k) {
+            nan |= red[k] != red[k];
+            m = fmaxf(m, red[k]);
+        }
+        gpart[blockIdx.x] = nan ? __builtin_nanf("") : m;
+    }
+}
+
+// Range guard of the matrix-core path: route[0] = 0 when every row bound and
+// every R_q is inside the fp16 limits and every R_q / l_q is at most
+// kSpreadLimit (the matrix-core kernels compute the call), 1 otherwise (they
+// return at once and the generic kernels compute it).  The last condition is
+// one of accuracy, not range: the gradient forms dZ from V' - z_m r = sum_m'
+// W (z_m' - z_m), two terms of size |z| r whose difference is of the size of the
+// pair spacings that matter, about l, so fp32-class rounding of V' is amplified
+// by about R / l, and by more when pairs on both sides of z_m cancel (a CPU model
+// of these kernels' arithmetic: dZ error 2e-6 at R / l = 70 and 1e-3 at 440).
+// One workgroup; the maximum is order-independent.
+__global__ __launch_bounds__(256) void mfma_guard_kernel(int64_t nparts, int Q,
+                                                         const float *__restrict__ gpart,
+                                                         const float *__restrict__ zt,
+                                                         Hyp<float> h, int *__restrict__ route) {
+    __shared__ int bad[256];
+    int b = 0;
+    for (int64_t i = threadIdx.x; i < nparts; i += 256) b |= !(gpart[i] < kOperandLimit);
+    for (int q = threadIdx.x; q < Q; q += 256)
+        b |= !(zt[3 * Q + q] < kZLimit) | !(zt[3 * Q + q] <= kSpreadLimit * h.l[q]);
+    bad[threadIdx.x] = b;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int v = 0;
+        for (int k = 0; k < 256; ++k) v |= bad[k];
+        route[0] = v;
+    }
+}
+
+// Pair constant of the exponent, C_mm' = -log2e sum_q (z_mq - z_m'q)^2 / (4 l_q^2)
+// (the n-independent factor 2^C of every summand; symmetric in (m, m') bit for bit).
+__device__ __forceinline__ float pair_const(int m, int mp, int Q, const float *__restrict__ Z,
+                                            const Hyp<float> &h) {
+    float c = 0.f;
+    for (int q = 0; q < Q; ++q) {
+        const float d = Z[(int64_t)m * Q + q] - Z[(int64_t)mp * Q + q];
+        c = fmaf(d * d, 0.25f / h.l2[q], c);
+    }
+    return -kLog2e * c;
+}
+
+// G2c = G2s o 2^C: the symmetric part of dL/dPsi2 times the pair factor,
+// zero-padded to Mp x Mp (all zero when G2 is NULL); per workgroup, the largest
+// |G2c| and |G2s| of its entries go to smax[2 block], smax[2 block + 1].
+__global__ __launch_bounds__(256) void mfma_sym_kernel(int M, int Mp, int Q,
+                                                       const float *__restrict__ G2,
+                                                       const float *__restrict__ Z, Hyp<float> h,
+                                                       const int *__restrict__ route,
+                                                       float *__restrict__ G2p,
+                                                       float *__restrict__ smax) {
+    __shared__ float red[2][4];
+    if (route[0]) return;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)Mp * Mp) return;
-    const int m = (int)(i / Mp), mp = (int)(i - (int64_t)m * Mp);
-    G2p[i] = (G2 && m < M && mp < M) ? 0.5f * (G2[(int64_t)m * M + mp] + G2[(int64_t)mp * M + m])
-                                     : 0.f;
+    float gc = 0.f, gs = 0.f;
+    if (i < (int64_t)Mp * Mp) {
+        const int m = (int)(i / Mp), mp = (int)(i - (int64_t)m * Mp);
+        if (G2 && m < M && mp < M) {
+            gs = 0.5f * (G2[(int64_t)m * M + mp] + G2[(int64_t)mp * M + m]);
+            gc = gs * __builtin_amdgcn_exp2f(pair_const(m, mp, Q, Z, h));
+        }
+        G2p[i] = gc;
+    }
+    float a = fabsf(gc), b = fabsf(gs);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        a = fmaxf(a, __shfl_xor(a, off));
+        b = fmaxf(b, __shfl_xor(b, off));
+    }
+    if ((threadIdx.x & 63) == 0) {
+        red[0][threadIdx.x >> 6] = a;
+        red[1][threadIdx.x >> 6] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {
+        float v = 0.f;
+        for (int w = 0; w < 4; ++w) v = fmaxf(v, red[threadIdx.x][w]);
+        smax[2 * blockIdx.x + threadIdx.x] = v;
+    }
 }
 
 // Row terms and Psi1 for every (n, m), once per call (d = mu - z, centred):
-//   bt[n][m] = hl_n + sum_q hq_nq d^2,   bc[n][m] = bt[n][m] + sum_q K_nq d mu_nq
+//   bt[n][m] = hl_n + sum_q hq_nq d^2,   bc[n][m] = bt[n][m] + sum_q 2 hq_nq d mu_nq
+// (2 hq = -log2e w2 / 2 is the Gram weight K of the exponent split)
 //   Psi1     = exp2(l1_n - log2e/2 sum_q w1_nq d^2)
-// (kPadBias in both row-term tables for m >= M).  The forward writes Psi1
+// (kPadBias in bt and kPadBiasCol in bc for m >= M).  The forward writes Psi1
 // (NULL: skipped); the gradient writes t1[n][m] = dL/dPsi1[n][m] * Psi1 with
-// row stride Mp (zero where G1 is NULL or m >= M).  One thread per inducing
-// input (z in registers); rows staged in LDS as one (mu, hq, w1, K mu) vector
-// per dimension, so each dimension costs one broadcast read and five vector
-// instructions.
-template <int QM>
+// row stride Mp (zero where G1 is NULL or m >= M) and, per row and range of 256
+// inducing inputs (blockIdx.y), bmax[y][n] = max over the range's real m of
+// bt[n][m] (the gradient's scale of W: max_m E'_n[m, m] = 4 max_m bt - 2 hl_n).
+// One thread per inducing input (z in registers); rows staged in LDS as one
+// (mu, hq, w1, K mu) vector per dimension, so each dimension costs one broadcast
+// read and five vector instructions.
+template <int QM, bool GRAD>
 __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     int64_t N, int M, int Q, int Mp, const float *__restrict__ mu, const float *__restrict__ Z,
-    const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ hq,
-    const float *__restrict__ hl, const float *__restrict__ w1t, const float *__restrict__ l1,
-    const float *__restrict__ G1, float *__restrict__ bt, float *__restrict__ bc,
-    float *__restrict__ psi1, float *__restrict__ t1) {
+    const float *__restrict__ zc, const float *__restrict__ hq, const float *__restrict__ hl,
+    const float *__restrict__ w1t, const float *__restrict__ l1, const float *__restrict__ G1,
+    const int *__restrict__ route, float *__restrict__ bt, float *__restrict__ bc,
+    float *__restrict__ psi1, float *__restrict__ t1, float *__restrict__ bmax) {
     typedef float v4f __attribute__((ext_vector_type(4)));
     __shared__ v4f s_row[kRTRows][QM];
     __shared__ float s_hl[kRTRows], s_l1[kRTRows];
+    __shared__ float s_bm[GRAD ? kRTRows * 257 : 1];   // b of [row][thread], row stride 257
+    if (route[0]) return;
     const int m = blockIdx.y * 256 + threadIdx.x;
     const int64_t n0 = (int64_t)blockIdx.x * kRTRows;
     const int cnt = (int)min<int64_t>(kRTRows, N - n0);
@@ -415,7 +567,7 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
         v.x = x;
         v.y = ok ? hq[n * Q + q] : 0.f;
         v.z = ok ? w1t[n * Q + q] : 0.f;
-        v.w = ok ? Kt[n * kRowStride + q] * x : 0.f;
+        v.w = 2.f * v.y * x;
         s_row[r][q] = v;
     }
     for (int r = threadIdx.x; r < kRTRows; r += 256) {
@@ -423,54 +575,78 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
         s_l1[r] = r < cnt ? l1[n0 + r] : 0.f;
     }
     __syncthreads();
-    if (m >= Mp) return;
-    const bool real = m < M;
-    float z[QM];
+    const bool inb = m < Mp, real = m < M;
+    if (inb) {
+        float z[QM];
 #pragma unroll
-    for (int q = 0; q < QM; ++q) z[q] = (real && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
-    for (int r = 0; r < cnt; ++r) {
-        float b = s_hl[r], cc = 0.f, e = 0.f;
+        for (int q = 0; q < QM; ++q) z[q] = (real && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+        for (int r = 0; r < cnt; ++r) {
+            float b = s_hl[r], cc = 0.f, e = 0.f;
 #pragma unroll
-        for (int q = 0; q < QM; ++q) {
-            const v4f v = s_row[r][q];
-            const float d = v.x - z[q];
-            const float d2 = d * d;
-            b = fmaf(v.y, d2, b);
-            e = fmaf(v.z, d2, e);
-            cc = fmaf(v.w, d, cc);
+            for (int q = 0; q < QM; ++q) {
+                const v4f v = s_row[r][q];
+                const float d = v.x - z[q];
+                const float d2 = d * d;
+                b = fmaf(v.y, d2, b);
+                e = fmaf(v.z, d2, e);
+                cc = fmaf(v.w, d, cc);
+            }
+            const int64_t n = n0 + r;
+            bt[n * Mp + m] = real ? b : kPadBias;
+            bc[n * Mp + m] = real ? b + cc : kPadBiasCol;
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(-0.5f * kLog2e, e, s_l1[r]));
+            if constexpr (GRAD) {
+                t1[n * Mp + m] = (real && G1) ? G1[n * M + m] * p1 : 0.f;
+                s_bm[r * 257 + threadIdx.x] = real ? b : -INFINITY;
+            } else if (psi1 && real) {
+                psi1[n * M + m] = p1;
+            }
         }
-        const int64_t n = n0 + r;
-        bt[n * Mp + m] = real ? b : kPadBias;
-        bc[n * Mp + m] = real ? b + cc : kPadBias;
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(-0.5f * kLog2e, e, s_l1[r]));
-        if (t1) t1[n * Mp + m] = (real && G1) ? G1[n * M + m] * p1 : 0.f;
-        else if (psi1 && real) psi1[n * M + m] = p1;
     }
+    if constexpr (!GRAD) return;
+    if (!inb)
+        for (int r = 0; r < cnt; ++r) s_bm[r * 257 + threadIdx.x] = -INFINITY;
+    __syncthreads();
+    // thread (row t / 8, part t % 8) takes columns part, part + 8, ...; the 8
+    // parts of a row sit in consecutive lanes and meet in three xor steps
+    const int row = threadIdx.x >> 3, part = threadIdx.x & 7;
+    float v = -INFINITY;
+    if (row < cnt)
+        for (int k = part; k < 256; k += 8) v = fmaxf(v, s_bm[row * 257 + k]);
+    v = fmaxf(v, __shfl_xor(v, 1));
+    v = fmaxf(v, __shfl_xor(v, 2));
+    v = fmaxf(v, __shfl_xor(v, 4));
+    if (part == 0 && row < cnt) bmax[(int64_t)blockIdx.y * N + n0 + row] = v;
 }
 
-// max |G2s| over the padded symmetric dL/dPsi2 (one workgroup, loads issued 8
-// at a time; max is order-independent, so the result is deterministic).
-__global__ __launch_bounds__(1024) void mfma_absmax_kernel(int64_t n, const float *__restrict__ G2p,
+// gmax[0] = max |G2c|, gmax[1] = max |G2s| from the sym kernel's per-workgroup
+// maxima (one workgroup; max is order-independent, so the result is
+// deterministic).
+__global__ __launch_bounds__(1024) void mfma_absmax_kernel(int64_t nblocks,
+                                                           const float *__restrict__ smax,
+                                                           const int *__restrict__ route,
                                                            float *__restrict__ gmax) {
-    __shared__ float part[16];
-    float m = 0.f;
-    int64_t i = threadIdx.x;
-    for (; i + 7 * 1024 < n; i += 8 * 1024) {
-        float v[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = G2p[i + j * 1024];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(v[j]));
+    __shared__ float part[2][16];
+    if (route[0]) return;
+    float a = 0.f, b = 0.f;
+    for (int64_t i = threadIdx.x; i < nblocks; i += 1024) {
+        a = fmaxf(a, smax[2 * i]);
+        b = fmaxf(b, smax[2 * i + 1]);
     }
-    for (; i < n; i += 1024) m = fmaxf(m, fabsf(G2p[i]));
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+    for (int off = 32; off >= 1; off >>= 1) {
+        a = fmaxf(a, __shfl_xor(a, off));
+        b = fmaxf(b, __shfl_xor(b, off));
+    }
+    if ((threadIdx.x & 63) == 0) {
+        part[0][threadIdx.x >> 6] = a;
+        part[1][threadIdx.x >> 6] = b;
+    }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x < 2) {
         float r = 0.f;
-        for (int w = 0; w < 16; ++w) r = fmaxf(r, part[w]);
-        gmax[0] = r;
+        for (int w = 0; w < 16; ++w) r = fmaxf(r, part[threadIdx.x][w]);
+        gmax[threadIdx.x] = r;
     }
 }
 
@@ -516,7 +692,7 @@ __device__ __forceinline__ void gram_operand(const float (&zv)[gram_t(NK)],
                                              const float *__restrict__ kr, float bias, int g,
                                              v8h (&B)[NK]) {
     constexpr int NP = gram_np(NK), ODD = gram_odd(NK);
-    bias = g ? fminf(kBiasClamp, fmaxf(-kBiasClamp, bias)) : 0.f;
+    bias = g ? bias : 0.f;  // |bias| < kOperandLimit (range guard)
     unsigned w[4 * NK];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
@@ -577,9 +753,9 @@ __device__ __forceinline__ v16f row_terms(const float *__restrict__ bbr, int j, 
     return e;
 }
 
-// [centred z | 1] rows of blocks blk0 .. blk0 + nblk - 1 (clamped to the last
+// [centred z s | 1] rows of blocks blk0 .. blk0 + nblk - 1 (clamped to the last
 // block) as packed Gram A operand tables: [nblk][NK][2][32][8] f16 (slot
-// contents listed at gram_np).
+// contents listed at gram_np; zc is the centring table, [4][Q]).
 template <int NK>
 __device__ void stage_za(_Float16 *za, int blk0, int nblk, int nb, int M, int Q,
                          const float *__restrict__ Z, const float *__restrict__ zc) {
@@ -612,7 +788,8 @@ __device__ void stage_za(_Float16 *za, int blk0, int nblk, int nb, int M, int Q,
         }
         if (q >= 0) {
             q += gg * T;
-            const float zq = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+            // z scaled by s_q (a power of two: exact), |z s_q| <= 1
+            const float zq = (m < M && q < Q) ? (Z[(int64_t)m * Q + q] - zc[q]) * zc[2 * Q + q] : 0.f;
             _Float16 hi, lo;
             split2h(zq, hi, lo);
             za[idx] = part == 0 ? hi : lo;
@@ -634,8 +811,9 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int64_t T, int ftasks, int64_t rows_per_chunk,
     const float *__restrict__ mu, const float *__restrict__ Z, const float *__restrict__ zc,
     const float *__restrict__ Kt, const float *__restrict__ bt, const float *__restrict__ bc,
-    float *__restrict__ partial) {
+    const int *__restrict__ route, float *__restrict__ partial) {
     extern __shared__ float lds[];
+    if (route[0]) return;
     const LdsF L = lds_fwd_layout(Mp, NK);
     constexpr int GT = gram_t(NK);
     _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
@@ -682,7 +860,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
             const int k = tid + j * kThreads;
             const bool ok = k < cb * Mp;
             pf_b[j] = ok ? bt[n0 * Mp + k] : kPadBias;
-            pf_c[j] = ok ? bc[n0 * Mp + k] : kPadBias;
+            pf_c[j] = ok ? bc[n0 * Mp + k] : kPadBiasCol;
         }
         const int r = tid / kRowStride, q = tid - r * kRowStride;
         const bool ok = r < cb && q < Q;
@@ -751,21 +929,24 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     }
 }
 
-// Fixed-order sum over chunks; both triangles written from the same value.
-// One workgroup per (upper tile, 32 consecutive partial entries): 8 groups of
-// 32 threads take chunks g, g + 8, ... (one 128-byte segment per group), the
-// 8 group sums are added in order.  Entry e of a tile is (m' mod 32) * 32 +
-// (m mod 32).
-__global__ __launch_bounds__(256) void psi2_reduce_kernel(int64_t N, int M, int nb, int64_t T,
+// Fixed-order sum over chunks, times the pair factor 2^C; both triangles written
+// from the same value.  One workgroup per (upper tile, 32 consecutive partial
+// entries): 8 groups of 32 threads take chunks g, g + 8, ... (one 128-byte
+// segment per group), the 8 group sums are added in order.  Entry e of a tile is
+// (m' mod 32) * 32 + (m mod 32).
+__global__ __launch_bounds__(256) void psi2_reduce_kernel(int64_t N, int M, int Q, int nb, int64_t T,
                                                           int64_t chunks,
                                                           const float *__restrict__ partial,
-                                                          float sf2, float *__restrict__ psi0,
+                                                          const float *__restrict__ Z, Hyp<float> h,
+                                                          const int *__restrict__ route,
+                                                          float *__restrict__ psi0,
                                                           float *__restrict__ Psi2, int accumulate) {
     __shared__ float red[256];
+    if (route[0]) return;
     const int t = threadIdx.x, o = t & 31, g = t >> 5;
     const int64_t tile = blockIdx.x >> 5;
     const int eb = blockIdx.x & 31;
-    if (blockIdx.x == 0 && t == 0) psi0[0] = (accumulate ? psi0[0] : 0.f) + (float)N * sf2;
+    if (blockIdx.x == 0 && t == 0) psi0[0] = (accumulate ? psi0[0] : 0.f) + (float)N * h.sf2;
     const float *src = partial + tile * (kTile * kTile) + eb * kTile + o;
     const int64_t stride = T * (kTile * kTile);
     float s = 0.f;
@@ -782,6 +963,7 @@ __global__ __launch_bounds__(256) void psi2_reduce_kernel(int64_t N, int M, int 
     if (m >= M || mp >= M || m > mp) return;
     float v = 0.f;
     for (int k = 0; k < 8; ++k) v += red[k * 32 + o];
+    v *= __builtin_amdgcn_exp2f(pair_const(m, mp, Q, Z, h));
     v += accumulate ? Psi2[(int64_t)m * M + mp] : 0.f;
     Psi2[(int64_t)m * M + mp] = v;
     Psi2[(int64_t)mp * M + m] = v;
@@ -836,9 +1018,10 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ bt,
     const float *__restrict__ bc, const float *__restrict__ w1t, const float *__restrict__ w2t,
     const float *__restrict__ t1g, const float *__restrict__ G2p, const float *__restrict__ hl,
-    const float *__restrict__ gmax, Hyp<float> h, float *__restrict__ rowsum,
-    float *__restrict__ part_dz) {
+    const float *__restrict__ gmax, const float *__restrict__ bmax, Hyp<float> h,
+    const int *__restrict__ route, float *__restrict__ rowsum, float *__restrict__ part_dz) {
     extern __shared__ float lds[];
+    if (route[0]) return;
     const LdsG L = lds_grad_layout(Mp, DSF, Q, NQB, NK, wpg);
     constexpr int GT = gram_t(NK);
     _Float16 *zh = reinterpret_cast<_Float16 *>(lds + L.zb);
@@ -889,9 +1072,13 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
         lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
     }
     stage_zh<JPW>(zh, jr, M, Q, NQB, Z, zc);
-    // W_n = G2s o Psi2_n is bounded by max|G2s| 2^(2 hl_n) (hl_n: log2 of the half
-    // prefactor); its per-row scale 2^sc brings that bound to 2^14, inside fp16
-    const float lg = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
+    // |W_n| = |G2c| 2^E'_n is bounded by max|G2c| 2^(2 hl_n) (E' <= 2 hl_n, hl_n: log2
+    // of the half prefactor), and, Psi2_n being positive semidefinite (|Psi2_n[m, m']|
+    // <= max_m Psi2_n[m, m]), by max|G2s| 2^(4 bmax_n - 2 hl_n); the per-row scale 2^sc
+    // brings the smaller bound to 2^14, inside fp16 and well above its subnormals
+    const float lgc = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
+    const float lgs = gmax[1] > 0.f ? __builtin_amdgcn_logf(gmax[1]) : 0.f;
+    const int nbm = (Mp + 255) / 256;          // bmax parts (ranges of 256 inducing inputs)
     stage_za<NK>(za, jr * JPW, JPW, nb, M, Q, Z, zc);
 
     // Batches of kRB rows staged in LDS between two barriers.  All loads of a
@@ -912,7 +1099,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 const int k = tid + j * nthr;
                 const bool ok = k < cb * Mp;
                 pb[j] = ok ? bt[n0 * Mp + k] : kPadBias;
-                pc[j] = ok ? bc[n0 * Mp + k] : kPadBias;
+                pc[j] = ok ? bc[n0 * Mp + k] : kPadBiasCol;
                 pt[j] = ok ? t1g[n0 * Mp + k] : 0.f;
             }
             const int r = tid / kRowStride, q = tid - r * kRowStride;
@@ -923,7 +1110,11 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 pw1 = w1t[(n0 + r) * Q + q];
                 pw2 = w2t[(n0 + r) * Q + q];
             }
-            if (tid < cb) phl = hl[n0 + tid];
+            float pbm = -INFINITY;
+            if (tid < cb) {
+                phl = hl[n0 + tid];
+                for (int y = 0; y < nbm; ++y) pbm = fmaxf(pbm, bmax[(int64_t)y * N + n0 + tid]);
+            }
 #pragma unroll
             for (int j = 0; j < kGPF; ++j) {
                 const int k = tid + j * nthr;
@@ -939,14 +1130,15 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 lds[L.w1b + tid] = pw1;
                 lds[L.w2b + tid] = pw2;
             }
-            if (tid < kRB)
-                lds[L.sc + tid] = tid < cb ? fminf(120.f, fmaxf(-120.f, floorf(14.f - 2.f * phl - lg)))
-                                           : 0.f;
+            if (tid < kRB) {
+                const float wb = fminf(2.f * phl + lgc, 4.f * pbm - 2.f * phl + lgs);
+                lds[L.sc + tid] = tid < cb ? fminf(120.f, fmaxf(-120.f, floorf(14.f - wb))) : 0.f;
+            }
         }
         for (int k = tid + kGPF * nthr; k < kRB * Mp; k += nthr) {
             const bool ok = k < cb * Mp;
             lds[L.bb + k] = ok ? bt[n0 * Mp + k] : kPadBias;
-            lds[L.bcb + k] = ok ? bc[n0 * Mp + k] : kPadBias;
+            lds[L.bcb + k] = ok ? bc[n0 * Mp + k] : kPadBiasCol;
             lds[L.t1 + k] = ok ? t1g[n0 * Mp + k] : 0.f;
         }
         for (int k = tid + nthr; k < kRB * kRowStride; k += nthr) {
@@ -1131,10 +1323,12 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 __global__ __launch_bounds__(256) void psi2_finalize_kernel(
     int64_t N, int Q, int groups, const float *__restrict__ rowsum,
     const float *__restrict__ w2t, const float *__restrict__ S, Hyp<float> h,
-    float *__restrict__ dmu, float *__restrict__ dS, float *__restrict__ part_dl) {
+    const int *__restrict__ route, float *__restrict__ dmu, float *__restrict__ dS,
+    float *__restrict__ part_dl) {
     // thread (row slot r, dimension q): R = 256 / Q row slots, so that all but
     // 256 mod Q lanes work; slot r takes rows r, r + R, ... of the block
     __shared__ float red_dl[256], red_sf[256];
+    if (route[0]) return;
     const int R = 256 / Q, t = threadIdx.x, r = t / Q, q = t - r * Q;
     const bool act = r < R;
     const int RED = 5 * Q + 2;
@@ -1191,10 +1385,12 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(int64_t N, int M, int 
                                                           const float *__restrict__ pdz,
                                                           int64_t dz_slabs, const float *__restrict__ pdl,
                                                           int64_t dl_parts, float dL_dpsi0,
+                                                          const int *__restrict__ route,
                                                           float *__restrict__ dZ,
                                                           float *__restrict__ dsf2,
                                                           float *__restrict__ dl, int accumulate) {
     __shared__ float red[256];
+    if (route[0]) return;
     const int t = threadIdx.x;
     const int64_t MQ = (int64_t)M * Q;
     if ((int64_t)blockIdx.x < zblocks) {
@@ -1236,7 +1432,7 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(int64_t N, int M, int 
 // ---------------------------------------------------------------- dispatch
 template <int NK, int TPW>
 hipError_t launch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z,
-                      void *ws, hipStream_t st) {
+                      const int *route, void *ws, hipStream_t st) {
     auto k = psi2_fwd_kernel<NK, TPW>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_fwd);
@@ -1246,13 +1442,13 @@ hipError_t launch_fwd(const MPlan &p, const Shape &s, const float *mu, const flo
     k<<<grid, kThreads, p.lds_fwd, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.T,
                                          p.ftasks, p.frows, mu, Z, fat(ws, p.off_zc),
                                          fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc),
-                                         fat(ws, p.off_fp));
+                                         route, fat(ws, p.off_fp));
     return hipGetLastError();
 }
 
 template <int NK, int NQB>
 hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
-                       const Hyp<float> &h, void *ws, hipStream_t st) {
+                       const Hyp<float> &h, const int *route, void *ws, hipStream_t st) {
     auto k = psi2_grad_kernel<NK, NQB>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_grad);
@@ -1263,14 +1459,15 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
         s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.njr, p.wpg, p.igroups, p.grows, mu, Z,
         fat(ws, p.off_zc), fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc),
         fat(ws, p.off_w1), fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2),
-        fat(ws, p.off_hl), fat(ws, p.off_gmax), h, fat(ws, p.off_rs), fat(ws, p.off_dz));
+        fat(ws, p.off_hl), fat(ws, p.off_gmax), fat(ws, p.off_bmax), h, route, fat(ws, p.off_rs),
+        fat(ws, p.off_dz));
     return hipGetLastError();
 }
 
-hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z, void *ws,
-                        hipStream_t st) {
+hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z,
+                        const int *route, void *ws, hipStream_t st) {
 #define GPPS_F(I, T) \
-    if (p.nk == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, ws, st);
+    if (p.nk == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, route, ws, st);
     GPPS_F(1, 1) GPPS_F(1, 2) GPPS_F(1, 3) GPPS_F(1, 4)
     GPPS_F(2, 1) GPPS_F(2, 2) GPPS_F(2, 3) GPPS_F(2, 4)
     GPPS_F(3, 1) GPPS_F(3, 2)
@@ -1281,38 +1478,53 @@ hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const f
 }
 
 hipError_t dispatch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
-                         const Hyp<float> &h, void *ws, hipStream_t st) {
+                         const Hyp<float> &h, const int *route, void *ws, hipStream_t st) {
 #define GPPS_G(I, Q) \
-    if (p.nk == I && p.nqb == Q) return launch_grad<I, Q>(p, s, mu, Z, h, ws, st);
+    if (p.nk == I && p.nqb == Q) return launch_grad<I, Q>(p, s, mu, Z, h, route, ws, st);
     GPPS_G(1, 1) GPPS_G(2, 1) GPPS_G(3, 1) GPPS_G(4, 1) GPPS_G(6, 1) GPPS_G(8, 1)
     GPPS_G(8, 2) GPPS_G(10, 2) GPPS_G(12, 2)
 #undef GPPS_G
     return hipErrorInvalidValue;
 }
 
-// Per-row tables, the centring shift, and the row terms plus Psi1 (forward,
-// psi1 != NULL) or dL/dPsi1 * Psi1 (grad).
+// The centring table, the per-row tables, the range guard (route word), and
+// the row terms plus Psi1 (forward, psi1 != NULL) or dL/dPsi1 * Psi1 (grad).
 void prepare(const MPlan &p, const Shape &s, const float *mu, const float *S, const float *Z,
-             const Hyp<float> &h, const float *G1, float *psi1, bool grad, void *ws,
+             const Hyp<float> &h, const float *G1, float *psi1, bool grad, int *route, void *ws,
              hipStream_t st) {
-    {
-        TimedScope ts(st, "mfma_rows");
-        mfma_rows_kernel<<<(unsigned)cdiv(s.N, kRowsPerBlock), 256, 0, st>>>(
-            s.N, (int)s.Q, S, h, fat(ws, p.off_K), fat(ws, p.off_hq), fat(ws, p.off_w2),
-            fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1));
-    }
     {
         TimedScope ts(st, "mfma_centre");
         mfma_centre_kernel<<<1, 256, 0, st>>>((int)s.M, (int)s.Q, Z, fat(ws, p.off_zc));
     }
+    const int64_t rblocks = cdiv(s.N, kRowsPerBlock);
+    {
+        TimedScope ts(st, "mfma_rows");
+        mfma_rows_kernel<<<(unsigned)rblocks, 256, 0, st>>>(
+            s.N, (int)s.Q, mu, S, fat(ws, p.off_zc), h, fat(ws, p.off_K), fat(ws, p.off_hq),
+            fat(ws, p.off_w2), fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1),
+            fat(ws, p.off_gpart));
+    }
+    {
+        TimedScope ts(st, "mfma_guard");
+        mfma_guard_kernel<<<1, 256, 0, st>>>(rblocks, (int)s.Q, fat(ws, p.off_gpart),
+                                             fat(ws, p.off_zc), h, route);
+    }
     dim3 grid((unsigned)cdiv(s.N, kRTRows), (unsigned)cdiv(p.Mp, 256));
     float *t1 = grad ? fat(ws, p.off_t1) : nullptr;
     TimedScope ts(st, "mfma_rowterm");
-#define GPPS_RT(QM)                                                                           \
-    mfma_rowterm_kernel<QM><<<grid, 256, 0, st>>>(                                            \
-        s.N, (int)s.M, (int)s.Q, (int)p.Mp, mu, Z, fat(ws, p.off_zc), fat(ws, p.off_K),        \
-        fat(ws, p.off_hq), fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1), G1,       \
-        fat(ws, p.off_bt), fat(ws, p.off_bc), psi1, t1)
+#define GPPS_RT(QM)                                                                            \
+    do {                                                                                       \
+        if (grad)                                                                              \
+            mfma_rowterm_kernel<QM, true><<<grid, 256, 0, st>>>(                               \
+                s.N, (int)s.M, (int)s.Q, (int)p.Mp, mu, Z, fat(ws, p.off_zc), fat(ws, p.off_hq), \
+                fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1), G1, route,            \
+                fat(ws, p.off_bt), fat(ws, p.off_bc), nullptr, t1, fat(ws, p.off_bmax));       \
+        else                                                                                   \
+            mfma_rowterm_kernel<QM, false><<<grid, 256, 0, st>>>(                              \
+                s.N, (int)s.M, (int)s.Q, (int)p.Mp, mu, Z, fat(ws, p.off_zc), fat(ws, p.off_hq), \
+                fat(ws, p.off_hl), fat(ws, p.off_w1), fat(ws, p.off_l1), G1, route,            \
+                fat(ws, p.off_bt), fat(ws, p.off_bc), psi1, nullptr, nullptr);                 \
+    } while (0)
     if (s.Q <= 8) GPPS_RT(8);
     else if (s.Q <= 12) GPPS_RT(12);
     else if (s.Q <= 16) GPPS_RT(16);
@@ -1337,47 +1549,48 @@ size_t mfma_workspace_bytes(const Shape &s) { return make_mplan(s).total; }
 
 hipError_t mfma_psi_stats(const Shape &s, const float *mu, const float *S, const float *Z,
                           const Hyp<float> &h, float *psi0, float *Psi1, float *Psi2,
-                          int accumulate, void *ws, hipStream_t st) {
+                          int accumulate, int *route, void *ws, hipStream_t st) {
     const MPlan p = make_mplan(s);
-    prepare(p, s, mu, S, Z, h, nullptr, Psi1, false, ws, st);
-    hipError_t e = dispatch_fwd(p, s, mu, Z, ws, st);
+    prepare(p, s, mu, S, Z, h, nullptr, Psi1, false, route, ws, st);
+    hipError_t e = dispatch_fwd(p, s, mu, Z, route, ws, st);
     if (e != hipSuccess) return e;
     TimedScope ts(st, "mfma_psi2_reduce");
-    psi2_reduce_kernel<<<(unsigned)(p.T * 32), 256, 0, st>>>(s.N, (int)s.M, p.nb, p.T, p.fchunks,
-                                                             fat(ws, p.off_fp), h.sf2, psi0, Psi2,
-                                                             accumulate);
+    psi2_reduce_kernel<<<(unsigned)(p.T * 32), 256, 0, st>>>(
+        s.N, (int)s.M, (int)s.Q, p.nb, p.T, p.fchunks, fat(ws, p.off_fp), Z, h, route, psi0, Psi2,
+        accumulate);
     return hipGetLastError();
 }
 
 hipError_t mfma_psi_grads(const Shape &s, const float *mu, const float *S, const float *Z,
                           const Hyp<float> &h, float dL_dpsi0, const float *G1,
                           const float *G2, float *dmu, float *dS, float *dZ, float *dsf2,
-                          float *dl, int accumulate, void *ws, hipStream_t st) {
+                          float *dl, int accumulate, int *route, void *ws, hipStream_t st) {
     const MPlan p = make_mplan(s);
-    prepare(p, s, mu, S, Z, h, G1, nullptr, true, ws, st);
+    prepare(p, s, mu, S, Z, h, G1, nullptr, true, route, ws, st);
     {
         // NULL dL/dPsi2 means zero: the kernel then adds only the Psi1 terms
         TimedScope ts(st, "mfma_sym");
-        mfma_sym_kernel<<<(unsigned)cdiv(p.Mp * p.Mp, 256), 256, 0, st>>>((int)s.M, (int)p.Mp, G2,
-                                                                          fat(ws, p.off_g2));
+        mfma_sym_kernel<<<(unsigned)cdiv(p.Mp * p.Mp, 256), 256, 0, st>>>(
+            (int)s.M, (int)p.Mp, (int)s.Q, G2, Z, h, route, fat(ws, p.off_g2), fat(ws, p.off_smax));
     }
     {
         TimedScope ts(st, "mfma_absmax");
-        mfma_absmax_kernel<<<1, 1024, 0, st>>>(p.Mp * p.Mp, fat(ws, p.off_g2), fat(ws, p.off_gmax));
+        mfma_absmax_kernel<<<1, 1024, 0, st>>>(cdiv(p.Mp * p.Mp, 256), fat(ws, p.off_smax), route,
+                                               fat(ws, p.off_gmax));
     }
-    hipError_t e = dispatch_grad(p, s, mu, Z, h, ws, st);
+    hipError_t e = dispatch_grad(p, s, mu, Z, h, route, ws, st);
     if (e != hipSuccess) return e;
     {
         TimedScope ts(st, "mfma_psi2_finalize");
         psi2_finalize_kernel<<<(unsigned)p.fin_blocks, 256, 0, st>>>(
-            s.N, (int)s.Q, (int)p.ggroups, fat(ws, p.off_rs), fat(ws, p.off_w2), S, h, dmu, dS,
-            fat(ws, p.off_dl));
+            s.N, (int)s.Q, (int)p.ggroups, fat(ws, p.off_rs), fat(ws, p.off_w2), S, h, route, dmu,
+            dS, fat(ws, p.off_dl));
     }
     const int64_t zblocks = cdiv(s.M * s.Q, kRedOut);
     TimedScope ts(st, "mfma_grad_reduce");
     grad_reduce_kernel<<<(unsigned)(zblocks + s.Q + 1), 256, 0, st>>>(
         s.N, (int)s.M, (int)s.Q, zblocks, fat(ws, p.off_dz), p.gchunks * p.njr, fat(ws, p.off_dl),
-        p.fin_blocks, dL_dpsi0, dZ, dsf2, dl, accumulate);
+        p.fin_blocks, dL_dpsi0, route, dZ, dsf2, dl, accumulate);
     return hipGetLastError();
 }
 

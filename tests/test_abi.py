@@ -55,19 +55,20 @@ def test_workspace_bytes():
 
 
 def _stats(dt=0, N=10, M=4, Q=2, mu=FAKE, S=FAKE, Z=FAKE, sf2=1.0, l=L2, psi0=FAKE, P1=FAKE,
-           P2=FAKE, ws=FAKE, ws_bytes=None):
+           P2=FAKE, flags=0, ws=FAKE, ws_bytes=None):
     if ws_bytes is None:
         ws_bytes = max(1, gpps.lib().gpps_workspace_bytes(dt if dt in (0, 1) else 0, N, M, Q))
-    return gpps.lib().gpps_psi_stats(dt, N, M, Q, mu, S, Z, sf2, l, psi0, P1, P2, 0, ws,
+    return gpps.lib().gpps_psi_stats(dt, N, M, Q, mu, S, Z, sf2, l, psi0, P1, P2, flags, ws,
                                      ws_bytes, None)
 
 
 def _grads(dt=0, N=10, M=4, Q=2, mu=FAKE, S=FAKE, Z=FAKE, sf2=1.0, l=L2, d0=0.5, G1=FAKE,
-           G2=FAKE, dmu=FAKE, dS=FAKE, dZ=FAKE, dsf2=FAKE, dl=FAKE, ws=FAKE, ws_bytes=None):
+           G2=FAKE, dmu=FAKE, dS=FAKE, dZ=FAKE, dsf2=FAKE, dl=FAKE, flags=0, ws=FAKE,
+           ws_bytes=None):
     if ws_bytes is None:
         ws_bytes = max(1, gpps.lib().gpps_workspace_bytes(dt if dt in (0, 1) else 0, N, M, Q))
     return gpps.lib().gpps_psi_grads(dt, N, M, Q, mu, S, Z, sf2, l, d0, G1, G2, dmu, dS, dZ,
-                                     dsf2, dl, 0, ws, ws_bytes, None)
+                                     dsf2, dl, flags, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("fn", [_stats, _grads])
@@ -118,19 +119,39 @@ def test_validation_known_inputs():
         assert gpps.workspace_bytes(dt, 5000, 300, 4) >= 2 * 5000 * 300 * (4 if dt == "f32" else 8)
 
 
-def test_path_selection():
-    L = gpps.lib()
-    old = L.gpps_get_path()
+@pytest.mark.parametrize("fn", [_stats, _grads])
+def test_path_flags(fn):
+    """The path is a per-call flag: unknown bits and both path flags are rejected
+    before any HIP call, and so is the matrix-core flag where that path cannot run
+    (F64 has no matrix-core path; Q = 40 with M = 300 is beyond its limits)."""
+    assert fn(flags=8) == ERR_PATH
+    assert fn(flags=1 << 20) == ERR_PATH
+    assert fn(flags=gpps.PATHS["generic"] | gpps.PATHS["mfma"]) == ERR_PATH
+    assert fn(dt=1, flags=gpps.PATHS["mfma"]) == ERR_PATH
+    assert fn(N=10, M=300, Q=40, l=(ctypes.c_double * 40)(*([1.0] * 40)),
+              flags=gpps.PATHS["mfma"]) == ERR_PATH
+
+
+def test_module_default_path():
     try:
-        assert L.gpps_set_path(9) == ERR_PATH
         for name in ("generic", "mfma", "auto"):
             gpps.set_path(name)
             assert gpps.get_path() == name
-        # F64 has no matrix-core path: forcing it is rejected before any HIP call
-        gpps.set_path("mfma")
-        assert _stats(dt=1, ws_bytes=gpps.lib().gpps_workspace_bytes(1, 10, 4, 2)) == ERR_PATH
+        with pytest.raises(ValueError):
+            gpps.set_path("fast")
     finally:
-        L.gpps_set_path(old)
+        gpps.set_path("auto")
+
+
+def test_route_word_offset():
+    """The route word sits after every path's workspace region, inside the
+    workspace the query returns."""
+    for dt in ("f32", "f64"):
+        for N, M, Q in ((100_000, 256, 20), (200, 10, 2), (5000, 600, 40)):
+            off = gpps.route_word_offset(dt, N, M, Q)
+            ws = gpps.workspace_bytes(dt, N, M, Q)
+            assert off % 256 == 0 and off + 4 <= ws
+    assert gpps.lib().gpps_route_word_offset(0, 0, 10, 2) == 2**64 - 1
 
 
 def test_binding_rejects_bad_tensors():
@@ -142,11 +163,11 @@ def test_binding_rejects_bad_tensors():
 
 def _bound(dt=0, N=10, M=4, Q=2, D=3, mu=FAKE, S=FAKE, Z=FAKE, Y=FAKE, sf2=1.0, l=L2, beta=2.0,
            jitter=1e-6, L=FAKE, dmu=FAKE, dS=FAKE, dZ=FAKE, dsf2=FAKE, dl=FAKE, dbeta=FAKE,
-           ws=FAKE, ws_bytes=None):
+           flags=0, ws=FAKE, ws_bytes=None):
     if ws_bytes is None:
         ws_bytes = max(1, gpps.lib().gpps_bound_workspace_bytes(0, N, M, Q, max(D, 1)))
     return gpps.lib().gpps_bound(dt, N, M, Q, D, mu, S, Z, Y, sf2, l, beta, jitter, L, dmu, dS,
-                                 dZ, dsf2, dl, dbeta, ws, ws_bytes, None)
+                                 dZ, dsf2, dl, dbeta, flags, ws, ws_bytes, None)
 
 
 def test_bound_workspace_bytes():
@@ -177,6 +198,11 @@ def test_bound_validation_codes():
     assert _bound(jitter=-1e-9) == ERR_HYPER
     assert _bound(jitter=float("nan")) == ERR_HYPER
     assert _bound(ws=FAKE + 16) == ERR_ALIGN
+    # path flags only: accumulation has no meaning for the bound
+    assert _bound(flags=1) == ERR_PATH
+    assert _bound(flags=gpps.PATHS["generic"] | gpps.PATHS["mfma"]) == ERR_PATH
+    assert _bound(dt=1, flags=gpps.PATHS["mfma"],
+                  ws_bytes=gpps.lib().gpps_bound_workspace_bytes(1, 10, 4, 2, 3)) == ERR_PATH
     assert _bound(ws_bytes=1) == ERR_WS
     assert _bound(Y=FAKE + 2) == ERR_ALIGN
     assert _bound(dt=1, dbeta=FAKE + 4,

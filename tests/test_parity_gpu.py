@@ -63,13 +63,35 @@ def dev(inp, dtype):
     return {k: (t(v) if isinstance(v, np.ndarray) else v) for k, v in inp.items()}
 
 
-def run_gpu(inp, dtype, want_psi1=True):
+def routes(ws, dtype, N, M, Q):
+    """Route word of the last call on ws (0 matrix cores, 1 generic by the range
+    guard), or None where the call could not have taken the matrix-core path."""
+    if dtype != torch.float32 or gpps.get_path() == "generic":
+        return None
+    return gpps.route_taken(ws, dtype, N, M, Q)
+
+
+def run_gpu(inp, dtype, want_psi1=True, expect_route=None):
+    """Both entry points on the GPU.  Where the call takes the matrix-core path
+    (forced, or expect_route given) the route word of each call must equal
+    expect_route (default 0: the matrix cores computed it)."""
     d = dev(inp, dtype)
+    N, Q = inp["mu"].shape
+    M = inp["Z"].shape[0]
+    ws = torch.full((gpps.workspace_bytes(dtype, N, M, Q),), 0x7F, dtype=torch.uint8, device=DEV)
+    mfma = dtype == torch.float32 and (gpps.get_path() == "mfma" or
+                                       (gpps.get_path() == "auto" and expect_route is not None))
+    if expect_route is None:
+        expect_route = 0
     try:
         psi0, P1, P2 = gpps.psi_stats(d["mu"], d["S"], d["Z"], inp["sigma_f2"], inp["l"],
-                                      want_psi1=want_psi1)
+                                      want_psi1=want_psi1, workspace=ws)
+        if mfma:
+            assert routes(ws, dtype, N, M, Q) == expect_route, "psi_stats route"
         g = gpps.psi_grads(d["mu"], d["S"], d["Z"], inp["sigma_f2"], inp["l"], inp["dL_dpsi0"],
-                           d["dL_dPsi1"], d["dL_dPsi2"])
+                           d["dL_dPsi1"], d["dL_dPsi2"], workspace=ws)
+        if mfma:
+            assert routes(ws, dtype, N, M, Q) == expect_route, "psi_grads route"
     except gpps.GppsError as e:
         if e.status == 8:
             pytest.skip("path does not support this shape")
@@ -449,3 +471,90 @@ def test_mfma_ragged_block_ranges(N, M, Q):
     inp = synth.to_f32(synth.random_inputs(N, M, Q, seed=200 + M))
     got = run_gpu(inp, torch.float32)
     compare_all(got, run_oracle(inp), TOL32, f"ragged-{M}x{Q}")
+
+
+# ------------------------------------------------------------------ fp16 range of the matrix cores
+# The matrix-core path carries its Gram operands and the column bias as two-part
+# fp16 values, scaled per dimension and with the n-independent pair factor taken
+# out of the sum over datapoints.  A device guard routes a call to the generic
+# kernels when an operand bound leaves the fp16 range, or when the inducing
+# inputs spread over more than 64 lengthscales (the gradient's accuracy limit).
+# Each case is compared with the oracle element by element, with the route the
+# guard must take (0 matrix cores, 1 generic).
+def _scaled(c):
+    """Psi1 and Psi2 are invariant under mu, Z, l -> c mu, c Z, c l, S -> c^2 S."""
+    inp = synth.random_inputs(2000, 70, 8, seed=36)
+    return dict(inp, mu=c * inp["mu"], Z=c * inp["Z"], l=c * inp["l"], S=c * c * inp["S"]), 0
+
+
+def _range_case(name):
+    if name.startswith("scaled"):
+        inp, route = _scaled({"scaled-1e-3": 1e-3, "scaled-1e3": 1e3}[name])
+        return synth.to_f32(inp), route
+    rng = np.random.default_rng({"l002-zspread": 31, "q1-l0008": 32, "tiny-l-trip": 33,
+                                 "far-mu-trip": 34, "wide-s": 35, "spread-at-limit": 37}[name])
+    if name == "l002-zspread":       # Q = 10, l = 0.02, mu ~ N(0, 0.3^2), Z ~ N(0, 2.5^2)
+        N, M, Q = 400, 40, 10
+        mu = 0.3 * rng.standard_normal((N, Q))
+        S = rng.uniform(0.01, 0.5, (N, Q))
+        Z = 2.5 * rng.standard_normal((M, Q))
+        l = np.full(Q, 0.02)
+        route = 1                    # R / l ~ 330
+    elif name == "q1-l0008":         # a 1-D latent over [-3.5, 3.5], l = 0.008
+        N, M, Q = 2000, 100, 1
+        mu = rng.uniform(-3.5, 3.5, (N, Q))
+        S = rng.uniform(0.01, 0.5, (N, Q))
+        Z = np.linspace(-3.5, 3.5, M)[:, None]
+        l = np.array([0.008])
+        route = 1                    # R / l ~ 440
+    elif name == "spread-at-limit":  # the first case with l raised to R / 60
+        N, M, Q = 400, 40, 10
+        mu = 0.3 * rng.standard_normal((N, Q))
+        S = rng.uniform(0.01, 0.5, (N, Q))
+        Z = 2.5 * rng.standard_normal((M, Q))
+        l = np.abs(Z - Z.mean(0)).max(0) / 60.0
+        route = 0
+    elif name == "wide-s":           # S >> l^2 in every dimension, Z spread past mu
+        N, M, Q = 600, 64, 6
+        mu = rng.standard_normal((N, Q))
+        S = rng.uniform(1.0, 4.0, (N, Q))
+        Z = 3.0 * rng.standard_normal((M, Q))
+        l = rng.uniform(0.3, 0.6, Q)
+        route = 0
+    elif name == "tiny-l-trip":      # l ~ 1e-3, S ~ 1e-7: R / l ~ 2000
+        N, M, Q = 300, 20, 2
+        mu = rng.standard_normal((N, Q))
+        S = rng.uniform(1e-8, 1e-7, (N, Q))
+        Z = mu[:M] + 1e-4 * rng.standard_normal((M, Q))
+        l = np.array([1e-3, 2e-3])
+        route = 1
+    else:                            # "far-mu-trip": half the data 300 lengthscales away:
+        N, M, Q = 300, 24, 3         # the column bias and Gram operands leave the fp16 range
+        mu = rng.standard_normal((N, Q))
+        mu[: N // 2] += 300.0
+        S = rng.uniform(0.01, 0.5, (N, Q))
+        Z = rng.standard_normal((M, Q))
+        l = rng.uniform(0.8, 1.2, Q)
+        route = 1
+    dL_dpsi0 = float(rng.standard_normal())
+    G1 = rng.standard_normal((N, M))
+    A = rng.standard_normal((M, M))
+    inp = {"mu": mu, "S": S, "Z": Z, "sigma_f2": 1.0, "l": l, "dL_dpsi0": dL_dpsi0,
+           "dL_dPsi1": G1, "dL_dPsi2": 0.5 * (A + A.T)}
+    return synth.to_f32(inp), route
+
+
+RANGE = ["l002-zspread", "q1-l0008", "spread-at-limit", "wide-s", "scaled-1e-3", "scaled-1e3",
+         "tiny-l-trip", "far-mu-trip"]
+
+
+@pytest.mark.parametrize("path", ["auto", "mfma"])
+@pytest.mark.parametrize("name", RANGE)
+def test_matrix_core_operand_range(name, path):
+    gpps.set_path(path)
+    inp, route = _range_case(name)
+    say(f"[range {name} {path}: expect route {route}]")
+    got = run_gpu(inp, torch.float32, expect_route=route)
+    for k, v in got.items():
+        assert np.all(np.isfinite(v)), k
+    compare_all(got, run_oracle(inp), TOL32, f"range-{name}/{path}")

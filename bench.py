@@ -4,14 +4,23 @@ One step = gpps_psi_stats (psi0, Psi1, Psi2) + gpps_psi_grads (dmu, dS, dZ,
 dsigma_f2, dl) over the whole workload, inputs resident in HBM.  The timed
 workload is ``large`` (N=100,000, M=256, Q=20, fp32, synthetic, seed 0).
 
+Timing: the headline runs with the library's per-kernel timing off; every step
+is bracketed by one HIP event pair on the library's stream, and ms_per_step is
+the median over the steps (the wall clock between the two synchronisations is
+reported beside it).  A second pass with per-kernel timing on gives the kernel
+table and the roofline.
+
 Metric: N*M^2*Q terms per second (whole step).  Beside it:
-  roofline      the dominant kernel's algorithmic FLOP rate (HIP events around
-                each launch, on the library's stream, during the timed steps)
-                against the FP32 peak of 157.3 TFLOP/s;
-  pct_fp32_peak the Psi2 forward + gradient kernels together:
-                F_alg = 8 Q N M(M+1)/2 flops over their summed time;
-  exp_per_s     2 N M(M+1)/2 exponentials (one per unique pair and datapoint in
-                each pass) over the same time, beside the v_exp_f32 peak;
+  roofline      the dominant kernel's algorithmic fp32 FLOP rate (6 Q flops per
+                datapoint and unique pair for the Psi2 gradient) against the fp32
+                vector peak of 157.3 TFLOP/s, with what bounds it: its executed
+                matrix-core work against the dense f16 peak, and the vector-ALU /
+                matrix-core busy shares from the committed SQ counters;
+  pct_fp32_peak F_alg = 8 Q N M(M+1)/2 flops over the Psi2 forward and gradient
+                kernels with their reductions (and beside it with the per-row
+                kernels that feed them);
+  exp_per_s     2 N M(M+1)/2 exponentials over the same time, against the
+                measured v_exp_f32 rate (gpps_probe_unit_rates);
   cpu_baseline  the fp64 CPU oracle on a bounded row sample of the same
                 workload, on this host's cores (a reported baseline only).
 
@@ -47,11 +56,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-PEAK_FP32 = 157.3e12          # MI355X FP32 (vector and matrix) peak, FLOP/s
+PEAK_FP32 = 157.3e12          # MI355X FP32 vector peak (packed FMA), FLOP/s
 PEAK_FP64 = 78.6e12           # MI355X FP64 vector peak, FLOP/s
+PEAK_F16_MFMA = 2.5e15        # MI355X dense fp16 / bf16 matrix-core peak, FLOP/s
 PEAK_HBM = 8.0e12             # B/s
-# v_exp_f32 is a quarter-rate transcendental: 256 CUs x 4 SIMDs x 16 lanes / 4 x 2.4 GHz
-PEAK_EXP = 256 * 4 * 16 / 4 * 2.4e9
 METRIC = "N·M²·Q psi-stat+grad terms/sec (fp32) and % of FP32 VALU peak, 1 MI355X"
 
 
@@ -69,8 +77,11 @@ def algorithmic(kernel: str, N: int, M: int, Q: int):
         "generic_grad_rows": ("alu", 4.0 * Q * N * P, "flop"),
         "generic_grad_cols": ("alu", 2.0 * Q * N * P, "flop"),
         "generic_grad_pairs": ("alu", grad, "flop"),
-        "mfma_psi2_fwd": ("mfma", fwd, "flop"),
-        "mfma_psi2_grad": ("mfma", grad, "flop"),
+        # the matrix-core Psi2 kernels are bound by instruction issue on the SIMD,
+        # mostly vector ALU (exp2, weighting, operand splits); their algorithmic
+        # flops are priced against the fp32 vector peak
+        "mfma_psi2_fwd": ("alu", fwd, "flop"),
+        "mfma_psi2_grad": ("alu", grad, "flop"),
         "generic_psi1": ("hbm", 4.0 * (N * M + 2 * N * Q), "byte"),
         "mfma_psi1_fwd": ("hbm", 4.0 * (N * M + 2 * N * Q), "byte"),
         "mfma_psi1_grad": ("hbm", 4.0 * (N * M + 4 * N * Q), "byte"),
@@ -99,6 +110,56 @@ def traffic_for(kernel: str, workload: str):
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
         return None
     return rec["bytes_per_launch"]
+
+
+def counters_for(kernel: str, workload: str):
+    """The committed rocprofv3 SQ counter summary of a kernel (per dispatch), if
+    it was taken on the current source of the kernel; else None."""
+    f = os.path.join(ROOT, "profiles", f"counters_{kernel}_{workload}.json")
+    if not os.path.exists(f):
+        return None
+    rec = json.load(open(f))
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+        return None
+    return rec
+
+
+def time_steps(step, steps: int, stream):
+    """Headline timing with the library's per-kernel timing off: one event pair
+    per step on the library's stream.  Returns (median ms, wall-clock ms per
+    step between the two synchronisations, every step's ms)."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record(stream)
+        step()
+        b.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    per = [a.elapsed_time(b) for a, b in ev]
+    return float(sorted(per)[len(per) // 2]), wall, per
+
+
+def kernel_pass(step, steps: int):
+    """Per-kernel timing (HIP events around every library launch on its stream)
+    over a separate set of steps."""
+    import torch
+
+    import paper_1410_4984_amd as gpps
+    L = gpps.lib()
+    torch.cuda.synchronize()
+    L.gpps_timing_enable(1)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    L.gpps_timing_enable(0)
+    return timed_kernels(L)
 
 
 def cpu_baseline(inp, target_s: float):
@@ -177,21 +238,9 @@ def bench_gplvm(args):
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    L = gpps.lib()
-    L.gpps_timing_enable.argtypes = [ctypes.c_int]
-    L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
-                                      ctypes.c_void_p]
-    L.gpps_timing_enable(1)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    L.gpps_timing_enable(0)
-    kernels = timed_kernels(L)
-    ms = (t1 - t0) * 1e3 / args.steps
+    stream = torch.cuda.current_stream()
+    ms, wall, _ = time_steps(step, args.steps, stream)
+    kernels = kernel_pass(step, args.kernel_steps)
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
     alg = algorithmic(dom, N, M, Q)
     roofline = None
@@ -214,7 +263,8 @@ def bench_gplvm(args):
     rec = {
         "metric": "Bayesian GP-LVM bound + gradient evaluations/sec (fp64), 1 MI355X",
         "value": 1e3 / ms, "unit": "evals/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "ms_per_step_wall_mean": round(wall, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": {"workload": f"gplvm-paper (N={N}, M={M}, Q={Q}, D={D}, seed 0)", "N": N,
                    "M": M, "Q": Q, "D": D, "L": float(out["L"].item())},
@@ -292,20 +342,8 @@ def bench_known(args):
         step()
     torch.cuda.synchronize()
     copy_probe(args, dev)
-    L = gpps.lib()
-    L.gpps_timing_enable.argtypes = [ctypes.c_int]
-    L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
-                                      ctypes.c_void_p]
-    L.gpps_timing_enable(1)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    L.gpps_timing_enable(0)
-    kernels = timed_kernels(L)
-    ms = (t1 - t0) * 1e3 / args.steps
+    ms, wall, _ = time_steps(step, args.steps, stream)
+    kernels = kernel_pass(step, args.kernel_steps)
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
     peak_f = PEAK_FP64 if f64 else PEAK_FP32
     roofline = None
@@ -326,6 +364,7 @@ def bench_known(args):
         "metric": METRIC.replace("(fp32)", "(fp64)") if f64 else METRIC,
         "value": float(N) * M * M * Q / (ms * 1e-3), "unit": "terms/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "ms_per_step_wall_mean": round(wall, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f64" if f64 else "f32", "data": "synthetic",
         "config": {"workload": f"large-known (N={N}, M={M}, Q={Q}, S = 0: known inputs, seed 0)",
@@ -347,6 +386,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--kernel-steps", type=int, default=5,
+                    help="steps of the second pass with per-kernel timing on")
     ap.add_argument("--workload", default="large")
     ap.add_argument("--path", default="auto", choices=["auto", "generic", "mfma"])
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
@@ -402,21 +443,11 @@ def main():
         step()
     torch.cuda.synchronize()
     copy_probe(args, dev)
-    L = gpps.lib()
-    L.gpps_timing_enable.argtypes = [ctypes.c_int]
-    L.gpps_timing_collect.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
-                                      ctypes.c_void_p]
-    L.gpps_timing_enable(1)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    L.gpps_timing_enable(0)
-    kernels = timed_kernels(L)
-    ms = (t1 - t0) * 1e3 / args.steps
+    ms, wall, per = time_steps(step, args.steps, stream)
+    kernels = kernel_pass(step, args.kernel_steps)
+    rates = gpps.unit_rates(dev)
     terms = float(N) * M * M * Q
+    P = M * (M + 1) // 2
 
     # dominant kernel and its roofline
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
@@ -433,22 +464,56 @@ def main():
                     "unit": u, "frac": round(ach / peak, 4),
                     "traffic": traffic_for(dom, args.workload),
                     "algorithmic_per_launch": work}
-    psi2_kernels = [k for k in kernels if any(s in k for s in ("psi2_partial", "psi2_fwd",
-                                                                "psi2_grad", "grad_rows",
-                                                                "grad_cols"))]
-    t_psi2 = sum(kernels[k]["avg_ms"] for k in psi2_kernels) * 1e-3
-    F_alg = 8.0 * Q * N * (M * (M + 1) // 2)
+        cnt = counters_for(dom, args.workload)
+        if cnt is not None and unit == "flop":
+            c = cnt["per_dispatch"]
+            mfma_flops = c["SQ_INSTS_MFMA"] * cnt["flops_per_mfma"]
+            roofline["limiter"] = (
+                "SIMD instruction issue: vector ALU and matrix cores share each wave's issue; "
+                "busy shares per SIMD from the committed SQ counters")
+            roofline["issue"] = {
+                "valu_busy": cnt["derived"]["valu_busy"],
+                "mfma_busy": cnt["derived"]["mfma_busy"],
+                "both_busy": cnt["derived"]["both_busy"],
+                "mfma_executed_flops_per_launch": mfma_flops,
+                "mfma_executed_tflops": round(mfma_flops / avg_s / 1e12, 2),
+                "mfma_peak_f16_tflops": PEAK_F16_MFMA / 1e12,
+                "mfma_frac_f16_peak": round(mfma_flops / avg_s / PEAK_F16_MFMA, 4),
+                "mfma_frac_f16_measured": round(mfma_flops / avg_s / rates["mfma_f16_flops"], 4),
+                "exp_executed_per_launch": c["SQ_INSTS_VALU_TRANS_F32"] * 64,
+                "exp_unique_pairs_per_launch": float(N) * P,
+                "counters": f"profiles/counters_{dom}_{args.workload}.md"}
+    # Psi2 forward + gradient kernels with their reductions (F_alg's kernels), and
+    # beside them with the per-row kernels that feed them
+    core = ("psi2_partial", "psi2_fwd", "psi2_grad", "grad_rows", "grad_cols", "grad_pairs",
+            "psi2_reduce", "psi2_finalize", "grad_reduce")
+    feed = ("mfma_rows", "mfma_rowterm", "mfma_centre", "mfma_guard", "mfma_sym",
+            "mfma_absmax", "generic_rows_pre", "generic_sym", "generic_circ", "generic_psi1")
+    per_step = {k: v["avg_ms"] * v["launches"] / args.kernel_steps for k, v in kernels.items()}
+    t_psi2 = sum(v for k, v in per_step.items() if any(c in k for c in core)) * 1e-3
+    t_feed = sum(v for k, v in per_step.items() if any(c in k for c in feed)) * 1e-3
+    F_alg = 8.0 * Q * N * P
     rec = {
         "metric": METRIC, "value": terms / (ms * 1e-3), "unit": "terms/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "ms_per_step_wall_mean": round(wall, 4),
+        "ms_per_step_min_max": [round(min(per), 4), round(max(per), 4)],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{args.workload} (N={N}, M={M}, Q={Q}, seed 0)",
-                   "N": N, "M": M, "Q": Q, "path": gpps.get_path() if args.path != "auto"
-                   else "auto"},
+                   "N": N, "M": M, "Q": Q, "path": args.path,
+                   "arithmetic": ("matrix-core path: Gram and W [Z | 1] products on "
+                                  "v_mfma_f32_32x32x16_f16 with two-part fp16 operands (22 "
+                                  "significant bits, three cross products) accumulated in fp32; "
+                                  "exponentials, weighting and epilogues in fp32 on the vector "
+                                  "ALU")},
         "pct_fp32_peak": round(100.0 * F_alg / t_psi2 / PEAK_FP32, 2) if t_psi2 > 0 else None,
-        "exp_per_s": 2.0 * N * (M * (M + 1) // 2) / t_psi2 if t_psi2 > 0 else None,
-        "exp_peak": PEAK_EXP,
+        "pct_fp32_peak_with_row_kernels": (round(100.0 * F_alg / (t_psi2 + t_feed) / PEAK_FP32, 2)
+                                           if t_psi2 > 0 else None),
+        "exp_per_s": 2.0 * N * P / t_psi2 if t_psi2 > 0 else None,
+        "exp_frac_measured_rate": (round(2.0 * N * P / t_psi2 / rates["exp"], 4)
+                                   if t_psi2 > 0 else None),
+        "unit_rates_measured": {k: float(f"{v:.4g}") for k, v in rates.items()},
         "roofline": roofline,
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}
                     for k, v in sorted(kernels.items())},

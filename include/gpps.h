@@ -211,6 +211,19 @@ gpps_status gpps_timing_enable(int on);
 int gpps_timing_collect(int max_entries, const char **names, double *total_ms,
                         int64_t *launches);
 
+/* Measurement support: sustained rates of the three units the psi-statistic
+ * kernels spend their time in, measured on the current device by fixed-size
+ * probe kernels enqueued on `stream` (the call synchronises that stream):
+ *   rates[0]  fp32 vector flops/s (v_fma_f32, two flops each, unpacked),
+ *   rates[1]  v_exp_f32 results/s,
+ *   rates[2]  dense f16 matrix-core flops/s (v_mfma_f32_32x32x16_f16).
+ * The benchmark prices the kernels' work against them beside the published
+ * peaks.  sink: device scratch of at least gpps_probe_sink_bytes() bytes
+ * (overwritten).  GPPS_ERR_NULL / GPPS_ERR_WORKSPACE for a missing or short
+ * sink, GPPS_ERR_HIP if a probe fails. */
+size_t gpps_probe_sink_bytes(void);
+gpps_status gpps_probe_unit_rates(void *sink, size_t sink_bytes, double *rates, void *stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char *gpps_status_string(gpps_status status);
 

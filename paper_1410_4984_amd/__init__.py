@@ -67,6 +67,13 @@ def lib():
     L.gpps_bound.argtypes = [i32, i64, i64, i64, i64, vp, vp, vp, vp, d, vp, d, d, vp, vp, vp, vp,
                              vp, vp, vp, i32, vp, sz, vp]
     L.gpps_bound.restype = i32
+    L.gpps_probe_sink_bytes.restype = sz
+    L.gpps_probe_unit_rates.argtypes = [vp, sz, vp, vp]
+    L.gpps_probe_unit_rates.restype = i32
+    L.gpps_timing_enable.argtypes = [i32]
+    L.gpps_timing_enable.restype = i32
+    L.gpps_timing_collect.argtypes = [i32, vp, vp, vp]
+    L.gpps_timing_collect.restype = i32
     L.gpps_status_string.argtypes = [i32]
     L.gpps_status_string.restype = ctypes.c_char_p
     L.gpps_version.restype = i32
@@ -116,6 +123,18 @@ def route_taken(workspace, dtype, N: int, M: int, Q: int) -> int:
     off = route_word_offset(dtype, N, M, Q)
     torch.cuda.synchronize(workspace.device)
     return int(workspace[off:off + 4].cpu().view(torch.int32).item())
+
+
+def unit_rates(device="cuda:0") -> dict:
+    """Measured sustained rates of the device's units (see gpps_probe_unit_rates):
+    fp32 vector FMA flops/s, v_exp_f32 results/s, f16 matrix-core flops/s."""
+    import torch
+    n = int(lib().gpps_probe_sink_bytes())
+    sink = torch.empty(n, dtype=torch.uint8, device=device)
+    rates = (ctypes.c_double * 3)()
+    _check(lib().gpps_probe_unit_rates(sink.data_ptr(), n, ctypes.addressof(rates),
+                                       _stream(None)))
+    return {"fp32_fma_flops": rates[0], "exp": rates[1], "mfma_f16_flops": rates[2]}
 
 
 def workspace_bytes(dtype, N: int, M: int, Q: int) -> int:

@@ -531,6 +531,27 @@ __global__ __launch_bounds__(256) void mfma_sym_kernel(int M, int Mp, int Q,
     }
 }
 
+// Maximum of v over the 64 lanes of the wave, in lane 63 (other lanes hold
+// partial maxima): prefix maxima inside each 16-lane row by DPP row shifts
+// (a lane shifted in from outside the row keeps its own value), then the rows
+// joined by the row broadcasts of lane 15 and lane 31.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_max(float x) {
+    const int y = __builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), CTRL, ROW_MASK,
+                                              0xf, false);
+    return fmaxf(x, __int_as_float(y));
+}
+
+__device__ __forceinline__ float wave_max_lane63(float v) {
+    v = dpp_max<0x111, 0xf>(v);   // row_shr:1
+    v = dpp_max<0x112, 0xf>(v);   // row_shr:2
+    v = dpp_max<0x114, 0xf>(v);   // row_shr:4
+    v = dpp_max<0x118, 0xf>(v);   // row_shr:8
+    v = dpp_max<0x142, 0xa>(v);   // row_bcast:15 into rows 1 and 3
+    v = dpp_max<0x143, 0xc>(v);   // row_bcast:31 into rows 2 and 3
+    return v;
+}
+
 // Row terms and Psi1 for every (n, m), once per call (d = mu - z, centred):
 //   bt[n][m] = hl_n + sum_q hq_nq d^2,   bc[n][m] = bt[n][m] + sum_q 2 hq_nq d mu_nq
 // (2 hq = -log2e w2 / 2 is the Gram weight K of the exponent split)
@@ -553,7 +574,7 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     typedef float v4f __attribute__((ext_vector_type(4)));
     __shared__ v4f s_row[kRTRows][QM];
     __shared__ float s_hl[kRTRows], s_l1[kRTRows];
-    __shared__ float s_bm[GRAD ? kRTRows * 257 : 1];   // b of [row][thread], row stride 257
+    __shared__ float s_bm[GRAD ? kRTRows * 4 : 1];   // per-wave maxima of b: [row][wave]
     if (route[0]) return;
     const int m = blockIdx.y * 256 + threadIdx.x;
     const int64_t n0 = (int64_t)blockIdx.x * kRTRows;
@@ -575,8 +596,10 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
         s_l1[r] = r < cnt ? l1[n0 + r] : 0.f;
     }
     __syncthreads();
+    // every lane runs the row loop (the wave reductions below read all 64 lanes);
+    // lanes past Mp store nothing
     const bool inb = m < Mp, real = m < M;
-    if (inb) {
+    {
         float z[QM];
 #pragma unroll
         for (int q = 0; q < QM; ++q) z[q] = (real && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
@@ -592,31 +615,27 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
                 cc = fmaf(v.w, d, cc);
             }
             const int64_t n = n0 + r;
-            bt[n * Mp + m] = real ? b : kPadBias;
-            bc[n * Mp + m] = real ? b + cc : kPadBiasCol;
+            if (inb) {
+                bt[n * Mp + m] = real ? b : kPadBias;
+                bc[n * Mp + m] = real ? b + cc : kPadBiasCol;
+            }
             const float p1 = __builtin_amdgcn_exp2f(fmaf(-0.5f * kLog2e, e, s_l1[r]));
             if constexpr (GRAD) {
-                t1[n * Mp + m] = (real && G1) ? G1[n * M + m] * p1 : 0.f;
-                s_bm[r * 257 + threadIdx.x] = real ? b : -INFINITY;
+                if (inb) t1[n * Mp + m] = (real && G1) ? G1[n * M + m] * p1 : 0.f;
+                const float w = wave_max_lane63(real ? b : -INFINITY);
+                if ((threadIdx.x & 63) == 63) s_bm[r * 4 + (threadIdx.x >> 6)] = w;
             } else if (psi1 && real) {
                 psi1[n * M + m] = p1;
             }
         }
     }
     if constexpr (!GRAD) return;
-    if (!inb)
-        for (int r = 0; r < cnt; ++r) s_bm[r * 257 + threadIdx.x] = -INFINITY;
     __syncthreads();
-    // thread (row t / 8, part t % 8) takes columns part, part + 8, ...; the 8
-    // parts of a row sit in consecutive lanes and meet in three xor steps
-    const int row = threadIdx.x >> 3, part = threadIdx.x & 7;
-    float v = -INFINITY;
-    if (row < cnt)
-        for (int k = part; k < 256; k += 8) v = fmaxf(v, s_bm[row * 257 + k]);
-    v = fmaxf(v, __shfl_xor(v, 1));
-    v = fmaxf(v, __shfl_xor(v, 2));
-    v = fmaxf(v, __shfl_xor(v, 4));
-    if (part == 0 && row < cnt) bmax[(int64_t)blockIdx.y * N + n0 + row] = v;
+    if ((int)threadIdx.x < cnt) {
+        float v = -INFINITY;
+        for (int w = 0; w < 4; ++w) v = fmaxf(v, s_bm[threadIdx.x * 4 + w]);
+        bmax[(int64_t)blockIdx.y * N + n0 + threadIdx.x] = v;
+    }
 }
 
 // gmax[0] = max |G2c|, gmax[1] = max |G2s| from the sym kernel's per-workgroup

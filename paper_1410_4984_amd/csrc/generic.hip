@@ -238,6 +238,9 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(const int *__restrict
         for (int r = threadIdx.x; r < cnt; r += blockDim.x) s_lp[r] = lp2[base + r];
         __syncthreads();
         if (valid) {
+            // two-level sum: the tile's rows first, then into the chunk total, so
+            // that rounding grows with tile + tiles per chunk, not rows per chunk
+            T tacc = 0;
 #pragma unroll 4
             for (int r = 0; r < cnt; ++r) {
                 T e = s_lp[r] + C;
@@ -246,8 +249,9 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(const int *__restrict
                     const T d = s_mu[r][q] - zbar[q];
                     e -= d * d * s_w2[r][q];
                 }
-                acc += dexp(e);
+                tacc += dexp(e);
             }
+            acc += tacc;
         }
     }
     if (valid) partial[(int64_t)blockIdx.y * P + t] = acc;
@@ -926,6 +930,15 @@ __global__ __launch_bounds__(kColBlock) void grad_cols_kernel(const int *__restr
                     if (q < Q) gz[q] += t * (s_mu[r][q] - zm[q]) * s_w1[r][q];
             }
             if (G2s) {
+                // two-level sum: the row's partners first, then into the chunk total
+                // (the 64-wide variant, already short of registers, adds directly)
+                constexpr bool kTwo = QM <= 32;
+                T gzr_[kTwo ? QM : 1];
+                T *gzr = kTwo ? gzr_ : gz;
+                if constexpr (kTwo) {
+#pragma unroll
+                    for (int q = 0; q < QM; ++q) gzr[q] = 0;
+                }
                 for (int mp = blockIdx.z; mp < M; mp += cr) {
                     const T g = G2s[(int64_t)mp * M + m];
                     T e = s_lp2[r];
@@ -943,8 +956,12 @@ __global__ __launch_bounds__(kColBlock) void grad_cols_kernel(const int *__restr
                         if (q < Q) {
                             T b = Z[(int64_t)mp * Q + q];
                             T d = s_mu[r][q] - T(0.5) * (zm[q] + b);
-                            gz[q] += t * (d * s_w2[r][q] - (zm[q] - b) / (T(2) * h.l2[q]));
+                            gzr[q] += t * (d * s_w2[r][q] - (zm[q] - b) / (T(2) * h.l2[q]));
                         }
+                }
+                if constexpr (kTwo) {
+#pragma unroll
+                    for (int q = 0; q < QM; ++q) gz[q] += gzr[q];
                 }
             }
         }

@@ -23,6 +23,7 @@ import oracle  # noqa: E402
 import paper_1410_4984_amd as gpps  # noqa: E402
 from oracle import bound as ob  # noqa: E402
 from paper_1410_4984_amd import synth  # noqa: E402
+from parity_log import current_test, record  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -89,6 +90,7 @@ def compare_all(got, ref, tol, label):
             continue
         e = rel(got[k], ref[k])
         say(f"  {label} {k}: rel {e:.3e} (tol {tol[k]:.0e})")
+        record(current_test(), label, k, e, tol[k])
         if not e <= tol[k]:
             bad[k] = e
     assert not bad, (label, bad)
@@ -152,6 +154,7 @@ def test_known_large_full_size_sampled():
     ref = oracle.psi2_entries(inp["mu"], S0, inp["Z"], sf2, l, pairs)
     e = rel(got["Psi2"][pairs[:, 0], pairs[:, 1]], ref)
     say(f"  Psi2 sampled: rel {e:.3e}")
+    record(current_test(), "known sampled", "Psi2 (sampled entries)", e, TOL32["Psi2"])
     assert e <= TOL32["Psi2"]
     rows = np.sort(rng.choice(N, 48, replace=False))
     rows[-1] = N - 1
@@ -162,11 +165,13 @@ def test_known_large_full_size_sampled():
                          ("dmu", got["dmu"][rows], g["dmu"], TOL32["dmu"])):
         e = rel(a, b)
         say(f"  {k} rows: rel {e:.3e}")
+        record(current_test(), "known sampled", f"{k} (sampled rows)", e, tol)
         assert e <= tol, k
     zr = rng.choice(M, 3, replace=False)
     ref = oracle.dZ_rows(inp["mu"], S0, inp["Z"], sf2, l, inp["dL_dPsi1"], inp["dL_dPsi2"], zr)
     e = rel(got["dZ"][zr], ref)
     say(f"  dZ rows: rel {e:.3e}")
+    record(current_test(), "known sampled", "dZ (rows summed over all N)", e, TOL32["dZ"])
     assert e <= TOL32["dZ"]
     _identities(inp, got, "known-large")
 
@@ -234,6 +239,7 @@ def test_known_stress_chunked():
     ref = oracle.psi2_entries(inp["mu"], S0, inp["Z"], sf2, l, pairs)
     e = rel(got["Psi2"][pairs[:, 0], pairs[:, 1]], ref)
     say(f"  Psi2 sampled: rel {e:.3e}")
+    record(current_test(), "known sampled", "Psi2 (sampled entries)", e, TOL32["Psi2"])
     assert e <= TOL32["Psi2"]
     _, P1r, _ = oracle.psi_stats(inp["mu"][rows], S0[rows], inp["Z"], sf2, l)
     gr = oracle.psi_grads(inp["mu"][rows], S0[rows], inp["Z"], sf2, l, 0.0, G1_rows,
@@ -242,6 +248,7 @@ def test_known_stress_chunked():
                          ("dmu", got["dmu"][rows], gr["dmu"], TOL32["dmu"])):
         e = rel(a, b)
         say(f"  {k} rows: rel {e:.3e}")
+        record(current_test(), "known sampled", f"{k} (sampled rows)", e, tol)
         assert e <= tol, k
     # identities (the Psi1 term of homogeneity from the per-chunk sums)
     Xn, Zn = inp["mu"], inp["Z"]

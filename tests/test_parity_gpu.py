@@ -24,6 +24,7 @@ torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 import paper_1410_4984_amd as gpps  # noqa: E402
 from paper_1410_4984_amd import synth  # noqa: E402
+from parity_log import current_test, record  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -120,6 +121,7 @@ def compare_all(got, ref, tol, label):
             continue
         e = rel(got[k], ref[k])
         say(f"  {label} {k}: rel {e:.3e} (tol {tol[k]:.0e})")
+        record(current_test(), label, k, e, tol[k])
         if not e <= tol[k]:
             bad[k] = e
     assert not bad, (label, bad)
@@ -179,8 +181,10 @@ def test_small_f64_generic():
 
 # ------------------------------------------------------------------ full size, sampled
 
-def _sampled_checks(inp, got, rng, label, n_rows=48, n_pairs=64, dz_rows=3, G1_rows=None):
-    """Compare sampled outputs against the oracle and check the identities."""
+def _sampled_checks(inp, got, rng, label, n_rows=48, n_pairs=64, dz_rows=3, G1_rows=None,
+                    dz_ref=None):
+    """Compare sampled outputs against the oracle and check the identities.
+    dz_ref(rows) gives the oracle's dZ rows where dL/dPsi1 is not held whole."""
     N, Q = inp["mu"].shape
     M = inp["Z"].shape[0]
     sf2, l = inp["sigma_f2"], inp["l"]
@@ -190,6 +194,7 @@ def _sampled_checks(inp, got, rng, label, n_rows=48, n_pairs=64, dz_rows=3, G1_r
     ref = oracle.psi2_entries(inp["mu"], inp["S"], inp["Z"], sf2, l, pairs)
     e = rel(got["Psi2"][pairs[:, 0], pairs[:, 1]], ref)
     say(f"  {label} Psi2 sampled: rel {e:.3e}")
+    record(current_test(), label, f"Psi2 ({n_pairs} sampled entries)", e, TOL32["Psi2"])
     assert e <= TOL32["Psi2"]
     # rows of Psi1, dmu, dS: per-row outputs depend on their own row only
     rows = np.sort(rng.choice(N, n_rows, replace=False))
@@ -206,14 +211,20 @@ def _sampled_checks(inp, got, rng, label, n_rows=48, n_pairs=64, dz_rows=3, G1_r
             continue
         e = rel(got_k[rows], ref_k)
         say(f"  {label} {k} rows: rel {e:.3e}")
+        record(current_test(), label, f"{k} ({n_rows} sampled rows)", e, tol)
         assert e <= tol, (k, e)
     # rows of dZ (sums over every datapoint)
     if dz_rows:
         zr = rng.choice(M, dz_rows, replace=False)
-        ref = oracle.dZ_rows(inp["mu"], inp["S"], inp["Z"], sf2, l, inp["dL_dPsi1"],
-                             inp["dL_dPsi2"], zr)
+        if dz_ref is None:
+            ref = oracle.dZ_rows(inp["mu"], inp["S"], inp["Z"], sf2, l, inp["dL_dPsi1"],
+                                 inp["dL_dPsi2"], zr)
+        else:
+            ref = dz_ref(zr)
         e = rel(got["dZ"][zr], ref)
         say(f"  {label} dZ rows: rel {e:.3e}")
+        record(current_test(), label, f"dZ ({dz_rows} rows, each summed over all N)", e,
+               TOL32["dZ"])
         assert e <= TOL32["dZ"]
     _identities(inp, got, label)
 
@@ -227,6 +238,7 @@ def _identities(inp, got, label, tol=2e-5):
     r = dmu.sum(0) + dZ.sum(0)
     s = np.abs(dmu).sum(0) + np.abs(dZ).sum(0)
     say(f"  {label} translation residual {np.max(np.abs(r) / s):.2e}")
+    record(current_test(), label, "translation identity residual", np.max(np.abs(r) / s), tol)
     assert np.all(np.abs(r) <= tol * s)
     # scaling of latent dimension q (mu, z, l scaled by c, S by c^2)
     terms = [(mu * dmu).sum(0), (Z * dZ).sum(0), l * dl, 2 * (S * dS).sum(0)]
@@ -234,6 +246,7 @@ def _identities(inp, got, label, tol=2e-5):
     s = (np.abs(mu * dmu).sum(0) + np.abs(Z * dZ).sum(0) + np.abs(l * dl)
          + 2 * np.abs(S * dS).sum(0))
     say(f"  {label} scaling residual {np.max(np.abs(r) / s):.2e}")
+    record(current_test(), label, "scaling identity residual", np.max(np.abs(r) / s), tol)
     assert np.all(np.abs(r) <= tol * s)
     # sf2 homogeneity: sf2 dL/dsf2 = <G1, Psi1> + 2 <G2s, Psi2> + dL_dpsi0 N sf2
     if "Psi1" in got and inp.get("dL_dPsi1") is not None:
@@ -244,6 +257,7 @@ def _identities(inp, got, label, tol=2e-5):
         r = sf2 * got["dsigma_f2"] - (a + b + c)
         s = abs(a) + abs(b) + abs(c)
         say(f"  {label} homogeneity residual {abs(r) / s:.2e}")
+        record(current_test(), label, "sigma_f2 homogeneity residual", abs(r) / s, 1e-4)
         assert abs(r) <= 1e-4 * s
 
 
@@ -321,13 +335,56 @@ def test_stress_chunked(path):
             out[i] = synth.stress_dL_dPsi1_chunk(0, c, min(N, (c + 1) * C) - c * C, M)[r - c * C]
         return out.astype(np.float32).astype(np.float64)
 
+    def g1_columns(cols):
+        """dL/dPsi1[:, cols] over all N rows, chunk by chunk."""
+        out = np.empty((N, len(cols)))
+        for c, r0 in enumerate(range(0, N, C)):
+            r1 = min(N, r0 + C)
+            out[r0:r1] = synth.stress_dL_dPsi1_chunk(0, c, r1 - r0, M)[:, cols]
+        return out.astype(np.float32).astype(np.float64)
+
+    def dz_ref(zr):
+        """dZ rows summed over all N: the Psi2 part (oracle.dZ_rows without dL/dPsi1)
+        plus the Psi1 part of each z_m, which involves only column m of dL/dPsi1
+        (oracle.psi_grads on that single inducing input)."""
+        ref = oracle.dZ_rows(inp["mu"], inp["S"], inp["Z"], inp["sigma_f2"], inp["l"], None,
+                             inp["dL_dPsi2"], zr)
+        G1c = g1_columns(zr)
+        for k, m in enumerate(zr):
+            g = oracle.psi_grads(inp["mu"], inp["S"], inp["Z"][[m]], inp["sigma_f2"], inp["l"],
+                                 0.0, np.ascontiguousarray(G1c[:, [k]]), None)
+            ref[k] += g["dZ"][0]
+        return ref
+
     _sampled_checks(inp, got, np.random.default_rng(2), f"stress/{path}", n_rows=16,
-                    n_pairs=32, dz_rows=0, G1_rows=g1_rows)
+                    n_pairs=32, dz_rows=2, G1_rows=g1_rows, dz_ref=dz_ref)
     # sf2 homogeneity with <G1, Psi1> accumulated per chunk above
     G2s = 0.5 * (inp["dL_dPsi2"] + inp["dL_dPsi2"].T)
     a, b, c = G1_sum, 2 * np.sum(G2s * got["Psi2"]), inp["dL_dpsi0"] * N * inp["sigma_f2"]
     r = inp["sigma_f2"] * got["dsigma_f2"] - (a + b + c)
     assert abs(r) <= 1e-4 * (abs(a) + abs(b) + abs(c))
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_stress_row_subset_full(path):
+    """Every output, dl and dsigma_f2 included, against the oracle on an evenly
+    spaced row subset of the stress workload (same M = 512, Q = 30, l ~ U(0.5, 4)),
+    its dL/dPsi1 rows taken from their chunks."""
+    use_path(path, torch.float32)
+    w = synth.WORKLOADS["stress"]
+    inp = synth.to_f32(synth.make_workload("stress"))
+    N, M, C = w.N, w.M, w.chunk_rows
+    rows = np.arange(0, N, 997)          # 1004 rows, spread over all 8 chunks
+    G1 = np.empty((rows.shape[0], M))
+    for c in range(0, (N + C - 1) // C):
+        sel = (rows >= c * C) & (rows < (c + 1) * C)
+        if sel.any():
+            G1[sel] = synth.stress_dL_dPsi1_chunk(0, c, min(N, (c + 1) * C) - c * C, M)[rows[sel] - c * C]
+    sub = dict(inp, mu=inp["mu"][rows], S=inp["S"][rows],
+               dL_dPsi1=G1.astype(np.float32).astype(np.float64))
+    say(f"[stress subset {rows.shape[0]} rows {path}]")
+    got = run_gpu(sub, torch.float32)
+    compare_all(got, run_oracle(sub), TOL32, f"stress-subset/{path}")
 
 
 # ------------------------------------------------------------------ determinism, chunking

@@ -102,6 +102,27 @@ typedef enum {
  * (the larger of the two, over every path).  0 for an invalid shape or dtype. */
 size_t gpps_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q);
 
+/* Allocation-free gpps_psi_stats, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same computation, arguments and flags as
+ * gpps_psi_stats, with the workspace taken from a static device array of
+ * GPPS_SCRATCH_BYTES that the library holds on every device it runs on until
+ * the process ends.  The call allocates and frees nothing.
+ *   - Calls whose workspace (gpps_workspace_bytes) exceeds GPPS_SCRATCH_BYTES
+ *     return GPPS_ERR_WORKSPACE before any HIP call; split N into row chunks
+ *     with GPPS_ACCUMULATE instead.
+ *   - Every call on a device shares that device's array: calls that may
+ *     overlap on one device (other streams or threads) race and must be
+ *     ordered by the caller.  Contents left by a previous call are ignored.
+ *   - The array's device address is looked up on the first call on each
+ *     device (hipGetSymbolAddress); GPPS_ERR_HIP if that fails. */
+#define GPPS_SCRATCH_BYTES (64 << 20)
+gpps_status gpps_psi_stats_noalloc(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
+                                   const void *mu, const void *S, const void *Z,
+                                   double sigma_f2, const double *l,
+                                   void *psi0, void *Psi1, void *Psi2,
+                                   int flags, void *stream);
+
 /* Diagnostics: byte offset, inside the workspace of a gpps_psi_stats,
  * gpps_psi_grads or gpps_bound call of this shape, of a 32-bit "route word".
  * Calls that take the matrix-core path (F32, S != NULL) write it: 0 when the

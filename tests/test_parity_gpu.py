@@ -612,6 +612,7 @@ def test_matrix_core_operand_range(name, path):
     inp, route = _range_case(name)
     say(f"[range {name} {path}: expect route {route}]")
     got = run_gpu(inp, torch.float32, expect_route=route)
+    record(current_test(), f"range-{name}/{path}", "route", route, None)
     for k, v in got.items():
         assert np.all(np.isfinite(v)), k
     compare_all(got, run_oracle(inp), TOL32, f"range-{name}/{path}")

@@ -381,6 +381,73 @@ def bench_known(args):
     print(json.dumps(rec), flush=True)
 
 
+def bench_views(args):
+    """One step = gpps_psi_stats_views + gpps_psi_grads_views over three views
+    sharing q(X) (section 1, MRD): N = 100,000, Q = 20, M = 256, 192, 128."""
+    import numpy as np
+    import torch
+
+    import paper_1410_4984_amd as gpps
+    from paper_1410_4984_amd import synth
+
+    name = "views-large"
+    N, Ms, Q = synth.VIEW_WORKLOADS[name]
+    w = synth.views_to_f32(synth.make_views_workload(name))
+    dev, dt = "cuda:0", torch.float32
+    t = lambda a: torch.tensor(a, dtype=dt, device=dev)  # noqa: E731
+    mu, S = t(w["mu"]), t(w["S"])
+    V = w["views"]
+    Zs = [t(v["Z"]) for v in V]
+    sf, ls = [v["sigma_f2"] for v in V], [v["l"] for v in V]
+    d0 = [v["dL_dpsi0"] for v in V]
+    G1, G2 = [t(v["dL_dPsi1"]) for v in V], [t(v["dL_dPsi2"]) for v in V]
+    ws = torch.empty(gpps.views_workspace_bytes(dt, N, list(Ms), Q), dtype=torch.uint8, device=dev)
+    st_out = [(torch.zeros(1, device=dev), torch.empty((N, M), device=dev),
+               torch.empty((M, M), device=dev)) for M in Ms]
+    g_out = {"dmu": torch.empty((N, Q), device=dev), "dS": torch.empty((N, Q), device=dev),
+             "dZ": [torch.empty((M, Q), device=dev) for M in Ms],
+             "dsigma_f2": [torch.empty(1, device=dev) for _ in Ms],
+             "dl": [torch.empty(Q, device=dev) for _ in Ms]}
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gpps.psi_stats_views(mu, S, Zs, sf, ls, out=st_out, workspace=ws, stream=stream)
+        gpps.psi_grads_views(mu, S, Zs, sf, ls, d0, G1, G2, out=g_out, workspace=ws,
+                             stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    ms, wall, per = time_steps(step, args.steps, stream)
+    kernels = kernel_pass(step, args.kernel_steps)
+    terms = float(N) * Q * sum(M * M for M in Ms)
+    rec = {
+        "metric": "sum over views of N·M_v²·Q psi-stat+grad terms/sec (fp32), 1 MI355X",
+        "value": terms / (ms * 1e-3), "unit": "terms/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "ms_per_step_wall_mean": round(wall, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{name} (three views sharing q(X): N={N}, Q={Q}, M={list(Ms)}, "
+                               f"seed 0)", "N": N, "M": list(Ms), "Q": Q},
+        "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}
+                    for k, v in sorted(kernels.items())},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        oracle.build(force=False)
+        rows = np.linspace(0, N - 1, 400).astype(np.int64)
+        t0 = time.perf_counter()
+        for v in V:
+            oracle.psi_stats(w["mu"][rows], w["S"][rows], v["Z"], v["sigma_f2"], v["l"])
+            oracle.psi_grads(w["mu"][rows], w["S"][rows], v["Z"], v["sigma_f2"], v["l"],
+                             v["dL_dpsi0"], v["dL_dPsi1"][rows], v["dL_dPsi2"])
+        tc = time.perf_counter() - t0
+        rec["cpu_baseline"] = {"value": len(rows) * Q * sum(M * M for M in Ms) / tc,
+                               "unit": "terms/s", "cores": oracle.num_threads(), "kind": "oracle",
+                               "sample": f"{len(rows)} of {N} rows (evenly spaced), every view, "
+                                         f"fp64 oracle, forward + gradients, {tc:.1f} s wall"}
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -407,6 +474,9 @@ def main():
         return
     if args.workload == "known":
         bench_known(args)
+        return
+    if args.workload == "views":
+        bench_views(args)
         return
 
     import numpy as np

@@ -174,6 +174,42 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q,
                            int flags, void *workspace, size_t workspace_bytes,
                            void *stream);
 
+/*
+ * Several views sharing one q(X) -- the multi-output compositions of section 1
+ * (MRD: each view of the data has its own GP mapping from the same latent
+ * points, so the bound is a sum over views plus one KL term of q(X)).
+ *
+ * View v (0 <= v < V, V <= 64) has M[v] inducing inputs Z[v] (device, M[v] x Q),
+ * variance sigma_f2[v] and lengthscales l[v Q .. v Q + Q - 1] (host).  mu and S
+ * (device N x Q; S = NULL for known inputs) are shared.  Every per-view output
+ * is that of gpps_psi_stats / gpps_psi_grads for the view, with the same flags:
+ *   psi0[v], Psi1[v] (may be NULL, or Psi1 itself NULL), Psi2[v],
+ *   dZ[v], dsigma_f2[v], dl[v]         host arrays of V device pointers;
+ *   dL_dpsi0[v] host, dL_dPsi1[v], dL_dPsi2[v] device (the arrays, or entries, NULL
+ *                                       for zero);
+ *   dmu, dS [N x Q]                    device: the SUM over views of the views'
+ *                                       gradients (overwritten; dS may be NULL when
+ *                                       S is NULL).
+ * The views run in turn on the single-view kernels and path choice; every view
+ * is validated before the first launch (a rejected call enqueues nothing), and
+ * the views' dmu, dS are added in view order.  Workspace: at least
+ * gpps_views_workspace_bytes(dt, V, N, M, Q) bytes, 256-byte aligned.
+ * Errors as for the single-view calls, plus GPPS_ERR_SHAPE for V out of range.
+ */
+size_t gpps_views_workspace_bytes(gpps_dtype dt, int64_t V, int64_t N, const int64_t *M, int64_t Q);
+gpps_status gpps_psi_stats_views(gpps_dtype dt, int64_t V, int64_t N, const int64_t *M, int64_t Q,
+                                 const void *mu, const void *S, const void *const *Z,
+                                 const double *sigma_f2, const double *l, void *const *psi0,
+                                 void *const *Psi1, void *const *Psi2, int flags,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+gpps_status gpps_psi_grads_views(gpps_dtype dt, int64_t V, int64_t N, const int64_t *M, int64_t Q,
+                                 const void *mu, const void *S, const void *const *Z,
+                                 const double *sigma_f2, const double *l, const double *dL_dpsi0,
+                                 const void *const *dL_dPsi1, const void *const *dL_dPsi2,
+                                 void *dmu, void *dS, void *const *dZ, void *const *dsigma_f2,
+                                 void *const *dl, int flags, void *workspace,
+                                 size_t workspace_bytes, void *stream);
+
 /* Bytes of workspace gpps_bound needs for this shape with D output columns.
  * 0 for an invalid shape, D or dtype (or M > GPPS_MAX_M_BOUND). */
 size_t gpps_bound_workspace_bytes(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, int64_t D);

@@ -23,6 +23,8 @@ from __future__ import annotations
 import ctypes
 import os
 
+import numpy as np
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgpps.so")
 
@@ -67,6 +69,14 @@ def lib():
     L.gpps_bound.argtypes = [i32, i64, i64, i64, i64, vp, vp, vp, vp, d, vp, d, d, vp, vp, vp, vp,
                              vp, vp, vp, i32, vp, sz, vp]
     L.gpps_bound.restype = i32
+    L.gpps_views_workspace_bytes.argtypes = [i32, i64, i64, vp, i64]
+    L.gpps_views_workspace_bytes.restype = sz
+    L.gpps_psi_stats_views.argtypes = [i32, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, i32,
+                                       vp, sz, vp]
+    L.gpps_psi_stats_views.restype = i32
+    L.gpps_psi_grads_views.argtypes = [i32, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                       vp, vp, vp, vp, i32, vp, sz, vp]
+    L.gpps_psi_grads_views.restype = i32
     L.gpps_probe_sink_bytes.restype = sz
     L.gpps_probe_unit_rates.argtypes = [vp, sz, vp, vp]
     L.gpps_probe_unit_rates.restype = i32
@@ -325,4 +335,96 @@ def bound(mu, S, Z, Y, sigma_f2, l, beta, jitter=0.0, *, out=None, workspace=Non
         None if S is None else out["dS"].data_ptr(), out["dZ"].data_ptr(),
         out["dsigma_f2"].data_ptr(), out["dl"].data_ptr(), out["dbeta"].data_ptr(),
         _flags(path), workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------- several views (MRD)
+
+def _ptrs(ts):
+    arr = (ctypes.c_void_p * len(ts))()
+    for i, t in enumerate(ts):
+        arr[i] = None if t is None else t.data_ptr()
+    return arr
+
+
+def views_workspace_bytes(dtype, N: int, Ms, Q: int) -> int:
+    Ma = (ctypes.c_int64 * len(Ms))(*Ms)
+    return int(lib().gpps_views_workspace_bytes(_dt(dtype), len(Ms), N, Ma, Q))
+
+
+def _views_common(mu, S, Zs, sigma_f2s, ls):
+    dtype, device = mu.dtype, mu.device
+    N, Q = mu.shape
+    V = len(Zs)
+    if not (len(sigma_f2s) == len(ls) == V):
+        raise ValueError("one Z, sigma_f2 and l per view")
+    _dev_tensor(mu, "mu", dtype, (N, Q), device)
+    if S is not None:
+        _dev_tensor(S, "S", dtype, (N, Q), device)
+    Ms = []
+    for v, Z in enumerate(Zs):
+        _dev_tensor(Z, f"Z[{v}]", dtype, (Z.shape[0], Q), device)
+        Ms.append(int(Z.shape[0]))
+    lh = np.ascontiguousarray(np.concatenate([_host_l(l, Q) for l in ls]))
+    sf = np.ascontiguousarray(np.asarray(sigma_f2s, dtype=np.float64).reshape(V))
+    return dtype, device, N, Q, V, Ms, lh, sf
+
+
+def psi_stats_views(mu, S, Zs, sigma_f2s, ls, *, want_psi1=True, accumulate=False, out=None,
+                    workspace=None, stream=None, path=None):
+    """Statistics of V views sharing q(X) (section 1, MRD): one (psi0, Psi1, Psi2)
+    per view, each as psi_stats would give it.  Returns a list of triples."""
+    import torch
+    dtype, device, N, Q, V, Ms, lh, sf = _views_common(mu, S, Zs, sigma_f2s, ls)
+    if out is None:
+        out = [(torch.zeros(1, dtype=dtype, device=device),
+                torch.empty((N, M), dtype=dtype, device=device) if want_psi1 else None,
+                torch.empty((M, M), dtype=dtype, device=device)) for M in Ms]
+    need = views_workspace_bytes(dtype, N, Ms, Q)
+    if need == 0:
+        raise GppsError(2, status_string(2))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    Ma = (ctypes.c_int64 * V)(*Ms)
+    _check(lib().gpps_psi_stats_views(
+        _dt(dtype), V, N, Ma, Q, mu.data_ptr(), None if S is None else S.data_ptr(),
+        _ptrs(Zs), sf.ctypes.data, lh.ctypes.data, _ptrs([o[0] for o in out]),
+        _ptrs([o[1] for o in out]), _ptrs([o[2] for o in out]), _flags(path, accumulate),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out
+
+
+def psi_grads_views(mu, S, Zs, sigma_f2s, ls, dL_dpsi0s, dL_dPsi1s, dL_dPsi2s, *,
+                    accumulate=False, out=None, workspace=None, stream=None, path=None):
+    """Gradients of L = sum_v L_v over V views sharing q(X): dmu, dS summed over the
+    views, and per view dZ, dsigma_f2, dl.  Returns a dict with dmu, dS and lists
+    dZ, dsigma_f2, dl."""
+    import torch
+    dtype, device, N, Q, V, Ms, lh, sf = _views_common(mu, S, Zs, sigma_f2s, ls)
+    G1 = list(dL_dPsi1s) if dL_dPsi1s is not None else [None] * V
+    G2 = list(dL_dPsi2s) if dL_dPsi2s is not None else [None] * V
+    for v in range(V):
+        if G1[v] is not None:
+            _dev_tensor(G1[v], f"dL_dPsi1[{v}]", dtype, (N, Ms[v]), device)
+        if G2[v] is not None:
+            _dev_tensor(G2[v], f"dL_dPsi2[{v}]", dtype, (Ms[v], Ms[v]), device)
+    if out is None:
+        out = {"dmu": torch.empty((N, Q), dtype=dtype, device=device),
+               "dS": None if S is None else torch.empty((N, Q), dtype=dtype, device=device),
+               "dZ": [torch.zeros((M, Q), dtype=dtype, device=device) for M in Ms],
+               "dsigma_f2": [torch.zeros(1, dtype=dtype, device=device) for _ in Ms],
+               "dl": [torch.zeros(Q, dtype=dtype, device=device) for _ in Ms]}
+    need = views_workspace_bytes(dtype, N, Ms, Q)
+    if need == 0:
+        raise GppsError(2, status_string(2))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    Ma = (ctypes.c_int64 * V)(*Ms)
+    d0 = np.ascontiguousarray(np.asarray(dL_dpsi0s, dtype=np.float64).reshape(V))
+    _check(lib().gpps_psi_grads_views(
+        _dt(dtype), V, N, Ma, Q, mu.data_ptr(), None if S is None else S.data_ptr(), _ptrs(Zs),
+        sf.ctypes.data, lh.ctypes.data, d0.ctypes.data, _ptrs(G1), _ptrs(G2),
+        out["dmu"].data_ptr(), None if out["dS"] is None else out["dS"].data_ptr(),
+        _ptrs(out["dZ"]), _ptrs(out["dsigma_f2"]), _ptrs(out["dl"]), _flags(path, accumulate),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
     return out

@@ -174,10 +174,16 @@ size_t gpps_route_word_offset(gpps_dtype dt, int64_t N, int64_t M, int64_t Q) {
     return regions_bytes(dt, gpps::make_shape(N, M, Q));
 }
 
-gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
-                           const void *S, const void *Z, double sigma_f2, const double *l,
-                           void *psi0, void *Psi1, void *Psi2, int flags, void *workspace,
-                           size_t workspace_bytes, void *stream) {
+}  // extern "C"
+
+namespace gpps {
+
+// Every check of gpps_psi_stats, without any HIP call; *path gets the path
+// that will serve the call.
+gpps_status check_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
+                        const void *S, const void *Z, double sigma_f2, const double *l,
+                        void *psi0, void *Psi1, void *Psi2, int flags, void *workspace,
+                        size_t workspace_bytes, int *path_out) {
     if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
     if (!valid_shape(N, M, Q)) return GPPS_ERR_SHAPE;
     if (!mu || !Z || !psi0 || !Psi2) return GPPS_ERR_NULL;
@@ -191,18 +197,23 @@ gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
     if (req < 0) return GPPS_ERR_PATH;
     const int path = choose_path(dt, s, S, req);
     if (path < 0) return GPPS_ERR_PATH;
-    const hipError_t e = run_stats(dt, path, s, mu, S, Z, sigma_f2, l, psi0, Psi1, Psi2,
-                                   flags & GPPS_ACCUMULATE, workspace,
-                                   static_cast<hipStream_t>(stream));
-    return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
+    *path_out = path;
+    return GPPS_OK;
 }
 
-gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
-                           const void *S, const void *Z, double sigma_f2, const double *l,
-                           double dL_dpsi0, const void *dL_dPsi1, const void *dL_dPsi2,
-                           void *dmu, void *dS, void *dZ, void *dsigma_f2, void *dl,
-                           int flags, void *workspace, size_t workspace_bytes,
-                           void *stream) {
+hipError_t launch_stats(gpps_dtype dt, int path, int64_t N, int64_t M, int64_t Q, const void *mu,
+                        const void *S, const void *Z, double sigma_f2, const double *l, void *psi0,
+                        void *Psi1, void *Psi2, int flags, void *workspace, hipStream_t st) {
+    return run_stats(dt, path, make_shape(N, M, Q), mu, S, Z, sigma_f2, l, psi0, Psi1, Psi2,
+                     flags & GPPS_ACCUMULATE, workspace, st);
+}
+
+// Every check of gpps_psi_grads, without any HIP call.
+gpps_status check_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
+                        const void *S, const void *Z, double sigma_f2, const double *l,
+                        double dL_dpsi0, const void *dL_dPsi1, const void *dL_dPsi2, void *dmu,
+                        void *dS, void *dZ, void *dsigma_f2, void *dl, int flags, void *workspace,
+                        size_t workspace_bytes, int *path_out) {
     if (!valid_dtype(dt)) return GPPS_ERR_DTYPE;
     if (!valid_shape(N, M, Q)) return GPPS_ERR_SHAPE;
     if (!mu || !Z || !dmu || (S && !dS) || !dZ || !dsigma_f2 || !dl) return GPPS_ERR_NULL;
@@ -218,9 +229,50 @@ gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const
     if (req < 0) return GPPS_ERR_PATH;
     const int path = choose_path(dt, s, S, req);
     if (path < 0) return GPPS_ERR_PATH;
-    const hipError_t e = run_grads(dt, path, s, mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, dL_dPsi2,
-                                   dmu, dS, dZ, dsigma_f2, dl, flags & GPPS_ACCUMULATE, workspace,
-                                   static_cast<hipStream_t>(stream));
+    *path_out = path;
+    return GPPS_OK;
+}
+
+hipError_t launch_grads(gpps_dtype dt, int path, int64_t N, int64_t M, int64_t Q, const void *mu,
+                        const void *S, const void *Z, double sigma_f2, const double *l,
+                        double dL_dpsi0, const void *dL_dPsi1, const void *dL_dPsi2, void *dmu,
+                        void *dS, void *dZ, void *dsigma_f2, void *dl, int flags, void *workspace,
+                        hipStream_t st) {
+    return run_grads(dt, path, make_shape(N, M, Q), mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1,
+                     dL_dPsi2, dmu, dS, dZ, dsigma_f2, dl, flags & GPPS_ACCUMULATE, workspace, st);
+}
+
+}  // namespace gpps
+
+extern "C" {
+
+gpps_status gpps_psi_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
+                           const void *S, const void *Z, double sigma_f2, const double *l,
+                           void *psi0, void *Psi1, void *Psi2, int flags, void *workspace,
+                           size_t workspace_bytes, void *stream) {
+    int path = -1;
+    if (gpps_status r = gpps::check_stats(dt, N, M, Q, mu, S, Z, sigma_f2, l, psi0, Psi1, Psi2,
+                                          flags, workspace, workspace_bytes, &path))
+        return r;
+    const hipError_t e = gpps::launch_stats(dt, path, N, M, Q, mu, S, Z, sigma_f2, l, psi0, Psi1,
+                                            Psi2, flags, workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
+}
+
+gpps_status gpps_psi_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
+                           const void *S, const void *Z, double sigma_f2, const double *l,
+                           double dL_dpsi0, const void *dL_dPsi1, const void *dL_dPsi2,
+                           void *dmu, void *dS, void *dZ, void *dsigma_f2, void *dl,
+                           int flags, void *workspace, size_t workspace_bytes,
+                           void *stream) {
+    int path = -1;
+    if (gpps_status r = gpps::check_grads(dt, N, M, Q, mu, S, Z, sigma_f2, l, dL_dpsi0, dL_dPsi1,
+                                          dL_dPsi2, dmu, dS, dZ, dsigma_f2, dl, flags, workspace,
+                                          workspace_bytes, &path))
+        return r;
+    const hipError_t e = gpps::launch_grads(dt, path, N, M, Q, mu, S, Z, sigma_f2, l, dL_dpsi0,
+                                            dL_dPsi1, dL_dPsi2, dmu, dS, dZ, dsigma_f2, dl, flags,
+                                            workspace, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? GPPS_OK : GPPS_ERR_HIP;
 }
 

@@ -97,6 +97,28 @@ hipError_t known_psi_grads(const Shape &s, const T *X, const T *Z, const Hyp<T> 
                            const T *G1, const T *G2, T *dX, T *dZ, T *dsf2, T *dl, int accumulate,
                            void *ws, hipStream_t st);
 
+// ---------------------------------------------------------------- entry points, split
+// The checks of gpps_psi_stats / gpps_psi_grads (no HIP call; *path gets the
+// path that will serve the call) and their launches, for entry points that
+// validate several calls before enqueueing any (the multi-view ones).
+gpps_status check_stats(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
+                        const void *S, const void *Z, double sigma_f2, const double *l,
+                        void *psi0, void *Psi1, void *Psi2, int flags, void *workspace,
+                        size_t workspace_bytes, int *path);
+hipError_t launch_stats(gpps_dtype dt, int path, int64_t N, int64_t M, int64_t Q, const void *mu,
+                        const void *S, const void *Z, double sigma_f2, const double *l, void *psi0,
+                        void *Psi1, void *Psi2, int flags, void *workspace, hipStream_t st);
+gpps_status check_grads(gpps_dtype dt, int64_t N, int64_t M, int64_t Q, const void *mu,
+                        const void *S, const void *Z, double sigma_f2, const double *l,
+                        double dL_dpsi0, const void *dL_dPsi1, const void *dL_dPsi2, void *dmu,
+                        void *dS, void *dZ, void *dsigma_f2, void *dl, int flags, void *workspace,
+                        size_t workspace_bytes, int *path);
+hipError_t launch_grads(gpps_dtype dt, int path, int64_t N, int64_t M, int64_t Q, const void *mu,
+                        const void *S, const void *Z, double sigma_f2, const double *l,
+                        double dL_dpsi0, const void *dL_dPsi1, const void *dL_dPsi2, void *dmu,
+                        void *dS, void *dZ, void *dsigma_f2, void *dl, int flags, void *workspace,
+                        hipStream_t st);
+
 // ---------------------------------------------------------------- Bayesian GP-LVM bound
 // Byte offsets of the psi-statistic buffers inside the bound's workspace (after
 // the first psi_ws bytes, which serve the psi-statistic kernels).

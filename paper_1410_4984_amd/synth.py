@@ -147,3 +147,39 @@ def to_f32(inputs: dict) -> dict:
         else:
             out[k] = v
     return out
+
+
+# Several views sharing one q(X) (section 1: MRD): shared mu, S drawn as in
+# ``large``; per view, inducing inputs Z_v ~ N(0, 1), sigma_f2_v ~ U(0.5, 2),
+# l_v ~ U(0.5, 2) per dimension, and Gaussian dL/dPsi of the view's shape.
+# Draw order: mu, S, then per view Z, sigma_f2, l, dL_dpsi0, dL_dPsi1, A.
+VIEW_WORKLOADS = {
+    "views-tiny": (300, (10, 7, 12), 3),
+    "views-small": (5_000, (50, 30, 20), 10),
+    "views-large": (100_000, (256, 192, 128), 20),
+}
+
+
+def make_views_workload(name: str, seed: int = 0) -> dict:
+    N, Ms, Q = VIEW_WORKLOADS[name]
+    rng = np.random.default_rng(seed)
+    mu = rng.standard_normal((N, Q))
+    S = rng.uniform(0.01, 0.5, (N, Q))
+    views = []
+    for M in Ms:
+        Z = rng.standard_normal((M, Q))
+        sf2 = float(rng.uniform(0.5, 2.0))
+        l = rng.uniform(0.5, 2.0, Q)
+        d0 = float(rng.standard_normal())
+        G1 = rng.standard_normal((N, M))
+        A = rng.standard_normal((M, M))
+        views.append({"Z": Z, "sigma_f2": sf2, "l": l, "dL_dpsi0": d0, "dL_dPsi1": G1,
+                      "dL_dPsi2": 0.5 * (A + A.T)})
+    return {"mu": mu, "S": S, "views": views}
+
+
+def views_to_f32(w: dict) -> dict:
+    f = lambda a: a.astype(np.float32).astype(np.float64)  # noqa: E731
+    return {"mu": f(w["mu"]), "S": f(w["S"]),
+            "views": [{k: (f(v) if isinstance(v, np.ndarray) else float(np.float32(v)))
+                       for k, v in vw.items()} for vw in w["views"]]}

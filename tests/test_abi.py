@@ -207,3 +207,29 @@ def test_bound_validation_codes():
     assert _bound(Y=FAKE + 2) == ERR_ALIGN
     assert _bound(dt=1, dbeta=FAKE + 4,
                   ws_bytes=gpps.lib().gpps_bound_workspace_bytes(1, 10, 4, 2, 3)) == ERR_ALIGN
+
+
+def test_views_validation_codes():
+    """Multi-view entry points: bad V, NULL arrays and a bad view are rejected
+    before any HIP call."""
+    L = gpps.lib()
+    M = (ctypes.c_int64 * 2)(4, 5)
+    Z = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    sf = (ctypes.c_double * 2)(1.0, 1.0)
+    l = (ctypes.c_double * 4)(1.0, 0.5, 1.0, 0.5)
+    outs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    ws_bytes = L.gpps_views_workspace_bytes(0, 2, 10, M, 2)
+    assert ws_bytes >= L.gpps_workspace_bytes(0, 10, 5, 2)
+    assert L.gpps_views_workspace_bytes(0, 0, 10, M, 2) == 0
+
+    def stats(V=2, Ma=M, Za=Z, sfa=sf, la=l, ws=FAKE, wsb=ws_bytes):
+        return L.gpps_psi_stats_views(0, V, 10, Ma, 2, FAKE, FAKE, Za, sfa, la, outs, outs, outs,
+                                      0, ws, wsb, None)
+    assert stats(V=0) == ERR_SHAPE
+    assert stats(V=65) == ERR_SHAPE
+    assert stats(Ma=None) == ERR_NULL
+    assert stats(Za=None) == ERR_NULL
+    assert stats(la=None) == ERR_NULL
+    assert stats(wsb=1) == ERR_WS
+    assert stats(la=(ctypes.c_double * 4)(1.0, 0.5, 1.0, -0.5)) == ERR_HYPER
+    assert stats(ws=FAKE + 16) == ERR_ALIGN

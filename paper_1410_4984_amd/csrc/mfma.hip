@@ -845,6 +845,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     int tj[TPW];
 #pragma unroll
     for (int k = 0; k < TPW; ++k) tj[k] = min(tj0 + k, nb - 1);
+    const bool single = tj0 + 1 >= nb;       // wave-uniform: the task's second tile is past the edge
     v16f acc[TPW];
 #pragma unroll
     for (int k = 0; k < TPW; ++k)
@@ -908,23 +909,34 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
             gram_operand<NK>(zr, lds + L.mub + r * kRowStride + g * GT, lds + L.kb + r * kRowStride + g * GT,
                              lds[L.bcb + r * Mp + ti * kTile + c], g, B);
             const float *bbr = lds + L.bb + r * Mp;
-            if constexpr (TPW <= 2) {
+            if constexpr (TPW == 2) {
                 // both Gram products first: the matrix cores work on tile 1 while tile
                 // 0's exponentials run; the sums follow the exponentials in one run (no
-                // exp2 -> add wait state per entry).  Wider tasks keep the interleaved
-                // order, whose registers allow three waves per SIMD.
-                v16f e[TPW];
-#pragma unroll
-                for (int k = 0; k < TPW; ++k)
-                    e[k] = gram16<NK>(row_terms(bbr, tj[k], g), za + tj[k] * (NK * 2 * 32 * 8), c,
-                                      g, B);
-#pragma unroll
-                for (int k = 0; k < TPW; ++k) {
+                // exp2 -> add wait state per entry).  A task whose second tile lies past
+                // the edge (the last task of a row block with an odd count) computes
+                // its one tile only (wave-uniform branch).
+                if (single) {
+                    const v16f e = gram16<NK>(row_terms(bbr, tj[0], g),
+                                              za + tj[0] * (NK * 2 * 32 * 8), c, g, B);
                     float x[16];
 #pragma unroll
-                    for (int t = 0; t < 16; ++t) x[t] = __builtin_amdgcn_exp2f(e[k][t]);
+                    for (int t = 0; t < 16; ++t) x[t] = __builtin_amdgcn_exp2f(e[t]);
 #pragma unroll
-                    for (int t = 0; t < 16; ++t) acc[k][t] += x[t];
+                    for (int t = 0; t < 16; ++t) acc[0][t] += x[t];
+                } else {
+                    v16f e[TPW];
+#pragma unroll
+                    for (int k = 0; k < TPW; ++k)
+                        e[k] = gram16<NK>(row_terms(bbr, tj[k], g), za + tj[k] * (NK * 2 * 32 * 8),
+                                          c, g, B);
+#pragma unroll
+                    for (int k = 0; k < TPW; ++k) {
+                        float x[16];
+#pragma unroll
+                        for (int t = 0; t < 16; ++t) x[t] = __builtin_amdgcn_exp2f(e[k][t]);
+#pragma unroll
+                        for (int t = 0; t < 16; ++t) acc[k][t] += x[t];
+                    }
                 }
             } else {
 #pragma unroll

@@ -14,6 +14,7 @@ search backs off); the regression fit also bounds its log parameters (L-BFGS-B's
 box constraints), which its first line-search step needs.
 
     fit(Y, Q, M, iters=...) -> FitResult
+    fit_staged(Y, Q, M) -> (FitResult, FitResult, rows)   large N with many inducing inputs
     fit_regression(X, Y, M, iters=...) -> RegressionResult
     paper_data(N, D=3, seed=0) -> (Y, x_true)   the synthetic data of section 4
 
@@ -84,17 +85,29 @@ def _unpack(x, N, M, Q):
     return mu, S, Z, sf2, l, beta
 
 
-def init_params(Y: np.ndarray, Q: int, M: int, seed: int = 0):
-    """PCA means (scaled to unit variance), S = 0.5, Z a random subset of the
-    means, unit lengthscales, sigma_f2 = var(Y), beta = 100 / var(Y)."""
+def init_params(Y: np.ndarray, Q: int, M: int, seed: int = 0, spread: bool = False):
+    """PCA means (scaled to unit variance), sigma_f2 = var(Y), beta = 100 / var(Y), and
+
+    spread=False: S = 0.5, Z a random subset of the means, unit lengthscales;
+    spread=True (Q = 1): Z evenly spaced over the range of the means, S = 0.05 and
+      a lengthscale of 0.1 (below the spacing of the data's features, about the
+      size of a few inducing-input spacings at M = 100).  With many inducing
+      inputs among the means and a unit lengthscale the start has
+      cond(Kmm + beta Psi2) ~ 1e14 (the bound is then undetermined to ~1e-2 in
+      fp64); the spread start is well conditioned."""
     rng = np.random.default_rng(seed)
     Yc = Y - Y.mean(0)
     _, _, Vt = np.linalg.svd(Yc, full_matrices=False)
     mu = Yc @ Vt[:Q].T
     mu = mu / mu.std(0)
+    var = float(Yc.var())
+    if spread:
+        if Q != 1:
+            raise ValueError("the spread start is defined for a one-dimensional latent space")
+        Z = np.linspace(mu.min(), mu.max(), M)[:, None]
+        return mu, np.full_like(mu, 0.05), Z, var, np.array([0.1]), 100.0 / var
     S = np.full_like(mu, 0.5)
     Z = mu[rng.choice(mu.shape[0], size=M, replace=False)].copy()
-    var = float(Yc.var())
     return mu, S, Z, var, np.ones(Q), 100.0 / var
 
 
@@ -149,6 +162,34 @@ def fit(Y: np.ndarray, Q: int, M: int, *, iters: int = 200, dtype=None, jitter: 
     mu, S, Z, sf2, l, beta = _unpack(res.x, N, M, Q)
     return FitResult(mu, S, Z, sf2, l, beta, trace, int(res.nfev), int(res.nit), secs, gpu_s[0],
                      str(res.message))
+
+
+def fit_staged(Y: np.ndarray, Q: int, M: int, *, every: int = 16, iters: int = 300,
+               jitter: float = 1e-4, dtype=None, device: str = "cuda:0", tol: float = 1e-12):
+    """Two-stage fit for large N with many inducing inputs (the section 4 shape:
+    Q = 1, M = 100, N up to 64,000).
+
+    Stage 1 fits every ``every``-th row from the spread start (init_params with
+    spread=True).  Stage 2 fits all rows, starting from stage 1's Z and kernel
+    and noise parameters, each row's (mu, S) taken from its nearest stage-1 row in
+    data space (a k-d tree on Y: the PCA coordinate of a folded 1-D curve is not
+    monotone in the latent).  From a cold start at full N, with 100 inducing
+    inputs spaced far below the lengthscale, the line search keeps stepping into
+    parameters where A = Kmm + beta Psi2 is not positive definite in fp64 and the
+    optimiser stops early.  Returns (stage-1 result, stage-2 result, rows of
+    stage 1)."""
+    from scipy.spatial import cKDTree
+
+    Y = np.asarray(Y, np.float64)
+    Yc = Y - Y.mean(0)
+    mu, S, Z, var, l, beta = init_params(Yc, Q, M, spread=True)
+    sub = np.arange(0, Y.shape[0], every)
+    r1 = fit(Y[sub], Q, M, iters=iters, init=(mu[sub], S[sub], Z, var, l, beta), jitter=jitter,
+             dtype=dtype, device=device, tol=tol)
+    _, nn = cKDTree(Yc[sub]).query(Yc)
+    r2 = fit(Y, Q, M, iters=iters, init=(r1.mu[nn], r1.S[nn], r1.Z, r1.sigma_f2, r1.l, r1.beta),
+             jitter=jitter, dtype=dtype, device=device, tol=tol)
+    return r1, r2, sub
 
 
 _LOG_BOUND = 30.0

@@ -417,15 +417,24 @@ def fp32_stats_spread(p, trials=3):
     return spread
 
 
+# Fixed bars of the fp32 regression bound per case and output.  random16's dZ
+# is the difference of its contributions through Kfu and through Kmm; its
+# oracle moves by 1.3e-4 when Psi1 and Psi2 carry a few fp32 units of error
+# (cond(A) = 5.6e3), so its bar is 5e-4; every other output of both cases moves
+# by less than 1e-5 and keeps the fp32 bar 1e-4.
+F32_BOUND_BARS = {"random16": {"dZ": 5e-4}, "grid25": {}}
+
+
 @pytest.mark.parametrize("case", ["random16", "grid25"])
 def test_regression_bound_f32_matches_oracle(case):
     """The fp32 path stores Psi1 and Psi2 in fp32; the bound's M x M algebra
     (fp64) amplifies their rounding by the conditioning of A = Kmm + beta Psi2,
     and dZ (a difference of its contributions through Kfu and through Kmm) most
-    of all.  Tolerance per output: max(1e-4, 10 x the oracle's own spread under
-    errors of a few fp32 units in Psi1 and Psi2).  The cases keep cond(A) <=
-    1e4 (checked): random16 is the harder one (dZ spread ~1e-4), grid25 a
-    well-spread design (every spread below 1e-5)."""
+    of all.  Tolerances are fixed per case and output (F32_BOUND_BARS, else
+    1e-4); each must be at least 3 x the oracle's own spread under errors of a
+    few fp32 units in Psi1 and Psi2, measured here, so that a bar follows from
+    the conditioning and not from the GPU's result.  The cases keep cond(A) <=
+    1e4 (checked)."""
     p = regression_problem(5000, 16, 2, 3, seed=7, jitter=1e-3) if case == "random16" \
         else _grid_problem()
     _, _, pc = ob.bound_terms(p["X"], None, p["Z"], p["Y"], p["sigma_f2"], p["l"], p["beta"],
@@ -435,15 +444,13 @@ def test_regression_bound_f32_matches_oracle(case):
     assert cond <= 1e4
     spread = fp32_stats_spread(p)
     got, ref = run_bound(p, torch.float32), oracle_bound(p, True)
-    e = abs(got["L"][0] - ref["L"]) / abs(ref["L"])
-    tol = max(1e-4, 10 * spread["L"])
-    say(f"  regression f32 {case} L: rel {e:.2e} (tol {tol:.1e})")
-    assert e <= tol
-    for k in BKEYS:
+    bars = F32_BOUND_BARS[case]
+    for k in ("L",) + BKEYS:
         r = np.asarray(ref[k])
-        e = rel(got[k].reshape(r.shape), r)
-        tol = max(1e-4, 10 * spread[k])
-        say(f"  regression f32 {case} {k}: rel {e:.2e} (tol {tol:.1e})")
-        assert e <= tol, k
-    if case == "grid25":
-        assert max(spread.values()) <= 1e-5
+        e = abs(got["L"][0] - ref["L"]) / abs(ref["L"]) if k == "L" else rel(got[k].reshape(r.shape), r)
+        bar = bars.get(k, 1e-4)
+        say(f"  regression f32 {case} {k}: rel {e:.2e} (bar {bar:.0e}, oracle fp32 spread "
+            f"{spread[k]:.1e})")
+        record(current_test(), f"regression-f32/{case}", k, e, bar)
+        assert spread[k] * 3 <= bar, (k, spread[k])
+        assert e <= bar, k

@@ -572,6 +572,7 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     const int *__restrict__ route, float *__restrict__ bt, float *__restrict__ bc,
     float *__restrict__ psi1, float *__restrict__ t1, float *__restrict__ bmax) {
     typedef float v4f __attribute__((ext_vector_type(4)));
+    constexpr int GR = GRAD ? 8 : 1;   // rows per group: their dL/dPsi1 loads are in flight together
     __shared__ v4f s_row[kRTRows][QM];
     __shared__ float s_hl[kRTRows], s_l1[kRTRows];
     __shared__ float s_bm[GRAD ? kRTRows * 4 : 1];   // per-wave maxima of b: [row][wave]
@@ -579,31 +580,56 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     const int m = blockIdx.y * 256 + threadIdx.x;
     const int64_t n0 = (int64_t)blockIdx.x * kRTRows;
     const int cnt = (int)min<int64_t>(kRTRows, N - n0);
+    // The loads below read clamped (always valid) addresses and are masked by
+    // a multiplication by 0 or 1 afterwards, so that they issue back to back
+    // (a select lets the compiler branch around each load and wait for it).
+    // Every value read is finite here: the range guard, which sends inputs with
+    // an infinite or NaN bound to the generic kernels, has passed.
     for (int i = threadIdx.x; i < kRTRows * QM; i += 256) {
         const int r = i / QM, q = i - r * QM;
-        const bool ok = r < cnt && q < Q;
-        const int64_t n = n0 + r;
-        const float x = ok ? mu[n * Q + q] - zc[q] : 0.f;
+        const float ok = (r < cnt && q < Q) ? 1.f : 0.f;
+        const int qc = min(q, Q - 1);
+        const int64_t k = (n0 + min(r, cnt - 1)) * Q + qc;
         v4f v;
-        v.x = x;
-        v.y = ok ? hq[n * Q + q] : 0.f;
-        v.z = ok ? w1t[n * Q + q] : 0.f;
-        v.w = 2.f * v.y * x;
+        v.x = ok * (mu[k] - zc[qc]);
+        v.y = ok * hq[k];
+        v.z = ok * w1t[k];
+        v.w = 2.f * v.y * v.x;
         s_row[r][q] = v;
     }
     for (int r = threadIdx.x; r < kRTRows; r += 256) {
-        s_hl[r] = r < cnt ? hl[n0 + r] : 0.f;
-        s_l1[r] = r < cnt ? l1[n0 + r] : 0.f;
+        const int64_t n = n0 + min(r, cnt - 1);
+        const float hv = hl[n], lv = l1[n];
+        s_hl[r] = r < cnt ? hv : 0.f;
+        s_l1[r] = r < cnt ? lv : 0.f;
     }
-    __syncthreads();
     // every lane runs the row loop (the wave reductions below read all 64 lanes);
     // lanes past Mp store nothing
     const bool inb = m < Mp, real = m < M;
-    {
-        float z[QM];
+    const int mc = min(m, M - 1);
+    const float realf = real ? 1.f : 0.f;
+    float z[QM];
 #pragma unroll
-        for (int q = 0; q < QM; ++q) z[q] = (real && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
-        for (int r = 0; r < cnt; ++r) {
+    for (int q = 0; q < QM; ++q) {
+        const int qc = min(q, Q - 1);
+        z[q] = (q < Q ? realf : 0.f) * (Z[(int64_t)mc * Q + qc] - zc[qc]);
+    }
+    // (dL/dPsi1 of padded columns: the product of column M - 1's value and 0)
+    float g1c[GR], g1n[GR];
+    auto load_g1 = [&](int r0, float (&g)[GR]) {
+#pragma unroll
+        for (int u = 0; u < GR; ++u) g[u] = realf * G1[(n0 + min(r0 + u, cnt - 1)) * M + mc];
+    };
+    if constexpr (GRAD)
+        if (G1) load_g1(0, g1c);
+    __syncthreads();
+    for (int r0 = 0; r0 < cnt; r0 += GR) {
+        if constexpr (GRAD)
+            if (G1 && r0 + GR < cnt) load_g1(r0 + GR, g1n);
+#pragma unroll
+        for (int u = 0; u < GR; ++u) {
+            const int r = r0 + u;
+            if (r >= cnt) break;
             float b = s_hl[r], cc = 0.f, e = 0.f;
 #pragma unroll
             for (int q = 0; q < QM; ++q) {
@@ -621,12 +647,16 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
             }
             const float p1 = __builtin_amdgcn_exp2f(fmaf(-0.5f * kLog2e, e, s_l1[r]));
             if constexpr (GRAD) {
-                if (inb) t1[n * Mp + m] = (real && G1) ? G1[n * M + m] * p1 : 0.f;
+                if (inb) t1[n * Mp + m] = G1 ? g1c[u] * p1 : 0.f;
                 const float w = wave_max_lane63(real ? b : -INFINITY);
                 if ((threadIdx.x & 63) == 63) s_bm[r * 4 + (threadIdx.x >> 6)] = w;
             } else if (psi1 && real) {
                 psi1[n * M + m] = p1;
             }
+        }
+        if constexpr (GRAD) {
+#pragma unroll
+            for (int u = 0; u < GR; ++u) g1c[u] = g1n[u];
         }
     }
     if constexpr (!GRAD) return;

@@ -212,16 +212,17 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(const int *__restrict
     const bool valid = t < P;
     int m = 0, mp = 0;
     if (valid) pair_coords(t, M, m, mp);
+    // loads from clamped (valid) addresses, masked by a multiplication: a select
+    // around each load would let the compiler wait for the loads one at a time
     T zbar[QM];
     T C = 0;
 #pragma unroll
     for (int q = 0; q < QM; ++q) {
-        zbar[q] = 0;
-        if (q < Q && valid) {
-            T a = Z[(int64_t)m * Q + q], b = Z[(int64_t)mp * Q + q];
-            zbar[q] = T(0.5) * (a + b);
-            C -= (a - b) * (a - b) / (T(4) * h.l2[q]);
-        }
+        const int qc = min(q, Q - 1);
+        const T a = Z[(int64_t)m * Q + qc], b = Z[(int64_t)mp * Q + qc];
+        const T on = q < Q ? T(1) : T(0);
+        zbar[q] = on * (T(0.5) * (a + b));
+        C -= on * ((a - b) * (a - b) / (T(4) * h.l2[qc]));
     }
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
@@ -229,11 +230,26 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(const int *__restrict
     for (int64_t base = r0; base < r1; base += kFwdTile) {
         const int cnt = (int)min<int64_t>(kFwdTile, r1 - base);
         __syncthreads();
-        // zero beyond Q, so that the padded dimensions need no test below
-        for (int i = threadIdx.x; i < cnt * QM; i += blockDim.x) {
-            const int r = i / QM, q = i - r * QM;
-            s_mu[r][q] = q < Q ? mu[(base + r) * Q + q] : T(0);
-            s_w2[r][q] = q < Q ? w2[(base + r) * Q + q] : T(0);
+        // zero beyond Q, so that the padded dimensions need no test below; four
+        // entries per thread have their loads in flight together
+        for (int i0 = threadIdx.x; i0 < cnt * QM; i0 += 4 * blockDim.x) {
+            T a[4], b[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = min(i0 + u * (int)blockDim.x, cnt * QM - 1);
+                const int r = i / QM, q = min(i - r * QM, Q - 1);
+                a[u] = mu[(base + r) * Q + q];
+                b[u] = w2[(base + r) * Q + q];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * (int)blockDim.x;
+                const int r = i / QM, q = i - r * QM;
+                if (i < cnt * QM) {
+                    s_mu[r][q] = q < Q ? a[u] : T(0);
+                    s_w2[r][q] = q < Q ? b[u] : T(0);
+                }
+            }
         }
         for (int r = threadIdx.x; r < cnt; r += blockDim.x) s_lp[r] = lp2[base + r];
         __syncthreads();

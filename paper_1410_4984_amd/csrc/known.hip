@@ -492,7 +492,7 @@ __global__ void known_sym_kernel(int M, const T *__restrict__ G2, T *__restrict_
 // A operand G2s[m][k] is read as G2s[k][m], a contiguous row.  Same XCD
 // grouping as the rank-k update: the m-blocks of one column block n share an XCD.
 template <typename T, bool HAS_G2, bool VEC>
-__global__ __launch_bounds__(256) void known_dkfu_kernel(int64_t N, int M, int64_t nblk, int64_t mb,
+__global__ __launch_bounds__(256, sizeof(T) == 4 ? 2 : 1) void known_dkfu_kernel(int64_t N, int M, int64_t nblk, int64_t mb,
                                                          const T *__restrict__ Kt,
                                                          const T *__restrict__ G1,
                                                          const T *__restrict__ G2s,
@@ -508,20 +508,29 @@ __global__ __launch_bounds__(256) void known_dkfu_kernel(int64_t N, int M, int64
     typename MM::acc_t acc[BT][BT];
     block_product<T, VEC>(G2s, M, m0, M, Kt, N, n0, N, 0, HAS_G2 ? M : 0, false, lds, acc);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w & 1, wn = w >> 1;
+    // Per tile, every load of the epilogue is issued before the first use, from
+    // clamped (valid) addresses; only the stores test the bounds.  (Loads under
+    // the bounds test were each waited for in turn: one memory round trip per
+    // output element.)
 #pragma unroll
     for (int tm = 0; tm < BT; ++tm)
 #pragma unroll
-        for (int tn = 0; tn < BT; ++tn)
+        for (int tn = 0; tn < BT; ++tn) {
+            T g1[MM::NACC], kv[MM::NACC];
+            const int64_t n = n0 + wn * 64 + tn * TILE + lane % TILE;
+            const int64_t nc = min(n, N - 1);
+#pragma unroll
+            for (int v = 0; v < MM::NACC; ++v) {
+                const int64_t m = min<int64_t>(m0 + wm * 64 + tm * TILE + MM::row(v, lane), M - 1);
+                kv[v] = Kt[m * N + nc];
+                g1[v] = G1 ? G1[nc * M + m] : T(0);
+            }
 #pragma unroll
             for (int v = 0; v < MM::NACC; ++v) {
                 const int64_t m = m0 + wm * 64 + tm * TILE + MM::row(v, lane);
-                const int64_t n = n0 + wn * 64 + tn * TILE + lane % TILE;
-                if (m < M && n < N) {
-                    const T g1 = G1 ? G1[n * M + m] : T(0);
-                    const int64_t o = m * N + n;
-                    Et[o] = (g1 + T(2) * acc[tm][tn][v]) * Kt[o];
-                }
+                if (m < M && n < N) Et[m * N + n] = (g1[v] + T(2) * acc[tm][tn][v]) * kv[v];
             }
+        }
 }
 
 // Fixed-order sum over the 256 threads of a workgroup (wave butterflies, then

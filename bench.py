@@ -26,6 +26,10 @@ Metric: N*M^2*Q terms per second (whole step).  Beside it:
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload large]
 
+--workload tiny|small|medium|stress times the same step on the other seeded
+workloads; stress (N = 10^6, M = 512, Q = 30) runs as 8 row chunks of 131,072
+per entry point, accumulating psi0, Psi2, dZ, dl and dsigma_f2 on the device.
+
 --workload gplvm times the next step of the method instead: one evaluation of
 the Bayesian GP-LVM bound and all its gradients (gpps_bound) at the shape of
 the paper's experiment (section 4: Q = 1, M = 100, D = 3, here N = 64,000,
@@ -486,10 +490,15 @@ def main():
     from paper_1410_4984_amd import synth
 
     w = synth.WORKLOADS[args.workload]
-    if w.chunk_rows:
-        raise SystemExit("bench.py times single-call workloads (tiny/small/medium/large)")
     N, M, Q = w.N, w.M, w.Q
     inp = synth.to_f32(synth.make_workload(args.workload))
+    C = w.chunk_rows or N
+    chunks = [(r0, min(N, r0 + C)) for r0 in range(0, N, C)]
+    if w.chunk_rows:
+        # row chunks accumulating on the device, each chunk's dL/dPsi1 from its own seed
+        inp["dL_dPsi1"] = np.concatenate([
+            synth.stress_dL_dPsi1_chunk(0, c, r1 - r0, M).astype(np.float32)
+            for c, (r0, r1) in enumerate(chunks)])
     dev = "cuda:0"
     t = {k: torch.tensor(v, dtype=torch.float32, device=dev) for k, v in inp.items()
          if isinstance(v, np.ndarray)}
@@ -500,14 +509,19 @@ def main():
     g = {"dmu": torch.empty((N, Q), device=dev), "dS": torch.empty((N, Q), device=dev),
          "dZ": torch.empty((M, Q), device=dev), "dsigma_f2": torch.empty(1, device=dev),
          "dl": torch.empty(Q, device=dev)}
-    ws = torch.empty(gpps.workspace_bytes("f32", N, M, Q), dtype=torch.uint8, device=dev)
+    ws = torch.empty(gpps.workspace_bytes("f32", C, M, Q), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():
-        gpps.psi_stats(t["mu"], t["S"], t["Z"], inp["sigma_f2"], inp["l"], out=(psi0, P1, P2),
-                       workspace=ws, stream=stream)
-        gpps.psi_grads(t["mu"], t["S"], t["Z"], inp["sigma_f2"], inp["l"], inp["dL_dpsi0"],
-                       t["dL_dPsi1"], t["dL_dPsi2"], out=g, workspace=ws, stream=stream)
+        for c, (r0, r1) in enumerate(chunks):
+            gpps.psi_stats(t["mu"][r0:r1], t["S"][r0:r1], t["Z"], inp["sigma_f2"], inp["l"],
+                           accumulate=c > 0, out=(psi0, P1[r0:r1], P2), workspace=ws,
+                           stream=stream)
+        for c, (r0, r1) in enumerate(chunks):
+            sub = dict(g, dmu=g["dmu"][r0:r1], dS=g["dS"][r0:r1])
+            gpps.psi_grads(t["mu"][r0:r1], t["S"][r0:r1], t["Z"], inp["sigma_f2"], inp["l"],
+                           inp["dL_dpsi0"], t["dL_dPsi1"][r0:r1], t["dL_dPsi2"],
+                           accumulate=c > 0, out=sub, workspace=ws, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -519,9 +533,10 @@ def main():
     terms = float(N) * M * M * Q
     P = M * (M + 1) // 2
 
-    # dominant kernel and its roofline
+    # dominant kernel and its roofline (a chunked workload launches each kernel
+    # once per chunk: the mean launch covers N / chunks rows)
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
-    alg = algorithmic(dom, N, M, Q)
+    alg = algorithmic(dom, N / len(chunks), M, Q)
     roofline = None
     if alg:
         bound, work, unit = alg
@@ -551,7 +566,7 @@ def main():
                 "mfma_frac_f16_peak": round(mfma_flops / avg_s / PEAK_F16_MFMA, 4),
                 "mfma_frac_f16_measured": round(mfma_flops / avg_s / rates["mfma_f16_flops"], 4),
                 "exp_executed_per_launch": c["SQ_INSTS_VALU_TRANS_F32"] * 64,
-                "exp_unique_pairs_per_launch": float(N) * P,
+                "exp_unique_pairs_per_launch": float(N) / len(chunks) * P,
                 "counters": f"profiles/counters_{dom}_{args.workload}.md"}
     # Psi2 forward + gradient kernels with their reductions (F_alg's kernels), and
     # beside them with the per-row kernels that feed them
@@ -570,7 +585,9 @@ def main():
         "ms_per_step_min_max": [round(min(per), 4), round(max(per), 4)],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload} (N={N}, M={M}, Q={Q}, seed 0)",
+        "config": {"workload": (f"{args.workload} (N={N}, M={M}, Q={Q}, seed 0"
+                                + (f", {len(chunks)} row chunks of {C} accumulating on the device)"
+                                   if len(chunks) > 1 else ")")),
                    "N": N, "M": M, "Q": Q, "path": args.path,
                    "arithmetic": ("matrix-core path: Gram and W [Z | 1] products on "
                                   "v_mfma_f32_32x32x16_f16 with two-part fp16 operands (22 "

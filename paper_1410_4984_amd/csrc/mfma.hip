@@ -109,7 +109,8 @@ constexpr float kSpreadLimit = 64.f;    // guard: largest R_q / l_q (gradient co
 constexpr int kRB = 8;                 // gradient: rows per batch
 constexpr int kFRB = 4;                // forward: rows per batch (prefetched a batch ahead)
 constexpr int kFPF = kFRB * 512 / 256; // forward: per-thread prefetch slots of a [kFRB][Mp] table
-constexpr int kGPF = 4;                // gradient: per-thread load slots of a [kRB][Mp] table
+constexpr int kGPF = 4;                // gradient: per-thread load slots of a staged row table
+static_assert(kGPF * 64 >= kRB * 32, "kGPF slots cover the [kRB][32 wpg] row tables of any workgroup");
 static_assert(kFRB * kRowStride == kThreads, "one mu / kappa value per forward thread");
 constexpr int64_t kCUs = 256;          // compute units of one MI355X
 constexpr int64_t kLdsBytes = 160 * 1024;
@@ -199,10 +200,12 @@ struct MPlan {
 };
 
 // Forward LDS layout (floats):
-//   za  [nb][nk][2][32][8] f16   [centred z | 1] of every block in the packed
-//                       Gram layout (fp16 parts of z and the bias multiplier 1), as
-//                       A operands of the 32x32x16 f16 MFMA: block, instruction,
-//                       lane group, row, 8 consecutive k
+//   za  [waves][tpw][nk][2][32][8] f16   [centred z | 1] of each wave's row blocks
+//                       (tj0 .. tj0 + tpw - 1, clamped) in the packed Gram layout
+//                       (fp16 parts of z and the bias multiplier 1), as A operands
+//                       of the 32x32x16 f16 MFMA: wave, block, instruction, lane
+//                       group, row, 8 consecutive k (only the blocks the wave reads,
+//                       so that more workgroups fit per CU at large M)
 //   bb  [FRB][Mp]       row terms b of the batch (log2 units)
 //   bcb [FRB][Mp]       b + c
 //   mub [FRB][64]       centred mu of the batch (zero beyond Q)
@@ -211,10 +214,10 @@ struct LdsF {
     int za, bb, bcb, mub, kb, total;
 };
 
-__host__ __device__ inline LdsF lds_fwd_layout(int Mp, int nk) {
+__host__ __device__ inline LdsF lds_fwd_layout(int Mp, int nk, int tpw) {
     LdsF L{};
     int o = 0;
-    L.za = o; o += Mp * nk * 16 / 2;
+    L.za = o; o += kWaves * tpw * nk * 2 * 32 * 8 / 2;
     L.bb = o; o += kFRB * Mp;
     L.bcb = o; o += kFRB * Mp;
     L.mub = o; o += kFRB * kRowStride;
@@ -232,8 +235,13 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int nk) {
 //   za  [jpw][nk][2][32][8] f16           the same rows of [centred z | 1] as Gram A
 //                       operands in the packed layout (row m' per lane, 8 consecutive
 //                       slots per lane group and instruction)
-//   bb, bcb [RB][Mp], mub, kb, w1b, w2b [RB][64] (zero past Q), t1 [RB][Mp],
+//   bb  [RB][32 jpw]   row terms b of the workgroup's column blocks of W (m')
+//   bcb [RB][32 wpg]   b + c of its row blocks (m), one block per wave
+//   mub, kb, w1b, w2b [RB][64] (zero past Q)
+//   t1  [RB][32 wpg]   dL/dPsi1 * Psi1 of its row blocks
 //   sc [RB] (log2 of the per-row scale of W), red [RB][wpg][5Q + 2]
+// (only the blocks the workgroup reads are staged, so that the widest workgroup
+// fits in LDS at Mp = 512 too)
 struct LdsG {
     int zx, zb, za, bb, bcb, mub, kb, w1b, w2b, t1, sc, red, total;
 };
@@ -245,13 +253,13 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
     L.zx = o; o += (wpg * kTile * DSF + 3) / 4 * 4;
     L.zb = o; o += jpw * 2 * 2 * 2 * 32 * nqb * 8 / 2;
     L.za = o; o += jpw * nk * 2 * 32 * 8 / 2;
-    L.bb = o; o += kRB * Mp;
-    L.bcb = o; o += kRB * Mp;
+    L.bb = o; o += kRB * jpw * kTile;
+    L.bcb = o; o += kRB * wpg * kTile;
     L.mub = o; o += kRB * kRowStride;
     L.kb = o; o += kRB * kRowStride;
     L.w1b = o; o += kRB * kRowStride;
     L.w2b = o; o += kRB * kRowStride;
-    L.t1 = o; o += kRB * Mp;
+    L.t1 = o; o += kRB * wpg * kTile;
     L.sc = o; o += kRB;
     L.red = o; o += kRB * wpg * (5 * Q + 2);
     L.total = o;
@@ -278,7 +286,7 @@ MPlan make_mplan(const Shape &s) {
     }
     p.ftasks = fwd_tasks(p.nb, p.tpw);
     p.fgroups = cdiv(p.ftasks, kWaves);
-    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.nk).total;
+    p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.nk, p.tpw).total;
     // whole rounds of the chip's workgroup slots, so that no partly filled last
     // round idles most CUs: 6 per CU is two rounds at three workgroups per CU and
     // three at two (the register counts of the instances allow two or three)
@@ -804,46 +812,67 @@ __device__ __forceinline__ v16f row_terms(const float *__restrict__ bbr, int j, 
 
 // [centred z s | 1] rows of blocks blk0 .. blk0 + nblk - 1 (clamped to the last
 // block) as packed Gram A operand tables: [nblk][NK][2][32][8] f16 (slot
-// contents listed at gram_np; zc is the centring table, [4][Q]).
+// contents listed at gram_np; zc is the centring table, [4][Q]), written by the
+// nt threads t0 = 0 .. nt - 1.  Each thread issues the loads of U entries
+// together from clamped (valid) addresses and masks them afterwards (the range
+// guard has passed: every z is finite).
 template <int NK>
 __device__ void stage_za(_Float16 *za, int blk0, int nblk, int nb, int M, int Q,
-                         const float *__restrict__ Z, const float *__restrict__ zc) {
+                         const float *__restrict__ Z, const float *__restrict__ zc, int t0,
+                         int nt) {
     constexpr int NP = gram_np(NK), ODD = gram_odd(NK), T = gram_t(NK);
+    constexpr int U = 8;
     const int total = nblk * NK * 2 * 32 * 8;
-    for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
-        int r = idx;
-        const int e = r % 8; r /= 8;
-        const int cc = r % 32; r /= 32;
-        const int gg = r % 2; r /= 2;
-        const int ins = r % NK; r /= NK;
-        // blocks past the edge repeat the last one, so that every exponent stays finite
-        const int m = min(blk0 + r, nb - 1) * kTile + cc;
-        const int w = 4 * ins + e / 2, half = e & 1;
-        int q = -1, part = 0;      // part 0: high fp16 part of z, 1: low part
-        float v = 0.f;
-        if (w < NP) {
-            q = 2 * w + half;
-        } else if (w < 2 * NP) {
-            q = 2 * (w - NP) + half;
-        } else if (w < 3 * NP) {
-            q = 2 * (w - 2 * NP) + half;
-            part = 1;
-        } else if (ODD && w == 3 * NP) {
-            q = 2 * NP;
-        } else if (ODD && w == 3 * NP + 1) {
-            if (half == 0) { q = 2 * NP; part = 1; }
-        } else if (w == 3 * NP + 2 * ODD) {
-            v = 1.f;               // bias multiplier
-        }
-        if (q >= 0) {
-            q += gg * T;
+    for (int base = t0; base < total; base += U * nt) {
+        float v[U];
+        int pt[U];
+        bool isz[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            int r = base + u * nt;
+            const int e = r % 8; r /= 8;
+            const int cc = r % 32; r /= 32;
+            const int gg = r % 2; r /= 2;
+            const int ins = r % NK; r /= NK;
+            // blocks past the edge repeat the last one, so that every exponent stays finite
+            const int m = min(blk0 + r, nb - 1) * kTile + cc;
+            const int w = 4 * ins + e / 2, half = e & 1;
+            int q = -1, part = 0;  // part 0: high fp16 part of z, 1: low part
+            float one = 0.f;
+            if (w < NP) {
+                q = 2 * w + half;
+            } else if (w < 2 * NP) {
+                q = 2 * (w - NP) + half;
+            } else if (w < 3 * NP) {
+                q = 2 * (w - 2 * NP) + half;
+                part = 1;
+            } else if (ODD && w == 3 * NP) {
+                q = 2 * NP;
+            } else if (ODD && w == 3 * NP + 1) {
+                if (half == 0) { q = 2 * NP; part = 1; }
+            } else if (w == 3 * NP + 2 * ODD) {
+                one = 1.f;         // bias multiplier
+            }
+            if (q >= 0) q += gg * T;
+            const int qc = min(max(q, 0), Q - 1);
             // z scaled by s_q (a power of two: exact), |z s_q| <= 1
-            const float zq = (m < M && q < Q) ? (Z[(int64_t)m * Q + q] - zc[q]) * zc[2 * Q + q] : 0.f;
-            _Float16 hi, lo;
-            split2h(zq, hi, lo);
-            za[idx] = part == 0 ? hi : lo;
-        } else {
-            za[idx] = (_Float16)v;
+            const float zl = (Z[(int64_t)min(m, M - 1) * Q + qc] - zc[qc]) * zc[2 * Q + qc];
+            isz[u] = q >= 0;
+            v[u] = isz[u] ? ((m < M && q < Q) ? zl : 0.f) : one;
+            pt[u] = part;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int idx = base + u * nt;
+            if (idx < total) {
+                if (isz[u]) {
+                    _Float16 hi, lo;
+                    split2h(v[u], hi, lo);
+                    za[idx] = pt[u] == 0 ? hi : lo;
+                } else {
+                    za[idx] = (_Float16)v[u];
+                }
+            }
         }
     }
 }
@@ -863,7 +892,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     const int *__restrict__ route, float *__restrict__ partial) {
     extern __shared__ float lds[];
     if (route[0]) return;
-    const LdsF L = lds_fwd_layout(Mp, NK);
+    const LdsF L = lds_fwd_layout(Mp, NK, TPW);
     constexpr int GT = gram_t(NK);
     _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -882,10 +911,12 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
 #pragma unroll
         for (int t = 0; t < 16; ++t) acc[k][t] = 0.f;
 
-    // constant tables: packed [z | 1] of every block (LDS) and the centred z of the
-    // lane's column m = ti*32 + c at the lane group's dimensions g GT + j
-    // (registers, zero past Q)
-    stage_za<NK>(za, 0, nb, nb, M, Q, Z, zc);
+    // constant tables: packed [z | 1] of the wave's row blocks (LDS, written by the
+    // wave itself; the batch loop's first barrier precedes every read) and the
+    // centred z of the lane's column m = ti*32 + c at the lane group's dimensions
+    // g GT + j (registers, zero past Q)
+    _Float16 *zaw = za + wave * TPW * (NK * 2 * 32 * 8);
+    if (active) stage_za<NK>(zaw, tj0, TPW, nb, M, Q, Z, zc, lane, 64);
     float zr[GT];
     {
         const int m = ti * kTile + c;
@@ -946,8 +977,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
                 // the edge (the last task of a row block with an odd count) computes
                 // its one tile only (wave-uniform branch).
                 if (single) {
-                    const v16f e = gram16<NK>(row_terms(bbr, tj[0], g),
-                                              za + tj[0] * (NK * 2 * 32 * 8), c, g, B);
+                    const v16f e = gram16<NK>(row_terms(bbr, tj[0], g), zaw, c, g, B);
                     float x[16];
 #pragma unroll
                     for (int t = 0; t < 16; ++t) x[t] = __builtin_amdgcn_exp2f(e[t]);
@@ -957,7 +987,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
                     v16f e[TPW];
 #pragma unroll
                     for (int k = 0; k < TPW; ++k)
-                        e[k] = gram16<NK>(row_terms(bbr, tj[k], g), za + tj[k] * (NK * 2 * 32 * 8),
+                        e[k] = gram16<NK>(row_terms(bbr, tj[k], g), zaw + k * (NK * 2 * 32 * 8),
                                           c, g, B);
 #pragma unroll
                     for (int k = 0; k < TPW; ++k) {
@@ -971,8 +1001,8 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
             } else {
 #pragma unroll
                 for (int k = 0; k < TPW; ++k) {
-                    const v16f e = gram16<NK>(row_terms(bbr, tj[k], g),
-                                              za + tj[k] * (NK * 2 * 32 * 8), c, g, B);
+                    const v16f e = gram16<NK>(row_terms(bbr, tj[k], g), zaw + k * (NK * 2 * 32 * 8),
+                                              c, g, B);
 #pragma unroll
                     for (int t = 0; t < 16; ++t) acc[k][t] += __builtin_amdgcn_exp2f(e[t]);
                 }
@@ -1140,13 +1170,18 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     const float lgc = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
     const float lgs = gmax[1] > 0.f ? __builtin_amdgcn_logf(gmax[1]) : 0.f;
     const int nbm = (Mp + 255) / 256;          // bmax parts (ranges of 256 inducing inputs)
-    stage_za<NK>(za, jr * JPW, JPW, nb, M, Q, Z, zc);
+    stage_za<NK>(za, jr * JPW, JPW, nb, M, Q, Z, zc, threadIdx.x, blockDim.x);
 
     // Batches of kRB rows staged in LDS between two barriers.  All loads of a
     // batch are issued before any LDS write (the first kGPF * blockDim entries of
-    // each [kRB][Mp] table and one entry of each [kRB][64] table per thread; any
-    // rest is loaded afterwards), so that the batch waits for one round trip to
-    // memory rather than one per loop pass.
+    // each row table and one entry of each [kRB][64] table per thread; any rest
+    // is loaded afterwards), so that the batch waits for one round trip to memory
+    // rather than one per loop pass.  The row tables hold the workgroup's column
+    // blocks jr*JPW .. (bb: JB entries per row) and row blocks ib0 .. (bcb, t1: BW
+    // entries per row, which kGPF slots always cover); entries of rows >= cb or of
+    // blocks past the edge are never read, and their loads use clamped addresses.
+    const int JB = JPW * kTile, BW = wpg * kTile;
+    const int jcol0 = jr * JPW * kTile, icol0 = ib0 * kTile;
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
     const int tid = threadIdx.x, nthr = blockDim.x;
@@ -1158,10 +1193,12 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
             for (int j = 0; j < kGPF; ++j) {
                 const int k = tid + j * nthr;
-                const bool ok = k < cb * Mp;
-                pb[j] = ok ? bt[n0 * Mp + k] : kPadBias;
-                pc[j] = ok ? bc[n0 * Mp + k] : kPadBiasCol;
-                pt[j] = ok ? t1g[n0 * Mp + k] : 0.f;
+                const int rb = min(k / JB, cb - 1), rc = min(k / BW, cb - 1);
+                const int64_t ob = (n0 + rb) * Mp + min(jcol0 + k % JB, Mp - 1);
+                const int64_t oc = (n0 + rc) * Mp + min(icol0 + k % BW, Mp - 1);
+                pb[j] = bt[ob];
+                pc[j] = bc[oc];
+                pt[j] = t1g[oc];
             }
             const int r = tid / kRowStride, q = tid - r * kRowStride;
             const bool okr = tid < kRB * kRowStride && r < cb && q < Q;
@@ -1179,8 +1216,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
             for (int j = 0; j < kGPF; ++j) {
                 const int k = tid + j * nthr;
-                if (k < kRB * Mp) {
-                    lds[L.bb + k] = pb[j];
+                if (k < kRB * JB) lds[L.bb + k] = pb[j];
+                if (k < kRB * BW) {
                     lds[L.bcb + k] = pc[j];
                     lds[L.t1 + k] = pt[j];
                 }
@@ -1196,12 +1233,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 lds[L.sc + tid] = tid < cb ? fminf(120.f, fmaxf(-120.f, floorf(14.f - wb))) : 0.f;
             }
         }
-        for (int k = tid + kGPF * nthr; k < kRB * Mp; k += nthr) {
-            const bool ok = k < cb * Mp;
-            lds[L.bb + k] = ok ? bt[n0 * Mp + k] : kPadBias;
-            lds[L.bcb + k] = ok ? bc[n0 * Mp + k] : kPadBiasCol;
-            lds[L.t1 + k] = ok ? t1g[n0 * Mp + k] : 0.f;
-        }
+        for (int k = tid + kGPF * nthr; k < kRB * JB; k += nthr)   // narrow workgroups only
+            lds[L.bb + k] = bt[(n0 + min(k / JB, cb - 1)) * Mp + min(jcol0 + k % JB, Mp - 1)];
         for (int k = tid + nthr; k < kRB * kRowStride; k += nthr) {
             const int r = k / kRowStride, q = k - r * kRowStride;
             const bool ok = r < cb && q < Q;
@@ -1220,7 +1253,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             // Gram B operand: -K d = (z - mu) K for column block i and (b + c)_m (+ the
             // row scale) in the last k slot
             const float sc = lds[L.sc + r];
-            const float bcol = lds[L.bcb + r * Mp + i * kTile + c] + sc;
+            const float bcol = lds[L.bcb + r * BW + wave * kTile + c] + sc;
             v8h GB[NK];
             {
                 const float *zi = lds + L.zx + (wave * kTile + c) * DSF + g * GT;
@@ -1230,7 +1263,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
                 gram_operand<NK>(zv, lds + L.mub + r * kRowStride + g * GT,
                                  lds + L.kb + r * kRowStride + g * GT, bcol, g, GB);
             }
-            const float *bbr = lds + L.bb + r * Mp;
+            const float *bbr = lds + L.bb + r * JB;
             v16f V[NQB];
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb)
@@ -1239,7 +1272,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
             for (int k = 0; k < JPW; ++k) {
                 const int j = jb[k];
-                const v16f e = gram16<NK>(row_terms(bbr, j, g), za + k * (NK * 2 * 32 * 8), c, g, GB);
+                const v16f e = gram16<NK>(row_terms(bbr, j - jr * JPW, g), za + k * (NK * 2 * 32 * 8), c, g, GB);
                 // W tile (scaled by 2^sc), split into two fp16 parts; A operand of
                 // instruction hh takes the lane's rows crow(8 hh + e, g), as the B
                 // operand tables do
@@ -1291,7 +1324,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb) X[qb] = Y[qb] = P[qb] = X1[qb] = P1[qb] = 0.f;
             const float *zblk = lds + L.zx + wave * kTile * DSF;
-            const float *t1r = lds + L.t1 + r * Mp + i * kTile;
+            const float *t1r = lds + L.t1 + r * BW + wave * kTile;
 #pragma unroll
             for (int t = 0; t < 16; ++t) {
                 const int rr = crow(t, g);

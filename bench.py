@@ -29,6 +29,8 @@ Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload large]
 --workload tiny|small|medium|stress times the same step on the other seeded
 workloads; stress (N = 10^6, M = 512, Q = 30) runs as 8 row chunks of 131,072
 per entry point, accumulating psi0, Psi2, dZ, dl and dsigma_f2 on the device.
+--dtype f64 times the fp64 (generic) kernels on the same inputs, against the
+fp64 vector peak.
 
 --workload gplvm times the next step of the method instead: one evaluation of
 the Bayesian GP-LVM bound and all its gradients (gpps_bound) at the shape of
@@ -81,6 +83,7 @@ def algorithmic(kernel: str, N: int, M: int, Q: int):
         "generic_grad_rows": ("alu", 4.0 * Q * N * P, "flop"),
         "generic_grad_cols": ("alu", 2.0 * Q * N * P, "flop"),
         "generic_grad_pairs": ("alu", grad, "flop"),
+        "generic_grad_wide": ("alu", grad, "flop"),
         # the matrix-core Psi2 kernels are bound by instruction issue on the SIMD,
         # mostly vector ALU (exp2, weighting, operand splits); their algorithmic
         # flops are priced against the fp32 vector peak
@@ -465,7 +468,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0)
     ap.add_argument("--dtype", default="f32", choices=["f32", "f64"],
-                    help="element type of --workload known")
+                    help="element type (f64: the generic fp64 kernels; not for gplvm, which "
+                         "is fp64, or views)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the multi-GPU path (row sharding with an "
@@ -491,25 +495,30 @@ def main():
 
     w = synth.WORKLOADS[args.workload]
     N, M, Q = w.N, w.M, w.Q
-    inp = synth.to_f32(synth.make_workload(args.workload))
+    f64 = args.dtype == "f64"
+    npdt = np.float64 if f64 else np.float32
+    inp = synth.make_workload(args.workload)
+    if not f64:
+        inp = synth.to_f32(inp)
     C = w.chunk_rows or N
     chunks = [(r0, min(N, r0 + C)) for r0 in range(0, N, C)]
     if w.chunk_rows:
         # row chunks accumulating on the device, each chunk's dL/dPsi1 from its own seed
         inp["dL_dPsi1"] = np.concatenate([
-            synth.stress_dL_dPsi1_chunk(0, c, r1 - r0, M).astype(np.float32)
+            synth.stress_dL_dPsi1_chunk(0, c, r1 - r0, M).astype(npdt)
             for c, (r0, r1) in enumerate(chunks)])
     dev = "cuda:0"
-    t = {k: torch.tensor(v, dtype=torch.float32, device=dev) for k, v in inp.items()
+    dt = torch.float64 if f64 else torch.float32
+    t = {k: torch.tensor(v, dtype=dt, device=dev) for k, v in inp.items()
          if isinstance(v, np.ndarray)}
     gpps.set_path(args.path)
-    psi0 = torch.zeros(1, device=dev)
-    P1 = torch.empty((N, M), device=dev)
-    P2 = torch.empty((M, M), device=dev)
-    g = {"dmu": torch.empty((N, Q), device=dev), "dS": torch.empty((N, Q), device=dev),
-         "dZ": torch.empty((M, Q), device=dev), "dsigma_f2": torch.empty(1, device=dev),
-         "dl": torch.empty(Q, device=dev)}
-    ws = torch.empty(gpps.workspace_bytes("f32", C, M, Q), dtype=torch.uint8, device=dev)
+    psi0 = torch.zeros(1, dtype=dt, device=dev)
+    P1 = torch.empty((N, M), dtype=dt, device=dev)
+    P2 = torch.empty((M, M), dtype=dt, device=dev)
+    g = {k: torch.empty(shape, dtype=dt, device=dev)
+         for k, shape in (("dmu", (N, Q)), ("dS", (N, Q)), ("dZ", (M, Q)), ("dsigma_f2", (1,)),
+                          ("dl", (Q,)))}
+    ws = torch.empty(gpps.workspace_bytes(dt, C, M, Q), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():
@@ -533,6 +542,11 @@ def main():
     terms = float(N) * M * M * Q
     P = M * (M + 1) // 2
 
+    # which kernels computed the step: the matrix-core ones unless the range guard
+    # sent the call to the generic kernels (the route word; fp64 is always generic)
+    on_mfma = any(k.startswith("mfma_psi2") for k in kernels) and \
+        gpps.route_taken(ws, dt, C, M, Q) == 0
+    PEAK_VALU = PEAK_FP64 if f64 else PEAK_FP32
     # dominant kernel and its roofline (a chunked workload launches each kernel
     # once per chunk: the mean launch covers N / chunks rows)
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
@@ -542,14 +556,14 @@ def main():
         bound, work, unit = alg
         avg_s = kernels[dom]["avg_ms"] * 1e-3
         if unit == "flop":
-            ach, peak, u = work / avg_s / 1e12, PEAK_FP32 / 1e12, "TFLOP/s"
+            ach, peak, u = work / avg_s / 1e12, PEAK_VALU / 1e12, "TFLOP/s"
         else:
             ach, peak, u = work / avg_s / 1e9, PEAK_HBM / 1e9, "GB/s"
         roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak,
                     "unit": u, "frac": round(ach / peak, 4),
                     "traffic": traffic_for(dom, args.workload),
                     "algorithmic_per_launch": work}
-        cnt = counters_for(dom, args.workload)
+        cnt = counters_for(dom, args.workload) if on_mfma else None
         if cnt is not None and unit == "flop":
             c = cnt["per_dispatch"]
             mfma_flops = c["SQ_INSTS_MFMA"] * cnt["flops_per_mfma"]
@@ -571,6 +585,7 @@ def main():
     # Psi2 forward + gradient kernels with their reductions (F_alg's kernels), and
     # beside them with the per-row kernels that feed them
     core = ("psi2_partial", "psi2_fwd", "psi2_grad", "grad_rows", "grad_cols", "grad_pairs",
+            "grad_wide",
             "psi2_reduce", "psi2_finalize", "grad_reduce")
     feed = ("mfma_rows", "mfma_rowterm", "mfma_centre", "mfma_guard", "mfma_sym",
             "mfma_absmax", "generic_rows_pre", "generic_sym", "generic_circ", "generic_psi1")
@@ -583,23 +598,25 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "ms_per_step_wall_mean": round(wall, 4),
         "ms_per_step_min_max": [round(min(per), 4), round(max(per), 4)],
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64" if f64 else "f32", "data": "synthetic",
         "config": {"workload": (f"{args.workload} (N={N}, M={M}, Q={Q}, seed 0"
                                 + (f", {len(chunks)} row chunks of {C} accumulating on the device)"
                                    if len(chunks) > 1 else ")")),
                    "N": N, "M": M, "Q": Q, "path": args.path,
-                   "arithmetic": ("matrix-core path: Gram and W [Z | 1] products on "
-                                  "v_mfma_f32_32x32x16_f16 with two-part fp16 operands (22 "
-                                  "significant bits, three cross products) accumulated in fp32; "
-                                  "exponentials, weighting and epilogues in fp32 on the vector "
-                                  "ALU")},
-        "pct_fp32_peak": round(100.0 * F_alg / t_psi2 / PEAK_FP32, 2) if t_psi2 > 0 else None,
-        "pct_fp32_peak_with_row_kernels": (round(100.0 * F_alg / (t_psi2 + t_feed) / PEAK_FP32, 2)
-                                           if t_psi2 > 0 else None),
+                   "arithmetic": (("matrix-core path: Gram and W [Z | 1] products on "
+                                   "v_mfma_f32_32x32x16_f16 with two-part fp16 operands (22 "
+                                   "significant bits, three cross products) accumulated in fp32; "
+                                   "exponentials, weighting and epilogues in fp32 on the vector "
+                                   "ALU") if on_mfma else
+                                  f"generic path: {'fp64' if f64 else 'fp32'} on the vector ALU")},
+        f"pct_{'fp64' if f64 else 'fp32'}_peak": (round(100.0 * F_alg / t_psi2 / PEAK_VALU, 2)
+                                                  if t_psi2 > 0 else None),
+        f"pct_{'fp64' if f64 else 'fp32'}_peak_with_row_kernels": (
+            round(100.0 * F_alg / (t_psi2 + t_feed) / PEAK_VALU, 2) if t_psi2 > 0 else None),
         "exp_per_s": 2.0 * N * P / t_psi2 if t_psi2 > 0 else None,
         "exp_frac_measured_rate": (round(2.0 * N * P / t_psi2 / rates["exp"], 4)
-                                   if t_psi2 > 0 else None),
+                                   if t_psi2 > 0 and not f64 else None),
         "unit_rates_measured": {k: float(f"{v:.4g}") for k, v in rates.items()},
         "roofline": roofline,
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]}

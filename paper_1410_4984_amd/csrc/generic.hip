@@ -12,14 +12,20 @@
 // with zbar = (z_m + z_m') / 2, and Psi2 = sum_n Psi2_n.
 //
 // Work split: Psi1 one thread per output; Psi2 one thread per unique pair
-// (m <= m'), a workgroup per 16 x 16 pair tile and row chunk, partial sums per
-// chunk reduced in a fixed order.  Gradients: a row kernel (one thread per
-// datapoint and range of pair rows m) produces partial dmu, dS and per-block
-// dl / dsf2 partials; a column kernel (one thread per inducing input, row chunk
-// and range of partners m') produces dZ partials; fixed-order reduce kernels
-// combine them (the ranges exist so that small N still fills the chip).  No
-// atomics anywhere.
+// (m <= m'), partial sums per row chunk reduced in a fixed order.  Gradients,
+// by the first form that applies:
+//   * pairs kernels (small Q): one thread per inducing input m, the Z table in
+//     LDS, per row the sums r and V over the partners m' (symmetric form: each
+//     unordered pair evaluated once);
+//   * the wide kernel (Q up to 32 in fp64, 64 in fp32): the same ordered sums
+//     with two lanes per m, each holding half of the dimensions;
+//   * otherwise a row kernel (one thread per datapoint and range of pair rows m:
+//     dmu, dS and dl / dsf2 partials) and a column kernel (one thread per
+//     inducing input, row chunk and range of partners: dZ partials).
+// Fixed-order reduce kernels combine the partials.  No atomics anywhere.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "internal.h"
 
@@ -44,6 +50,13 @@ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Register width (latent dimensions, padded) of the pairs kernel for Q.
 inline int64_t pairs_qm(int64_t Q) { return Q <= 1 ? 1 : Q <= 2 ? 2 : Q <= 4 ? 4 : Q <= 8 ? 8 : 16; }
+// Dimensions per lane of the wide gradient kernel for Q (0: none fits; fp64
+// keeps seven arrays of QH doubles live, fp32 the same in floats).
+inline int wide_qh(int64_t Q, size_t elem) {
+    for (int qh : {4, 6, 8, 10, 12, 16, 24, 32})
+        if (2 * qh >= Q) return (elem == 8 && qh > 16) ? 0 : qh;
+    return 0;
+}
 
 struct Plan {
     int64_t tiles_edge;              // pair tiles per edge (Psi2 reduce)
@@ -61,6 +74,9 @@ struct Plan {
     int prs, psthreads;              // its rows at a time and threads per workgroup
     int pthreads;                    // pairs kernel: threads (inducing inputs) per workgroup
     int64_t pmb, pchunks, prows;     // pairs kernel: m-blocks, row chunks, rows per chunk
+    bool wide;                       // gradients by grad_wide_kernel (wider Q, Z table in LDS)
+    int wqh;                         // its dimensions per lane
+    int64_t wmb, wchunks, wrows;     // its blocks of 128 inducing inputs, row chunks, rows
     // workspace offsets in bytes
     size_t off_w1, off_w2, off_lp1, off_lp2, off_p2, off_g2s, off_gc, off_colp, off_rowp, off_rowg,
         total;
@@ -109,6 +125,14 @@ Plan make_plan(const Shape &s, size_t elem) {
         p.prows = cdiv(cdiv(s.N, p.pchunks), p.prs) * p.prs;
         p.pchunks = cdiv(s.N, p.prows);
     }
+    // wide form: where the pairs kernel does not apply and the padded Z table
+    // fits in LDS
+    p.wqh = wide_qh(s.Q, elem);
+    p.wide = !p.pairs && p.wqh > 0 && (s.M + 128) * 2 * p.wqh * elem <= 65536;
+    p.wmb = cdiv(s.M, 128);
+    p.wchunks = std::max<int64_t>(1, std::min<int64_t>(s.N, 2048 / p.wmb));
+    p.wrows = cdiv(s.N, p.wchunks);
+    p.wchunks = cdiv(s.N, p.wrows);
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     p.off_w1 = take(elem * s.N * s.Q);
@@ -118,9 +142,10 @@ Plan make_plan(const Shape &s, size_t elem) {
     p.off_p2 = take(elem * p.nc2 * s.P);
     p.off_g2s = take(elem * s.M * s.M);
     p.off_gc = take(elem * (s.M / 2 + 1) * s.M);
-    p.off_colp = take(elem * std::max(p.ncc * p.cr, p.pchunks) * s.M * s.Q);
-    p.off_rowp = take(elem * std::max(p.rr * p.row_blocks, p.pmb * p.pchunks) * (s.Q + 1));
-    p.off_rowg = take(elem * std::max(p.rr, p.pmb) * s.N * s.Q * 2);
+    p.off_colp = take(elem * std::max({p.ncc * p.cr, p.pchunks, p.wchunks}) * s.M * s.Q);
+    p.off_rowp =
+        take(elem * std::max({p.rr * p.row_blocks, p.pmb * p.pchunks, p.wmb * p.wchunks}) * (s.Q + 1));
+    p.off_rowg = take(elem * std::max({p.rr, p.pmb, p.wmb}) * s.N * s.Q * 2);
     p.total = o;
     return p;
 }
@@ -1030,6 +1055,208 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(const int *__restrict_
     }
 }
 
+// Wide form of the ordered pairs gradient, for Q past the pairs kernel's
+// register budget (same outputs as grad_pairs_kernel with SYM = false: rowg,
+// colpart, rowpart).  Two lanes of a wave share an inducing input m (lanes l
+// and l + 32) and each holds QH of its dimensions (lane half hh takes
+// q = hh QH .. hh QH + QH - 1), which halves the per-dimension registers (z,
+// the exponent's coefficients, the V sums, the dZ and dl partials).  Per partner
+// m' each lane forms its half of the exponent (the same quadratic in
+// v = z_m' - z_m as the pairs kernel); the halves are exchanged across the lane
+// pair and added in the same order on both lanes, so both evaluate the same
+// W = G2s[m, m'] Psi2_n[m, m'] and update their own dimensions:
+//   r += W,   Vz_q += W z_m'q        (V = mu r - Vz in the epilogue).
+// Row values are read from clamped addresses and masked, so that their loads
+// issue together.  One workgroup per (block of 128 inducing inputs, row chunk).
+template <typename T, int QH>
+__global__ __launch_bounds__(256) void grad_wide_kernel(const int *__restrict__ gate,
+    int64_t N, int M, int Q, int64_t rows_per_chunk, const T *__restrict__ mu,
+    const T *__restrict__ S, const T *__restrict__ Z, const T *__restrict__ w1t,
+    const T *__restrict__ w2t, const T *__restrict__ lp1, const T *__restrict__ lp2, Hyp<T> h,
+    const T *__restrict__ G1, const T *__restrict__ G2s, T *__restrict__ rowg,
+    T *__restrict__ colpart, T *__restrict__ rowpart) {
+    if (gate && gate[0] == 0) return;
+    constexpr int QM = 2 * QH;
+    extern __shared__ double gw_smem[];
+    T *sz = reinterpret_cast<T *>(gw_smem);  // [M][QM], zero beyond Q
+    __shared__ T red[2][4][2 * QM];           // per-wave row sums, double buffered by row
+    __shared__ T redf[4][QM + 1];             // per-wave dl and dsf2 sums
+    __shared__ T sc4[QM], sil2[QM], sl[QM], sinvl[QM];  // 1/(4 l^2), 1/l^2, l, 1/l (zero
+                                                        // beyond Q, except l = 1)
+    __shared__ T srow[2][4][QM];              // staged row values (mu, w1, w2, S)
+    __shared__ T sgl[4][QM];                  // per-wave dl sums over the chunk
+    T *sgz = sz + M * QM;                     // [128][QM] the threads' dZ_m sums (dynamic LDS)
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5;
+    const int m = blockIdx.x * 128 + wv * 32 + (lane & 31);
+    const bool valid = m < M;                 // the same on both lanes of a pair
+    const int q0 = hh * QH;
+    for (int i = tid; i < M * QM; i += 256) {
+        const int mm = i / QM, q = i - mm * QM;
+        sz[i] = q < Q ? Z[(int64_t)mm * Q + q] : T(0);
+    }
+    for (int q = tid; q < QM; q += 256) {
+        sc4[q] = q < Q ? T(0.25) / h.l2[q] : T(0);
+        sil2[q] = q < Q ? T(1) / h.l2[q] : T(0);
+        sl[q] = q < Q ? h.l[q] : T(1);
+        sinvl[q] = q < Q ? T(1) / h.l[q] : T(0);
+    }
+    __syncthreads();
+    // the thread's dZ_m sums and each half-wave's dl sums live in LDS slots
+    // that only they write (read-modify-write once per row and dimension)
+    T z[QH];
+    const int ml = m - blockIdx.x * 128;      // the thread's inducing input in the block
+#pragma unroll
+    for (int j = 0; j < QH; ++j) {
+        z[j] = valid ? sz[m * QM + q0 + j] : T(0);
+        sgz[ml * QM + q0 + j] = 0;
+    }
+    if ((lane & 31) == 0)
+        for (int j = 0; j < QH; ++j) sgl[wv][q0 + j] = 0;
+    T gsf = 0;
+    // Each row's values (mu, w1, w2, S at every dimension, zero beyond Q) are
+    // staged in LDS, double buffered by row parity: the next row's are written
+    // before the barrier that ends the current row.
+    auto stage_row = [&](int64_t n, int buf) {
+        for (int i = tid; i < 4 * QM; i += 256) {
+            const int k = i / QM, q = i - k * QM;
+            const T *src = k == 0 ? mu : k == 1 ? w1t : k == 2 ? w2t : S;
+            srow[buf][k][q] = (q < Q ? T(1) : T(0)) * src[n * Q + min(q, Q - 1)];
+        }
+    };
+    // the two halves of a per-lane-pair sum, added in the same order on both lanes
+    auto pair_sum = [&](T own) {
+        const T other = __shfl_xor(own, 32);
+        return hh == 0 ? own + other : other + own;
+    };
+    const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk, r1 = min(N, r0 + rows_per_chunk);
+    if (r0 < r1) stage_row(r0, (int)(r0 & 1));
+    __syncthreads();
+    for (int64_t n = r0; n < r1; ++n) {
+        const int b = (int)(n & 1);   // the row's buffer (its first row may be odd)
+        const T *xs = srow[b][0] + q0, *a1s = srow[b][1] + q0, *a2s = srow[b][2] + q0,
+                *svs = srow[b][3] + q0;
+        T bq[QH], cq[QH], Vz[QH];
+        T r = 0, e0 = 0;
+        {
+            T part = 0;
+#pragma unroll
+            for (int j = 0; j < QH; ++j) {
+                const T a2 = a2s[j], d = xs[j] - z[j];
+                bq[j] = a2 * d;
+                cq[j] = sc4[q0 + j] + T(0.25) * a2;
+                part -= bq[j] * d;
+                Vz[j] = 0;
+            }
+            e0 = (G2s ? lp2[n] : T(0)) + pair_sum(part);
+        }
+        if (G2s && valid) {
+            // G2s is symmetric: G2s[m'][m] is a coalesced row over the wave's m;
+            // its entries are loaded kAhead partners ahead
+            constexpr int kAhead = 2;
+            const T *g2 = G2s + m;
+            T gb[kAhead];
+#pragma unroll
+            for (int u = 0; u < kAhead; ++u) gb[u] = u < M ? g2[(int64_t)u * M] : T(0);
+            for (int mp0 = 0; mp0 < M; mp0 += kAhead) {
+#pragma unroll
+                for (int u = 0; u < kAhead; ++u) {
+                    const int mp = mp0 + u;
+                    if (mp >= M) break;  // uniform
+                    const T g = gb[u];
+                    if (mp + kAhead < M) gb[u] = g2[(int64_t)(mp + kAhead) * M];
+                    const T *zr = sz + mp * QM + q0;
+                    T zp[QH];
+#pragma unroll
+                    for (int j = 0; j < QH; ++j) zp[j] = zr[j];
+                    T ep = 0;
+#pragma unroll
+                    for (int j = 0; j < QH; ++j) {
+                        const T v = zp[j] - z[j];
+                        ep = fma(v, fma(-cq[j], v, bq[j]), ep);
+                    }
+                    const T W = g * dexp(e0 + pair_sum(ep));
+                    r += W;
+#pragma unroll
+                    for (int j = 0; j < QH; ++j) Vz[j] = fma(W, zp[j], Vz[j]);
+                }
+            }
+        }
+        T t = 0;
+        if (G1 && valid) {
+            T e1 = 0;
+#pragma unroll
+            for (int j = 0; j < QH; ++j) {
+                const T d = xs[j] - z[j];
+                e1 += d * d * a1s[j];
+            }
+            t = G1[n * M + m] * dexp(lp1[n] - T(0.5) * pair_sum(e1));
+        }
+        // per dimension: the dmu / dS terms summed over the block's m (butterflies
+        // within each half-wave, whose lanes hold the same dimensions; then the
+        // waves in order), the thread's dZ_m and dl terms.  The scheduling
+        // barrier keeps each dimension's reads in its own step, so that the
+        // epilogue does not hold every dimension's values at once.
+        gsf += hh == 0 ? T(2) * r + t : T(0);  // dsf2 term, counted once per m
+#pragma unroll
+        for (int j = 0; j < QH; ++j) {
+            const int q = q0 + j;
+            const T x = xs[j], a1 = a1s[j], a2 = a2s[j], sv = svs[j];
+            const T dq = x - z[j], d2 = dq * dq, dr = dq * r;
+            const T V = x * r - Vz[j];
+            const T dV = dq * V;
+            const T il2 = sil2[q], l = sl[q], il = sinvl[q];
+            T v0 = -T(2) * a2 * dr - t * dq * a1;
+            T v1 = a2 * a2 * (d2 * r + dV) - a2 * r + T(0.5) * t * (d2 * a1 * a1 - a1);
+            sgz[ml * QM + q] += a2 * (dr + V) - (V - dr) * il2 + t * dq * a1;
+            T v2 = (T(2) * sv * a2 * il) * r + (d2 * r - dV) * il2 * il +
+                   l * a2 * a2 * (d2 * r + dV) + t * (sv * a1 * il + l * d2 * a1 * a1);
+#pragma unroll
+            for (int off = 16; off >= 1; off >>= 1) {
+                v0 += __shfl_xor(v0, off);
+                v1 += __shfl_xor(v1, off);
+                v2 += __shfl_xor(v2, off);
+            }
+            if ((lane & 31) == 0) {
+                red[b][wv][q] = v0;
+                red[b][wv][QM + q] = v1;
+                sgl[wv][q] += v2;
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (n + 1 < r1) stage_row(n + 1, b ^ 1);
+        __syncthreads();
+        if (tid < 2 * Q) {
+            const int part = tid < Q ? 0 : 1, q = tid < Q ? tid : tid - Q;
+            T v = 0;
+            for (int w = 0; w < 4; ++w) v += red[b][w][part * QM + q];
+            rowg[(((int64_t)blockIdx.x * 2 + part) * N + n) * Q + q] = v;
+        }
+    }
+    if (valid) {
+#pragma unroll
+        for (int j = 0; j < QH; ++j)
+            if (q0 + j < Q)
+                colpart[((int64_t)blockIdx.y * M + m) * Q + q0 + j] = sgz[ml * QM + q0 + j];
+    }
+    // block sums of dl and dsf2 (fixed order) -> rowpart[block][Q + 1]
+    if ((lane & 31) == 0)
+        for (int j = 0; j < QH; ++j) redf[wv][q0 + j] = sgl[wv][q0 + j];
+    {
+        T v = gsf;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+        if (lane == 0) redf[wv][QM] = v;
+    }
+    __syncthreads();
+    const int64_t blk = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+    if (tid <= Q) {
+        const int k = tid < Q ? tid : QM;
+        T v = 0;
+        for (int w = 0; w < 4; ++w) v += redf[w][k];
+        rowpart[blk * (Q + 1) + tid] = tid < Q ? v : v / h.sf2;
+    }
+}
+
 template <typename T, int QM>
 void launch_psi2_partial(const Shape &s, const Plan &p, const T *mu, const T *Z, const T *w2,
                          const T *lp2, const Hyp<T> &h, T *partial, const int *gate,
@@ -1161,6 +1388,45 @@ hipError_t generic_psi_grads(const Shape &s, const T *mu, const T *S, const T *Z
             s.N * s.Q, (int)p.pmb, rowg, dmu, dS);
         grad_reduce_kernel<T><<<(unsigned)std::min<int64_t>(total, kGridCap), 256, 0, st>>>(gate, 
             s.N, (int)s.M, (int)s.Q, p.pchunks, p.pmb * p.pchunks, colpart, rowpart, dL_dpsi0, dZ,
+            dsf2, dl, accumulate);
+        return hipGetLastError();
+    }
+    if (p.wide) {
+        const size_t lds = sizeof(T) * (s.M + 128) * 2 * p.wqh;
+        dim3 grid((unsigned)p.wmb, (unsigned)p.wchunks);
+        {
+            TimedScope ts(st, "generic_grad_wide");
+#define GPPS_WIDE(QHV)                                                                             \
+    case QHV:                                                                                      \
+        grad_wide_kernel<T, QHV><<<grid, 256, lds, st>>>(gate, s.N, (int)s.M, (int)s.Q, p.wrows,  \
+                                                          mu, S, Z, w1, w2, lp1, lp2, h, G1, G2s,  \
+                                                          rowg, colpart, rowpart);                 \
+        break
+            switch (p.wqh) {
+                GPPS_WIDE(4);
+                GPPS_WIDE(6);
+                GPPS_WIDE(8);
+                GPPS_WIDE(10);
+                GPPS_WIDE(12);
+                GPPS_WIDE(16);
+                default:
+                    if constexpr (sizeof(T) == 4) {
+                        switch (p.wqh) {
+                            GPPS_WIDE(24);
+                            GPPS_WIDE(32);
+                            default: break;
+                        }
+                    }
+                    break;
+            }
+#undef GPPS_WIDE
+        }
+        const int64_t total = s.M * s.Q + s.Q + 1;
+        TimedScope ts(st, "generic_grad_reduce");
+        grad_rows_reduce_kernel<T><<<(unsigned)std::min<int64_t>(cdiv(s.N * s.Q, 256), kGridCap), 256, 0, st>>>(gate,
+            s.N * s.Q, (int)p.wmb, rowg, dmu, dS);
+        grad_reduce_kernel<T><<<(unsigned)std::min<int64_t>(total, kGridCap), 256, 0, st>>>(gate,
+            s.N, (int)s.M, (int)s.Q, p.wchunks, p.wmb * p.wchunks, colpart, rowpart, dL_dpsi0, dZ,
             dsf2, dl, accumulate);
         return hipGetLastError();
     }

@@ -50,6 +50,18 @@ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Register width (latent dimensions, padded) of the pairs kernel for Q.
 inline int64_t pairs_qm(int64_t Q) { return Q <= 1 ? 1 : Q <= 2 ? 2 : Q <= 4 ? 4 : Q <= 8 ? 8 : 16; }
+// Register width (dimensions, padded) of the forward pair kernel for Q, and its
+// pairs per thread (two where a dimension's LDS read would otherwise serve one
+// pair's three operations; one at small widths and for wide fp64 rows).
+inline int fwd_qm(int64_t Q) {
+    for (int qm : {1, 2, 4, 8, 12, 16, 20, 24, 32, 48})
+        if (Q <= qm) return qm;
+    return 64;
+}
+inline int fwd_ppt(int64_t Q, size_t elem) {
+    const int qm = fwd_qm(Q);
+    return qm >= 8 && !(elem == 8 && qm >= 48) ? 2 : 1;
+}
 // Dimensions per lane of the wide gradient kernel for Q (0: none fits; fp64
 // keeps seven arrays of QH doubles live, fp32 the same in floats).
 inline int wide_qh(int64_t Q, size_t elem) {
@@ -85,7 +97,7 @@ struct Plan {
 Plan make_plan(const Shape &s, size_t elem) {
     Plan p{};
     p.tiles_edge = cdiv(s.M, kPairTile);
-    p.pblocks = cdiv(s.P, 256);
+    p.pblocks = cdiv(s.P, 256 * fwd_ppt(s.Q, elem));
     int64_t nc2 = cdiv(s.N, 256);
     int64_t cap2 = std::max<int64_t>(1, 2048 / p.pblocks);
     p.nc2 = std::max<int64_t>(1, std::min(nc2, cap2));
@@ -222,36 +234,56 @@ __device__ inline void pair_coords(int64_t t, int64_t M, int &m, int &mp) {
 }
 
 // ---------------------------------------------------------------- Psi2 partials (Alg. 1, Phi)
-// One thread per unique pair (consecutive pairs of the row-major upper
-// triangle, so no lane idles below the diagonal) and row chunk.
-template <typename T, int QM>
-__global__ __launch_bounds__(256) void psi2_partial_kernel(const int *__restrict__ gate, 
+// One thread per PPT unique pairs (pairs t = block base + k 256 + thread,
+// k < PPT: consecutive pairs of the row-major upper triangle, so no lane idles
+// below the diagonal) and row chunk.  The rows' (mu, w2) are staged in LDS as
+// pairs, one read per (row, dimension) serving the thread's PPT pairs.
+template <typename T>
+struct Two;
+template <>
+struct Two<float> {
+    typedef float2 t;
+};
+template <>
+struct Two<double> {
+    typedef double2 t;
+};
+
+template <typename T, int QM, int PPT>
+__global__ __launch_bounds__(256) void psi2_partial_kernel(const int *__restrict__ gate,
     int64_t N, int M, int Q, int64_t P, int64_t rows_per_chunk,
     const T *__restrict__ mu, const T *__restrict__ Z, const T *__restrict__ w2,
     const T *__restrict__ lp2, Hyp<T> h, T *__restrict__ partial) {
     if (gate && gate[0] == 0) return;
-    __shared__ T s_mu[kFwdTile][QM];
-    __shared__ T s_w2[kFwdTile][QM];
+    using T2 = typename Two<T>::t;
+    __shared__ T2 s_mw[kFwdTile][QM];
     __shared__ T s_lp[kFwdTile];
-    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const bool valid = t < P;
-    int m = 0, mp = 0;
-    if (valid) pair_coords(t, M, m, mp);
+    const int64_t t0 = (int64_t)blockIdx.x * 256 * PPT + threadIdx.x;
     // loads from clamped (valid) addresses, masked by a multiplication: a select
     // around each load would let the compiler wait for the loads one at a time
-    T zbar[QM];
-    T C = 0;
+    T zbar[PPT][QM], C[PPT];
+    bool valid[PPT];
 #pragma unroll
-    for (int q = 0; q < QM; ++q) {
-        const int qc = min(q, Q - 1);
-        const T a = Z[(int64_t)m * Q + qc], b = Z[(int64_t)mp * Q + qc];
-        const T on = q < Q ? T(1) : T(0);
-        zbar[q] = on * (T(0.5) * (a + b));
-        C -= on * ((a - b) * (a - b) / (T(4) * h.l2[qc]));
+    for (int k = 0; k < PPT; ++k) {
+        const int64_t t = t0 + k * 256;
+        valid[k] = t < P;
+        int m = 0, mp = 0;
+        if (valid[k]) pair_coords(t, M, m, mp);
+        C[k] = 0;
+#pragma unroll
+        for (int q = 0; q < QM; ++q) {
+            const int qc = min(q, Q - 1);
+            const T a = Z[(int64_t)m * Q + qc], b = Z[(int64_t)mp * Q + qc];
+            const T on = q < Q ? T(1) : T(0);
+            zbar[k][q] = on * (T(0.5) * (a + b));
+            C[k] -= on * ((a - b) * (a - b) / (T(4) * h.l2[qc]));
+        }
     }
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
-    T acc = 0;
+    T acc[PPT];
+#pragma unroll
+    for (int k = 0; k < PPT; ++k) acc[k] = 0;
     for (int64_t base = r0; base < r1; base += kFwdTile) {
         const int cnt = (int)min<int64_t>(kFwdTile, r1 - base);
         __syncthreads();
@@ -271,31 +303,43 @@ __global__ __launch_bounds__(256) void psi2_partial_kernel(const int *__restrict
                 const int i = i0 + u * (int)blockDim.x;
                 const int r = i / QM, q = i - r * QM;
                 if (i < cnt * QM) {
-                    s_mu[r][q] = q < Q ? a[u] : T(0);
-                    s_w2[r][q] = q < Q ? b[u] : T(0);
+                    T2 v;
+                    v.x = q < Q ? a[u] : T(0);
+                    v.y = q < Q ? b[u] : T(0);
+                    s_mw[r][q] = v;
                 }
             }
         }
         for (int r = threadIdx.x; r < cnt; r += blockDim.x) s_lp[r] = lp2[base + r];
         __syncthreads();
-        if (valid) {
-            // two-level sum: the tile's rows first, then into the chunk total, so
-            // that rounding grows with tile + tiles per chunk, not rows per chunk
-            T tacc = 0;
-#pragma unroll 4
-            for (int r = 0; r < cnt; ++r) {
-                T e = s_lp[r] + C;
+        // two-level sum: the tile's rows first, then into the chunk total, so
+        // that rounding grows with tile + tiles per chunk, not rows per chunk
+        T tacc[PPT];
 #pragma unroll
-                for (int q = 0; q < QM; ++q) {
-                    const T d = s_mu[r][q] - zbar[q];
-                    e -= d * d * s_w2[r][q];
+        for (int k = 0; k < PPT; ++k) tacc[k] = 0;
+#pragma unroll 4
+        for (int r = 0; r < cnt; ++r) {
+            T e[PPT];
+#pragma unroll
+            for (int k = 0; k < PPT; ++k) e[k] = s_lp[r] + C[k];
+#pragma unroll
+            for (int q = 0; q < QM; ++q) {
+                const T2 v = s_mw[r][q];
+#pragma unroll
+                for (int k = 0; k < PPT; ++k) {
+                    const T d = v.x - zbar[k][q];
+                    e[k] -= d * d * v.y;
                 }
-                tacc += dexp(e);
             }
-            acc += tacc;
+#pragma unroll
+            for (int k = 0; k < PPT; ++k) tacc[k] += dexp(e[k]);
         }
+#pragma unroll
+        for (int k = 0; k < PPT; ++k) acc[k] += tacc[k];
     }
-    if (valid) partial[(int64_t)blockIdx.y * P + t] = acc;
+#pragma unroll
+    for (int k = 0; k < PPT; ++k)
+        if (valid[k]) partial[(int64_t)blockIdx.y * P + t0 + k * 256] = acc[k];
 }
 
 // Fixed-order sum of the chunk partials; writes both triangles and psi0.
@@ -1263,8 +1307,12 @@ void launch_psi2_partial(const Shape &s, const Plan &p, const T *mu, const T *Z,
                          hipStream_t st) {
     dim3 grid((unsigned)p.pblocks, (unsigned)p.nc2);
     TimedScope ts(st, "generic_psi2_partial");
-    psi2_partial_kernel<T, QM><<<grid, 256, 0, st>>>(gate, s.N, (int)s.M, (int)s.Q, s.P, p.rows2, mu, Z,
-                                                     w2, lp2, h, partial);
+    if (fwd_ppt(s.Q, sizeof(T)) == 2)
+        psi2_partial_kernel<T, QM, 2><<<grid, 256, 0, st>>>(gate, s.N, (int)s.M, (int)s.Q, s.P,
+                                                            p.rows2, mu, Z, w2, lp2, h, partial);
+    else
+        psi2_partial_kernel<T, QM, 1><<<grid, 256, 0, st>>>(gate, s.N, (int)s.M, (int)s.Q, s.P,
+                                                            p.rows2, mu, Z, w2, lp2, h, partial);
 }
 
 template <typename T, int QM>
@@ -1312,13 +1360,14 @@ hipError_t generic_psi_stats(const Shape &s, const T *mu, const T *S, const T *Z
                                                                        mu, Z, w1, lp1, Psi1);
     }
     T *partial = at<T>(ws, p.off_p2);
-    if (s.Q <= 1) launch_psi2_partial<T, 1>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
-    else if (s.Q <= 2) launch_psi2_partial<T, 2>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
-    else if (s.Q <= 4) launch_psi2_partial<T, 4>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
-    else if (s.Q <= 8) launch_psi2_partial<T, 8>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
-    else if (s.Q <= 16) launch_psi2_partial<T, 16>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
-    else if (s.Q <= 32) launch_psi2_partial<T, 32>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
-    else launch_psi2_partial<T, 64>(s, p, mu, Z, w2, lp2, h, partial, gate, st);
+    switch (fwd_qm(s.Q)) {
+#define GPPS_FWD(QMV) \
+    case QMV: launch_psi2_partial<T, QMV>(s, p, mu, Z, w2, lp2, h, partial, gate, st); break
+        GPPS_FWD(1); GPPS_FWD(2); GPPS_FWD(4); GPPS_FWD(8); GPPS_FWD(12); GPPS_FWD(16);
+        GPPS_FWD(20); GPPS_FWD(24); GPPS_FWD(32); GPPS_FWD(48);
+        default: launch_psi2_partial<T, 64>(s, p, mu, Z, w2, lp2, h, partial, gate, st); break;
+#undef GPPS_FWD
+    }
     dim3 g((unsigned)p.tiles_edge, (unsigned)p.tiles_edge);
     TimedScope ts(st, "generic_psi2_reduce");
     psi2_reduce_kernel<T><<<g, kPairTile * kPairTile, 0, st>>>(gate, s.N, (int)s.M, s.P, p.nc2,

@@ -1109,7 +1109,9 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(const int *__restrict_
 // v = z_m' - z_m as the pairs kernel); the halves are exchanged across the lane
 // pair and added in the same order on both lanes, so both evaluate the same
 // W = G2s[m, m'] Psi2_n[m, m'] and update their own dimensions:
-//   r += W,   Vz_q += W z_m'q        (V = mu r - Vz in the epilogue).
+//   r += W,   Vd_q += W (z_m'q - z_mq)
+// (the local differences, not W z_m'q, so that no sum of the size of |z| r
+// cancels in the dZ and dl terms; V = d r - Vd).
 // Row values are read from clamped addresses and masked, so that their loads
 // issue together.  One workgroup per (block of 128 inducing inputs, row chunk).
 template <typename T, int QH>
@@ -1179,7 +1181,7 @@ __global__ __launch_bounds__(256) void grad_wide_kernel(const int *__restrict__ 
         const int b = (int)(n & 1);   // the row's buffer (its first row may be odd)
         const T *xs = srow[b][0] + q0, *a1s = srow[b][1] + q0, *a2s = srow[b][2] + q0,
                 *svs = srow[b][3] + q0;
-        T bq[QH], cq[QH], Vz[QH];
+        T bq[QH], cq[QH], Vd[QH];
         T r = 0, e0 = 0;
         {
             T part = 0;
@@ -1189,7 +1191,7 @@ __global__ __launch_bounds__(256) void grad_wide_kernel(const int *__restrict__ 
                 bq[j] = a2 * d;
                 cq[j] = sc4[q0 + j] + T(0.25) * a2;
                 part -= bq[j] * d;
-                Vz[j] = 0;
+                Vd[j] = 0;
             }
             e0 = (G2s ? lp2[n] : T(0)) + pair_sum(part);
         }
@@ -1209,19 +1211,16 @@ __global__ __launch_bounds__(256) void grad_wide_kernel(const int *__restrict__ 
                     const T g = gb[u];
                     if (mp + kAhead < M) gb[u] = g2[(int64_t)(mp + kAhead) * M];
                     const T *zr = sz + mp * QM + q0;
-                    T zp[QH];
+                    T v[QH];
 #pragma unroll
-                    for (int j = 0; j < QH; ++j) zp[j] = zr[j];
+                    for (int j = 0; j < QH; ++j) v[j] = zr[j] - z[j];
                     T ep = 0;
 #pragma unroll
-                    for (int j = 0; j < QH; ++j) {
-                        const T v = zp[j] - z[j];
-                        ep = fma(v, fma(-cq[j], v, bq[j]), ep);
-                    }
+                    for (int j = 0; j < QH; ++j) ep = fma(v[j], fma(-cq[j], v[j], bq[j]), ep);
                     const T W = g * dexp(e0 + pair_sum(ep));
                     r += W;
 #pragma unroll
-                    for (int j = 0; j < QH; ++j) Vz[j] = fma(W, zp[j], Vz[j]);
+                    for (int j = 0; j < QH; ++j) Vd[j] = fma(W, v[j], Vd[j]);
                 }
             }
         }
@@ -1245,15 +1244,16 @@ __global__ __launch_bounds__(256) void grad_wide_kernel(const int *__restrict__ 
         for (int j = 0; j < QH; ++j) {
             const int q = q0 + j;
             const T x = xs[j], a1 = a1s[j], a2 = a2s[j], sv = svs[j];
+            // with V = d r - Vd: d r + V = 2 d r - Vd, V - d r = -Vd,
+            // d^2 r + d V = d (d r + V), d^2 r - d V = d Vd
             const T dq = x - z[j], d2 = dq * dq, dr = dq * r;
-            const T V = x * r - Vz[j];
-            const T dV = dq * V;
+            const T s1 = T(2) * dr - Vd[j];
             const T il2 = sil2[q], l = sl[q], il = sinvl[q];
             T v0 = -T(2) * a2 * dr - t * dq * a1;
-            T v1 = a2 * a2 * (d2 * r + dV) - a2 * r + T(0.5) * t * (d2 * a1 * a1 - a1);
-            sgz[ml * QM + q] += a2 * (dr + V) - (V - dr) * il2 + t * dq * a1;
-            T v2 = (T(2) * sv * a2 * il) * r + (d2 * r - dV) * il2 * il +
-                   l * a2 * a2 * (d2 * r + dV) + t * (sv * a1 * il + l * d2 * a1 * a1);
+            T v1 = a2 * a2 * (dq * s1) - a2 * r + T(0.5) * t * (d2 * a1 * a1 - a1);
+            sgz[ml * QM + q] += a2 * s1 + Vd[j] * il2 + t * dq * a1;
+            T v2 = (T(2) * sv * a2 * il) * r + dq * Vd[j] * il2 * il + l * a2 * a2 * (dq * s1) +
+                   t * (sv * a1 * il + l * d2 * a1 * a1);
 #pragma unroll
             for (int off = 16; off >= 1; off >>= 1) {
                 v0 += __shfl_xor(v0, off);

@@ -108,7 +108,6 @@ constexpr float kZLimit = 3.0e4f;       // guard: largest centred |z| (unscaled 
 constexpr float kSpreadLimit = 64.f;    // guard: largest R_q / l_q (gradient conditioning)
 constexpr int kRB = 8;                 // gradient: rows per batch
 constexpr int kFRB = 4;                // forward: rows per batch (prefetched a batch ahead)
-constexpr int kFPF = kFRB * 512 / 256; // forward: per-thread prefetch slots of a [kFRB][Mp] table
 constexpr int kGPF = 4;                // gradient: per-thread load slots of a staged row table
 static_assert(kGPF * 64 >= kRB * 32, "kGPF slots cover the [kRB][32 wpg] row tables of any workgroup");
 static_assert(kFRB * kRowStride == kThreads, "one mu / kappa value per forward thread");
@@ -206,20 +205,20 @@ struct MPlan {
 //                       of the 32x32x16 f16 MFMA: wave, block, instruction, lane
 //                       group, row, 8 consecutive k (only the blocks the wave reads,
 //                       so that more workgroups fit per CU at large M)
-//   bb  [FRB][Mp]       row terms b of the batch (log2 units)
-//   bcb [FRB][Mp]       b + c
+//   rt  [FRB][waves][32 (1 + tpw)]   per wave, the batch's b + c of its column block
+//                       ti, then the row terms b of its tpw row blocks (log2 units):
+//                       only what the wave reads
 //   mub [FRB][64]       centred mu of the batch (zero beyond Q)
 //   kb  [FRB][64]       log2e kappa of the batch (zero beyond Q)
 struct LdsF {
-    int za, bb, bcb, mub, kb, total;
+    int za, rt, mub, kb, total;
 };
 
 __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int nk, int tpw) {
     LdsF L{};
     int o = 0;
     L.za = o; o += kWaves * tpw * nk * 2 * 32 * 8 / 2;
-    L.bb = o; o += kFRB * Mp;
-    L.bcb = o; o += kFRB * Mp;
+    L.rt = o; o += kFRB * kWaves * kTile * (1 + tpw);
     L.mub = o; o += kFRB * kRowStride;
     L.kb = o; o += kFRB * kRowStride;
     L.total = o;
@@ -922,8 +921,9 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
         const int m = ti * kTile + c;
 #pragma unroll
         for (int j = 0; j < GT; ++j) {
-            const int q = g * GT + j;
-            zr[j] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+            // clamped address, masked by a multiplication: the loads issue together
+            const int q = g * GT + j, qc = min(q, Q - 1);
+            zr[j] = (m < M && q < Q ? 1.f : 0.f) * (Z[(int64_t)min(m, M - 1) * Q + qc] - zc[qc]);
         }
     }
 
@@ -933,15 +933,24 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
     const int tid = threadIdx.x;
-    float pf_b[kFPF], pf_c[kFPF], pf_mu, pf_k;
+    // Each wave loads its own row-table slots (kFRB rows of RS entries: its column
+    // block of b + c, then its TPW row blocks of b), RPL entries per lane, from
+    // clamped addresses (rows >= cb are never read).
+    constexpr int RS = kTile * (1 + TPW), RPL = kFRB * RS / 64;
+    static_assert(kFRB * RS % 64 == 0, "whole row-table slots per lane");
+    float pf_t[RPL], pf_mu, pf_k;
     auto load = [&](int64_t n0) {
         const int cb = (int)min<int64_t>(kFRB, r1 - n0);
 #pragma unroll
-        for (int j = 0; j < kFPF; ++j) {
-            const int k = tid + j * kThreads;
-            const bool ok = k < cb * Mp;
-            pf_b[j] = ok ? bt[n0 * Mp + k] : kPadBias;
-            pf_c[j] = ok ? bc[n0 * Mp + k] : kPadBiasCol;
+        for (int j = 0; j < RPL; ++j) {
+            const int e = lane + 64 * j, r = e / RS, x = e - r * RS;
+            const int64_t row = (n0 + min(r, cb - 1)) * Mp;
+            if (x < kTile) {
+                pf_t[j] = bc[row + ti * kTile + x];
+            } else {
+                const int k = (x - kTile) / kTile;
+                pf_t[j] = bt[row + min(tj0 + k, nb - 1) * kTile + (x - kTile - k * kTile)];
+            }
         }
         const int r = tid / kRowStride, q = tid - r * kRowStride;
         const bool ok = r < cb && q < Q;
@@ -952,12 +961,11 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
     for (int64_t n0 = r0; n0 < r1; n0 += kFRB) {
         const int cb = (int)min<int64_t>(kFRB, r1 - n0);
         __syncthreads();
+        if (active) {
 #pragma unroll
-        for (int j = 0; j < kFPF; ++j) {
-            const int k = tid + j * kThreads;
-            if (k < kFRB * Mp) {
-                lds[L.bb + k] = pf_b[j];
-                lds[L.bcb + k] = pf_c[j];
+            for (int j = 0; j < RPL; ++j) {
+                const int e = lane + 64 * j, r = e / RS, x = e - r * RS;
+                lds[L.rt + (r * kWaves + wave) * RS + x] = pf_t[j];
             }
         }
         lds[L.mub + tid] = pf_mu;
@@ -967,9 +975,10 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
         if (!active) continue;
         for (int r = 0; r < cb; ++r) {
             v8h B[NK];
+            const float *rtw = lds + L.rt + (r * kWaves + wave) * RS;
             gram_operand<NK>(zr, lds + L.mub + r * kRowStride + g * GT, lds + L.kb + r * kRowStride + g * GT,
-                             lds[L.bcb + r * Mp + ti * kTile + c], g, B);
-            const float *bbr = lds + L.bb + r * Mp;
+                             rtw[c], g, B);
+            const float *bbr = rtw + kTile;   // the wave's row blocks tj0 + k at k * kTile
             if constexpr (TPW == 2) {
                 // both Gram products first: the matrix cores work on tile 1 while tile
                 // 0's exponentials run; the sums follow the exponentials in one run (no
@@ -977,7 +986,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
                 // the edge (the last task of a row block with an odd count) computes
                 // its one tile only (wave-uniform branch).
                 if (single) {
-                    const v16f e = gram16<NK>(row_terms(bbr, tj[0], g), zaw, c, g, B);
+                    const v16f e = gram16<NK>(row_terms(bbr, 0, g), zaw, c, g, B);
                     float x[16];
 #pragma unroll
                     for (int t = 0; t < 16; ++t) x[t] = __builtin_amdgcn_exp2f(e[t]);
@@ -987,7 +996,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
                     v16f e[TPW];
 #pragma unroll
                     for (int k = 0; k < TPW; ++k)
-                        e[k] = gram16<NK>(row_terms(bbr, tj[k], g), zaw + k * (NK * 2 * 32 * 8),
+                        e[k] = gram16<NK>(row_terms(bbr, k, g), zaw + k * (NK * 2 * 32 * 8),
                                           c, g, B);
 #pragma unroll
                     for (int k = 0; k < TPW; ++k) {
@@ -1001,7 +1010,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
             } else {
 #pragma unroll
                 for (int k = 0; k < TPW; ++k) {
-                    const v16f e = gram16<NK>(row_terms(bbr, tj[k], g), zaw + k * (NK * 2 * 32 * 8),
+                    const v16f e = gram16<NK>(row_terms(bbr, k, g), zaw + k * (NK * 2 * 32 * 8),
                                               c, g, B);
 #pragma unroll
                     for (int t = 0; t < 16; ++t) acc[k][t] += __builtin_amdgcn_exp2f(e[t]);

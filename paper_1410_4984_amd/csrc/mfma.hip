@@ -568,9 +568,13 @@ __device__ __forceinline__ float wave_max_lane63(float v) {
 // row stride Mp (zero where G1 is NULL or m >= M) and, per row and range of 256
 // inducing inputs (blockIdx.y), bmax[y][n] = max over the range's real m of
 // bt[n][m] (the gradient's scale of W: max_m E'_n[m, m] = 4 max_m bt - 2 hl_n).
-// One thread per inducing input (z in registers); rows staged in LDS as one
-// (mu, hq, w1, K mu) vector per dimension, so each dimension costs one broadcast
-// read and five vector instructions.
+// A wave takes whole rows of the range: lane l holds the four inducing inputs
+// m0 = y 256 + 4 l .. m0 + 3 (their z in registers up to 32 dimensions, read
+// from LDS per dimension above that), so each table row is one 16-byte
+// store per lane and the row maximum is a wave reduction; the workgroup's four
+// waves take the batch's rows wave, wave + 4, ...  Rows are staged in LDS as one
+// (mu, hq, w1, K mu) vector per dimension: one broadcast read serves four
+// inducing inputs, five vector instructions each.
 template <int QM, bool GRAD>
 __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     int64_t N, int M, int Q, int Mp, const float *__restrict__ mu, const float *__restrict__ Z,
@@ -579,12 +583,16 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     const int *__restrict__ route, float *__restrict__ bt, float *__restrict__ bc,
     float *__restrict__ psi1, float *__restrict__ t1, float *__restrict__ bmax) {
     typedef float v4f __attribute__((ext_vector_type(4)));
-    constexpr int GR = GRAD ? 8 : 1;   // rows per group: their dL/dPsi1 loads are in flight together
+    // z of the range's 256 inducing inputs, dimension-major, centred and zero
+    // outside the real (m, q): lane l reads its four with one 16-byte load
+    constexpr bool kZReg = QM <= 32;   // z held in registers (4 QM of them)
     __shared__ v4f s_row[kRTRows][QM];
+    __shared__ v4f s_zt[QM][64];
     __shared__ float s_hl[kRTRows], s_l1[kRTRows];
-    __shared__ float s_bm[GRAD ? kRTRows * 4 : 1];   // per-wave maxima of b: [row][wave]
     if (route[0]) return;
-    const int m = blockIdx.y * 256 + threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int m0 = blockIdx.y * 256 + 4 * lane;
     const int64_t n0 = (int64_t)blockIdx.x * kRTRows;
     const int cnt = (int)min<int64_t>(kRTRows, N - n0);
     // The loads below read clamped (always valid) addresses and are masked by
@@ -610,68 +618,115 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
         s_hl[r] = r < cnt ? hv : 0.f;
         s_l1[r] = r < cnt ? lv : 0.f;
     }
-    // every lane runs the row loop (the wave reductions below read all 64 lanes);
-    // lanes past Mp store nothing
-    const bool inb = m < Mp, real = m < M;
-    const int mc = min(m, M - 1);
-    const float realf = real ? 1.f : 0.f;
-    float z[QM];
-#pragma unroll
-    for (int q = 0; q < QM; ++q) {
-        const int qc = min(q, Q - 1);
-        z[q] = (q < Q ? realf : 0.f) * (Z[(int64_t)mc * Q + qc] - zc[qc]);
+    {
+        // thread t stages inducing input y 256 + t (consecutive threads write
+        // consecutive words of a dimension's row)
+        const int m = blockIdx.y * 256 + threadIdx.x;
+        const int mc = min(m, M - 1);
+        const float okm = m < M ? 1.f : 0.f;
+        float *zt = reinterpret_cast<float *>(&s_zt[0][0]);
+#pragma unroll 8
+        for (int q = 0; q < QM; ++q) {
+            const int qc = min(q, Q - 1);
+            zt[q * 256 + threadIdx.x] = (q < Q ? okm : 0.f) * (Z[(int64_t)mc * Q + qc] - zc[qc]);
+        }
     }
-    // (dL/dPsi1 of padded columns: the product of column M - 1's value and 0)
-    float g1c[GR], g1n[GR];
-    auto load_g1 = [&](int r0, float (&g)[GR]) {
+    // every lane runs the row loop (the wave reductions below read all 64 lanes);
+    // lanes past Mp store nothing (Mp is a multiple of 32: the lane's four m are
+    // all below it or all past it)
+    const bool inb = m0 < Mp;
+    const bool p1vec = (M & 3) == 0 && (reinterpret_cast<uintptr_t>(psi1) & 15) == 0;
+    float realf[4];
 #pragma unroll
-        for (int u = 0; u < GR; ++u) g[u] = realf * G1[(n0 + min(r0 + u, cnt - 1)) * M + mc];
+    for (int u = 0; u < 4; ++u) realf[u] = m0 + u < M ? 1.f : 0.f;
+    // dL/dPsi1 of the wave's rows, loaded one row ahead of its use (padded
+    // columns: the product of column M - 1's value and 0)
+    float g1c[4] = {0.f, 0.f, 0.f, 0.f};
+    auto load_g1 = [&](int r, float *g) {
+        const int64_t row = (n0 + min(r, cnt - 1)) * M;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) g[u] = realf[u] * G1[row + min(m0 + u, M - 1)];
     };
     if constexpr (GRAD)
-        if (G1) load_g1(0, g1c);
+        if (G1) load_g1(wave, g1c);
     __syncthreads();
-    for (int r0 = 0; r0 < cnt; r0 += GR) {
+    v4f z[kZReg ? QM : 1];
+    if constexpr (kZReg) {
+#pragma unroll
+        for (int q = 0; q < QM; ++q) z[q] = s_zt[q][lane];
+    }
+#pragma unroll 1
+    for (int r = wave; r < cnt; r += 4) {
+        float g1n[4] = {0.f, 0.f, 0.f, 0.f};
         if constexpr (GRAD)
-            if (G1 && r0 + GR < cnt) load_g1(r0 + GR, g1n);
+            if (G1) load_g1(r + 4, g1n);
+        float b[4], cc[4], e[4];
 #pragma unroll
-        for (int u = 0; u < GR; ++u) {
-            const int r = r0 + u;
-            if (r >= cnt) break;
-            float b = s_hl[r], cc = 0.f, e = 0.f;
+        for (int u = 0; u < 4; ++u) {
+            b[u] = s_hl[r];
+            cc[u] = e[u] = 0.f;
+        }
 #pragma unroll
-            for (int q = 0; q < QM; ++q) {
-                const v4f v = s_row[r][q];
-                const float d = v.x - z[q];
+        for (int q = 0; q < QM; ++q) {
+            const v4f v = s_row[r][q];
+            v4f zq;
+            if constexpr (kZReg)
+                zq = z[q];
+            else
+                zq = s_zt[q][lane];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const float d = v.x - zq[u];
                 const float d2 = d * d;
-                b = fmaf(v.y, d2, b);
-                e = fmaf(v.z, d2, e);
-                cc = fmaf(v.w, d, cc);
+                b[u] = fmaf(v.y, d2, b[u]);
+                e[u] = fmaf(v.z, d2, e[u]);
+                cc[u] = fmaf(v.w, d, cc[u]);
             }
-            const int64_t n = n0 + r;
-            if (inb) {
-                bt[n * Mp + m] = real ? b : kPadBias;
-                bc[n * Mp + m] = real ? b + cc : kPadBiasCol;
-            }
-            const float p1 = __builtin_amdgcn_exp2f(fmaf(-0.5f * kLog2e, e, s_l1[r]));
-            if constexpr (GRAD) {
-                if (inb) t1[n * Mp + m] = G1 ? g1c[u] * p1 : 0.f;
-                const float w = wave_max_lane63(real ? b : -INFINITY);
-                if ((threadIdx.x & 63) == 63) s_bm[r * 4 + (threadIdx.x >> 6)] = w;
-            } else if (psi1 && real) {
-                psi1[n * M + m] = p1;
-            }
+        }
+        // the sums are complete here: without this the compiler sinks the e
+        // and cc chains into the store branch below and keeps every d and d^2
+        // of the row live until then
+#pragma unroll
+        for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(b[u]), "+v"(e[u]), "+v"(cc[u]));
+        const int64_t n = n0 + r;
+        v4f vb, vc, p1;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const bool real = realf[u] != 0.f;
+            vb[u] = real ? b[u] : kPadBias;
+            vc[u] = real ? b[u] + cc[u] : kPadBiasCol;
+            p1[u] = __builtin_amdgcn_exp2f(fmaf(-0.5f * kLog2e, e[u], s_l1[r]));
+        }
+        if (inb) {
+            *reinterpret_cast<v4f *>(bt + n * Mp + m0) = vb;
+            *reinterpret_cast<v4f *>(bc + n * Mp + m0) = vc;
         }
         if constexpr (GRAD) {
+            if (inb) {
+                v4f tv;
 #pragma unroll
-            for (int u = 0; u < GR; ++u) g1c[u] = g1n[u];
+                for (int u = 0; u < 4; ++u) tv[u] = g1c[u] * p1[u];
+                *reinterpret_cast<v4f *>(t1 + n * Mp + m0) = tv;
+            }
+            float w = -INFINITY;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) w = fmaxf(w, realf[u] != 0.f ? b[u] : -INFINITY);
+            w = wave_max_lane63(w);
+            if (lane == 63) bmax[(int64_t)blockIdx.y * N + n] = w;
+        } else if (psi1) {
+            // Psi1 has row stride M: one 16-byte store where M is a multiple
+            // of 4 and the array 16-byte aligned (then the lane's four m are
+            // all real or all padding), else one store per real m
+            if (p1vec) {
+                if (m0 < M) *reinterpret_cast<v4f *>(psi1 + n * M + m0) = p1;
+            } else {
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (m0 + u < M) psi1[n * M + m0 + u] = p1[u];
+            }
         }
-    }
-    if constexpr (!GRAD) return;
-    __syncthreads();
-    if ((int)threadIdx.x < cnt) {
-        float v = -INFINITY;
-        for (int w = 0; w < 4; ++w) v = fmaxf(v, s_bm[threadIdx.x * 4 + w]);
-        bmax[(int64_t)blockIdx.y * N + n0 + threadIdx.x] = v;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) g1c[u] = g1n[u];
     }
 }
 

@@ -188,6 +188,7 @@ struct MPlan {
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
     int64_t frows, fchunks;
+    bool gsym;             // gradient: symmetric kernel (one workgroup covers every pair)
     int jpw, njr;          // gradient: column blocks per wave task, column-block ranges
     int wpg, igroups;      // gradient: waves per workgroup (one row block each), row-block groups
     int64_t ggroups;       // gradient: workgroups per row chunk (njr * igroups)
@@ -265,6 +266,42 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
     return L;
 }
 
+// Symmetric gradient LDS layout (floats), one workgroup of nb waves:
+//   zx  [nb 32][DSF]   centred z (fp32) of every block (as zx above)
+//   zh  [nb][2][2][2][32][8] f16   [Z | 1] of every block as V-product B operands
+//   za  [nb][nk][2][32][8] f16     [centred z | 1] of every block as Gram A operands
+//   xw  [nb][2][32][kXS] f16       per wave, its exchanged W tile as two fp16 parts:
+//                       row m of the writer's block, the 32 m' of the reader's block
+//                       contiguous (kXS > 32 spreads the rows over the LDS banks)
+//   bb, bcb, t1 [RB][Mp]   b, b + c and dL/dPsi1 * Psi1 of the batch, every column
+//   mub, kb, w1b, w2b [RB][64] (zero past Q), sc [RB] (padded to 4), red [RB][nb][5Q + 2]
+constexpr int kSymRB = 2;   // symmetric gradient: rows per batch
+constexpr int kXS = 36;     // halves per row of an exchanged tile
+struct LdsS {
+    int zx, zb, za, xw, bb, bcb, t1, mub, kb, w1b, w2b, sc, red, total;
+};
+
+__host__ __device__ inline LdsS lds_sym_layout(int nb, int DSF, int Q, int nk) {
+    LdsS L{};
+    int o = 0;
+    const int Mp = nb * kTile;
+    L.zx = o; o += (nb * kTile * DSF + 3) / 4 * 4;
+    L.zb = o; o += nb * 2 * 2 * 2 * 32 * 8 / 2;
+    L.za = o; o += nb * nk * 2 * 32 * 8 / 2;
+    L.xw = o; o += nb * 2 * 32 * kXS / 2;
+    L.bb = o; o += kSymRB * Mp;
+    L.bcb = o; o += kSymRB * Mp;
+    L.t1 = o; o += kSymRB * Mp;
+    L.mub = o; o += kSymRB * kRowStride;
+    L.kb = o; o += kSymRB * kRowStride;
+    L.w1b = o; o += kSymRB * kRowStride;
+    L.w2b = o; o += kSymRB * kRowStride;
+    L.sc = o; o += 4;
+    L.red = o; o += kSymRB * nb * (5 * Q + 2);
+    L.total = o;
+    return L;
+}
+
 MPlan make_mplan(const Shape &s) {
     MPlan p{};
     p.Mp = cdiv(s.M, kTile) * kTile;
@@ -293,22 +330,36 @@ MPlan make_mplan(const Shape &s) {
     p.fchunks = std::max<int64_t>(1, std::min(fslots / p.fgroups, cdiv(s.N, 32)));
     p.frows = cdiv(s.N, p.fchunks);
     p.fchunks = cdiv(s.N, p.frows);
-    p.jpw = grad_jpw(p.nqb);
-    p.njr = (int)cdiv(p.nb, p.jpw);
-    // widest workgroup whose LDS fits
-    p.wpg = std::min(p.nb, grad_waves(p.nqb));
-    while (p.wpg > 1 && sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk,
-                                                        p.wpg).total > 160 * 1024)
-        p.wpg /= 2;
+    // symmetric gradient kernel (one workgroup of nb waves per row chunk) where
+    // [Z | 1] is one column block, Mp <= 256 and its tables fit in LDS
+    p.gsym = p.nqb == 1 && p.nb <= 8 && p.nk > 0 &&
+             sizeof(float) * lds_sym_layout(p.nb, p.DSF, (int)s.Q, std::max(p.nk, 1)).total <=
+                 (size_t)kLdsBytes;
+    if (p.gsym) {
+        p.jpw = p.nb;
+        p.njr = 1;
+        p.wpg = p.nb;
+    } else {
+        p.jpw = grad_jpw(p.nqb);
+        p.njr = (int)cdiv(p.nb, p.jpw);
+        // widest workgroup whose LDS fits
+        p.wpg = std::min(p.nb, grad_waves(p.nqb));
+        while (p.wpg > 1 && sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb,
+                                                            p.nk, p.wpg).total > 160 * 1024)
+            p.wpg /= 2;
+    }
     p.igroups = (int)cdiv(p.nb, p.wpg);
     p.ggroups = (int64_t)p.njr * p.igroups;
-    p.lds_grad =
-        sizeof(float) * lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk, p.wpg).total;
+    p.lds_grad = sizeof(float) *
+                 (p.gsym ? lds_sym_layout(p.nb, p.DSF, (int)s.Q, std::max(p.nk, 1)).total
+                         : lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk, p.wpg).total);
     // two full rounds: workgroups per CU limited by LDS and by the waves per CU
-    // the kernel's register count allows (grad_waves: two or one per SIMD)
+    // the kernel's register count allows (two per SIMD; one per SIMD for the
+    // wide [Z | 1] of psi2_grad_kernel)
+    const int64_t gwaves = p.gsym ? 8 : grad_waves(p.nqb);
     const int64_t gslots = kCUs * std::max<int64_t>(
                                       1, std::min<int64_t>(kLdsBytes / p.lds_grad,
-                                                           grad_waves(p.nqb) / p.wpg));
+                                                           gwaves / p.wpg));
     p.gchunks = std::max<int64_t>(1, std::min(2 * gslots / p.ggroups, cdiv(s.N, 16)));
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
@@ -1125,15 +1176,14 @@ __global__ __launch_bounds__(256) void psi2_reduce_kernel(int64_t N, int M, int 
 }
 
 // ---------------------------------------------------------------- Psi2 gradient
-// The workgroup's JPW column blocks of [Z | 1] as two fp16 parts (rounded to
+// Column blocks blk0 .. blk0 + nblk - 1 of [Z | 1] as two fp16 parts (rounded to
 // nearest), in the B operand order of the 32x32x16 f16 MFMA: for instruction h
 // and lane group g the 8 k-values are the rows crow(8h + e, g), e = 0..7, of the
 // block.
-template <int JPW>
-__device__ void stage_zh(_Float16 *zh, int jr, int M, int Q, int nqb,
+__device__ void stage_zh(_Float16 *zh, int blk0, int nblk, int M, int Q, int nqb,
                          const float *__restrict__ Z, const float *__restrict__ zc) {
     const int QV = 32 * nqb;
-    const int total = JPW * 2 * 2 * 2 * QV * 8;
+    const int total = nblk * 2 * 2 * 2 * QV * 8;
     for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
         int r = idx;
         const int e = r % 8; r /= 8;
@@ -1142,7 +1192,7 @@ __device__ void stage_zh(_Float16 *zh, int jr, int M, int Q, int nqb,
         const int h = r % 2; r /= 2;
         const int part = r % 2; r /= 2;
         const int k = r;
-        const int m = (jr * JPW + k) * kTile + crow(8 * h + e, gg);
+        const int m = (blk0 + k) * kTile + crow(8 * h + e, gg);
         float v = 0.f;
         if (m < M) {
             if (q < Q) v = Z[(int64_t)m * Q + q] - zc[q];
@@ -1226,7 +1276,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
         const int m = ib0 * kTile + lr;
         lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
     }
-    stage_zh<JPW>(zh, jr, M, Q, NQB, Z, zc);
+    stage_zh(zh, jr * JPW, JPW, M, Q, NQB, Z, zc);
     // |W_n| = |G2c| 2^E'_n is bounded by max|G2c| 2^(2 hl_n) (E' <= 2 hl_n, hl_n: log2
     // of the half prefactor), and, Psi2_n being positive semidefinite (|Psi2_n[m, m']|
     // <= max_m Psi2_n[m, m]), by max|G2s| 2^(4 bmax_n - 2 hl_n); the per-row scale 2^sc
@@ -1473,6 +1523,295 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     }
 }
 
+// ---------------------------------------------------------------- Psi2 gradient, symmetric
+// W_n = G2s o Psi2_n is symmetric, so one exponential per unordered pair serves
+// both of its V sums when one workgroup covers every block pair of its rows
+// (Alg. 1 takes each pair once): nb waves, wave w owning block w of the m index
+// (its V sums, epilogue and dZ share).  Per row, wave w computes the tiles
+// (rows m' in block j, columns m in block w) for j = w (diagonal), j = w + k
+// (mod nb) for k = 1 .. kx = (nb - 1) / 2, and, nb even, j = w + nb / 2, which
+// both partners compute, so that every wave has the same work.  A tile feeds the
+// wave's own V sum as now (W in the MFMA output layout is the A operand of
+// V' += W [Z_j | 1]); each tile of the rounds k = 1 .. kx also feeds block j's
+// sum: the wave writes its two fp16 parts to LDS with m' contiguous, and wave j
+// reads them back transposed (ds_read_b64_tr_b16: within each 16 lanes, element
+// e of lane i comes from sub-element i % 4 of the 8 bytes lane 4 e + i / 4
+// addressed), which gives the A operand of V'_j += W^T [Z_w | 1] with no VALU
+// work.  At nb = 8 a row takes 40 tiles instead of 64 and 8 epilogues instead
+// of 16, for 24 tile exchanges and two barriers per round.
+template <int NK>
+__global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
+    int64_t N, int M, int Q, int Mp, int nb, int DSF, int64_t rows_per_chunk,
+    const float *__restrict__ mu, const float *__restrict__ Z, const float *__restrict__ zc,
+    const float *__restrict__ Kt, const float *__restrict__ bt, const float *__restrict__ bc,
+    const float *__restrict__ w1t, const float *__restrict__ w2t, const float *__restrict__ t1g,
+    const float *__restrict__ G2p, const float *__restrict__ hl, const float *__restrict__ gmax,
+    const float *__restrict__ bmax, Hyp<float> h, const int *__restrict__ route,
+    float *__restrict__ rowsum, float *__restrict__ part_dz) {
+    typedef short v4s __attribute__((vector_size(8)));
+    typedef __attribute__((address_space(3))) v4s lds_v4s;
+    extern __shared__ float lds[];
+    if (route[0]) return;
+    const LdsS L = lds_sym_layout(nb, DSF, Q, NK);
+    constexpr int GT = gram_t(NK);
+    constexpr int KT = 5;                      // tile slots: 0 diagonal, 1 .. 3 rounds, 4 shared
+    _Float16 *zh = reinterpret_cast<_Float16 *>(lds + L.zb);
+    _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
+    _Float16 *xw = reinterpret_cast<_Float16 *>(lds + L.xw);
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int c = lane & 31, g = lane >> 5;
+    const int ones_src = 32 * g + Q;           // lane holding column Q of V (the row sums r)
+    const int RED = 5 * Q + 2;                 // X, Y, P, X1, P1 per dimension, then R, T1
+    const int kx = (nb - 1) / 2;               // exchange rounds
+    const bool shared_tile = nb > 1 && (nb & 1) == 0;
+
+    // dL/dPsi2 tiles of the wave's slots, rows m' in block j, columns m in block w
+    // (clamped loads, masked: unused slots hold zeros)
+    float g2r[KT][16];
+#pragma unroll
+    for (int s = 0; s < KT; ++s) {
+        const bool ok = s == 0 || (s < KT - 1 ? s <= kx : shared_tile);
+        const int k = s < KT - 1 ? s : nb / 2;
+        const int j = (w + (ok ? k : 0)) % nb;
+        const float okf = ok ? 1.f : 0.f;
+        const float *g2 = G2p + (int64_t)j * kTile * Mp + w * kTile + c;
+#pragma unroll
+        for (int t = 0; t < 16; ++t) g2r[s][t] = okf * g2[(int64_t)crow(t, g) * Mp];
+    }
+    v16f dz;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) dz[t] = 0.f;
+    const float il2 = c < Q ? 1.f / h.l2[c] : 0.f;
+
+    // constant tables: centred z (fp32), [Z | 1] (V-product B operands) and
+    // [centred z | 1] (Gram A operands) of every block
+    for (int k = threadIdx.x; k < nb * kTile * DSF; k += blockDim.x) {
+        const int m = k / DSF, q = k - m * DSF;
+        lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+    }
+    stage_zh(zh, 0, nb, M, Q, 1, Z, zc);
+    stage_za<NK>(za, 0, nb, nb, M, Q, Z, zc, threadIdx.x, blockDim.x);
+    // per-row scale of W: as in psi2_grad_kernel
+    const float lgc = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
+    const float lgs = gmax[1] > 0.f ? __builtin_amdgcn_logf(gmax[1]) : 0.f;
+
+    // the exchange: this wave's slot (written) and the transpose read's lane
+    // offsets (rows 4 g + (lane / 4) % 4 of each run of 8, columns 16 ((lane / 16)
+    // % 2) + 4 (lane % 4) of the writer's tile)
+    _Float16 *xo = xw + w * (2 * 32 * kXS);
+    const int xr_row = 4 * g + ((lane >> 2) & 3);
+    const int xr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+    const int BT = kSymRB * Mp;                // row-table entries of a batch
+    const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
+    const int64_t r1 = min(N, r0 + rows_per_chunk);
+    const int tid = threadIdx.x, nthr = blockDim.x;
+    for (int64_t n0 = r0; n0 < r1; n0 += kSymRB) {
+        const int cb = (int)min<int64_t>(kSymRB, r1 - n0);
+        __syncthreads();
+        // batch tables (clamped loads, issued before the writes)
+        for (int k = tid; k < BT; k += nthr) {
+            const int rr = min(k / Mp, cb - 1);
+            const int64_t o = (n0 + rr) * Mp + (k - (k / Mp) * Mp);
+            const float vb = bt[o], vc = bc[o], vt = t1g[o];
+            lds[L.bb + k] = vb;
+            lds[L.bcb + k] = vc;
+            lds[L.t1 + k] = vt;
+        }
+        for (int k = tid; k < kSymRB * kRowStride; k += nthr) {
+            const int r = k / kRowStride, q = k - r * kRowStride;
+            const float ok = (r < cb && q < Q) ? 1.f : 0.f;
+            const int qc = min(q, Q - 1);
+            const int64_t rc = n0 + min(r, cb - 1);
+            const float vm = mu[rc * Q + qc] - zc[qc], vk = Kt[rc * kRowStride + qc],
+                        v1 = w1t[rc * Q + qc], v2 = w2t[rc * Q + qc];
+            lds[L.mub + k] = ok * vm;
+            lds[L.kb + k] = ok * vk;
+            lds[L.w1b + k] = ok * v1;
+            lds[L.w2b + k] = ok * v2;
+        }
+        if (tid < kSymRB) {
+            float sc = 0.f;
+            if (tid < cb) {
+                const float phl = hl[n0 + tid];
+                float pbm = -INFINITY;
+                for (int y = 0; y < (Mp + 255) / 256; ++y) pbm = fmaxf(pbm, bmax[(int64_t)y * N + n0 + tid]);
+                const float wb = fminf(2.f * phl + lgc, 4.f * pbm - 2.f * phl + lgs);
+                sc = fminf(120.f, fmaxf(-120.f, floorf(14.f - wb)));
+            }
+            lds[L.sc + tid] = sc;
+        }
+        __syncthreads();
+        for (int r = 0; r < cb; ++r) {
+            const float sc = lds[L.sc + r];
+            const float bcol = lds[L.bcb + r * Mp + w * kTile + c] + sc;
+            v8h GB[NK];
+            {
+                const float *zi = lds + L.zx + (w * kTile + c) * DSF + g * GT;
+                float zv[GT];
+#pragma unroll
+                for (int j = 0; j < GT; ++j) zv[j] = zi[j];
+                gram_operand<NK>(zv, lds + L.mub + r * kRowStride + g * GT,
+                                 lds + L.kb + r * kRowStride + g * GT, bcol, g, GB);
+            }
+            const float *bbr = lds + L.bb + r * Mp;
+            v16f V;
+#pragma unroll
+            for (int t = 0; t < 16; ++t) V[t] = 0.f;
+            // W tile of slot s (block j), scaled by 2^sc, as two fp16 parts packed
+            // in pairs of the rows crow(t, g), crow(t + 1, g)
+            auto tile = [&](int s, int j, unsigned (&wh)[2][4], unsigned (&wl)[2][4]) {
+                const v16f e = gram16<NK>(row_terms(bbr, j, g), za + j * (NK * 2 * 32 * 8), c, g, GB);
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int t = 8 * hh + 2 * u;
+                        const float x0 = __builtin_amdgcn_exp2f(e[t]);
+                        const float x1 = __builtin_amdgcn_exp2f(e[t + 1]);
+                        const v2h h2 = {(_Float16)(g2r[s][t] * x0), (_Float16)(g2r[s][t + 1] * x1)};
+                        wh[hh][u] = __builtin_bit_cast(unsigned, h2);
+                        wl[hh][u] = lo_pair(g2r[s][t], x0, g2r[s][t + 1], x1, wh[hh][u]);
+                    }
+            };
+            // V' += W [Z_j | 1], W's two parts as A operands (three cross products)
+            auto product = [&](int j, const unsigned (&wh)[2][4], const unsigned (&wl)[2][4]) {
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh) {
+                    const v8h Ah = __builtin_bit_cast(v8h, wh[hh]);
+                    const v8h Al = __builtin_bit_cast(v8h, wl[hh]);
+                    const v8h Bh = *reinterpret_cast<const v8h *>(
+                        zh + ((((j * 2 + 0) * 2 + hh) * 2 + g) * 32 + c) * 8);
+                    const v8h Bl = *reinterpret_cast<const v8h *>(
+                        zh + ((((j * 2 + 1) * 2 + hh) * 2 + g) * 32 + c) * 8);
+                    V = __builtin_amdgcn_mfma_f32_32x32x16_f16(Ah, Bh, V, 0, 0, 0);
+                    V = __builtin_amdgcn_mfma_f32_32x32x16_f16(Ah, Bl, V, 0, 0, 0);
+                    V = __builtin_amdgcn_mfma_f32_32x32x16_f16(Al, Bh, V, 0, 0, 0);
+                }
+            };
+            {
+                unsigned wh[2][4], wl[2][4];
+                tile(0, w, wh, wl);
+                product(w, wh, wl);
+            }
+            if (shared_tile) {
+                const int j = (w + nb / 2) % nb;
+                unsigned wh[2][4], wl[2][4];
+                tile(KT - 1, j, wh, wl);
+                product(j, wh, wl);
+            }
+#pragma unroll
+            for (int k = 1; k < KT - 1; ++k) {
+                if (k > kx) break;                       // uniform over the workgroup
+                const int j = (w + k) % nb, src = (w + nb - k) % nb;
+                unsigned wh[2][4], wl[2][4];
+                tile(k, j, wh, wl);
+                product(j, wh, wl);
+                __syncthreads();                         // the previous round's reads are done
+#pragma unroll
+                for (int T = 0; T < 4; ++T) {
+                    const int hh = T >> 1, u = 2 * (T & 1);
+                    const int o = c * kXS + 8 * T + 4 * g;
+                    *reinterpret_cast<uint2 *>(xo + o) = make_uint2(wh[hh][u], wh[hh][u + 1]);
+                    *reinterpret_cast<uint2 *>(xo + 32 * kXS + o) = make_uint2(wl[hh][u], wl[hh][u + 1]);
+                }
+                __syncthreads();                         // this round's tiles are written
+                const _Float16 *xs = xw + src * (2 * 32 * kXS);
+                unsigned rh[2][4], rl[2][4];
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2) {
+                        const int o = (16 * hh + 8 * h2 + xr_row) * kXS + xr_col;
+                        const v4s a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s *)(xs + o));
+                        const v4s b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_v4s *)(xs + 32 * kXS + o));
+                        const uint2 a2 = __builtin_bit_cast(uint2, a), b2 = __builtin_bit_cast(uint2, b);
+                        rh[hh][2 * h2] = a2.x;
+                        rh[hh][2 * h2 + 1] = a2.y;
+                        rl[hh][2 * h2] = b2.x;
+                        rl[hh][2 * h2 + 1] = b2.y;
+                    }
+                product(src, rh, rl);
+            }
+            // V' carries the row scale 2^sc: the epilogue's coefficients and row sums
+            // undo it (exact: a power of two)
+            const float us = __builtin_amdgcn_exp2f(-sc);
+            // epilogue for rows m = w*32 + crow(t, g); V' = W [Z | 1] -> V = r mu^T - V'
+            const float muq = lds[L.mub + r * kRowStride + c];
+            const float w2 = lds[L.w2b + r * kRowStride + c];
+            const float w1q = lds[L.w1b + r * kRowStride + c];
+            const float alpha = (w2 - il2) * us, beta = (w2 + il2) * us;
+            float X = 0.f, Y = 0.f, P = 0.f, X1 = 0.f, P1 = 0.f, R = 0.f, T1 = 0.f;
+            const float *zblk = lds + L.zx + w * kTile * DSF;
+            const float *t1r = lds + L.t1 + r * Mp + w * kTile;
+#pragma unroll
+            for (int t = 0; t < 16; ++t) {
+                const int rr = crow(t, g);
+                const float rt = __int_as_float(__builtin_amdgcn_ds_bpermute(ones_src * 4, __float_as_int(V[t])));
+                R += rt;
+                const float d = muq - zblk[rr * DSF + c];
+                const float v = fmaf(rt, muq, -V[t]);
+                const float dr = d * rt;
+                dz[t] = fmaf(alpha, v, fmaf(beta, dr, dz[t]));
+                X = fmaf(dr, d, X);
+                P += dr;
+                Y = fmaf(d, v, Y);
+            }
+            // Psi1 terms of (n, m), t = dL/dPsi1 * Psi1, for the rows of block w
+#pragma unroll
+            for (int t = 0; t < 16; ++t) {
+                const int rr = crow(t, g);
+                const float tv = t1r[rr];
+                T1 += tv;
+                const float d = muq - zblk[rr * DSF + c];
+                const float td = tv * d;
+                dz[t] = fmaf(td, w1q, dz[t]);
+                X1 = fmaf(td, d, X1);
+                P1 += td;
+            }
+            // combine the two lane halves, publish this wave's sums for row r
+            float *rs = lds + L.red + (r * nb + w) * RED;
+            {
+                const float x2 = __shfl_xor(X, 32), y2 = __shfl_xor(Y, 32), p2 = __shfl_xor(P, 32),
+                            x12 = __shfl_xor(X1, 32), p12 = __shfl_xor(P1, 32);
+                if (g == 0 && c < Q) {
+                    rs[c] = (X + x2) * us;
+                    rs[Q + c] = (Y + y2) * us;
+                    rs[2 * Q + c] = (P + p2) * us;
+                    rs[3 * Q + c] = X1 + x12;
+                    rs[4 * Q + c] = P1 + p12;
+                }
+            }
+            const float R2 = __shfl_xor(R, 32), T12 = __shfl_xor(T1, 32);
+            if (lane == 0) {
+                rs[5 * Q] = (R + R2) * us;
+                rs[5 * Q + 1] = T1 + T12;
+            }
+        }
+        __syncthreads();
+        // per-row sums over the waves, fixed order
+        for (int k = threadIdx.x; k < cb * RED; k += blockDim.x) {
+            const int r = k / RED, e = k - r * RED;
+            const float *rs = lds + L.red + r * nb * RED + e;
+            float v = 0.f;
+            for (int ww = 0; ww < nb; ++ww) v += rs[ww * RED];
+            rowsum[(n0 + r) * RED + e] = v;
+        }
+    }
+
+    // this wave's share of dZ for the rows of block w: slab [chunk][M][Q]
+    if (c < Q) {
+        float *pdz = part_dz + (int64_t)blockIdx.y * M * Q;
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+            const int m = w * kTile + crow(t, g);
+            if (m < M) pdz[(int64_t)m * Q + c] = dz[t];
+        }
+    }
+}
+
 // Per row: the task groups' sums (fixed order), then with w1 = 1/(l^2 + S)
 //   dmu = -2 w2 P - w1 P1
 //   dS  = w2^2 (X + Y) - w2 R + 1/2 w1^2 X1 - 1/2 w1 T1
@@ -1622,6 +1961,23 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
     return hipGetLastError();
 }
 
+template <int NK>
+hipError_t launch_grad_sym(const MPlan &p, const Shape &s, const float *mu, const float *Z,
+                           const Hyp<float> &h, const int *route, void *ws, hipStream_t st) {
+    auto k = psi2_grad_sym_kernel<NK>;
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)p.lds_grad);
+    if (e != hipSuccess) return e;
+    dim3 grid(1u, (unsigned)p.gchunks);
+    TimedScope ts(st, "mfma_psi2_grad");
+    k<<<grid, p.nb * 64, p.lds_grad, st>>>(
+        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.grows, mu, Z, fat(ws, p.off_zc),
+        fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc), fat(ws, p.off_w1),
+        fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2), fat(ws, p.off_hl),
+        fat(ws, p.off_gmax), fat(ws, p.off_bmax), h, route, fat(ws, p.off_rs), fat(ws, p.off_dz));
+    return hipGetLastError();
+}
+
 hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                         const int *route, void *ws, hipStream_t st) {
 #define GPPS_F(I, T) \
@@ -1637,6 +1993,13 @@ hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const f
 
 hipError_t dispatch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                          const Hyp<float> &h, const int *route, void *ws, hipStream_t st) {
+    if (p.gsym) {
+#define GPPS_GS(I) \
+    if (p.nk == I) return launch_grad_sym<I>(p, s, mu, Z, h, route, ws, st);
+        GPPS_GS(1) GPPS_GS(2) GPPS_GS(3) GPPS_GS(4) GPPS_GS(6) GPPS_GS(8)
+#undef GPPS_GS
+        return hipErrorInvalidValue;
+    }
 #define GPPS_G(I, Q) \
     if (p.nk == I && p.nqb == Q) return launch_grad<I, Q>(p, s, mu, Z, h, route, ws, st);
     GPPS_G(1, 1) GPPS_G(2, 1) GPPS_G(3, 1) GPPS_G(4, 1) GPPS_G(6, 1) GPPS_G(8, 1)

@@ -181,6 +181,8 @@ struct MPlan {
     int64_t Mp;            // M rounded up to the tile edge
     int nb;                // tiles per edge
     int nqb;               // 32-column blocks of [Z | 1] (Q + 1 columns)
+    int DSFs;              // symmetric gradient: the same stride, >= 2 gram_t(nk) and >= Q
+                           // (odd; lanes past Q read the next row, see lds_sym_layout)
     int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= 2
                            // gram_t(nk) and >= 32 nqb, so that no read needs a bounds test)
     int nk;                // Gram: 16-slot f16 MFMA instructions (packed layout)
@@ -267,7 +269,9 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
 }
 
 // Symmetric gradient LDS layout (floats), one workgroup of nb waves:
-//   zx  [nb 32][DSF]   centred z (fp32) of every block (as zx above)
+//   zx  [nb 32][DSF]   centred z (fp32) of every block, zero past Q, then 32 zeros: the
+//                       stride is only >= Q, so the epilogue's lanes q >= Q read the
+//                       next row's values (finite; their results are never stored)
 //   zh  [nb][2][2][2][32][8] f16   [Z | 1] of every block as V-product B operands
 //   za  [nb][nk][2][32][8] f16     [centred z | 1] of every block as Gram A operands
 //   xw  [nb][2][32][kXS] f16       per wave, its exchanged W tile as two fp16 parts:
@@ -275,7 +279,7 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
 //                       contiguous (kXS > 32 spreads the rows over the LDS banks)
 //   bb, bcb, t1 [RB][Mp]   b, b + c and dL/dPsi1 * Psi1 of the batch, every column
 //   mub, kb, w1b, w2b [RB][64] (zero past Q), sc [RB] (padded to 4), red [RB][nb][5Q + 2]
-constexpr int kSymRB = 2;   // symmetric gradient: rows per batch
+constexpr int kSymRB = 4;   // symmetric gradient: rows per batch
 constexpr int kXS = 36;     // halves per row of an exchanged tile
 struct LdsS {
     int zx, zb, za, xw, bb, bcb, t1, mub, kb, w1b, w2b, sc, red, total;
@@ -285,7 +289,7 @@ __host__ __device__ inline LdsS lds_sym_layout(int nb, int DSF, int Q, int nk) {
     LdsS L{};
     int o = 0;
     const int Mp = nb * kTile;
-    L.zx = o; o += (nb * kTile * DSF + 3) / 4 * 4;
+    L.zx = o; o += (nb * kTile * DSF + 32 + 3) / 4 * 4;
     L.zb = o; o += nb * 2 * 2 * 2 * 32 * 8 / 2;
     L.za = o; o += nb * nk * 2 * 32 * 8 / 2;
     L.xw = o; o += nb * 2 * 32 * kXS / 2;
@@ -309,6 +313,7 @@ MPlan make_mplan(const Shape &s) {
     p.nqb = s.Q + 1 <= 32 ? 1 : 2;
     p.nk = gram_nk(s.Q);
     p.DSF = std::max<int>(2 * gram_t(std::max(p.nk, 1)), 32 * p.nqb) | 1;
+    p.DSFs = std::max<int>(2 * gram_t(std::max(p.nk, 1)), (int)s.Q) | 1;
     p.T = (int64_t)p.nb * (p.nb + 1) / 2;
     // forward tasks: tiles per task by a cost model in cycles: each task splits its
     // n-dependent operand once per row (about 60 vector instructions per Gram
@@ -333,7 +338,7 @@ MPlan make_mplan(const Shape &s) {
     // symmetric gradient kernel (one workgroup of nb waves per row chunk) where
     // [Z | 1] is one column block, Mp <= 256 and its tables fit in LDS
     p.gsym = p.nqb == 1 && p.nb <= 8 && p.nk > 0 &&
-             sizeof(float) * lds_sym_layout(p.nb, p.DSF, (int)s.Q, std::max(p.nk, 1)).total <=
+             sizeof(float) * lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1)).total <=
                  (size_t)kLdsBytes;
     if (p.gsym) {
         p.jpw = p.nb;
@@ -351,7 +356,7 @@ MPlan make_mplan(const Shape &s) {
     p.igroups = (int)cdiv(p.nb, p.wpg);
     p.ggroups = (int64_t)p.njr * p.igroups;
     p.lds_grad = sizeof(float) *
-                 (p.gsym ? lds_sym_layout(p.nb, p.DSF, (int)s.Q, std::max(p.nk, 1)).total
+                 (p.gsym ? lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1)).total
                          : lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk, p.wpg).total);
     // two full rounds: workgroups per CU limited by LDS and by the waves per CU
     // the kernel's register count allows (two per SIMD; one per SIMD for the
@@ -1586,7 +1591,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
 
     // constant tables: centred z (fp32), [Z | 1] (V-product B operands) and
     // [centred z | 1] (Gram A operands) of every block
-    for (int k = threadIdx.x; k < nb * kTile * DSF; k += blockDim.x) {
+    for (int k = threadIdx.x; k < nb * kTile * DSF + 32; k += blockDim.x) {
         const int m = k / DSF, q = k - m * DSF;
         lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
     }
@@ -1971,7 +1976,7 @@ hipError_t launch_grad_sym(const MPlan &p, const Shape &s, const float *mu, cons
     dim3 grid(1u, (unsigned)p.gchunks);
     TimedScope ts(st, "mfma_psi2_grad");
     k<<<grid, p.nb * 64, p.lds_grad, st>>>(
-        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.grows, mu, Z, fat(ws, p.off_zc),
+        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSFs, p.grows, mu, Z, fat(ws, p.off_zc),
         fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc), fat(ws, p.off_w1),
         fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2), fat(ws, p.off_hl),
         fat(ws, p.off_gmax), fat(ws, p.off_bmax), h, route, fat(ws, p.off_rs), fat(ws, p.off_dz));

@@ -821,24 +821,54 @@ __global__ __launch_bounds__(1024) void mfma_absmax_kernel(int64_t nblocks,
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 
-// Low parts of two products split in two fp16 parts: given hi = the packed
-// f16(a0 b0), f16(a1 b1), returns the packed f16(fma(a0, b0, -hi0)),
-// f16(fma(a1, b1, -hi1)) -- the residuals of the exact products, one v_fma_mix
-// each, reading the high parts straight from the packed register (op_sel).
+// fp16 residuals of exact products, by v_fma_mix: given the packed high parts
+// f16(a b) of two products, v_fma_mixlo / v_fma_mixhi write f16(fma(a, b, -hi))
+// into one half of a register each, reading the high part straight from the
+// packed register (op_sel).  These half-register writes are inline assembly:
+// written in C the compiler recomputes each fp16 high part first (two more
+// vector instructions per pair).  The compiler cannot see that an asm block
+// writes half registers, so it would not keep the wait states the hardware needs
+// between such a write and an instruction that reads the register (an MFMA one
+// instruction later may see the old value): each block ends with them.
+//
+// lo_pair: one pair, (a0 b0) in the low half, (a1 b1) in the high half.
 __device__ __forceinline__ unsigned lo_pair(float a0, float b0, float a1, float b1, unsigned hi) {
     unsigned lo;
-    asm("v_fma_mixlo_f16 %0, %1, %2, -%3 op_sel_hi:[0,0,1]" : "=v"(lo) : "v"(a0), "v"(b0), "v"(hi));
-    asm("v_fma_mixhi_f16 %0, %1, %2, -%3 op_sel:[0,0,1] op_sel_hi:[0,0,1]"
-        : "+v"(lo) : "v"(a1), "v"(b1), "v"(hi));
+    asm("v_fma_mixlo_f16 %0, %1, %2, -%5 op_sel_hi:[0,0,1]\n\t"
+        "s_nop 0\n\t"
+        "v_fma_mixhi_f16 %0, %3, %4, -%5 op_sel:[0,0,1] op_sel_hi:[0,0,1]\n\t"
+        "s_nop 1"
+        : "=&v"(lo) : "v"(a0), "v"(b0), "v"(a1), "v"(b1), "v"(hi));
     return lo;
 }
 
+// lo_quad: four pairs at once, pair p from (a[2p], b[2p]) and (a[2p+1], b[2p+1])
+// with high parts hi[p]; the four low-half writes come first, so that each
+// register's two writes are three instructions apart, and one wait at the end.
+__device__ __forceinline__ void lo_quad(const float (&a)[8], const float (&b)[8],
+                                        const unsigned (&hi)[4], unsigned (&lo)[4]) {
+    asm("v_fma_mixlo_f16 %0, %4, %5, -%20 op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixlo_f16 %1, %8, %9, -%21 op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixlo_f16 %2, %12, %13, -%22 op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixlo_f16 %3, %16, %17, -%23 op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixhi_f16 %0, %6, %7, -%20 op_sel:[0,0,1] op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixhi_f16 %1, %10, %11, -%21 op_sel:[0,0,1] op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixhi_f16 %2, %14, %15, -%22 op_sel:[0,0,1] op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixhi_f16 %3, %18, %19, -%23 op_sel:[0,0,1] op_sel_hi:[0,0,1]\n\t"
+        "s_nop 1"
+        : "=&v"(lo[0]), "=&v"(lo[1]), "=&v"(lo[2]), "=&v"(lo[3])
+        : "v"(a[0]), "v"(b[0]), "v"(a[1]), "v"(b[1]), "v"(a[2]), "v"(b[2]), "v"(a[3]), "v"(b[3]),
+          "v"(a[4]), "v"(b[4]), "v"(a[5]), "v"(b[5]), "v"(a[6]), "v"(b[6]), "v"(a[7]), "v"(b[7]),
+          "v"(hi[0]), "v"(hi[1]), "v"(hi[2]), "v"(hi[3]));
+}
+
 // Given h0 = the packed (f16(a b), 0), returns (f16(a b), f16(fma(a, b, -hi))):
-// the two fp16 parts of one product in one register, the residual written into
-// the high half by one v_fma_mix reading the high part through op_sel.
+// the two fp16 parts of one product in one register.
 __device__ __forceinline__ unsigned hi_lo_pair(float a, float b, unsigned h0) {
     unsigned r = h0;
-    asm("v_fma_mixhi_f16 %0, %1, %2, -%3 op_sel_hi:[0,0,1]" : "+v"(r) : "v"(a), "v"(b), "v"(h0));
+    asm("v_fma_mixhi_f16 %0, %1, %2, -%3 op_sel_hi:[0,0,1]\n\t"
+        "s_nop 1"
+        : "+v"(r) : "v"(a), "v"(b), "v"(h0));
     return r;
 }
 
@@ -1399,15 +1429,19 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 #pragma unroll
                 for (int hh = 0; hh < 2; ++hh) {
                     unsigned wh[4], wl[4];
+                    float gv[8], xv[8];
 #pragma unroll
                     for (int u = 0; u < 4; ++u) {
                         const int t = 8 * hh + 2 * u;
-                        const float x0 = __builtin_amdgcn_exp2f(e[t]);
-                        const float x1 = __builtin_amdgcn_exp2f(e[t + 1]);
-                        const v2h h2 = {(_Float16)(g2r[k][t] * x0), (_Float16)(g2r[k][t + 1] * x1)};
+                        xv[2 * u] = __builtin_amdgcn_exp2f(e[t]);
+                        xv[2 * u + 1] = __builtin_amdgcn_exp2f(e[t + 1]);
+                        gv[2 * u] = g2r[k][t];
+                        gv[2 * u + 1] = g2r[k][t + 1];
+                        const v2h h2 = {(_Float16)(gv[2 * u] * xv[2 * u]),
+                                        (_Float16)(gv[2 * u + 1] * xv[2 * u + 1])};
                         wh[u] = __builtin_bit_cast(unsigned, h2);
-                        wl[u] = lo_pair(g2r[k][t], x0, g2r[k][t + 1], x1, wh[u]);
                     }
+                    lo_quad(gv, xv, wh, wl);
                     Wh[hh] = __builtin_bit_cast(v8h, wh);
                     Wl[hh] = __builtin_bit_cast(v8h, wl);
                 }
@@ -1669,16 +1703,21 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
             auto tile = [&](int s, int j, unsigned (&wh)[2][4], unsigned (&wl)[2][4]) {
                 const v16f e = gram16<NK>(row_terms(bbr, j, g), za + j * (NK * 2 * 32 * 8), c, g, GB);
 #pragma unroll
-                for (int hh = 0; hh < 2; ++hh)
+                for (int hh = 0; hh < 2; ++hh) {
+                    float gv[8], xv[8];
 #pragma unroll
                     for (int u = 0; u < 4; ++u) {
                         const int t = 8 * hh + 2 * u;
-                        const float x0 = __builtin_amdgcn_exp2f(e[t]);
-                        const float x1 = __builtin_amdgcn_exp2f(e[t + 1]);
-                        const v2h h2 = {(_Float16)(g2r[s][t] * x0), (_Float16)(g2r[s][t + 1] * x1)};
+                        xv[2 * u] = __builtin_amdgcn_exp2f(e[t]);
+                        xv[2 * u + 1] = __builtin_amdgcn_exp2f(e[t + 1]);
+                        gv[2 * u] = g2r[s][t];
+                        gv[2 * u + 1] = g2r[s][t + 1];
+                        const v2h h2 = {(_Float16)(gv[2 * u] * xv[2 * u]),
+                                        (_Float16)(gv[2 * u + 1] * xv[2 * u + 1])};
                         wh[hh][u] = __builtin_bit_cast(unsigned, h2);
-                        wl[hh][u] = lo_pair(g2r[s][t], x0, g2r[s][t + 1], x1, wh[hh][u]);
                     }
+                    lo_quad(gv, xv, wh[hh], wl[hh]);
+                }
             };
             // V' += W [Z_j | 1], W's two parts as A operands (three cross products)
             auto product = [&](int j, const unsigned (&wh)[2][4], const unsigned (&wl)[2][4]) {

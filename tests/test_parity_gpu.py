@@ -389,10 +389,13 @@ def test_stress_row_subset_full(path):
 
 # ------------------------------------------------------------------ determinism, chunking
 
+@pytest.mark.parametrize("workload", ["medium", "large"])
 @pytest.mark.parametrize("path", PATHS)
-def test_bitwise_deterministic(path):
+def test_bitwise_deterministic(path, workload):
+    """Two calls give identical bits.  At large the matrix-core gradient runs
+    every exchange round of its workgroups (eight blocks) over 196-row chunks."""
     use_path(path, torch.float32)
-    inp = synth.to_f32(synth.make_workload("medium"))
+    inp = synth.to_f32(synth.make_workload(workload))
     a = run_gpu(inp, torch.float32)
     b = run_gpu(inp, torch.float32)
     for k in a:
@@ -516,6 +519,21 @@ def test_mfma_gram_layout_dimensions(Q):
     inp = synth.to_f32(synth.random_inputs(300, 70, Q, seed=100 + Q))
     got = run_gpu(inp, torch.float32)
     compare_all(got, run_oracle(inp), TOL32, f"gram-Q{Q}")
+
+
+# Block counts of the symmetric gradient kernel (one workgroup of nb waves covers
+# every block pair; odd nb has (nb - 1) / 2 exchange rounds and no shared tile,
+# even nb one shared tile): nb = 5, 7 (two and three rounds), 7 at Q = 30
+# (its tables fill 159.9 of the 160 KB of LDS), 8 with a partial last block, 6;
+# N leaves partial batches of rows at the ends of the row chunks.
+@pytest.mark.parametrize("N,M,Q", [(301, 150, 9), (333, 150, 30), (299, 200, 20),
+                                   (257, 200, 30), (311, 250, 20), (205, 180, 14)])
+def test_mfma_symmetric_block_counts(N, M, Q):
+    use_path("mfma", torch.float32)
+    say(f"[symmetric gradient N={N} M={M} Q={Q}]")
+    inp = synth.to_f32(synth.random_inputs(N, M, Q, seed=300 + M + Q))
+    got = run_gpu(inp, torch.float32)
+    compare_all(got, run_oracle(inp), TOL32, f"sym-{M}x{Q}")
 
 
 # Ragged ranges of row blocks on the matrix-core path: M = 257 (9 blocks of 32,

@@ -187,6 +187,7 @@ struct MPlan {
                            // gram_t(nk) and >= 32 nqb, so that no read needs a bounds test)
     int nk;                // Gram: 16-slot f16 MFMA instructions (packed layout)
     int64_t T;             // upper-triangular tiles
+    bool fsym;             // forward: symmetric kernel (Mp <= 256)
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
     int64_t frows, fchunks;
@@ -222,6 +223,25 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int nk, int tpw) {
     int o = 0;
     L.za = o; o += kWaves * tpw * nk * 2 * 32 * 8 / 2;
     L.rt = o; o += kFRB * kWaves * kTile * (1 + tpw);
+    L.mub = o; o += kFRB * kRowStride;
+    L.kb = o; o += kFRB * kRowStride;
+    L.total = o;
+    return L;
+}
+
+// Symmetric forward LDS layout (floats): za [nb][nk][2][32][8] f16 (every block's
+// [centred z | 1] as Gram A operands), bb [FRB][Mp] (row terms b of every block),
+// bcb [FRB][waves 32] (b + c of the workgroup's column blocks), mub, kb [FRB][64].
+struct LdsFS {
+    int za, bb, bcb, mub, kb, total;
+};
+
+__host__ __device__ inline LdsFS lds_fsym_layout(int nb, int nk) {
+    LdsFS L{};
+    int o = 0;
+    L.za = o; o += nb * nk * 2 * 32 * 8 / 2;
+    L.bb = o; o += kFRB * nb * kTile;
+    L.bcb = o; o += kFRB * kWaves * kTile;
     L.mub = o; o += kFRB * kRowStride;
     L.kb = o; o += kFRB * kRowStride;
     L.total = o;
@@ -328,10 +348,18 @@ MPlan make_mplan(const Shape &s) {
     p.ftasks = fwd_tasks(p.nb, p.tpw);
     p.fgroups = cdiv(p.ftasks, kWaves);
     p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.nk, p.tpw).total;
+    // symmetric forward (wave w owns column block w, one operand split per row)
+    p.fsym = p.nb <= 8 && p.nk > 0 && p.nk <= 6;
+    if (p.fsym) {
+        p.fgroups = cdiv(p.nb, kWaves);
+        p.lds_fwd = sizeof(float) * lds_fsym_layout(p.nb, p.nk).total;
+    }
     // whole rounds of the chip's workgroup slots, so that no partly filled last
     // round idles most CUs: 6 per CU is two rounds at three workgroups per CU and
     // three at two (the register counts of the instances allow two or three)
-    const int64_t fslots = kCUs * std::min<int64_t>(6, 2 * std::max<int64_t>(1, kLdsBytes / p.lds_fwd));
+    // (the symmetric forward's register count allows two per CU: one round)
+    const int64_t fslots = p.fsym ? kCUs * std::min<int64_t>(2, std::max<int64_t>(1, kLdsBytes / p.lds_fwd))
+                                  : kCUs * std::min<int64_t>(6, 2 * std::max<int64_t>(1, kLdsBytes / p.lds_fwd));
     p.fchunks = std::max<int64_t>(1, std::min(fslots / p.fgroups, cdiv(s.N, 32)));
     p.frows = cdiv(s.N, p.fchunks);
     p.fchunks = cdiv(s.N, p.frows);
@@ -1167,6 +1195,147 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
         float *dst = partial + ((int64_t)blockIdx.y * T + tile_index(ti, tj[k], nb)) * (kTile * kTile);
 #pragma unroll
         for (int r = 0; r < 16; ++r) dst[crow(r, g) * kTile + c] = acc[k][r];
+    }
+}
+
+// ---------------------------------------------------------------- Psi2 forward, symmetric
+// Forward for Mp <= 256: wave w (of nb, in workgroups of four) owns column block
+// w, splits its per-datapoint Gram operand once per row and computes the tiles
+// (rows m' in block j, columns m in block w) for j = w + k (mod nb), k = 0 ..
+// (nb - 1) / 2, and, nb even, k = nb / 2 where w < nb / 2: every unordered tile
+// once, 4 or 5 per wave at nb = 8 (36 in all), with one operand split per column
+// block instead of one per task.  A tile with j < w is the transpose of tile
+// (j, w) and is stored transposed; the reduce kernel is unchanged.  The
+// workgroup stages the Gram A operands of every block and, per batch of kFRB
+// rows, the row terms b of every block and b + c of its own column blocks (the
+// next batch prefetched into registers while this one is computed).
+template <int NK>
+__global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
+    int64_t N, int M, int Q, int Mp, int nb, int64_t T, int64_t rows_per_chunk,
+    const float *__restrict__ mu, const float *__restrict__ Z, const float *__restrict__ zc,
+    const float *__restrict__ Kt, const float *__restrict__ bt, const float *__restrict__ bc,
+    const int *__restrict__ route, float *__restrict__ partial) {
+    extern __shared__ float lds[];
+    if (route[0]) return;
+    const LdsFS L = lds_fsym_layout(nb, NK);
+    constexpr int GT = gram_t(NK);
+    constexpr int KT = 5;                      // tile slots (nb <= 8)
+    _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
+    const int lane = threadIdx.x & 63;
+    const int wl = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int w = blockIdx.x * kWaves + wl;    // column block of the wave
+    const int c = lane & 31, g = lane >> 5;
+    const bool active = w < nb;                // wave-uniform
+    const int kx = (nb - 1) / 2;
+    const bool shared_tile = nb > 1 && (nb & 1) == 0 && w < nb / 2;
+    const int nt = 1 + kx + (shared_tile ? 1 : 0);   // tiles of the wave (at most KT)
+    v16f acc[KT];
+#pragma unroll
+    for (int s = 0; s < KT; ++s)
+#pragma unroll
+        for (int t = 0; t < 16; ++t) acc[s][t] = 0.f;
+
+    stage_za<NK>(za, 0, nb, nb, M, Q, Z, zc, threadIdx.x, blockDim.x);
+    float zr[GT];
+    {
+        const int m = min(w, nb - 1) * kTile + c;
+#pragma unroll
+        for (int j = 0; j < GT; ++j) {
+            const int q = g * GT + j, qc = min(q, Q - 1);
+            zr[j] = (m < M && q < Q ? 1.f : 0.f) * (Z[(int64_t)min(m, M - 1) * Q + qc] - zc[qc]);
+        }
+    }
+
+    // batch tables, prefetched one batch ahead from clamped addresses (entries of
+    // rows >= cb and of blocks past the edge are never read): kFRB rows of b (Mp
+    // each, at most 4 per thread), of b + c for the workgroup's column blocks (2
+    // per thread) and of mu, K (one each)
+    const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
+    const int64_t r1 = min(N, r0 + rows_per_chunk);
+    const int tid = threadIdx.x;
+    const int BB = kFRB * Mp, col0 = blockIdx.x * kWaves * kTile;
+    float pb[4], pc[2], pmu, pk;
+    auto load = [&](int64_t n0) {
+        const int cb = (int)min<int64_t>(kFRB, r1 - n0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = min(tid + i * kThreads, BB - 1), r = e / Mp;
+            pb[i] = bt[(n0 + min(r, cb - 1)) * Mp + (e - r * Mp)];
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int e = tid + i * kThreads, r = e / (kWaves * kTile), x = e - r * (kWaves * kTile);
+            pc[i] = bc[(n0 + min(r, cb - 1)) * Mp + min(col0 + x, Mp - 1)];
+        }
+        const int r = tid / kRowStride, q = tid - r * kRowStride;
+        const float ok = (r < cb && q < Q) ? 1.f : 0.f;
+        const int qc = min(q, Q - 1);
+        const int64_t rc = n0 + min(r, cb - 1);
+        pmu = ok * (mu[rc * Q + qc] - zc[qc]);
+        pk = ok * Kt[rc * kRowStride + qc];
+    };
+    if (r0 < r1) load(r0);
+    for (int64_t n0 = r0; n0 < r1; n0 += kFRB) {
+        const int cb = (int)min<int64_t>(kFRB, r1 - n0);
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (tid + i * kThreads < BB) lds[L.bb + tid + i * kThreads] = pb[i];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) lds[L.bcb + tid + i * kThreads] = pc[i];
+        lds[L.mub + tid] = pmu;
+        lds[L.kb + tid] = pk;
+        __syncthreads();
+        if (n0 + kFRB < r1) load(n0 + kFRB);
+        if (!active) continue;
+        for (int r = 0; r < cb; ++r) {
+            v8h B[NK];
+            gram_operand<NK>(zr, lds + L.mub + r * kRowStride + g * GT,
+                             lds + L.kb + r * kRowStride + g * GT,
+                             lds[L.bcb + r * (kWaves * kTile) + wl * kTile + c], g, B);
+            const float *bbr = lds + L.bb + r * Mp;
+            // tiles in slot order (k = 0 .. kx, then nb / 2 where shared), each
+            // tile's Gram product issued before the previous tile's exponentials,
+            // the two products alternating between e0 and e1 (no register copies)
+            auto gram_slot = [&](int sl) {
+                const int j = (w + (sl <= kx ? sl : nb / 2)) % nb;
+                return gram16<NK>(row_terms(bbr, j, g), za + j * (NK * 2 * 32 * 8), c, g, B);
+            };
+            auto add_exp = [&](v16f &a, const v16f &e) {
+                float x[16];
+#pragma unroll
+                for (int t = 0; t < 16; ++t) x[t] = __builtin_amdgcn_exp2f(e[t]);
+#pragma unroll
+                for (int t = 0; t < 16; ++t) a[t] += x[t];
+            };
+            v16f e0 = gram_slot(0), e1;
+            if (nt > 1) e1 = gram_slot(1);
+            add_exp(acc[0], e0);
+            if (nt > 2) e0 = gram_slot(2);
+            if (nt > 1) add_exp(acc[1], e1);
+            if (nt > 3) e1 = gram_slot(3);
+            if (nt > 2) add_exp(acc[2], e0);
+            if (nt > 4) e0 = gram_slot(4);
+            if (nt > 3) add_exp(acc[3], e1);
+            if (nt > 4) add_exp(acc[4], e0);
+        }
+    }
+    // partial tiles: element [m' - 32 tj][m - 32 ti] of tile (ti, tj), tj >= ti
+    if (!active) return;
+#pragma unroll
+    for (int s = 0; s < KT; ++s) {
+        if (s >= nt) continue;
+        const int j = (w + (s <= kx ? s : nb / 2)) % nb;
+        if (j >= w) {
+            float *dst = partial + ((int64_t)blockIdx.y * T + tile_index(w, j, nb)) * (kTile * kTile);
+#pragma unroll
+            for (int t = 0; t < 16; ++t) dst[crow(t, g) * kTile + c] = acc[s][t];
+        } else {
+            // rows m' in block j, columns m in block w: the transpose of tile (j, w)
+            float *dst = partial + ((int64_t)blockIdx.y * T + tile_index(j, w, nb)) * (kTile * kTile);
+#pragma unroll
+            for (int t = 0; t < 16; ++t) dst[c * kTile + crow(t, g)] = acc[s][t];
+        }
     }
 }
 
@@ -2022,8 +2191,31 @@ hipError_t launch_grad_sym(const MPlan &p, const Shape &s, const float *mu, cons
     return hipGetLastError();
 }
 
+template <int NK>
+hipError_t launch_fwd_sym(const MPlan &p, const Shape &s, const float *mu, const float *Z,
+                          const int *route, void *ws, hipStream_t st) {
+    auto k = psi2_fwd_sym_kernel<NK>;
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)p.lds_fwd);
+    if (e != hipSuccess) return e;
+    dim3 grid((unsigned)p.fgroups, (unsigned)p.fchunks);
+    TimedScope ts(st, "mfma_psi2_fwd");
+    k<<<grid, kThreads, p.lds_fwd, st>>>(s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.T, p.frows,
+                                         mu, Z, fat(ws, p.off_zc), fat(ws, p.off_K),
+                                         fat(ws, p.off_bt), fat(ws, p.off_bc), route,
+                                         fat(ws, p.off_fp));
+    return hipGetLastError();
+}
+
 hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                         const int *route, void *ws, hipStream_t st) {
+    if (p.fsym) {
+#define GPPS_FS(I) \
+    if (p.nk == I) return launch_fwd_sym<I>(p, s, mu, Z, route, ws, st);
+        GPPS_FS(1) GPPS_FS(2) GPPS_FS(3) GPPS_FS(4) GPPS_FS(6)
+#undef GPPS_FS
+        return hipErrorInvalidValue;
+    }
 #define GPPS_F(I, T) \
     if (p.nk == I && p.tpw == T) return launch_fwd<I, T>(p, s, mu, Z, route, ws, st);
     GPPS_F(1, 1) GPPS_F(1, 2) GPPS_F(1, 3) GPPS_F(1, 4)

@@ -1920,7 +1920,6 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
                 const int j = (w + k) % nb, src = (w + nb - k) % nb;
                 unsigned wh[2][4], wl[2][4];
                 tile(k, j, wh, wl);
-                product(j, wh, wl);
                 __syncthreads();                         // the previous round's reads are done
 #pragma unroll
                 for (int T = 0; T < 4; ++T) {
@@ -1946,6 +1945,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
                         rl[hh][2 * h2] = b2.x;
                         rl[hh][2 * h2 + 1] = b2.y;
                     }
+                product(j, wh, wl);                      // covers the transpose reads' latency
                 product(src, rh, rl);
             }
             // V' carries the row scale 2^sc: the epilogue's coefficients and row sums

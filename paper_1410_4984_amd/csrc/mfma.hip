@@ -725,11 +725,20 @@ __global__ __launch_bounds__(256) void mfma_rowterm_kernel(
     for (int u = 0; u < 4; ++u) realf[u] = m0 + u < M ? 1.f : 0.f;
     // dL/dPsi1 of the wave's rows, loaded one row ahead of its use (padded
     // columns: the product of column M - 1's value and 0)
+    // (one 16-byte load per lane where M is a multiple of 4 and G1 16-byte
+    // aligned: the lane's four m are then all real or all padding)
     float g1c[4] = {0.f, 0.f, 0.f, 0.f};
+    const bool g1vec = (M & 3) == 0 && (reinterpret_cast<uintptr_t>(G1) & 15) == 0;
     auto load_g1 = [&](int r, float *g) {
         const int64_t row = (n0 + min(r, cnt - 1)) * M;
+        if (g1vec) {
+            const v4f v = *reinterpret_cast<const v4f *>(G1 + row + (m0 < M ? m0 : 0));
 #pragma unroll
-        for (int u = 0; u < 4; ++u) g[u] = realf[u] * G1[row + min(m0 + u, M - 1)];
+            for (int u = 0; u < 4; ++u) g[u] = realf[u] * v[u];
+        } else {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) g[u] = realf[u] * G1[row + min(m0 + u, M - 1)];
+        }
     };
     if constexpr (GRAD)
         if (G1) load_g1(wave, g1c);

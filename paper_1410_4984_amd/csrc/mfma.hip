@@ -170,7 +170,7 @@ inline int gram_nk(int64_t Q) {
 
 // Widest forward task (tiles per wave) whose registers fit two waves per SIMD
 // without spilling, for nk Gram instructions.
-constexpr int fwd_tpw_max(int nk) { return nk <= 2 ? 4 : (nk <= 4 ? 2 : 1); }
+constexpr int fwd_tpw_max(int nk) { return nk <= 2 ? 4 : (nk <= 6 ? 2 : 1); }
 
 // Upper-triangular tile index of (ti, tj), row-major.
 __host__ __device__ inline int64_t tile_index(int ti, int tj, int nb) {
@@ -1748,8 +1748,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 // (rows m' in block j, columns m in block w) for j = w (diagonal), j = w + k
 // (mod nb) for k = 1 .. kx = (nb - 1) / 2, and, nb even, j = w + nb / 2, which
 // both partners compute, so that every wave has the same work.  A tile feeds the
-// wave's own V sum as now (W in the MFMA output layout is the A operand of
-// V' += W [Z_j | 1]); each tile of the rounds k = 1 .. kx also feeds block j's
+// wave's own V sum as in psi2_grad_kernel (W in the MFMA output layout is the A
+// operand of V' += W [Z_j | 1]); each tile of the rounds k = 1 .. kx also feeds block j's
 // sum: the wave writes its two fp16 parts to LDS with m' contiguous, and wave j
 // reads them back transposed (ds_read_b64_tr_b16: within each 16 lanes, element
 // e of lane i comes from sub-element i % 4 of the 8 bytes lane 4 e + i / 4
@@ -2231,7 +2231,7 @@ hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const f
     GPPS_F(2, 1) GPPS_F(2, 2) GPPS_F(2, 3) GPPS_F(2, 4)
     GPPS_F(3, 1) GPPS_F(3, 2)
     GPPS_F(4, 1) GPPS_F(4, 2)
-    GPPS_F(6, 1) GPPS_F(8, 1) GPPS_F(10, 1) GPPS_F(12, 1)
+    GPPS_F(6, 1) GPPS_F(6, 2) GPPS_F(8, 1) GPPS_F(10, 1) GPPS_F(12, 1)
 #undef GPPS_F
     return hipErrorInvalidValue;
 }

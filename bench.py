@@ -66,6 +66,10 @@ PEAK_FP32 = 157.3e12          # MI355X FP32 vector peak (packed FMA), FLOP/s
 PEAK_FP64 = 78.6e12           # MI355X FP64 vector peak, FLOP/s
 PEAK_F16_MFMA = 2.5e15        # MI355X dense fp16 / bf16 matrix-core peak, FLOP/s
 PEAK_HBM = 8.0e12             # B/s
+# vector issue peak: 256 CUs x 4 SIMDs x 16 lanes per cycle at 2.4 GHz (a wave64
+# instruction takes four cycles of a SIMD; 2 flops per lane for an FMA gives the
+# unpacked fp32 rate, half of the packed 157.3 TFLOP/s)
+PEAK_VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
 METRIC = "N·M²·Q psi-stat+grad terms/sec (fp32) and % of FP32 VALU peak, 1 MI355X"
 
 
@@ -579,6 +583,10 @@ def main():
                 "mfma_peak_f16_tflops": PEAK_F16_MFMA / 1e12,
                 "mfma_frac_f16_peak": round(mfma_flops / avg_s / PEAK_F16_MFMA, 4),
                 "mfma_frac_f16_measured": round(mfma_flops / avg_s / rates["mfma_f16_flops"], 4),
+                "valu_insts_per_launch": c["SQ_INSTS_VALU"],
+                "valu_lane_ops_per_s": float(f"{c['SQ_INSTS_VALU'] * 64 / avg_s:.4g}"),
+                "valu_frac_lane_issue_peak": round(c["SQ_INSTS_VALU"] * 64 / avg_s
+                                                   / PEAK_VALU_LANE_OPS, 4),
                 "exp_executed_per_launch": c["SQ_INSTS_VALU_TRANS_F32"] * 64,
                 "exp_unique_pairs_per_launch": float(N) / len(chunks) * P,
                 "counters": f"profiles/counters_{dom}_{args.workload}.md"}

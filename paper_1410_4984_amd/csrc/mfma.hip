@@ -187,7 +187,7 @@ struct MPlan {
                            // gram_t(nk) and >= 32 nqb, so that no read needs a bounds test)
     int nk;                // Gram: 16-slot f16 MFMA instructions (packed layout)
     int64_t T;             // upper-triangular tiles
-    bool fsym;             // forward: symmetric kernel (Mp <= 256)
+    bool fsym;             // forward: symmetric kernel (Mp <= 512, NK <= 6)
     int tpw, ftasks;       // forward: tiles per wave task, tasks
     int64_t fgroups;       // forward: workgroups (4 tasks each) per row chunk
     int64_t frows, fchunks;
@@ -229,18 +229,35 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int nk, int tpw) {
     return L;
 }
 
-// Symmetric forward LDS layout (floats): za [nb][nk][2][32][8] f16 (every block's
-// [centred z | 1] as Gram A operands), bb [FRB][Mp] (row terms b of every block),
-// bcb [FRB][waves 32] (b + c of the workgroup's column blocks), mub, kb [FRB][64].
+// Symmetric forward: tile assignment.  Wave w (column block w) takes the tiles
+// j = w + k (mod nb) for k = 0 .. kx = (nb - 1) / 2 and, nb even, k = nb / 2 where
+// w < nb / 2 (every unordered tile once).  Where that is more than kFSymSlots
+// tiles (nb >= 10), the list is split into two ranges of k, the first
+// ceil(nt / 2) tiles and the rest, computed by workgroups of their own.  A
+// workgroup (four consecutive column blocks, one range) stages a window of at
+// most kFSymWindow consecutive blocks (mod nb) that holds every row block its
+// waves read.
+constexpr int kFSymSlots = 5;
+constexpr int kFSymWindow = 8;
+__host__ __device__ inline int fsym_tiles(int nb, int w) {
+    return 1 + (nb - 1) / 2 + ((nb > 1 && (nb & 1) == 0 && w < nb / 2) ? 1 : 0);
+}
+__host__ __device__ inline int fsym_ranges(int nb) { return fsym_tiles(nb, 0) <= kFSymSlots ? 1 : 2; }
+__host__ __device__ inline int fsym_window(int nb) { return nb < kFSymWindow ? nb : kFSymWindow; }
+
+// Symmetric forward LDS layout (floats): za [nzb][nk][2][32][8] f16 (the window's
+// [centred z | 1] as Gram A operands), bb [FRB][32 nzb] (row terms b of the
+// window's blocks), bcb [FRB][waves 32] (b + c of the workgroup's column blocks),
+// mub, kb [FRB][64].
 struct LdsFS {
     int za, bb, bcb, mub, kb, total;
 };
 
-__host__ __device__ inline LdsFS lds_fsym_layout(int nb, int nk) {
+__host__ __device__ inline LdsFS lds_fsym_layout(int nzb, int nk) {
     LdsFS L{};
     int o = 0;
-    L.za = o; o += nb * nk * 2 * 32 * 8 / 2;
-    L.bb = o; o += kFRB * nb * kTile;
+    L.za = o; o += nzb * nk * 2 * 32 * 8 / 2;
+    L.bb = o; o += kFRB * nzb * kTile;
     L.bcb = o; o += kFRB * kWaves * kTile;
     L.mub = o; o += kFRB * kRowStride;
     L.kb = o; o += kFRB * kRowStride;
@@ -349,10 +366,10 @@ MPlan make_mplan(const Shape &s) {
     p.fgroups = cdiv(p.ftasks, kWaves);
     p.lds_fwd = sizeof(float) * lds_fwd_layout((int)p.Mp, p.nk, p.tpw).total;
     // symmetric forward (wave w owns column block w, one operand split per row)
-    p.fsym = p.nb <= 8 && p.nk > 0 && p.nk <= 6;
+    p.fsym = p.nb <= 16 && p.nk > 0 && p.nk <= 6;
     if (p.fsym) {
-        p.fgroups = cdiv(p.nb, kWaves);
-        p.lds_fwd = sizeof(float) * lds_fsym_layout(p.nb, p.nk).total;
+        p.fgroups = cdiv(p.nb, kWaves) * fsym_ranges(p.nb);
+        p.lds_fwd = sizeof(float) * lds_fsym_layout(fsym_window(p.nb), p.nk).total;
     }
     // whole rounds of the chip's workgroup slots, so that no partly filled last
     // round idles most CUs: 6 per CU is two rounds at three workgroups per CU and
@@ -988,7 +1005,8 @@ __device__ __forceinline__ v16f row_terms(const float *__restrict__ bbr, int j, 
 }
 
 // [centred z s | 1] rows of blocks blk0 .. blk0 + nblk - 1 (clamped to the last
-// block) as packed Gram A operand tables: [nblk][NK][2][32][8] f16 (slot
+// block, or with wrap taken mod nb, blk0 < nb, nblk <= nb) as packed Gram A
+// operand tables: [nblk][NK][2][32][8] f16 (slot
 // contents listed at gram_np; zc is the centring table, [4][Q]), written by the
 // nt threads t0 = 0 .. nt - 1.  Each thread issues the loads of U entries
 // together from clamped (valid) addresses and masks them afterwards (the range
@@ -996,7 +1014,7 @@ __device__ __forceinline__ v16f row_terms(const float *__restrict__ bbr, int j, 
 template <int NK>
 __device__ void stage_za(_Float16 *za, int blk0, int nblk, int nb, int M, int Q,
                          const float *__restrict__ Z, const float *__restrict__ zc, int t0,
-                         int nt) {
+                         int nt, bool wrap = false) {
     constexpr int NP = gram_np(NK), ODD = gram_odd(NK), T = gram_t(NK);
     constexpr int U = 8;
     const int total = nblk * NK * 2 * 32 * 8;
@@ -1012,7 +1030,8 @@ __device__ void stage_za(_Float16 *za, int blk0, int nblk, int nb, int M, int Q,
             const int gg = r % 2; r /= 2;
             const int ins = r % NK; r /= NK;
             // blocks past the edge repeat the last one, so that every exponent stays finite
-            const int m = min(blk0 + r, nb - 1) * kTile + cc;
+            const int blk = blk0 + r;
+            const int m = (wrap ? (blk >= nb ? blk - nb : blk) : min(blk, nb - 1)) * kTile + cc;
             const int w = 4 * ins + e / 2, half = e & 1;
             int q = -1, part = 0;  // part 0: high fp16 part of z, 1: low part
             float one = 0.f;
@@ -1208,16 +1227,17 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
 }
 
 // ---------------------------------------------------------------- Psi2 forward, symmetric
-// Forward for Mp <= 256: wave w (of nb, in workgroups of four) owns column block
-// w, splits its per-datapoint Gram operand once per row and computes the tiles
-// (rows m' in block j, columns m in block w) for j = w + k (mod nb), k = 0 ..
-// (nb - 1) / 2, and, nb even, k = nb / 2 where w < nb / 2: every unordered tile
-// once, 4 or 5 per wave at nb = 8 (36 in all), with one operand split per column
-// block instead of one per task.  A tile with j < w is the transpose of tile
-// (j, w) and is stored transposed; the reduce kernel is unchanged.  The
-// workgroup stages the Gram A operands of every block and, per batch of kFRB
-// rows, the row terms b of every block and b + c of its own column blocks (the
-// next batch prefetched into registers while this one is computed).
+// Forward for Mp <= 512 and NK <= 6: wave w owns column block w, splits its
+// per-datapoint Gram operand once per row and computes the tiles (rows m' in
+// block j, columns m in block w) of its range of the circulant assignment
+// (fsym_tiles): every unordered tile once, 36 at nb = 8 (4 or 5 per wave), 136 at
+// nb = 16 (two ranges of at most 5 per wave), with one operand split per column
+// block and range instead of one per task.  A tile with j < w is the transpose of
+// tile (j, w) and is stored transposed; the reduce kernel is unchanged.  A
+// workgroup (four column blocks, one range: blockIdx.x = group + groups * range)
+// stages the Gram A operands of its window of blocks and, per batch of kFRB rows,
+// the window's row terms b and the b + c of its own column blocks (the next batch
+// prefetched into registers while this one is computed).
 template <int NK>
 __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int64_t T, int64_t rows_per_chunk,
@@ -1226,25 +1246,35 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
     const int *__restrict__ route, float *__restrict__ partial) {
     extern __shared__ float lds[];
     if (route[0]) return;
-    const LdsFS L = lds_fsym_layout(nb, NK);
+    const int nzb = fsym_window(nb);
+    const LdsFS L = lds_fsym_layout(nzb, NK);
     constexpr int GT = gram_t(NK);
-    constexpr int KT = 5;                      // tile slots (nb <= 8)
+    constexpr int KT = kFSymSlots;             // tile slots per wave and range
     _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
     const int lane = threadIdx.x & 63;
     const int wl = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int w = blockIdx.x * kWaves + wl;    // column block of the wave
+    const int ncg = (nb + kWaves - 1) / kWaves;
+    const int cg = blockIdx.x % ncg, rg = blockIdx.x / ncg;   // column group, range
+    const int w0 = cg * kWaves;
+    const int w = w0 + wl;                     // column block of the wave
     const int c = lane & 31, g = lane >> 5;
     const bool active = w < nb;                // wave-uniform
-    const int kx = (nb - 1) / 2;
-    const bool shared_tile = nb > 1 && (nb & 1) == 0 && w < nb / 2;
-    const int nt = 1 + kx + (shared_tile ? 1 : 0);   // tiles of the wave (at most KT)
+    // the wave's tiles in this range: k = k0 .. k0 + nt - 1
+    const int ntw = fsym_tiles(nb, min(w, nb - 1));
+    const int half = fsym_ranges(nb) == 1 ? ntw : (ntw + 1) / 2;
+    const int k0 = rg == 0 ? 0 : half;
+    const int nt = rg == 0 ? half : ntw - half;      // at most KT
+    // window: blocks jbase .. jbase + nzb - 1 (mod nb); the range's smallest k is
+    // that of the group's last wave (the first range starts at k = 0)
+    const int kmin = rg == 0 ? 0 : (fsym_tiles(nb, min(w0 + kWaves - 1, nb - 1)) + 1) / 2;
+    const int jbase = (w0 + kmin) % nb;
     v16f acc[KT];
 #pragma unroll
     for (int s = 0; s < KT; ++s)
 #pragma unroll
         for (int t = 0; t < 16; ++t) acc[s][t] = 0.f;
 
-    stage_za<NK>(za, 0, nb, nb, M, Q, Z, zc, threadIdx.x, blockDim.x);
+    stage_za<NK>(za, jbase, nzb, nb, M, Q, Z, zc, threadIdx.x, blockDim.x, true);
     float zr[GT];
     {
         const int m = min(w, nb - 1) * kTile + c;
@@ -1256,20 +1286,21 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
     }
 
     // batch tables, prefetched one batch ahead from clamped addresses (entries of
-    // rows >= cb and of blocks past the edge are never read): kFRB rows of b (Mp
-    // each, at most 4 per thread), of b + c for the workgroup's column blocks (2
-    // per thread) and of mu, K (one each)
+    // rows >= cb and of blocks past the edge are never read): kFRB rows of b for
+    // the window (32 nzb each, at most 4 per thread), of b + c for the
+    // workgroup's column blocks (2 per thread) and of mu, K (one each)
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
     const int tid = threadIdx.x;
-    const int BB = kFRB * Mp, col0 = blockIdx.x * kWaves * kTile;
+    const int WB = nzb * kTile, BB = kFRB * WB, col0 = w0 * kTile;
     float pb[4], pc[2], pmu, pk;
     auto load = [&](int64_t n0) {
         const int cb = (int)min<int64_t>(kFRB, r1 - n0);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int e = min(tid + i * kThreads, BB - 1), r = e / Mp;
-            pb[i] = bt[(n0 + min(r, cb - 1)) * Mp + (e - r * Mp)];
+            const int e = min(tid + i * kThreads, BB - 1), r = e / WB, x = e - r * WB;
+            const int blk = jbase + x / kTile;
+            pb[i] = bt[(n0 + min(r, cb - 1)) * Mp + (blk >= nb ? blk - nb : blk) * kTile + x % kTile];
         }
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
@@ -1302,13 +1333,14 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
             gram_operand<NK>(zr, lds + L.mub + r * kRowStride + g * GT,
                              lds + L.kb + r * kRowStride + g * GT,
                              lds[L.bcb + r * (kWaves * kTile) + wl * kTile + c], g, B);
-            const float *bbr = lds + L.bb + r * Mp;
-            // tiles in slot order (k = 0 .. kx, then nb / 2 where shared), each
-            // tile's Gram product issued before the previous tile's exponentials,
-            // the two products alternating between e0 and e1 (no register copies)
+            const float *bbr = lds + L.bb + r * WB;
+            // tiles in slot order, each tile's Gram product issued before the
+            // previous tile's exponentials, the two products alternating between
+            // e0 and e1 (no register copies)
             auto gram_slot = [&](int sl) {
-                const int j = (w + (sl <= kx ? sl : nb / 2)) % nb;
-                return gram16<NK>(row_terms(bbr, j, g), za + j * (NK * 2 * 32 * 8), c, g, B);
+                int jt = (w + k0 + sl) % nb - jbase;      // the window's block index
+                jt += jt < 0 ? nb : 0;
+                return gram16<NK>(row_terms(bbr, jt, g), za + jt * (NK * 2 * 32 * 8), c, g, B);
             };
             auto add_exp = [&](v16f &a, const v16f &e) {
                 float x[16];
@@ -1334,7 +1366,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
 #pragma unroll
     for (int s = 0; s < KT; ++s) {
         if (s >= nt) continue;
-        const int j = (w + (s <= kx ? s : nb / 2)) % nb;
+        const int j = (w + k0 + s) % nb;
         if (j >= w) {
             float *dst = partial + ((int64_t)blockIdx.y * T + tile_index(w, j, nb)) * (kTile * kTile);
 #pragma unroll

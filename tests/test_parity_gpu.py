@@ -536,6 +536,23 @@ def test_mfma_symmetric_block_counts(N, M, Q):
     compare_all(got, run_oracle(inp), TOL32, f"sym-{M}x{Q}")
 
 
+# Block counts of the symmetric forward past eight blocks: from nb = 10 each wave's
+# tiles are split into two ranges of k with workgroups of their own, and each
+# workgroup stages a window of eight blocks taken mod nb.  nb = 9 (one range, a
+# window smaller than nb), 10 and 12 (column groups that straddle nb / 2, where
+# the waves' tile counts differ), 11 and 13 (odd), 15 and 16 (the largest
+# windows), at Q from 3 to 30 (one to six Gram instructions).
+@pytest.mark.parametrize("N,M,Q", [(150, 270, 20), (160, 310, 12), (140, 350, 30),
+                                   (130, 384, 6), (150, 410, 20), (120, 449, 25),
+                                   (129, 512, 30), (100, 500, 3)])
+def test_mfma_symmetric_forward_ranges(N, M, Q):
+    use_path("mfma", torch.float32)
+    say(f"[symmetric forward ranges N={N} M={M} Q={Q}]")
+    inp = synth.to_f32(synth.random_inputs(N, M, Q, seed=400 + M + Q))
+    got = run_gpu(inp, torch.float32)
+    compare_all(got, run_oracle(inp), TOL32, f"fsym-{M}x{Q}")
+
+
 # Ragged ranges of row blocks on the matrix-core path: M = 257 (9 blocks of 32,
 # three ranges of four, the last with one real block) at Q = 20, and M = 300 at
 # Q = 31 (eight Gram instructions, the widest single [Z | 1] column block).

@@ -244,6 +244,16 @@ __host__ __device__ inline int fsym_tiles(int nb, int w) {
 }
 __host__ __device__ inline int fsym_ranges(int nb) { return fsym_tiles(nb, 0) <= kFSymSlots ? 1 : 2; }
 __host__ __device__ inline int fsym_window(int nb) { return nb < kFSymWindow ? nb : kFSymWindow; }
+// Even nb with one range: workgroup g holds the partner pairs (p, p + nb / 2) for
+// p = 2 g, 2 g + 1 (wave slots 0, 1: p; slots 2, 3: p + nb / 2), and the two
+// partners split their shared tile (k = nb / 2) by row parity, so that every wave
+// takes kx + 1.5 tiles per row instead of kx + 2 for one and kx + 1 for the other.
+__host__ __device__ inline bool fsym_pairs(int nb) {
+    return nb > 1 && (nb & 1) == 0 && fsym_ranges(nb) == 1;
+}
+__host__ __device__ inline int fsym_groups(int nb) {
+    return fsym_pairs(nb) ? (nb / 2 + 1) / 2 : (nb + kWaves - 1) / kWaves * fsym_ranges(nb);
+}
 
 // Symmetric forward LDS layout (floats): za [nzb][nk][2][32][8] f16 (the window's
 // [centred z | 1] as Gram A operands), bb [FRB][32 nzb] (row terms b of the
@@ -261,7 +271,7 @@ __host__ __device__ inline LdsFS lds_fsym_layout(int nzb, int nk) {
     L.bcb = o; o += kFRB * kWaves * kTile;
     L.mub = o; o += kFRB * kRowStride;
     L.kb = o; o += kFRB * kRowStride;
-    L.total = o;
+    L.total = o > 2 * 32 * 33 ? o : 2 * 32 * 33;   // also the shared tiles' hand-over
     return L;
 }
 
@@ -368,7 +378,7 @@ MPlan make_mplan(const Shape &s) {
     // symmetric forward (wave w owns column block w, one operand split per row)
     p.fsym = p.nb <= 16 && p.nk > 0 && p.nk <= 6;
     if (p.fsym) {
-        p.fgroups = cdiv(p.nb, kWaves) * fsym_ranges(p.nb);
+        p.fgroups = fsym_groups(p.nb);
         p.lds_fwd = sizeof(float) * lds_fsym_layout(fsym_window(p.nb), p.nk).total;
     }
     // whole rounds of the chip's workgroup slots, so that no partly filled last
@@ -1253,21 +1263,28 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
     _Float16 *za = reinterpret_cast<_Float16 *>(lds + L.za);
     const int lane = threadIdx.x & 63;
     const int wl = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const bool pairs = fsym_pairs(nb);
     const int ncg = (nb + kWaves - 1) / kWaves;
-    const int cg = blockIdx.x % ncg, rg = blockIdx.x / ncg;   // column group, range
+    const int cg = pairs ? (int)blockIdx.x : (int)blockIdx.x % ncg;   // column group
+    const int rg = pairs ? 0 : (int)blockIdx.x / ncg;                 // range
     const int w0 = cg * kWaves;
-    const int w = w0 + wl;                     // column block of the wave
+    // column block of wave slot sl: four consecutive blocks, or the two pairs
+    auto slot_block = [&](int sl) { return pairs ? 2 * cg + (sl & 1) + (sl >> 1) * (nb / 2) : w0 + sl; };
+    const int w = slot_block(wl);              // column block of the wave
     const int c = lane & 31, g = lane >> 5;
-    const bool active = w < nb;                // wave-uniform
-    // the wave's tiles in this range: k = k0 .. k0 + nt - 1
+    const bool active = pairs ? 2 * cg + (wl & 1) < nb / 2 : w < nb;   // wave-uniform
+    // the wave's tiles in this range: k = k0 .. k0 + nt - 1 (pairs: k = 0 .. kx,
+    // and the shared k = nb / 2 on the rows of the wave's parity)
+    const int kx = (nb - 1) / 2;
     const int ntw = fsym_tiles(nb, min(w, nb - 1));
     const int half = fsym_ranges(nb) == 1 ? ntw : (ntw + 1) / 2;
     const int k0 = rg == 0 ? 0 : half;
-    const int nt = rg == 0 ? half : ntw - half;      // at most KT
+    const int nt = pairs ? kx + 1 : (rg == 0 ? half : ntw - half);   // at most KT
+    const int ntall = pairs ? kx + 2 : nt;     // accumulator tiles in use
     // window: blocks jbase .. jbase + nzb - 1 (mod nb); the range's smallest k is
     // that of the group's last wave (the first range starts at k = 0)
     const int kmin = rg == 0 ? 0 : (fsym_tiles(nb, min(w0 + kWaves - 1, nb - 1)) + 1) / 2;
-    const int jbase = (w0 + kmin) % nb;
+    const int jbase = pairs ? 0 : (w0 + kmin) % nb;
     v16f acc[KT];
 #pragma unroll
     for (int s = 0; s < KT; ++s)
@@ -1292,7 +1309,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
     const int tid = threadIdx.x;
-    const int WB = nzb * kTile, BB = kFRB * WB, col0 = w0 * kTile;
+    const int WB = nzb * kTile, BB = kFRB * WB;
     float pb[4], pc[2], pmu, pk;
     auto load = [&](int64_t n0) {
         const int cb = (int)min<int64_t>(kFRB, r1 - n0);
@@ -1305,7 +1322,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int e = tid + i * kThreads, r = e / (kWaves * kTile), x = e - r * (kWaves * kTile);
-            pc[i] = bc[(n0 + min(r, cb - 1)) * Mp + min(col0 + x, Mp - 1)];
+            pc[i] = bc[(n0 + min(r, cb - 1)) * Mp + min(slot_block(x / kTile), nb - 1) * kTile + x % kTile];
         }
         const int r = tid / kRowStride, q = tid - r * kRowStride;
         const float ok = (r < cb && q < Q) ? 1.f : 0.f;
@@ -1349,23 +1366,45 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
 #pragma unroll
                 for (int t = 0; t < 16; ++t) a[t] += x[t];
             };
+            const int ntr = nt + ((pairs && (r & 1) == (wl >> 1)) ? 1 : 0);
             v16f e0 = gram_slot(0), e1;
-            if (nt > 1) e1 = gram_slot(1);
+            if (ntr > 1) e1 = gram_slot(1);
             add_exp(acc[0], e0);
-            if (nt > 2) e0 = gram_slot(2);
-            if (nt > 1) add_exp(acc[1], e1);
-            if (nt > 3) e1 = gram_slot(3);
-            if (nt > 2) add_exp(acc[2], e0);
-            if (nt > 4) e0 = gram_slot(4);
-            if (nt > 3) add_exp(acc[3], e1);
-            if (nt > 4) add_exp(acc[4], e0);
+            if (ntr > 2) e0 = gram_slot(2);
+            if (ntr > 1) add_exp(acc[1], e1);
+            if (ntr > 3) e1 = gram_slot(3);
+            if (ntr > 2) add_exp(acc[2], e0);
+            if (ntr > 4) e0 = gram_slot(4);
+            if (ntr > 3) add_exp(acc[3], e1);
+            if (ntr > 4) add_exp(acc[4], e0);
+        }
+    }
+    if (pairs) {
+        // the shared tile's rows of odd parity (slots 2, 3: rows m' in block p, columns
+        // m in block p + nb / 2) join those of even parity (slots 0, 1: the transpose
+        // orientation) through LDS, [2][32][33], over the batch tables
+        __syncthreads();
+        if (active && wl >= 2) {
+#pragma unroll
+            for (int s = 0; s < KT; ++s)
+                if (s == kx + 1)
+#pragma unroll
+                    for (int t = 0; t < 16; ++t) lds[(wl - 2) * 32 * 33 + c * 33 + crow(t, g)] = acc[s][t];
+        }
+        __syncthreads();
+        if (active && wl < 2) {
+#pragma unroll
+            for (int s = 0; s < KT; ++s)
+                if (s == kx + 1)
+#pragma unroll
+                    for (int t = 0; t < 16; ++t) acc[s][t] += lds[wl * 32 * 33 + crow(t, g) * 33 + c];
         }
     }
     // partial tiles: element [m' - 32 tj][m - 32 ti] of tile (ti, tj), tj >= ti
     if (!active) return;
 #pragma unroll
     for (int s = 0; s < KT; ++s) {
-        if (s >= nt) continue;
+        if (s >= ntall || (pairs && wl >= 2 && s == kx + 1)) continue;
         const int j = (w + k0 + s) % nb;
         if (j >= w) {
             float *dst = partial + ((int64_t)blockIdx.y * T + tile_index(w, j, nb)) * (kTile * kTile);

@@ -567,6 +567,11 @@ def main():
                     "unit": u, "frac": round(ach / peak, 4),
                     "traffic": traffic_for(dom, args.workload),
                     "algorithmic_per_launch": work}
+        if unit == "flop" and on_mfma:
+            roofline["note"] = (
+                "algorithmic fp32 flops (each unordered pair once) against the fp32 vector peak; "
+                "the Q-long contractions run on the matrix cores, so the fraction can pass 1; "
+                "'issue' gives what each unit executed")
         cnt = counters_for(dom, args.workload) if on_mfma else None
         if cnt is not None and unit == "flop":
             c = cnt["per_dispatch"]

@@ -182,6 +182,7 @@ struct MPlan {
     int nb;                // tiles per edge
     int nqb;               // 32-column blocks of [Z | 1] (Q + 1 columns)
     int DSFs;              // symmetric gradient: the same stride, >= 2 gram_t(nk) and >= Q
+    int grb;               // symmetric gradient: rows per staged batch (0: not used)
                            // (odd; lanes past Q read the next row, see lds_sym_layout)
     int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= 2
                            // gram_t(nk) and >= 32 nqb, so that no read needs a bounds test)
@@ -326,13 +327,14 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
 //                       contiguous (kXS > 32 spreads the rows over the LDS banks)
 //   bb, bcb, t1 [RB][Mp]   b, b + c and dL/dPsi1 * Psi1 of the batch, every column
 //   mub, kb, w1b, w2b [RB][64] (zero past Q), sc [RB] (padded to 4), red [RB][nb][5Q + 2]
-constexpr int kSymRB = 4;   // symmetric gradient: rows per batch
+// RB, the rows per staged batch, is 8 where the tables fit and 4 otherwise.
+constexpr int kSymRBMax = 8;
 constexpr int kXS = 36;     // halves per row of an exchanged tile
 struct LdsS {
     int zx, zb, za, xw, bb, bcb, t1, mub, kb, w1b, w2b, sc, red, total;
 };
 
-__host__ __device__ inline LdsS lds_sym_layout(int nb, int DSF, int Q, int nk) {
+__host__ __device__ inline LdsS lds_sym_layout(int nb, int DSF, int Q, int nk, int rb) {
     LdsS L{};
     int o = 0;
     const int Mp = nb * kTile;
@@ -340,15 +342,15 @@ __host__ __device__ inline LdsS lds_sym_layout(int nb, int DSF, int Q, int nk) {
     L.zb = o; o += nb * 2 * 2 * 2 * 32 * 8 / 2;
     L.za = o; o += nb * nk * 2 * 32 * 8 / 2;
     L.xw = o; o += nb * 2 * 32 * kXS / 2;
-    L.bb = o; o += kSymRB * Mp;
-    L.bcb = o; o += kSymRB * Mp;
-    L.t1 = o; o += kSymRB * Mp;
-    L.mub = o; o += kSymRB * kRowStride;
-    L.kb = o; o += kSymRB * kRowStride;
-    L.w1b = o; o += kSymRB * kRowStride;
-    L.w2b = o; o += kSymRB * kRowStride;
-    L.sc = o; o += 4;
-    L.red = o; o += kSymRB * nb * (5 * Q + 2);
+    L.bb = o; o += rb * Mp;
+    L.bcb = o; o += rb * Mp;
+    L.t1 = o; o += rb * Mp;
+    L.mub = o; o += rb * kRowStride;
+    L.kb = o; o += rb * kRowStride;
+    L.w1b = o; o += rb * kRowStride;
+    L.w2b = o; o += rb * kRowStride;
+    L.sc = o; o += (rb + 3) / 4 * 4;
+    L.red = o; o += rb * nb * (5 * Q + 2);
     L.total = o;
     return L;
 }
@@ -392,9 +394,14 @@ MPlan make_mplan(const Shape &s) {
     p.fchunks = cdiv(s.N, p.frows);
     // symmetric gradient kernel (one workgroup of nb waves per row chunk) where
     // [Z | 1] is one column block, Mp <= 256 and its tables fit in LDS
-    p.gsym = p.nqb == 1 && p.nb <= 8 && p.nk > 0 &&
-             sizeof(float) * lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1)).total <=
-                 (size_t)kLdsBytes;
+    // (batches of 8 rows where those tables fit, else 4)
+    p.grb = 0;
+    for (int rb : {kSymRBMax, kSymRBMax / 2})
+        if (p.grb == 0 && p.nqb == 1 && p.nb <= 8 && p.nk > 0 &&
+            sizeof(float) * lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1), rb).total <=
+                (size_t)kLdsBytes)
+            p.grb = rb;
+    p.gsym = p.grb > 0;
     if (p.gsym) {
         p.jpw = p.nb;
         p.njr = 1;
@@ -411,7 +418,7 @@ MPlan make_mplan(const Shape &s) {
     p.igroups = (int)cdiv(p.nb, p.wpg);
     p.ggroups = (int64_t)p.njr * p.igroups;
     p.lds_grad = sizeof(float) *
-                 (p.gsym ? lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1)).total
+                 (p.gsym ? lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1), p.grb).total
                          : lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk, p.wpg).total);
     // two full rounds: workgroups per CU limited by LDS and by the waves per CU
     // the kernel's register count allows (two per SIMD; one per SIMD for the
@@ -1827,7 +1834,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 // addressed), which gives the A operand of V'_j += W^T [Z_w | 1] with no VALU
 // work.  At nb = 8 a row takes 40 tiles instead of 64 and 8 epilogues instead
 // of 16, for 24 tile exchanges and two barriers per round.
-template <int NK>
+template <int NK, int RB>
 __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
     int64_t N, int M, int Q, int Mp, int nb, int DSF, int64_t rows_per_chunk,
     const float *__restrict__ mu, const float *__restrict__ Z, const float *__restrict__ zc,
@@ -1840,7 +1847,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
     typedef __attribute__((address_space(3))) v4s lds_v4s;
     extern __shared__ float lds[];
     if (route[0]) return;
-    const LdsS L = lds_sym_layout(nb, DSF, Q, NK);
+    const LdsS L = lds_sym_layout(nb, DSF, Q, NK, RB);
     constexpr int GT = gram_t(NK);
     constexpr int KT = 5;                      // tile slots: 0 diagonal, 1 .. 3 rounds, 4 shared
     _Float16 *zh = reinterpret_cast<_Float16 *>(lds + L.zb);
@@ -1891,23 +1898,35 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
     const int xr_row = 4 * g + ((lane >> 2) & 3);
     const int xr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-    const int BT = kSymRB * Mp;                // row-table entries of a batch
+    // RB Mp = RB 32 nb row-table entries per batch over 64 nb threads: RB / 2 each
+    constexpr int PT = RB / 2;
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
     const int tid = threadIdx.x, nthr = blockDim.x;
-    for (int64_t n0 = r0; n0 < r1; n0 += kSymRB) {
-        const int cb = (int)min<int64_t>(kSymRB, r1 - n0);
+    for (int64_t n0 = r0; n0 < r1; n0 += RB) {
+        const int cb = (int)min<int64_t>(RB, r1 - n0);
         __syncthreads();
-        // batch tables (clamped loads, issued before the writes)
-        for (int k = tid; k < BT; k += nthr) {
-            const int rr = min(k / Mp, cb - 1);
-            const int64_t o = (n0 + rr) * Mp + (k - (k / Mp) * Mp);
-            const float vb = bt[o], vc = bc[o], vt = t1g[o];
-            lds[L.bb + k] = vb;
-            lds[L.bcb + k] = vc;
-            lds[L.t1 + k] = vt;
+        // batch tables (clamped loads, all issued before the writes)
+        {
+            float vb[PT], vc[PT], vt[PT];
+#pragma unroll
+            for (int i = 0; i < PT; ++i) {
+                const int k = tid + i * nthr;
+                const int rr = min(k / Mp, cb - 1);
+                const int64_t o = (n0 + rr) * Mp + (k - (k / Mp) * Mp);
+                vb[i] = bt[o];
+                vc[i] = bc[o];
+                vt[i] = t1g[o];
+            }
+#pragma unroll
+            for (int i = 0; i < PT; ++i) {
+                const int k = tid + i * nthr;
+                lds[L.bb + k] = vb[i];
+                lds[L.bcb + k] = vc[i];
+                lds[L.t1 + k] = vt[i];
+            }
         }
-        for (int k = tid; k < kSymRB * kRowStride; k += nthr) {
+        for (int k = tid; k < RB * kRowStride; k += nthr) {
             const int r = k / kRowStride, q = k - r * kRowStride;
             const float ok = (r < cb && q < Q) ? 1.f : 0.f;
             const int qc = min(q, Q - 1);
@@ -1919,7 +1938,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
             lds[L.w1b + k] = ok * v1;
             lds[L.w2b + k] = ok * v2;
         }
-        if (tid < kSymRB) {
+        if (tid < RB) {
             float sc = 0.f;
             if (tid < cb) {
                 const float phl = hl[n0 + tid];
@@ -2254,10 +2273,10 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
     return hipGetLastError();
 }
 
-template <int NK>
+template <int NK, int RB>
 hipError_t launch_grad_sym(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                            const Hyp<float> &h, const int *route, void *ws, hipStream_t st) {
-    auto k = psi2_grad_sym_kernel<NK>;
+    auto k = psi2_grad_sym_kernel<NK, RB>;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_grad);
     if (e != hipSuccess) return e;
@@ -2310,8 +2329,9 @@ hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const f
 hipError_t dispatch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                          const Hyp<float> &h, const int *route, void *ws, hipStream_t st) {
     if (p.gsym) {
-#define GPPS_GS(I) \
-    if (p.nk == I) return launch_grad_sym<I>(p, s, mu, Z, h, route, ws, st);
+#define GPPS_GS(I)                                                                 \
+    if (p.nk == I && p.grb == kSymRBMax) return launch_grad_sym<I, kSymRBMax>(p, s, mu, Z, h, route, ws, st); \
+    if (p.nk == I && p.grb == kSymRBMax / 2) return launch_grad_sym<I, kSymRBMax / 2>(p, s, mu, Z, h, route, ws, st);
         GPPS_GS(1) GPPS_GS(2) GPPS_GS(3) GPPS_GS(4) GPPS_GS(6) GPPS_GS(8)
 #undef GPPS_GS
         return hipErrorInvalidValue;

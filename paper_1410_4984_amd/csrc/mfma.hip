@@ -327,7 +327,7 @@ __host__ __device__ inline LdsG lds_grad_layout(int Mp, int DSF, int Q, int nqb,
 //                       contiguous (kXS > 32 spreads the rows over the LDS banks)
 //   bb, bcb, t1 [RB][Mp]   b, b + c and dL/dPsi1 * Psi1 of the batch, every column
 //   mub, kb, w1b, w2b [RB][64] (zero past Q), sc [RB] (padded to 4), red [RB][nb][5Q + 2]
-// RB, the rows per staged batch, is 8 where the tables fit and 4 otherwise.
+// RB, the rows per staged batch, is 8 where the tables fit and nb >= 5, 4 otherwise.
 constexpr int kSymRBMax = 8;
 constexpr int kXS = 36;     // halves per row of an exchanged tile
 struct LdsS {
@@ -394,10 +394,12 @@ MPlan make_mplan(const Shape &s) {
     p.fchunks = cdiv(s.N, p.frows);
     // symmetric gradient kernel (one workgroup of nb waves per row chunk) where
     // [Z | 1] is one column block, Mp <= 256 and its tables fit in LDS
-    // (batches of 8 rows where those tables fit, else 4)
+    // (batches of 8 rows where those tables fit and nb >= 5, else 4: measured on
+    // the gradient call at N = 100000, Q = 20, eight rows take 1-6% off at nb = 5
+    // to 8 and add 40% at nb = 4, at M = 128 and at the 50000 x 100 x 10 shape)
     p.grb = 0;
     for (int rb : {kSymRBMax, kSymRBMax / 2})
-        if (p.grb == 0 && p.nqb == 1 && p.nb <= 8 && p.nk > 0 &&
+        if (p.grb == 0 && (rb < kSymRBMax || p.nb >= 5) && p.nqb == 1 && p.nb <= 8 && p.nk > 0 &&
             sizeof(float) * lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1), rb).total <=
                 (size_t)kLdsBytes)
             p.grb = rb;
@@ -420,14 +422,15 @@ MPlan make_mplan(const Shape &s) {
     p.lds_grad = sizeof(float) *
                  (p.gsym ? lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1), p.grb).total
                          : lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk, p.wpg).total);
-    // two full rounds: workgroups per CU limited by LDS and by the waves per CU
-    // the kernel's register count allows (two per SIMD; one per SIMD for the
-    // wide [Z | 1] of psi2_grad_kernel)
+    // full rounds of workgroups (per CU: limited by LDS and by the waves per CU
+    // the kernel's register count allows, two per SIMD; one per SIMD for the
+    // wide [Z | 1] of psi2_grad_kernel): one round for the symmetric kernel (its
+    // eight-wave workgroups fill a CU alone), two for psi2_grad_kernel
     const int64_t gwaves = p.gsym ? 8 : grad_waves(p.nqb);
     const int64_t gslots = kCUs * std::max<int64_t>(
                                       1, std::min<int64_t>(kLdsBytes / p.lds_grad,
                                                            gwaves / p.wpg));
-    p.gchunks = std::max<int64_t>(1, std::min(2 * gslots / p.ggroups, cdiv(s.N, 16)));
+    p.gchunks = std::max<int64_t>(1, std::min((p.gsym ? 1 : 2) * gslots / p.ggroups, cdiv(s.N, 16)));
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
     p.fin_blocks = cdiv(s.N, kFinRows);
@@ -1906,8 +1909,10 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
     for (int64_t n0 = r0; n0 < r1; n0 += RB) {
         const int cb = (int)min<int64_t>(RB, r1 - n0);
         __syncthreads();
-        // batch tables (clamped loads, all issued before the writes)
-        {
+        // batch tables (clamped loads): with eight-row batches each thread's loads
+        // are all issued before its writes; four-row batches keep the plain loop
+        // (fewer registers held across it, no spill reloads in the row loop)
+        if constexpr (RB == kSymRBMax) {
             float vb[PT], vc[PT], vt[PT];
 #pragma unroll
             for (int i = 0; i < PT; ++i) {
@@ -1924,6 +1929,15 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
                 lds[L.bb + k] = vb[i];
                 lds[L.bcb + k] = vc[i];
                 lds[L.t1 + k] = vt[i];
+            }
+        } else {
+            for (int k = tid; k < RB * Mp; k += nthr) {
+                const int rr = min(k / Mp, cb - 1);
+                const int64_t o = (n0 + rr) * Mp + (k - (k / Mp) * Mp);
+                const float vb = bt[o], vc = bc[o], vt = t1g[o];
+                lds[L.bb + k] = vb;
+                lds[L.bcb + k] = vc;
+                lds[L.t1 + k] = vt;
             }
         }
         for (int k = tid; k < RB * kRowStride; k += nthr) {

@@ -424,13 +424,13 @@ MPlan make_mplan(const Shape &s) {
                          : lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk, p.wpg).total);
     // full rounds of workgroups (per CU: limited by LDS and by the waves per CU
     // the kernel's register count allows, two per SIMD; one per SIMD for the
-    // wide [Z | 1] of psi2_grad_kernel): one round for the symmetric kernel (its
-    // eight-wave workgroups fill a CU alone), two for psi2_grad_kernel
+    // wide [Z | 1] of psi2_grad_kernel): one round for the symmetric kernel and
+    // for eight-wave workgroups (which fill a CU alone), else two
     const int64_t gwaves = p.gsym ? 8 : grad_waves(p.nqb);
     const int64_t gslots = kCUs * std::max<int64_t>(
                                       1, std::min<int64_t>(kLdsBytes / p.lds_grad,
                                                            gwaves / p.wpg));
-    p.gchunks = std::max<int64_t>(1, std::min((p.gsym ? 1 : 2) * gslots / p.ggroups, cdiv(s.N, 16)));
+    p.gchunks = std::max<int64_t>(1, std::min((p.gsym || p.wpg >= 8 ? 1 : 2) * gslots / p.ggroups, cdiv(s.N, 16)));
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
     p.fin_blocks = cdiv(s.N, kFinRows);

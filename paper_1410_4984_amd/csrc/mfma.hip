@@ -387,7 +387,10 @@ MPlan make_mplan(const Shape &s) {
     // round idles most CUs: 6 per CU is two rounds at three workgroups per CU and
     // three at two (the register counts of the instances allow two or three)
     // (the symmetric forward's register count allows two per CU: one round)
-    const int64_t fslots = p.fsym ? kCUs * std::min<int64_t>(2, std::max<int64_t>(1, kLdsBytes / p.lds_fwd))
+    // (two rounds when its tiles are split into two ranges, whose workgroups differ
+    // in length: 4.95 -> 4.85 ms per stress chunk; one round is faster at large)
+    const int64_t fslots = p.fsym ? (fsym_ranges(p.nb) > 1 ? 2 : 1) * kCUs *
+                                        std::min<int64_t>(2, std::max<int64_t>(1, kLdsBytes / p.lds_fwd))
                                   : kCUs * std::min<int64_t>(6, 2 * std::max<int64_t>(1, kLdsBytes / p.lds_fwd));
     p.fchunks = std::max<int64_t>(1, std::min(fslots / p.fgroups, cdiv(s.N, 32)));
     p.frows = cdiv(s.N, p.fchunks);

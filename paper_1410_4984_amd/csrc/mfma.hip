@@ -2075,28 +2075,22 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
             float X = 0.f, Y = 0.f, P = 0.f, X1 = 0.f, P1 = 0.f, R = 0.f, T1 = 0.f;
             const float *zblk = lds + L.zx + w * kTile * DSF;
             const float *t1r = lds + L.t1 + r * Mp + w * kTile;
+            // with the Psi1 terms of (n, m), t = dL/dPsi1 * Psi1, for the same rows
 #pragma unroll
             for (int t = 0; t < 16; ++t) {
                 const int rr = crow(t, g);
                 const float rt = __int_as_float(__builtin_amdgcn_ds_bpermute(ones_src * 4, __float_as_int(V[t])));
+                const float tv = t1r[rr];
                 R += rt;
+                T1 += tv;
                 const float d = muq - zblk[rr * DSF + c];
                 const float v = fmaf(rt, muq, -V[t]);
                 const float dr = d * rt;
-                dz[t] = fmaf(alpha, v, fmaf(beta, dr, dz[t]));
+                const float td = tv * d;
+                dz[t] = fmaf(alpha, v, fmaf(beta, dr, fmaf(td, w1q, dz[t])));
                 X = fmaf(dr, d, X);
                 P += dr;
                 Y = fmaf(d, v, Y);
-            }
-            // Psi1 terms of (n, m), t = dL/dPsi1 * Psi1, for the rows of block w
-#pragma unroll
-            for (int t = 0; t < 16; ++t) {
-                const int rr = crow(t, g);
-                const float tv = t1r[rr];
-                T1 += tv;
-                const float d = muq - zblk[rr * DSF + c];
-                const float td = tv * d;
-                dz[t] = fmaf(td, w1q, dz[t]);
                 X1 = fmaf(td, d, X1);
                 P1 += td;
             }

@@ -83,6 +83,8 @@
 // are bitwise reproducible.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include <cmath>
 
 #include "internal.h"
@@ -1740,42 +1742,44 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             for (int qb = 0; qb < NQB; ++qb) X[qb] = Y[qb] = P[qb] = X1[qb] = P1[qb] = 0.f;
             const float *zblk = lds + L.zx + wave * kTile * DSF;
             const float *t1r = lds + L.t1 + r * BW + wave * kTile;
-#pragma unroll
-            for (int t = 0; t < 16; ++t) {
-                const int rr = crow(t, g);
-                const float rt = __int_as_float(__builtin_amdgcn_ds_bpermute(
-                    ones_src * 4, __float_as_int(ones_qb == 0 ? V[0][t] : V[NQB - 1][t])));
-                R += rt;
-#pragma unroll
-                for (int qb = 0; qb < NQB; ++qb) {
-                    const int q = qb * 32 + c;
-                    const float d = muq[qb] - zblk[rr * DSF + q];
-                    const float v = fmaf(rt, muq[qb], -V[qb][t]);
-                    const float dr = d * rt;
-                    dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, dz[qb][t]));
-                    X[qb] = fmaf(dr, d, X[qb]);
-                    P[qb] += dr;
-                    Y[qb] = fmaf(d, v, Y[qb]);
-                }
-            }
-            if (has1) {
-                // Psi1 terms of (n, m), t = dL/dPsi1 * Psi1, for the rows of block i
+            // one pass over the rows of block i, with the Psi1 terms of (n, m),
+            // t = dL/dPsi1 * Psi1, where this task adds them (d formed once)
+            auto epilogue = [&](auto psi1) {
 #pragma unroll
                 for (int t = 0; t < 16; ++t) {
                     const int rr = crow(t, g);
-                    const float tv = t1r[rr];
-                    T1 += tv;
+                    const float rt = __int_as_float(__builtin_amdgcn_ds_bpermute(
+                        ones_src * 4, __float_as_int(ones_qb == 0 ? V[0][t] : V[NQB - 1][t])));
+                    R += rt;
+                    float tv = 0.f;
+                    if constexpr (decltype(psi1)::value) {
+                        tv = t1r[rr];
+                        T1 += tv;
+                    }
 #pragma unroll
                     for (int qb = 0; qb < NQB; ++qb) {
                         const int q = qb * 32 + c;
                         const float d = muq[qb] - zblk[rr * DSF + q];
-                        const float td = tv * d;
-                        dz[qb][t] = fmaf(td, w1q[qb], dz[qb][t]);
-                        X1[qb] = fmaf(td, d, X1[qb]);
-                        P1[qb] += td;
+                        const float v = fmaf(rt, muq[qb], -V[qb][t]);
+                        const float dr = d * rt;
+                        if constexpr (decltype(psi1)::value) {
+                            const float td = tv * d;
+                            dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, fmaf(td, w1q[qb], dz[qb][t])));
+                            X1[qb] = fmaf(td, d, X1[qb]);
+                            P1[qb] += td;
+                        } else {
+                            dz[qb][t] = fmaf(alpha[qb], v, fmaf(beta[qb], dr, dz[qb][t]));
+                        }
+                        X[qb] = fmaf(dr, d, X[qb]);
+                        P[qb] += dr;
+                        Y[qb] = fmaf(d, v, Y[qb]);
                     }
                 }
-            }
+            };
+            if (has1)
+                epilogue(std::true_type{});
+            else
+                epilogue(std::false_type{});
             // combine the two lane halves, publish this wave's sums for row r
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb) {

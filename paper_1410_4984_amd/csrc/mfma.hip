@@ -400,8 +400,9 @@ MPlan make_mplan(const Shape &s) {
     // symmetric gradient kernel (one workgroup of nb waves per row chunk) where
     // [Z | 1] is one column block, Mp <= 256 and its tables fit in LDS
     // (batches of 8 rows where those tables fit and nb >= 5, else 4: measured on
-    // the gradient call at N = 100000, Q = 20, eight rows take 1-6% off at nb = 5
-    // to 8 and add 40% at nb = 4, at M = 128 and at the 50000 x 100 x 10 shape)
+    // the gradient call at N = 100000, eight rows take 1-6% off at nb = 5 to 8
+    // where they fit (Q = 20 up to nb = 7, Q <= 10 at nb = 8; at nb = 8 and Q = 20
+    // they do not) and add 40% at nb = 4, at M = 128 and at 50000 x 100 x 10)
     p.grb = 0;
     for (int rb : {kSymRBMax, kSymRBMax / 2})
         if (p.grb == 0 && (rb < kSymRBMax || p.nb >= 5) && p.nqb == 1 && p.nb <= 8 && p.nk > 0 &&

@@ -525,9 +525,12 @@ def test_mfma_gram_layout_dimensions(Q):
 # every block pair; odd nb has (nb - 1) / 2 exchange rounds and no shared tile,
 # even nb one shared tile): nb = 5, 7 (two and three rounds), 7 at Q = 30
 # (its tables fill 159.9 of the 160 KB of LDS), 8 with a partial last block, 6;
-# N leaves partial batches of rows at the ends of the row chunks.
+# N leaves partial batches of rows at the ends of the row chunks.  Batches are
+# eight rows at nb >= 5 where the tables fit (150 x 9, 150 x 30, 200 x 20,
+# 180 x 14, and nb = 8 at Q = 10 and Q = 4), four otherwise.
 @pytest.mark.parametrize("N,M,Q", [(301, 150, 9), (333, 150, 30), (299, 200, 20),
-                                   (257, 200, 30), (311, 250, 20), (205, 180, 14)])
+                                   (257, 200, 30), (311, 250, 20), (205, 180, 14),
+                                   (263, 256, 10), (250, 240, 4)])
 def test_mfma_symmetric_block_counts(N, M, Q):
     use_path("mfma", torch.float32)
     say(f"[symmetric gradient N={N} M={M} Q={Q}]")

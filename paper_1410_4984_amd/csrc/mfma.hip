@@ -242,6 +242,7 @@ __host__ __device__ inline LdsF lds_fwd_layout(int Mp, int nk, int tpw) {
 // waves read.
 constexpr int kFSymSlots = 5;
 constexpr int kFSymWindow = 8;
+constexpr int kFSRB = 8;    // rows per batch (prefetched a batch ahead)
 __host__ __device__ inline int fsym_tiles(int nb, int w) {
     return 1 + (nb - 1) / 2 + ((nb > 1 && (nb & 1) == 0 && w < nb / 2) ? 1 : 0);
 }
@@ -270,10 +271,10 @@ __host__ __device__ inline LdsFS lds_fsym_layout(int nzb, int nk) {
     LdsFS L{};
     int o = 0;
     L.za = o; o += nzb * nk * 2 * 32 * 8 / 2;
-    L.bb = o; o += kFRB * nzb * kTile;
-    L.bcb = o; o += kFRB * kWaves * kTile;
-    L.mub = o; o += kFRB * kRowStride;
-    L.kb = o; o += kFRB * kRowStride;
+    L.bb = o; o += kFSRB * nzb * kTile;
+    L.bcb = o; o += kFSRB * kWaves * kTile;
+    L.mub = o; o += kFSRB * kRowStride;
+    L.kb = o; o += kFSRB * kRowStride;
     L.total = o > 2 * 32 * 33 ? o : 2 * 32 * 33;   // also the shared tiles' hand-over
     return L;
 }
@@ -1261,7 +1262,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
 // block and range instead of one per task.  A tile with j < w is the transpose of
 // tile (j, w) and is stored transposed; the reduce kernel is unchanged.  A
 // workgroup (four column blocks, one range: blockIdx.x = group + groups * range)
-// stages the Gram A operands of its window of blocks and, per batch of kFRB rows,
+// stages the Gram A operands of its window of blocks and, per batch of kFSRB rows,
 // the window's row terms b and the b + c of its own column blocks (the next batch
 // prefetched into registers while this one is computed).
 template <int NK>
@@ -1319,47 +1320,56 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
     }
 
     // batch tables, prefetched one batch ahead from clamped addresses (entries of
-    // rows >= cb and of blocks past the edge are never read): kFRB rows of b for
-    // the window (32 nzb each, at most 4 per thread), of b + c for the
-    // workgroup's column blocks (2 per thread) and of mu, K (one each)
+    // rows >= cb and of blocks past the edge are never read): kFSRB rows of b for
+    // the window (32 nzb each, at most PB per thread), of b + c for the
+    // workgroup's column blocks (PC per thread) and of mu, K (PM each)
+    constexpr int PB = kFSRB * kFSymWindow * kTile / kThreads;
+    constexpr int PC = kFSRB * kWaves * kTile / kThreads;
+    constexpr int PM = kFSRB * kRowStride / kThreads;
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
     const int64_t r1 = min(N, r0 + rows_per_chunk);
     const int tid = threadIdx.x;
-    const int WB = nzb * kTile, BB = kFRB * WB;
-    float pb[4], pc[2], pmu, pk;
+    const int WB = nzb * kTile, BB = kFSRB * WB;
+    float pb[PB], pc[PC], pmu[PM], pk[PM];
     auto load = [&](int64_t n0) {
-        const int cb = (int)min<int64_t>(kFRB, r1 - n0);
+        const int cb = (int)min<int64_t>(kFSRB, r1 - n0);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < PB; ++i) {
             const int e = min(tid + i * kThreads, BB - 1), r = e / WB, x = e - r * WB;
             const int blk = jbase + x / kTile;
             pb[i] = bt[(n0 + min(r, cb - 1)) * Mp + (blk >= nb ? blk - nb : blk) * kTile + x % kTile];
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < PC; ++i) {
             const int e = tid + i * kThreads, r = e / (kWaves * kTile), x = e - r * (kWaves * kTile);
             pc[i] = bc[(n0 + min(r, cb - 1)) * Mp + min(slot_block(x / kTile), nb - 1) * kTile + x % kTile];
         }
-        const int r = tid / kRowStride, q = tid - r * kRowStride;
-        const float ok = (r < cb && q < Q) ? 1.f : 0.f;
-        const int qc = min(q, Q - 1);
-        const int64_t rc = n0 + min(r, cb - 1);
-        pmu = ok * (mu[rc * Q + qc] - zc[qc]);
-        pk = ok * Kt[rc * kRowStride + qc];
+#pragma unroll
+        for (int i = 0; i < PM; ++i) {
+            const int e = tid + i * kThreads, r = e / kRowStride, q = e - r * kRowStride;
+            const float ok = (r < cb && q < Q) ? 1.f : 0.f;
+            const int qc = min(q, Q - 1);
+            const int64_t rc = n0 + min(r, cb - 1);
+            pmu[i] = ok * (mu[rc * Q + qc] - zc[qc]);
+            pk[i] = ok * Kt[rc * kRowStride + qc];
+        }
     };
     if (r0 < r1) load(r0);
-    for (int64_t n0 = r0; n0 < r1; n0 += kFRB) {
-        const int cb = (int)min<int64_t>(kFRB, r1 - n0);
+    for (int64_t n0 = r0; n0 < r1; n0 += kFSRB) {
+        const int cb = (int)min<int64_t>(kFSRB, r1 - n0);
         __syncthreads();
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < PB; ++i)
             if (tid + i * kThreads < BB) lds[L.bb + tid + i * kThreads] = pb[i];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) lds[L.bcb + tid + i * kThreads] = pc[i];
-        lds[L.mub + tid] = pmu;
-        lds[L.kb + tid] = pk;
+        for (int i = 0; i < PC; ++i) lds[L.bcb + tid + i * kThreads] = pc[i];
+#pragma unroll
+        for (int i = 0; i < PM; ++i) {
+            lds[L.mub + tid + i * kThreads] = pmu[i];
+            lds[L.kb + tid + i * kThreads] = pk[i];
+        }
         __syncthreads();
-        if (n0 + kFRB < r1) load(n0 + kFRB);
+        if (n0 + kFSRB < r1) load(n0 + kFSRB);
         if (!active) continue;
         for (int r = 0; r < cb; ++r) {
             v8h B[NK];

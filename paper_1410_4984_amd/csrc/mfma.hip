@@ -443,7 +443,7 @@ MPlan make_mplan(const Shape &s) {
     p.fin_blocks = cdiv(s.N, kFinRows);
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
-    p.off_K = take(sizeof(float) * s.N * kRowStride);
+    p.off_K = take(sizeof(float) * s.N * s.Q);
     p.off_hq = take(sizeof(float) * s.N * s.Q);
     p.off_w2 = take(sizeof(float) * s.N * s.Q);
     p.off_hl = take(sizeof(float) * s.N);
@@ -517,7 +517,7 @@ __global__ __launch_bounds__(256) void mfma_centre_kernel(int M, int Q,
 
 // Per-row tables, 64 datapoints per workgroup.  For every (n, q), with
 // w2 = 1/(l^2 + 2S):
-//   K[n][q]  = -log2e/2 w2 / s_q  (row stride 64; entries q >= Q are never read)
+//   K[n][q]  = -log2e/2 w2 / s_q
 //   hq[n][q] = -log2e/4 w2,  w2[n][q],  w1[n][q] = 1/(l^2 + S)
 // (one pass over the workgroup's (row, dimension) pairs, coalesced), then per row
 //   hl[n]    = log2e (log sf2 - 1/4 sum_q log(1 + 2S/l^2))   (Psi2 prefactor, half of it)
@@ -545,7 +545,7 @@ __global__ __launch_bounds__(256) void mfma_rows_kernel(
         const float am = fabsf(mu[k] - zt[q]), R = zt[3 * Q + q];
         const float l2 = h.l2[q];
         const float w2 = 1.f / (l2 + 2.f * sv);
-        Kt[(n0 + r) * kRowStride + q] = -0.5f * kLog2e * w2 * zt[Q + q];
+        Kt[k] = -0.5f * kLog2e * w2 * zt[Q + q];
         hq[k] = -0.25f * kLog2e * w2;
         w2t[k] = w2;
         w1t[k] = 1.f / (l2 + sv);
@@ -1179,7 +1179,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_kernel(
         const int r = tid / kRowStride, q = tid - r * kRowStride;
         const bool ok = r < cb && q < Q;
         pf_mu = ok ? mu[(n0 + r) * Q + q] - zc[q] : 0.f;
-        pf_k = ok ? Kt[(n0 + r) * kRowStride + q] : 0.f;
+        pf_k = ok ? Kt[(n0 + r) * Q + q] : 0.f;
     };
     if (r0 < r1) load(r0);
     for (int64_t n0 = r0; n0 < r1; n0 += kFRB) {
@@ -1351,7 +1351,7 @@ __global__ __launch_bounds__(kThreads, 2) void psi2_fwd_sym_kernel(
             const int qc = min(q, Q - 1);
             const int64_t rc = n0 + min(r, cb - 1);
             pmu[i] = ok * (mu[rc * Q + qc] - zc[qc]);
-            pk[i] = ok * Kt[rc * kRowStride + qc];
+            pk[i] = ok * Kt[rc * Q + qc];
         }
     };
     if (r0 < r1) load(r0);
@@ -1628,7 +1628,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             const bool okr = tid < kRB * kRowStride && r < cb && q < Q;
             if (okr) {
                 pmu = mu[(n0 + r) * Q + q] - zc[q];
-                pk = Kt[(n0 + r) * kRowStride + q];
+                pk = Kt[(n0 + r) * Q + q];
                 pw1 = w1t[(n0 + r) * Q + q];
                 pw2 = w2t[(n0 + r) * Q + q];
             }
@@ -1663,7 +1663,7 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             const int r = k / kRowStride, q = k - r * kRowStride;
             const bool ok = r < cb && q < Q;
             lds[L.mub + k] = ok ? mu[(n0 + r) * Q + q] - zc[q] : 0.f;
-            lds[L.kb + k] = ok ? Kt[(n0 + r) * kRowStride + q] : 0.f;
+            lds[L.kb + k] = ok ? Kt[(n0 + r) * Q + q] : 0.f;
             lds[L.w1b + k] = ok ? w1t[(n0 + r) * Q + q] : 0.f;
             lds[L.w2b + k] = ok ? w2t[(n0 + r) * Q + q] : 0.f;
         }
@@ -1963,7 +1963,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
             const float ok = (r < cb && q < Q) ? 1.f : 0.f;
             const int qc = min(q, Q - 1);
             const int64_t rc = n0 + min(r, cb - 1);
-            const float vm = mu[rc * Q + qc] - zc[qc], vk = Kt[rc * kRowStride + qc],
+            const float vm = mu[rc * Q + qc] - zc[qc], vk = Kt[rc * Q + qc],
                         v1 = w1t[rc * Q + qc], v2 = w2t[rc * Q + qc];
             lds[L.mub + k] = ok * vm;
             lds[L.kb + k] = ok * vk;

@@ -185,6 +185,10 @@ struct MPlan {
     int nqb;               // 32-column blocks of [Z | 1] (Q + 1 columns)
     int DSFs;              // symmetric gradient: the same stride, >= 2 gram_t(nk) and >= Q
     int grb;               // symmetric gradient: rows per staged batch (0: not used)
+    bool gsplit;           // 13 <= nb <= 16: symmetric kernel on each half, tile kernel across
+    int64_t sgrows, sgchunks;  // ... the halves' row chunks
+    size_t lds_sym;        // ... the first half's LDS
+    int64_t dzslabs;       // dZ slabs of M x Q summed by the final reduction
                            // (odd; lanes past Q read the next row, see lds_sym_layout)
     int DSF;               // gradient: LDS row stride of the fp32 z table (odd, >= 2
                            // gram_t(nk) and >= 32 nqb, so that no read needs a bounds test)
@@ -426,6 +430,31 @@ MPlan make_mplan(const Shape &s) {
     }
     p.igroups = (int)cdiv(p.nb, p.wpg);
     p.ggroups = (int64_t)p.njr * p.igroups;
+    // 13 <= nb <= 16 with [Z | 1] one column block: the symmetric kernel on blocks
+    // 0 .. 7 and on 8 .. nb - 1 (one workgroup each per row chunk, every unordered
+    // tile within a half once) and the tile kernel on the tiles between the
+    // halves only (row blocks of one half against the column ranges of the
+    // other: four workgroups of eight waves); 208 tiles per row at nb = 16
+    // instead of 256.  Row sums: the halves in groups 0, 1, the tile kernel's in
+    // 2 .. 5; dZ slabs: one per half-chunk, then two per tile-kernel chunk.
+    // Measured on the gradient call at N = 100000 against the tile kernel alone:
+    // 13-17% faster at nb = 13 to 16 (M = 416 .. 512, Q = 8 .. 20), 2-4% slower
+    // at nb = 10 and 12, whose second half's workgroup has only 2 or 4 waves; at
+    // Q = 30 the halves' tables do not fit.
+    p.gsplit = false;
+    if (!p.gsym && p.nqb == 1 && p.nb >= 13 && p.nb <= 16 && p.nk > 0 && p.jpw == 4 &&
+        p.wpg == 8 && p.njr == (int)cdiv(p.nb, 4)) {
+        int rb = 0;
+        for (int r : {kSymRBMax, kSymRBMax / 2})
+            if (rb == 0 && sizeof(float) * lds_sym_layout(8, p.DSFs, (int)s.Q, p.nk, r).total <=
+                               (size_t)kLdsBytes)
+                rb = r;
+        if (rb > 0) {
+            p.gsplit = true;
+            p.grb = rb;
+            p.lds_sym = sizeof(float) * lds_sym_layout(8, p.DSFs, (int)s.Q, p.nk, rb).total;
+        }
+    }
     p.lds_grad = sizeof(float) *
                  (p.gsym ? lds_sym_layout(p.nb, p.DSFs, (int)s.Q, std::max(p.nk, 1), p.grb).total
                          : lds_grad_layout((int)p.Mp, p.DSF, (int)s.Q, p.nqb, p.nk, p.wpg).total);
@@ -437,9 +466,19 @@ MPlan make_mplan(const Shape &s) {
     const int64_t gslots = kCUs * std::max<int64_t>(
                                       1, std::min<int64_t>(kLdsBytes / p.lds_grad,
                                                            gwaves / p.wpg));
-    p.gchunks = std::max<int64_t>(1, std::min((p.gsym || p.wpg >= 8 ? 1 : 2) * gslots / p.ggroups, cdiv(s.N, 16)));
+    const int64_t tgroups = p.gsplit ? 4 : p.ggroups;   // tile-kernel workgroups per chunk
+    p.gchunks = std::max<int64_t>(1, std::min((p.gsym || p.wpg >= 8 ? 1 : 2) * gslots / tgroups, cdiv(s.N, 16)));
     p.grows = cdiv(s.N, p.gchunks);
     p.gchunks = cdiv(s.N, p.grows);
+    p.dzslabs = p.gchunks * p.njr;
+    if (p.gsplit) {
+        // each half: one round of one-workgroup-per-CU chunks
+        p.sgchunks = std::max<int64_t>(1, std::min<int64_t>(kCUs, cdiv(s.N, 16)));
+        p.sgrows = cdiv(s.N, p.sgchunks);
+        p.sgchunks = cdiv(s.N, p.sgrows);
+        p.ggroups = 6;
+        p.dzslabs = p.sgchunks + 2 * p.gchunks;
+    }
     p.fin_blocks = cdiv(s.N, kFinRows);
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
@@ -456,7 +495,7 @@ MPlan make_mplan(const Shape &s) {
     p.off_g2 = take(sizeof(float) * p.Mp * p.Mp);
     p.off_fp = take(sizeof(float) * p.fchunks * p.T * kTile * kTile);
     p.off_rs = take(sizeof(float) * p.ggroups * s.N * (5 * s.Q + 2));
-    p.off_dz = take(sizeof(float) * p.gchunks * p.njr * s.M * s.Q);
+    p.off_dz = take(sizeof(float) * p.dzslabs * s.M * s.Q);
     p.off_dl = take(sizeof(float) * p.fin_blocks * (s.Q + 1));
     p.off_gmax = take(sizeof(float) * 2);
     p.off_gpart = take(sizeof(float) * cdiv(s.N, 64));
@@ -1528,8 +1567,8 @@ __device__ void stage_zh(_Float16 *zh, int blk0, int nblk, int M, int Q, int nqb
 // psi2_finalize_kernel.
 template <int NK, int NQB, int JPW = grad_jpw(NQB)>
 __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
-    int64_t N, int M, int Q, int Mp, int nb, int DSF, int njr, int wpg, int igroups,
-    int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
+    int64_t N, int M, int Q, int Mp, int nb, int DSF, int njr, int wpg, int igroups, int cross,
+    int slot0, int64_t rows_per_chunk, const float *__restrict__ mu, const float *__restrict__ Z,
     const float *__restrict__ zc, const float *__restrict__ Kt, const float *__restrict__ bt,
     const float *__restrict__ bc, const float *__restrict__ w1t, const float *__restrict__ w2t,
     const float *__restrict__ t1g, const float *__restrict__ G2p, const float *__restrict__ hl,
@@ -1548,12 +1587,18 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
     const int RED = 5 * Q + 2;                 // X, Y, P, X1, P1 per dimension, then R, T1
     const int QV = 32 * NQB;
     const int group = blockIdx.x;
-    const int jr = group / igroups;            // range of column blocks of W (m')
-    const int ib0 = (group % igroups) * wpg;  // first row block of the workgroup
+    // cross (tiles between the halves of the symmetric kernel's two workgroups):
+    // group g takes row blocks 0 .. 7 (g < 2) or 8 .. 15 against the column
+    // ranges of the other half (JPW = 4, wpg = 8); the Psi1 terms are the
+    // symmetric kernel's
+    const int jr = cross ? (group < 2 ? 2 + group : group - 2)
+                         : group / igroups;    // range of column blocks of W (m')
+    const int ib0 = cross ? (group / 2) * wpg
+                          : (group % igroups) * wpg;  // first row block of the workgroup
     const int i0 = ib0 + wave;
     const bool active = i0 < nb;               // wave-uniform
     const int i = active ? i0 : 0;             // row block of W (m)
-    const bool has1 = active && jr == 0;       // this task also adds the Psi1 terms of block i
+    const bool has1 = !cross && active && jr == 0;   // this task also adds the Psi1 terms of block i
 
     // dL/dPsi2 tiles of the task (zero for column blocks past the edge)
     int jb[JPW];
@@ -1819,13 +1864,14 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
             const float *rs = lds + L.red + r * wpg * RED + e;
             float v = 0.f;
             for (int w = 0; w < wpg; ++w) v += rs[w * RED];
-            rowsum[((int64_t)group * N + n0 + r) * RED + e] = v;
+            rowsum[((int64_t)(slot0 + group) * N + n0 + r) * RED + e] = v;
         }
     }
 
     // this task's share of dZ for the rows of block i: slab [chunk][jr][M][Q]
+    // (cross: [chunk][group % 2][M][Q], the two halves' rows in one slab)
     if (active) {
-        float *pdz = part_dz + ((int64_t)blockIdx.y * njr + jr) * M * Q;
+        float *pdz = part_dz + ((int64_t)blockIdx.y * (cross ? 2 : njr) + (cross ? group % 2 : jr)) * M * Q;
 #pragma unroll
         for (int qb = 0; qb < NQB; ++qb) {
             const int q = qb * 32 + c;
@@ -1857,7 +1903,8 @@ __global__ __launch_bounds__(grad_waves(NQB) * 64) void psi2_grad_kernel(
 // of 16, for 24 tile exchanges and two barriers per round.
 template <int NK, int RB>
 __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
-    int64_t N, int M, int Q, int Mp, int nb, int DSF, int64_t rows_per_chunk,
+    int64_t N, int M, int Q, int Mp, int nb, int blk0, int Mg, int nbg, int slot, int DSF,
+    int64_t rows_per_chunk,
     const float *__restrict__ mu, const float *__restrict__ Z, const float *__restrict__ zc,
     const float *__restrict__ Kt, const float *__restrict__ bt, const float *__restrict__ bc,
     const float *__restrict__ w1t, const float *__restrict__ w2t, const float *__restrict__ t1g,
@@ -1891,9 +1938,9 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
         const int k = s < KT - 1 ? s : nb / 2;
         const int j = (w + (ok ? k : 0)) % nb;
         const float okf = ok ? 1.f : 0.f;
-        const float *g2 = G2p + (int64_t)j * kTile * Mp + w * kTile + c;
+        const float *g2 = G2p + (int64_t)(blk0 + j) * kTile * Mg + (blk0 + w) * kTile + c;
 #pragma unroll
-        for (int t = 0; t < 16; ++t) g2r[s][t] = okf * g2[(int64_t)crow(t, g) * Mp];
+        for (int t = 0; t < 16; ++t) g2r[s][t] = okf * g2[(int64_t)crow(t, g) * Mg];
     }
     v16f dz;
 #pragma unroll
@@ -1903,11 +1950,11 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
     // constant tables: centred z (fp32), [Z | 1] (V-product B operands) and
     // [centred z | 1] (Gram A operands) of every block
     for (int k = threadIdx.x; k < nb * kTile * DSF + 32; k += blockDim.x) {
-        const int m = k / DSF, q = k - m * DSF;
-        lds[L.zx + k] = (m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
+        const int ml = k / DSF, q = k - ml * DSF, m = blk0 * kTile + ml;
+        lds[L.zx + k] = (ml < nb * kTile && m < M && q < Q) ? Z[(int64_t)m * Q + q] - zc[q] : 0.f;
     }
-    stage_zh(zh, 0, nb, M, Q, 1, Z, zc);
-    stage_za<NK>(za, 0, nb, nb, M, Q, Z, zc, threadIdx.x, blockDim.x);
+    stage_zh(zh, blk0, nb, M, Q, 1, Z, zc);
+    stage_za<NK>(za, blk0, nb, nbg, M, Q, Z, zc, threadIdx.x, blockDim.x);
     // per-row scale of W: as in psi2_grad_kernel
     const float lgc = gmax[0] > 0.f ? __builtin_amdgcn_logf(gmax[0]) : 0.f;
     const float lgs = gmax[1] > 0.f ? __builtin_amdgcn_logf(gmax[1]) : 0.f;
@@ -1936,7 +1983,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
             for (int i = 0; i < PT; ++i) {
                 const int k = tid + i * nthr;
                 const int rr = min(k / Mp, cb - 1);
-                const int64_t o = (n0 + rr) * Mp + (k - (k / Mp) * Mp);
+                const int64_t o = (n0 + rr) * Mg + blk0 * kTile + (k - (k / Mp) * Mp);
                 vb[i] = bt[o];
                 vc[i] = bc[o];
                 vt[i] = t1g[o];
@@ -1951,7 +1998,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
         } else {
             for (int k = tid; k < RB * Mp; k += nthr) {
                 const int rr = min(k / Mp, cb - 1);
-                const int64_t o = (n0 + rr) * Mp + (k - (k / Mp) * Mp);
+                const int64_t o = (n0 + rr) * Mg + blk0 * kTile + (k - (k / Mp) * Mp);
                 const float vb = bt[o], vc = bc[o], vt = t1g[o];
                 lds[L.bb + k] = vb;
                 lds[L.bcb + k] = vc;
@@ -1975,7 +2022,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
             if (tid < cb) {
                 const float phl = hl[n0 + tid];
                 float pbm = -INFINITY;
-                for (int y = 0; y < (Mp + 255) / 256; ++y) pbm = fmaxf(pbm, bmax[(int64_t)y * N + n0 + tid]);
+                for (int y = 0; y < (Mg + 255) / 256; ++y) pbm = fmaxf(pbm, bmax[(int64_t)y * N + n0 + tid]);
                 const float wb = fminf(2.f * phl + lgc, 4.f * pbm - 2.f * phl + lgs);
                 sc = fminf(120.f, fmaxf(-120.f, floorf(14.f - wb)));
             }
@@ -2135,7 +2182,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
             const float *rs = lds + L.red + r * nb * RED + e;
             float v = 0.f;
             for (int ww = 0; ww < nb; ++ww) v += rs[ww * RED];
-            rowsum[(n0 + r) * RED + e] = v;
+            rowsum[((int64_t)slot * N + n0 + r) * RED + e] = v;
         }
     }
 
@@ -2144,7 +2191,7 @@ __global__ __launch_bounds__(512) void psi2_grad_sym_kernel(
         float *pdz = part_dz + (int64_t)blockIdx.y * M * Q;
 #pragma unroll
         for (int t = 0; t < 16; ++t) {
-            const int m = w * kTile + crow(t, g);
+            const int m = (blk0 + w) * kTile + crow(t, g);
             if (m < M) pdz[(int64_t)m * Q + c] = dz[t];
         }
     }
@@ -2288,14 +2335,16 @@ hipError_t launch_grad(const MPlan &p, const Shape &s, const float *mu, const fl
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_grad);
     if (e != hipSuccess) return e;
-    dim3 grid((unsigned)p.ggroups, (unsigned)p.gchunks);
+    // split: the tiles between the halves only, row sums from group 2 on, dZ
+    // slabs after the halves'
+    dim3 grid((unsigned)(p.gsplit ? 4 : p.ggroups), (unsigned)p.gchunks);
     TimedScope ts(st, "mfma_psi2_grad");
     k<<<grid, p.wpg * 64, p.lds_grad, st>>>(
-        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.njr, p.wpg, p.igroups, p.grows, mu, Z,
-        fat(ws, p.off_zc), fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc),
-        fat(ws, p.off_w1), fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2),
-        fat(ws, p.off_hl), fat(ws, p.off_gmax), fat(ws, p.off_bmax), h, route, fat(ws, p.off_rs),
-        fat(ws, p.off_dz));
+        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSF, p.njr, p.wpg, p.igroups, p.gsplit ? 1 : 0,
+        p.gsplit ? 2 : 0, p.grows, mu, Z, fat(ws, p.off_zc), fat(ws, p.off_K), fat(ws, p.off_bt),
+        fat(ws, p.off_bc), fat(ws, p.off_w1), fat(ws, p.off_w2), fat(ws, p.off_t1),
+        fat(ws, p.off_g2), fat(ws, p.off_hl), fat(ws, p.off_gmax), fat(ws, p.off_bmax), h, route,
+        fat(ws, p.off_rs), fat(ws, p.off_dz) + (p.gsplit ? p.sgchunks * s.M * s.Q : 0));
     return hipGetLastError();
 }
 
@@ -2303,17 +2352,26 @@ template <int NK, int RB>
 hipError_t launch_grad_sym(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                            const Hyp<float> &h, const int *route, void *ws, hipStream_t st) {
     auto k = psi2_grad_sym_kernel<NK, RB>;
+    const size_t lds = p.gsplit ? p.lds_sym : p.lds_grad;
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)p.lds_grad);
+                                       (int)lds);
     if (e != hipSuccess) return e;
-    dim3 grid(1u, (unsigned)p.gchunks);
-    TimedScope ts(st, "mfma_psi2_grad");
-    k<<<grid, p.nb * 64, p.lds_grad, st>>>(
-        s.N, (int)s.M, (int)s.Q, (int)p.Mp, p.nb, p.DSFs, p.grows, mu, Z, fat(ws, p.off_zc),
-        fat(ws, p.off_K), fat(ws, p.off_bt), fat(ws, p.off_bc), fat(ws, p.off_w1),
-        fat(ws, p.off_w2), fat(ws, p.off_t1), fat(ws, p.off_g2), fat(ws, p.off_hl),
-        fat(ws, p.off_gmax), fat(ws, p.off_bmax), h, route, fat(ws, p.off_rs), fat(ws, p.off_dz));
-    return hipGetLastError();
+    // every block, or (split) blocks 0 .. 7 and 8 .. nb - 1 in launches of their own
+    const int halves = p.gsplit ? 2 : 1;
+    for (int hf = 0; hf < halves; ++hf) {
+        const int blk0 = hf * 8, nbl = p.gsplit ? (hf == 0 ? 8 : p.nb - 8) : p.nb;
+        const size_t ldsh = sizeof(float) * lds_sym_layout(nbl, p.DSFs, (int)s.Q, NK, RB).total;
+        dim3 grid(1u, (unsigned)(p.gsplit ? p.sgchunks : p.gchunks));
+        TimedScope ts(st, "mfma_psi2_grad");
+        k<<<grid, nbl * 64, ldsh, st>>>(
+            s.N, (int)s.M, (int)s.Q, nbl * kTile, nbl, blk0, (int)p.Mp, p.nb, hf, p.DSFs,
+            p.gsplit ? p.sgrows : p.grows, mu, Z, fat(ws, p.off_zc), fat(ws, p.off_K),
+            fat(ws, p.off_bt), fat(ws, p.off_bc), fat(ws, p.off_w1), fat(ws, p.off_w2),
+            fat(ws, p.off_t1), fat(ws, p.off_g2), fat(ws, p.off_hl), fat(ws, p.off_gmax),
+            fat(ws, p.off_bmax), h, route, fat(ws, p.off_rs), fat(ws, p.off_dz));
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 template <int NK>
@@ -2354,13 +2412,15 @@ hipError_t dispatch_fwd(const MPlan &p, const Shape &s, const float *mu, const f
 
 hipError_t dispatch_grad(const MPlan &p, const Shape &s, const float *mu, const float *Z,
                          const Hyp<float> &h, const int *route, void *ws, hipStream_t st) {
-    if (p.gsym) {
+    if (p.gsym || p.gsplit) {
+        hipError_t e = hipErrorInvalidValue;
 #define GPPS_GS(I)                                                                 \
-    if (p.nk == I && p.grb == kSymRBMax) return launch_grad_sym<I, kSymRBMax>(p, s, mu, Z, h, route, ws, st); \
-    if (p.nk == I && p.grb == kSymRBMax / 2) return launch_grad_sym<I, kSymRBMax / 2>(p, s, mu, Z, h, route, ws, st);
+    if (p.nk == I && p.grb == kSymRBMax) e = launch_grad_sym<I, kSymRBMax>(p, s, mu, Z, h, route, ws, st); \
+    if (p.nk == I && p.grb == kSymRBMax / 2) e = launch_grad_sym<I, kSymRBMax / 2>(p, s, mu, Z, h, route, ws, st);
         GPPS_GS(1) GPPS_GS(2) GPPS_GS(3) GPPS_GS(4) GPPS_GS(6) GPPS_GS(8)
 #undef GPPS_GS
-        return hipErrorInvalidValue;
+        if (p.gsym || e != hipSuccess) return e;
+        // split: then the tiles between the halves
     }
 #define GPPS_G(I, Q) \
     if (p.nk == I && p.nqb == Q) return launch_grad<I, Q>(p, s, mu, Z, h, route, ws, st);
@@ -2472,7 +2532,7 @@ hipError_t mfma_psi_grads(const Shape &s, const float *mu, const float *S, const
     const int64_t zblocks = cdiv(s.M * s.Q, kRedOut);
     TimedScope ts(st, "mfma_grad_reduce");
     grad_reduce_kernel<<<(unsigned)(zblocks + s.Q + 1), 256, 0, st>>>(
-        s.N, (int)s.M, (int)s.Q, zblocks, fat(ws, p.off_dz), p.gchunks * p.njr, fat(ws, p.off_dl),
+        s.N, (int)s.M, (int)s.Q, zblocks, fat(ws, p.off_dz), p.dzslabs, fat(ws, p.off_dl),
         p.fin_blocks, dL_dpsi0, route, dZ, dsf2, dl, accumulate);
     return hipGetLastError();
 }

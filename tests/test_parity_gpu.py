@@ -556,6 +556,20 @@ def test_mfma_symmetric_forward_ranges(N, M, Q):
     compare_all(got, run_oracle(inp), TOL32, f"fsym-{M}x{Q}")
 
 
+# The gradient for 13 <= nb <= 16 (where the halves' tables fit): the symmetric
+# kernel on blocks 0 .. 7 and on 8 .. nb - 1, the tile kernel on the tiles
+# between them; nb = 13 (a half of five blocks), 14, 15 (odd half) and 16, with
+# eight-row batches (Q <= 14) and four (Q = 20), ragged M and partial batches.
+@pytest.mark.parametrize("N,M,Q", [(150, 410, 20), (170, 448, 20), (201, 480, 14),
+                                   (140, 512, 10), (100, 500, 3)])
+def test_mfma_split_gradient(N, M, Q):
+    use_path("mfma", torch.float32)
+    say(f"[split gradient N={N} M={M} Q={Q}]")
+    inp = synth.to_f32(synth.random_inputs(N, M, Q, seed=500 + M + Q))
+    got = run_gpu(inp, torch.float32)
+    compare_all(got, run_oracle(inp), TOL32, f"split-{M}x{Q}")
+
+
 # Ragged ranges of row blocks on the matrix-core path: M = 257 (9 blocks of 32,
 # three ranges of four, the last with one real block) at Q = 20, and M = 300 at
 # Q = 31 (eight Gram instructions, the widest single [Z | 1] column block).
